@@ -1,0 +1,242 @@
+/*
+ * dpgrad.h -- C ABI of libdpgrad.so: the DP-SGD gradient step on one AMD
+ * Instinct MI355X (gfx950), in hand-written HIP kernels.
+ *
+ * The step (Opacus, arXiv 2109.12298, section 1 and figure 1): compute every
+ * sample's gradient, clip each sample's l2 norm (taken over all parameters)
+ * to C, add the clipped gradients over the batch, add Gaussian noise of
+ * standard deviation sigma*C, and divide by the batch size.  The per-sample
+ * gradients come from each layer's stored input activations A and the
+ * backprops B at its output ("highway gradients"; appendix "Vectorized
+ * Computation"), and the fields the paper's appendix "Tracking Gradients"
+ * names map onto these outputs: grad_sample -> the per-sample gradients,
+ * summed_grad -> the clipped sum, grad -> the noised average.
+ *
+ * Conventions shared by every entry point
+ *  - Return a dp_status.  Arguments are validated on the host before anything
+ *    is enqueued; an invalid call enqueues nothing and returns DP_EINVAL,
+ *    DP_EDTYPE or DP_EUNSUPPORTED.  DP_EHIP means a kernel launch failed.
+ *    Nothing throws across the ABI.
+ *  - No entry point allocates, frees or synchronizes.  Every pointer is a
+ *    caller-owned device pointer (unless stated) to a dense row-major array;
+ *    all work is enqueued on the caller's `stream` (NULL = default stream),
+ *    so results are ready when the caller's own synchronization says so.
+ *  - Scratch memory: entry points taking `ws` need a caller-owned device
+ *    workspace of at least the size reported by the matching
+ *    *_workspace_bytes() query (which is host-only and may be called at any
+ *    time); `ws` may be NULL only when that size is 0.  The workspace holds
+ *    nothing between calls.
+ *  - Input dtype: DP_F32 or DP_BF16 for activations/backprops.  Per-sample
+ *    gradients, norms, sums and outputs are always fp32, accumulated in fp32.
+ *  - `scale` (s) multiplies every backprop: s = 1 takes B as backprops of the
+ *    summed per-sample losses, so each result is the gradient of that
+ *    sample's own loss; callers holding backprops of a batch-mean loss pass
+ *    s = N.
+ *  - Device-side conditions are OR-ed into `*status` (a caller-owned device
+ *    int32, zeroed by the caller; may be NULL to ignore them):
+ *    DP_FLAG_BAD_INDEX (a token id outside [0, V)), DP_FLAG_NONFINITE (a
+ *    per-sample norm that is NaN or infinite), DP_FLAG_CAP (CSR capacity
+ *    exceeded).  The caller reads the word after its own synchronization.
+ *  - Results are deterministic: no floating-point atomics, every reduction
+ *    has a fixed order, so the same inputs give the same bits run to run.
+ *  - Entry points are stateless and re-entrant; calls on different streams
+ *    with disjoint outputs and workspaces may overlap.
+ */
+#ifndef DPGRAD_H
+#define DPGRAD_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum dp_status {
+    DP_OK = 0,
+    DP_EINVAL = 1,       /* a null required pointer, a bad size, a too-small workspace */
+    DP_EDTYPE = 2,       /* an unknown dp_dtype */
+    DP_EUNSUPPORTED = 3, /* a valid request this library does not implement (e.g. groups != 1) */
+    DP_ECAP = 4,         /* a host-checkable capacity is too small */
+    DP_EHIP = 5          /* a HIP launch failed */
+} dp_status;
+
+typedef enum dp_dtype { DP_F32 = 0, DP_BF16 = 1 } dp_dtype;
+
+enum {
+    DP_FLAG_BAD_INDEX = 1,
+    DP_FLAG_NONFINITE = 2,
+    DP_FLAG_CAP = 4
+};
+
+/* Human-readable text for a status code (static storage; never NULL). */
+const char *dp_status_string(dp_status s);
+
+/* ABI version of this header; bumped on any incompatible change. */
+int dp_abi_version(void);
+
+/* ---------------------------------------------------------------------------
+ * Per-sample gradients (row a of the step: grad_sample)
+ * ------------------------------------------------------------------------- */
+
+/* Linear layer y_t = W x_t + b applied at T positions per sample.  Per the
+ * per-sample equation of the appendix "Vectorized Computation" (the einsum
+ * "n...i,n...j->nij" of B and A, extra dimensions summed):
+ *   gW[n][i][j] = s * sum_t B[n][t][i] * A[n][t][j]
+ *   gb[n][i]    = s * sum_t B[n][t][i]
+ *   sqnorm[n]   = sum_ij gW[n][i][j]^2 + sum_i gb[n][i]^2   (overwritten)
+ * A: [N][T][d_in] of `dt`;  B: [N][T][d_out] of `dt`  (T = 1: [N][d_in], [N][d_out]).
+ * gW: fp32 [N][d_out][d_in] (required); gb: fp32 [N][d_out] or NULL (no bias);
+ * sqnorm: fp32 [N] or NULL.  N >= 0, T >= 0 (T = 0 gives zeros), d_in, d_out >= 1.
+ * T = 1 runs a bandwidth-bound outer product; T > 1 a per-sample MFMA GEMM
+ * with K = T. */
+size_t dp_grad_sample_linear_workspace_bytes(int64_t N, int64_t T, int64_t d_in,
+                                             int64_t d_out, dp_dtype dt);
+dp_status dp_grad_sample_linear(const void *A, const void *B, dp_dtype dt, int64_t N,
+                                int64_t T, int64_t d_in, int64_t d_out, float scale,
+                                float *gW, float *gb, float *sqnorm, int32_t *status,
+                                void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Conv2d (cross-correlation, zero padding) with groups = 1 and dilation = 1.
+ * The paper defers this layer's formula to its tutorials; it is the weight
+ * gradient of the convolution restricted to one sample:
+ *   gW[n][co][ci][u][v] = s * sum_{oh,ow} GY[n][co][oh][ow] * X[n][ci][oh*sh+u-ph][ow*sw+v-pw]
+ *   gb[n][co]           = s * sum_{oh,ow} GY[n][co][oh][ow]
+ * (input positions inside the padding contribute zero), i.e. the product of
+ * GY_n [Cout][Ho*Wo] with the transposed unfold (im2col) of X_n, whose rows are
+ * ordered (ci, u, v) like the weight.  The unfold is never materialized.
+ * X: [N][Cin][H][W] of `dt`; GY: [N][Cout][Ho][Wo] of `dt`, where Ho and Wo
+ * must equal (H + 2ph - kh)/sh + 1 and (W + 2pw - kw)/sw + 1 (else DP_EINVAL).
+ * gW fp32 [N][Cout][Cin][kh][kw]; gb fp32 [N][Cout] or NULL; sqnorm fp32 [N]
+ * or NULL (overwritten with the layer's squared norm).
+ * dh, dw != 1 or groups != 1 return DP_EUNSUPPORTED. */
+size_t dp_grad_sample_conv2d_workspace_bytes(int64_t N, int64_t Cin, int64_t Cout,
+                                             int64_t kh, int64_t kw);
+dp_status dp_grad_sample_conv2d(const void *X, const void *GY, dp_dtype dt, int64_t N,
+                                int64_t Cin, int64_t H, int64_t W, int64_t Cout,
+                                int64_t Ho, int64_t Wo, int64_t kh, int64_t kw, int64_t sh,
+                                int64_t sw, int64_t ph, int64_t pw, int64_t dh, int64_t dw,
+                                int64_t groups, float scale, float *gW, float *gb,
+                                float *sqnorm, int32_t *status, void *ws, size_t ws_bytes,
+                                hipStream_t stream);
+
+/* Embedding y_t = E[ids[n][t]] over a [V][D] table.  Sample n's gradient is
+ * zero except on the rows of the ids it holds; row v is s * sum of B[n][t][:]
+ * over the positions t with ids[n][t] = v.  Returned sparse, as CSR over the
+ * batch (a dense [N][V][D] gradient is never formed):
+ *   row_ptr[n] .. row_ptr[n+1]   the stored rows of sample n
+ *   uniq_ids[k]                  the id of stored row k; ascending within a sample
+ *   rows[k][:]                   its gradient row (positions added in ascending t)
+ *   sqnorm[n]                    sum of the squares of sample n's rows (overwritten)
+ * ids: int64 [N][T]; B: [N][T][D] of `dt`; row_ptr int64 [N+1]; uniq_ids int64
+ * [cap]; rows fp32 [cap][D]; sqnorm fp32 [N] or NULL.  cap >= N*T always
+ * suffices; a smaller cap that the data overflows sets DP_FLAG_CAP, row_ptr
+ * still holds the true counts and rows past cap are not written.  An id
+ * outside [0, V) sets DP_FLAG_BAD_INDEX and its position is left out.
+ * Needs T <= 4096 (else DP_EUNSUPPORTED) and V < 2^31. */
+size_t dp_grad_sample_embedding_workspace_bytes(int64_t N, int64_t T);
+dp_status dp_grad_sample_embedding(const int64_t *ids, const void *B, dp_dtype dt, int64_t N,
+                                   int64_t T, int64_t V, int64_t D, float scale,
+                                   int64_t *row_ptr, int64_t *uniq_ids, float *rows,
+                                   int64_t cap, float *sqnorm, int32_t *status, void *ws,
+                                   size_t ws_bytes, hipStream_t stream);
+
+/* LayerNorm's elementwise affine y = gamma * xhat + beta over D features at T
+ * positions (the paper lists normalization layers among those supported):
+ *   ggamma[n][k] = s * sum_t B[n][t][k] * xhat[n][t][k]
+ *   gbeta[n][k]  = s * sum_t B[n][t][k]
+ * xhat, B: [N][T][D] of `dt`; ggamma, gbeta fp32 [N][D]; sqnorm fp32 [N] or NULL. */
+size_t dp_grad_sample_layernorm_workspace_bytes(int64_t N, int64_t T, int64_t D);
+dp_status dp_grad_sample_layernorm(const void *xhat, const void *B, dp_dtype dt, int64_t N,
+                                   int64_t T, int64_t D, float scale, float *ggamma,
+                                   float *gbeta, float *sqnorm, int32_t *status, void *ws,
+                                   size_t ws_bytes, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * Norms and clipping
+ * ------------------------------------------------------------------------- */
+
+/* norm[n] = sqrt(sum_l sqnorm[l][n]), layers added in ascending l: the l2
+ * norm of sample n's gradient over all parameters (section 1: clip each
+ * per-sample gradient's l2 norm).  sqnorm fp32 [n_layers][N]; norm fp32 [N].
+ * A NaN or infinite norm sets DP_FLAG_NONFINITE. */
+dp_status dp_per_sample_norms(const float *sqnorm, int32_t n_layers, int64_t N, float *norm,
+                              int32_t *status, hipStream_t stream);
+
+/* sqnorm[n] = sum_e G[n][e]^2 for an already materialized per-sample gradient
+ * G fp32 [N][numel] (overwritten). */
+dp_status dp_sqnorm_from_grads(const float *G, int64_t N, int64_t numel, float *sqnorm,
+                               int32_t *status, hipStream_t stream);
+
+/* Clip factors c[n] = min(1, C / (norm[n] + 1e-6)), computed in fp32.
+ * C = +inf gives 1; a NaN or infinite norm gives NaN (and DP_FLAG_NONFINITE)
+ * so a broken sample poisons the sum rather than passing unclipped.
+ * C must be > 0 (else DP_EINVAL). */
+dp_status dp_clip_factors(const float *norm, int64_t N, float C, float *c, int32_t *status,
+                          hipStream_t stream);
+
+/* Clipped sum of a materialized per-sample gradient (summed_grad):
+ *   sum[e] = sum_n c_n * G[n][e], n ascending, c_n as in dp_clip_factors.
+ * G fp32 [N][numel]; norm fp32 [N]; sum fp32 [numel] (N = 0 writes zeros);
+ * c_out fp32 [N] or NULL receives the factors. */
+size_t dp_clip_accumulate_workspace_bytes(int64_t N, int64_t numel);
+dp_status dp_clip_accumulate(const float *G, const float *norm, float C, int64_t N,
+                             int64_t numel, float *sum, float *c_out, int32_t *status,
+                             void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Clipped sum of a Linear layer computed from A and B without reading the
+ * per-sample gradients: with c_n as above,
+ *   sumW = s * sum_n c_n * B_n^T A_n  (one GEMM with K = N*T: B^T diag(c) A)
+ *   sumb = s * sum_n c_n * sum_t B[n][t][:]
+ * Same A/B layout as dp_grad_sample_linear; sumW fp32 [d_out][d_in]; sumb fp32
+ * [d_out] or NULL.  The K range is split over workgroups and the partial sums
+ * are added in a fixed order in a second pass. */
+size_t dp_clip_accumulate_linear_workspace_bytes(int64_t N, int64_t T, int64_t d_in,
+                                                 int64_t d_out, dp_dtype dt);
+dp_status dp_clip_accumulate_linear(const void *A, const void *B, dp_dtype dt, int64_t N,
+                                    int64_t T, int64_t d_in, int64_t d_out, float scale,
+                                    const float *norm, float C, float *sumW, float *sumb,
+                                    int32_t *status, void *ws, size_t ws_bytes,
+                                    hipStream_t stream);
+
+/* Dense clipped sum of CSR embedding gradients (as dp_grad_sample_embedding
+ * writes them): sum[v][:] = sum_n c_n * (sample n's row for id v, if any),
+ * n ascending; rows no sample touched are written as zeros.
+ * row_ptr int64 [N+1]; uniq_ids int64 [row_ptr[N]]; rows fp32 [row_ptr[N]][D];
+ * sum fp32 [V][D].  Stored ids outside [0, V) set DP_FLAG_BAD_INDEX and are
+ * ignored. */
+dp_status dp_clip_accumulate_embedding(const int64_t *row_ptr, const int64_t *uniq_ids,
+                                       const float *rows, const float *norm, float C,
+                                       int64_t N, int64_t V, int64_t D, float *sum,
+                                       int32_t *status, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * Noise and averaging (grad)
+ * ------------------------------------------------------------------------- */
+
+/* out[e] = (sum[e] + sigma * C * z[e]) / denom for one parameter tensor.
+ * z[e] is element e of the tensor's normal stream: Philox4x32-10 (Salmon et
+ * al., SC'11) with key (seed_lo, seed_hi) and counter (e/4, param_index,
+ * step_lo, step_hi); each 4-word block gives four normals by Box-Muller on
+ * word pairs (w0,w1) and (w2,w3) with u1 = (w>>8)+1)/2^24, u2 = (w>>8)/2^24,
+ * z = sqrt(-2 ln u1) * (cos, sin)(2 pi u2).  Element e takes normal e mod 4.
+ * The noise is a pure function of (seed, step, param_index, e), so a resumed
+ * run reproduces it and every data-parallel rank would draw the same values.
+ * sigma = 0 adds nothing (also for C = +inf); sigma > 0 with C = +inf, or
+ * denom <= 0, or sigma < 0 is DP_EINVAL.  out may equal sum (in place).
+ * sum, out: fp32 [numel]. */
+dp_status dp_add_noise(const float *sum, float *out, int64_t numel, uint64_t seed, uint64_t step,
+                       uint32_t param_index, float sigma, float C, float denom,
+                       int32_t *status, hipStream_t stream);
+
+/* The raw stream behind dp_add_noise: z fp32 [numel] (or NULL) receives the
+ * normals, raw uint32 [numel] (or NULL) the Philox words. */
+dp_status dp_philox_normals(float *z, uint32_t *raw, int64_t numel, uint64_t seed,
+                            uint64_t step, uint32_t param_index, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DPGRAD_H */

@@ -1,0 +1,242 @@
+"""Thin ctypes binding of libdpgrad.so (declared in include/dpgrad.h).
+
+Each function has the name and argument order of its C entry point and only
+marshals arguments: device pointers may be given as torch tensors (their
+``data_ptr()``), raw integer addresses or None; ``ws_bytes`` is taken from the
+workspace tensor; ``stream`` defaults to torch's current HIP stream.  A status
+other than DP_OK raises :class:`DPError`.  There is no fallback: if the
+library is not built, loading fails loudly.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libdpgrad.so")
+
+DP_OK, DP_EINVAL, DP_EDTYPE, DP_EUNSUPPORTED, DP_ECAP, DP_EHIP = range(6)
+DP_F32, DP_BF16 = 0, 1
+DP_FLAG_BAD_INDEX, DP_FLAG_NONFINITE, DP_FLAG_CAP = 1, 2, 4
+
+# (name, restype, argtypes) of every exported entry point
+_P = ctypes.c_void_p
+_I64 = ctypes.c_int64
+_F = ctypes.c_float
+_SZ = ctypes.c_size_t
+_I32 = ctypes.c_int32
+_U32 = ctypes.c_uint32
+_U64 = ctypes.c_uint64
+_ST = ctypes.c_int
+
+SIGNATURES = {
+    "dp_status_string": (ctypes.c_char_p, [_ST]),
+    "dp_abi_version": (ctypes.c_int, []),
+    "dp_grad_sample_linear_workspace_bytes": (_SZ, [_I64, _I64, _I64, _I64, _ST]),
+    "dp_grad_sample_linear": (_ST, [_P, _P, _ST, _I64, _I64, _I64, _I64, _F, _P, _P, _P, _P, _P, _SZ, _P]),
+    "dp_grad_sample_conv2d_workspace_bytes": (_SZ, [_I64, _I64, _I64, _I64, _I64]),
+    "dp_grad_sample_conv2d": (_ST, [_P, _P, _ST] + [_I64] * 16 + [_F, _P, _P, _P, _P, _P, _SZ, _P]),
+    "dp_grad_sample_embedding_workspace_bytes": (_SZ, [_I64, _I64]),
+    "dp_grad_sample_embedding": (_ST, [_P, _P, _ST, _I64, _I64, _I64, _I64, _F, _P, _P, _P, _I64, _P,
+                                       _P, _P, _SZ, _P]),
+    "dp_grad_sample_layernorm_workspace_bytes": (_SZ, [_I64, _I64, _I64]),
+    "dp_grad_sample_layernorm": (_ST, [_P, _P, _ST, _I64, _I64, _I64, _F, _P, _P, _P, _P, _P, _SZ, _P]),
+    "dp_per_sample_norms": (_ST, [_P, _I32, _I64, _P, _P, _P]),
+    "dp_sqnorm_from_grads": (_ST, [_P, _I64, _I64, _P, _P, _P]),
+    "dp_clip_factors": (_ST, [_P, _I64, _F, _P, _P, _P]),
+    "dp_clip_accumulate_workspace_bytes": (_SZ, [_I64, _I64]),
+    "dp_clip_accumulate": (_ST, [_P, _P, _F, _I64, _I64, _P, _P, _P, _P, _SZ, _P]),
+    "dp_clip_accumulate_linear_workspace_bytes": (_SZ, [_I64, _I64, _I64, _I64, _ST]),
+    "dp_clip_accumulate_linear": (_ST, [_P, _P, _ST, _I64, _I64, _I64, _I64, _F, _P, _F, _P, _P, _P, _P,
+                                        _SZ, _P]),
+    "dp_clip_accumulate_embedding": (_ST, [_P, _P, _P, _P, _F, _I64, _I64, _I64, _P, _P, _P]),
+    "dp_add_noise": (_ST, [_P, _P, _I64, _U64, _U64, _U32, _F, _F, _F, _P, _P]),
+    "dp_philox_normals": (_ST, [_P, _P, _I64, _U64, _U64, _U32, _P]),
+}
+
+
+class DPError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        super().__init__("%s: %s" % (where, status_string(code)))
+
+
+_lib = None
+
+
+def lib():
+    """Load libdpgrad.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libdpgrad.so is not built (%s); run `python -m paper_2109_12298_amd.build`"
+                               % LIB_PATH)
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def status_string(code: int) -> str:
+    return lib().dp_status_string(code).decode()
+
+
+def dp_status_string(code: int) -> str:
+    return status_string(code)
+
+
+def dp_abi_version() -> int:
+    return lib().dp_abi_version()
+
+
+def _ptr(x):
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def _nbytes(x) -> int:
+    if x is None:
+        return 0
+    return x.numel() * x.element_size()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def dtype_of(t) -> int:
+    import torch
+    if t.dtype == torch.float32:
+        return DP_F32
+    if t.dtype == torch.bfloat16:
+        return DP_BF16
+    raise TypeError("unsupported dtype %s" % t.dtype)
+
+
+def _check(code: int, where: str):
+    if code != DP_OK:
+        raise DPError(code, where)
+
+
+# ---------------------------------------------------------------------------
+# per-sample gradients
+# ---------------------------------------------------------------------------
+
+def dp_grad_sample_linear_workspace_bytes(N, T, d_in, d_out, dt) -> int:
+    return lib().dp_grad_sample_linear_workspace_bytes(N, T, d_in, d_out, dt)
+
+
+def dp_grad_sample_linear(A, B, dt, N, T, d_in, d_out, scale, gW, gb=None, sqnorm=None, status=None,
+                          ws=None, stream=None):
+    _check(lib().dp_grad_sample_linear(_ptr(A), _ptr(B), dt, N, T, d_in, d_out, scale, _ptr(gW), _ptr(gb),
+                                       _ptr(sqnorm), _ptr(status), _ptr(ws), _nbytes(ws), _stream(stream)),
+           "dp_grad_sample_linear")
+
+
+def dp_grad_sample_conv2d_workspace_bytes(N, Cin, Cout, kh, kw) -> int:
+    return lib().dp_grad_sample_conv2d_workspace_bytes(N, Cin, Cout, kh, kw)
+
+
+def dp_grad_sample_conv2d(X, GY, dt, N, Cin, H, W, Cout, Ho, Wo, kh, kw, sh, sw, ph, pw, dh, dw, groups,
+                          scale, gW, gb=None, sqnorm=None, status=None, ws=None, stream=None):
+    _check(lib().dp_grad_sample_conv2d(_ptr(X), _ptr(GY), dt, N, Cin, H, W, Cout, Ho, Wo, kh, kw, sh, sw, ph,
+                                       pw, dh, dw, groups, scale, _ptr(gW), _ptr(gb), _ptr(sqnorm),
+                                       _ptr(status), _ptr(ws), _nbytes(ws), _stream(stream)),
+           "dp_grad_sample_conv2d")
+
+
+def dp_grad_sample_embedding_workspace_bytes(N, T) -> int:
+    return lib().dp_grad_sample_embedding_workspace_bytes(N, T)
+
+
+def dp_grad_sample_embedding(ids, B, dt, N, T, V, D, scale, row_ptr, uniq_ids, rows, cap, sqnorm=None,
+                             status=None, ws=None, stream=None):
+    _check(lib().dp_grad_sample_embedding(_ptr(ids), _ptr(B), dt, N, T, V, D, scale, _ptr(row_ptr),
+                                          _ptr(uniq_ids), _ptr(rows), cap, _ptr(sqnorm), _ptr(status),
+                                          _ptr(ws), _nbytes(ws), _stream(stream)),
+           "dp_grad_sample_embedding")
+
+
+def dp_grad_sample_layernorm_workspace_bytes(N, T, D) -> int:
+    return lib().dp_grad_sample_layernorm_workspace_bytes(N, T, D)
+
+
+def dp_grad_sample_layernorm(xhat, B, dt, N, T, D, scale, ggamma, gbeta, sqnorm=None, status=None, ws=None,
+                             stream=None):
+    _check(lib().dp_grad_sample_layernorm(_ptr(xhat), _ptr(B), dt, N, T, D, scale, _ptr(ggamma), _ptr(gbeta),
+                                          _ptr(sqnorm), _ptr(status), _ptr(ws), _nbytes(ws),
+                                          _stream(stream)),
+           "dp_grad_sample_layernorm")
+
+
+# ---------------------------------------------------------------------------
+# norms and clipping
+# ---------------------------------------------------------------------------
+
+def dp_per_sample_norms(sqnorm, n_layers, N, norm, status=None, stream=None):
+    _check(lib().dp_per_sample_norms(_ptr(sqnorm), n_layers, N, _ptr(norm), _ptr(status), _stream(stream)),
+           "dp_per_sample_norms")
+
+
+def dp_sqnorm_from_grads(G, N, numel, sqnorm, status=None, stream=None):
+    _check(lib().dp_sqnorm_from_grads(_ptr(G), N, numel, _ptr(sqnorm), _ptr(status), _stream(stream)),
+           "dp_sqnorm_from_grads")
+
+
+def dp_clip_factors(norm, N, C, c, status=None, stream=None):
+    _check(lib().dp_clip_factors(_ptr(norm), N, C, _ptr(c), _ptr(status), _stream(stream)), "dp_clip_factors")
+
+
+def dp_clip_accumulate_workspace_bytes(N, numel) -> int:
+    return lib().dp_clip_accumulate_workspace_bytes(N, numel)
+
+
+def dp_clip_accumulate(G, norm, C, N, numel, sum, c_out=None, status=None, ws=None, stream=None):
+    _check(lib().dp_clip_accumulate(_ptr(G), _ptr(norm), C, N, numel, _ptr(sum), _ptr(c_out), _ptr(status),
+                                    _ptr(ws), _nbytes(ws), _stream(stream)),
+           "dp_clip_accumulate")
+
+
+def dp_clip_accumulate_linear_workspace_bytes(N, T, d_in, d_out, dt) -> int:
+    return lib().dp_clip_accumulate_linear_workspace_bytes(N, T, d_in, d_out, dt)
+
+
+def dp_clip_accumulate_linear(A, B, dt, N, T, d_in, d_out, scale, norm, C, sumW, sumb=None, status=None,
+                              ws=None, stream=None):
+    _check(lib().dp_clip_accumulate_linear(_ptr(A), _ptr(B), dt, N, T, d_in, d_out, scale, _ptr(norm), C,
+                                           _ptr(sumW), _ptr(sumb), _ptr(status), _ptr(ws), _nbytes(ws),
+                                           _stream(stream)),
+           "dp_clip_accumulate_linear")
+
+
+def dp_clip_accumulate_embedding(row_ptr, uniq_ids, rows, norm, C, N, V, D, sum, status=None, stream=None):
+    _check(lib().dp_clip_accumulate_embedding(_ptr(row_ptr), _ptr(uniq_ids), _ptr(rows), _ptr(norm), C, N, V,
+                                              D, _ptr(sum), _ptr(status), _stream(stream)),
+           "dp_clip_accumulate_embedding")
+
+
+# ---------------------------------------------------------------------------
+# noise
+# ---------------------------------------------------------------------------
+
+def dp_add_noise(sum, out, numel, seed, step, param_index, sigma, C, denom, status=None, stream=None):
+    _check(lib().dp_add_noise(_ptr(sum), _ptr(out), numel, seed, step, param_index, sigma, C, denom,
+                              _ptr(status), _stream(stream)),
+           "dp_add_noise")
+
+
+def dp_philox_normals(z, raw, numel, seed, step, param_index, stream=None):
+    _check(lib().dp_philox_normals(_ptr(z), _ptr(raw), numel, seed, step, param_index, _stream(stream)),
+           "dp_philox_normals")

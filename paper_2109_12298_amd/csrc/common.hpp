@@ -1,0 +1,125 @@
+// Shared device/host helpers of libdpgrad (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "dpgrad.h"
+
+namespace dpg {
+
+typedef int64_t i64;
+
+constexpr int kWave = 64;
+
+// ---------------------------------------------------------------------------
+// host-side argument checks (no HIP call happens before these pass)
+// ---------------------------------------------------------------------------
+#define DPG_REQUIRE(cond, code)                                                    \
+    do {                                                                           \
+        if (!(cond)) return (code);                                                \
+    } while (0)
+
+inline bool dtype_ok(dp_dtype dt) { return dt == DP_F32 || dt == DP_BF16; }
+inline size_t dtype_bytes(dp_dtype dt) { return dt == DP_BF16 ? 2 : 4; }
+
+inline dp_status launch_status()
+{
+    hipError_t e = hipGetLastError();
+    return e == hipSuccess ? DP_OK : DP_EHIP;
+}
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+inline bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+inline i64 ceil_div(i64 a, i64 b) { return (a + b - 1) / b; }
+
+// ---------------------------------------------------------------------------
+// element loads (bf16 is carried as its raw 16 bits)
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float bf16_to_f32(uint16_t b)
+{
+    return __uint_as_float(static_cast<uint32_t>(b) << 16);
+}
+
+template <typename T>
+__device__ __forceinline__ float load_elem(const T *p, i64 i);
+
+template <>
+__device__ __forceinline__ float load_elem<float>(const float *p, i64 i)
+{
+    return p[i];
+}
+
+template <>
+__device__ __forceinline__ float load_elem<uint16_t>(const uint16_t *p, i64 i)
+{
+    return bf16_to_f32(p[i]);
+}
+
+// ---------------------------------------------------------------------------
+// device-side status flags (rare: only on bad input)
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void raise_flag(int32_t *status, int32_t flag)
+{
+    if (status) atomicOr(status, flag);
+}
+
+// Clip factor min(1, C / (norm + 1e-6)) in fp32; C = +inf gives 1 and a
+// non-finite norm gives NaN (never silently 1).
+__device__ __forceinline__ float clip_factor(float norm, float C)
+{
+    if (!isfinite(norm)) return __builtin_nanf("");
+    if (isinf(C)) return 1.0f;
+    float q = C / (norm + 1e-6f);
+    return q < 1.0f ? q : 1.0f;
+}
+
+// ---------------------------------------------------------------------------
+// fixed-order reductions
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float wave_sum(float v)
+{
+    // butterfly over the 64 lanes; every lane ends with the same value and the
+    // order of additions depends only on lane positions (deterministic)
+    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, kWave);
+    return v;
+}
+
+// Sum over a block of `nthreads` (multiple of 64, <= 1024). Result valid in all
+// threads. `red` is __shared__ float[16].
+__device__ __forceinline__ float block_sum(float v, float *red)
+{
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wid = threadIdx.x / kWave;
+    const int nw = (blockDim.x + kWave - 1) / kWave;
+    v = wave_sum(v);
+    __syncthreads();
+    if (lane == 0) red[wid] = v;
+    __syncthreads();
+    float s = 0.0f;
+    for (int w = 0; w < nw; ++w) s += red[w];
+    return s;
+}
+
+// ---------------------------------------------------------------------------
+// zero fill by a kernel (kept out of hipMemsetAsync so that callers may
+// capture the launches in a HIP graph)
+// ---------------------------------------------------------------------------
+template <int Unused = 0>
+__global__ void fill_zero_kernel(float *__restrict__ p, i64 n)
+{
+    for (i64 i = (i64)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (i64)gridDim.x * blockDim.x)
+        p[i] = 0.0f;
+}
+
+inline void zero_fill(float *p, i64 n, hipStream_t stream)
+{
+    if (p == nullptr || n <= 0) return;
+    i64 blocks = (n + 255) / 256;
+    if (blocks > 4096) blocks = 4096;
+    fill_zero_kernel<0><<<(unsigned)blocks, 256, 0, stream>>>(p, n);
+}
+
+}  // namespace dpg

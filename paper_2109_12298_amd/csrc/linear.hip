@@ -1,0 +1,395 @@
+// Linear layer: per-sample gradients and the fused clipped sum.
+//
+// Per-sample gradient of y_t = W x_t + b for sample n (appendix "Vectorized
+// Computation"; extra dimensions summed):
+//   gW_n = s * B_n^T A_n   (d_out x d_in, K = T positions),  gb_n = s * sum_t B_n,t
+// T = 1 is a rank-one outer product: pure HBM write traffic (about one flop
+// per 4 bytes written), so it gets a store-streaming kernel whose norm is the
+// closed form s^2 |B_n|^2 (|A_n|^2 + 1).  T > 1 is a real per-sample GEMM on
+// MFMA with the squared-norm partials taken from the accumulators in the
+// epilogue.
+//
+// Fused clipped sum: sum_n c_n gW_n = s * B^T diag(c) A, one GEMM whose K runs
+// over all N*T rows, split over workgroups; partial tiles go to the workspace
+// and a second kernel adds them in split order (no atomics).
+#include "common.hpp"
+#include "mfma_tile.hpp"
+
+namespace dpg {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kBM = 64, kBN = 64, kBK = 32;
+
+template <typename T>
+__device__ __forceinline__ float4 load4(const T *p, i64 i);
+
+template <>
+__device__ __forceinline__ float4 load4<float>(const float *p, i64 i)
+{
+    return *reinterpret_cast<const float4 *>(p + i);
+}
+
+template <>
+__device__ __forceinline__ float4 load4<uint16_t>(const uint16_t *p, i64 i)
+{
+    const uint2 u = *reinterpret_cast<const uint2 *>(p + i);
+    return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
+                       __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u));
+}
+
+// ---------------------------------------------------------------------------
+// T = 1: gW[n][i][:] = s * B[n][i] * A[n][:]
+// ---------------------------------------------------------------------------
+template <typename T, bool VEC>
+__global__ __launch_bounds__(kThreads) void outer_kernel(const T *__restrict__ A,
+                                                         const T *__restrict__ B, i64 din,
+                                                         i64 dout, int rows, int bps, float scale,
+                                                         float *__restrict__ gW,
+                                                         float *__restrict__ gb,
+                                                         float *__restrict__ sqnorm)
+{
+    __shared__ float red[16];
+    const i64 n = blockIdx.x / bps;
+    const int rb = blockIdx.x % bps;
+    const i64 i0 = (i64)rb * rows;
+    const i64 i1 = i0 + rows < dout ? i0 + rows : dout;
+    const T *An = A + n * din;
+    const T *Bn = B + n * dout;
+    float *G = gW + n * dout * din;
+
+    if (VEC) {
+        const i64 nv = din / 4;
+        for (i64 j4 = threadIdx.x; j4 < nv; j4 += kThreads) {
+            const float4 a = load4<T>(An, 4 * j4);
+            for (i64 i = i0; i < i1; ++i) {
+                const float b = scale * load_elem<T>(Bn, i);
+                float4 v = make_float4(b * a.x, b * a.y, b * a.z, b * a.w);
+                *reinterpret_cast<float4 *>(G + i * din + 4 * j4) = v;
+            }
+        }
+    } else {
+        for (i64 j = threadIdx.x; j < din; j += kThreads) {
+            const float a = load_elem<T>(An, j);
+            for (i64 i = i0; i < i1; ++i) G[i * din + j] = scale * load_elem<T>(Bn, i) * a;
+        }
+    }
+    if (gb) {
+        for (i64 i = i0 + threadIdx.x; i < i1; i += kThreads) gb[n * dout + i] = scale * load_elem<T>(Bn, i);
+    }
+    if (sqnorm && rb == 0) {
+        float na = 0.0f, nb = 0.0f;
+        for (i64 j = threadIdx.x; j < din; j += kThreads) {
+            const float a = load_elem<T>(An, j);
+            na += a * a;
+        }
+        for (i64 i = threadIdx.x; i < dout; i += kThreads) {
+            const float b = load_elem<T>(Bn, i);
+            nb += b * b;
+        }
+        na = block_sum(na, red);
+        nb = block_sum(nb, red);
+        if (threadIdx.x == 0) sqnorm[n] = scale * scale * nb * (na + (gb ? 1.0f : 0.0f));
+    }
+}
+
+// ---------------------------------------------------------------------------
+// T > 1: per-sample GEMM on MFMA.  Block = (sample n, tile of gW_n).
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(kThreads) void per_sample_gemm_kernel(
+    const T *__restrict__ A, const T *__restrict__ B, i64 Tn, i64 din, i64 dout, int tiles_n,
+    int tiles, float scale, float *__restrict__ gW, float *__restrict__ gb,
+    float *__restrict__ partial)
+{
+    __shared__ float As[kBK * kBM];
+    __shared__ float Bs[kBK * kBN];
+    __shared__ float red[16];
+    const i64 n = blockIdx.x / tiles;
+    const int tile = blockIdx.x % tiles;
+    const int tm = tile / tiles_n, tn = tile % tiles_n;
+    const i64 m0 = (i64)tm * kBM, n0 = (i64)tn * kBN;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = (wave >> 1) * (kBM / 2), wn = (wave & 1) * (kBN / 2);
+    const T *Bn = B + n * Tn * dout;
+    const T *An = A + n * Tn * din;
+    const bool do_bias = gb != nullptr && tn == 0;
+
+    MfmaTile<kBM, kBN> t;
+    t.zero();
+    float bias_acc = 0.0f;
+
+    for (i64 k0 = 0; k0 < Tn; k0 += kBK) {
+        for (int e = tid; e < kBK * kBM; e += kThreads) {
+            const int kk = e / kBM, ii = e % kBM;
+            const i64 k = k0 + kk, i = m0 + ii;
+            As[e] = (k < Tn && i < dout) ? load_elem<T>(Bn, k * dout + i) : 0.0f;
+        }
+        for (int e = tid; e < kBK * kBN; e += kThreads) {
+            const int kk = e / kBN, jj = e % kBN;
+            const i64 k = k0 + kk, j = n0 + jj;
+            Bs[e] = (k < Tn && j < din) ? load_elem<T>(An, k * din + j) : 0.0f;
+        }
+        __syncthreads();
+        t.template mma<kBK>(As, kBM, Bs, kBN, wm, wn, lane);
+        if (do_bias && tid < kBM) {
+#pragma unroll 8
+            for (int kk = 0; kk < kBK; ++kk) bias_acc += As[kk * kBM + tid];
+        }
+        __syncthreads();
+    }
+
+    float sq = 0.0f;
+    float *G = gW + n * dout * din;
+    t.for_each(wm, wn, lane, [&](int r, int c, float v) {
+        const i64 i = m0 + r, j = n0 + c;
+        if (i < dout && j < din) {
+            const float g = scale * v;
+            G[i * din + j] = g;
+            sq += g * g;
+        }
+    });
+    if (do_bias && tid < kBM && m0 + tid < dout) {
+        const float g = scale * bias_acc;
+        gb[n * dout + m0 + tid] = g;
+        sq += g * g;
+    }
+    sq = block_sum(sq, red);
+    if (partial && tid == 0) partial[n * tiles + tile] = sq;
+}
+
+// sqnorm[n] = sum of the sample's tile partials, in tile order.
+__global__ void reduce_partials_kernel(const float *__restrict__ partial, i64 N, int tiles,
+                                       float *__restrict__ sqnorm)
+{
+    const i64 n = (i64)blockIdx.x * blockDim.x + threadIdx.x;
+    if (n >= N) return;
+    float s = 0.0f;
+    for (int t = 0; t < tiles; ++t) s += partial[n * tiles + t];
+    sqnorm[n] = s;
+}
+
+// ---------------------------------------------------------------------------
+// Fused clipped sum: block = (split, tile).  Rows of the flattened [N*T]
+// operands are scaled by s * c_n as they are staged.
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(kThreads) void clipsum_gemm_kernel(
+    const T *__restrict__ A, const T *__restrict__ B, i64 Tn, i64 rows_total, i64 rows_per_split,
+    i64 din, i64 dout, int tiles_n, int tiles, float scale, const float *__restrict__ norm,
+    float C, float *__restrict__ outW, float *__restrict__ outb, i64 split_strideW,
+    i64 split_strideb)
+{
+    __shared__ float As[kBK * kBM];
+    __shared__ float Bs[kBK * kBN];
+    __shared__ float rs[kBK];
+    const int split = blockIdx.x / tiles;
+    const int tile = blockIdx.x % tiles;
+    const int tm = tile / tiles_n, tn = tile % tiles_n;
+    const i64 m0 = (i64)tm * kBM, n0 = (i64)tn * kBN;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = (wave >> 1) * (kBM / 2), wn = (wave & 1) * (kBN / 2);
+    const i64 r0 = (i64)split * rows_per_split;
+    const i64 r1 = r0 + rows_per_split < rows_total ? r0 + rows_per_split : rows_total;
+    const bool do_bias = outb != nullptr && tn == 0;
+
+    MfmaTile<kBM, kBN> t;
+    t.zero();
+    float bias_acc = 0.0f;
+
+    for (i64 k0 = r0; k0 < r1; k0 += kBK) {
+        if (tid < kBK) {
+            const i64 k = k0 + tid;
+            rs[tid] = k < r1 ? scale * clip_factor(norm[k / Tn], C) : 0.0f;
+        }
+        __syncthreads();
+        for (int e = tid; e < kBK * kBM; e += kThreads) {
+            const int kk = e / kBM, ii = e % kBM;
+            const i64 k = k0 + kk, i = m0 + ii;
+            As[e] = (k < r1 && i < dout) ? rs[kk] * load_elem<T>(B, k * dout + i) : 0.0f;
+        }
+        for (int e = tid; e < kBK * kBN; e += kThreads) {
+            const int kk = e / kBN, jj = e % kBN;
+            const i64 k = k0 + kk, j = n0 + jj;
+            Bs[e] = (k < r1 && j < din) ? load_elem<T>(A, k * din + j) : 0.0f;
+        }
+        __syncthreads();
+        t.template mma<kBK>(As, kBM, Bs, kBN, wm, wn, lane);
+        if (do_bias && tid < kBM) {
+#pragma unroll 8
+            for (int kk = 0; kk < kBK; ++kk) bias_acc += As[kk * kBM + tid];
+        }
+        __syncthreads();
+    }
+
+    float *O = outW + (i64)split * split_strideW;
+    t.for_each(wm, wn, lane, [&](int r, int c, float v) {
+        const i64 i = m0 + r, j = n0 + c;
+        if (i < dout && j < din) O[i * din + j] = v;
+    });
+    if (do_bias && tid < kBM && m0 + tid < dout) outb[(i64)split * split_strideb + m0 + tid] = bias_acc;
+}
+
+// out[e] = sum_s part[s][e], s ascending.
+__global__ void split_sum_kernel(const float *__restrict__ part, int splits, i64 count,
+                                 float *__restrict__ out)
+{
+    const i64 e = (i64)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= count) return;
+    float s = 0.0f;
+    for (int k = 0; k < splits; ++k) s += part[(i64)k * count + e];
+    out[e] = s;
+}
+
+struct ClipSplit {
+    int tiles_n, tiles, splits;
+    i64 rows_per_split;
+};
+
+ClipSplit clip_split(i64 N, i64 T, i64 din, i64 dout)
+{
+    ClipSplit s;
+    s.tiles_n = (int)ceil_div(din, kBN);
+    s.tiles = (int)ceil_div(dout, kBM) * s.tiles_n;
+    const i64 rows = N * T;
+    const i64 chunks = ceil_div(rows, kBK);
+    i64 want = ceil_div(1024, s.tiles);           // aim for ~1024 workgroups
+    if (want > chunks) want = chunks;
+    if (want > 256) want = 256;
+    if (want < 1) want = 1;
+    s.rows_per_split = ceil_div(chunks, want) * kBK;
+    s.splits = (int)(rows > 0 ? ceil_div(rows, s.rows_per_split) : 1);
+    return s;
+}
+
+dp_status check_linear(const void *A, const void *B, dp_dtype dt, i64 N, i64 T, i64 din, i64 dout)
+{
+    DPG_REQUIRE(dtype_ok(dt), DP_EDTYPE);
+    DPG_REQUIRE(N >= 0 && T >= 0 && din >= 1 && dout >= 1, DP_EINVAL);
+    DPG_REQUIRE(N * T == 0 || (A != nullptr && B != nullptr), DP_EINVAL);
+    DPG_REQUIRE(N < (i64(1) << 40) && T < (i64(1) << 40), DP_EINVAL);
+    return DP_OK;
+}
+
+}  // namespace
+}  // namespace dpg
+
+using namespace dpg;
+
+extern "C" size_t dp_grad_sample_linear_workspace_bytes(int64_t N, int64_t T, int64_t d_in,
+                                                        int64_t d_out, dp_dtype dt)
+{
+    (void)dt;
+    if (N <= 0 || T <= 1 || d_in <= 0 || d_out <= 0) return 0;
+    const i64 tiles = ceil_div(d_in, kBN) * ceil_div(d_out, kBM);
+    return (size_t)(N * tiles) * sizeof(float);
+}
+
+extern "C" dp_status dp_grad_sample_linear(const void *A, const void *B, dp_dtype dt, int64_t N,
+                                           int64_t T, int64_t d_in, int64_t d_out, float scale,
+                                           float *gW, float *gb, float *sqnorm, int32_t *status,
+                                           void *ws, size_t ws_bytes, hipStream_t stream)
+{
+    (void)status;
+    dp_status st = check_linear(A, B, dt, N, T, d_in, d_out);
+    if (st != DP_OK) return st;
+    DPG_REQUIRE(N == 0 || gW != nullptr, DP_EINVAL);
+    const size_t need = dp_grad_sample_linear_workspace_bytes(N, T, d_in, d_out, dt);
+    DPG_REQUIRE(ws_bytes >= need && (need == 0 || ws != nullptr), DP_EINVAL);
+    if (N == 0) return DP_OK;
+
+    if (T == 0) {
+        // empty sum over positions: every gradient and norm is zero
+        zero_fill(gW, N * d_out * d_in, stream);
+        zero_fill(gb, N * d_out, stream);
+        zero_fill(sqnorm, N, stream);
+        return launch_status();
+    }
+    if (T == 1) {
+        int rows = (int)(8192 / d_in);
+        if (rows < 1) rows = 1;
+        if (rows > d_out) rows = (int)d_out;
+        const int bps = (int)ceil_div(d_out, rows);
+        const dim3 grid((unsigned)(N * bps));
+        const bool vec = (d_in % 4) == 0 && aligned(A, dt == DP_F32 ? 16 : 8) && aligned(gW, 16);
+        if (dt == DP_F32) {
+            if (vec)
+                outer_kernel<float, true><<<grid, kThreads, 0, stream>>>(
+                    (const float *)A, (const float *)B, d_in, d_out, rows, bps, scale, gW, gb, sqnorm);
+            else
+                outer_kernel<float, false><<<grid, kThreads, 0, stream>>>(
+                    (const float *)A, (const float *)B, d_in, d_out, rows, bps, scale, gW, gb, sqnorm);
+        } else {
+            if (vec)
+                outer_kernel<uint16_t, true><<<grid, kThreads, 0, stream>>>(
+                    (const uint16_t *)A, (const uint16_t *)B, d_in, d_out, rows, bps, scale, gW, gb, sqnorm);
+            else
+                outer_kernel<uint16_t, false><<<grid, kThreads, 0, stream>>>(
+                    (const uint16_t *)A, (const uint16_t *)B, d_in, d_out, rows, bps, scale, gW, gb, sqnorm);
+        }
+        return launch_status();
+    }
+
+    const int tiles_n = (int)ceil_div(d_in, kBN);
+    const int tiles = (int)ceil_div(d_out, kBM) * tiles_n;
+    float *partial = sqnorm ? (float *)ws : nullptr;
+    const dim3 grid((unsigned)(N * tiles));
+    if (dt == DP_F32)
+        per_sample_gemm_kernel<float><<<grid, kThreads, 0, stream>>>(
+            (const float *)A, (const float *)B, T, d_in, d_out, tiles_n, tiles, scale, gW, gb, partial);
+    else
+        per_sample_gemm_kernel<uint16_t><<<grid, kThreads, 0, stream>>>(
+            (const uint16_t *)A, (const uint16_t *)B, T, d_in, d_out, tiles_n, tiles, scale, gW, gb, partial);
+    if (sqnorm)
+        reduce_partials_kernel<<<(unsigned)ceil_div(N, 256), 256, 0, stream>>>(partial, N, tiles, sqnorm);
+    return launch_status();
+}
+
+extern "C" size_t dp_clip_accumulate_linear_workspace_bytes(int64_t N, int64_t T, int64_t d_in,
+                                                            int64_t d_out, dp_dtype dt)
+{
+    (void)dt;
+    if (N <= 0 || T <= 0 || d_in <= 0 || d_out <= 0) return 0;
+    const ClipSplit s = clip_split(N, T, d_in, d_out);
+    if (s.splits <= 1) return 0;
+    return (size_t)s.splits * (size_t)(d_out * d_in + d_out) * sizeof(float);
+}
+
+extern "C" dp_status dp_clip_accumulate_linear(const void *A, const void *B, dp_dtype dt,
+                                               int64_t N, int64_t T, int64_t d_in, int64_t d_out,
+                                               float scale, const float *norm, float C,
+                                               float *sumW, float *sumb, int32_t *status,
+                                               void *ws, size_t ws_bytes, hipStream_t stream)
+{
+    (void)status;
+    dp_status st = check_linear(A, B, dt, N, T, d_in, d_out);
+    if (st != DP_OK) return st;
+    DPG_REQUIRE(sumW != nullptr && (N == 0 || norm != nullptr), DP_EINVAL);
+    DPG_REQUIRE(C > 0.0f, DP_EINVAL);
+    const size_t need = dp_clip_accumulate_linear_workspace_bytes(N, T, d_in, d_out, dt);
+    DPG_REQUIRE(ws_bytes >= need && (need == 0 || ws != nullptr), DP_EINVAL);
+    if (N * T == 0) {
+        zero_fill(sumW, d_out * d_in, stream);
+        zero_fill(sumb, d_out, stream);
+        return launch_status();
+    }
+    const ClipSplit s = clip_split(N, T, d_in, d_out);
+    const i64 cw = d_out * d_in;
+    float *pw = s.splits > 1 ? (float *)ws : sumW;
+    float *pb = sumb ? (s.splits > 1 ? (float *)ws + (i64)s.splits * cw : sumb) : nullptr;
+    const dim3 grid((unsigned)(s.splits * s.tiles));
+    if (dt == DP_F32)
+        clipsum_gemm_kernel<float><<<grid, kThreads, 0, stream>>>(
+            (const float *)A, (const float *)B, T, N * T, s.rows_per_split, d_in, d_out, s.tiles_n,
+            s.tiles, scale, norm, C, pw, pb, cw, d_out);
+    else
+        clipsum_gemm_kernel<uint16_t><<<grid, kThreads, 0, stream>>>(
+            (const uint16_t *)A, (const uint16_t *)B, T, N * T, s.rows_per_split, d_in, d_out,
+            s.tiles_n, s.tiles, scale, norm, C, pw, pb, cw, d_out);
+    if (s.splits > 1) {
+        split_sum_kernel<<<(unsigned)ceil_div(cw, 256), 256, 0, stream>>>(pw, s.splits, cw, sumW);
+        if (sumb)
+            split_sum_kernel<<<(unsigned)ceil_div(d_out, 256), 256, 0, stream>>>(pb, s.splits, d_out, sumb);
+    }
+    return launch_status();
+}

@@ -1,0 +1,132 @@
+"""C-ABI contract on the CPU: the library loads, exports every declared symbol,
+and rejects invalid arguments on the host before anything reaches HIP."""
+import math
+import os
+import re
+
+import pytest
+
+from paper_2109_12298_amd import binding as dp
+from paper_2109_12298_amd import step as stepmod
+from paper_2109_12298_amd import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_symbols():
+    names = set()
+    inc = os.path.join(ROOT, "include")
+    for fn in os.listdir(inc):
+        if fn.endswith(".h"):
+            text = open(os.path.join(inc, fn)).read()
+            text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+            names |= set(re.findall(r"\b(dp_[a-z0-9_]+)\s*\(", text))
+    return names
+
+
+def test_library_exports_every_declared_symbol():
+    L = dp.lib()
+    names = declared_symbols()
+    assert len(names) >= 20
+    for n in names:
+        assert hasattr(L, n), n
+    assert names == set(dp.SIGNATURES), names ^ set(dp.SIGNATURES)
+
+
+def test_status_strings_and_version():
+    assert dp.dp_abi_version() == 1
+    for code in range(6):
+        s = dp.dp_status_string(code)
+        assert s.startswith(["DP_OK", "DP_EINVAL", "DP_EDTYPE", "DP_EUNSUPPORTED", "DP_ECAP", "DP_EHIP"][code])
+    assert dp.dp_status_string(99) == "unknown dp_status"
+
+
+def code_of(fn, *a, **k):
+    try:
+        fn(*a, **k)
+    except dp.DPError as e:
+        return e.code
+    return dp.DP_OK
+
+
+# Addresses below are never dereferenced: every call fails validation first.
+FAKE = 0x1000
+
+
+def test_linear_validation():
+    f = dp.dp_grad_sample_linear
+    assert code_of(f, FAKE, FAKE, 7, 2, 1, 3, 4, 1.0, FAKE, stream=0) == dp.DP_EDTYPE
+    assert code_of(f, FAKE, FAKE, dp.DP_F32, -1, 1, 3, 4, 1.0, FAKE, stream=0) == dp.DP_EINVAL
+    assert code_of(f, FAKE, FAKE, dp.DP_F32, 2, 1, 0, 4, 1.0, FAKE, stream=0) == dp.DP_EINVAL
+    assert code_of(f, None, FAKE, dp.DP_F32, 2, 1, 3, 4, 1.0, FAKE, stream=0) == dp.DP_EINVAL
+    assert code_of(f, FAKE, FAKE, dp.DP_F32, 2, 1, 3, 4, 1.0, None, stream=0) == dp.DP_EINVAL
+    # T > 1 with a per-sample norm needs a workspace
+    assert dp.dp_grad_sample_linear_workspace_bytes(2, 8, 3, 4, dp.DP_F32) > 0
+    assert code_of(f, FAKE, FAKE, dp.DP_F32, 2, 8, 3, 4, 1.0, FAKE, None, FAKE, stream=0) == dp.DP_EINVAL
+    assert dp.dp_grad_sample_linear_workspace_bytes(2, 1, 3, 4, dp.DP_F32) == 0
+
+
+def test_conv_validation():
+    f = dp.dp_grad_sample_conv2d
+    # N, Cin, H, W, Cout, Ho, Wo, kh, kw, sh, sw, ph, pw, dh, dw, groups
+    good = (2, 3, 8, 8, 4, 8, 8, 3, 3, 1, 1, 1, 1, 1, 1, 1)
+    assert code_of(f, FAKE, FAKE, dp.DP_F32, *good[:15], 2, 1.0, FAKE, stream=0) == dp.DP_EUNSUPPORTED
+    bad_dil = good[:13] + (2, 1, 1)
+    assert code_of(f, FAKE, FAKE, dp.DP_F32, *bad_dil, 1.0, FAKE, stream=0) == dp.DP_EUNSUPPORTED
+    bad_ho = good[:5] + (7,) + good[6:]
+    assert code_of(f, FAKE, FAKE, dp.DP_F32, *bad_ho, 1.0, FAKE, stream=0) == dp.DP_EINVAL
+    too_small = (2, 3, 2, 2, 4, 0, 0, 5, 5, 1, 1, 0, 0, 1, 1, 1)
+    assert code_of(f, FAKE, FAKE, dp.DP_F32, *too_small, 1.0, FAKE, stream=0) == dp.DP_EINVAL
+    assert code_of(f, FAKE, FAKE, 9, *good, 1.0, FAKE, stream=0) == dp.DP_EDTYPE
+
+
+def test_embedding_layernorm_validation():
+    f = dp.dp_grad_sample_embedding
+    assert code_of(f, FAKE, FAKE, dp.DP_F32, 2, 5000, 10, 4, 1.0, FAKE, FAKE, FAKE, 10, stream=0) == \
+        dp.DP_EUNSUPPORTED
+    assert code_of(f, FAKE, FAKE, dp.DP_F32, 2, 5, 2**31, 4, 1.0, FAKE, FAKE, FAKE, 10, stream=0) == dp.DP_EINVAL
+    assert code_of(f, FAKE, FAKE, dp.DP_F32, 2, 5, 10, 4, 1.0, None, FAKE, FAKE, 10, stream=0) == dp.DP_EINVAL
+    assert code_of(f, FAKE, FAKE, dp.DP_F32, 2, 5, 10, 4, 1.0, FAKE, FAKE, FAKE, 10, None, None, None,
+                   stream=0) == dp.DP_EINVAL   # workspace required
+    g = dp.dp_grad_sample_layernorm
+    assert code_of(g, FAKE, FAKE, dp.DP_F32, 2, 5, 0, 1.0, FAKE, FAKE, stream=0) == dp.DP_EINVAL
+    assert code_of(g, FAKE, FAKE, dp.DP_F32, 2, 5, 8, 1.0, FAKE, None, stream=0) == dp.DP_EINVAL
+
+
+def test_clip_and_noise_validation():
+    assert code_of(dp.dp_clip_factors, FAKE, 4, 0.0, FAKE, stream=0) == dp.DP_EINVAL
+    assert code_of(dp.dp_clip_factors, FAKE, 4, -1.0, FAKE, stream=0) == dp.DP_EINVAL
+    assert code_of(dp.dp_per_sample_norms, None, 2, 4, FAKE, stream=0) == dp.DP_EINVAL
+    assert code_of(dp.dp_clip_accumulate, FAKE, FAKE, 1.0, 4, 10, None, stream=0) == dp.DP_EINVAL
+    n = dp.dp_clip_accumulate_workspace_bytes(4096, 10)
+    assert n > 0
+    assert code_of(dp.dp_clip_accumulate, FAKE, FAKE, 1.0, 4096, 10, FAKE, stream=0) == dp.DP_EINVAL
+    assert code_of(dp.dp_clip_accumulate_embedding, FAKE, FAKE, FAKE, FAKE, 1.0, 2, 0, 4, FAKE,
+                   stream=0) == dp.DP_EINVAL
+    f = dp.dp_add_noise
+    assert code_of(f, FAKE, FAKE, 16, 0, 0, 0, 1.0, math.inf, 4.0, stream=0) == dp.DP_EINVAL  # sigma>0, C=inf
+    assert code_of(f, FAKE, FAKE, 16, 0, 0, 0, -1.0, 1.0, 4.0, stream=0) == dp.DP_EINVAL
+    assert code_of(f, FAKE, FAKE, 16, 0, 0, 0, 1.0, 1.0, 0.0, stream=0) == dp.DP_EINVAL
+    assert code_of(f, None, FAKE, 16, 0, 0, 0, 1.0, 1.0, 1.0, stream=0) == dp.DP_EINVAL
+    assert code_of(f, FAKE, FAKE, 2**34 + 4, 0, 0, 0, 1.0, 1.0, 1.0, stream=0) == dp.DP_EINVAL
+    # empty inputs are valid no-ops that enqueue nothing
+    assert code_of(f, None, None, 0, 0, 0, 0, 1.0, 1.0, 1.0, stream=0) == dp.DP_OK
+    assert code_of(dp.dp_philox_normals, None, None, 0, 0, 0, 0, stream=0) == dp.DP_OK
+    assert code_of(dp.dp_grad_sample_linear, None, None, dp.DP_F32, 0, 3, 4, 5, 1.0, None, stream=0) == dp.DP_OK
+
+
+def test_clip_sum_route_choice():
+    # T = 1 Linear: the fused GEMM reads A and B (N*(d_in+d_out)) instead of N*P grads
+    assert stepmod.linear_clip_mode(W.Linear("fc1", 512, 32), 256, W.F32) == "fused"
+    # LSTM weights (K = N*T = 16384, small outputs): rereading the grads is cheaper
+    assert stepmod.linear_clip_mode(W.Linear("ih", 100, 400, T=256), 64, W.F32) == "colreduce"
+
+
+def test_product_path_never_touches_the_oracle():
+    pkg = os.path.join(ROOT, "paper_2109_12298_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for fn in files:
+            if fn.endswith((".py", ".hip", ".hpp", ".h", ".cpp")):
+                text = open(os.path.join(dirpath, fn)).read()
+                assert "import oracle" not in text and "from oracle" not in text, fn
+                assert "dp_oracle" not in text and "liboracle" not in text, fn

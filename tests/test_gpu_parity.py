@@ -1,0 +1,320 @@
+"""GPU parity: every step of the HIP path against the fp64 oracle on the same
+seeded inputs, through the C ABI.  Sizes keep the oracle to seconds while
+still spanning several tiles and ragged tails."""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from compare import RTOL, assert_g12, assert_rel
+from paper_2109_12298_amd import binding as dp
+from paper_2109_12298_amd import workloads as W
+from paper_2109_12298_amd.step import DPStep
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def say(*a):
+    print("[case]", *a, file=sys.stderr, flush=True)
+
+
+def compare_step(wl, inputs, got, ref, rtol, what):
+    for li, g, r in zip(inputs, got["grads"], ref["grads"]):
+        name = li.layer.name
+        if "csr" in r:
+            rp, uq, rows = g["csr"]
+            rrp, ruq, rrows = r["csr"]
+            np.testing.assert_array_equal(rp, rrp, err_msg=what + " row_ptr " + name)
+            np.testing.assert_array_equal(uq, ruq, err_msg=what + " uniq " + name)
+            assert_g12(rows, rrows, rtol, what + " rows " + name)
+        else:
+            for k in r:
+                assert_g12(g[k], r[k], rtol, "%s grad %s.%s" % (what, name, k))
+    assert_rel(got["sq_layers"], ref["sq_layers"], rtol, what + " sqnorm")
+    assert_rel(got["norm"], ref["norm"], rtol, what + " norm")
+    for k in ref["S"]:
+        assert_g12(got["S"][k], ref["S"][k], rtol, what + " S " + k)
+    for k in ref["out"]:
+        assert_g12(got["out"][k], ref["out"][k], rtol, what + " out " + k)
+    assert got["status"] == 0
+
+
+SMALL = [("linear_tiny", None), ("mnist_cnn", None), ("cifar_cnn", 3), ("text_lstm", 5),
+         ("transformer_block", 2)]
+
+
+@pytest.mark.parametrize("name,n", SMALL)
+@pytest.mark.parametrize("mode", ["auto", "fused", "colreduce"])
+def test_workload_step_matches_oracle(name, n, mode):
+    wl = W.get(name)
+    if mode != "auto" and not any(isinstance(l, W.Linear) for l in wl.layers):
+        pytest.skip("no Linear layer")
+    say(name, "n=", n, "mode=", mode)
+    inputs = W.make_inputs(wl, n=n)
+    st = DPStep(wl, inputs, DEV, clip_mode=mode)
+    st.run(step=3)
+    got = st.results()
+    ref = oracle.dp_step(wl, inputs, step=3)
+    compare_step(wl, inputs, got, ref, RTOL[wl.dtype], name)
+
+
+def test_runs_are_bitwise_deterministic():
+    wl = W.get("text_lstm")
+    inputs = W.make_inputs(wl, n=7)
+    st = DPStep(wl, inputs, DEV)
+    say("determinism text_lstm")
+    st.run(step=1)
+    a = st.results()
+    st.run(step=1)
+    b = st.results()
+    for k in a["out"]:
+        np.testing.assert_array_equal(a["out"][k], b["out"][k])
+        np.testing.assert_array_equal(a["S"][k], b["S"][k])
+    np.testing.assert_array_equal(a["norm"], b["norm"])
+
+
+def test_noise_stream_bits_and_values():
+    for numel, seed, step, pidx in [(1, 0, 0, 0), (7, 3, 5, 2), (1000003, 0, 0, 1), (4096, 2**63 + 11, 2**40 + 3, 9)]:
+        say("philox", numel, seed, step, pidx)
+        z = torch.empty(numel, dtype=torch.float32, device=DEV)
+        raw = torch.empty(numel, dtype=torch.int32, device=DEV)
+        dp.dp_philox_normals(z, raw, numel, seed, step, pidx)
+        torch.cuda.synchronize()
+        rraw, rz = oracle.philox_normals(numel, seed, step, pidx)
+        np.testing.assert_array_equal(raw.cpu().numpy().view(np.uint32), rraw)
+        zg = z.cpu().numpy().astype(np.float64)
+        assert np.max(np.abs(zg - rz) / (1 + np.abs(rz))) < 2e-6
+
+
+def test_add_noise_matches_oracle_and_is_resumable():
+    r = np.random.default_rng(0)
+    S = r.standard_normal(12345).astype(np.float32)
+    St = torch.from_numpy(S).to(DEV)
+    outs = []
+    for step in range(3):
+        say("add_noise step", step)
+        o = torch.empty_like(St)
+        dp.dp_add_noise(St, o, S.size, 42, step, 7, 0.8, 1.5, 32.0)
+        outs.append(o.cpu().numpy())
+        ref = oracle.add_noise(S.astype(np.float64), 42, step, 7, 0.8, 1.5, 32.0)
+        assert_g12(outs[-1], ref, 1e-5, "add_noise")
+    # resume: a fresh call for step 1 reproduces it exactly; in place is allowed
+    o = St.clone()
+    dp.dp_add_noise(o, o, S.size, 42, 1, 7, 0.8, 1.5, 32.0)
+    np.testing.assert_array_equal(o.cpu().numpy(), outs[1])
+    # sigma = 0 with C = inf: plain division
+    o = torch.empty_like(St)
+    dp.dp_add_noise(St, o, S.size, 42, 0, 7, 0.0, math.inf, 4.0)
+    np.testing.assert_array_equal(o.cpu().numpy(), S / np.float32(4.0))
+
+
+LINEAR_SHAPES = [(1, 1, 1, 1), (3, 1, 37, 13), (2, 2, 5, 3), (4, 5, 37, 13), (3, 33, 65, 70),
+                 (2, 70, 130, 64), (5, 1, 4096, 10), (2, 17, 3, 129)]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("N,T,din,dout", LINEAR_SHAPES)
+def test_linear_ragged_shapes(dtype, N, T, din, dout):
+    say("linear", dtype, N, T, din, dout)
+    r = np.random.default_rng(N * 1000 + T)
+    A = r.standard_normal((N, T, din)).astype(np.float32)
+    B = (r.standard_normal((N, T, dout)) / 8).astype(np.float32)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    At = torch.from_numpy(A).to(tdt).to(DEV)
+    Bt = torch.from_numpy(B).to(tdt).to(DEV)
+    dt = dp.DP_BF16 if dtype == "bf16" else dp.DP_F32
+    gW = torch.empty((N, dout, din), device=DEV)
+    gb = torch.empty((N, dout), device=DEV)
+    sq = torch.empty(N, device=DEV)
+    ws = torch.empty(max(dp.dp_grad_sample_linear_workspace_bytes(N, T, din, dout, dt), 1),
+                     dtype=torch.uint8, device=DEV)
+    dp.dp_grad_sample_linear(At, Bt, dt, N, T, din, dout, 0.7, gW, gb, sq, None, ws)
+    Ad = At.float().cpu().numpy().astype(np.float64)
+    Bd = Bt.float().cpu().numpy().astype(np.float64)
+    rW, rb = oracle.linear_grad(Ad, Bd, 0.7)
+    rsq = np.zeros(N)
+    oracle.sqnorm_accumulate(rW, rsq); oracle.sqnorm_accumulate(rb, rsq)
+    assert_g12(gW.cpu().numpy(), rW, 1e-4, "gW")
+    assert_g12(gb.cpu().numpy(), rb, 1e-4, "gb")
+    assert_rel(sq.cpu().numpy(), rsq, 1e-4, "sqnorm")
+    # fused clipped sum against the oracle's clipped sum of the per-sample grads
+    norm = np.sqrt(rsq)
+    C = float(np.median(norm))
+    c = oracle.clip_factors(norm, C)
+    normt = torch.from_numpy(norm.astype(np.float32)).to(DEV)
+    sW = torch.empty((dout, din), device=DEV)
+    sb = torch.empty(dout, device=DEV)
+    ws2 = torch.empty(max(dp.dp_clip_accumulate_linear_workspace_bytes(N, T, din, dout, dt), 1),
+                      dtype=torch.uint8, device=DEV)
+    dp.dp_clip_accumulate_linear(At, Bt, dt, N, T, din, dout, 0.7, normt, C, sW, sb, None, ws2)
+    cf = oracle.clip_factors(norm.astype(np.float32).astype(np.float64), C)
+    assert_g12(sW.cpu().numpy(), oracle.clip_sum(rW, cf), 1e-4, "fused sumW")
+    assert_g12(sb.cpu().numpy(), oracle.clip_sum(rb, cf), 1e-4, "fused sumb")
+    # column reduction over the stored per-sample grads
+    s2 = torch.empty((dout, din), device=DEV)
+    cout = torch.empty(N, device=DEV)
+    ws3 = torch.empty(max(dp.dp_clip_accumulate_workspace_bytes(N, dout * din), 1), dtype=torch.uint8, device=DEV)
+    dp.dp_clip_accumulate(gW, normt, C, N, dout * din, s2, cout, None, ws3)
+    assert_g12(s2.cpu().numpy(), oracle.clip_sum(rW, cf), 1e-4, "colreduce sumW")
+    assert_rel(cout.cpu().numpy(), cf, 1e-6, "c")
+
+
+CONV_SHAPES = [  # N, Cin, H, W, Cout, kh, kw, sh, sw, ph, pw
+    (2, 3, 7, 9, 5, 3, 3, 2, 2, 1, 1), (3, 1, 28, 28, 16, 8, 8, 2, 2, 3, 3), (2, 16, 13, 13, 32, 4, 4, 2, 2, 0, 0),
+    (2, 3, 32, 32, 32, 3, 3, 1, 1, 1, 1), (1, 70, 6, 5, 33, 1, 1, 1, 1, 0, 0), (2, 5, 9, 4, 66, 2, 3, 1, 2, 1, 0),
+    (1, 130, 8, 8, 129, 3, 3, 1, 1, 1, 1)]
+
+
+@pytest.mark.parametrize("shape", CONV_SHAPES)
+def test_conv_shapes(shape):
+    N, Cin, H, Wd, Cout, kh, kw, sh, sw, ph, pw = shape
+    say("conv", shape)
+    Ho = (H + 2 * ph - kh) // sh + 1
+    Wo = (Wd + 2 * pw - kw) // sw + 1
+    r = np.random.default_rng(sum(shape))
+    X = r.standard_normal((N, Cin, H, Wd)).astype(np.float32)
+    GY = (r.standard_normal((N, Cout, Ho, Wo)) / 4).astype(np.float32)
+    Xt, Gt = torch.from_numpy(X).to(DEV), torch.from_numpy(GY).to(DEV)
+    gW = torch.empty((N, Cout, Cin, kh, kw), device=DEV)
+    gb = torch.empty((N, Cout), device=DEV)
+    sq = torch.empty(N, device=DEV)
+    ws = torch.empty(max(dp.dp_grad_sample_conv2d_workspace_bytes(N, Cin, Cout, kh, kw), 1), dtype=torch.uint8,
+                     device=DEV)
+    dp.dp_grad_sample_conv2d(Xt, Gt, dp.DP_F32, N, Cin, H, Wd, Cout, Ho, Wo, kh, kw, sh, sw, ph, pw, 1, 1, 1, 1.3,
+                             gW, gb, sq, None, ws)
+    rW, rb = oracle.conv2d_grad(X, GY, (kh, kw), (sh, sw), (ph, pw), 1.3)
+    rsq = np.zeros(N)
+    oracle.sqnorm_accumulate(rW, rsq); oracle.sqnorm_accumulate(rb, rsq)
+    assert_g12(gW.cpu().numpy(), rW, 1e-4, "conv gW")
+    assert_g12(gb.cpu().numpy(), rb, 1e-4, "conv gb")
+    assert_rel(sq.cpu().numpy(), rsq, 1e-4, "conv sqnorm")
+
+
+def run_embedding(ids, B, V, cap=None, scale=1.0):
+    N, T = ids.shape
+    D = B.shape[2]
+    cap = N * T if cap is None else cap
+    idt = torch.from_numpy(ids).to(DEV)
+    Bt = torch.from_numpy(B.astype(np.float32)).to(DEV)
+    rp = torch.empty(N + 1, dtype=torch.int64, device=DEV)
+    uq = torch.full((max(cap, 1),), -7, dtype=torch.int64, device=DEV)
+    rows = torch.zeros((max(cap, 1), D), device=DEV)
+    sq = torch.empty(N, device=DEV)
+    st = torch.zeros(1, dtype=torch.int32, device=DEV)
+    ws = torch.empty(max(dp.dp_grad_sample_embedding_workspace_bytes(N, T), 1), dtype=torch.uint8, device=DEV)
+    dp.dp_grad_sample_embedding(idt, Bt, dp.DP_F32, N, T, V, D, scale, rp, uq, rows, cap, sq, st, ws)
+    torch.cuda.synchronize()
+    return rp.cpu().numpy(), uq.cpu().numpy(), rows.cpu().numpy(), sq.cpu().numpy(), int(st.item())
+
+
+@pytest.mark.parametrize("case", ["zipf", "truncated", "all_equal", "all_distinct", "T1", "long"])
+def test_embedding_cases(case):
+    say("embedding", case)
+    r = np.random.default_rng(11)
+    V, D = 1000, 37
+    if case == "zipf":
+        ids = np.minimum(r.zipf(1.1, (9, 256)), V) - 1
+    elif case == "truncated":
+        wl = W.Workload(99, "t", 6, W.F32, 1.0, 1.0, (W.Embedding("e", V, D, 200, truncate=True),))
+        ids = W.make_inputs(wl)[0].ids
+    elif case == "all_equal":
+        ids = np.full((3, 50), 17)
+    elif case == "all_distinct":
+        ids = np.stack([r.permutation(V)[:300] for _ in range(4)])
+    elif case == "T1":
+        ids = r.integers(0, V, (8, 1))
+    else:
+        ids = r.integers(0, 40, (2, 4096))
+    ids = ids.astype(np.int64)
+    B = r.standard_normal(ids.shape + (D,))
+    B32 = B.astype(np.float32).astype(np.float64)
+    rp, uq, rows, sq, st = run_embedding(ids, B, V, scale=0.5)
+    rrp, ruq, rrows = oracle.embedding_grad(ids, B32, V, 0.5)
+    assert st == 0
+    np.testing.assert_array_equal(rp, rrp)
+    np.testing.assert_array_equal(uq[:rp[-1]], ruq)
+    assert_g12(rows[:rp[-1]], rrows, 1e-4, "rows")
+    rsq = np.array([np.sum(rrows[rrp[n]:rrp[n + 1]] ** 2) for n in range(ids.shape[0])])
+    assert_rel(sq, rsq, 1e-4, "sqnorm")
+    # dense clipped sum
+    norm = np.sqrt(rsq)
+    C = float(np.median(norm))
+    c = oracle.clip_factors(norm.astype(np.float32).astype(np.float64), C)
+    S = torch.empty((V, D), device=DEV)
+    dp.dp_clip_accumulate_embedding(torch.from_numpy(rp).to(DEV), torch.from_numpy(uq).to(DEV),
+                                    torch.from_numpy(rows).to(DEV), torch.from_numpy(norm.astype(np.float32)).to(DEV),
+                                    C, ids.shape[0], V, D, S)
+    assert_g12(S.cpu().numpy(), oracle.clip_sum_embedding(rrp, ruq, rrows, c, V), 1e-4, "dense S")
+
+
+def test_embedding_flags():
+    r = np.random.default_rng(12)
+    ids = r.integers(0, 50, (3, 20)).astype(np.int64)
+    B = r.standard_normal((3, 20, 4))
+    # capacity too small: flagged, true counts kept, nothing written past cap
+    say("embedding cap")
+    rp, uq, rows, sq, st = run_embedding(ids, B, 50, cap=10)
+    assert st & dp.DP_FLAG_CAP
+    rrp, _, _ = oracle.embedding_grad(ids, B, 50)
+    np.testing.assert_array_equal(rp, rrp)
+    # an id outside [0, V): flagged and left out
+    say("embedding bad id")
+    bad = ids.copy(); bad[1, 3] = 50; bad[2, 0] = -1
+    rp, uq, rows, sq, st = run_embedding(bad, B, 50)
+    assert st & dp.DP_FLAG_BAD_INDEX
+
+
+def test_layernorm_and_empty_inputs():
+    r = np.random.default_rng(13)
+    N, T, D = 3, 37, 771
+    xh = r.standard_normal((N, T, D)).astype(np.float32)
+    B = r.standard_normal((N, T, D)).astype(np.float32)
+    say("layernorm")
+    g = torch.empty((N, D), device=DEV); b = torch.empty((N, D), device=DEV); sq = torch.empty(N, device=DEV)
+    ws = torch.empty(dp.dp_grad_sample_layernorm_workspace_bytes(N, T, D), dtype=torch.uint8, device=DEV)
+    dp.dp_grad_sample_layernorm(torch.from_numpy(xh).to(DEV), torch.from_numpy(B).to(DEV), dp.DP_F32, N, T, D, 2.0,
+                                g, b, sq, None, ws)
+    rg, rb = oracle.layernorm_grad(xh, B, 2.0)
+    assert_g12(g.cpu().numpy(), rg, 1e-4, "ggamma")
+    assert_g12(b.cpu().numpy(), rb, 1e-4, "gbeta")
+    assert_rel(sq.cpu().numpy(), (rg ** 2).sum(1) + (rb ** 2).sum(1), 1e-4, "ln sqnorm")
+    # T = 0: empty sums are zero
+    say("linear T=0")
+    gW = torch.full((2, 3, 4), 5.0, device=DEV); gbias = torch.full((2, 3), 5.0, device=DEV)
+    sq = torch.full((2,), 5.0, device=DEV)
+    dp.dp_grad_sample_linear(None, None, dp.DP_F32, 2, 0, 4, 3, 1.0, gW, gbias, sq, None, None)
+    assert float(gW.abs().sum()) == 0 and float(gbias.abs().sum()) == 0 and float(sq.abs().sum()) == 0
+    # N = 0: the clipped sum is zero
+    say("clip N=0")
+    S = torch.full((10,), 5.0, device=DEV)
+    dp.dp_clip_accumulate(None, None, 1.0, 0, 10, S)
+    assert float(S.abs().sum()) == 0
+
+
+def test_nonfinite_sample_poisons_instead_of_passing():
+    wl = W.get("linear_tiny")
+    inputs = W.make_inputs(wl, n=8)
+    inputs[0].B[3, 0] = np.nan
+    say("nonfinite")
+    st = DPStep(wl, inputs, DEV)
+    st.run()
+    got = st.results()
+    assert got["status"] & dp.DP_FLAG_NONFINITE
+    assert math.isnan(got["norm"][3])
+    assert np.isnan(got["S"]["fc.weight"]).any()
+
+
+def test_sigma0_Cinf_reproduces_the_mean_gradient():
+    wl = W.get("mnist_cnn")
+    inputs = W.make_inputs(wl, n=16)
+    say("sigma0 Cinf")
+    st = DPStep(wl, inputs, DEV, C=math.inf, sigma=0.0)
+    st.run()
+    got = st.results()
+    ref = oracle.dp_step(wl, inputs, C=math.inf, sigma=0.0)
+    for k in ref["out"]:
+        assert_g12(got["out"][k], ref["out"][k], 1e-4, k)
