@@ -1,0 +1,276 @@
+"""Benchmark: DP-SGD gradient steps per second on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME]
+
+A step is one pass of the whole hot path over one batch whose inputs are
+already resident in HBM: per-sample gradients of every layer, per-sample
+norms, clip factors, clipped sums, noise and division.  W untimed steps, then
+K timed steps between two device synchronizations; value = samples / second.
+
+Alongside: the dominant kernel's roofline (algorithmic bytes or flops per
+launch over its average duration, timed with HIP events on its own stream
+during the timed steps), HBM traffic from committed rocprofv3 counter runs
+when they still match the kernel source, and the fp64 oracle timed on the
+host's cores on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}     # dense MFMA peaks
+METRIC = "DP-SGD grad step samples/sec at 1 MI355X; achieved HBM GB/s / MFMA util"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+# ---------------------------------------------------------------------------
+# algorithmic cost of each call of the step
+# ---------------------------------------------------------------------------
+
+def call_costs(st):
+    """name -> (algorithmic bytes, flops, kernel name) for each call of one step."""
+    from paper_2109_12298_amd import workloads as W
+    N = st.N
+    e = 2 if st.wl.dtype == W.BF16 else 4
+    out = {}
+    for lb in st.layers:
+        L = lb.layer
+        if isinstance(L, W.Linear):
+            bias = L.d_out if L.bias else 0
+            grads = N * (L.d_out * L.d_in + bias) * 4
+            if L.T == 1:
+                out["grad:" + L.name] = (N * (L.d_in + L.d_out) * e + grads + N * 4, N * L.d_out * L.d_in,
+                                         "outer_kernel")
+            else:
+                out["grad:" + L.name] = (N * L.T * (L.d_in + L.d_out) * e + grads + N * 4,
+                                         2 * N * L.T * L.d_in * L.d_out, "per_sample_gemm_kernel")
+            if lb.clip_mode == "fused":
+                out["clip:" + L.name] = (N * L.T * (L.d_in + L.d_out) * e + (L.d_out * L.d_in + bias) * 4,
+                                         2 * N * L.T * L.d_in * L.d_out, "clipsum_gemm_kernel")
+            else:
+                out["clip:" + L.name] = (grads + (L.d_out * L.d_in + bias) * 4, 2 * N * L.n_params,
+                                         "colsum_kernel")
+        elif isinstance(L, W.Conv2d):
+            ho, wo = L.out_hw
+            kk = L.c_in * L.k[0] * L.k[1]
+            grads = N * L.n_params * 4
+            out["grad:" + L.name] = (N * (L.c_in * L.h * L.w + L.c_out * ho * wo) * e + grads + N * 4,
+                                     2 * N * L.c_out * kk * ho * wo, "conv_per_sample_kernel")
+            out["clip:" + L.name] = (grads + L.n_params * 4, 2 * N * L.n_params, "colsum_kernel")
+        elif isinstance(L, W.Embedding):
+            nnz_bound = N * L.T
+            out["grad:" + L.name] = (N * L.T * (8 + L.D * e) + N * L.T * (L.D * 4 + 8), N * L.T * L.D,
+                                     "emb_rows_kernel")
+            out["clip:" + L.name] = (nnz_bound * L.D * 4 + L.V * L.D * 4, 2 * nnz_bound * L.D,
+                                     "emb_clipsum_kernel")
+        elif isinstance(L, W.LayerNorm):
+            out["grad:" + L.name] = (2 * N * L.T * L.D * e + 2 * N * L.D * 4, 3 * N * L.T * L.D,
+                                     "ln_partial_kernel")
+            out["clip:" + L.name] = (2 * N * L.D * 4 + 2 * L.D * 4, 4 * N * L.D, "colsum_kernel")
+    P = st.wl.n_params
+    out["noise"] = (8 * P, 0, "add_noise_kernel")
+    return out
+
+
+def src_hash(paths):
+    h = hashlib.sha256()
+    for p in paths:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+KERNEL_SOURCES = {
+    "outer_kernel": ["paper_2109_12298_amd/csrc/linear.hip"],
+    "per_sample_gemm_kernel": ["paper_2109_12298_amd/csrc/linear.hip", "paper_2109_12298_amd/csrc/mfma_tile.hpp"],
+    "clipsum_gemm_kernel": ["paper_2109_12298_amd/csrc/linear.hip", "paper_2109_12298_amd/csrc/mfma_tile.hpp"],
+    "conv_per_sample_kernel": ["paper_2109_12298_amd/csrc/conv2d.hip", "paper_2109_12298_amd/csrc/mfma_tile.hpp"],
+    "colsum_kernel": ["paper_2109_12298_amd/csrc/clip.hip"],
+    "emb_rows_kernel": ["paper_2109_12298_amd/csrc/embedding.hip"],
+    "emb_clipsum_kernel": ["paper_2109_12298_amd/csrc/clip.hip"],
+    "ln_partial_kernel": ["paper_2109_12298_amd/csrc/layernorm.hip"],
+    "add_noise_kernel": ["paper_2109_12298_amd/csrc/noise.hip"],
+}
+
+
+def traffic_for(kernel, workload, call):
+    """HBM bytes per launch from committed counter runs, if the kernel source is unchanged."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        table = json.load(f)
+    rec = table.get("%s/%s" % (workload, call))
+    if not rec or rec.get("kernel") != kernel:
+        return None
+    if rec.get("source_sha") != src_hash(KERNEL_SOURCES.get(kernel, [])):
+        return None
+    return rec.get("bytes_per_launch")
+
+
+# ---------------------------------------------------------------------------
+# CPU baseline: the oracle on a bounded sample
+# ---------------------------------------------------------------------------
+
+def cpu_baseline(wl, inputs, budget_s: float):
+    import numpy as np
+    import oracle
+    from paper_2109_12298_amd import workloads as W
+    N = wl.N
+    # a sample of n samples, grown until one oracle step takes a good part of the budget
+    n = max(1, min(N, 8))
+    while True:
+        sub = [W.LayerInputs(li.layer, A=None if li.A is None else li.A[:n], B=li.B[:n],
+                             ids=None if li.ids is None else li.ids[:n]) for li in inputs]
+        t0 = time.perf_counter()
+        oracle.dp_step(wl, sub, step=0, denom=float(N))
+        dt = time.perf_counter() - t0
+        if dt > budget_s / 4 or n >= N:
+            break
+        n = min(N, n * 4 if dt < budget_s / 40 else n * 2)
+    reps, total = 1, dt
+    while total < budget_s and reps < 100000:
+        t0 = time.perf_counter()
+        oracle.dp_step(wl, sub, step=reps, denom=float(N))
+        total += time.perf_counter() - t0
+        reps += 1
+    return {"value": reps * n / total, "unit": "samples/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": "%d of the %d samples of one batch, whole step (grads, norms, clip, sum, noise), "
+                      "%d repetitions, %.1f s" % (n, N, reps, total)}
+
+
+# ---------------------------------------------------------------------------
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="mnist_cnn")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--breakdown", action="store_true", help="print per-call event times to stderr")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="also run a plain device copy of this size (for counter calibration)")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py: this build runs the DP-SGD step on one GPU only; --gpus %d is not supported "
+              "(the step shards by samples, see the design notes)" % max(args.gpus, world), file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2109_12298_amd import workloads as W
+    from paper_2109_12298_amd.step import DPStep
+
+    wl = W.get(args.workload)
+    log("[bench] workload %s: drawing inputs" % wl.name)
+    inputs = W.make_inputs(wl)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    st = DPStep(wl, inputs, dev)
+    stream = torch.cuda.current_stream(dev)
+    costs = call_costs(st)
+
+    # find the dominant call: event-time every call over a few steps
+    names = list(costs)
+    ev = {n: [] for n in names}
+
+    def mark_all(name, where):
+        e = torch.cuda.Event(enable_timing=True)
+        e.record(stream)
+        if where == "start":
+            ev[name].append([e, None])
+        else:
+            ev[name][-1][1] = e
+
+    for i in range(3):
+        st.run(step=i)
+    for i in range(10):
+        st.run(step=i, mark=mark_all)
+    torch.cuda.synchronize()
+    avg = {n: sum(a.elapsed_time(b) for a, b in ev[n]) / len(ev[n]) for n in names if ev[n]}
+    dominant = max(avg, key=avg.get)
+    if args.breakdown:
+        for n in names:
+            b, f, k = costs[n]
+            log("[breakdown] %-18s %9.2f us  %10.3f MB  %9.3f GFLOP  %s" % (n, avg[n] * 1e3, b / 1e6, f / 1e9, k))
+
+    # warmup, then the timed steps; events bracket the dominant call only
+    for i in range(args.warmup):
+        st.run(step=i)
+    dom = []
+
+    def mark_dom(name, where):
+        if name != dominant:
+            return
+        e = torch.cuda.Event(enable_timing=True)
+        e.record(stream)
+        if where == "start":
+            dom.append([e, None])
+        else:
+            dom[-1][1] = e
+
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        st.run(step=args.warmup + i, mark=mark_dom)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    status = int(st.status.item())
+    if status != 0:
+        log("[bench] device status flags %d" % status)
+    if args.copy_calibration_mib > 0:
+        nb = args.copy_calibration_mib << 20
+        a = torch.empty(nb // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+
+    ms = elapsed * 1e3 / args.steps
+    dom_ms = sum(a.elapsed_time(b) for a, b in dom) / len(dom)
+    nbytes, flops, kname = costs[dominant]
+    dt_s = dom_ms * 1e-3
+    hbm_s = nbytes / (HBM_PEAK_GBS * 1e9)
+    dtype = "bf16" if wl.dtype == W.BF16 else "f32"
+    mfma_dtype = "f32"   # the per-sample contractions run on fp32 MFMA for both input dtypes
+    mfma_s = flops / (PEAK_TFLOPS[mfma_dtype] * 1e12) if kname.endswith("gemm_kernel") or "conv" in kname else 0
+    if mfma_s > hbm_s:
+        roof = {"bound": "mfma", "achieved": round(flops / dt_s / 1e12, 3), "peak": PEAK_TFLOPS[mfma_dtype],
+                "unit": "TFLOP/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": round(nbytes / dt_s / 1e9, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s"}
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    roof["traffic"] = traffic_for(kname, wl.name, dominant)
+    roof.update({"kernel": kname, "call": dominant, "avg_us": round(dom_ms * 1e3, 2),
+                 "algorithmic_bytes": nbytes, "algorithmic_flops": flops})
+
+    line = {"metric": METRIC, "value": round(wl.N * args.steps / elapsed, 1), "unit": "samples/s",
+            "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": dtype,
+            "data": "synthetic",
+            "config": {"workload": wl.name, "batch": wl.N, "params": wl.n_params,
+                       "layers": [l.name for l in wl.layers], "C": wl.C, "sigma": wl.sigma},
+            "roofline": roof}
+    if not args.no_cpu_baseline:
+        log("[bench] timing the oracle on the host")
+        line["cpu_baseline"] = cpu_baseline(wl, inputs, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -61,10 +61,15 @@ def lib():
         L.dpo_clip_sum_embedding.argtypes = [_i64, _i64, _d, _d, _L, _L, _L, _d]
         L.dpo_philox4x32_10.argtypes = [_u32, _u32, _u32]
         L.dpo_philox_normals.argtypes = [_L, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint32, _u32, _d]
+        L.dpo_num_threads.restype = ctypes.c_int
         L.dpo_add_noise.argtypes = [_d, _L, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint32,
                                     ctypes.c_double, ctypes.c_double, ctypes.c_double, _d]
         _lib = L
     return _lib
+
+
+def num_threads() -> int:
+    return int(lib().dpo_num_threads())
 
 
 def _f64(a) -> np.ndarray:

@@ -21,9 +21,13 @@
  * summation order is fixed.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
+
+/* Number of OpenMP threads the parallel loops below use. */
+int dpo_num_threads(void) { return omp_get_max_threads(); }
 
 /* ---------------------------------------------------------------------------
  * Per-sample gradients

@@ -289,6 +289,31 @@ def test_clip_invariants():
     np.testing.assert_allclose(S, (G * oracle.clip_factors(norm, C)[:, None]).sum(0), rtol=1e-12)
 
 
+def test_clipped_sum_is_the_gradient_of_the_reweighted_loss():
+    """Weighting sample n's loss by its clip factor c_n and differentiating the
+    sum gives sum_n c_n g_n (the reweighting of the paper's related-work
+    section): an autograd route to the clipped sum that never forms g_n."""
+    wl = W.get("cifar_cnn")
+    inputs = W.make_inputs(wl, n=3)
+    res = oracle.dp_step(wl, inputs, C=0.02, sigma=0.0)
+    c = torch.from_numpy(res["c"])
+    assert float(c.max()) < 1.0          # every sample clipped at this C
+    for li in inputs[:2] + inputs[-1:]:
+        layer = li.layer
+        A = torch.from_numpy(li.A.astype(np.float64)); B = torch.from_numpy(li.B.astype(np.float64))
+        if isinstance(layer, W.Conv2d):
+            mod = torch.nn.Conv2d(layer.c_in, layer.c_out, layer.k, layer.stride, layer.pad).double()
+            w = c.view(-1, 1, 1, 1)
+        else:
+            mod = torch.nn.Linear(layer.d_in, layer.d_out).double()
+            w = c.view(-1, 1)
+        (w * B * mod(A)).sum().backward()
+        np.testing.assert_allclose(res["S"][layer.name + ".weight"], mod.weight.grad.numpy(), rtol=1e-10,
+                                   atol=1e-14)
+        np.testing.assert_allclose(res["S"][layer.name + ".bias"], mod.bias.grad.numpy(), rtol=1e-10,
+                                   atol=1e-14)
+
+
 def test_sigma0_Cinf_gives_the_non_private_mean_gradient():
     """sigma = 0 and C = inf reproduce the ordinary gradient of the mean loss."""
     wl = W.get("mnist_cnn")
