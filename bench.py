@@ -45,6 +45,7 @@ def call_costs(st):
     N = st.N
     e = 2 if st.wl.dtype == W.BF16 else 4
     out = {}
+    col_bytes = 0
     for lb in st.layers:
         L = lb.layer
         if isinstance(L, W.Linear):
@@ -60,15 +61,14 @@ def call_costs(st):
                 out["clip:" + L.name] = (N * L.T * (L.d_in + L.d_out) * e + (L.d_out * L.d_in + bias) * 4,
                                          2 * N * L.T * L.d_in * L.d_out, "clipsum_gemm_kernel")
             else:
-                out["clip:" + L.name] = (grads + (L.d_out * L.d_in + bias) * 4, 2 * N * L.n_params,
-                                         "colsum_kernel")
+                col_bytes += grads
         elif isinstance(L, W.Conv2d):
             ho, wo = L.out_hw
             kk = L.c_in * L.k[0] * L.k[1]
             grads = N * L.n_params * 4
             out["grad:" + L.name] = (N * (L.c_in * L.h * L.w + L.c_out * ho * wo) * e + grads + N * 4,
                                      2 * N * L.c_out * kk * ho * wo, "conv_per_sample_kernel")
-            out["clip:" + L.name] = (grads + L.n_params * 4, 2 * N * L.n_params, "colsum_kernel")
+            col_bytes += grads
         elif isinstance(L, W.Embedding):
             nnz_bound = N * L.T
             out["grad:" + L.name] = (N * L.T * (8 + L.D * e) + N * L.T * (L.D * 4 + 8), N * L.T * L.D,
@@ -78,9 +78,11 @@ def call_costs(st):
         elif isinstance(L, W.LayerNorm):
             out["grad:" + L.name] = (2 * N * L.T * L.D * e + 2 * N * L.D * 4, 3 * N * L.T * L.D,
                                      "ln_partial_kernel")
-            out["clip:" + L.name] = (2 * N * L.D * 4 + 2 * L.D * 4, 4 * N * L.D, "colsum_kernel")
+            col_bytes += 2 * N * L.D * 4
+    out["norms"] = (len(st.layers) * N * 4 + N * 4, len(st.layers) * N, "norms_kernel")
     P = st.wl.n_params
-    out["noise"] = (8 * P, 0, "add_noise_kernel")
+    # grouped clip + noise: read the column-reduced grads once, write S and out, read fused S
+    out["clip+noise"] = (col_bytes + 12 * P, 0, "colsum_many_kernel+finish_many_kernel")
     return out
 
 
@@ -102,6 +104,9 @@ KERNEL_SOURCES = {
     "emb_clipsum_kernel": ["paper_2109_12298_amd/csrc/clip.hip"],
     "ln_partial_kernel": ["paper_2109_12298_amd/csrc/layernorm.hip"],
     "add_noise_kernel": ["paper_2109_12298_amd/csrc/noise.hip"],
+    "colsum_many_kernel+finish_many_kernel": ["paper_2109_12298_amd/csrc/group.hip",
+                                              "paper_2109_12298_amd/csrc/philox.hpp"],
+    "norms_kernel": ["paper_2109_12298_amd/csrc/clip.hip"],
 }
 
 
@@ -163,6 +168,7 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--breakdown", action="store_true", help="print per-call event times to stderr")
+    ap.add_argument("--eager", action="store_true", help="time eager launches instead of graph replays")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run a plain device copy of this size (for counter calibration)")
     args = ap.parse_args()
@@ -185,7 +191,7 @@ def main():
     stream = torch.cuda.current_stream(dev)
     costs = call_costs(st)
 
-    # find the dominant call: event-time every call over a few steps
+    # find the dominant call: event-time every call over a few eager steps
     names = list(costs)
     ev = {n: [] for n in names}
 
@@ -206,12 +212,32 @@ def main():
     dominant = max(avg, key=avg.get)
     if args.breakdown:
         for n in names:
+            if n not in avg:
+                continue
             b, f, k = costs[n]
             log("[breakdown] %-18s %9.2f us  %10.3f MB  %9.3f GFLOP  %s" % (n, avg[n] * 1e3, b / 1e6, f / 1e9, k))
 
-    # warmup, then the timed steps; events bracket the dominant call only
+    # the timed region: K whole steps, replayed from one captured HIP graph
+    # (eager launches with --eager)
+    if not args.eager:
+        st.capture(first_step=0)
     for i in range(args.warmup):
-        st.run(step=i)
+        st.replay() if not args.eager else st.run(step=i)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        if args.eager:
+            st.run(step=args.warmup + i)
+        else:
+            st.replay()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    status = int(st.status.item())
+    if status != 0:
+        log("[bench] device status flags %d" % status)
+
+    # the dominant call's kernel time: HIP events on the step's stream around
+    # that call, over K eager steps
     dom = []
 
     def mark_dom(name, where):
@@ -225,14 +251,11 @@ def main():
             dom[-1][1] = e
 
     torch.cuda.synchronize()
-    t0 = time.perf_counter()
+    t1 = time.perf_counter()
     for i in range(args.steps):
-        st.run(step=args.warmup + i, mark=mark_dom)
+        st.run(step=i, mark=mark_dom)
     torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    status = int(st.status.item())
-    if status != 0:
-        log("[bench] device status flags %d" % status)
+    eager_ms = (time.perf_counter() - t1) * 1e3 / args.steps
     if args.copy_calibration_mib > 0:
         nb = args.copy_calibration_mib << 20
         a = torch.empty(nb // 4, dtype=torch.float32, device=dev).fill_(1.0)
@@ -249,6 +272,7 @@ def main():
     dtype = "bf16" if wl.dtype == W.BF16 else "f32"
     mfma_dtype = "f32"   # the per-sample contractions run on fp32 MFMA for both input dtypes
     mfma_s = flops / (PEAK_TFLOPS[mfma_dtype] * 1e12) if kname.endswith("gemm_kernel") or "conv" in kname else 0
+    # (noise and the column reduction are VALU/HBM work: compared against HBM)
     if mfma_s > hbm_s:
         roof = {"bound": "mfma", "achieved": round(flops / dt_s / 1e12, 3), "peak": PEAK_TFLOPS[mfma_dtype],
                 "unit": "TFLOP/s"}
@@ -261,6 +285,7 @@ def main():
 
     line = {"metric": METRIC, "value": round(wl.N * args.steps / elapsed, 1), "unit": "samples/s",
             "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+            "launch": "eager" if args.eager else "hip_graph", "eager_ms_per_step": round(eager_ms, 4),
             "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": dtype,
             "data": "synthetic",
             "config": {"workload": wl.name, "batch": wl.N, "params": wl.n_params,

@@ -111,8 +111,9 @@ dp_status dp_grad_sample_linear(const void *A, const void *B, dp_dtype dt, int64
  * gW fp32 [N][Cout][Cin][kh][kw]; gb fp32 [N][Cout] or NULL; sqnorm fp32 [N]
  * or NULL (overwritten with the layer's squared norm).
  * dh, dw != 1 or groups != 1 return DP_EUNSUPPORTED. */
-size_t dp_grad_sample_conv2d_workspace_bytes(int64_t N, int64_t Cin, int64_t Cout,
-                                             int64_t kh, int64_t kw);
+size_t dp_grad_sample_conv2d_workspace_bytes(int64_t N, int64_t Cin, int64_t H, int64_t W,
+                                             int64_t Cout, int64_t kh, int64_t kw, int64_t sh,
+                                             int64_t sw, int64_t ph, int64_t pw);
 dp_status dp_grad_sample_conv2d(const void *X, const void *GY, dp_dtype dt, int64_t N,
                                 int64_t Cin, int64_t H, int64_t W, int64_t Cout,
                                 int64_t Ho, int64_t Wo, int64_t kh, int64_t kw, int64_t sh,
@@ -210,6 +211,45 @@ dp_status dp_clip_accumulate_embedding(const int64_t *row_ptr, const int64_t *un
                                        const float *rows, const float *norm, float C,
                                        int64_t N, int64_t V, int64_t D, float *sum,
                                        int32_t *status, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * Grouped clipped sums and noise over many parameter tensors
+ * ------------------------------------------------------------------------- */
+
+/* One parameter tensor of dp_clip_noise_many. */
+typedef struct dp_param {
+    const float *grad_sample; /* fp32 [N][numel] per-sample gradients (used with DP_PARAM_REDUCE;
+                                 may be NULL when N = 0) */
+    float *sum;               /* fp32 [numel] clipped sum (summed_grad): written with
+                                 DP_PARAM_REDUCE, read otherwise (fused routes formed it) */
+    float *out;               /* fp32 [numel] noised average (grad), or NULL for no output */
+    int64_t numel;
+    uint32_t param_index;     /* index of the tensor's noise stream (see dp_add_noise) */
+    uint32_t flags;           /* DP_PARAM_REDUCE or 0; other bits must be 0 */
+} dp_param;
+
+enum { DP_PARAM_REDUCE = 1 };
+
+/* For every tensor of `params` (a host array of `count` entries, read during
+ * the call only): with DP_PARAM_REDUCE, sum = sum_n c_n * grad_sample[n]
+ * with c_n = min(1, C / (norm[n] + 1e-6)) as dp_clip_accumulate (n ascending;
+ * N = 0 gives zeros); then, if out is given, out = (sum + sigma*C*z) / denom
+ * with z the tensor's stream as in dp_add_noise at step
+ * step + (*step_dev if step_dev is not NULL, read on the device).  The device
+ * step lets one captured graph replay the call at an advancing step (see
+ * dp_step_advance).  This is the optimizer part of the step (clip, sum,
+ * noise, average) in two launches for all tensors, with the same results as
+ * dp_clip_accumulate followed by dp_add_noise.  Workspace from
+ * dp_clip_noise_many_workspace_bytes (same params, count and N). */
+size_t dp_clip_noise_many_workspace_bytes(const dp_param *params, int32_t count, int64_t N);
+dp_status dp_clip_noise_many(const dp_param *params, int32_t count, int64_t N, const float *norm,
+                             float C, uint64_t seed, uint64_t step, const uint64_t *step_dev,
+                             float sigma, float denom, int32_t *status, void *ws, size_t ws_bytes,
+                             hipStream_t stream);
+
+/* *step_dev += by, on the device (one tiny kernel): advances the step counter
+ * a captured graph reads through dp_clip_noise_many. */
+dp_status dp_step_advance(uint64_t *step_dev, uint64_t by, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
  * Noise and averaging (grad)

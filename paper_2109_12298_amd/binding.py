@@ -35,7 +35,7 @@ SIGNATURES = {
     "dp_abi_version": (ctypes.c_int, []),
     "dp_grad_sample_linear_workspace_bytes": (_SZ, [_I64, _I64, _I64, _I64, _ST]),
     "dp_grad_sample_linear": (_ST, [_P, _P, _ST, _I64, _I64, _I64, _I64, _F, _P, _P, _P, _P, _P, _SZ, _P]),
-    "dp_grad_sample_conv2d_workspace_bytes": (_SZ, [_I64, _I64, _I64, _I64, _I64]),
+    "dp_grad_sample_conv2d_workspace_bytes": (_SZ, [_I64] * 11),
     "dp_grad_sample_conv2d": (_ST, [_P, _P, _ST] + [_I64] * 16 + [_F, _P, _P, _P, _P, _P, _SZ, _P]),
     "dp_grad_sample_embedding_workspace_bytes": (_SZ, [_I64, _I64]),
     "dp_grad_sample_embedding": (_ST, [_P, _P, _ST, _I64, _I64, _I64, _I64, _F, _P, _P, _P, _I64, _P,
@@ -51,9 +51,37 @@ SIGNATURES = {
     "dp_clip_accumulate_linear": (_ST, [_P, _P, _ST, _I64, _I64, _I64, _I64, _F, _P, _F, _P, _P, _P, _P,
                                         _SZ, _P]),
     "dp_clip_accumulate_embedding": (_ST, [_P, _P, _P, _P, _F, _I64, _I64, _I64, _P, _P, _P]),
+    "dp_clip_noise_many_workspace_bytes": (_SZ, [_P, _I32, _I64]),
+    "dp_clip_noise_many": (_ST, [_P, _I32, _I64, _P, _F, _U64, _U64, _P, _F, _F, _P, _P, _SZ, _P]),
+    "dp_step_advance": (_ST, [_P, _U64, _P]),
     "dp_add_noise": (_ST, [_P, _P, _I64, _U64, _U64, _U32, _F, _F, _F, _P, _P]),
     "dp_philox_normals": (_ST, [_P, _P, _I64, _U64, _U64, _U32, _P]),
 }
+
+
+class DPParam(ctypes.Structure):
+    """struct dp_param of dpgrad.h."""
+    _fields_ = [("grad_sample", ctypes.c_void_p), ("sum", ctypes.c_void_p), ("out", ctypes.c_void_p),
+                ("numel", ctypes.c_int64), ("param_index", ctypes.c_uint32), ("flags", ctypes.c_uint32)]
+
+
+DP_PARAM_REDUCE = 1
+
+
+def make_params(entries):
+    """A dp_param array from (grad_sample, sum, out, numel, param_index) tuples.
+
+    grad_sample None means the sum is already formed (no DP_PARAM_REDUCE);
+    an empty tensor (N = 0) still asks for the reduction."""
+    arr = (DPParam * max(len(entries), 1))()
+    for i, (g, s, o, numel, pidx) in enumerate(entries):
+        arr[i].grad_sample = _ptr(g)
+        arr[i].sum = _ptr(s)
+        arr[i].out = _ptr(o)
+        arr[i].numel = int(numel)
+        arr[i].param_index = int(pidx)
+        arr[i].flags = DP_PARAM_REDUCE if g is not None else 0
+    return arr
 
 
 class DPError(RuntimeError):
@@ -145,8 +173,8 @@ def dp_grad_sample_linear(A, B, dt, N, T, d_in, d_out, scale, gW, gb=None, sqnor
            "dp_grad_sample_linear")
 
 
-def dp_grad_sample_conv2d_workspace_bytes(N, Cin, Cout, kh, kw) -> int:
-    return lib().dp_grad_sample_conv2d_workspace_bytes(N, Cin, Cout, kh, kw)
+def dp_grad_sample_conv2d_workspace_bytes(N, Cin, H, W, Cout, kh, kw, sh, sw, ph, pw) -> int:
+    return lib().dp_grad_sample_conv2d_workspace_bytes(N, Cin, H, W, Cout, kh, kw, sh, sw, ph, pw)
 
 
 def dp_grad_sample_conv2d(X, GY, dt, N, Cin, H, W, Cout, Ho, Wo, kh, kw, sh, sw, ph, pw, dh, dw, groups,
@@ -225,6 +253,26 @@ def dp_clip_accumulate_embedding(row_ptr, uniq_ids, rows, norm, C, N, V, D, sum,
     _check(lib().dp_clip_accumulate_embedding(_ptr(row_ptr), _ptr(uniq_ids), _ptr(rows), _ptr(norm), C, N, V,
                                               D, _ptr(sum), _ptr(status), _stream(stream)),
            "dp_clip_accumulate_embedding")
+
+
+# ---------------------------------------------------------------------------
+# grouped clip + noise
+# ---------------------------------------------------------------------------
+
+def dp_clip_noise_many_workspace_bytes(params, count, N) -> int:
+    return lib().dp_clip_noise_many_workspace_bytes(ctypes.cast(params, ctypes.c_void_p), count, N)
+
+
+def dp_clip_noise_many(params, count, N, norm, C, seed, step, step_dev, sigma, denom, status=None, ws=None,
+                       stream=None):
+    _check(lib().dp_clip_noise_many(ctypes.cast(params, ctypes.c_void_p), count, N, _ptr(norm), C, seed, step,
+                                    _ptr(step_dev), sigma, denom, _ptr(status), _ptr(ws), _nbytes(ws),
+                                    _stream(stream)),
+           "dp_clip_noise_many")
+
+
+def dp_step_advance(step_dev, by=1, stream=None):
+    _check(lib().dp_step_advance(_ptr(step_dev), by, _stream(stream)), "dp_step_advance")
 
 
 # ---------------------------------------------------------------------------

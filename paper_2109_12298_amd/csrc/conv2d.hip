@@ -2,10 +2,23 @@
 //
 // For sample n the weight gradient is the product of the output backprop
 // GY_n [Cout][L] (L = Ho*Wo positions) with the transposed unfold of the
-// input, U_n [L][Cin*kh*kw], whose column (ci, u, v) at position (oh, ow)
-// is X_n[ci][oh*sh+u-ph][ow*sw+v-pw] (zero in the padding).  The unfold is
-// never written to memory: each K-chunk of positions gathers its slice of
-// U_n straight into LDS.  M = Cout, N = Cin*kh*kw, K = L.
+// input, U_n [L][Cin*kh*kw], whose column kk = (ci, u, v) at position
+// p = (oh, ow) is X_n[ci][oh*sh+u-ph][ow*sw+v-pw] (zero in the padding).
+// The unfold is never formed, in HBM or in LDS.
+//
+// Fast path: a workgroup owns one (sample, kk-tile, co-tile).  It stages the
+// input planes its kk-tile touches once, with a zero halo, in LDS; every
+// unfold element is then one LDS read at (per-lane kk offset) + (per-position
+// offset from a small table).  The MFMA "rows" run over kk, which is the
+// contiguous index of the weight, so each lane ends holding four consecutive
+// gradient entries and stores them as one float4.  The four waves split the
+// output tile and/or the position (K) range; K-split partial tiles are added
+// in LDS in wave order.  A sample whose gradient fits in one tile gets its
+// squared norm written directly; otherwise tile partials go to the workspace
+// and a second kernel adds them in tile order.
+//
+// Fallback (input planes too large for LDS): the same contraction with the
+// unfold gathered through the cache into a K-major LDS tile per chunk.
 #include "common.hpp"
 #include "mfma_tile.hpp"
 
@@ -13,85 +26,306 @@ namespace dpg {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kBM = 64, kBN = 64, kBK = 32;
+constexpr int kLdsBudget = 60 * 1024;   // dynamic LDS per workgroup (static arrays come on top)
+constexpr int kStage = 8;               // global loads in flight per thread while staging
 
 struct ConvShape {
-    i64 Cin, H, W, Cout, Ho, Wo, kh, kw, sh, sw, ph, pw;
+    int Cin, H, W, Cout, Ho, Wo, kh, kw, sh, sw, ph, pw;
+    int L, KK, khw;
 };
 
-template <typename T>
+// ---------------------------------------------------------------------------
+// fast path
+// ---------------------------------------------------------------------------
+template <int FM, int FN, int WM, int WN, int WK>
+struct ConvTile {
+    static_assert(WM * WN * WK == 4, "four waves");
+    static constexpr int BM = WM * FM * 32;   // kk
+    static constexpr int BN = WN * FN * 32;   // co
+    static constexpr int LDG = BN + 1;        // padded row of the staged backprop chunk
+    static constexpr int RED = (WK - 1) * WM * WN * FM * FN * 16 * 64;  // floats for the K-split sum
+};
+
+struct ConvGeom {
+    int Hp, Wp, plane;   // padded input plane
+    int nplanes;         // planes staged per workgroup (upper bound)
+    int tiles_m, tiles_n, tiles;
+    int vec;             // float4 stores allowed (KK % 4 == 0 and gW 16-byte aligned)
+    int bk;              // positions per staged chunk (multiple of 8)
+};
+
+template <typename T, int FM, int FN, int WM, int WN, int WK>
 __global__ __launch_bounds__(kThreads) void conv_per_sample_kernel(
-    const T *__restrict__ X, const T *__restrict__ GY, ConvShape s, int tiles_n, int tiles,
-    float scale, float *__restrict__ gW, float *__restrict__ gb, float *__restrict__ partial)
+    const T *__restrict__ X, const T *__restrict__ GY, ConvShape s, ConvGeom g, float scale,
+    float *__restrict__ gW, float *__restrict__ gb, float *__restrict__ sqout, int direct)
 {
-    __shared__ float As[kBK * kBM];
-    __shared__ float Bs[kBK * kBN];
-    __shared__ float red[16];
-    const i64 n = blockIdx.x / tiles;
-    const int tile = blockIdx.x % tiles;
-    const int tm = tile / tiles_n, tn = tile % tiles_n;
-    const i64 m0 = (i64)tm * kBM, n0 = (i64)tn * kBN;
+    using Cfg = ConvTile<FM, FN, WM, WN, WK>;
+    extern __shared__ float lds[];
+    __shared__ float red16[16];
+
+    const int n = blockIdx.x / g.tiles;
+    const int tile = blockIdx.x % g.tiles;
+    const int tm = tile / g.tiles_n, tn = tile % g.tiles_n;
+    const int m0 = tm * Cfg::BM;   // first kk
+    const int n0 = tn * Cfg::BN;   // first co
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = (wave >> 1) * (kBM / 2), wn = (wave & 1) * (kBN / 2);
-    const i64 L = s.Ho * s.Wo;
-    const i64 KK = s.Cin * s.kh * s.kw;
-    const i64 khw = s.kh * s.kw;
-    const T *Xn = X + n * s.Cin * s.H * s.W;
-    const T *Gn = GY + n * s.Cout * L;
-    const bool do_bias = gb != nullptr && tn == 0;
+    const int wk = wave % WK;
+    const int wmn = wave / WK;
+    const int wm = wmn % WM, wn = wmn / WM;
 
-    MfmaTile<kBM, kBN> t;
-    t.zero();
-    float bias_acc = 0.0f;
+    const int BK = g.bk;
+    float *Xs = lds;
+    float *Gs = lds + g.nplanes * g.plane;
+    int *offp = reinterpret_cast<int *>(Gs + BK * Cfg::LDG);
 
-    for (i64 k0 = 0; k0 < L; k0 += kBK) {
-        // A operand: As[kk][ii] = GY_n[m0+ii][k0+kk] (consecutive threads walk positions)
-        for (int e = tid; e < kBK * kBM; e += kThreads) {
-            const int ii = e / kBK, kk = e % kBK;
-            const i64 p = k0 + kk, co = m0 + ii;
-            As[kk * kBM + ii] = (p < L && co < s.Cout) ? load_elem<T>(Gn, co * L + p) : 0.0f;
-        }
-        // B operand: Bs[kk][jj] = U_n[k0+kk][n0+jj], gathered from the input
-        for (int e = tid; e < kBK * kBN; e += kThreads) {
-            const int jj = e / kBK, kk = e % kBK;
-            const i64 p = k0 + kk, j = n0 + jj;
-            float v = 0.0f;
-            if (p < L && j < KK) {
-                const i64 ci = j / khw, rem = j % khw;
-                const i64 u = rem / s.kw, vv = rem % s.kw;
-                const i64 oh = p / s.Wo, ow = p % s.Wo;
-                const i64 ih = oh * s.sh + u - s.ph, iw = ow * s.sw + vv - s.pw;
+    // ---- stage the input planes this kk-tile reads, zero halo included
+    const int ci0 = m0 / s.khw;
+    int ci1 = (m0 + Cfg::BM - 1) / s.khw + 1;
+    if (ci1 > s.Cin) ci1 = s.Cin;
+    const int np = ci1 - ci0;
+    const T *Xn = X + (i64)n * s.Cin * s.H * s.W;
+    // kStage loads in flight per thread before any is written to LDS
+    const int xtotal = np * g.plane;
+    for (int i0 = tid; i0 < xtotal; i0 += kThreads * kStage) {
+        float v[kStage];
+#pragma unroll
+        for (int j = 0; j < kStage; ++j) {
+            const int idx = i0 + j * kThreads;
+            v[j] = 0.0f;
+            if (idx < xtotal) {
+                const int c = idx / g.plane;
+                const int rem = idx - c * g.plane;
+                const int r = rem / g.Wp;
+                const int q = rem - r * g.Wp;
+                const int ih = r - s.ph, iw = q - s.pw;
                 if (ih >= 0 && ih < s.H && iw >= 0 && iw < s.W)
-                    v = load_elem<T>(Xn, (ci * s.H + ih) * s.W + iw);
+                    v[j] = load_elem<T>(Xn, ((i64)(ci0 + c) * s.H + ih) * s.W + iw);
             }
-            Bs[kk * kBN + jj] = v;
+        }
+#pragma unroll
+        for (int j = 0; j < kStage; ++j) {
+            const int idx = i0 + j * kThreads;
+            if (idx < xtotal) Xs[idx] = v[j];
+        }
+    }
+
+    // ---- per-lane unfold column offsets
+    int offkk[FM];
+    bool vkk[FM];
+#pragma unroll
+    for (int x = 0; x < FM; ++x) {
+        const int kk = m0 + wm * FM * 32 + x * 32 + (lane & 31);
+        vkk[x] = kk < s.KK;
+        const int k2 = vkk[x] ? kk : 0;
+        const int ci = k2 / s.khw;
+        const int rem = k2 - ci * s.khw;
+        const int u = rem / s.kw;
+        const int v = rem - u * s.kw;
+        offkk[x] = vkk[x] ? (ci - ci0) * g.plane + u * g.Wp + v : 0;
+    }
+
+    f32x16 acc[FM][FN];
+#pragma unroll
+    for (int x = 0; x < FM; ++x)
+#pragma unroll
+        for (int y = 0; y < FN; ++y)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[x][y][r] = 0.0f;
+
+    const bool do_bias = gb != nullptr && tm == 0;
+    float bias_acc = 0.0f;
+    const T *Gn = GY + (i64)n * s.Cout * s.L;
+
+    for (int p0 = 0; p0 < s.L; p0 += BK) {
+        __syncthreads();   // previous chunk fully consumed (and Xs staged, first time)
+        const int gtotal = Cfg::BN * BK;
+        for (int e0 = tid; e0 < gtotal; e0 += kThreads * kStage) {
+            float v[kStage];
+            int at[kStage];
+#pragma unroll
+            for (int j = 0; j < kStage; ++j) {
+                const int e = e0 + j * kThreads;
+                const int co = e / BK, p = e - co * BK;
+                at[j] = e < gtotal ? p * Cfg::LDG + co : -1;
+                v[j] = 0.0f;
+                if (e < gtotal && n0 + co < s.Cout && p0 + p < s.L)
+                    v[j] = load_elem<T>(Gn, (i64)(n0 + co) * s.L + p0 + p);
+            }
+#pragma unroll
+            for (int j = 0; j < kStage; ++j)
+                if (at[j] >= 0) Gs[at[j]] = v[j];
+        }
+        for (int t = tid; t < BK; t += kThreads) {
+            const int p = p0 + t;
+            int o = 0;
+            if (p < s.L) {
+                const int oh = p / s.Wo, ow = p - oh * s.Wo;
+                o = oh * s.sh * g.Wp + ow * s.sw;
+            }
+            offp[t] = o;
         }
         __syncthreads();
-        t.template mma<kBK>(As, kBM, Bs, kBN, wm, wn, lane);
-        if (do_bias && tid < kBM) {
-#pragma unroll 8
-            for (int kk = 0; kk < kBK; ++kk) bias_acc += As[kk * kBM + tid];
+        const int kpairs = (s.L - p0 < BK ? s.L - p0 + 1 : BK) >> 1;
+        for (int q = wk; q < kpairs; q += WK) {
+            const int ks = 2 * q + (lane >> 5);
+            const int op = offp[ks];
+            float a[FM], b[FN];
+#pragma unroll
+            for (int x = 0; x < FM; ++x) a[x] = vkk[x] ? Xs[offkk[x] + op] : 0.0f;
+#pragma unroll
+            for (int y = 0; y < FN; ++y) b[y] = Gs[ks * Cfg::LDG + wn * FN * 32 + y * 32 + (lane & 31)];
+#pragma unroll
+            for (int x = 0; x < FM; ++x)
+#pragma unroll
+                for (int y = 0; y < FN; ++y)
+                    acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[x], b[y], acc[x][y], 0, 0, 0);
+        }
+        if (do_bias && tid < Cfg::BN) {
+            for (int p = 0; p < 2 * kpairs; ++p) bias_acc += Gs[p * Cfg::LDG + tid];
+        }
+    }
+
+    // ---- add the K-split partial tiles (wave order), reusing the staging LDS
+    if (WK > 1) {
+        __syncthreads();
+        float *R = lds;
+        if (wk > 0) {
+            float *dst = R + (((wk - 1) * WM * WN + wmn) * FM * FN) * 16 * 64;
+#pragma unroll
+            for (int x = 0; x < FM; ++x)
+#pragma unroll
+                for (int y = 0; y < FN; ++y)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) dst[((x * FN + y) * 16 + r) * 64 + lane] = acc[x][y][r];
         }
         __syncthreads();
+        if (wk == 0) {
+            for (int w = 1; w < WK; ++w) {
+                const float *src = R + (((w - 1) * WM * WN + wmn) * FM * FN) * 16 * 64;
+#pragma unroll
+                for (int x = 0; x < FM; ++x)
+#pragma unroll
+                    for (int y = 0; y < FN; ++y)
+#pragma unroll
+                        for (int r = 0; r < 16; ++r) acc[x][y][r] += src[((x * FN + y) * 16 + r) * 64 + lane];
+            }
+        }
     }
 
     float sq = 0.0f;
-    float *G = gW + n * s.Cout * KK;
+    if (wk == 0) {
+        const bool vec = g.vec != 0;
+        float *G = gW + (i64)n * s.Cout * s.KK;
+#pragma unroll
+        for (int x = 0; x < FM; ++x)
+#pragma unroll
+            for (int y = 0; y < FN; ++y) {
+                const int co = n0 + wn * FN * 32 + y * 32 + (lane & 31);
+                if (co >= s.Cout) continue;
+#pragma unroll
+                for (int rb = 0; rb < 4; ++rb) {
+                    const int kk = m0 + wm * FM * 32 + x * 32 + 8 * rb + 4 * (lane >> 5);
+                    const float g0 = scale * acc[x][y][4 * rb + 0], g1 = scale * acc[x][y][4 * rb + 1];
+                    const float g2 = scale * acc[x][y][4 * rb + 2], g3 = scale * acc[x][y][4 * rb + 3];
+                    float *dst = G + (i64)co * s.KK + kk;
+                    if (vec && kk + 3 < s.KK) {
+                        *reinterpret_cast<float4 *>(dst) = make_float4(g0, g1, g2, g3);
+                        sq += g0 * g0 + g1 * g1 + g2 * g2 + g3 * g3;
+                    } else {
+                        if (kk + 0 < s.KK) { dst[0] = g0; sq += g0 * g0; }
+                        if (kk + 1 < s.KK) { dst[1] = g1; sq += g1 * g1; }
+                        if (kk + 2 < s.KK) { dst[2] = g2; sq += g2 * g2; }
+                        if (kk + 3 < s.KK) { dst[3] = g3; sq += g3 * g3; }
+                    }
+                }
+            }
+    }
+    if (do_bias && tid < Cfg::BN && n0 + tid < s.Cout) {
+        const float v = scale * bias_acc;
+        gb[(i64)n * s.Cout + n0 + tid] = v;
+        sq += v * v;
+    }
+    sq = block_sum(sq, red16);
+    if (sqout && tid == 0) {
+        if (direct) sqout[n] = sq;
+        else sqout[(i64)n * g.tiles + tile] = sq;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// fallback: unfold gathered per chunk through the cache
+// ---------------------------------------------------------------------------
+constexpr int kGM = 64, kGN = 64, kGK = 32;
+
+template <typename T>
+__global__ __launch_bounds__(kThreads) void conv_generic_kernel(
+    const T *__restrict__ X, const T *__restrict__ GY, ConvShape s, int tiles_n, int tiles,
+    float scale, float *__restrict__ gW, float *__restrict__ gb, float *__restrict__ sqout,
+    int direct)
+{
+    __shared__ float As[kGK * kGM];   // [p][co]
+    __shared__ float Bs[kGK * kGN];   // [p][kk]
+    __shared__ float red[16];
+    const int n = blockIdx.x / tiles;
+    const int tile = blockIdx.x % tiles;
+    const int tm = tile / tiles_n, tn = tile % tiles_n;
+    const int m0 = tm * kGM, n0 = tn * kGN;    // m: co, n: kk
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = (wave >> 1) * (kGM / 2), wn = (wave & 1) * (kGN / 2);
+    const T *Xn = X + (i64)n * s.Cin * s.H * s.W;
+    const T *Gn = GY + (i64)n * s.Cout * s.L;
+    const bool do_bias = gb != nullptr && tn == 0;
+
+    MfmaTile<kGM, kGN> t;
+    t.zero();
+    float bias_acc = 0.0f;
+    for (int k0 = 0; k0 < s.L; k0 += kGK) {
+        for (int e = tid; e < kGK * kGM; e += kThreads) {
+            const int ii = e / kGK, kk = e % kGK;
+            const int p = k0 + kk, co = m0 + ii;
+            As[kk * kGM + ii] = (p < s.L && co < s.Cout) ? load_elem<T>(Gn, (i64)co * s.L + p) : 0.0f;
+        }
+        for (int e = tid; e < kGK * kGN; e += kThreads) {
+            const int jj = e / kGK, kk = e % kGK;
+            const int p = k0 + kk, j = n0 + jj;
+            float v = 0.0f;
+            if (p < s.L && j < s.KK) {
+                const int ci = j / s.khw, rem = j - ci * s.khw;
+                const int u = rem / s.kw, vv = rem - u * s.kw;
+                const int oh = p / s.Wo, ow = p - oh * s.Wo;
+                const int ih = oh * s.sh + u - s.ph, iw = ow * s.sw + vv - s.pw;
+                if (ih >= 0 && ih < s.H && iw >= 0 && iw < s.W)
+                    v = load_elem<T>(Xn, ((i64)ci * s.H + ih) * s.W + iw);
+            }
+            Bs[kk * kGN + jj] = v;
+        }
+        __syncthreads();
+        t.template mma<kGK>(As, kGM, Bs, kGN, wm, wn, lane);
+        if (do_bias && tid < kGM) {
+            for (int kk = 0; kk < kGK; ++kk) bias_acc += As[kk * kGM + tid];
+        }
+        __syncthreads();
+    }
+    float sq = 0.0f;
+    float *G = gW + (i64)n * s.Cout * s.KK;
     t.for_each(wm, wn, lane, [&](int r, int c, float v) {
-        const i64 i = m0 + r, j = n0 + c;
-        if (i < s.Cout && j < KK) {
-            const float g = scale * v;
-            G[i * KK + j] = g;
-            sq += g * g;
+        const int co = m0 + r, kk = n0 + c;
+        if (co < s.Cout && kk < s.KK) {
+            const float gv = scale * v;
+            G[(i64)co * s.KK + kk] = gv;
+            sq += gv * gv;
         }
     });
-    if (do_bias && tid < kBM && m0 + tid < s.Cout) {
-        const float g = scale * bias_acc;
-        gb[n * s.Cout + m0 + tid] = g;
-        sq += g * g;
+    if (do_bias && tid < kGM && m0 + tid < s.Cout) {
+        const float v = scale * bias_acc;
+        gb[(i64)n * s.Cout + m0 + tid] = v;
+        sq += v * v;
     }
     sq = block_sum(sq, red);
-    if (partial && tid == 0) partial[n * tiles + tile] = sq;
+    if (sqout && tid == 0) {
+        if (direct) sqout[n] = sq;
+        else sqout[(i64)n * tiles + tile] = sq;
+    }
 }
 
 __global__ void conv_reduce_partials_kernel(const float *__restrict__ partial, i64 N, int tiles,
@@ -104,10 +338,133 @@ __global__ void conv_reduce_partials_kernel(const float *__restrict__ partial, i
     sqnorm[n] = s;
 }
 
-int conv_tiles(i64 Cin, i64 Cout, i64 kh, i64 kw, int *tiles_n)
+// ---------------------------------------------------------------------------
+// host: pick a tile configuration
+// ---------------------------------------------------------------------------
+struct Plan {
+    int cfg;                 // index into kConfigs, or -1 for the fallback
+    ConvGeom g;
+    size_t lds;
+};
+
+struct CfgDesc {
+    int FM, FN, WM, WN, WK;
+};
+
+constexpr CfgDesc kConfigs[] = {
+    {1, 1, 1, 1, 4},   // 32 x 32
+    {2, 1, 1, 1, 4},   // 64 x 32
+    {1, 2, 1, 1, 4},   // 32 x 64
+    {2, 2, 1, 1, 4},   // 64 x 64
+    {2, 1, 2, 1, 2},   // 128 x 32
+    {2, 1, 4, 1, 1},   // 256 x 32
+    {2, 2, 2, 1, 2},   // 128 x 64
+    {2, 2, 2, 2, 1},   // 128 x 128
+    {2, 2, 1, 2, 2},   // 64 x 128
+};
+constexpr int kNumConfigs = sizeof(kConfigs) / sizeof(kConfigs[0]);
+
+ConvGeom geom_for(const CfgDesc &c, const ConvShape &s)
 {
-    *tiles_n = (int)ceil_div(Cin * kh * kw, kBN);
-    return (int)ceil_div(Cout, kBM) * *tiles_n;
+    ConvGeom g;
+    g.Hp = s.H + 2 * s.ph;
+    g.Wp = s.W + 2 * s.pw;
+    g.plane = g.Hp * g.Wp;
+    const int BM = c.WM * c.FM * 32, BN = c.WN * c.FN * 32;
+    int np = (BM - 1) / s.khw + 2;
+    if (np > s.Cin) np = s.Cin;
+    g.nplanes = np;
+    g.tiles_m = (s.KK + BM - 1) / BM;
+    g.tiles_n = (s.Cout + BN - 1) / BN;
+    g.tiles = g.tiles_m * g.tiles_n;
+    g.vec = 0;
+    return g;
+}
+
+// Positions per staged chunk: the whole sample when it fits (one load round
+// trip), else as many as the LDS budget allows; a multiple of 8, at least 64.
+int chunk_for(const CfgDesc &c, const ConvGeom &g, const ConvShape &s)
+{
+    const int BN = c.WN * c.FN * 32;
+    const long avail = (long)kLdsBudget / 4 - (long)g.nplanes * g.plane;
+    long bk = avail / (BN + 2);
+    bk &= ~7L;
+    const int need = (s.L + 7) & ~7;
+    if (bk > need) bk = need;
+    if (bk < 64) bk = need < 64 ? need : 64;
+    return (int)bk;
+}
+
+size_t lds_for(const CfgDesc &c, const ConvGeom &g)
+{
+    const int BN = c.WN * c.FN * 32;
+    const size_t stage = (size_t)g.nplanes * g.plane + (size_t)g.bk * (BN + 2);
+    const size_t redf = (size_t)(c.WK - 1) * c.WM * c.WN * c.FM * c.FN * 16 * 64;
+    return (stage > redf ? stage : redf) * sizeof(float);
+}
+
+Plan plan_conv(const ConvShape &s)
+{
+    Plan best;
+    best.cfg = -1;
+    double best_cost = 0;
+    for (int i = 0; i < kNumConfigs; ++i) {
+        const CfgDesc &c = kConfigs[i];
+        ConvGeom g = geom_for(c, s);
+        g.bk = chunk_for(c, g, s);
+        const size_t lds = lds_for(c, g);
+        if (lds > (size_t)kLdsBudget) continue;
+        const int BM = c.WM * c.FM * 32, BN = c.WN * c.FN * 32;
+        // padded MFMA area, plus the re-staging of input planes per tile
+        const double area = (double)g.tiles_m * BM * g.tiles_n * BN;
+        const double stage = (double)g.tiles * g.nplanes * g.plane / 8.0;
+        const double cost = area + stage + (g.tiles > 1 ? 2048.0 : 0.0);
+        if (best.cfg < 0 || cost < best_cost) {
+            best.cfg = i;
+            best.g = g;
+            best.lds = lds;
+            best_cost = cost;
+        }
+    }
+    return best;
+}
+
+template <typename T, int FM, int FN, int WM, int WN, int WK>
+void launch_fast(const void *X, const void *GY, const ConvShape &s, const Plan &p, i64 N, float scale,
+                 float *gW, float *gb, float *sqout, int direct, hipStream_t stream)
+{
+    conv_per_sample_kernel<T, FM, FN, WM, WN, WK><<<(unsigned)(N * p.g.tiles), kThreads, p.lds, stream>>>(
+        (const T *)X, (const T *)GY, s, p.g, scale, gW, gb, sqout, direct);
+}
+
+template <typename T>
+void dispatch_fast(const void *X, const void *GY, const ConvShape &s, const Plan &p, i64 N, float scale,
+                   float *gW, float *gb, float *sqout, int direct, hipStream_t stream)
+{
+    switch (p.cfg) {
+    case 0: launch_fast<T, 1, 1, 1, 1, 4>(X, GY, s, p, N, scale, gW, gb, sqout, direct, stream); break;
+    case 1: launch_fast<T, 2, 1, 1, 1, 4>(X, GY, s, p, N, scale, gW, gb, sqout, direct, stream); break;
+    case 2: launch_fast<T, 1, 2, 1, 1, 4>(X, GY, s, p, N, scale, gW, gb, sqout, direct, stream); break;
+    case 3: launch_fast<T, 2, 2, 1, 1, 4>(X, GY, s, p, N, scale, gW, gb, sqout, direct, stream); break;
+    case 4: launch_fast<T, 2, 1, 2, 1, 2>(X, GY, s, p, N, scale, gW, gb, sqout, direct, stream); break;
+    case 5: launch_fast<T, 2, 1, 4, 1, 1>(X, GY, s, p, N, scale, gW, gb, sqout, direct, stream); break;
+    case 6: launch_fast<T, 2, 2, 2, 1, 2>(X, GY, s, p, N, scale, gW, gb, sqout, direct, stream); break;
+    case 7: launch_fast<T, 2, 2, 2, 2, 1>(X, GY, s, p, N, scale, gW, gb, sqout, direct, stream); break;
+    default: launch_fast<T, 2, 2, 1, 2, 2>(X, GY, s, p, N, scale, gW, gb, sqout, direct, stream); break;
+    }
+}
+
+int conv_tiles(const ConvShape &s)
+{
+    const Plan p = plan_conv(s);
+    if (p.cfg >= 0) return p.g.tiles;
+    return ((s.KK + kGN - 1) / kGN) * ((s.Cout + kGM - 1) / kGM);
+}
+
+bool fits_int32(i64 Cin, i64 H, i64 W, i64 Cout, i64 kh, i64 kw)
+{
+    const i64 lim = i64(1) << 30;
+    return Cin * H * W < lim && Cout * H * W < lim && Cin * kh * kw < lim && (H + 2 * kh) * (W + 2 * kw) < lim;
 }
 
 }  // namespace
@@ -115,13 +472,36 @@ int conv_tiles(i64 Cin, i64 Cout, i64 kh, i64 kw, int *tiles_n)
 
 using namespace dpg;
 
-extern "C" size_t dp_grad_sample_conv2d_workspace_bytes(int64_t N, int64_t Cin, int64_t Cout,
-                                                        int64_t kh, int64_t kw)
+static ConvShape make_shape(int64_t Cin, int64_t H, int64_t W, int64_t Cout, int64_t kh, int64_t kw,
+                            int64_t sh, int64_t sw, int64_t ph, int64_t pw)
 {
-    if (N <= 0 || Cin <= 0 || Cout <= 0 || kh <= 0 || kw <= 0) return 0;
-    int tn;
-    const int tiles = conv_tiles(Cin, Cout, kh, kw, &tn);
-    return (size_t)(N * tiles) * sizeof(float);
+    ConvShape s;
+    s.Cin = (int)Cin; s.H = (int)H; s.W = (int)W; s.Cout = (int)Cout; s.kh = (int)kh; s.kw = (int)kw;
+    s.sh = (int)sh; s.sw = (int)sw; s.ph = (int)ph; s.pw = (int)pw;
+    s.Ho = (int)((H + 2 * ph - kh) / sh + 1);
+    s.Wo = (int)((W + 2 * pw - kw) / sw + 1);
+    s.L = s.Ho * s.Wo;
+    s.khw = s.kh * s.kw;
+    s.KK = s.Cin * s.khw;
+    return s;
+}
+
+static bool shape_ok(int64_t Cin, int64_t H, int64_t W, int64_t Cout, int64_t kh, int64_t kw, int64_t sh,
+                     int64_t sw, int64_t ph, int64_t pw)
+{
+    return Cin >= 1 && H >= 1 && W >= 1 && Cout >= 1 && kh >= 1 && kw >= 1 && sh >= 1 && sw >= 1 &&
+           ph >= 0 && pw >= 0 && H + 2 * ph >= kh && W + 2 * pw >= kw;
+}
+
+extern "C" size_t dp_grad_sample_conv2d_workspace_bytes(int64_t N, int64_t Cin, int64_t H, int64_t W,
+                                                        int64_t Cout, int64_t kh, int64_t kw, int64_t sh,
+                                                        int64_t sw, int64_t ph, int64_t pw)
+{
+    if (N <= 0 || !shape_ok(Cin, H, W, Cout, kh, kw, sh, sw, ph, pw)) return 0;
+    if (!fits_int32(Cin, H + 2 * ph, W + 2 * pw, Cout, kh, kw)) return 0;
+    const ConvShape s = make_shape(Cin, H, W, Cout, kh, kw, sh, sw, ph, pw);
+    const int tiles = conv_tiles(s);
+    return tiles > 1 ? (size_t)(N * tiles) * sizeof(float) : 0;
 }
 
 extern "C" dp_status dp_grad_sample_conv2d(const void *X, const void *GY, dp_dtype dt, int64_t N,
@@ -140,24 +520,35 @@ extern "C" dp_status dp_grad_sample_conv2d(const void *X, const void *GY, dp_dty
     DPG_REQUIRE(groups == 1 && dh == 1 && dw == 1, DP_EUNSUPPORTED);
     DPG_REQUIRE(H + 2 * ph >= kh && W + 2 * pw >= kw, DP_EINVAL);
     DPG_REQUIRE(Ho == (H + 2 * ph - kh) / sh + 1 && Wo == (W + 2 * pw - kw) / sw + 1, DP_EINVAL);
+    DPG_REQUIRE(fits_int32(Cin, H + 2 * ph, W + 2 * pw, Cout, kh, kw), DP_EUNSUPPORTED);
     DPG_REQUIRE(N == 0 || (X != nullptr && GY != nullptr && gW != nullptr), DP_EINVAL);
-    const size_t need = dp_grad_sample_conv2d_workspace_bytes(N, Cin, Cout, kh, kw);
+    const size_t need = dp_grad_sample_conv2d_workspace_bytes(N, Cin, H, W, Cout, kh, kw, sh, sw, ph, pw);
     DPG_REQUIRE(ws_bytes >= need && (need == 0 || ws != nullptr), DP_EINVAL);
     if (N == 0) return DP_OK;
 
-    ConvShape s{Cin, H, W, Cout, Ho, Wo, kh, kw, sh, sw, ph, pw};
-    int tiles_n;
-    const int tiles = conv_tiles(Cin, Cout, kh, kw, &tiles_n);
-    float *partial = sqnorm ? (float *)ws : nullptr;
-    const dim3 grid((unsigned)(N * tiles));
-    if (dt == DP_F32)
-        conv_per_sample_kernel<float><<<grid, kThreads, 0, stream>>>(
-            (const float *)X, (const float *)GY, s, tiles_n, tiles, scale, gW, gb, partial);
-    else
-        conv_per_sample_kernel<uint16_t><<<grid, kThreads, 0, stream>>>(
-            (const uint16_t *)X, (const uint16_t *)GY, s, tiles_n, tiles, scale, gW, gb, partial);
-    if (sqnorm)
-        conv_reduce_partials_kernel<<<(unsigned)ceil_div(N, 256), 256, 0, stream>>>(partial, N, tiles,
+    const ConvShape s = make_shape(Cin, H, W, Cout, kh, kw, sh, sw, ph, pw);
+    Plan p = plan_conv(s);
+    p.g.vec = (s.KK % 4 == 0) && aligned(gW, 16);
+    const int tiles = p.cfg >= 0 ? p.g.tiles : conv_tiles(s);
+    const int direct = tiles == 1;
+    float *sqout = sqnorm ? (direct ? sqnorm : (float *)ws) : nullptr;
+    const bool bf = dt == DP_BF16;
+    if (p.cfg >= 0) {
+        if (bf) dispatch_fast<uint16_t>(X, GY, s, p, N, scale, gW, gb, sqout, direct, stream);
+        else dispatch_fast<float>(X, GY, s, p, N, scale, gW, gb, sqout, direct, stream);
+    } else {
+        const int tiles_n = (s.KK + kGN - 1) / kGN;
+        const dim3 grid((unsigned)(N * tiles));
+        if (bf)
+            conv_generic_kernel<uint16_t><<<grid, kThreads, 0, stream>>>((const uint16_t *)X, (const uint16_t *)GY,
+                                                                       s, tiles_n, tiles, scale, gW, gb, sqout,
+                                                                       direct);
+        else
+            conv_generic_kernel<float><<<grid, kThreads, 0, stream>>>((const float *)X, (const float *)GY, s,
+                                                                    tiles_n, tiles, scale, gW, gb, sqout, direct);
+    }
+    if (sqnorm && !direct)
+        conv_reduce_partials_kernel<<<(unsigned)ceil_div(N, 256), 256, 0, stream>>>((float *)ws, N, tiles,
                                                                                    sqnorm);
     return launch_status();
 }

@@ -20,6 +20,7 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kBM = 64, kBN = 64, kBK = 32;
+constexpr int kOuterMaxRows = 1024;   // gW rows per outer-product workgroup
 
 template <typename T>
 __device__ __forceinline__ float4 load4(const T *p, i64 i);
@@ -54,16 +55,20 @@ __global__ __launch_bounds__(kThreads) void outer_kernel(const T *__restrict__ A
     const int rb = blockIdx.x % bps;
     const i64 i0 = (i64)rb * rows;
     const i64 i1 = i0 + rows < dout ? i0 + rows : dout;
+    __shared__ float bsh[kOuterMaxRows];
     const T *An = A + n * din;
     const T *Bn = B + n * dout;
     float *G = gW + n * dout * din;
+    // the block's backprop entries, scaled, in LDS (one load round trip)
+    for (i64 i = i0 + threadIdx.x; i < i1; i += kThreads) bsh[i - i0] = scale * load_elem<T>(Bn, i);
+    __syncthreads();
 
     if (VEC) {
         const i64 nv = din / 4;
         for (i64 j4 = threadIdx.x; j4 < nv; j4 += kThreads) {
             const float4 a = load4<T>(An, 4 * j4);
             for (i64 i = i0; i < i1; ++i) {
-                const float b = scale * load_elem<T>(Bn, i);
+                const float b = bsh[i - i0];
                 float4 v = make_float4(b * a.x, b * a.y, b * a.z, b * a.w);
                 *reinterpret_cast<float4 *>(G + i * din + 4 * j4) = v;
             }
@@ -71,7 +76,7 @@ __global__ __launch_bounds__(kThreads) void outer_kernel(const T *__restrict__ A
     } else {
         for (i64 j = threadIdx.x; j < din; j += kThreads) {
             const float a = load_elem<T>(An, j);
-            for (i64 i = i0; i < i1; ++i) G[i * din + j] = scale * load_elem<T>(Bn, i) * a;
+            for (i64 i = i0; i < i1; ++i) G[i * din + j] = bsh[i - i0] * a;
         }
     }
     if (gb) {
@@ -308,6 +313,7 @@ extern "C" dp_status dp_grad_sample_linear(const void *A, const void *B, dp_dtyp
     if (T == 1) {
         int rows = (int)(8192 / d_in);
         if (rows < 1) rows = 1;
+        if (rows > kOuterMaxRows) rows = kOuterMaxRows;
         if (rows > d_out) rows = (int)d_out;
         const int bps = (int)ceil_div(d_out, rows);
         const dim3 grid((unsigned)(N * bps));

@@ -5,12 +5,18 @@ layer from its stored activations and backprops, per-sample l2 norms over all
 parameters, clip factors, the clipped sum over the batch, Gaussian noise,
 division by the batch size.  Every arithmetic step runs in libdpgrad's HIP
 kernels; this module only owns the device buffers (allocated once, up front)
-and enqueues the calls, in order, on one stream.
+and enqueues the calls, in order, on one stream:
 
-For a Linear layer the clipped sum is formed one of two ways, whichever moves
-fewer bytes / flops at the roofline: a column reduction over the stored
-per-sample gradients (reads N*P floats) or the fused GEMM B^T diag(c) A
-(reads A and B again, 2*N*T*d_in*d_out flops).
+  1. one per-sample-gradient call per layer (each also writes that layer's
+     row of per-sample squared norms);
+  2. dp_per_sample_norms;
+  3. fused clipped sums where they are cheaper (Linear: B^T diag(c) A;
+     Embedding: CSR -> dense);
+  4. one dp_clip_noise_many for every parameter tensor: column-reduces the
+     remaining per-sample gradients and writes every tensor's noised average.
+
+A step can be captured once as a HIP graph and replayed; the noise step then
+comes from a device counter that the graph advances itself.
 """
 from __future__ import annotations
 
@@ -23,9 +29,12 @@ from . import binding as dp
 from . import workloads as W
 
 HBM_BYTES_PER_S = 8.0e12
-# matrix-core peaks used by the clipped-sum cost model (the fused GEMM runs on
-# fp32 MFMA for both input dtypes)
+# Matrix-core peak used by the clipped-sum cost model (the fused GEMM runs on
+# fp32 MFMA for both input dtypes), and the cost of the extra launches the
+# fused route adds (the GEMM and its split reduction) next to the grouped
+# column reduction, which is shared by all tensors.
 FUSED_FLOPS_PER_S = {W.F32: 157.3e12, W.BF16: 157.3e12}
+LAUNCH_S = 3e-6
 
 
 @dataclass
@@ -40,6 +49,8 @@ class LayerBufs:
     uniq: object = None
     rows: object = None
     clip_mode: str = "colreduce"
+    ws: object = None          # scratch of the per-sample-gradient call
+    ws_clip: object = None     # scratch of the fused clipped sum
 
 
 def _torch():
@@ -58,9 +69,10 @@ def to_device(a: np.ndarray, dtype: str, device):
 
 
 def linear_clip_mode(layer: W.Linear, N: int, dtype: str) -> str:
+    """'fused' (B^T diag(c) A from A and B) or 'colreduce' (read the stored grads)."""
     elt = 2 if dtype == W.BF16 else 4
     fused = (2.0 * N * layer.T * layer.d_in * layer.d_out / FUSED_FLOPS_PER_S[dtype]
-             + N * layer.T * (layer.d_in + layer.d_out) * elt / HBM_BYTES_PER_S)
+             + N * layer.T * (layer.d_in + layer.d_out) * elt / HBM_BYTES_PER_S + 2 * LAUNCH_S)
     col = N * layer.n_params * 4 / HBM_BYTES_PER_S
     return "fused" if fused < col else "colreduce"
 
@@ -83,44 +95,42 @@ class DPStep:
         N = self.N
         f32 = dict(dtype=torch.float32, device=self.device)
         self.layers: List[LayerBufs] = []
-        ws_need = 0
         for li in inputs:
             layer = li.layer
             lb = LayerBufs(layer)
             if li.A is not None:
                 lb.A = to_device(li.A, wl.dtype, self.device)
             lb.B = to_device(li.B, wl.dtype, self.device)
+            need_g = need_c = 0
             if isinstance(layer, W.Linear):
                 lb.gW = torch.empty((N, layer.d_out, layer.d_in), **f32)
                 lb.gb = torch.empty((N, layer.d_out), **f32) if layer.bias else None
                 lb.clip_mode = linear_clip_mode(layer, N, wl.dtype) if clip_mode == "auto" else clip_mode
-                ws_need = max(ws_need, dp.dp_grad_sample_linear_workspace_bytes(N, layer.T, layer.d_in,
-                                                                                layer.d_out, self.dt))
+                need_g = dp.dp_grad_sample_linear_workspace_bytes(N, layer.T, layer.d_in, layer.d_out, self.dt)
                 if lb.clip_mode == "fused":
-                    ws_need = max(ws_need, dp.dp_clip_accumulate_linear_workspace_bytes(
-                        N, layer.T, layer.d_in, layer.d_out, self.dt))
-                else:
-                    ws_need = max(ws_need, dp.dp_clip_accumulate_workspace_bytes(N, layer.d_out * layer.d_in))
+                    need_c = dp.dp_clip_accumulate_linear_workspace_bytes(N, layer.T, layer.d_in, layer.d_out,
+                                                                          self.dt)
             elif isinstance(layer, W.Conv2d):
                 lb.gW = torch.empty((N, layer.c_out, layer.c_in) + tuple(layer.k), **f32)
                 lb.gb = torch.empty((N, layer.c_out), **f32) if layer.bias else None
-                ws_need = max(ws_need, dp.dp_grad_sample_conv2d_workspace_bytes(N, layer.c_in, layer.c_out,
-                                                                                *layer.k))
-                ws_need = max(ws_need, dp.dp_clip_accumulate_workspace_bytes(N, layer.n_params))
+                need_g = dp.dp_grad_sample_conv2d_workspace_bytes(
+                    N, layer.c_in, layer.h, layer.w, layer.c_out, layer.k[0], layer.k[1], layer.stride[0],
+                    layer.stride[1], layer.pad[0], layer.pad[1])
             elif isinstance(layer, W.Embedding):
                 lb.ids = to_device(li.ids, "", self.device)
                 cap = N * layer.T
                 lb.row_ptr = torch.empty(N + 1, dtype=torch.int64, device=self.device)
                 lb.uniq = torch.empty(max(cap, 1), dtype=torch.int64, device=self.device)
                 lb.rows = torch.empty((max(cap, 1), layer.D), **f32)
-                ws_need = max(ws_need, dp.dp_grad_sample_embedding_workspace_bytes(N, layer.T))
+                need_g = dp.dp_grad_sample_embedding_workspace_bytes(N, layer.T)
             elif isinstance(layer, W.LayerNorm):
                 lb.gW = torch.empty((N, layer.D), **f32)
                 lb.gb = torch.empty((N, layer.D), **f32)
-                ws_need = max(ws_need, dp.dp_grad_sample_layernorm_workspace_bytes(N, layer.T, layer.D))
-                ws_need = max(ws_need, dp.dp_clip_accumulate_workspace_bytes(N, layer.D))
+                need_g = dp.dp_grad_sample_layernorm_workspace_bytes(N, layer.T, layer.D)
+            # each layer has its own scratch, so its calls may run concurrently with other layers'
+            lb.ws = torch.empty(max(need_g, 256), dtype=torch.uint8, device=self.device)
+            lb.ws_clip = torch.empty(max(need_c, 256), dtype=torch.uint8, device=self.device)
             self.layers.append(lb)
-        self.ws = torch.empty(max(ws_need, 256), dtype=torch.uint8, device=self.device)
         self.sqnorm = torch.empty((len(self.layers), N), **f32)
         self.norm = torch.empty(N, **f32)
         self.status = torch.zeros(1, dtype=torch.int32, device=self.device)
@@ -130,6 +140,30 @@ class DPStep:
         for name, shape in self.params:
             self.S[name] = torch.empty(shape, **f32)
             self.out[name] = torch.empty(shape, **f32)
+        # the grouped clip/noise call: per-sample grads for column-reduced tensors
+        entries = []
+        for pidx, (name, shape) in enumerate(self.params):
+            entries.append((self._grad_for(name), self.S[name], self.out[name], int(np.prod(shape)), pidx))
+        self.group = dp.make_params(entries)
+        self.group_count = len(entries)
+        need = dp.dp_clip_noise_many_workspace_bytes(self.group, self.group_count, N)
+        self.ws = torch.empty(max(need, 256), dtype=torch.uint8, device=self.device)
+        self.step_dev = torch.zeros(1, dtype=torch.int64, device=self.device)
+        self.graph = None
+        self._side = None
+
+    def _grad_for(self, pname: str):
+        """The per-sample grad buffer of a parameter if it is column-reduced, else None."""
+        lname, key = pname.rsplit(".", 1)
+        for lb in self.layers:
+            if lb.layer.name != lname:
+                continue
+            if isinstance(lb.layer, W.Embedding):
+                return None
+            if isinstance(lb.layer, W.Linear) and lb.clip_mode == "fused":
+                return None
+            return lb.gW if key == "weight" else lb.gb
+        raise KeyError(pname)
 
     # ------------------------------------------------------------------ pieces
     def grad_sample(self, i: int, stream=None):
@@ -138,64 +172,120 @@ class DPStep:
         N, s, sq = self.N, self.scale, self.sqnorm[i]
         if isinstance(layer, W.Linear):
             dp.dp_grad_sample_linear(lb.A, lb.B, self.dt, N, layer.T, layer.d_in, layer.d_out, s, lb.gW, lb.gb,
-                                     sq, self.status, self.ws, stream)
+                                     sq, self.status, lb.ws, stream)
         elif isinstance(layer, W.Conv2d):
             ho, wo = layer.out_hw
             dp.dp_grad_sample_conv2d(lb.A, lb.B, self.dt, N, layer.c_in, layer.h, layer.w, layer.c_out, ho, wo,
                                      layer.k[0], layer.k[1], layer.stride[0], layer.stride[1], layer.pad[0],
-                                     layer.pad[1], 1, 1, 1, s, lb.gW, lb.gb, sq, self.status, self.ws, stream)
+                                     layer.pad[1], 1, 1, 1, s, lb.gW, lb.gb, sq, self.status, lb.ws, stream)
         elif isinstance(layer, W.Embedding):
             dp.dp_grad_sample_embedding(lb.ids, lb.B, self.dt, N, layer.T, layer.V, layer.D, s, lb.row_ptr,
-                                        lb.uniq, lb.rows, N * layer.T, sq, self.status, self.ws, stream)
+                                        lb.uniq, lb.rows, N * layer.T, sq, self.status, lb.ws, stream)
         elif isinstance(layer, W.LayerNorm):
             dp.dp_grad_sample_layernorm(lb.A, lb.B, self.dt, N, layer.T, layer.D, s, lb.gW, lb.gb, sq,
-                                        self.status, self.ws, stream)
+                                        self.status, lb.ws, stream)
 
     def norms(self, stream=None):
         dp.dp_per_sample_norms(self.sqnorm, len(self.layers), self.N, self.norm, self.status, stream)
 
-    def clip_sum(self, i: int, stream=None):
+    def fused_clip_sum(self, i: int, stream=None):
+        """Clipped sums formed without reading per-sample grads (fused Linear, Embedding)."""
         lb = self.layers[i]
         layer = lb.layer
-        N, C = self.N, self.C
         name = layer.name
         if isinstance(layer, W.Linear) and lb.clip_mode == "fused":
-            dp.dp_clip_accumulate_linear(lb.A, lb.B, self.dt, N, layer.T, layer.d_in, layer.d_out, self.scale,
-                                         self.norm, C, self.S[name + ".weight"], self.S.get(name + ".bias"),
-                                         self.status, self.ws, stream)
+            dp.dp_clip_accumulate_linear(lb.A, lb.B, self.dt, self.N, layer.T, layer.d_in, layer.d_out,
+                                         self.scale, self.norm, self.C, self.S[name + ".weight"],
+                                         self.S.get(name + ".bias"), self.status, lb.ws_clip, stream)
         elif isinstance(layer, W.Embedding):
-            dp.dp_clip_accumulate_embedding(lb.row_ptr, lb.uniq, lb.rows, self.norm, C, N, layer.V, layer.D,
-                                            self.S[name + ".weight"], self.status, stream)
-        else:
-            for key, g in (("weight", lb.gW), ("bias", lb.gb)):
-                if g is None:
-                    continue
-                numel = g[0].numel() if N > 0 else int(np.prod(self.S[name + "." + key].shape))
-                dp.dp_clip_accumulate(g, self.norm, C, N, numel, self.S[name + "." + key], None,
-                                      self.status, self.ws, stream)
+            dp.dp_clip_accumulate_embedding(lb.row_ptr, lb.uniq, lb.rows, self.norm, self.C, self.N, layer.V,
+                                            layer.D, self.S[name + ".weight"], self.status, stream)
 
-    def noise(self, step: int, stream=None):
-        for pidx, (name, shape) in enumerate(self.params):
-            S = self.S[name]
-            dp.dp_add_noise(S, self.out[name], S.numel(), self.seed, step, pidx, self.sigma, self.C, self.denom,
-                            self.status, stream)
+    def clip_noise(self, step: int, step_dev=None, stream=None):
+        dp.dp_clip_noise_many(self.group, self.group_count, self.N, self.norm, self.C, self.seed, step, step_dev,
+                              self.sigma, self.denom, self.status, self.ws, stream)
+
+    def _fork(self, n):
+        torch = _torch()
+        if self._side is None or len(self._side) < n:
+            self._side = [torch.cuda.Stream(self.device) for _ in range(n)]
+        return self._side[:n]
 
     # ------------------------------------------------------------------ whole step
-    def run(self, step: int = 0, stream=None, mark: Optional[Callable[[str, str], None]] = None):
-        """Enqueue one whole step; nothing is synchronized here."""
+    def run(self, step: int = 0, stream=None, mark: Optional[Callable[[str, str], None]] = None, step_dev=None,
+            parallel: bool = False, advance: bool = False):
+        """Enqueue one whole step; nothing is synchronized here.
+
+        parallel: the layers' per-sample-gradient calls (independent of each
+        other) and the fused clipped sums run on side streams forked from and
+        joined back into the current stream.  advance: also enqueue
+        dp_step_advance on step_dev, in a branch ahead of the noise."""
+        torch = _torch()
         self.status.zero_()
-        for i, lb in enumerate(self.layers):
-            if mark: mark("grad:" + lb.layer.name, "start")
-            self.grad_sample(i, stream)
-            if mark: mark("grad:" + lb.layer.name, "end")
-        self.norms(stream)
-        for i, lb in enumerate(self.layers):
-            if mark: mark("clip:" + lb.layer.name, "start")
-            self.clip_sum(i, stream)
-            if mark: mark("clip:" + lb.layer.name, "end")
-        if mark: mark("noise", "start")
-        self.noise(step, stream)
-        if mark: mark("noise", "end")
+        if not parallel:
+            if advance:
+                dp.dp_step_advance(step_dev, 1, stream)
+            for i, lb in enumerate(self.layers):
+                if mark: mark("grad:" + lb.layer.name, "start")
+                self.grad_sample(i, stream)
+                if mark: mark("grad:" + lb.layer.name, "end")
+            if mark: mark("norms", "start")
+            self.norms(stream)
+            if mark: mark("norms", "end")
+            for i, lb in enumerate(self.layers):
+                if isinstance(lb.layer, W.Embedding) or lb.clip_mode == "fused":
+                    if mark: mark("clip:" + lb.layer.name, "start")
+                    self.fused_clip_sum(i, stream)
+                    if mark: mark("clip:" + lb.layer.name, "end")
+            if mark: mark("clip+noise", "start")
+            self.clip_noise(step, step_dev, stream)
+            if mark: mark("clip+noise", "end")
+            return
+        main = torch.cuda.current_stream(self.device)
+        side = self._fork(len(self.layers) + 1)
+        for i in range(len(self.layers)):
+            side[i].wait_stream(main)
+            with torch.cuda.stream(side[i]):
+                self.grad_sample(i)
+        if advance:
+            side[-1].wait_stream(main)
+            with torch.cuda.stream(side[-1]):
+                dp.dp_step_advance(step_dev, 1)
+        for s_ in side:
+            main.wait_stream(s_)
+        self.norms()
+        fused = [i for i, lb in enumerate(self.layers)
+                 if isinstance(lb.layer, W.Embedding) or lb.clip_mode == "fused"]
+        for k, i in enumerate(fused):
+            side[k].wait_stream(main)
+            with torch.cuda.stream(side[k]):
+                self.fused_clip_sum(i)
+        for k in range(len(fused)):
+            main.wait_stream(side[k])
+        self.clip_noise(step, step_dev)
+
+    def capture(self, first_step: int = 0, parallel: bool = True):
+        """Capture one step as a HIP graph; replay r runs step first_step + r.
+
+        The graph advances its own device step counter (in a branch that runs
+        before the noise), so nothing is re-recorded between replays."""
+        torch = _torch()
+        side = torch.cuda.Stream(self.device)
+        side.wait_stream(torch.cuda.current_stream(self.device))
+        with torch.cuda.stream(side):
+            self.run(step=0, parallel=parallel)          # warm up outside the capture
+        torch.cuda.current_stream(self.device).wait_stream(side)
+        torch.cuda.synchronize(self.device)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            self.run(step=0, step_dev=self.step_dev, parallel=parallel, advance=True)
+        torch.cuda.synchronize(self.device)
+        self.step_dev.fill_(first_step - 1)    # advanced to first_step by the first replay
+        self.graph = g
+        return g
+
+    def replay(self):
+        self.graph.replay()
 
     def results(self) -> Dict[str, object]:
         """Copy everything back to host numpy arrays (synchronizes)."""

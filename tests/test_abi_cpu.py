@@ -116,8 +116,10 @@ def test_clip_and_noise_validation():
 
 
 def test_clip_sum_route_choice():
-    # T = 1 Linear: the fused GEMM reads A and B (N*(d_in+d_out)) instead of N*P grads
-    assert stepmod.linear_clip_mode(W.Linear("fc1", 512, 32), 256, W.F32) == "fused"
+    # small T = 1 Linear: rereading 16.8 MB of grads in the shared grouped launch beats two extra launches
+    assert stepmod.linear_clip_mode(W.Linear("fc1", 512, 32), 256, W.F32) == "colreduce"
+    # a wide T = 1 Linear on a big batch: the fused GEMM reads N*(d_in+d_out) instead of N*P
+    assert stepmod.linear_clip_mode(W.Linear("big", 4096, 1024), 4096, W.F32) == "fused"
     # LSTM weights (K = N*T = 16384, small outputs): rereading the grads is cheaper
     assert stepmod.linear_clip_mode(W.Linear("ih", 100, 400, T=256), 64, W.F32) == "colreduce"
 

@@ -166,7 +166,12 @@ def test_linear_ragged_shapes(dtype, N, T, din, dout):
 CONV_SHAPES = [  # N, Cin, H, W, Cout, kh, kw, sh, sw, ph, pw
     (2, 3, 7, 9, 5, 3, 3, 2, 2, 1, 1), (3, 1, 28, 28, 16, 8, 8, 2, 2, 3, 3), (2, 16, 13, 13, 32, 4, 4, 2, 2, 0, 0),
     (2, 3, 32, 32, 32, 3, 3, 1, 1, 1, 1), (1, 70, 6, 5, 33, 1, 1, 1, 1, 0, 0), (2, 5, 9, 4, 66, 2, 3, 1, 2, 1, 0),
-    (1, 130, 8, 8, 129, 3, 3, 1, 1, 1, 1)]
+    (1, 130, 8, 8, 129, 3, 3, 1, 1, 1, 1),
+    (2, 8, 10, 10, 32, 4, 4, 1, 1, 0, 0),      # 128 x 32 tile, two-way K split
+    (1, 2, 130, 130, 4, 3, 3, 1, 1, 1, 1),     # input planes too large for LDS: gathered fallback
+    (2, 32, 32, 32, 64, 3, 3, 1, 1, 1, 1), (2, 64, 16, 16, 64, 3, 3, 1, 1, 1, 1),
+    (2, 64, 16, 16, 128, 3, 3, 1, 1, 1, 1), (2, 128, 8, 8, 128, 3, 3, 1, 1, 1, 1),
+    (2, 128, 8, 8, 256, 3, 3, 1, 1, 1, 1)]
 
 
 @pytest.mark.parametrize("shape", CONV_SHAPES)
@@ -182,8 +187,8 @@ def test_conv_shapes(shape):
     gW = torch.empty((N, Cout, Cin, kh, kw), device=DEV)
     gb = torch.empty((N, Cout), device=DEV)
     sq = torch.empty(N, device=DEV)
-    ws = torch.empty(max(dp.dp_grad_sample_conv2d_workspace_bytes(N, Cin, Cout, kh, kw), 1), dtype=torch.uint8,
-                     device=DEV)
+    ws = torch.empty(max(dp.dp_grad_sample_conv2d_workspace_bytes(N, Cin, H, Wd, Cout, kh, kw, sh, sw, ph, pw), 1),
+                     dtype=torch.uint8, device=DEV)
     dp.dp_grad_sample_conv2d(Xt, Gt, dp.DP_F32, N, Cin, H, Wd, Cout, Ho, Wo, kh, kw, sh, sw, ph, pw, 1, 1, 1, 1.3,
                              gW, gb, sq, None, ws)
     rW, rb = oracle.conv2d_grad(X, GY, (kh, kw), (sh, sw), (ph, pw), 1.3)
@@ -318,3 +323,60 @@ def test_sigma0_Cinf_reproduces_the_mean_gradient():
     ref = oracle.dp_step(wl, inputs, C=math.inf, sigma=0.0)
     for k in ref["out"]:
         assert_g12(got["out"][k], ref["out"][k], 1e-4, k)
+
+
+def test_clip_noise_many_matches_the_single_tensor_calls():
+    r = np.random.default_rng(21)
+    for N in (0, 5, 300):
+        say("clip_noise_many N=", N)
+        shapes = [1, 7, 1024, 4099, 16, 33 * 3]
+        norm = torch.from_numpy(r.uniform(0.1, 3.0, max(N, 1)).astype(np.float32)).to(DEV)
+        entries, refs = [], []
+        for i, numel in enumerate(shapes):
+            G = torch.from_numpy(r.standard_normal((max(N, 1), numel)).astype(np.float32)).to(DEV)[:N]
+            S = torch.full((numel,), 7.0, device=DEV)
+            O = torch.empty(numel, device=DEV)
+            if i % 3 == 2:      # sum given (fused route): only noise
+                S = torch.from_numpy(r.standard_normal(numel).astype(np.float32)).to(DEV)
+                entries.append((None, S, O, numel, i + 3))
+            elif i % 3 == 1:    # clip only, no output
+                entries.append((G, S, None, numel, i + 3))
+            else:
+                entries.append((G, S, O, numel, i + 3))
+            refs.append((G, S.clone(), O))
+        params = dp.make_params(entries)
+        ws = torch.empty(max(dp.dp_clip_noise_many_workspace_bytes(params, len(entries), N), 1), dtype=torch.uint8,
+                         device=DEV)
+        dp.dp_clip_noise_many(params, len(entries), N, norm, 1.3, 5, 9, None, 0.7, 11.0, None, ws)
+        for (g, s, o, numel, pidx), (G, S0, _) in zip(entries, refs):
+            if g is not None:
+                Sr = torch.empty(numel, device=DEV)
+                ws2 = torch.empty(max(dp.dp_clip_accumulate_workspace_bytes(N, numel), 1), dtype=torch.uint8,
+                                  device=DEV)
+                dp.dp_clip_accumulate(G if N else None, norm if N else None, 1.3, N, numel, Sr, None, None, ws2)
+                assert_g12(s.cpu().numpy(), Sr.cpu().numpy(), 1e-6, "sum")
+            else:
+                Sr = S0
+            if o is not None:
+                Or = torch.empty(numel, device=DEV)
+                dp.dp_add_noise(Sr, Or, numel, 5, 9, pidx, 0.7, 1.3, 11.0)
+                assert_g12(o.cpu().numpy(), Or.cpu().numpy(), 1e-6, "out")
+
+
+def test_graph_replay_matches_eager_steps():
+    wl = W.get("mnist_cnn")
+    inputs = W.make_inputs(wl, n=20)
+    st = DPStep(wl, inputs, DEV)
+    say("graph capture mnist_cnn")
+    st.capture(first_step=4)
+    eager = DPStep(wl, inputs, DEV)
+    for k in range(4):
+        st.replay()
+        got = st.results()
+        eager.run(step=4 + k)                      # eager work between replays
+        ref = eager.results()
+        for name in ref["out"]:
+            np.testing.assert_array_equal(got["out"][name], ref["out"][name], err_msg="replay %d %s" % (k, name))
+            np.testing.assert_array_equal(got["S"][name], ref["S"][name])
+        np.testing.assert_array_equal(got["norm"], ref["norm"])
+    assert int(st.step_dev.item()) == 7     # the counter holds the last replayed step
