@@ -40,10 +40,11 @@ def log(*a):
 # ---------------------------------------------------------------------------
 
 def call_costs(st):
-    """name -> (algorithmic bytes, flops, kernel name) for each call of one step."""
+    """name -> (algorithmic bytes, flops, kernel name, MFMA peak key or None) per call of one step."""
     from paper_2109_12298_amd import workloads as W
     N = st.N
-    e = 2 if st.wl.dtype == W.BF16 else 4
+    bf = st.wl.dtype == W.BF16
+    e = 2 if bf else 4
     out = {}
     col_bytes = 0
     for lb in st.layers:
@@ -51,15 +52,20 @@ def call_costs(st):
         if isinstance(L, W.Linear):
             bias = L.d_out if L.bias else 0
             grads = N * (L.d_out * L.d_in + bias) * 4
+            bf_mfma = bf and L.T > 1 and L.d_in % 8 == 0 and L.d_out % 8 == 0
             if L.T == 1:
                 out["grad:" + L.name] = (N * (L.d_in + L.d_out) * e + grads + N * 4, N * L.d_out * L.d_in,
-                                         "outer_kernel")
+                                         "outer_kernel", None)
             else:
                 out["grad:" + L.name] = (N * L.T * (L.d_in + L.d_out) * e + grads + N * 4,
-                                         2 * N * L.T * L.d_in * L.d_out, "per_sample_gemm_kernel")
+                                         2 * N * L.T * L.d_in * L.d_out,
+                                         "bf16_per_sample_kernel" if bf_mfma else "per_sample_gemm_kernel",
+                                         "bf16" if bf_mfma else "f32")
             if lb.clip_mode == "fused":
                 out["clip:" + L.name] = (N * L.T * (L.d_in + L.d_out) * e + (L.d_out * L.d_in + bias) * 4,
-                                         2 * N * L.T * L.d_in * L.d_out, "clipsum_gemm_kernel")
+                                         2 * N * L.T * L.d_in * L.d_out,
+                                         "bf16_clipsum_kernel" if bf_mfma else "clipsum_gemm_kernel",
+                                         "bf16" if bf_mfma else "f32")
             else:
                 col_bytes += grads
         elif isinstance(L, W.Conv2d):
@@ -67,22 +73,22 @@ def call_costs(st):
             kk = L.c_in * L.k[0] * L.k[1]
             grads = N * L.n_params * 4
             out["grad:" + L.name] = (N * (L.c_in * L.h * L.w + L.c_out * ho * wo) * e + grads + N * 4,
-                                     2 * N * L.c_out * kk * ho * wo, "conv_per_sample_kernel")
+                                     2 * N * L.c_out * kk * ho * wo, "conv_per_sample_kernel", "f32")
             col_bytes += grads
         elif isinstance(L, W.Embedding):
             nnz_bound = N * L.T
             out["grad:" + L.name] = (N * L.T * (8 + L.D * e) + N * L.T * (L.D * 4 + 8), N * L.T * L.D,
-                                     "emb_rows_kernel")
+                                     "emb_rows_kernel", None)
             out["clip:" + L.name] = (nnz_bound * L.D * 4 + L.V * L.D * 4, 2 * nnz_bound * L.D,
-                                     "emb_clipsum_kernel")
+                                     "emb_clipsum_kernel", None)
         elif isinstance(L, W.LayerNorm):
             out["grad:" + L.name] = (2 * N * L.T * L.D * e + 2 * N * L.D * 4, 3 * N * L.T * L.D,
-                                     "ln_partial_kernel")
+                                     "ln_partial_kernel", None)
             col_bytes += 2 * N * L.D * 4
-    out["norms"] = (len(st.layers) * N * 4 + N * 4, len(st.layers) * N, "norms_kernel")
+    out["norms"] = (len(st.layers) * N * 4 + N * 4, len(st.layers) * N, "norms_kernel", None)
     P = st.wl.n_params
     # grouped clip + noise: read the column-reduced grads once, write S and out, read fused S
-    out["clip+noise"] = (col_bytes + 12 * P, 0, "colsum_many_kernel+finish_many_kernel")
+    out["clip+noise"] = (col_bytes + 12 * P, 0, "colsum_many_kernel+finish_many_kernel", None)
     return out
 
 
@@ -96,6 +102,8 @@ def src_hash(paths):
 
 KERNEL_SOURCES = {
     "outer_kernel": ["paper_2109_12298_amd/csrc/linear.hip"],
+    "bf16_per_sample_kernel": ["paper_2109_12298_amd/csrc/linear_bf16.hip"],
+    "bf16_clipsum_kernel": ["paper_2109_12298_amd/csrc/linear_bf16.hip"],
     "per_sample_gemm_kernel": ["paper_2109_12298_amd/csrc/linear.hip", "paper_2109_12298_amd/csrc/mfma_tile.hpp"],
     "clipsum_gemm_kernel": ["paper_2109_12298_amd/csrc/linear.hip", "paper_2109_12298_amd/csrc/mfma_tile.hpp"],
     "conv_per_sample_kernel": ["paper_2109_12298_amd/csrc/conv2d.hip", "paper_2109_12298_amd/csrc/mfma_tile.hpp"],
@@ -214,7 +222,7 @@ def main():
         for n in names:
             if n not in avg:
                 continue
-            b, f, k = costs[n]
+            b, f, k, _ = costs[n]
             log("[breakdown] %-18s %9.2f us  %10.3f MB  %9.3f GFLOP  %s" % (n, avg[n] * 1e3, b / 1e6, f / 1e9, k))
 
     # the timed region: K whole steps, replayed from one captured HIP graph
@@ -266,13 +274,13 @@ def main():
 
     ms = elapsed * 1e3 / args.steps
     dom_ms = sum(a.elapsed_time(b) for a, b in dom) / len(dom)
-    nbytes, flops, kname = costs[dominant]
+    nbytes, flops, kname, mfma_dtype = costs[dominant]
     dt_s = dom_ms * 1e-3
     hbm_s = nbytes / (HBM_PEAK_GBS * 1e9)
     dtype = "bf16" if wl.dtype == W.BF16 else "f32"
-    mfma_dtype = "f32"   # the per-sample contractions run on fp32 MFMA for both input dtypes
-    mfma_s = flops / (PEAK_TFLOPS[mfma_dtype] * 1e12) if kname.endswith("gemm_kernel") or "conv" in kname else 0
-    # (noise and the column reduction are VALU/HBM work: compared against HBM)
+    # MFMA kernels are priced at their own input type's matrix peak; noise and
+    # the column reductions are VALU/HBM work and are compared against HBM
+    mfma_s = flops / (PEAK_TFLOPS[mfma_dtype] * 1e12) if mfma_dtype else 0.0
     if mfma_s > hbm_s:
         roof = {"bound": "mfma", "achieved": round(flops / dt_s / 1e12, 3), "peak": PEAK_TFLOPS[mfma_dtype],
                 "unit": "TFLOP/s"}

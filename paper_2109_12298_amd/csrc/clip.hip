@@ -19,7 +19,7 @@ __global__ void norms_kernel(const float *__restrict__ sq, int L, i64 N, float *
     const i64 n = (i64)blockIdx.x * blockDim.x + threadIdx.x;
     if (n >= N) return;
     float s = 0.0f;
-    for (int l = 0; l < L; ++l) s += sq[(i64)l * N + n];
+    s = ordered_sum(sq + n, N, L);
     const float r = sqrtf(s);
     if (!isfinite(r)) raise_flag(status, DP_FLAG_NONFINITE);
     norm[n] = r;
@@ -107,7 +107,7 @@ __global__ void range_sum_kernel(const float *__restrict__ part, int splits, i64
     const i64 e = (i64)blockIdx.x * blockDim.x + threadIdx.x;
     if (e >= count) return;
     float s = 0.0f;
-    for (int k = 0; k < splits; ++k) s += part[(i64)k * count + e];
+    s = ordered_sum(part + e, count, splits);
     out[e] = s;
 }
 

@@ -33,7 +33,7 @@ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 inline bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
-inline i64 ceil_div(i64 a, i64 b) { return (a + b - 1) / b; }
+__host__ __device__ inline i64 ceil_div(i64 a, i64 b) { return (a + b - 1) / b; }
 
 // ---------------------------------------------------------------------------
 // element loads (bf16 is carried as its raw 16 bits)
@@ -56,6 +56,21 @@ template <>
 __device__ __forceinline__ float load_elem<uint16_t>(const uint16_t *p, i64 i)
 {
     return bf16_to_f32(p[i]);
+}
+
+// ---------------------------------------------------------------------------
+// XCD-aware block order.  Workgroups are dispatched round-robin over the 8
+// XCDs (each with its own L2): block b runs on XCD b % 8.  Renumbering so that
+// XCD x gets a contiguous range of logical blocks keeps neighbouring tiles,
+// which share operand tiles, in one L2.  A bijection on [0, nb).
+// ---------------------------------------------------------------------------
+constexpr int kXcds = 8;
+
+__device__ __forceinline__ i64 xcd_swizzle(i64 b, i64 nb)
+{
+    const i64 q = nb / kXcds, r = nb % kXcds;
+    const i64 x = b % kXcds, k = b / kXcds;
+    return x * q + (x < r ? x : r) + k;
 }
 
 // ---------------------------------------------------------------------------
@@ -101,6 +116,45 @@ __device__ __forceinline__ float block_sum(float v, float *red)
     float s = 0.0f;
     for (int w = 0; w < nw; ++w) s += red[w];
     return s;
+}
+
+// sum_k p[k * stride] for k = 0 .. count-1, added in ascending k, with eight
+// loads in flight at a time (a loop of dependent single loads is bound by
+// memory latency, not bandwidth).
+__device__ __forceinline__ float ordered_sum(const float *__restrict__ p, i64 stride, int count)
+{
+    float s = 0.0f;
+    for (int k = 0; k < count; k += 8) {
+        float v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = k + j < count ? p[(i64)(k + j) * stride] : 0.0f;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) s += v[j];
+    }
+    return s;
+}
+
+// One wave per sample: sqnorm[n] = sum of the sample's `parts` tile partials
+// (lane l adds partials l, l+64, ... in order, then a fixed butterfly).
+template <int Unused = 0>
+__global__ void sum_partials_kernel(const float *__restrict__ partial, i64 N, int parts,
+                                    float *__restrict__ sqnorm)
+{
+    const i64 n = (i64)blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
+    const int lane = threadIdx.x & (kWave - 1);
+    if (n >= N) return;
+    const float *p = partial + n * parts;
+    float s = 0.0f;
+    for (int t = lane; t < parts; t += kWave) s += p[t];
+    s = wave_sum(s);
+    if (lane == 0) sqnorm[n] = s;
+}
+
+inline void sum_partials(const float *partial, i64 N, int parts, float *sqnorm, hipStream_t stream)
+{
+    const int per_block = 4;
+    sum_partials_kernel<0><<<(unsigned)((N + per_block - 1) / per_block), per_block * kWave, 0, stream>>>(
+        partial, N, parts, sqnorm);
 }
 
 // ---------------------------------------------------------------------------

@@ -63,8 +63,9 @@ __global__ __launch_bounds__(kThreads) void conv_per_sample_kernel(
     extern __shared__ float lds[];
     __shared__ float red16[16];
 
-    const int n = blockIdx.x / g.tiles;
-    const int tile = blockIdx.x % g.tiles;
+    const i64 bsw = xcd_swizzle(blockIdx.x, gridDim.x);
+    const int n = (int)(bsw / g.tiles);
+    const int tile = (int)(bsw % g.tiles);
     const int tm = tile / g.tiles_n, tn = tile % g.tiles_n;
     const int m0 = tm * Cfg::BM;   // first kk
     const int n0 = tn * Cfg::BN;   // first co
@@ -328,16 +329,6 @@ __global__ __launch_bounds__(kThreads) void conv_generic_kernel(
     }
 }
 
-__global__ void conv_reduce_partials_kernel(const float *__restrict__ partial, i64 N, int tiles,
-                                            float *__restrict__ sqnorm)
-{
-    const i64 n = (i64)blockIdx.x * blockDim.x + threadIdx.x;
-    if (n >= N) return;
-    float s = 0.0f;
-    for (int t = 0; t < tiles; ++t) s += partial[n * tiles + t];
-    sqnorm[n] = s;
-}
-
 // ---------------------------------------------------------------------------
 // host: pick a tile configuration
 // ---------------------------------------------------------------------------
@@ -548,7 +539,6 @@ extern "C" dp_status dp_grad_sample_conv2d(const void *X, const void *GY, dp_dty
                                                                     tiles_n, tiles, scale, gW, gb, sqout, direct);
     }
     if (sqnorm && !direct)
-        conv_reduce_partials_kernel<<<(unsigned)ceil_div(N, 256), 256, 0, stream>>>((float *)ws, N, tiles,
-                                                                                   sqnorm);
+        sum_partials((const float *)ws, N, tiles, sqnorm, stream);
     return launch_status();
 }

@@ -10,6 +10,65 @@ namespace {
 
 constexpr int kThreads = 256;
 
+// four consecutive features of one row as fp32
+template <typename T>
+__device__ __forceinline__ float4 load4f(const T *p);
+
+template <>
+__device__ __forceinline__ float4 load4f<float>(const float *p)
+{
+    return *reinterpret_cast<const float4 *>(p);
+}
+
+template <>
+__device__ __forceinline__ float4 load4f<uint16_t>(const uint16_t *p)
+{
+    const uint2 u = *reinterpret_cast<const uint2 *>(p);
+    return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
+                       __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u));
+}
+
+// Vector path (D % 4 == 0, aligned rows): a thread owns four features and
+// keeps four rows' loads in flight; rows are still added in ascending t.
+template <typename T>
+__global__ __launch_bounds__(kThreads) void ln_partial_vec_kernel(const T *__restrict__ xh,
+                                                                  const T *__restrict__ B, i64 Tn,
+                                                                  i64 D, int splits, i64 per,
+                                                                  float *__restrict__ part)
+{
+    const i64 n = blockIdx.x / splits;
+    const int sp = blockIdx.x % splits;
+    const i64 t0 = (i64)sp * per;
+    const i64 t1 = t0 + per < Tn ? t0 + per : Tn;
+    float *pg = part + ((i64)n * splits + sp) * 2 * D;
+    for (i64 k = 4 * (i64)threadIdx.x; k < D; k += 4 * kThreads) {
+        float4 ag = make_float4(0.f, 0.f, 0.f, 0.f), ab = ag;
+        i64 t = t0;
+        for (; t + 4 <= t1; t += 4) {
+            float4 b[4], x[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const i64 idx = (n * Tn + t + r) * D + k;
+                b[r] = load4f<T>(B + idx);
+                x[r] = load4f<T>(xh + idx);
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                ag.x += b[r].x * x[r].x; ag.y += b[r].y * x[r].y; ag.z += b[r].z * x[r].z; ag.w += b[r].w * x[r].w;
+                ab.x += b[r].x; ab.y += b[r].y; ab.z += b[r].z; ab.w += b[r].w;
+            }
+        }
+        for (; t < t1; ++t) {
+            const i64 idx = (n * Tn + t) * D + k;
+            const float4 b = load4f<T>(B + idx), x = load4f<T>(xh + idx);
+            ag.x += b.x * x.x; ag.y += b.y * x.y; ag.z += b.z * x.z; ag.w += b.w * x.w;
+            ab.x += b.x; ab.y += b.y; ab.z += b.z; ab.w += b.w;
+        }
+        *reinterpret_cast<float4 *>(pg + k) = ag;
+        *reinterpret_cast<float4 *>(pg + D + k) = ab;
+    }
+}
+
 template <typename T>
 __global__ __launch_bounds__(kThreads) void ln_partial_kernel(const T *__restrict__ xh,
                                                               const T *__restrict__ B, i64 Tn,
@@ -44,12 +103,9 @@ __global__ __launch_bounds__(kThreads) void ln_finish_kernel(const float *__rest
     const i64 n = blockIdx.x;
     float sq = 0.0f;
     for (i64 k = threadIdx.x; k < D; k += kThreads) {
-        float ag = 0.0f, ab = 0.0f;
-        for (int sp = 0; sp < splits; ++sp) {
-            const float *pg = part + ((i64)n * splits + sp) * 2 * D;
-            ag += pg[k];
-            ab += pg[D + k];
-        }
+        const float *pg = part + (i64)n * splits * 2 * D;
+        float ag = ordered_sum(pg + k, 2 * D, splits);
+        float ab = ordered_sum(pg + D + k, 2 * D, splits);
         ag *= scale;
         ab *= scale;
         gg[n * D + k] = ag;
@@ -103,7 +159,14 @@ extern "C" dp_status dp_grad_sample_layernorm(const void *xhat, const void *B, d
     float *part = (float *)ws;
     if (T > 0) {
         const dim3 grid((unsigned)(N * splits));
-        if (dt == DP_F32)
+        const bool vec = D % 4 == 0 && aligned(xhat, dt == DP_F32 ? 16 : 8) && aligned(B, dt == DP_F32 ? 16 : 8);
+        if (vec && dt == DP_F32)
+            ln_partial_vec_kernel<float><<<grid, kThreads, 0, stream>>>((const float *)xhat, (const float *)B,
+                                                                        T, D, splits, per, part);
+        else if (vec)
+            ln_partial_vec_kernel<uint16_t><<<grid, kThreads, 0, stream>>>(
+                (const uint16_t *)xhat, (const uint16_t *)B, T, D, splits, per, part);
+        else if (dt == DP_F32)
             ln_partial_kernel<float><<<grid, kThreads, 0, stream>>>((const float *)xhat, (const float *)B,
                                                                     T, D, splits, per, part);
         else

@@ -14,6 +14,7 @@
 // and a second kernel adds them in split order (no atomics).
 #include "common.hpp"
 #include "mfma_tile.hpp"
+#include "linear_bf16.hpp"
 
 namespace dpg {
 namespace {
@@ -110,8 +111,9 @@ __global__ __launch_bounds__(kThreads) void per_sample_gemm_kernel(
     __shared__ float As[kBK * kBM];
     __shared__ float Bs[kBK * kBN];
     __shared__ float red[16];
-    const i64 n = blockIdx.x / tiles;
-    const int tile = blockIdx.x % tiles;
+    const i64 bsw = xcd_swizzle(blockIdx.x, gridDim.x);
+    const i64 n = bsw / tiles;
+    const int tile = (int)(bsw % tiles);
     const int tm = tile / tiles_n, tn = tile % tiles_n;
     const i64 m0 = (i64)tm * kBM, n0 = (i64)tn * kBN;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -163,17 +165,6 @@ __global__ __launch_bounds__(kThreads) void per_sample_gemm_kernel(
     if (partial && tid == 0) partial[n * tiles + tile] = sq;
 }
 
-// sqnorm[n] = sum of the sample's tile partials, in tile order.
-__global__ void reduce_partials_kernel(const float *__restrict__ partial, i64 N, int tiles,
-                                       float *__restrict__ sqnorm)
-{
-    const i64 n = (i64)blockIdx.x * blockDim.x + threadIdx.x;
-    if (n >= N) return;
-    float s = 0.0f;
-    for (int t = 0; t < tiles; ++t) s += partial[n * tiles + t];
-    sqnorm[n] = s;
-}
-
 // ---------------------------------------------------------------------------
 // Fused clipped sum: block = (split, tile).  Rows of the flattened [N*T]
 // operands are scaled by s * c_n as they are staged.
@@ -188,8 +179,9 @@ __global__ __launch_bounds__(kThreads) void clipsum_gemm_kernel(
     __shared__ float As[kBK * kBM];
     __shared__ float Bs[kBK * kBN];
     __shared__ float rs[kBK];
-    const int split = blockIdx.x / tiles;
-    const int tile = blockIdx.x % tiles;
+    const i64 bsw = xcd_swizzle(blockIdx.x, gridDim.x);
+    const int split = (int)(bsw / tiles);
+    const int tile = (int)(bsw % tiles);
     const int tm = tile / tiles_n, tn = tile % tiles_n;
     const i64 m0 = (i64)tm * kBM, n0 = (i64)tn * kBN;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -242,7 +234,7 @@ __global__ void split_sum_kernel(const float *__restrict__ part, int splits, i64
     const i64 e = (i64)blockIdx.x * blockDim.x + threadIdx.x;
     if (e >= count) return;
     float s = 0.0f;
-    for (int k = 0; k < splits; ++k) s += part[(i64)k * count + e];
+    s = ordered_sum(part + e, count, splits);
     out[e] = s;
 }
 
@@ -286,6 +278,7 @@ extern "C" size_t dp_grad_sample_linear_workspace_bytes(int64_t N, int64_t T, in
 {
     (void)dt;
     if (N <= 0 || T <= 1 || d_in <= 0 || d_out <= 0) return 0;
+    // enough for either path (the 64x64 fp32-MFMA tiles outnumber the 128x128 bf16 ones)
     const i64 tiles = ceil_div(d_in, kBN) * ceil_div(d_out, kBM);
     return (size_t)(N * tiles) * sizeof(float);
 }
@@ -336,9 +329,15 @@ extern "C" dp_status dp_grad_sample_linear(const void *A, const void *B, dp_dtyp
         return launch_status();
     }
 
+    float *partial = sqnorm ? (float *)ws : nullptr;
+    if (dt == DP_BF16 && bf16_path_ok(A, B, gW, T, d_in, d_out)) {
+        bf16_grad_sample(A, B, N, T, d_in, d_out, scale, gW, gb, partial, stream);
+        if (sqnorm)
+            sum_partials(partial, N, bf16_tiles(d_in, d_out), sqnorm, stream);
+        return launch_status();
+    }
     const int tiles_n = (int)ceil_div(d_in, kBN);
     const int tiles = (int)ceil_div(d_out, kBM) * tiles_n;
-    float *partial = sqnorm ? (float *)ws : nullptr;
     const dim3 grid((unsigned)(N * tiles));
     if (dt == DP_F32)
         per_sample_gemm_kernel<float><<<grid, kThreads, 0, stream>>>(
@@ -347,18 +346,21 @@ extern "C" dp_status dp_grad_sample_linear(const void *A, const void *B, dp_dtyp
         per_sample_gemm_kernel<uint16_t><<<grid, kThreads, 0, stream>>>(
             (const uint16_t *)A, (const uint16_t *)B, T, d_in, d_out, tiles_n, tiles, scale, gW, gb, partial);
     if (sqnorm)
-        reduce_partials_kernel<<<(unsigned)ceil_div(N, 256), 256, 0, stream>>>(partial, N, tiles, sqnorm);
+        sum_partials(partial, N, tiles, sqnorm, stream);
     return launch_status();
 }
 
 extern "C" size_t dp_clip_accumulate_linear_workspace_bytes(int64_t N, int64_t T, int64_t d_in,
                                                             int64_t d_out, dp_dtype dt)
 {
-    (void)dt;
     if (N <= 0 || T <= 0 || d_in <= 0 || d_out <= 0) return 0;
     const ClipSplit s = clip_split(N, T, d_in, d_out);
-    if (s.splits <= 1) return 0;
-    return (size_t)s.splits * (size_t)(d_out * d_in + d_out) * sizeof(float);
+    size_t need = s.splits > 1 ? (size_t)s.splits * (size_t)(d_out * d_in + d_out) * sizeof(float) : 0;
+    if (dt == DP_BF16) {
+        const size_t b = bf16_clip_workspace(N, T, d_in, d_out);
+        if (b > need) need = b;
+    }
+    return need;
 }
 
 extern "C" dp_status dp_clip_accumulate_linear(const void *A, const void *B, dp_dtype dt,
@@ -377,6 +379,10 @@ extern "C" dp_status dp_clip_accumulate_linear(const void *A, const void *B, dp_
     if (N * T == 0) {
         zero_fill(sumW, d_out * d_in, stream);
         zero_fill(sumb, d_out, stream);
+        return launch_status();
+    }
+    if (dt == DP_BF16 && bf16_path_ok(A, B, sumW, T, d_in, d_out) && (sumb == nullptr || aligned(sumb, 4))) {
+        bf16_clip_accumulate(A, B, N, T, d_in, d_out, scale, norm, C, sumW, sumb, ws, stream);
         return launch_status();
     }
     const ClipSplit s = clip_split(N, T, d_in, d_out);

@@ -34,6 +34,7 @@ HBM_BYTES_PER_S = 8.0e12
 # fused route adds (the GEMM and its split reduction) next to the grouped
 # column reduction, which is shared by all tensors.
 FUSED_FLOPS_PER_S = {W.F32: 157.3e12, W.BF16: 157.3e12}
+BF16_FLOPS_PER_S = 2.5e15   # bf16 inputs with T > 1 and feature sizes that are multiples of 8
 LAUNCH_S = 3e-6
 
 
@@ -71,7 +72,9 @@ def to_device(a: np.ndarray, dtype: str, device):
 def linear_clip_mode(layer: W.Linear, N: int, dtype: str) -> str:
     """'fused' (B^T diag(c) A from A and B) or 'colreduce' (read the stored grads)."""
     elt = 2 if dtype == W.BF16 else 4
-    fused = (2.0 * N * layer.T * layer.d_in * layer.d_out / FUSED_FLOPS_PER_S[dtype]
+    bf16_mfma = dtype == W.BF16 and layer.T > 1 and layer.d_in % 8 == 0 and layer.d_out % 8 == 0
+    peak = BF16_FLOPS_PER_S if bf16_mfma else FUSED_FLOPS_PER_S[dtype]
+    fused = (2.0 * N * layer.T * layer.d_in * layer.d_out / peak
              + N * layer.T * (layer.d_in + layer.d_out) * elt / HBM_BYTES_PER_S + 2 * LAUNCH_S)
     col = N * layer.n_params * 4 / HBM_BYTES_PER_S
     return "fused" if fused < col else "colreduce"

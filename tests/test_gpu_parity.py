@@ -113,7 +113,9 @@ def test_add_noise_matches_oracle_and_is_resumable():
 
 
 LINEAR_SHAPES = [(1, 1, 1, 1), (3, 1, 37, 13), (2, 2, 5, 3), (4, 5, 37, 13), (3, 33, 65, 70),
-                 (2, 70, 130, 64), (5, 1, 4096, 10), (2, 17, 3, 129)]
+                 (2, 70, 130, 64), (5, 1, 4096, 10), (2, 17, 3, 129),
+                 # feature sizes that are multiples of 8: the bf16 MFMA path for bf16 inputs
+                 (1, 2, 8, 8), (3, 33, 136, 72), (2, 130, 264, 392), (2, 64, 128, 128), (9, 16, 256, 24)]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -287,6 +289,18 @@ def test_layernorm_and_empty_inputs():
     assert_g12(g.cpu().numpy(), rg, 1e-4, "ggamma")
     assert_g12(b.cpu().numpy(), rb, 1e-4, "gbeta")
     assert_rel(sq.cpu().numpy(), (rg ** 2).sum(1) + (rb ** 2).sum(1), 1e-4, "ln sqnorm")
+    # the vector path (D % 4 == 0), bf16 and fp32, with a position count that is not a multiple of 4
+    for dtype in (torch.float32, torch.bfloat16):
+        N2, T2, D2 = 3, 41, 1028
+        xh2 = torch.from_numpy(r.standard_normal((N2, T2, D2)).astype(np.float32)).to(dtype)
+        B2 = torch.from_numpy(r.standard_normal((N2, T2, D2)).astype(np.float32)).to(dtype)
+        g2 = torch.empty((N2, D2), device=DEV); b2 = torch.empty((N2, D2), device=DEV)
+        ws2 = torch.empty(dp.dp_grad_sample_layernorm_workspace_bytes(N2, T2, D2), dtype=torch.uint8, device=DEV)
+        dt2 = dp.DP_BF16 if dtype == torch.bfloat16 else dp.DP_F32
+        dp.dp_grad_sample_layernorm(xh2.to(DEV), B2.to(DEV), dt2, N2, T2, D2, 1.0, g2, b2, None, None, ws2)
+        rg2, rb2 = oracle.layernorm_grad(xh2.float().numpy(), B2.float().numpy(), 1.0)
+        assert_g12(g2.cpu().numpy(), rg2, 1e-4, "ggamma vec")
+        assert_g12(b2.cpu().numpy(), rb2, 1e-4, "gbeta vec")
     # T = 0: empty sums are zero
     say("linear T=0")
     gW = torch.full((2, 3, 4), 5.0, device=DEV); gbias = torch.full((2, 3), 5.0, device=DEV)
