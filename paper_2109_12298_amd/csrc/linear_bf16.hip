@@ -9,65 +9,43 @@
 // Layout.  MFMA rows run over j (d_in, the weight's contiguous index), MFMA
 // columns over i (d_out): each lane ends with four consecutive j of one row
 // and stores them as one float4.  Both operands arrive K-major ([t][feature],
-// feature contiguous) while the MFMA wants eight consecutive t per lane, so
-// staging loads 8x8 blocks (eight 16-byte rows of eight features), transposes
-// them in registers and writes eight 16-byte LDS rows with t contiguous.
-// LDS rows are padded by 16 bytes so the 16-byte operand reads of 16 lanes hit
-// distinct banks.
+// feature contiguous) and are copied into LDS unchanged, 16 bytes at a time.
+// The MFMA wants eight consecutive t per lane; gfx950's transposing LDS read
+// (ds_read_b64_tr_b16) delivers them: within each 16-lane group, source lane s
+// reads four features of row t0 + s/4 and lane i receives feature i of rows
+// t0..t0+3.  Two such reads (rows +0 and +4) form one 8-element operand.
+// The LDS row stride (320 bytes) puts the four rows of a read on distinct
+// banks.
 #include "common.hpp"
 
 namespace dpg {
 namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+typedef short i16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) i16x4_t lds_i16x4_t;
 
 constexpr int kThreads = 256;
-constexpr int TBM = 128;      // j per tile
-constexpr int TBN = 128;      // i per tile
-constexpr int TBK = 64;       // t per staged chunk
-constexpr int LDK = TBK + 8;  // LDS row stride in bf16 elements
+constexpr int TBM = 128;       // j per tile
+constexpr int TBN = 128;       // i per tile
+constexpr int TBK = 64;        // t per staged chunk
+constexpr int RS = 160;        // LDS row stride in bf16 elements (128 features + 32 pad)
+constexpr int kCopies = 8;     // 16-byte copies per thread per chunk (both operands)
 
-__device__ __forceinline__ uint32_t lo_pair(uint32_t a, uint32_t b) { return (a & 0xffffu) | (b << 16); }
-__device__ __forceinline__ uint32_t hi_pair(uint32_t a, uint32_t b) { return (a >> 16) | (b & 0xffff0000u); }
-
-// One operand chunk: rows t0..t0+TBK of a [T][ld] bf16 matrix, features
-// f0..f0+128.  Thread `slot` (0..127) owns the 8x8 block (t-block slot/16,
-// feature-block slot%16): load_8x8 fetches its eight 16-byte rows into
-// registers, store_8x8 transposes them and writes L[feature][t] (row stride
-// LDK).  Splitting the two lets the next chunk's loads fly during the MFMAs.
-struct Block8 {
-    uint4 r[8];
-};
-
-__device__ __forceinline__ void load_8x8(const uint16_t *__restrict__ src, i64 ld, i64 T, i64 t0, i64 F, i64 f0,
-                                         int slot, Block8 &in)
+// One 8-element MFMA operand (eight consecutive t of one feature per lane)
+// from a [t][RS] LDS tile: rows t_base.., features f_base..f_base+32.
+__device__ __forceinline__ bf16x8_t read_operand(const uint16_t *L, int t_base, int f_base, int lane)
 {
-    const int tb = slot >> 4, fb = slot & 15;
-    const i64 f = f0 + 8 * fb;
-#pragma unroll
-    for (int r = 0; r < 8; ++r) {
-        const i64 t = t0 + 8 * tb + r;
-        if (t < T && f < F) in.r[r] = *reinterpret_cast<const uint4 *>(src + t * ld + f);
-        else in.r[r] = make_uint4(0u, 0u, 0u, 0u);
-    }
-}
-
-__device__ __forceinline__ void store_8x8(const Block8 &in, int slot, uint16_t *L)
-{
-    const int tb = slot >> 4, fb = slot & 15;
-    // out[q] = the eight t-values of feature f+q, pairs (t=2w, 2w+1) per word
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-        uint32_t w[4];
-#pragma unroll
-        for (int p = 0; p < 4; ++p) {
-            const uint32_t *a = reinterpret_cast<const uint32_t *>(&in.r[2 * p]);
-            const uint32_t *b = reinterpret_cast<const uint32_t *>(&in.r[2 * p + 1]);
-            w[p] = (q & 1) ? hi_pair(a[q >> 1], b[q >> 1]) : lo_pair(a[q >> 1], b[q >> 1]);
-        }
-        *reinterpret_cast<uint4 *>(L + (8 * fb + q) * LDK + 8 * tb) = make_uint4(w[0], w[1], w[2], w[3]);
-    }
+    const int g = lane >> 4, s = lane & 15;
+    const int t = t_base + 8 * (g >> 1) + (s >> 2);
+    const int f = f_base + 16 * (g & 1) + 4 * (s & 3);
+    const uint16_t *p = L + t * RS + f;
+    const i16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t *)p);
+    const i16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t *)(p + 4 * RS));
+    const i16x8_t v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+    return __builtin_bit_cast(bf16x8_t, v);
 }
 
 struct Acc {
@@ -86,16 +64,13 @@ struct Acc {
 __device__ __forceinline__ void mma_chunk(const uint16_t *As, const uint16_t *Bs, int wm, int wn, int lane,
                                           Acc &acc)
 {
-    const int li = lane & 31, kg = lane >> 5;
 #pragma unroll
     for (int ks = 0; ks < TBK / 16; ++ks) {
         bf16x8_t a[2], b[2];
 #pragma unroll
-        for (int x = 0; x < 2; ++x)
-            a[x] = *reinterpret_cast<const bf16x8_t *>(As + (wm + 32 * x + li) * LDK + 16 * ks + 8 * kg);
+        for (int x = 0; x < 2; ++x) a[x] = read_operand(As, 16 * ks, wm + 32 * x, lane);
 #pragma unroll
-        for (int y = 0; y < 2; ++y)
-            b[y] = *reinterpret_cast<const bf16x8_t *>(Bs + (wn + 32 * y + li) * LDK + 16 * ks + 8 * kg);
+        for (int y = 0; y < 2; ++y) b[y] = read_operand(Bs, 16 * ks, wn + 32 * y, lane);
 #pragma unroll
         for (int x = 0; x < 2; ++x)
 #pragma unroll
@@ -104,29 +79,67 @@ __device__ __forceinline__ void mma_chunk(const uint16_t *As, const uint16_t *Bs
     }
 }
 
-// Threads 0..127 stage the activation operand (features j), 128..255 the
-// backprop operand (features i).
-__device__ __forceinline__ void load_chunk(const uint16_t *An, const uint16_t *Bn, i64 T, i64 t0, i64 din,
-                                           i64 dout, i64 m0, i64 n0, Block8 &in)
+// Staging.  Threads 0..127 copy the activation tile (features j), 128..255
+// the backprop tile (features i): copy k of thread `slot` is row slot/16 + 8k,
+// 16-byte column slot%16.  Rows past T or features past F (F % 8 == 0) read a
+// clamped valid address and are zeroed when written.
+struct Stage {
+    uint4 v[kCopies];
+};
+
+struct StageGeom {
+    const uint16_t *src;   // operand base of the current sample
+    i64 ld;                // row length (features)
+    i64 F, f0;             // feature count, first feature of the tile
+    uint16_t *L;           // LDS tile
+};
+
+__device__ __forceinline__ void stage_load(const StageGeom &sg, i64 T, i64 t0, Stage &st)
 {
-    const int tid = threadIdx.x;
-    if (tid < 128) load_8x8(An, din, T, t0, din, m0, tid, in);
-    else load_8x8(Bn, dout, T, t0, dout, n0, tid - 128, in);
+    const int slot = threadIdx.x & 127;
+    const int row0 = slot >> 4, col = slot & 15;
+    i64 f = sg.f0 + 8 * col;
+    f = f < sg.F ? f : sg.F - 8;
+#pragma unroll
+    for (int k = 0; k < kCopies; ++k) {
+        i64 t = t0 + row0 + 8 * k;
+        t = t < T ? t : T - 1;
+        st.v[k] = *reinterpret_cast<const uint4 *>(sg.src + t * sg.ld + f);
+    }
 }
 
-__device__ __forceinline__ void store_chunk(const Block8 &in, uint16_t *As, uint16_t *Bs)
+__device__ __forceinline__ void stage_store(const StageGeom &sg, i64 T, i64 t0, const Stage &st)
 {
-    const int tid = threadIdx.x;
-    if (tid < 128) store_8x8(in, tid, As);
-    else store_8x8(in, tid - 128, Bs);
+    const int slot = threadIdx.x & 127;
+    const int row0 = slot >> 4, col = slot & 15;
+    const bool fok = sg.f0 + 8 * col < sg.F;
+#pragma unroll
+    for (int k = 0; k < kCopies; ++k) {
+        const int row = row0 + 8 * k;
+        const bool ok = fok && t0 + row < T;
+        *reinterpret_cast<uint4 *>(sg.L + row * RS + 8 * col) = ok ? st.v[k] : make_uint4(0u, 0u, 0u, 0u);
+    }
 }
 
-__device__ __forceinline__ float bias_chunk(const uint16_t *Bs, int row)
+__device__ __forceinline__ float bias_chunk(const uint16_t *Bs, int feature)
 {
     float s = 0.0f;
 #pragma unroll 8
-    for (int t = 0; t < TBK; ++t) s += bf16_to_f32(Bs[row * LDK + t]);
+    for (int t = 0; t < TBK; ++t) s += bf16_to_f32(Bs[t * RS + feature]);
     return s;
+}
+
+__device__ __forceinline__ StageGeom geom_for(const uint16_t *An, const uint16_t *Bn, i64 din, i64 dout, i64 m0,
+                                              i64 n0, uint16_t *As, uint16_t *Bs)
+{
+    const bool isA = threadIdx.x < 128;   // uniform per wave
+    StageGeom g;
+    g.src = isA ? An : Bn;
+    g.ld = isA ? din : dout;
+    g.F = g.ld;
+    g.f0 = isA ? m0 : n0;
+    g.L = isA ? As : Bs;
+    return g;
 }
 
 // Per-sample gradients.  Block = (sample, j-tile, i-tile).
@@ -134,8 +147,8 @@ __global__ __launch_bounds__(kThreads) void bf16_per_sample_kernel(
     const uint16_t *__restrict__ A, const uint16_t *__restrict__ B, i64 T, i64 din, i64 dout, int tiles_m,
     int tiles, float scale, float *__restrict__ gW, float *__restrict__ gb, float *__restrict__ partial)
 {
-    __shared__ uint16_t As[TBM * LDK];
-    __shared__ uint16_t Bs[TBN * LDK];
+    __shared__ uint16_t As[TBK * RS];
+    __shared__ uint16_t Bs[TBK * RS];
     __shared__ float red[16];
     const i64 b = xcd_swizzle(blockIdx.x, gridDim.x);
     const i64 n = b / tiles;
@@ -144,28 +157,27 @@ __global__ __launch_bounds__(kThreads) void bf16_per_sample_kernel(
     const i64 m0 = (i64)tm * TBM, n0 = (i64)tn * TBN;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = (wave >> 1) * 64, wn = (wave & 1) * 64;
-    const uint16_t *An = A + n * T * din;
-    const uint16_t *Bn = B + n * T * dout;
     const bool do_bias = gb != nullptr && tm == 0;
+    const StageGeom sg = geom_for(A + n * T * din, B + n * T * dout, din, dout, m0, n0, As, Bs);
 
     Acc acc;
     acc.zero();
     float bias_acc = 0.0f;
     const int nchunks = (int)ceil_div(T, TBK);
-    // one LDS buffer (four workgroups fit a CU); the next chunk's global loads
-    // are in flight in registers while this chunk's MFMAs run
-    Block8 in;
-    load_chunk(An, Bn, T, 0, din, dout, m0, n0, in);
-    store_chunk(in, As, Bs);
+    // one LDS buffer (several workgroups per CU); the next chunk's loads are in
+    // flight in registers while this chunk's MFMAs run
+    Stage st;
+    stage_load(sg, T, 0, st);
+    stage_store(sg, T, 0, st);
     __syncthreads();
     for (int c = 0; c < nchunks; ++c) {
         const bool more = c + 1 < nchunks;
-        if (more) load_chunk(An, Bn, T, (i64)(c + 1) * TBK, din, dout, m0, n0, in);
+        if (more) stage_load(sg, T, (i64)(c + 1) * TBK, st);
         mma_chunk(As, Bs, wm, wn, lane, acc);
         if (do_bias && tid < TBN) bias_acc += bias_chunk(Bs, tid);
         if (more) {
             __syncthreads();
-            store_chunk(in, As, Bs);
+            stage_store(sg, T, (i64)(c + 1) * TBK, st);
             __syncthreads();
         }
     }
@@ -205,8 +217,8 @@ __global__ __launch_bounds__(kThreads) void bf16_clipsum_kernel(
     int tiles_m, int tiles, i64 per_split, float scale, const float *__restrict__ norm, float C,
     float *__restrict__ outW, float *__restrict__ outb, i64 strideW, i64 strideb)
 {
-    __shared__ uint16_t As[TBM * LDK];
-    __shared__ uint16_t Bs[TBN * LDK];
+    __shared__ uint16_t As[TBK * RS];
+    __shared__ uint16_t Bs[TBK * RS];
     const i64 bb = xcd_swizzle(blockIdx.x, gridDim.x);
     const int split = (int)(bb / tiles);
     const int tile = (int)(bb % tiles);
@@ -223,26 +235,36 @@ __global__ __launch_bounds__(kThreads) void bf16_clipsum_kernel(
     acc.zero();
     float bias_tot = 0.0f, bias_acc = 0.0f;
     // (sample, chunk) pairs of this range, flattened so loads run ahead across samples
+    // (no 64-bit division in the loop: the sample and chunk advance as counters)
     const int cps = (int)ceil_div(T, TBK);
-    const i64 total = (s1 - s0) * cps;
-    Block8 in;
+    const int total = (int)(s1 - s0) * cps;
+    const StageGeom sg0 = geom_for(A, B, din, dout, m0, n0, As, Bs);
+    const i64 sstride = T * sg0.ld;   // elements between two samples of this thread's operand
+    Stage st;
+    StageGeom sgn = sg0;
+    sgn.src += s0 * sstride;
     if (total > 0) {
-        load_chunk(A + s0 * T * din, B + s0 * T * dout, T, 0, din, dout, m0, n0, in);
-        store_chunk(in, As, Bs);
+        stage_load(sgn, T, 0, st);
+        stage_store(sgn, T, 0, st);
     }
     __syncthreads();
-    for (i64 c = 0; c < total; ++c) {
+    i64 cur_sample = s0;          // sample of chunk c
+    int nxt_chunk = 1;            // chunk-in-sample of chunk c + 1
+    for (int c = 0; c < total; ++c) {
         const bool more = c + 1 < total;
-        if (more) {
-            const i64 nn = s0 + (c + 1) / cps;
-            const i64 t0 = (i64)((c + 1) % cps) * TBK;
-            load_chunk(A + nn * T * din, B + nn * T * dout, T, t0, din, dout, m0, n0, in);
+        const bool sample_done = nxt_chunk == cps;
+        if (sample_done) {
+            nxt_chunk = 0;
+            sgn.src += sstride;
         }
+        const i64 tn0 = (i64)nxt_chunk * TBK;
+        if (more) stage_load(sgn, T, tn0, st);
         mma_chunk(As, Bs, wm, wn, lane, acc);
         if (do_bias && tid < TBN) bias_acc += bias_chunk(Bs, tid);
-        if ((c + 1) % cps == 0) {
+        if (sample_done) {
             // the sample's product is complete: add it with its clip factor
-            const float cs = scale * clip_factor(norm[s0 + c / cps], C);
+            const float cs = scale * clip_factor(norm[cur_sample], C);
+            ++cur_sample;
 #pragma unroll
             for (int x = 0; x < 2; ++x)
 #pragma unroll
@@ -257,9 +279,10 @@ __global__ __launch_bounds__(kThreads) void bf16_clipsum_kernel(
         }
         if (more) {
             __syncthreads();
-            store_chunk(in, As, Bs);
+            stage_store(sgn, T, tn0, st);
             __syncthreads();
         }
+        ++nxt_chunk;
     }
 
     float *O = outW + (i64)split * strideW;

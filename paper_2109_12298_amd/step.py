@@ -28,13 +28,15 @@ import numpy as np
 from . import binding as dp
 from . import workloads as W
 
-HBM_BYTES_PER_S = 8.0e12
-# Matrix-core peak used by the clipped-sum cost model (the fused GEMM runs on
-# fp32 MFMA for both input dtypes), and the cost of the extra launches the
-# fused route adds (the GEMM and its split reduction) next to the grouped
-# column reduction, which is shared by all tensors.
-FUSED_FLOPS_PER_S = {W.F32: 157.3e12, W.BF16: 157.3e12}
-BF16_FLOPS_PER_S = 2.5e15   # bf16 inputs with T > 1 and feature sizes that are multiples of 8
+# Effective rates measured on MI355X for the clipped-sum route choice (not
+# spec peaks): the column reduction streams at ~4.5 TB/s; the fused GEMM
+# reaches ~60 TFLOP/s on fp32 MFMA and ~190 TFLOP/s on the bf16 MFMA path
+# (it is latency-bound at these tile counts); each extra launch of the fused
+# route (the GEMM and its split reduction) costs ~3 us next to the grouped
+# column reduction, which all tensors share.
+HBM_BYTES_PER_S = 4.5e12
+FUSED_FLOPS_PER_S = {W.F32: 60e12, W.BF16: 60e12}
+BF16_FLOPS_PER_S = 190e12   # bf16 inputs with T > 1 and feature sizes that are multiples of 8
 LAUNCH_S = 3e-6
 
 
