@@ -1,0 +1,138 @@
+"""Parity at the full workload sizes, in the launch configuration the benchmark
+times (one captured HIP graph with parallel layer branches, replayed), on
+sampled outputs the oracle computes one at a time:
+
+  - per-sample gradients, per-layer squared norms and norms of sampled samples
+    (the oracle runs on those samples' inputs only);
+  - clipped sums at sampled weight elements: the oracle forms that element's
+    per-sample gradients for every sample from the element's slice of the
+    inputs, and adds them with the clip factors of the device norms (which
+    are themselves checked above on the sampled samples);
+  - noised outputs at sampled elements, through the oracle's Philox stream.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from compare import RTOL, assert_g12, assert_rel
+from paper_2109_12298_amd import workloads as W
+from paper_2109_12298_amd.step import DPStep
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def say(*a):
+    print("[case]", *a, file=sys.stderr, flush=True)
+
+
+def device_values(wl, a):
+    return None if a is None else W.rounded_like_device(wl, a).astype(np.float64)
+
+
+def sub_inputs(wl, inputs, idx):
+    out = []
+    for li in inputs:
+        out.append(W.LayerInputs(li.layer, A=None if li.A is None else li.A[idx],
+                                 B=li.B[idx], ids=None if li.ids is None else li.ids[idx]))
+    return out
+
+
+def element_grads(wl, li, key, index, scale):
+    """Per-sample gradient of one parameter element for every sample (oracle, sliced inputs)."""
+    layer = li.layer
+    A = device_values(wl, li.A)
+    B = device_values(wl, li.B)
+    if isinstance(layer, W.Linear):
+        if A.ndim == 2:
+            A = A[:, None, :]
+            B = B[:, None, :]
+        if key == "bias":
+            (i,) = index
+            _, gb = oracle.linear_grad(A[:, :, :1], B[:, :, i:i + 1], scale)
+            return gb[:, 0]
+        i, j = index
+        gW, _ = oracle.linear_grad(A[:, :, j:j + 1], B[:, :, i:i + 1], scale, bias=False)
+        return gW[:, 0, 0]
+    if isinstance(layer, W.Conv2d):
+        if key == "bias":
+            (co,) = index
+            _, gb = oracle.conv2d_grad(A[:, :1], B[:, co:co + 1], layer.k, layer.stride, layer.pad, scale)
+            return gb[:, 0]
+        co, ci, u, v = index
+        gW, _ = oracle.conv2d_grad(A[:, ci:ci + 1], B[:, co:co + 1], layer.k, layer.stride, layer.pad, scale,
+                                   bias=False)
+        return gW[:, 0, 0, u, v]
+    if isinstance(layer, W.LayerNorm):
+        (k,) = index
+        gg, gbt = oracle.layernorm_grad(A[:, :, k:k + 1], B[:, :, k:k + 1], scale)
+        return (gg if key == "weight" else gbt)[:, 0]
+    if isinstance(layer, W.Embedding):
+        v, d = index
+        N = li.ids.shape[0]
+        g = np.zeros(N)
+        for n in range(N):
+            hit = li.ids[n] == v
+            g[n] = scale * B[n][hit, d].sum() if hit.any() else 0.0
+        return g
+    raise TypeError(layer)
+
+
+@pytest.mark.parametrize("name", ["linear_tiny", "mnist_cnn", "cifar_cnn", "text_lstm", "transformer_block"])
+def test_full_size_sampled_parity(name):
+    wl = W.get(name)
+    rtol = RTOL[wl.dtype]
+    say("full size", name, "drawing inputs")
+    inputs = W.make_inputs(wl)
+    N = wl.N
+    st = DPStep(wl, inputs, DEV)
+    step = 11
+    st.capture(first_step=step)
+    st.replay()
+    torch.cuda.synchronize()
+    say("full size", name, "replayed step", step)
+    assert int(st.status.item()) == 0
+    norm_dev = st.norm.cpu().numpy().astype(np.float64)
+    sq_dev = st.sqnorm.cpu().numpy()
+    r = np.random.default_rng(123)
+    samples = sorted({0, N - 1, int(r.integers(0, N))})
+
+    # per-sample gradients, squared norms, norms of the sampled samples
+    ref = oracle.dp_step(wl, sub_inputs(wl, inputs, samples), step=step, denom=float(N), noise=False)
+    for k, n in enumerate(samples):
+        for li_idx, (lb, g_ref) in enumerate(zip(st.layers, ref["grads"])):
+            if "csr" in g_ref:
+                rp, uq, rows = g_ref["csr"]
+                rp_dev = lb.row_ptr.cpu().numpy()
+                lo, hi = int(rp_dev[n]), int(rp_dev[n + 1])
+                np.testing.assert_array_equal(lb.uniq[lo:hi].cpu().numpy(), uq[rp[k]:rp[k + 1]])
+                assert_g12(lb.rows[lo:hi].cpu().numpy(), rows[rp[k]:rp[k + 1]], rtol, "emb rows")
+            else:
+                assert_g12(lb.gW[n].cpu().numpy(), g_ref["weight"][k], rtol, "%s weight n=%d" % (lb.layer.name, n))
+                if "bias" in g_ref:
+                    assert_g12(lb.gb[n].cpu().numpy(), g_ref["bias"][k], rtol, "%s bias n=%d" % (lb.layer.name, n))
+        assert_rel(sq_dev[:, n], ref["sq_layers"][:, k], rtol, "sqnorm n=%d" % n)
+        assert_rel(norm_dev[n], ref["norm"][k], rtol, "norm n=%d" % n)
+
+    # clipped sums and noised outputs at sampled elements
+    c = oracle.clip_factors(norm_dev.astype(np.float32).astype(np.float64), wl.C)
+    params = wl.param_tensors()
+    for pidx, (pname, shape) in enumerate(params):
+        lname, key = pname.rsplit(".", 1)
+        li = next(x for x in inputs if x.layer.name == lname)
+        numel = int(np.prod(shape))
+        flat_idx = sorted({0, numel - 1} | {int(e) for e in r.integers(0, numel, 3)})
+        S_dev = st.S[pname].reshape(-1)[flat_idx].cpu().numpy()
+        out_dev = st.out[pname].reshape(-1)[flat_idx].cpu().numpy()
+        S_ref = np.array([np.dot(c, element_grads(wl, li, key, np.unravel_index(e, shape), wl.scale))
+                          for e in flat_idx])
+        _, z = oracle.philox_normals(numel, wl.seed, step, pidx)
+        out_ref = (S_ref + wl.sigma * wl.C * z[flat_idx]) / float(N)
+        # sums of many terms near zero: judge against the magnitude of the terms
+        scale_S = max(float(np.max(np.abs(S_ref))), 1e-30)
+        assert np.max(np.abs(S_dev - S_ref)) <= rtol * (scale_S + np.abs(S_ref)).max(), (pname, S_dev, S_ref)
+        assert_g12(out_dev, out_ref, rtol, "out " + pname)
+    say("full size", name, "ok")
