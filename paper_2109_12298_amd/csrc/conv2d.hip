@@ -52,7 +52,23 @@ struct ConvGeom {
     int tiles_m, tiles_n, tiles;
     int vec;             // float4 stores allowed (KK % 4 == 0 and gW 16-byte aligned)
     int bk;              // positions per staged chunk (multiple of 8)
+    float inv_plane, inv_wp, inv_bk, inv_wo;   // reciprocals for divmod
 };
+
+// q = x / d, r = x % d for 0 <= x < 2^22 via a float reciprocal, corrected to
+// the exact quotient (the float estimate is off by at most one)
+__device__ __forceinline__ void divmod(int x, int d, float inv_d, int &q, int &r)
+{
+    q = (int)((float)x * inv_d);
+    r = x - q * d;
+    if (r < 0) {
+        --q;
+        r += d;
+    } else if (r >= d) {
+        ++q;
+        r -= d;
+    }
+}
 
 template <typename T, int FM, int FN, int WM, int WN, int WK>
 __global__ __launch_bounds__(kThreads) void conv_per_sample_kernel(
@@ -94,10 +110,9 @@ __global__ __launch_bounds__(kThreads) void conv_per_sample_kernel(
             const int idx = i0 + j * kThreads;
             v[j] = 0.0f;
             if (idx < xtotal) {
-                const int c = idx / g.plane;
-                const int rem = idx - c * g.plane;
-                const int r = rem / g.Wp;
-                const int q = rem - r * g.Wp;
+                int c, rem, r, q;
+                divmod(idx, g.plane, g.inv_plane, c, rem);
+                divmod(rem, g.Wp, g.inv_wp, r, q);
                 const int ih = r - s.ph, iw = q - s.pw;
                 if (ih >= 0 && ih < s.H && iw >= 0 && iw < s.W)
                     v[j] = load_elem<T>(Xn, ((i64)(ci0 + c) * s.H + ih) * s.W + iw);
@@ -146,7 +161,8 @@ __global__ __launch_bounds__(kThreads) void conv_per_sample_kernel(
 #pragma unroll
             for (int j = 0; j < kStage; ++j) {
                 const int e = e0 + j * kThreads;
-                const int co = e / BK, p = e - co * BK;
+                int co, p;
+                divmod(e, BK, g.inv_bk, co, p);
                 at[j] = e < gtotal ? p * Cfg::LDG + co : -1;
                 v[j] = 0.0f;
                 if (e < gtotal && n0 + co < s.Cout && p0 + p < s.L)
@@ -160,13 +176,15 @@ __global__ __launch_bounds__(kThreads) void conv_per_sample_kernel(
             const int p = p0 + t;
             int o = 0;
             if (p < s.L) {
-                const int oh = p / s.Wo, ow = p - oh * s.Wo;
+                int oh, ow;
+                divmod(p, s.Wo, g.inv_wo, oh, ow);
                 o = oh * s.sh * g.Wp + ow * s.sw;
             }
             offp[t] = o;
         }
         __syncthreads();
         const int kpairs = (s.L - p0 < BK ? s.L - p0 + 1 : BK) >> 1;
+#pragma unroll 2
         for (int q = wk; q < kpairs; q += WK) {
             const int ks = 2 * q + (lane >> 5);
             const int op = offp[ks];
@@ -520,6 +538,12 @@ extern "C" dp_status dp_grad_sample_conv2d(const void *X, const void *GY, dp_dty
     const ConvShape s = make_shape(Cin, H, W, Cout, kh, kw, sh, sw, ph, pw);
     Plan p = plan_conv(s);
     p.g.vec = (s.KK % 4 == 0) && aligned(gW, 16);
+    if (p.cfg >= 0) {
+        p.g.inv_plane = 1.0f / (float)p.g.plane;
+        p.g.inv_wp = 1.0f / (float)p.g.Wp;
+        p.g.inv_bk = 1.0f / (float)p.g.bk;
+        p.g.inv_wo = 1.0f / (float)s.Wo;
+    }
     const int tiles = p.cfg >= 0 ? p.g.tiles : conv_tiles(s);
     const int direct = tiles == 1;
     float *sqout = sqnorm ? (direct ? sqnorm : (float *)ws) : nullptr;

@@ -60,39 +60,65 @@ __global__ __launch_bounds__(kThreads) void outer_kernel(const T *__restrict__ A
     const T *An = A + n * din;
     const T *Bn = B + n * dout;
     float *G = gW + n * dout * din;
-    // the block's backprop entries, scaled, in LDS (one load round trip)
-    for (i64 i = i0 + threadIdx.x; i < i1; i += kThreads) bsh[i - i0] = scale * load_elem<T>(Bn, i);
-    __syncthreads();
+    const bool do_norm = sqnorm != nullptr && rb == 0;
 
-    if (VEC) {
-        const i64 nv = din / 4;
-        for (i64 j4 = threadIdx.x; j4 < nv; j4 += kThreads) {
-            const float4 a = load4<T>(An, 4 * j4);
-            for (i64 i = i0; i < i1; ++i) {
-                const float b = bsh[i - i0];
-                float4 v = make_float4(b * a.x, b * a.y, b * a.z, b * a.w);
-                *reinterpret_cast<float4 *>(G + i * din + 4 * j4) = v;
-            }
-        }
-    } else {
-        for (i64 j = threadIdx.x; j < din; j += kThreads) {
-            const float a = load_elem<T>(An, j);
-            for (i64 i = i0; i < i1; ++i) G[i * din + j] = bsh[i - i0] * a;
+    // Every load of the block is issued before the one barrier: the sample's
+    // activation (kept in registers when it fits), the block's backprop rows
+    // (into LDS), and, for the norm, the whole backprop row.
+    constexpr int KA = 4;
+    const i64 nv = VEC ? din / 4 : 0;
+    const bool inreg = VEC && nv <= (i64)kThreads * KA;
+    float4 a[KA];
+    float na = 0.0f, nb = 0.0f;
+    if (inreg) {
+#pragma unroll
+        for (int k = 0; k < KA; ++k) {
+            const i64 j4 = threadIdx.x + (i64)k * kThreads;
+            a[k] = j4 < nv ? load4<T>(An, 4 * j4) : make_float4(0.f, 0.f, 0.f, 0.f);
         }
     }
-    if (gb) {
-        for (i64 i = i0 + threadIdx.x; i < i1; i += kThreads) gb[n * dout + i] = scale * load_elem<T>(Bn, i);
-    }
-    if (sqnorm && rb == 0) {
-        float na = 0.0f, nb = 0.0f;
-        for (i64 j = threadIdx.x; j < din; j += kThreads) {
-            const float a = load_elem<T>(An, j);
-            na += a * a;
-        }
+    if (do_norm) {
         for (i64 i = threadIdx.x; i < dout; i += kThreads) {
             const float b = load_elem<T>(Bn, i);
             nb += b * b;
         }
+    }
+    for (i64 i = i0 + threadIdx.x; i < i1; i += kThreads) bsh[i - i0] = scale * load_elem<T>(Bn, i);
+    __syncthreads();
+
+    if (inreg) {
+#pragma unroll
+        for (int k = 0; k < KA; ++k) {
+            const i64 j4 = threadIdx.x + (i64)k * kThreads;
+            if (j4 >= nv) break;
+            na += a[k].x * a[k].x + a[k].y * a[k].y + a[k].z * a[k].z + a[k].w * a[k].w;
+            for (i64 i = i0; i < i1; ++i) {
+                const float b = bsh[i - i0];
+                *reinterpret_cast<float4 *>(G + i * din + 4 * j4) =
+                    make_float4(b * a[k].x, b * a[k].y, b * a[k].z, b * a[k].w);
+            }
+        }
+    } else if (VEC) {
+        for (i64 j4 = threadIdx.x; j4 < nv; j4 += kThreads) {
+            const float4 av = load4<T>(An, 4 * j4);
+            na += av.x * av.x + av.y * av.y + av.z * av.z + av.w * av.w;
+            for (i64 i = i0; i < i1; ++i) {
+                const float b = bsh[i - i0];
+                *reinterpret_cast<float4 *>(G + i * din + 4 * j4) = make_float4(b * av.x, b * av.y, b * av.z, b * av.w);
+            }
+        }
+    } else {
+        for (i64 j = threadIdx.x; j < din; j += kThreads) {
+            const float av = load_elem<T>(An, j);
+            na += av * av;
+            for (i64 i = i0; i < i1; ++i) G[i * din + j] = bsh[i - i0] * av;
+        }
+    }
+    if (gb) {
+        for (i64 i = i0 + threadIdx.x; i < i1; i += kThreads) gb[n * dout + i] = bsh[i - i0];
+    }
+    if (do_norm) {
+        // closed form of the rank-one gradient: s^2 |B_n|^2 (|A_n|^2 + 1)
         na = block_sum(na, red);
         nb = block_sum(nb, red);
         if (threadIdx.x == 0) sqnorm[n] = scale * scale * nb * (na + (gb ? 1.0f : 0.0f));
