@@ -22,6 +22,8 @@
 #include "common.hpp"
 #include "mfma_tile.hpp"
 
+#include <type_traits>
+
 namespace dpg {
 namespace {
 
@@ -52,21 +54,60 @@ struct ConvGeom {
     int tiles_m, tiles_n, tiles;
     int vec;             // float4 stores allowed (KK % 4 == 0 and gW 16-byte aligned)
     int bk;              // positions per staged chunk (multiple of 8)
-    float inv_plane, inv_wp, inv_bk, inv_wo;   // reciprocals for divmod
+    int one;             // whole sample staged with one load per register (see kOneX, kOneG)
+    int xvec, gvec;      // one-shot staging may use float4 loads of X / GY
+    int rowstep;         // sh * Wp: padded-plane offset of one output row
+    float inv_plane, inv_wp, inv_bk, inv_wo, inv_hw, inv_w, inv_l;   // reciprocals for divmod
 };
 
+// elements per thread held in registers by the one-shot staging
+constexpr int kOneX = 16;
+constexpr int kOneG = 16;
+
 // q = x / d, r = x % d for 0 <= x < 2^22 via a float reciprocal, corrected to
-// the exact quotient (the float estimate is off by at most one)
+// the exact quotient without branches (the float estimate is off by at most one)
 __device__ __forceinline__ void divmod(int x, int d, float inv_d, int &q, int &r)
 {
     q = (int)((float)x * inv_d);
     r = x - q * d;
-    if (r < 0) {
-        --q;
-        r += d;
-    } else if (r >= d) {
-        ++q;
-        r -= d;
+    q += (r >= d ? 1 : 0) - (r < 0 ? 1 : 0);
+    r = x - q * d;
+}
+
+// Flat element held in register j by thread tid of a one-shot load.
+__device__ __forceinline__ int flat_at(int j, int tid, bool vec)
+{
+    return vec ? 4 * (tid + (j >> 2) * kThreads) + (j & 3) : tid + j * kThreads;
+}
+
+// Loads elements [0, count) of src (count >= 1) into registers, all loads
+// issued before any is used; addresses past the end are clamped and their
+// values zeroed, so there is no branch.  vec: float4 loads (count % 4 == 0,
+// src 16-byte aligned).
+template <int EPT, typename T>
+__device__ __forceinline__ void flat_load(const T *__restrict__ src, int count, bool vec, int tid, float (&v)[EPT])
+{
+    if constexpr (std::is_same<T, float>::value) {
+        if (vec) {
+#pragma unroll
+            for (int j = 0; j < EPT / 4; ++j) {
+                const int e = 4 * (tid + j * kThreads);
+                const int ec = e < count ? e : count - 4;
+                const float4 q = *reinterpret_cast<const float4 *>(src + ec);
+                const bool ok = e < count;
+                v[4 * j + 0] = ok ? q.x : 0.0f;
+                v[4 * j + 1] = ok ? q.y : 0.0f;
+                v[4 * j + 2] = ok ? q.z : 0.0f;
+                v[4 * j + 3] = ok ? q.w : 0.0f;
+            }
+            return;
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < EPT; ++j) {
+        const int e = tid + j * kThreads;
+        const float x = load_elem<T>(src, e < count ? e : count - 1);
+        v[j] = e < count ? x : 0.0f;
     }
 }
 
@@ -78,6 +119,7 @@ __global__ __launch_bounds__(kThreads) void conv_per_sample_kernel(
     using Cfg = ConvTile<FM, FN, WM, WN, WK>;
     extern __shared__ float lds[];
     __shared__ float red16[16];
+    __shared__ float bpart[kThreads];
 
     const i64 bsw = xcd_swizzle(blockIdx.x, gridDim.x);
     const int n = (int)(bsw / g.tiles);
@@ -93,35 +135,78 @@ __global__ __launch_bounds__(kThreads) void conv_per_sample_kernel(
     const int BK = g.bk;
     float *Xs = lds;
     float *Gs = lds + g.nplanes * g.plane;
-    int *offp = reinterpret_cast<int *>(Gs + BK * Cfg::LDG);
 
-    // ---- stage the input planes this kk-tile reads, zero halo included
     const int ci0 = m0 / s.khw;
     int ci1 = (m0 + Cfg::BM - 1) / s.khw + 1;
     if (ci1 > s.Cin) ci1 = s.Cin;
     const int np = ci1 - ci0;
-    const T *Xn = X + (i64)n * s.Cin * s.H * s.W;
-    // kStage loads in flight per thread before any is written to LDS
-    const int xtotal = np * g.plane;
-    for (int i0 = tid; i0 < xtotal; i0 += kThreads * kStage) {
-        float v[kStage];
+    const int nco = s.Cout - n0 < Cfg::BN ? s.Cout - n0 : Cfg::BN;
+    const int HW = s.H * s.W;
+    const T *Xn = X + (i64)n * s.Cin * HW;
+    const T *Gn = GY + (i64)n * s.Cout * s.L;
+    const bool pad = (s.ph | s.pw) != 0;
+
+    if (g.one) {
+        // ---- whole sample in one round trip: every load of X and GY is in
+        // flight before the first is written to LDS
+        float xv[kOneX], gv[kOneG];
+        const int xcount = np * HW, gcount = nco * s.L;
+        flat_load<kOneX>(Xn + (i64)ci0 * HW, xcount, g.xvec != 0, tid, xv);
+        flat_load<kOneG>(Gn + (i64)n0 * s.L, gcount, g.gvec != 0, tid, gv);
+        if (pad) {   // zero halo (disjoint from the interior written below)
+            float *trash = Gs + BK * Cfg::LDG;
+            for (int idx = tid; idx < np * g.plane; idx += kThreads) {
+                int c, rem, r, q;
+                divmod(idx, g.plane, g.inv_plane, c, rem);
+                divmod(rem, g.Wp, g.inv_wp, r, q);
+                const bool halo = r < s.ph || r >= s.ph + s.H || q < s.pw || q >= s.pw + s.W;
+                *(halo ? Xs + idx : trash + lane) = 0.0f;
+            }
+        }
+        if ((s.L & 1) && tid < Cfg::BN) Gs[s.L * Cfg::LDG + tid] = 0.0f;   // odd tail of the last position pair
+        // registers past the end go to this lane's slot of a trash row
+        float *trash = Gs + BK * Cfg::LDG;
 #pragma unroll
-        for (int j = 0; j < kStage; ++j) {
-            const int idx = i0 + j * kThreads;
-            v[j] = 0.0f;
-            if (idx < xtotal) {
+        for (int j = 0; j < kOneX; ++j) {
+            const int e = flat_at(j, tid, g.xvec != 0);
+            int c, rem, ih, iw;
+            divmod(e, HW, g.inv_hw, c, rem);
+            divmod(rem, s.W, g.inv_w, ih, iw);
+            float *dst = e < xcount ? Xs + c * g.plane + (ih + s.ph) * g.Wp + iw + s.pw : trash + lane;
+            *dst = xv[j];
+        }
+#pragma unroll
+        for (int j = 0; j < kOneG; ++j) {
+            const int e = flat_at(j, tid, g.gvec != 0);
+            int co, p;
+            divmod(e, s.L, g.inv_l, co, p);
+            float *dst = e < gcount ? Gs + p * Cfg::LDG + co : trash + lane;
+            *dst = gv[j];
+        }
+    } else {
+        // ---- stage the input planes this kk-tile reads, zero halo included;
+        // kStage loads in flight per thread before any is written to LDS
+        const int xtotal = np * g.plane;
+        const T *Xc = Xn + (i64)ci0 * HW;
+        float *trash = Gs + BK * Cfg::LDG;
+        for (int i0 = tid; i0 < xtotal; i0 += kThreads * kStage) {
+            float v[kStage];
+#pragma unroll
+            for (int j = 0; j < kStage; ++j) {
+                const int idx = i0 + j * kThreads;
                 int c, rem, r, q;
                 divmod(idx, g.plane, g.inv_plane, c, rem);
                 divmod(rem, g.Wp, g.inv_wp, r, q);
                 const int ih = r - s.ph, iw = q - s.pw;
-                if (ih >= 0 && ih < s.H && iw >= 0 && iw < s.W)
-                    v[j] = load_elem<T>(Xn, ((i64)(ci0 + c) * s.H + ih) * s.W + iw);
+                const bool in = idx < xtotal && ih >= 0 && ih < s.H && iw >= 0 && iw < s.W;
+                const float x = load_elem<T>(Xc, in ? (c * s.H + ih) * s.W + iw : 0);
+                v[j] = in ? x : 0.0f;
             }
-        }
 #pragma unroll
-        for (int j = 0; j < kStage; ++j) {
-            const int idx = i0 + j * kThreads;
-            if (idx < xtotal) Xs[idx] = v[j];
+            for (int j = 0; j < kStage; ++j) {
+                const int idx = i0 + j * kThreads;
+                *(idx < xtotal ? Xs + idx : trash + lane) = v[j];
+            }
         }
     }
 
@@ -148,59 +233,67 @@ __global__ __launch_bounds__(kThreads) void conv_per_sample_kernel(
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[x][y][r] = 0.0f;
 
+    // bias: thread (seg, co) adds positions seg, seg + nseg, ... of each chunk
     const bool do_bias = gb != nullptr && tm == 0;
+    constexpr int kSeg = kThreads / Cfg::BN;
+    const int bco = tid % Cfg::BN, bseg = tid / Cfg::BN;
     float bias_acc = 0.0f;
-    const T *Gn = GY + (i64)n * s.Cout * s.L;
 
     for (int p0 = 0; p0 < s.L; p0 += BK) {
-        __syncthreads();   // previous chunk fully consumed (and Xs staged, first time)
-        const int gtotal = Cfg::BN * BK;
-        for (int e0 = tid; e0 < gtotal; e0 += kThreads * kStage) {
-            float v[kStage];
-            int at[kStage];
+        if (!g.one) {
+            if (p0 > 0) __syncthreads();   // previous chunk fully consumed
+            const int gtotal = Cfg::BN * BK;
+            const T *Gc = Gn + (i64)n0 * s.L + p0;
+            float *trash = Gs + BK * Cfg::LDG;
+            for (int e0 = tid; e0 < gtotal; e0 += kThreads * kStage) {
+                float v[kStage];
+                float *at[kStage];
 #pragma unroll
-            for (int j = 0; j < kStage; ++j) {
-                const int e = e0 + j * kThreads;
-                int co, p;
-                divmod(e, BK, g.inv_bk, co, p);
-                at[j] = e < gtotal ? p * Cfg::LDG + co : -1;
-                v[j] = 0.0f;
-                if (e < gtotal && n0 + co < s.Cout && p0 + p < s.L)
-                    v[j] = load_elem<T>(Gn, (i64)(n0 + co) * s.L + p0 + p);
-            }
+                for (int j = 0; j < kStage; ++j) {
+                    const int e = e0 + j * kThreads;
+                    int co, p;
+                    divmod(e, BK, g.inv_bk, co, p);
+                    at[j] = e < gtotal ? Gs + p * Cfg::LDG + co : trash + lane;
+                    const bool in = e < gtotal && co < nco && p0 + p < s.L;
+                    const float x = load_elem<T>(Gc, in ? co * s.L + p : 0);
+                    v[j] = in ? x : 0.0f;
+                }
 #pragma unroll
-            for (int j = 0; j < kStage; ++j)
-                if (at[j] >= 0) Gs[at[j]] = v[j];
-        }
-        for (int t = tid; t < BK; t += kThreads) {
-            const int p = p0 + t;
-            int o = 0;
-            if (p < s.L) {
-                int oh, ow;
-                divmod(p, s.Wo, g.inv_wo, oh, ow);
-                o = oh * s.sh * g.Wp + ow * s.sw;
+                for (int j = 0; j < kStage; ++j) *at[j] = v[j];
             }
-            offp[t] = o;
         }
         __syncthreads();
-        const int kpairs = (s.L - p0 < BK ? s.L - p0 + 1 : BK) >> 1;
-#pragma unroll 2
-        for (int q = wk; q < kpairs; q += WK) {
-            const int ks = 2 * q + (lane >> 5);
-            const int op = offp[ks];
-            float a[FM], b[FN];
+        const int len = s.L - p0 < BK ? s.L - p0 : BK;
+        const int kpairs = (len + 1) >> 1;
+        // two position pairs per trip (the second masked to zero past the
+        // end) so that the LDS reads of both are issued before the MFMAs
+        for (int q0 = wk; q0 < kpairs; q0 += 2 * WK) {
+            float a[2][FM], b[2][FN];
 #pragma unroll
-            for (int x = 0; x < FM; ++x) a[x] = vkk[x] ? Xs[offkk[x] + op] : 0.0f;
+            for (int h = 0; h < 2; ++h) {
+                const bool ok = q0 + h * WK < kpairs;
+                const int ks = ok ? 2 * (q0 + h * WK) + (lane >> 5) : 0;
+                int oh, ow;
+                divmod(p0 + ks, s.Wo, g.inv_wo, oh, ow);
+                const int op = ks < len ? oh * g.rowstep + ow * s.sw : 0;
 #pragma unroll
-            for (int y = 0; y < FN; ++y) b[y] = Gs[ks * Cfg::LDG + wn * FN * 32 + y * 32 + (lane & 31)];
+                for (int x = 0; x < FM; ++x) a[h][x] = vkk[x] ? Xs[offkk[x] + op] : 0.0f;
 #pragma unroll
-            for (int x = 0; x < FM; ++x)
+                for (int y = 0; y < FN; ++y) {
+                    const float v = Gs[ks * Cfg::LDG + wn * FN * 32 + y * 32 + (lane & 31)];
+                    b[h][y] = ok ? v : 0.0f;
+                }
+            }
 #pragma unroll
-                for (int y = 0; y < FN; ++y)
-                    acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[x], b[y], acc[x][y], 0, 0, 0);
+            for (int h = 0; h < 2; ++h)
+#pragma unroll
+                for (int x = 0; x < FM; ++x)
+#pragma unroll
+                    for (int y = 0; y < FN; ++y)
+                        acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[h][x], b[h][y], acc[x][y], 0, 0, 0);
         }
-        if (do_bias && tid < Cfg::BN) {
-            for (int p = 0; p < 2 * kpairs; ++p) bias_acc += Gs[p * Cfg::LDG + tid];
+        if (do_bias) {
+            for (int p = bseg; p < len; p += kSeg) bias_acc += Gs[p * Cfg::LDG + bco];
         }
     }
 
@@ -259,10 +352,17 @@ __global__ __launch_bounds__(kThreads) void conv_per_sample_kernel(
                 }
             }
     }
-    if (do_bias && tid < Cfg::BN && n0 + tid < s.Cout) {
-        const float v = scale * bias_acc;
-        gb[(i64)n * s.Cout + n0 + tid] = v;
-        sq += v * v;
+    if (do_bias) {   // segments added in order
+        bpart[tid] = bias_acc;
+        __syncthreads();
+        if (tid < nco) {
+            float b = 0.0f;
+#pragma unroll
+            for (int k = 0; k < kSeg; ++k) b += bpart[k * Cfg::BN + tid];
+            const float v = scale * b;
+            gb[(i64)n * s.Cout + n0 + tid] = v;
+            sq += v * v;
+        }
     }
     sq = block_sum(sq, red16);
     if (sqout && tid == 0) {
@@ -387,6 +487,7 @@ ConvGeom geom_for(const CfgDesc &c, const ConvShape &s)
     g.tiles_n = (s.Cout + BN - 1) / BN;
     g.tiles = g.tiles_m * g.tiles_n;
     g.vec = 0;
+    g.one = g.xvec = g.gvec = 0;
     return g;
 }
 
@@ -395,8 +496,8 @@ ConvGeom geom_for(const CfgDesc &c, const ConvShape &s)
 int chunk_for(const CfgDesc &c, const ConvGeom &g, const ConvShape &s)
 {
     const int BN = c.WN * c.FN * 32;
-    const long avail = (long)kLdsBudget / 4 - (long)g.nplanes * g.plane;
-    long bk = avail / (BN + 2);
+    const long avail = (long)kLdsBudget / 4 - (long)g.nplanes * g.plane - 64;
+    long bk = avail / (BN + 1);
     bk &= ~7L;
     const int need = (s.L + 7) & ~7;
     if (bk > need) bk = need;
@@ -407,7 +508,7 @@ int chunk_for(const CfgDesc &c, const ConvGeom &g, const ConvShape &s)
 size_t lds_for(const CfgDesc &c, const ConvGeom &g)
 {
     const int BN = c.WN * c.FN * 32;
-    const size_t stage = (size_t)g.nplanes * g.plane + (size_t)g.bk * (BN + 2);
+    const size_t stage = (size_t)g.nplanes * g.plane + (size_t)g.bk * (BN + 1) + 64;
     const size_t redf = (size_t)(c.WK - 1) * c.WM * c.WN * c.FM * c.FN * 16 * 64;
     return (stage > redf ? stage : redf) * sizeof(float);
 }
@@ -536,6 +637,7 @@ extern "C" dp_status dp_grad_sample_conv2d(const void *X, const void *GY, dp_dty
     if (N == 0) return DP_OK;
 
     const ConvShape s = make_shape(Cin, H, W, Cout, kh, kw, sh, sw, ph, pw);
+    const bool bf = dt == DP_BF16;
     Plan p = plan_conv(s);
     p.g.vec = (s.KK % 4 == 0) && aligned(gW, 16);
     if (p.cfg >= 0) {
@@ -543,11 +645,20 @@ extern "C" dp_status dp_grad_sample_conv2d(const void *X, const void *GY, dp_dty
         p.g.inv_wp = 1.0f / (float)p.g.Wp;
         p.g.inv_bk = 1.0f / (float)p.g.bk;
         p.g.inv_wo = 1.0f / (float)s.Wo;
+        p.g.inv_hw = 1.0f / (float)(s.H * s.W);
+        p.g.inv_w = 1.0f / (float)s.W;
+        p.g.inv_l = 1.0f / (float)s.L;
+        p.g.rowstep = s.sh * p.g.Wp;
+        const CfgDesc &c = kConfigs[p.cfg];
+        const long BN = c.WN * c.FN * 32;
+        p.g.one = p.g.bk >= s.L && (long)p.g.nplanes * s.H * s.W <= (long)kThreads * kOneX &&
+                  BN * s.L <= (long)kThreads * kOneG;
+        p.g.xvec = !bf && (s.H * s.W) % 4 == 0 && aligned(X, 16);
+        p.g.gvec = !bf && ((long)s.Cout * s.L) % 4 == 0 && aligned(GY, 16);
     }
     const int tiles = p.cfg >= 0 ? p.g.tiles : conv_tiles(s);
     const int direct = tiles == 1;
     float *sqout = sqnorm ? (direct ? sqnorm : (float *)ws) : nullptr;
-    const bool bf = dt == DP_BF16;
     if (p.cfg >= 0) {
         if (bf) dispatch_fast<uint16_t>(X, GY, s, p, N, scale, gW, gb, sqout, direct, stream);
         else dispatch_fast<float>(X, GY, s, p, N, scale, gW, gb, sqout, direct, stream);

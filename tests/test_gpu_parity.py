@@ -201,6 +201,32 @@ def test_conv_shapes(shape):
     assert_rel(sq.cpu().numpy(), rsq, 1e-4, "conv sqnorm")
 
 
+@pytest.mark.parametrize("shape", [CONV_SHAPES[1], CONV_SHAPES[2], CONV_SHAPES[3], CONV_SHAPES[5]])
+def test_conv_shapes_bf16(shape):
+    """bf16 inputs (scalar staging loads) against the oracle on the rounded values."""
+    N, Cin, H, Wd, Cout, kh, kw, sh, sw, ph, pw = shape
+    say("conv bf16", shape)
+    Ho = (H + 2 * ph - kh) // sh + 1
+    Wo = (Wd + 2 * pw - kw) // sw + 1
+    r = np.random.default_rng(sum(shape) + 1)
+    X = torch.from_numpy(r.standard_normal((N, Cin, H, Wd)).astype(np.float32)).to(torch.bfloat16)
+    GY = torch.from_numpy((r.standard_normal((N, Cout, Ho, Wo)) / 4).astype(np.float32)).to(torch.bfloat16)
+    gW = torch.empty((N, Cout, Cin, kh, kw), device=DEV)
+    gb = torch.empty((N, Cout), device=DEV)
+    sq = torch.empty(N, device=DEV)
+    ws = torch.empty(max(dp.dp_grad_sample_conv2d_workspace_bytes(N, Cin, H, Wd, Cout, kh, kw, sh, sw, ph, pw), 1),
+                     dtype=torch.uint8, device=DEV)
+    dp.dp_grad_sample_conv2d(X.to(DEV), GY.to(DEV), dp.DP_BF16, N, Cin, H, Wd, Cout, Ho, Wo, kh, kw, sh, sw, ph, pw,
+                             1, 1, 1, 0.9, gW, gb, sq, None, ws)
+    Xr, Gr = X.float().numpy().astype(np.float64), GY.float().numpy().astype(np.float64)
+    rW, rb = oracle.conv2d_grad(Xr, Gr, (kh, kw), (sh, sw), (ph, pw), 0.9)
+    rsq = np.zeros(N)
+    oracle.sqnorm_accumulate(rW, rsq); oracle.sqnorm_accumulate(rb, rsq)
+    assert_g12(gW.cpu().numpy(), rW, 1e-4, "conv bf16 gW")
+    assert_g12(gb.cpu().numpy(), rb, 1e-4, "conv bf16 gb")
+    assert_rel(sq.cpu().numpy(), rsq, 1e-4, "conv bf16 sqnorm")
+
+
 def run_embedding(ids, B, V, cap=None, scale=1.0):
     N, T = ids.shape
     D = B.shape[2]
