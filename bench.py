@@ -7,11 +7,25 @@ already resident in HBM: per-sample gradients of every layer, per-sample
 norms, clip factors, clipped sums, noise and division.  W untimed steps, then
 K timed steps between two device synchronizations; value = samples / second.
 
-Alongside: the dominant kernel's roofline (algorithmic bytes or flops per
-launch over its average duration, timed with HIP events on its own stream
-during the timed steps), HBM traffic from committed rocprofv3 counter runs
-when they still match the kernel source, and the fp64 oracle timed on the
-host's cores on a bounded sample of the same workload.
+Alongside: the dominant call's roofline (algorithmic bytes or flops per
+launch over its average duration, timed with HIP events on the step's stream
+around K back-to-back launches of that call after the timed steps), HBM
+traffic from committed rocprofv3 counter runs when they still match the
+kernel source, and the fp64 oracle timed on the host's cores on a bounded
+sample of the same workload.
+
+Counter runs (two passes, one counter each) and their reduction:
+
+    rocprofv3 --pmc FETCH_SIZE -f csv -d DIR_F -o c -- python bench.py --copy-calibration-mib 512 ...
+    rocprofv3 --pmc WRITE_SIZE -f csv -d DIR_W -o c -- python bench.py --copy-calibration-mib 512 ...
+    python bench.py --record-traffic META DIR_F/c_counter_collection.csv DIR_W/c_counter_collection.csv
+
+(META: the file the counter runs wrote with --meta-out.)
+
+The launches of the dominant call and the calibration copy are bracketed by a
+one-byte-element fill kernel that nothing else launches, so the reduction can
+find them in the dispatch list; each counter is scaled by the ratio of the
+copy's true bytes to what the counter reads for it.
 """
 from __future__ import annotations
 
@@ -137,6 +151,62 @@ def traffic_for(kernel, workload, call):
 # CPU baseline: the oracle on a bounded sample
 # ---------------------------------------------------------------------------
 
+SENTINEL = "FillFunctor<signed char>"
+
+
+def record_traffic(meta_path, fetch_csv, write_csv):
+    """Reduce two counter runs to HBM bytes per launch of the dominant call; update profiles/traffic.json."""
+    import csv
+
+    def load(path, counter):
+        rows = {}
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter:
+                continue
+            d = int(r["Dispatch_Id"])
+            rows[d] = (r["Kernel_Name"], rows.get(d, ("", 0.0))[1] + float(r["Counter_Value"]))
+        return [rows[d] for d in sorted(rows)]
+
+    def regions(seq):
+        # every measured block is bracketed by a pair of sentinel dispatches
+        cut = [i for i, (k, _) in enumerate(seq) if SENTINEL in k]
+        return [seq[a + 1:b] for a, b in zip(cut[0::2], cut[1::2])]
+
+    with open(meta_path) as f:
+        meta = json.load(f)
+    calls = meta["calls"]
+    per = {}
+    for name, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
+        reg = regions(load(path, name))
+        if len(reg) != len(calls) + 1:
+            raise SystemExit("record-traffic: %d sentinel regions in %s, expected %d"
+                             % (len(reg), path, len(calls) + 1))
+        copy = reg[-1]                       # [call 0] ... [call n-1] [copy]
+        counted = sum(v for _, v in copy) * 1024.0      # a copy reads and writes copy_bytes
+        factor = meta["copy_bytes"] / counted
+        for n, r in zip(calls, reg):
+            kernels = sorted({k.replace("(anonymous namespace)::", "").replace("void ", "").split("(")[0]
+                              for k, _ in r})
+            per.setdefault(n, {})[name] = (sum(v for _, v in r) * 1024.0 * factor / meta["launches"], factor,
+                                           kernels)
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    table = json.load(open(path)) if os.path.exists(path) else {}
+    for n in calls:
+        kern = meta["kernels"][n]
+        f, w = per[n]["FETCH_SIZE"], per[n]["WRITE_SIZE"]
+        table["%s/%s" % (meta["workload"], n)] = {
+            "kernel": kern, "source_sha": src_hash(KERNEL_SOURCES.get(kern, [])),
+            "bytes_per_launch": round(f[0] + w[0]), "fetch_bytes_per_launch": round(f[0]),
+            "write_bytes_per_launch": round(w[0]), "fetch_scale": round(f[1], 4), "write_scale": round(w[1], 4),
+            "algorithmic_bytes": meta["algorithmic_bytes"][n], "dispatched": f[2]}
+    with open(path, "w") as fh:
+        json.dump(table, fh, indent=1, sort_keys=True)
+        fh.write("\n")
+    for n in calls:
+        k = "%s/%s" % (meta["workload"], n)
+        print(k, table[k]["bytes_per_launch"], "algorithmic", table[k]["algorithmic_bytes"])
+
+
 def cpu_baseline(wl, inputs, budget_s: float):
     import numpy as np
     import oracle
@@ -179,7 +249,13 @@ def main():
     ap.add_argument("--eager", action="store_true", help="time eager launches instead of graph replays")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run a plain device copy of this size (for counter calibration)")
+    ap.add_argument("--meta-out", default="", help="write the dominant call's name and launch count here")
+    ap.add_argument("--record-traffic", nargs=3, metavar=("META", "FETCH_CSV", "WRITE_CSV"),
+                    help="reduce two rocprofv3 counter runs of this benchmark into profiles/traffic.json")
     args = ap.parse_args()
+    if args.record_traffic:
+        record_traffic(*args.record_traffic)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py: this build runs the DP-SGD step on one GPU only; --gpus %d is not supported "
@@ -199,31 +275,9 @@ def main():
     stream = torch.cuda.current_stream(dev)
     costs = call_costs(st)
 
-    # find the dominant call: event-time every call over a few eager steps
-    names = list(costs)
-    ev = {n: [] for n in names}
-
-    def mark_all(name, where):
-        e = torch.cuda.Event(enable_timing=True)
-        e.record(stream)
-        if where == "start":
-            ev[name].append([e, None])
-        else:
-            ev[name][-1][1] = e
-
     for i in range(3):
         st.run(step=i)
-    for i in range(10):
-        st.run(step=i, mark=mark_all)
     torch.cuda.synchronize()
-    avg = {n: sum(a.elapsed_time(b) for a, b in ev[n]) / len(ev[n]) for n in names if ev[n]}
-    dominant = max(avg, key=avg.get)
-    if args.breakdown:
-        for n in names:
-            if n not in avg:
-                continue
-            b, f, k, _ = costs[n]
-            log("[breakdown] %-18s %9.2f us  %10.3f MB  %9.3f GFLOP  %s" % (n, avg[n] * 1e3, b / 1e6, f / 1e9, k))
 
     # the timed region: K whole steps, replayed from one captured HIP graph
     # (eager launches with --eager)
@@ -244,36 +298,62 @@ def main():
     if status != 0:
         log("[bench] device status flags %d" % status)
 
-    # the dominant call's kernel time: HIP events on the step's stream around
-    # that call, over K eager steps
-    dom = []
-
-    def mark_dom(name, where):
-        if name != dominant:
-            return
-        e = torch.cuda.Event(enable_timing=True)
-        e.record(stream)
-        if where == "start":
-            dom.append([e, None])
-        else:
-            dom[-1][1] = e
-
+    # eager launches of the same steps, for comparison
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     for i in range(args.steps):
-        st.run(step=i, mark=mark_dom)
+        st.run(step=i)
     torch.cuda.synchronize()
     eager_ms = (time.perf_counter() - t1) * 1e3 / args.steps
+
+    # each call's kernel time: HIP events on the step's stream around one
+    # replay of a HIP graph holding K back-to-back launches of that call
+    # alone (so the GPU, not the host's launch rate, sets the pace);
+    # consecutive blocks are bracketed by a sentinel kernel so that counter
+    # runs can attribute every dispatch
+    names = list(costs)
+    sentinel = torch.empty(64, dtype=torch.int8, device=dev)
+    avg = {}
+    for n in names:
+        side = torch.cuda.Stream(dev)
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            st.call(n, step=0)                  # warm up outside the capture
+        stream.wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for i in range(args.steps):
+                st.call(n, step=i)
+        g.replay()                              # first replay uploads the graph
+        torch.cuda.synchronize()
+        sentinel.fill_(1)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        g.replay()
+        e1.record(stream)
+        sentinel.fill_(1)
+        torch.cuda.synchronize()
+        avg[n] = e0.elapsed_time(e1) / args.steps
+        del g
     if args.copy_calibration_mib > 0:
         nb = args.copy_calibration_mib << 20
         a = torch.empty(nb // 4, dtype=torch.float32, device=dev).fill_(1.0)
         b = torch.empty_like(a)
-        for _ in range(3):
-            b.copy_(a)
         torch.cuda.synchronize()
+        sentinel.fill_(1)
+        b.copy_(a)
+        sentinel.fill_(1)
+        torch.cuda.synchronize()
+    dominant = max(avg, key=avg.get)
+    dom_ms = avg[dominant]
+    if args.breakdown:
+        for n in names:
+            b, f, k, _ = costs[n]
+            log("[breakdown] %-18s %9.2f us  %10.3f MB  %9.3f GFLOP  %s" % (n, avg[n] * 1e3, b / 1e6, f / 1e9, k))
 
     ms = elapsed * 1e3 / args.steps
-    dom_ms = sum(a.elapsed_time(b) for a, b in dom) / len(dom)
     nbytes, flops, kname, mfma_dtype = costs[dominant]
     dt_s = dom_ms * 1e-3
     hbm_s = nbytes / (HBM_PEAK_GBS * 1e9)
@@ -299,6 +379,13 @@ def main():
             "config": {"workload": wl.name, "batch": wl.N, "params": wl.n_params,
                        "layers": [l.name for l in wl.layers], "C": wl.C, "sigma": wl.sigma},
             "roofline": roof}
+    if args.meta_out:
+        with open(args.meta_out, "w") as f:
+            json.dump({"workload": wl.name, "calls": names, "launches": args.steps,
+                       "kernels": {n: costs[n][2] for n in names},
+                       "algorithmic_bytes": {n: costs[n][0] for n in names},
+                       "avg_us": {n: round(avg[n] * 1e3, 2) for n in names},
+                       "copy_bytes": args.copy_calibration_mib << 20}, f)
     if not args.no_cpu_baseline:
         log("[bench] timing the oracle on the host")
         line["cpu_baseline"] = cpu_baseline(wl, inputs, args.cpu_seconds)

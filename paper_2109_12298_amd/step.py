@@ -210,6 +210,20 @@ class DPStep:
         dp.dp_clip_noise_many(self.group, self.group_count, self.N, self.norm, self.C, self.seed, step, step_dev,
                               self.sigma, self.denom, self.status, self.ws, stream)
 
+    def call(self, name: str, step: int = 0, stream=None):
+        """Enqueue one named call of the step ("grad:<layer>", "norms", "clip:<layer>", "clip+noise")."""
+        if name == "norms":
+            return self.norms(stream)
+        if name == "clip+noise":
+            return self.clip_noise(step, None, stream)
+        kind, lname = name.split(":", 1)
+        i = next(k for k, lb in enumerate(self.layers) if lb.layer.name == lname)
+        if kind == "grad":
+            return self.grad_sample(i, stream)
+        if kind == "clip":
+            return self.fused_clip_sum(i, stream)
+        raise KeyError(name)
+
     def _fork(self, n):
         torch = _torch()
         if self._side is None or len(self._side) < n:
