@@ -41,11 +41,12 @@ struct ConvShape {
 // ---------------------------------------------------------------------------
 template <int FM, int FN, int WM, int WN, int WK>
 struct ConvTile {
-    static_assert(WM * WN * WK == 4, "four waves");
+    static_assert(WM * WN * WK == 4 || WM * WN * WK == 8, "four or eight waves");
+    static_assert((WK & (WK - 1)) == 0, "K split is a power of two");
+    static constexpr int NT = 64 * WM * WN * WK;   // threads
     static constexpr int BM = WM * FM * 32;   // kk
     static constexpr int BN = WN * FN * 32;   // co
     static constexpr int LDG = BN + 1;        // padded row of the staged backprop chunk
-    static constexpr int RED = (WK - 1) * WM * WN * FM * FN * 16 * 64;  // floats for the K-split sum
 };
 
 struct ConvGeom {
@@ -75,23 +76,24 @@ __device__ __forceinline__ void divmod(int x, int d, float inv_d, int &q, int &r
 }
 
 // Flat element held in register j by thread tid of a one-shot load.
+template <int NT>
 __device__ __forceinline__ int flat_at(int j, int tid, bool vec)
 {
-    return vec ? 4 * (tid + (j >> 2) * kThreads) + (j & 3) : tid + j * kThreads;
+    return vec ? 4 * (tid + (j >> 2) * NT) + (j & 3) : tid + j * NT;
 }
 
 // Loads elements [0, count) of src (count >= 1) into registers, all loads
 // issued before any is used; addresses past the end are clamped and their
 // values zeroed, so there is no branch.  vec: float4 loads (count % 4 == 0,
 // src 16-byte aligned).
-template <int EPT, typename T>
+template <int EPT, int NT, typename T>
 __device__ __forceinline__ void flat_load(const T *__restrict__ src, int count, bool vec, int tid, float (&v)[EPT])
 {
     if constexpr (std::is_same<T, float>::value) {
         if (vec) {
 #pragma unroll
             for (int j = 0; j < EPT / 4; ++j) {
-                const int e = 4 * (tid + j * kThreads);
+                const int e = 4 * (tid + j * NT);
                 const int ec = e < count ? e : count - 4;
                 const float4 q = *reinterpret_cast<const float4 *>(src + ec);
                 const bool ok = e < count;
@@ -105,21 +107,22 @@ __device__ __forceinline__ void flat_load(const T *__restrict__ src, int count, 
     }
 #pragma unroll
     for (int j = 0; j < EPT; ++j) {
-        const int e = tid + j * kThreads;
+        const int e = tid + j * NT;
         const float x = load_elem<T>(src, e < count ? e : count - 1);
         v[j] = e < count ? x : 0.0f;
     }
 }
 
 template <typename T, int FM, int FN, int WM, int WN, int WK>
-__global__ __launch_bounds__(kThreads) void conv_per_sample_kernel(
+__global__ __launch_bounds__(64 * WM * WN * WK) void conv_per_sample_kernel(
     const T *__restrict__ X, const T *__restrict__ GY, ConvShape s, ConvGeom g, float scale,
     float *__restrict__ gW, float *__restrict__ gb, float *__restrict__ sqout, int direct)
 {
     using Cfg = ConvTile<FM, FN, WM, WN, WK>;
+    constexpr int NT = Cfg::NT;
     extern __shared__ float lds[];
     __shared__ float red16[16];
-    __shared__ float bpart[kThreads];
+    __shared__ float bpart[NT];
 
     const i64 bsw = xcd_swizzle(blockIdx.x, gridDim.x);
     const int n = (int)(bsw / g.tiles);
@@ -151,11 +154,11 @@ __global__ __launch_bounds__(kThreads) void conv_per_sample_kernel(
         // flight before the first is written to LDS
         float xv[kOneX], gv[kOneG];
         const int xcount = np * HW, gcount = nco * s.L;
-        flat_load<kOneX>(Xn + (i64)ci0 * HW, xcount, g.xvec != 0, tid, xv);
-        flat_load<kOneG>(Gn + (i64)n0 * s.L, gcount, g.gvec != 0, tid, gv);
+        flat_load<kOneX, NT>(Xn + (i64)ci0 * HW, xcount, g.xvec != 0, tid, xv);
+        flat_load<kOneG, NT>(Gn + (i64)n0 * s.L, gcount, g.gvec != 0, tid, gv);
         if (pad) {   // zero halo (disjoint from the interior written below)
             float *trash = Gs + BK * Cfg::LDG;
-            for (int idx = tid; idx < np * g.plane; idx += kThreads) {
+            for (int idx = tid; idx < np * g.plane; idx += NT) {
                 int c, rem, r, q;
                 divmod(idx, g.plane, g.inv_plane, c, rem);
                 divmod(rem, g.Wp, g.inv_wp, r, q);
@@ -168,7 +171,7 @@ __global__ __launch_bounds__(kThreads) void conv_per_sample_kernel(
         float *trash = Gs + BK * Cfg::LDG;
 #pragma unroll
         for (int j = 0; j < kOneX; ++j) {
-            const int e = flat_at(j, tid, g.xvec != 0);
+            const int e = flat_at<NT>(j, tid, g.xvec != 0);
             int c, rem, ih, iw;
             divmod(e, HW, g.inv_hw, c, rem);
             divmod(rem, s.W, g.inv_w, ih, iw);
@@ -177,7 +180,7 @@ __global__ __launch_bounds__(kThreads) void conv_per_sample_kernel(
         }
 #pragma unroll
         for (int j = 0; j < kOneG; ++j) {
-            const int e = flat_at(j, tid, g.gvec != 0);
+            const int e = flat_at<NT>(j, tid, g.gvec != 0);
             int co, p;
             divmod(e, s.L, g.inv_l, co, p);
             float *dst = e < gcount ? Gs + p * Cfg::LDG + co : trash + lane;
@@ -189,11 +192,11 @@ __global__ __launch_bounds__(kThreads) void conv_per_sample_kernel(
         const int xtotal = np * g.plane;
         const T *Xc = Xn + (i64)ci0 * HW;
         float *trash = Gs + BK * Cfg::LDG;
-        for (int i0 = tid; i0 < xtotal; i0 += kThreads * kStage) {
+        for (int i0 = tid; i0 < xtotal; i0 += NT * kStage) {
             float v[kStage];
 #pragma unroll
             for (int j = 0; j < kStage; ++j) {
-                const int idx = i0 + j * kThreads;
+                const int idx = i0 + j * NT;
                 int c, rem, r, q;
                 divmod(idx, g.plane, g.inv_plane, c, rem);
                 divmod(rem, g.Wp, g.inv_wp, r, q);
@@ -204,7 +207,7 @@ __global__ __launch_bounds__(kThreads) void conv_per_sample_kernel(
             }
 #pragma unroll
             for (int j = 0; j < kStage; ++j) {
-                const int idx = i0 + j * kThreads;
+                const int idx = i0 + j * NT;
                 *(idx < xtotal ? Xs + idx : trash + lane) = v[j];
             }
         }
@@ -235,7 +238,7 @@ __global__ __launch_bounds__(kThreads) void conv_per_sample_kernel(
 
     // bias: thread (seg, co) adds positions seg, seg + nseg, ... of each chunk
     const bool do_bias = gb != nullptr && tm == 0;
-    constexpr int kSeg = kThreads / Cfg::BN;
+    constexpr int kSeg = NT / Cfg::BN;
     const int bco = tid % Cfg::BN, bseg = tid / Cfg::BN;
     float bias_acc = 0.0f;
 
@@ -245,12 +248,12 @@ __global__ __launch_bounds__(kThreads) void conv_per_sample_kernel(
             const int gtotal = Cfg::BN * BK;
             const T *Gc = Gn + (i64)n0 * s.L + p0;
             float *trash = Gs + BK * Cfg::LDG;
-            for (int e0 = tid; e0 < gtotal; e0 += kThreads * kStage) {
+            for (int e0 = tid; e0 < gtotal; e0 += NT * kStage) {
                 float v[kStage];
                 float *at[kStage];
 #pragma unroll
                 for (int j = 0; j < kStage; ++j) {
-                    const int e = e0 + j * kThreads;
+                    const int e = e0 + j * NT;
                     int co, p;
                     divmod(e, BK, g.inv_bk, co, p);
                     at[j] = e < gtotal ? Gs + p * Cfg::LDG + co : trash + lane;
@@ -297,23 +300,27 @@ __global__ __launch_bounds__(kThreads) void conv_per_sample_kernel(
         }
     }
 
-    // ---- add the K-split partial tiles (wave order), reusing the staging LDS
+    // ---- add the K-split partial tiles pairwise in a fixed tree (wave k
+    // takes wave k + w/2), reusing the staging LDS
     if (WK > 1) {
-        __syncthreads();
+        constexpr int kTile = FM * FN * 16 * 64;   // floats of one wave's accumulators
         float *R = lds;
-        if (wk > 0) {
-            float *dst = R + (((wk - 1) * WM * WN + wmn) * FM * FN) * 16 * 64;
 #pragma unroll
-            for (int x = 0; x < FM; ++x)
+        for (int w = WK; w > 1; w >>= 1) {
+            const int half = w >> 1;
+            __syncthreads();
+            if (wk >= half && wk < w) {
+                float *dst = R + ((wk - half) * WM * WN + wmn) * kTile;
 #pragma unroll
-                for (int y = 0; y < FN; ++y)
+                for (int x = 0; x < FM; ++x)
 #pragma unroll
-                    for (int r = 0; r < 16; ++r) dst[((x * FN + y) * 16 + r) * 64 + lane] = acc[x][y][r];
-        }
-        __syncthreads();
-        if (wk == 0) {
-            for (int w = 1; w < WK; ++w) {
-                const float *src = R + (((w - 1) * WM * WN + wmn) * FM * FN) * 16 * 64;
+                    for (int y = 0; y < FN; ++y)
+#pragma unroll
+                        for (int r = 0; r < 16; ++r) dst[((x * FN + y) * 16 + r) * 64 + lane] = acc[x][y][r];
+            }
+            __syncthreads();
+            if (wk < half) {
+                const float *src = R + (wk * WM * WN + wmn) * kTile;
 #pragma unroll
                 for (int x = 0; x < FM; ++x)
 #pragma unroll
@@ -470,8 +477,14 @@ constexpr CfgDesc kConfigs[] = {
     {2, 2, 2, 1, 2},   // 128 x 64
     {2, 2, 2, 2, 1},   // 128 x 128
     {2, 2, 1, 2, 2},   // 64 x 128
+    // eight waves: for grids too small to fill the chip with four-wave blocks
+    {1, 1, 1, 1, 8},   // 32 x 32
+    {2, 1, 1, 1, 8},   // 64 x 32
+    {2, 1, 2, 1, 4},   // 128 x 32
+    {2, 1, 4, 1, 2},   // 256 x 32
 };
 constexpr int kNumConfigs = sizeof(kConfigs) / sizeof(kConfigs[0]);
+static_assert(kNumConfigs == 13, "dispatch_fast lists every configuration");
 
 ConvGeom geom_for(const CfgDesc &c, const ConvShape &s)
 {
@@ -505,15 +518,22 @@ int chunk_for(const CfgDesc &c, const ConvGeom &g, const ConvShape &s)
     return (int)bk;
 }
 
+int threads_of(const CfgDesc &c) { return 64 * c.WM * c.WN * c.WK; }
+
 size_t lds_for(const CfgDesc &c, const ConvGeom &g)
 {
     const int BN = c.WN * c.FN * 32;
     const size_t stage = (size_t)g.nplanes * g.plane + (size_t)g.bk * (BN + 1) + 64;
-    const size_t redf = (size_t)(c.WK - 1) * c.WM * c.WN * c.FM * c.FN * 16 * 64;
+    const size_t redf = (size_t)(c.WK / 2) * c.WM * c.WN * c.FM * c.FN * 16 * 64;
     return (stage > redf ? stage : redf) * sizeof(float);
 }
 
-Plan plan_conv(const ConvShape &s)
+// Grids of at most this many workgroups leave CUs idle or nearly so; their
+// blocks get eight waves, so that each wave's serial share of the sample is
+// halved and two waves per SIMD hide each other's latencies.
+constexpr long kSmallGrid = 512;
+
+Plan plan_conv(const ConvShape &s, long N)
 {
     Plan best;
     best.cfg = -1;
@@ -528,7 +548,9 @@ Plan plan_conv(const ConvShape &s)
         // padded MFMA area, plus the re-staging of input planes per tile
         const double area = (double)g.tiles_m * BM * g.tiles_n * BN;
         const double stage = (double)g.tiles * g.nplanes * g.plane / 8.0;
-        const double cost = area + stage + (g.tiles > 1 ? 2048.0 : 0.0);
+        double cost = area + stage + (g.tiles > 1 ? 2048.0 : 0.0);
+        const bool small = N * g.tiles <= kSmallGrid;
+        if (threads_of(c) == 512) cost *= small ? 0.7 : 1.05;
         if (best.cfg < 0 || cost < best_cost) {
             best.cfg = i;
             best.g = g;
@@ -543,7 +565,7 @@ template <typename T, int FM, int FN, int WM, int WN, int WK>
 void launch_fast(const void *X, const void *GY, const ConvShape &s, const Plan &p, i64 N, float scale,
                  float *gW, float *gb, float *sqout, int direct, hipStream_t stream)
 {
-    conv_per_sample_kernel<T, FM, FN, WM, WN, WK><<<(unsigned)(N * p.g.tiles), kThreads, p.lds, stream>>>(
+    conv_per_sample_kernel<T, FM, FN, WM, WN, WK><<<(unsigned)(N * p.g.tiles), 64 * WM * WN * WK, p.lds, stream>>>(
         (const T *)X, (const T *)GY, s, p.g, scale, gW, gb, sqout, direct);
 }
 
@@ -560,13 +582,17 @@ void dispatch_fast(const void *X, const void *GY, const ConvShape &s, const Plan
     case 5: launch_fast<T, 2, 1, 4, 1, 1>(X, GY, s, p, N, scale, gW, gb, sqout, direct, stream); break;
     case 6: launch_fast<T, 2, 2, 2, 1, 2>(X, GY, s, p, N, scale, gW, gb, sqout, direct, stream); break;
     case 7: launch_fast<T, 2, 2, 2, 2, 1>(X, GY, s, p, N, scale, gW, gb, sqout, direct, stream); break;
-    default: launch_fast<T, 2, 2, 1, 2, 2>(X, GY, s, p, N, scale, gW, gb, sqout, direct, stream); break;
+    case 8: launch_fast<T, 2, 2, 1, 2, 2>(X, GY, s, p, N, scale, gW, gb, sqout, direct, stream); break;
+    case 9: launch_fast<T, 1, 1, 1, 1, 8>(X, GY, s, p, N, scale, gW, gb, sqout, direct, stream); break;
+    case 10: launch_fast<T, 2, 1, 1, 1, 8>(X, GY, s, p, N, scale, gW, gb, sqout, direct, stream); break;
+    case 11: launch_fast<T, 2, 1, 2, 1, 4>(X, GY, s, p, N, scale, gW, gb, sqout, direct, stream); break;
+    default: launch_fast<T, 2, 1, 4, 1, 2>(X, GY, s, p, N, scale, gW, gb, sqout, direct, stream); break;
     }
 }
 
-int conv_tiles(const ConvShape &s)
+int conv_tiles(const ConvShape &s, long N)
 {
-    const Plan p = plan_conv(s);
+    const Plan p = plan_conv(s, N);
     if (p.cfg >= 0) return p.g.tiles;
     return ((s.KK + kGN - 1) / kGN) * ((s.Cout + kGM - 1) / kGM);
 }
@@ -610,7 +636,7 @@ extern "C" size_t dp_grad_sample_conv2d_workspace_bytes(int64_t N, int64_t Cin, 
     if (N <= 0 || !shape_ok(Cin, H, W, Cout, kh, kw, sh, sw, ph, pw)) return 0;
     if (!fits_int32(Cin, H + 2 * ph, W + 2 * pw, Cout, kh, kw)) return 0;
     const ConvShape s = make_shape(Cin, H, W, Cout, kh, kw, sh, sw, ph, pw);
-    const int tiles = conv_tiles(s);
+    const int tiles = conv_tiles(s, (long)N);
     return tiles > 1 ? (size_t)(N * tiles) * sizeof(float) : 0;
 }
 
@@ -638,7 +664,7 @@ extern "C" dp_status dp_grad_sample_conv2d(const void *X, const void *GY, dp_dty
 
     const ConvShape s = make_shape(Cin, H, W, Cout, kh, kw, sh, sw, ph, pw);
     const bool bf = dt == DP_BF16;
-    Plan p = plan_conv(s);
+    Plan p = plan_conv(s, (long)N);
     p.g.vec = (s.KK % 4 == 0) && aligned(gW, 16);
     if (p.cfg >= 0) {
         p.g.inv_plane = 1.0f / (float)p.g.plane;
@@ -651,12 +677,12 @@ extern "C" dp_status dp_grad_sample_conv2d(const void *X, const void *GY, dp_dty
         p.g.rowstep = s.sh * p.g.Wp;
         const CfgDesc &c = kConfigs[p.cfg];
         const long BN = c.WN * c.FN * 32;
-        p.g.one = p.g.bk >= s.L && (long)p.g.nplanes * s.H * s.W <= (long)kThreads * kOneX &&
-                  BN * s.L <= (long)kThreads * kOneG;
+        const long nt = threads_of(c);
+        p.g.one = p.g.bk >= s.L && (long)p.g.nplanes * s.H * s.W <= nt * kOneX && BN * s.L <= nt * kOneG;
         p.g.xvec = !bf && (s.H * s.W) % 4 == 0 && aligned(X, 16);
         p.g.gvec = !bf && ((long)s.Cout * s.L) % 4 == 0 && aligned(GY, 16);
     }
-    const int tiles = p.cfg >= 0 ? p.g.tiles : conv_tiles(s);
+    const int tiles = p.cfg >= 0 ? p.g.tiles : conv_tiles(s, (long)N);
     const int direct = tiles == 1;
     float *sqout = sqnorm ? (direct ? sqnorm : (float *)ws) : nullptr;
     if (p.cfg >= 0) {

@@ -176,7 +176,26 @@ CONV_SHAPES = [  # N, Cin, H, W, Cout, kh, kw, sh, sw, ph, pw
     (2, 128, 8, 8, 256, 3, 3, 1, 1, 1, 1)]
 
 
-@pytest.mark.parametrize("shape", CONV_SHAPES)
+# One shape per tile configuration of the fast path and staging mode (whole
+# sample in one load round trip, or position chunks); batch sizes above 512
+# workgroups select the four-wave tiles, smaller grids the eight-wave ones.
+CONV_CONFIG_SHAPES = [
+    (520, 1, 20, 21, 5, 1, 1, 1, 1, 1, 1), (520, 1, 5, 6, 5, 1, 1, 2, 2, 0, 0),            # 32 x 32, 4 waves
+    (520, 33, 13, 14, 5, 1, 1, 1, 1, 1, 1), (520, 33, 5, 6, 5, 1, 1, 2, 2, 0, 0),          # 64 x 32, 4 waves
+    (1, 1, 13, 14, 33, 1, 1, 1, 1, 1, 1), (1, 1, 5, 6, 33, 1, 1, 2, 2, 0, 0),              # 32 x 64
+    (1, 33, 11, 12, 33, 1, 1, 1, 1, 1, 1), (1, 33, 5, 6, 33, 1, 1, 2, 2, 0, 0),            # 64 x 64
+    (520, 24, 20, 21, 5, 2, 2, 2, 2, 1, 1), (520, 8, 5, 6, 5, 3, 3, 2, 2, 1, 1),           # 128 x 32, 4 waves
+    (520, 24, 20, 21, 5, 3, 3, 2, 2, 1, 1), (520, 20, 5, 6, 5, 3, 3, 2, 2, 1, 1),          # 256 x 32, 4 waves
+    (260, 24, 20, 21, 33, 2, 2, 2, 2, 0, 0), (260, 8, 5, 6, 33, 3, 3, 2, 2, 1, 1),         # 128 x 64
+    (130, 12, 20, 21, 128, 3, 3, 2, 2, 0, 0), (130, 12, 5, 6, 128, 3, 3, 2, 2, 1, 1),      # 128 x 128
+    (1, 12, 20, 21, 128, 2, 2, 2, 2, 0, 0), (1, 64, 6, 7, 128, 1, 1, 2, 2, 1, 1),          # 64 x 128
+    (1, 1, 20, 21, 5, 1, 1, 1, 1, 1, 1), (1, 1, 5, 6, 5, 1, 1, 2, 2, 0, 0),                # 32 x 32, 8 waves
+    (1, 33, 13, 14, 5, 1, 1, 1, 1, 1, 1), (1, 33, 5, 6, 5, 1, 1, 2, 2, 0, 0),              # 64 x 32, 8 waves
+    (1, 24, 20, 21, 5, 2, 2, 2, 2, 1, 1), (1, 8, 5, 6, 5, 3, 3, 2, 2, 1, 1),               # 128 x 32, 8 waves
+    (1, 24, 20, 21, 5, 3, 3, 2, 2, 1, 1), (1, 20, 5, 6, 5, 3, 3, 2, 2, 1, 1)]              # 256 x 32, 8 waves
+
+
+@pytest.mark.parametrize("shape", CONV_SHAPES + CONV_CONFIG_SHAPES)
 def test_conv_shapes(shape):
     N, Cin, H, Wd, Cout, kh, kw, sh, sw, ph, pw = shape
     say("conv", shape)
