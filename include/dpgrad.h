@@ -204,13 +204,18 @@ dp_status dp_clip_accumulate_linear(const void *A, const void *B, dp_dtype dt, i
 /* Dense clipped sum of CSR embedding gradients (as dp_grad_sample_embedding
  * writes them): sum[v][:] = sum_n c_n * (sample n's row for id v, if any),
  * n ascending; rows no sample touched are written as zeros.
- * row_ptr int64 [N+1]; uniq_ids int64 [row_ptr[N]]; rows fp32 [row_ptr[N]][D];
- * sum fp32 [V][D].  Stored ids outside [0, V) set DP_FLAG_BAD_INDEX and are
- * ignored. */
+ * row_ptr int64 [N+1]; uniq_ids int64 [cap]; rows fp32 [cap][D] (the arrays
+ * and cap given to dp_grad_sample_embedding); sum fp32 [V][D].  Stored rows
+ * at index cap or beyond are left out and set DP_FLAG_CAP; stored ids outside
+ * [0, V) set DP_FLAG_BAD_INDEX and are left out.  Needs 64 * V < 2^31 and
+ * cap < 2^31 (else DP_EUNSUPPORTED).  The workspace (16-byte aligned) holds
+ * an inverted index of 64 samples at a time. */
+size_t dp_clip_accumulate_embedding_workspace_bytes(int64_t N, int64_t V);
 dp_status dp_clip_accumulate_embedding(const int64_t *row_ptr, const int64_t *uniq_ids,
-                                       const float *rows, const float *norm, float C,
+                                       const float *rows, int64_t cap, const float *norm, float C,
                                        int64_t N, int64_t V, int64_t D, float *sum,
-                                       int32_t *status, hipStream_t stream);
+                                       int32_t *status, void *ws, size_t ws_bytes,
+                                       hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
  * Grouped clipped sums and noise over many parameter tensors

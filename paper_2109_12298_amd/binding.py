@@ -50,7 +50,8 @@ SIGNATURES = {
     "dp_clip_accumulate_linear_workspace_bytes": (_SZ, [_I64, _I64, _I64, _I64, _ST]),
     "dp_clip_accumulate_linear": (_ST, [_P, _P, _ST, _I64, _I64, _I64, _I64, _F, _P, _F, _P, _P, _P, _P,
                                         _SZ, _P]),
-    "dp_clip_accumulate_embedding": (_ST, [_P, _P, _P, _P, _F, _I64, _I64, _I64, _P, _P, _P]),
+    "dp_clip_accumulate_embedding_workspace_bytes": (_SZ, [_I64, _I64]),
+    "dp_clip_accumulate_embedding": (_ST, [_P, _P, _P, _I64, _P, _F, _I64, _I64, _I64, _P, _P, _P, _SZ, _P]),
     "dp_clip_noise_many_workspace_bytes": (_SZ, [_P, _I32, _I64]),
     "dp_clip_noise_many": (_ST, [_P, _I32, _I64, _P, _F, _U64, _U64, _P, _F, _F, _P, _P, _SZ, _P]),
     "dp_step_advance": (_ST, [_P, _U64, _P]),
@@ -249,9 +250,15 @@ def dp_clip_accumulate_linear(A, B, dt, N, T, d_in, d_out, scale, norm, C, sumW,
            "dp_clip_accumulate_linear")
 
 
-def dp_clip_accumulate_embedding(row_ptr, uniq_ids, rows, norm, C, N, V, D, sum, status=None, stream=None):
-    _check(lib().dp_clip_accumulate_embedding(_ptr(row_ptr), _ptr(uniq_ids), _ptr(rows), _ptr(norm), C, N, V,
-                                              D, _ptr(sum), _ptr(status), _stream(stream)),
+def dp_clip_accumulate_embedding_workspace_bytes(N, V) -> int:
+    return lib().dp_clip_accumulate_embedding_workspace_bytes(N, V)
+
+
+def dp_clip_accumulate_embedding(row_ptr, uniq_ids, rows, cap, norm, C, N, V, D, sum, status=None, ws=None,
+                                 stream=None):
+    _check(lib().dp_clip_accumulate_embedding(_ptr(row_ptr), _ptr(uniq_ids), _ptr(rows), cap, _ptr(norm), C, N,
+                                              V, D, _ptr(sum), _ptr(status), _ptr(ws), _nbytes(ws),
+                                              _stream(stream)),
            "dp_clip_accumulate_embedding")
 
 

@@ -133,58 +133,101 @@ ColSplit col_split(i64 N, i64 numel, bool vec_ok)
     return s;
 }
 
-// One wave per embedding row v.  Lane l binary-searches sample (n0 + l)'s
-// sorted ids for v; the hits are then visited in ascending sample order.
-constexpr int kEmbR = 4;   // columns per lane per pass: the wave covers 256 columns
+// Embedding clipped sum over CSR rows, 64 samples (one wave's lanes) at a
+// time.  The chunk's CSR is inverted into a dense map [V][64] of row indices
+// (-1 where a sample does not hold id v): a fill, then one scatter per stored
+// row.  A wave per id v then reads its 64 map entries with one coalesced load
+// and adds the hit rows in ascending sample order, eight rows' loads in flight
+// at a time, onto the previous chunks' sum.
+constexpr int kChunk = 64;
+constexpr int kEmbBatch = 8;
 
+__global__ void emb_map_fill_kernel(int32_t *__restrict__ map, i64 n4)
+{
+    const i64 i = (i64)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n4) reinterpret_cast<int4 *>(map)[i] = make_int4(-1, -1, -1, -1);
+}
+
+// one workgroup per sample of the chunk: map[uniq[k]][n - n0] = k
+__global__ __launch_bounds__(kThreads) void emb_map_scatter_kernel(
+    const int64_t *__restrict__ row_ptr, const int64_t *__restrict__ uniq, i64 n0, i64 V, i64 cap,
+    int32_t *__restrict__ map, int32_t *status)
+{
+    const i64 n = n0 + blockIdx.x;
+    const i64 lo = row_ptr[n], hi = row_ptr[n + 1];
+    if (hi > cap && threadIdx.x == 0) raise_flag(status, DP_FLAG_CAP);
+    const i64 end = hi < cap ? hi : cap;
+    for (i64 k = lo + threadIdx.x; k < end; k += kThreads) {
+        const int64_t v = uniq[k];
+        if (v < 0 || v >= V) raise_flag(status, DP_FLAG_BAD_INDEX);
+        else map[v * kChunk + blockIdx.x] = (int32_t)k;
+    }
+}
+
+template <int VEC>
 __global__ __launch_bounds__(kThreads) void emb_clipsum_kernel(
-    const int64_t *__restrict__ row_ptr, const int64_t *__restrict__ uniq,
-    const float *__restrict__ rows, const float *__restrict__ norm, float C, i64 N, i64 V, i64 D,
-    float *__restrict__ sum, int32_t *status)
+    const int32_t *__restrict__ map, const float *__restrict__ rows, const float *__restrict__ norm, float C,
+    i64 n0, int nc, i64 V, i64 D, int first, float *__restrict__ sum)
 {
     const int lane = threadIdx.x & 63;
-    const i64 gtid = (i64)blockIdx.x * blockDim.x + threadIdx.x;
-    const i64 nthreads = (i64)gridDim.x * blockDim.x;
-    // stored ids outside [0, V) are reported and never matched
-    const i64 nnz = row_ptr[N];
-    for (i64 e = gtid; e < nnz; e += nthreads)
-        if (uniq[e] < 0 || uniq[e] >= V) raise_flag(status, DP_FLAG_BAD_INDEX);
-
     const i64 v = (i64)blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
     if (v >= V) return;
-    for (i64 d0 = 0; d0 < D; d0 += 64 * kEmbR) {
-        float acc[kEmbR];
+    const int hit = lane < nc ? map[v * kChunk + lane] : -1;
+    const float cn = lane < nc ? clip_factor(norm[n0 + lane], C) : 0.0f;
+    const uint64_t all = __ballot(hit >= 0);
+    for (i64 c0 = 0; c0 < D; c0 += 64 * VEC) {
+        const i64 c = c0 + (i64)VEC * lane;
+        const bool on = c < D;
+        const i64 cc = on ? c : 0;
+        float acc[VEC];
 #pragma unroll
-        for (int q = 0; q < kEmbR; ++q) acc[q] = 0.0f;
-        for (i64 nc = 0; nc < N; nc += 64) {
-            const i64 n = nc + lane;
-            i64 hit = -1;
-            if (n < N) {
-                i64 lo = row_ptr[n], hi = row_ptr[n + 1];
-                while (lo < hi) {
-                    const i64 mid = lo + ((hi - lo) >> 1);
-                    if (uniq[mid] < v) lo = mid + 1;
-                    else hi = mid;
-                }
-                if (lo < row_ptr[n + 1] && uniq[lo] == v) hit = lo;
-            }
-            uint64_t mask = __ballot(hit >= 0);
-            while (mask) {
-                const int b = __ffsll((unsigned long long)mask) - 1;
-                mask &= mask - 1;
-                const i64 k = __shfl(hit, b, 64);
-                const float cn = clip_factor(norm[nc + b], C);
-#pragma unroll
-                for (int q = 0; q < kEmbR; ++q) {
-                    const i64 d = d0 + lane + 64 * q;
-                    if (d < D) acc[q] += cn * rows[k * D + d];
-                }
+        for (int i = 0; i < VEC; ++i) acc[i] = 0.0f;
+        if (!first && on) {
+            if constexpr (VEC == 4) {
+                const float4 q = *reinterpret_cast<const float4 *>(sum + v * D + c);
+                acc[0] = q.x; acc[1] = q.y; acc[2] = q.z; acc[3] = q.w;
+            } else {
+                acc[0] = sum[v * D + c];
             }
         }
+        // batches of the hit lanes in ascending order; slots past the last
+        // hit repeat the first (a valid row) and are not added
+        const int first_hit = all ? __ffsll((unsigned long long)all) - 1 : 0;
+        uint64_t mask = all;
+        while (mask) {
+            int kk[kEmbBatch];
+            float cj[kEmbBatch];
+            bool ok[kEmbBatch];
 #pragma unroll
-        for (int q = 0; q < kEmbR; ++q) {
-            const i64 d = d0 + lane + 64 * q;
-            if (d < D) sum[v * D + d] = acc[q];
+            for (int j = 0; j < kEmbBatch; ++j) {
+                ok[j] = mask != 0;
+                const int b = ok[j] ? __ffsll((unsigned long long)mask) - 1 : first_hit;
+                mask &= mask - 1;
+                kk[j] = __shfl(hit, b, 64);
+                cj[j] = __shfl(cn, b, 64);
+            }
+            float x[kEmbBatch][VEC];
+#pragma unroll
+            for (int j = 0; j < kEmbBatch; ++j) {
+                const float *src = rows + (i64)kk[j] * D + cc;
+                if constexpr (VEC == 4) {
+                    const float4 q = *reinterpret_cast<const float4 *>(src);
+                    x[j][0] = q.x; x[j][1] = q.y; x[j][2] = q.z; x[j][3] = q.w;
+                } else {
+                    x[j][0] = src[0];
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < kEmbBatch; ++j)
+                if (ok[j])
+#pragma unroll
+                    for (int i = 0; i < VEC; ++i) acc[i] += cj[j] * x[j][i];
+        }
+        if (on) {
+            if constexpr (VEC == 4)
+                *reinterpret_cast<float4 *>(sum + v * D + c) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+            else
+                sum[v * D + c] = acc[0];
         }
     }
 }
@@ -267,16 +310,46 @@ extern "C" dp_status dp_clip_accumulate(const float *G, const float *norm, float
     return launch_status();
 }
 
-extern "C" dp_status dp_clip_accumulate_embedding(const int64_t *row_ptr, const int64_t *uniq_ids,
-                                                  const float *rows, const float *norm, float C,
-                                                  int64_t N, int64_t V, int64_t D, float *sum,
-                                                  int32_t *status, hipStream_t stream)
+extern "C" size_t dp_clip_accumulate_embedding_workspace_bytes(int64_t N, int64_t V)
 {
-    DPG_REQUIRE(N >= 0 && V >= 1 && D >= 1 && C > 0.0f, DP_EINVAL);
+    if (N <= 0 || V <= 0) return 0;
+    return (size_t)V * kChunk * sizeof(int32_t);
+}
+
+extern "C" dp_status dp_clip_accumulate_embedding(const int64_t *row_ptr, const int64_t *uniq_ids,
+                                                  const float *rows, int64_t cap, const float *norm, float C,
+                                                  int64_t N, int64_t V, int64_t D, float *sum,
+                                                  int32_t *status, void *ws, size_t ws_bytes,
+                                                  hipStream_t stream)
+{
+    DPG_REQUIRE(N >= 0 && V >= 1 && D >= 1 && cap >= 0 && C > 0.0f, DP_EINVAL);
+    DPG_REQUIRE(V < (i64(1) << 31) / kChunk, DP_EUNSUPPORTED);
     DPG_REQUIRE(row_ptr != nullptr && sum != nullptr, DP_EINVAL);
-    DPG_REQUIRE(N == 0 || (norm != nullptr && uniq_ids != nullptr && rows != nullptr), DP_EINVAL);
-    const unsigned blocks = (unsigned)ceil_div(V, kThreads / 64);
-    emb_clipsum_kernel<<<blocks, kThreads, 0, stream>>>(row_ptr, uniq_ids, rows, norm, C, N, V, D,
-                                                        sum, status);
+    DPG_REQUIRE(N == 0 || norm != nullptr, DP_EINVAL);
+    DPG_REQUIRE(cap == 0 || (uniq_ids != nullptr && rows != nullptr), DP_EINVAL);
+    DPG_REQUIRE(cap < (i64(1) << 31), DP_EUNSUPPORTED);
+    const size_t need = dp_clip_accumulate_embedding_workspace_bytes(N, V);
+    DPG_REQUIRE(ws_bytes >= need && (need == 0 || ws != nullptr), DP_EINVAL);
+    DPG_REQUIRE(need == 0 || aligned(ws, 16), DP_EINVAL);
+    if (N == 0) {
+        zero_fill(sum, V * D, stream);
+        return launch_status();
+    }
+    int32_t *map = (int32_t *)ws;
+    const i64 n4 = V * kChunk / 4;
+    const bool vec = D % 4 == 0 && aligned(rows, 16) && aligned(sum, 16);
+    const unsigned vblocks = (unsigned)ceil_div(V, kThreads / 64);
+    for (i64 n0 = 0; n0 < N; n0 += kChunk) {
+        const int nc = (int)(N - n0 < kChunk ? N - n0 : kChunk);
+        emb_map_fill_kernel<<<(unsigned)ceil_div(n4, kThreads), kThreads, 0, stream>>>(map, n4);
+        emb_map_scatter_kernel<<<(unsigned)nc, kThreads, 0, stream>>>(row_ptr, uniq_ids, n0, V, cap, map,
+                                                                       status);
+        if (vec)
+            emb_clipsum_kernel<4><<<vblocks, kThreads, 0, stream>>>(map, rows, norm, C, n0, nc, V, D, n0 == 0,
+                                                                    sum);
+        else
+            emb_clipsum_kernel<1><<<vblocks, kThreads, 0, stream>>>(map, rows, norm, C, n0, nc, V, D, n0 == 0,
+                                                                    sum);
+    }
     return launch_status();
 }

@@ -10,10 +10,15 @@
 //   Segment starts come from a block scan of the "new id" flags.
 // Pass 2 (one workgroup): exclusive scan of the per-sample distinct counts
 //   into row_ptr.
-// Pass 3 (one workgroup per sample): each (segment, column) sums its
-//   positions in ascending t and writes the CSR row; the sample's squared
-//   norm is a fixed-order block reduction.  No atomics on data.
+// Pass 3 (one wave per sample and segment slot, so the grid fills the chip
+//   even for a small batch): the wave sums the segment's backprop rows in
+//   ascending t, eight positions' loads in flight at a time, lanes over the
+//   columns (four per lane when the rows allow 16- or 8-byte loads), and
+//   writes the CSR row and its squared norm; the sample's norm is then added
+//   over its slots in slot order.  No atomics on data.
 #include "common.hpp"
+
+#include <type_traits>
 
 namespace dpg {
 namespace {
@@ -43,7 +48,9 @@ __device__ int block_exclusive_scan(int v, int *buf, int &total)
 struct EmbWs {
     int32_t *perm;      // [N][T]   positions in sorted order
     int32_t *segstart;  // [N][T+1] first sorted index of each segment, then the end
+    int32_t *segid;     // [N][T]   id of each segment
     int32_t *counts;    // [N]      distinct valid ids
+    float *sqpart;      // [N][T]   squared norm of each segment slot (0 past the last)
 };
 
 __global__ __launch_bounds__(kThreads) void emb_sort_kernel(const int64_t *__restrict__ ids, i64 T,
@@ -105,7 +112,10 @@ __global__ __launch_bounds__(kThreads) void emb_sort_kernel(const int64_t *__res
         const uint64_t k = keys[r];
         if (k == kNoKey) continue;
         perm[r] = (int32_t)(k & 0xffffffffu);
-        if (r == 0 || (keys[r - 1] >> 32) != (k >> 32)) seg[s++] = r;
+        if (r == 0 || (keys[r - 1] >> 32) != (k >> 32)) {
+            w.segid[n * T + s] = (int32_t)(k >> 32);
+            seg[s++] = r;
+        }
     }
     if (tid == 0) {
         seg[nseg] = nvalid;
@@ -142,36 +152,85 @@ __global__ __launch_bounds__(kThreads) void emb_scan_kernel(const int32_t *__res
     }
 }
 
-template <typename T>
-__global__ __launch_bounds__(kThreads) void emb_rows_kernel(
-    const int64_t *__restrict__ ids, const T *__restrict__ B, i64 Tn, i64 D, float scale, EmbWs w,
-    const int64_t *__restrict__ row_ptr, int64_t *__restrict__ uniq, float *__restrict__ rows,
-    i64 cap, float *__restrict__ sqnorm, int32_t *status)
+// VEC consecutive row elements as floats (VEC = 4: one 16-byte fp32 or
+// 8-byte bf16 load, the address aligned to that size).
+template <typename T, int VEC>
+__device__ __forceinline__ void load_vec(const T *p, float (&v)[VEC])
 {
-    __shared__ float red[16];
-    const i64 n = blockIdx.x;
-    const int tid = threadIdx.x;
-    const i64 off = row_ptr[n];
+    if constexpr (VEC == 4 && std::is_same<T, float>::value) {
+        const float4 q = *reinterpret_cast<const float4 *>(p);
+        v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
+    } else if constexpr (VEC == 4) {
+        const uint2 q = *reinterpret_cast<const uint2 *>(p);
+        v[0] = bf16_to_f32((uint16_t)(q.x & 0xffffu)); v[1] = bf16_to_f32((uint16_t)(q.x >> 16));
+        v[2] = bf16_to_f32((uint16_t)(q.y & 0xffffu)); v[3] = bf16_to_f32((uint16_t)(q.y >> 16));
+    } else {
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) v[i] = load_elem<T>(p, i);
+    }
+}
+
+constexpr int kBatch = 8;   // positions whose loads are in flight together
+
+template <typename T, int VEC>
+__global__ __launch_bounds__(64) void emb_rows_kernel(
+    const T *__restrict__ B, i64 Tn, i64 D, float scale, EmbWs w, const int64_t *__restrict__ row_ptr,
+    int64_t *__restrict__ uniq, float *__restrict__ rows, i64 cap, int32_t *status)
+{
+    const i64 n = blockIdx.x / Tn;
+    const int s = (int)(blockIdx.x % Tn);
+    const int lane = threadIdx.x;
     const int u = w.counts[n];
+    if (s >= u) {
+        if (lane == 0) w.sqpart[n * Tn + s] = 0.0f;
+        return;
+    }
+    const i64 k = row_ptr[n] + s;                 // CSR row of this segment
+    if (s == u - 1 && k >= cap && lane == 0) raise_flag(status, DP_FLAG_CAP);
+    const bool keep = k < cap;
     const int32_t *perm = w.perm + n * Tn;
     const int32_t *seg = w.segstart + n * (Tn + 1);
+    const int r0 = seg[s], r1 = seg[s + 1];
+    if (keep && lane == 0) uniq[k] = w.segid[n * Tn + s];
     const T *Bn = B + n * Tn * D;
-    if (off + u > cap && tid == 0) raise_flag(status, DP_FLAG_CAP);
-    for (int s = tid; s < u; s += kThreads)
-        if (off + s < cap) uniq[off + s] = ids[n * Tn + perm[seg[s]]];
     float sq = 0.0f;
-    const i64 work = (i64)u * D;
-    for (i64 idx = tid; idx < work; idx += kThreads) {
-        const int s = (int)(idx / D);
-        const i64 d = idx % D;
-        float acc = 0.0f;
-        for (int r = seg[s]; r < seg[s + 1]; ++r) acc += load_elem<T>(Bn, (i64)perm[r] * D + d);
-        const float g = scale * acc;
-        sq += g * g;
-        if (off + s < cap) rows[(off + s) * D + d] = g;
+    for (i64 c0 = 0; c0 < D; c0 += 64 * VEC) {
+        const i64 c = c0 + (i64)VEC * lane;
+        const bool on = c < D;
+        const i64 cc = on ? c : 0;
+        float acc[VEC];
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) acc[i] = 0.0f;
+        for (int r = r0; r < r1; r += kBatch) {
+            float v[kBatch][VEC];
+#pragma unroll
+            for (int j = 0; j < kBatch; ++j) {
+                const int rj = r + j < r1 ? r + j : r1 - 1;
+                load_vec<T, VEC>(Bn + (i64)perm[rj] * D + cc, v[j]);
+            }
+#pragma unroll
+            for (int j = 0; j < kBatch; ++j)
+                if (r + j < r1)
+#pragma unroll
+                    for (int i = 0; i < VEC; ++i) acc[i] += v[j][i];
+        }
+        if (on) {
+            float g[VEC];
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) {
+                g[i] = scale * acc[i];
+                sq += g[i] * g[i];
+            }
+            if (keep) {
+                if constexpr (VEC == 4)
+                    *reinterpret_cast<float4 *>(rows + k * D + c) = make_float4(g[0], g[1], g[2], g[3]);
+                else
+                    rows[k * D + c] = g[0];
+            }
+        }
     }
-    sq = block_sum(sq, red);
-    if (sqnorm && tid == 0) sqnorm[n] = sq;
+    sq = wave_sum(sq);
+    if (lane == 0) w.sqpart[n * Tn + s] = sq;
 }
 
 EmbWs carve(void *ws, i64 N, i64 T)
@@ -182,7 +241,11 @@ EmbWs carve(void *ws, i64 N, i64 T)
     p += align_up(sizeof(int32_t) * N * T, 256);
     w.segstart = (int32_t *)p;
     p += align_up(sizeof(int32_t) * N * (T + 1), 256);
+    w.segid = (int32_t *)p;
+    p += align_up(sizeof(int32_t) * N * T, 256);
     w.counts = (int32_t *)p;
+    p += align_up(sizeof(int32_t) * N, 256);
+    w.sqpart = (float *)p;
     return w;
 }
 
@@ -194,8 +257,8 @@ using namespace dpg;
 extern "C" size_t dp_grad_sample_embedding_workspace_bytes(int64_t N, int64_t T)
 {
     if (N <= 0 || T < 0) return 0;
-    return align_up(sizeof(int32_t) * N * T, 256) + align_up(sizeof(int32_t) * N * (T + 1), 256) +
-           align_up(sizeof(int32_t) * N, 256);
+    return 2 * align_up(sizeof(int32_t) * N * T, 256) + align_up(sizeof(int32_t) * N * (T + 1), 256) +
+           align_up(sizeof(int32_t) * N, 256) + align_up(sizeof(float) * N * T, 256);
 }
 
 extern "C" dp_status dp_grad_sample_embedding(const int64_t *ids, const void *B, dp_dtype dt,
@@ -224,11 +287,30 @@ extern "C" dp_status dp_grad_sample_embedding(const int64_t *ids, const void *B,
     while (P2 < T) P2 <<= 1;
     emb_sort_kernel<<<(unsigned)N, kThreads, sizeof(uint64_t) * P2, stream>>>(ids, T, V, P2, w, status);
     emb_scan_kernel<<<1, kThreads, 0, stream>>>(w.counts, N, row_ptr);
-    if (dt == DP_F32)
-        emb_rows_kernel<float><<<(unsigned)N, kThreads, 0, stream>>>(
-            ids, (const float *)B, T, D, scale, w, row_ptr, uniq_ids, rows, cap, sqnorm, status);
-    else
-        emb_rows_kernel<uint16_t><<<(unsigned)N, kThreads, 0, stream>>>(
-            ids, (const uint16_t *)B, T, D, scale, w, row_ptr, uniq_ids, rows, cap, sqnorm, status);
+    if (T > 0) {
+        const unsigned grid = (unsigned)(N * T);
+        // four columns per lane when every row starts on a 16-byte (fp32) or
+        // 8-byte (bf16) boundary, and rows likewise
+        const bool vec = D % 4 == 0 && aligned(rows, 16) && aligned(B, dt == DP_F32 ? 16 : 8);
+        if (dt == DP_F32) {
+            if (vec)
+                emb_rows_kernel<float, 4><<<grid, 64, 0, stream>>>((const float *)B, T, D, scale, w, row_ptr,
+                                                                   uniq_ids, rows, cap, status);
+            else
+                emb_rows_kernel<float, 1><<<grid, 64, 0, stream>>>((const float *)B, T, D, scale, w, row_ptr,
+                                                                   uniq_ids, rows, cap, status);
+        } else {
+            if (vec)
+                emb_rows_kernel<uint16_t, 4><<<grid, 64, 0, stream>>>((const uint16_t *)B, T, D, scale, w,
+                                                                      row_ptr, uniq_ids, rows, cap, status);
+            else
+                emb_rows_kernel<uint16_t, 1><<<grid, 64, 0, stream>>>((const uint16_t *)B, T, D, scale, w,
+                                                                      row_ptr, uniq_ids, rows, cap, status);
+        }
+    }
+    if (sqnorm) {
+        if (T > 0) sum_partials(w.sqpart, N, (int)T, sqnorm, stream);
+        else zero_fill(sqnorm, N, stream);
+    }
     return launch_status();
 }

@@ -128,6 +128,7 @@ class DPStep:
                 lb.uniq = torch.empty(max(cap, 1), dtype=torch.int64, device=self.device)
                 lb.rows = torch.empty((max(cap, 1), layer.D), **f32)
                 need_g = dp.dp_grad_sample_embedding_workspace_bytes(N, layer.T)
+                need_c = dp.dp_clip_accumulate_embedding_workspace_bytes(N, layer.V)
             elif isinstance(layer, W.LayerNorm):
                 lb.gW = torch.empty((N, layer.D), **f32)
                 lb.gb = torch.empty((N, layer.D), **f32)
@@ -203,8 +204,9 @@ class DPStep:
                                          self.scale, self.norm, self.C, self.S[name + ".weight"],
                                          self.S.get(name + ".bias"), self.status, lb.ws_clip, stream)
         elif isinstance(layer, W.Embedding):
-            dp.dp_clip_accumulate_embedding(lb.row_ptr, lb.uniq, lb.rows, self.norm, self.C, self.N, layer.V,
-                                            layer.D, self.S[name + ".weight"], self.status, stream)
+            dp.dp_clip_accumulate_embedding(lb.row_ptr, lb.uniq, lb.rows, lb.uniq.shape[0], self.norm, self.C,
+                                            self.N, layer.V, layer.D, self.S[name + ".weight"], self.status,
+                                            lb.ws_clip, stream)
 
     def clip_noise(self, step: int, step_dev=None, stream=None):
         dp.dp_clip_noise_many(self.group, self.group_count, self.N, self.norm, self.C, self.seed, step, step_dev,

@@ -101,8 +101,12 @@ def test_clip_and_noise_validation():
     n = dp.dp_clip_accumulate_workspace_bytes(4096, 10)
     assert n > 0
     assert code_of(dp.dp_clip_accumulate, FAKE, FAKE, 1.0, 4096, 10, FAKE, stream=0) == dp.DP_EINVAL
-    assert code_of(dp.dp_clip_accumulate_embedding, FAKE, FAKE, FAKE, FAKE, 1.0, 2, 0, 4, FAKE,
+    assert code_of(dp.dp_clip_accumulate_embedding, FAKE, FAKE, FAKE, 8, FAKE, 1.0, 2, 0, 4, FAKE,
                    stream=0) == dp.DP_EINVAL
+    nb = dp.dp_clip_accumulate_embedding_workspace_bytes(2, 10)
+    assert nb >= 10 * 64 * 4
+    assert code_of(dp.dp_clip_accumulate_embedding, FAKE, FAKE, FAKE, 8, FAKE, 1.0, 2, 10, 4, FAKE,
+                   stream=0) == dp.DP_EINVAL     # workspace missing
     f = dp.dp_add_noise
     assert code_of(f, FAKE, FAKE, 16, 0, 0, 0, 1.0, math.inf, 4.0, stream=0) == dp.DP_EINVAL  # sigma>0, C=inf
     assert code_of(f, FAKE, FAKE, 16, 0, 0, 0, -1.0, 1.0, 4.0, stream=0) == dp.DP_EINVAL

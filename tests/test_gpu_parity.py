@@ -246,28 +246,34 @@ def test_conv_shapes_bf16(shape):
     assert_rel(sq.cpu().numpy(), rsq, 1e-4, "conv bf16 sqnorm")
 
 
-def run_embedding(ids, B, V, cap=None, scale=1.0):
+def run_embedding(ids, B, V, cap=None, scale=1.0, dt=None):
     N, T = ids.shape
     D = B.shape[2]
     cap = N * T if cap is None else cap
+    dt = dp.DP_F32 if dt is None else dt
     idt = torch.from_numpy(ids).to(DEV)
     Bt = torch.from_numpy(B.astype(np.float32)).to(DEV)
+    if dt == dp.DP_BF16:
+        Bt = Bt.to(torch.bfloat16)
     rp = torch.empty(N + 1, dtype=torch.int64, device=DEV)
     uq = torch.full((max(cap, 1),), -7, dtype=torch.int64, device=DEV)
     rows = torch.zeros((max(cap, 1), D), device=DEV)
     sq = torch.empty(N, device=DEV)
     st = torch.zeros(1, dtype=torch.int32, device=DEV)
     ws = torch.empty(max(dp.dp_grad_sample_embedding_workspace_bytes(N, T), 1), dtype=torch.uint8, device=DEV)
-    dp.dp_grad_sample_embedding(idt, Bt, dp.DP_F32, N, T, V, D, scale, rp, uq, rows, cap, sq, st, ws)
+    dp.dp_grad_sample_embedding(idt, Bt, dt, N, T, V, D, scale, rp, uq, rows, cap, sq, st, ws)
     torch.cuda.synchronize()
     return rp.cpu().numpy(), uq.cpu().numpy(), rows.cpu().numpy(), sq.cpu().numpy(), int(st.item())
 
 
-@pytest.mark.parametrize("case", ["zipf", "truncated", "all_equal", "all_distinct", "T1", "long"])
-def test_embedding_cases(case):
-    say("embedding", case)
+@pytest.mark.parametrize("D", [37, 100])
+@pytest.mark.parametrize("case", ["zipf", "truncated", "all_equal", "all_distinct", "T1", "long", "batch130",
+                                  "bf16"])
+def test_embedding_cases(case, D):
+    say("embedding", case, D)
     r = np.random.default_rng(11)
-    V, D = 1000, 37
+    V = 1000
+    dt = dp.DP_F32
     if case == "zipf":
         ids = np.minimum(r.zipf(1.1, (9, 256)), V) - 1
     elif case == "truncated":
@@ -279,12 +285,20 @@ def test_embedding_cases(case):
         ids = np.stack([r.permutation(V)[:300] for _ in range(4)])
     elif case == "T1":
         ids = r.integers(0, V, (8, 1))
+    elif case == "batch130":        # three 64-sample chunks in the clipped sum
+        ids = np.minimum(r.zipf(1.1, (130, 64)), V) - 1
+    elif case == "bf16":
+        ids = np.minimum(r.zipf(1.1, (9, 100)), V) - 1
+        dt = dp.DP_BF16
     else:
         ids = r.integers(0, 40, (2, 4096))
     ids = ids.astype(np.int64)
     B = r.standard_normal(ids.shape + (D,))
-    B32 = B.astype(np.float32).astype(np.float64)
-    rp, uq, rows, sq, st = run_embedding(ids, B, V, scale=0.5)
+    if dt == dp.DP_BF16:
+        B32 = torch.from_numpy(B.astype(np.float32)).to(torch.bfloat16).float().numpy().astype(np.float64)
+    else:
+        B32 = B.astype(np.float32).astype(np.float64)
+    rp, uq, rows, sq, st = run_embedding(ids, B, V, scale=0.5, dt=dt)
     rrp, ruq, rrows = oracle.embedding_grad(ids, B32, V, 0.5)
     assert st == 0
     np.testing.assert_array_equal(rp, rrp)
@@ -296,10 +310,12 @@ def test_embedding_cases(case):
     norm = np.sqrt(rsq)
     C = float(np.median(norm))
     c = oracle.clip_factors(norm.astype(np.float32).astype(np.float64), C)
-    S = torch.empty((V, D), device=DEV)
+    S = torch.full((V, D), 7.0, device=DEV)
+    N = ids.shape[0]
+    wsc = torch.empty(dp.dp_clip_accumulate_embedding_workspace_bytes(N, V), dtype=torch.uint8, device=DEV)
     dp.dp_clip_accumulate_embedding(torch.from_numpy(rp).to(DEV), torch.from_numpy(uq).to(DEV),
-                                    torch.from_numpy(rows).to(DEV), torch.from_numpy(norm.astype(np.float32)).to(DEV),
-                                    C, ids.shape[0], V, D, S)
+                                    torch.from_numpy(rows).to(DEV), rows.shape[0],
+                                    torch.from_numpy(norm.astype(np.float32)).to(DEV), C, N, V, D, S, None, wsc)
     assert_g12(S.cpu().numpy(), oracle.clip_sum_embedding(rrp, ruq, rrows, c, V), 1e-4, "dense S")
 
 
@@ -313,6 +329,19 @@ def test_embedding_flags():
     assert st & dp.DP_FLAG_CAP
     rrp, _, _ = oracle.embedding_grad(ids, B, 50)
     np.testing.assert_array_equal(rp, rrp)
+    # the clipped sum over the truncated CSR: flagged, and only the stored rows count
+    say("embedding clip cap")
+    S = torch.empty((50, 4), device=DEV)
+    stt = torch.zeros(1, dtype=torch.int32, device=DEV)
+    wsc = torch.empty(dp.dp_clip_accumulate_embedding_workspace_bytes(3, 50), dtype=torch.uint8, device=DEV)
+    dp.dp_clip_accumulate_embedding(torch.from_numpy(rp).to(DEV), torch.from_numpy(uq).to(DEV),
+                                    torch.from_numpy(rows).to(DEV), 10, torch.ones(3, device=DEV), 1e9, 3, 50, 4, S,
+                                    stt, wsc)
+    assert int(stt.item()) & dp.DP_FLAG_CAP
+    ref = np.zeros((50, 4))
+    for k in range(10):
+        ref[uq[k]] += rows[k]
+    assert_g12(S.cpu().numpy(), ref, 1e-5, "clip over capped CSR")
     # an id outside [0, V): flagged and left out
     say("embedding bad id")
     bad = ids.copy(); bad[1, 3] = 50; bad[2, 0] = -1
