@@ -73,7 +73,7 @@ def call_costs(st):
             else:
                 out["grad:" + L.name] = (N * L.T * (L.d_in + L.d_out) * e + grads + N * 4,
                                          2 * N * L.T * L.d_in * L.d_out,
-                                         "bf16_per_sample_kernel" if bf_mfma else "per_sample_gemm_kernel",
+                                         "bf16_per_sample_kernel" if bf_mfma else "ps_gemm_kernel",
                                          "bf16" if bf_mfma else "f32")
             if lb.clip_mode == "fused":
                 out["clip:" + L.name] = (N * L.T * (L.d_in + L.d_out) * e + (L.d_out * L.d_in + bias) * 4,
@@ -118,7 +118,7 @@ KERNEL_SOURCES = {
     "outer_kernel": ["paper_2109_12298_amd/csrc/linear.hip"],
     "bf16_per_sample_kernel": ["paper_2109_12298_amd/csrc/linear_bf16.hip"],
     "bf16_clipsum_kernel": ["paper_2109_12298_amd/csrc/linear_bf16.hip"],
-    "per_sample_gemm_kernel": ["paper_2109_12298_amd/csrc/linear.hip", "paper_2109_12298_amd/csrc/mfma_tile.hpp"],
+    "ps_gemm_kernel": ["paper_2109_12298_amd/csrc/linear.hip"],
     "clipsum_gemm_kernel": ["paper_2109_12298_amd/csrc/linear.hip", "paper_2109_12298_amd/csrc/mfma_tile.hpp"],
     "conv_per_sample_kernel": ["paper_2109_12298_amd/csrc/conv2d.hip", "paper_2109_12298_amd/csrc/mfma_tile.hpp"],
     "colsum_kernel": ["paper_2109_12298_amd/csrc/clip.hip"],

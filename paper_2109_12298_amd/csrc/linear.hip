@@ -126,65 +126,133 @@ __global__ __launch_bounds__(kThreads) void outer_kernel(const T *__restrict__ A
 }
 
 // ---------------------------------------------------------------------------
-// T > 1: per-sample GEMM on MFMA.  Block = (sample n, tile of gW_n).
+// T > 1: per-sample GEMM on MFMA.  Block = (sample n, 64 x 64 tile of gW_n).
+// MFMA rows run over j (d_in, the contiguous index of gW), so each lane ends
+// with four consecutive entries of a row of gW and stores them as one float4;
+// columns run over i (d_out).  Both operands are staged K-major exactly as
+// they lie in memory ([t][feature]), with 16-byte loads when the rows allow;
+// the next chunk of positions is loaded into registers while the current
+// one is multiplied.
 // ---------------------------------------------------------------------------
-template <typename T>
-__global__ __launch_bounds__(kThreads) void per_sample_gemm_kernel(
-    const T *__restrict__ A, const T *__restrict__ B, i64 Tn, i64 din, i64 dout, int tiles_n,
+constexpr int kPM = 64, kPN = 64, kPK = 32;
+
+template <typename T, int VEC>
+__device__ __forceinline__ void load_group(const T *p, float (&v)[VEC])
+{
+    if constexpr (VEC == 4) {
+        const float4 q = load4<T>(p, 0);
+        v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
+    } else {
+        v[0] = load_elem<T>(p, 0);
+    }
+}
+
+template <typename T, int VEC>
+__global__ __launch_bounds__(kThreads) void ps_gemm_kernel(
+    const T *__restrict__ A, const T *__restrict__ B, i64 Tn, i64 din, i64 dout, int tiles_j,
     int tiles, float scale, float *__restrict__ gW, float *__restrict__ gb,
     float *__restrict__ partial)
 {
-    __shared__ float As[kBK * kBM];
-    __shared__ float Bs[kBK * kBN];
+    __shared__ float As[kPK * kPM];   // [t][j]
+    __shared__ float Bs[kPK * kPN];   // [t][i]
     __shared__ float red[16];
     const i64 bsw = xcd_swizzle(blockIdx.x, gridDim.x);
     const i64 n = bsw / tiles;
     const int tile = (int)(bsw % tiles);
-    const int tm = tile / tiles_n, tn = tile % tiles_n;
-    const i64 m0 = (i64)tm * kBM, n0 = (i64)tn * kBN;
+    const int ti = tile / tiles_j, tj = tile % tiles_j;
+    const i64 j0 = (i64)tj * kPM, i0 = (i64)ti * kPN;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = (wave >> 1) * (kBM / 2), wn = (wave & 1) * (kBN / 2);
-    const T *Bn = B + n * Tn * dout;
+    const int wm = (wave & 1) * 32, wn = (wave >> 1) * 32;
     const T *An = A + n * Tn * din;
-    const bool do_bias = gb != nullptr && tn == 0;
+    const T *Bn = B + n * Tn * dout;
+    const bool do_bias = gb != nullptr && tj == 0;
 
-    MfmaTile<kBM, kBN> t;
-    t.zero();
+    // staging: VEC-wide groups, group g = tid + 256 q at row g / GPR
+    constexpr int GPR = kPM / VEC;
+    constexpr int NG = kPK * kPM / VEC / kThreads;
+    static_assert(kPM == kPN && NG * VEC * kThreads == kPK * kPM, "staging map");
+    float ra[NG][VEC], rb[NG][VEC];
+    auto load = [&](i64 t0) {
+#pragma unroll
+        for (int q = 0; q < NG; ++q) {
+            const int g = tid + kThreads * q;
+            const int r = g / GPR, c = (g % GPR) * VEC;
+            const i64 t = t0 + r;
+            const bool okA = t < Tn && j0 + c < din;   // VEC = 4: d_in % 4 == 0, whole group in or out
+            const bool okB = t < Tn && i0 + c < dout;
+            load_group<T, VEC>(An + (okA ? t * din + j0 + c : 0), ra[q]);
+            load_group<T, VEC>(Bn + (okB ? t * dout + i0 + c : 0), rb[q]);
+#pragma unroll
+            for (int v = 0; v < VEC; ++v) {
+                ra[q][v] = okA ? ra[q][v] : 0.0f;
+                rb[q][v] = okB ? rb[q][v] : 0.0f;
+            }
+        }
+    };
+    auto store = [&]() {
+#pragma unroll
+        for (int q = 0; q < NG; ++q) {
+            const int g = tid + kThreads * q;
+            const int r = g / GPR, c = (g % GPR) * VEC;
+            if constexpr (VEC == 4) {
+                *reinterpret_cast<float4 *>(As + r * kPM + c) = make_float4(ra[q][0], ra[q][1], ra[q][2], ra[q][3]);
+                *reinterpret_cast<float4 *>(Bs + r * kPN + c) = make_float4(rb[q][0], rb[q][1], rb[q][2], rb[q][3]);
+            } else {
+                As[r * kPM + c] = ra[q][0];
+                Bs[r * kPN + c] = rb[q][0];
+            }
+        }
+    };
+
+    f32x16 acc;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
     float bias_acc = 0.0f;
-
-    for (i64 k0 = 0; k0 < Tn; k0 += kBK) {
-        for (int e = tid; e < kBK * kBM; e += kThreads) {
-            const int kk = e / kBM, ii = e % kBM;
-            const i64 k = k0 + kk, i = m0 + ii;
-            As[e] = (k < Tn && i < dout) ? load_elem<T>(Bn, k * dout + i) : 0.0f;
-        }
-        for (int e = tid; e < kBK * kBN; e += kThreads) {
-            const int kk = e / kBN, jj = e % kBN;
-            const i64 k = k0 + kk, j = n0 + jj;
-            Bs[e] = (k < Tn && j < din) ? load_elem<T>(An, k * din + j) : 0.0f;
-        }
+    load(0);
+    for (i64 t0 = 0; t0 < Tn; t0 += kPK) {
+        __syncthreads();   // previous chunk consumed
+        store();
         __syncthreads();
-        t.template mma<kBK>(As, kBM, Bs, kBN, wm, wn, lane);
-        if (do_bias && tid < kBM) {
+        if (t0 + kPK < Tn) load(t0 + kPK);
+        const int li = lane & 31, lk = lane >> 5;
+#pragma unroll
+        for (int kk = 0; kk < kPK; kk += 2) {
+            const float a = As[(kk + lk) * kPM + wm + li];
+            const float b = Bs[(kk + lk) * kPN + wn + li];
+            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, acc, 0, 0, 0);
+        }
+        if (do_bias && tid < kPN) {
 #pragma unroll 8
-            for (int kk = 0; kk < kBK; ++kk) bias_acc += As[kk * kBM + tid];
+            for (int kk = 0; kk < kPK; ++kk) bias_acc += Bs[kk * kPN + tid];
         }
-        __syncthreads();
     }
 
+    // acc[r] holds gW[i][j], j = j0 + wm + 8 (r / 4) + 4 (lane / 32) + r % 4, i = i0 + wn + lane % 32
     float sq = 0.0f;
-    float *G = gW + n * dout * din;
-    t.for_each(wm, wn, lane, [&](int r, int c, float v) {
-        const i64 i = m0 + r, j = n0 + c;
-        if (i < dout && j < din) {
-            const float g = scale * v;
-            G[i * din + j] = g;
-            sq += g * g;
+    const i64 i = i0 + wn + (lane & 31);
+    if (i < dout) {
+        float *G = gW + n * dout * din + i * din;
+#pragma unroll
+        for (int rb4 = 0; rb4 < 4; ++rb4) {
+            const i64 j = j0 + wm + 8 * rb4 + 4 * (lane >> 5);
+            const float g0 = scale * acc[4 * rb4 + 0], g1 = scale * acc[4 * rb4 + 1];
+            const float g2 = scale * acc[4 * rb4 + 2], g3 = scale * acc[4 * rb4 + 3];
+            if (VEC == 4) {
+                if (j < din) {
+                    *reinterpret_cast<float4 *>(G + j) = make_float4(g0, g1, g2, g3);
+                    sq += g0 * g0 + g1 * g1 + g2 * g2 + g3 * g3;
+                }
+            } else {
+                if (j + 0 < din) { G[j + 0] = g0; sq += g0 * g0; }
+                if (j + 1 < din) { G[j + 1] = g1; sq += g1 * g1; }
+                if (j + 2 < din) { G[j + 2] = g2; sq += g2 * g2; }
+                if (j + 3 < din) { G[j + 3] = g3; sq += g3 * g3; }
+            }
         }
-    });
-    if (do_bias && tid < kBM && m0 + tid < dout) {
+    }
+    if (do_bias && tid < kPN && i0 + tid < dout) {
         const float g = scale * bias_acc;
-        gb[n * dout + m0 + tid] = g;
+        gb[n * dout + i0 + tid] = g;
         sq += g * g;
     }
     sq = block_sum(sq, red);
@@ -305,7 +373,7 @@ extern "C" size_t dp_grad_sample_linear_workspace_bytes(int64_t N, int64_t T, in
     (void)dt;
     if (N <= 0 || T <= 1 || d_in <= 0 || d_out <= 0) return 0;
     // enough for either path (the 64x64 fp32-MFMA tiles outnumber the 128x128 bf16 ones)
-    const i64 tiles = ceil_div(d_in, kBN) * ceil_div(d_out, kBM);
+    const i64 tiles = ceil_div(d_in, kPM) * ceil_div(d_out, kPN);
     return (size_t)(N * tiles) * sizeof(float);
 }
 
@@ -362,15 +430,30 @@ extern "C" dp_status dp_grad_sample_linear(const void *A, const void *B, dp_dtyp
             sum_partials(partial, N, bf16_tiles(d_in, d_out), sqnorm, stream);
         return launch_status();
     }
-    const int tiles_n = (int)ceil_div(d_in, kBN);
-    const int tiles = (int)ceil_div(d_out, kBM) * tiles_n;
+    const int tiles_j = (int)ceil_div(d_in, kPM);
+    const int tiles = (int)ceil_div(d_out, kPN) * tiles_j;
     const dim3 grid((unsigned)(N * tiles));
-    if (dt == DP_F32)
-        per_sample_gemm_kernel<float><<<grid, kThreads, 0, stream>>>(
-            (const float *)A, (const float *)B, T, d_in, d_out, tiles_n, tiles, scale, gW, gb, partial);
-    else
-        per_sample_gemm_kernel<uint16_t><<<grid, kThreads, 0, stream>>>(
-            (const uint16_t *)A, (const uint16_t *)B, T, d_in, d_out, tiles_n, tiles, scale, gW, gb, partial);
+    // 16-byte (fp32) / 8-byte (bf16) operand loads and float4 stores when
+    // every row starts on such a boundary
+    const size_t ea = dt == DP_F32 ? 16 : 8;
+    const bool vec = d_in % 4 == 0 && d_out % 4 == 0 && aligned(A, ea) && aligned(B, ea) && aligned(gW, 16);
+    if (dt == DP_F32) {
+        if (vec)
+            ps_gemm_kernel<float, 4><<<grid, kThreads, 0, stream>>>(
+                (const float *)A, (const float *)B, T, d_in, d_out, tiles_j, tiles, scale, gW, gb, partial);
+        else
+            ps_gemm_kernel<float, 1><<<grid, kThreads, 0, stream>>>(
+                (const float *)A, (const float *)B, T, d_in, d_out, tiles_j, tiles, scale, gW, gb, partial);
+    } else {
+        if (vec)
+            ps_gemm_kernel<uint16_t, 4><<<grid, kThreads, 0, stream>>>(
+                (const uint16_t *)A, (const uint16_t *)B, T, d_in, d_out, tiles_j, tiles, scale, gW, gb,
+                partial);
+        else
+            ps_gemm_kernel<uint16_t, 1><<<grid, kThreads, 0, stream>>>(
+                (const uint16_t *)A, (const uint16_t *)B, T, d_in, d_out, tiles_j, tiles, scale, gW, gb,
+                partial);
+    }
     if (sqnorm)
         sum_partials(partial, N, tiles, sqnorm, stream);
     return launch_status();

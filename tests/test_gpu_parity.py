@@ -115,7 +115,9 @@ def test_add_noise_matches_oracle_and_is_resumable():
 LINEAR_SHAPES = [(1, 1, 1, 1), (3, 1, 37, 13), (2, 2, 5, 3), (4, 5, 37, 13), (3, 33, 65, 70),
                  (2, 70, 130, 64), (5, 1, 4096, 10), (2, 17, 3, 129),
                  # feature sizes that are multiples of 8: the bf16 MFMA path for bf16 inputs
-                 (1, 2, 8, 8), (3, 33, 136, 72), (2, 130, 264, 392), (2, 64, 128, 128), (9, 16, 256, 24)]
+                 (1, 2, 8, 8), (3, 33, 136, 72), (2, 130, 264, 392), (2, 64, 128, 128), (9, 16, 256, 24),
+                 # multiples of 4 but not 8: 16-byte fp32 / 8-byte bf16 loads on the fp32-MFMA path
+                 (3, 40, 100, 20), (2, 256, 100, 400)]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
