@@ -76,10 +76,15 @@ def call_costs(st):
                                          "bf16_per_sample_kernel" if bf_mfma else "ps_gemm_kernel",
                                          "bf16" if bf_mfma else "f32")
             if lb.clip_mode == "fused":
-                out["clip:" + L.name] = (N * L.T * (L.d_in + L.d_out) * e + (L.d_out * L.d_in + bias) * 4,
-                                         2 * N * L.T * L.d_in * L.d_out,
-                                         "bf16_clipsum_kernel" if bf_mfma else "clipsum_gemm_kernel",
-                                         "bf16" if bf_mfma else "f32")
+                # all fused Linear layers' weight sums share one grouped call; their
+                # bias sums are column reductions of the stored bias gradients
+                grouped = bf and L.T % 32 == 0 and L.d_in % 8 == 0 and L.d_out % 8 == 0
+                b0, f0, _, _ = out.get("clip:linears", (0, 0, None, None))
+                out["clip:linears"] = (b0 + N * L.T * (L.d_in + L.d_out) * e + L.d_out * L.d_in * 4,
+                                       f0 + 2 * N * L.T * L.d_in * L.d_out,
+                                       "bf16_clipsum_many_kernel" if grouped else "clipsum_gemm_kernel",
+                                       "bf16" if grouped else "f32")
+                col_bytes += N * bias * 4
             else:
                 col_bytes += grads
         elif isinstance(L, W.Conv2d):
@@ -118,6 +123,7 @@ KERNEL_SOURCES = {
     "outer_kernel": ["paper_2109_12298_amd/csrc/linear.hip"],
     "bf16_per_sample_kernel": ["paper_2109_12298_amd/csrc/linear_bf16.hip"],
     "bf16_clipsum_kernel": ["paper_2109_12298_amd/csrc/linear_bf16.hip"],
+    "bf16_clipsum_many_kernel": ["paper_2109_12298_amd/csrc/clipsum_many.hip"],
     "ps_gemm_kernel": ["paper_2109_12298_amd/csrc/linear.hip"],
     "clipsum_gemm_kernel": ["paper_2109_12298_amd/csrc/linear.hip", "paper_2109_12298_amd/csrc/mfma_tile.hpp"],
     "conv_per_sample_kernel": ["paper_2109_12298_amd/csrc/conv2d.hip", "paper_2109_12298_amd/csrc/mfma_tile.hpp"],
@@ -244,6 +250,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="mnist_cnn")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--clip-mode", default="auto", choices=["auto", "fused", "colreduce"],
+                    help="clipped-sum route of Linear layers (default: per layer by modelled cost)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--breakdown", action="store_true", help="print per-call event times to stderr")
     ap.add_argument("--eager", action="store_true", help="time eager launches instead of graph replays")
@@ -271,7 +279,7 @@ def main():
     inputs = W.make_inputs(wl)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    st = DPStep(wl, inputs, dev)
+    st = DPStep(wl, inputs, dev, clip_mode=args.clip_mode)
     stream = torch.cuda.current_stream(dev)
     costs = call_costs(st)
 

@@ -201,6 +201,35 @@ dp_status dp_clip_accumulate_linear(const void *A, const void *B, dp_dtype dt, i
                                     int32_t *status, void *ws, size_t ws_bytes,
                                     hipStream_t stream);
 
+/* One Linear layer of dp_clip_accumulate_linear_many: the arguments of
+ * dp_clip_accumulate_linear that differ between layers. */
+typedef struct dp_linear_clip {
+    const void *A;       /* activations [N][T][d_in] */
+    const void *B;       /* backprops [N][T][d_out] */
+    int64_t T, d_in, d_out;
+    float scale;         /* s */
+    float *sumW;         /* fp32 [d_out][d_in] clipped sum of the weight gradients */
+    float *sumb;         /* fp32 [d_out] clipped sum of the bias gradients, or NULL */
+} dp_linear_clip;
+
+/* dp_clip_accumulate_linear for `count` layers that share N, the norms, C
+ * and dtype (items: a host array read during the call only), with the same
+ * results: sumW = s * sum_n c_n * B_n^T A_n, sumb = s * sum_n c_n * sum_t
+ * B_n[t] (section 1: clip each sample's gradient, then add).  bf16 layers
+ * with T a multiple of 32, d_in and d_out multiples of 8, and 16-byte aligned
+ * A, B, sumW share one launch (at most 16 layers per launch; each workgroup
+ * holds a 256 x 128 output tile over the whole N*T sum, with the clip factor
+ * applied in fp32 sample by sample, so no partial sums are written); every
+ * other layer runs dp_clip_accumulate_linear's kernels, one after another on
+ * `stream`, sharing the workspace.  Validation as dp_clip_accumulate_linear;
+ * the workspace is the size dp_clip_accumulate_linear_many_workspace_bytes
+ * reports for the same items (0 when every layer takes the grouped launch). */
+size_t dp_clip_accumulate_linear_many_workspace_bytes(const dp_linear_clip *items, int32_t count,
+                                                      dp_dtype dt, int64_t N);
+dp_status dp_clip_accumulate_linear_many(const dp_linear_clip *items, int32_t count, dp_dtype dt,
+                                         int64_t N, const float *norm, float C, int32_t *status,
+                                         void *ws, size_t ws_bytes, hipStream_t stream);
+
 /* Dense clipped sum of CSR embedding gradients (as dp_grad_sample_embedding
  * writes them): sum[v][:] = sum_n c_n * (sample n's row for id v, if any),
  * n ascending; rows no sample touched are written as zeros.

@@ -50,6 +50,8 @@ SIGNATURES = {
     "dp_clip_accumulate_linear_workspace_bytes": (_SZ, [_I64, _I64, _I64, _I64, _ST]),
     "dp_clip_accumulate_linear": (_ST, [_P, _P, _ST, _I64, _I64, _I64, _I64, _F, _P, _F, _P, _P, _P, _P,
                                         _SZ, _P]),
+    "dp_clip_accumulate_linear_many_workspace_bytes": (_SZ, [_P, _I32, _ST, _I64]),
+    "dp_clip_accumulate_linear_many": (_ST, [_P, _I32, _ST, _I64, _P, _F, _P, _P, _SZ, _P]),
     "dp_clip_accumulate_embedding_workspace_bytes": (_SZ, [_I64, _I64]),
     "dp_clip_accumulate_embedding": (_ST, [_P, _P, _P, _I64, _P, _F, _I64, _I64, _I64, _P, _P, _P, _SZ, _P]),
     "dp_clip_noise_many_workspace_bytes": (_SZ, [_P, _I32, _I64]),
@@ -82,6 +84,26 @@ def make_params(entries):
         arr[i].numel = int(numel)
         arr[i].param_index = int(pidx)
         arr[i].flags = DP_PARAM_REDUCE if g is not None else 0
+    return arr
+
+
+class DPLinearClip(ctypes.Structure):
+    """struct dp_linear_clip of dpgrad.h."""
+    _fields_ = [("A", ctypes.c_void_p), ("B", ctypes.c_void_p), ("T", ctypes.c_int64), ("d_in", ctypes.c_int64),
+                ("d_out", ctypes.c_int64), ("scale", ctypes.c_float), ("sumW", ctypes.c_void_p),
+                ("sumb", ctypes.c_void_p)]
+
+
+def make_linear_clips(entries):
+    """A dp_linear_clip array from (A, B, T, d_in, d_out, scale, sumW, sumb) tuples."""
+    arr = (DPLinearClip * max(len(entries), 1))()
+    for i, (A, B, T, d_in, d_out, scale, sumW, sumb) in enumerate(entries):
+        arr[i].A = _ptr(A)
+        arr[i].B = _ptr(B)
+        arr[i].T, arr[i].d_in, arr[i].d_out = int(T), int(d_in), int(d_out)
+        arr[i].scale = float(scale)
+        arr[i].sumW = _ptr(sumW)
+        arr[i].sumb = _ptr(sumb)
     return arr
 
 
@@ -248,6 +270,16 @@ def dp_clip_accumulate_linear(A, B, dt, N, T, d_in, d_out, scale, norm, C, sumW,
                                            _ptr(sumW), _ptr(sumb), _ptr(status), _ptr(ws), _nbytes(ws),
                                            _stream(stream)),
            "dp_clip_accumulate_linear")
+
+
+def dp_clip_accumulate_linear_many_workspace_bytes(items, count, dt, N) -> int:
+    return lib().dp_clip_accumulate_linear_many_workspace_bytes(ctypes.cast(items, ctypes.c_void_p), count, dt, N)
+
+
+def dp_clip_accumulate_linear_many(items, count, dt, N, norm, C, status=None, ws=None, stream=None):
+    _check(lib().dp_clip_accumulate_linear_many(ctypes.cast(items, ctypes.c_void_p), count, dt, N, _ptr(norm), C,
+                                                _ptr(status), _ptr(ws), _nbytes(ws), _stream(stream)),
+           "dp_clip_accumulate_linear_many")
 
 
 def dp_clip_accumulate_embedding_workspace_bytes(N, V) -> int:

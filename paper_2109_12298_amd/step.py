@@ -30,13 +30,14 @@ from . import workloads as W
 
 # Effective rates measured on MI355X for the clipped-sum route choice (not
 # spec peaks): the column reduction streams at ~4.5 TB/s; the fused GEMM
-# reaches ~60 TFLOP/s on fp32 MFMA and ~190 TFLOP/s on the bf16 MFMA path
-# (it is latency-bound at these tile counts); each extra launch of the fused
-# route (the GEMM and its split reduction) costs ~3 us next to the grouped
-# column reduction, which all tensors share.
+# reaches ~60 TFLOP/s on fp32 MFMA, ~190 TFLOP/s on the single-layer bf16
+# path and ~650 TFLOP/s in the grouped bf16 launch (T a multiple of 32,
+# feature sizes multiples of 8); each extra launch of the fused route costs
+# ~3 us next to the grouped column reduction, which all tensors share.
 HBM_BYTES_PER_S = 4.5e12
 FUSED_FLOPS_PER_S = {W.F32: 60e12, W.BF16: 60e12}
-BF16_FLOPS_PER_S = 190e12   # bf16 inputs with T > 1 and feature sizes that are multiples of 8
+BF16_FLOPS_PER_S = 190e12
+BF16_GROUPED_FLOPS_PER_S = 650e12
 LAUNCH_S = 3e-6
 
 
@@ -75,7 +76,8 @@ def linear_clip_mode(layer: W.Linear, N: int, dtype: str) -> str:
     """'fused' (B^T diag(c) A from A and B) or 'colreduce' (read the stored grads)."""
     elt = 2 if dtype == W.BF16 else 4
     bf16_mfma = dtype == W.BF16 and layer.T > 1 and layer.d_in % 8 == 0 and layer.d_out % 8 == 0
-    peak = BF16_FLOPS_PER_S if bf16_mfma else FUSED_FLOPS_PER_S[dtype]
+    grouped = bf16_mfma and layer.T % 32 == 0
+    peak = BF16_GROUPED_FLOPS_PER_S if grouped else BF16_FLOPS_PER_S if bf16_mfma else FUSED_FLOPS_PER_S[dtype]
     fused = (2.0 * N * layer.T * layer.d_in * layer.d_out / peak
              + N * layer.T * (layer.d_in + layer.d_out) * elt / HBM_BYTES_PER_S + 2 * LAUNCH_S)
     col = N * layer.n_params * 4 / HBM_BYTES_PER_S
@@ -112,9 +114,6 @@ class DPStep:
                 lb.gb = torch.empty((N, layer.d_out), **f32) if layer.bias else None
                 lb.clip_mode = linear_clip_mode(layer, N, wl.dtype) if clip_mode == "auto" else clip_mode
                 need_g = dp.dp_grad_sample_linear_workspace_bytes(N, layer.T, layer.d_in, layer.d_out, self.dt)
-                if lb.clip_mode == "fused":
-                    need_c = dp.dp_clip_accumulate_linear_workspace_bytes(N, layer.T, layer.d_in, layer.d_out,
-                                                                          self.dt)
             elif isinstance(layer, W.Conv2d):
                 lb.gW = torch.empty((N, layer.c_out, layer.c_in) + tuple(layer.k), **f32)
                 lb.gb = torch.empty((N, layer.c_out), **f32) if layer.bias else None
@@ -146,6 +145,19 @@ class DPStep:
         for name, shape in self.params:
             self.S[name] = torch.empty(shape, **f32)
             self.out[name] = torch.empty(shape, **f32)
+        # the fused Linear clipped sums (B^T diag(c) A) run as one grouped call
+        self.fused_linear = [i for i, lb in enumerate(self.layers)
+                             if isinstance(lb.layer, W.Linear) and lb.clip_mode == "fused"]
+        ents = []
+        for i in self.fused_linear:
+            lb = self.layers[i]
+            L = lb.layer
+            # the bias sums are column reductions of the stored per-sample bias
+            # gradients (N x d_out values) in the grouped clip/noise call
+            ents.append((lb.A, lb.B, L.T, L.d_in, L.d_out, self.scale, self.S[L.name + ".weight"], None))
+        self.linear_items = dp.make_linear_clips(ents)
+        need = dp.dp_clip_accumulate_linear_many_workspace_bytes(self.linear_items, len(ents), self.dt, N)
+        self.ws_linear = torch.empty(max(need, 256), dtype=torch.uint8, device=self.device)
         # the grouped clip/noise call: per-sample grads for column-reduced tensors
         entries = []
         for pidx, (name, shape) in enumerate(self.params):
@@ -166,7 +178,7 @@ class DPStep:
                 continue
             if isinstance(lb.layer, W.Embedding):
                 return None
-            if isinstance(lb.layer, W.Linear) and lb.clip_mode == "fused":
+            if isinstance(lb.layer, W.Linear) and lb.clip_mode == "fused" and key == "weight":
                 return None
             return lb.gW if key == "weight" else lb.gb
         raise KeyError(pname)
@@ -194,16 +206,18 @@ class DPStep:
     def norms(self, stream=None):
         dp.dp_per_sample_norms(self.sqnorm, len(self.layers), self.N, self.norm, self.status, stream)
 
+    def linear_clip_sums(self, stream=None):
+        """The fused Linear layers' clipped sums, in one grouped call."""
+        if self.fused_linear:
+            dp.dp_clip_accumulate_linear_many(self.linear_items, len(self.fused_linear), self.dt, self.N, self.norm,
+                                              self.C, self.status, self.ws_linear, stream)
+
     def fused_clip_sum(self, i: int, stream=None):
-        """Clipped sums formed without reading per-sample grads (fused Linear, Embedding)."""
+        """Clipped sums formed without reading per-sample grads (Embedding)."""
         lb = self.layers[i]
         layer = lb.layer
         name = layer.name
-        if isinstance(layer, W.Linear) and lb.clip_mode == "fused":
-            dp.dp_clip_accumulate_linear(lb.A, lb.B, self.dt, self.N, layer.T, layer.d_in, layer.d_out,
-                                         self.scale, self.norm, self.C, self.S[name + ".weight"],
-                                         self.S.get(name + ".bias"), self.status, lb.ws_clip, stream)
-        elif isinstance(layer, W.Embedding):
+        if isinstance(layer, W.Embedding):
             dp.dp_clip_accumulate_embedding(lb.row_ptr, lb.uniq, lb.rows, lb.uniq.shape[0], self.norm, self.C,
                                             self.N, layer.V, layer.D, self.S[name + ".weight"], self.status,
                                             lb.ws_clip, stream)
@@ -218,6 +232,8 @@ class DPStep:
             return self.norms(stream)
         if name == "clip+noise":
             return self.clip_noise(step, None, stream)
+        if name == "clip:linears":
+            return self.linear_clip_sums(stream)
         kind, lname = name.split(":", 1)
         i = next(k for k, lb in enumerate(self.layers) if lb.layer.name == lname)
         if kind == "grad":
@@ -253,8 +269,12 @@ class DPStep:
             if mark: mark("norms", "start")
             self.norms(stream)
             if mark: mark("norms", "end")
+            if self.fused_linear:
+                if mark: mark("clip:linears", "start")
+                self.linear_clip_sums(stream)
+                if mark: mark("clip:linears", "end")
             for i, lb in enumerate(self.layers):
-                if isinstance(lb.layer, W.Embedding) or lb.clip_mode == "fused":
+                if isinstance(lb.layer, W.Embedding):
                     if mark: mark("clip:" + lb.layer.name, "start")
                     self.fused_clip_sum(i, stream)
                     if mark: mark("clip:" + lb.layer.name, "end")
@@ -275,13 +295,17 @@ class DPStep:
         for s_ in side:
             main.wait_stream(s_)
         self.norms()
-        fused = [i for i, lb in enumerate(self.layers)
-                 if isinstance(lb.layer, W.Embedding) or lb.clip_mode == "fused"]
+        fused = [i for i, lb in enumerate(self.layers) if isinstance(lb.layer, W.Embedding)]
         for k, i in enumerate(fused):
             side[k].wait_stream(main)
             with torch.cuda.stream(side[k]):
                 self.fused_clip_sum(i)
-        for k in range(len(fused)):
+        k_lin = len(fused)
+        if self.fused_linear:
+            side[k_lin].wait_stream(main)
+            with torch.cuda.stream(side[k_lin]):
+                self.linear_clip_sums()
+        for k in range(len(fused) + (1 if self.fused_linear else 0)):
             main.wait_stream(side[k])
         self.clip_noise(step, step_dev)
 
