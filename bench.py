@@ -71,8 +71,10 @@ def call_costs(st):
                 out["grad:" + L.name] = (N * (L.d_in + L.d_out) * e + grads + N * 4, N * L.d_out * L.d_in,
                                          "outer_kernel", None)
             else:
+                staged = bf_mfma and L.T % 32 == 0
                 out["grad:" + L.name] = (N * L.T * (L.d_in + L.d_out) * e + grads + N * 4,
                                          2 * N * L.T * L.d_in * L.d_out,
+                                         "bf16_grad_sample_kernel" if staged else
                                          "bf16_per_sample_kernel" if bf_mfma else "ps_gemm_kernel",
                                          "bf16" if bf_mfma else "f32")
             if lb.clip_mode == "fused":
@@ -123,7 +125,10 @@ KERNEL_SOURCES = {
     "outer_kernel": ["paper_2109_12298_amd/csrc/linear.hip"],
     "bf16_per_sample_kernel": ["paper_2109_12298_amd/csrc/linear_bf16.hip"],
     "bf16_clipsum_kernel": ["paper_2109_12298_amd/csrc/linear_bf16.hip"],
-    "bf16_clipsum_many_kernel": ["paper_2109_12298_amd/csrc/clipsum_many.hip"],
+    "bf16_clipsum_many_kernel": ["paper_2109_12298_amd/csrc/clipsum_many.hip",
+                                 "paper_2109_12298_amd/csrc/bf16_stage.hpp"],
+    "bf16_grad_sample_kernel": ["paper_2109_12298_amd/csrc/grad_sample_bf16.hip",
+                                "paper_2109_12298_amd/csrc/bf16_stage.hpp"],
     "ps_gemm_kernel": ["paper_2109_12298_amd/csrc/linear.hip"],
     "clipsum_gemm_kernel": ["paper_2109_12298_amd/csrc/linear.hip", "paper_2109_12298_amd/csrc/mfma_tile.hpp"],
     "conv_per_sample_kernel": ["paper_2109_12298_amd/csrc/conv2d.hip", "paper_2109_12298_amd/csrc/mfma_tile.hpp"],

@@ -40,41 +40,29 @@
 // four different quarters of the 256-byte bank window: no bank conflicts.
 // Each k-step's twelve operand reads (for the next k-step) are issued between
 // its eight MFMAs.
-#include "common.hpp"
+#include "bf16_stage.hpp"
 #include "clipsum_many.hpp"
 
 #include <type_traits>
 
-// the stage loads clobber M0 on purpose (see dma16)
-#pragma clang diagnostic ignored "-Winline-asm"
-
 namespace dpg {
 namespace {
 
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef short i16x4_t __attribute__((ext_vector_type(4)));
-typedef short i16x8_t __attribute__((ext_vector_type(8)));
-typedef float f32x16_t __attribute__((ext_vector_type(16)));
-typedef __attribute__((address_space(3))) i16x4_t lds_i16x4_t;
+using namespace bf16s;
 
 constexpr int BMJ = 256;                         // j (d_in) per tile
 constexpr int BNI = 128;                         // i (d_out) per tile
-constexpr int BK = 32;                           // rows per stage (two k-steps of 16)
 constexpr int kStages = 4;
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
-constexpr int A_ROW = BMJ * 2;                   // bytes per staged A row
-constexpr int B_ROW = BNI * 2;
-constexpr int A_BYTES = BK * A_ROW;              // 16 KB
-constexpr int B_BYTES = BK * B_ROW;              // 8 KB
-constexpr int STAGE_BYTES = A_BYTES + B_BYTES;   // 24 KB
-constexpr int A_INSTR = A_BYTES / 1024 / kWaves; // direct loads per wave per stage: A (4)
-constexpr int B_INSTR = B_BYTES / 1024 / kWaves; //                                   B (2)
-constexpr int LOADS = A_INSTR + B_INSTR;
+typedef StagePlan<BMJ, BNI, kWaves> Plan;
+constexpr int A_ROW = Plan::A_ROW, B_ROW = Plan::B_ROW;
+constexpr int A_BYTES = Plan::A_BYTES;           // 16 KB
+constexpr int STAGE_BYTES = Plan::STAGE_BYTES;   // 24 KB
 constexpr int BIAS_ROWS = BK * 32 / kThreads;     // stage rows per thread in the bias sums
 constexpr int kChunkN = 4000;                    // samples per launch (clip factors in LDS)
-static_assert(A_INSTR * kWaves * 1024 == A_BYTES && B_INSTR * kWaves * 1024 == B_BYTES, "stage split");
 static_assert(kStages * STAGE_BYTES + 2 * kChunkN * 4 + 256 <= 160 * 1024, "LDS budget");
+typedef Frag<4, 2> WaveFrag;                     // a wave's 128 (j) x 64 (i) part of the tile
 
 struct Item {
     const uint16_t *A;
@@ -101,148 +89,9 @@ __device__ __forceinline__ int find_item(const int *blk0, int count, int b)
     return p;
 }
 
-// byte offset of (row t, feature f) in a swizzled staged tile of row length `row_bytes`
-__device__ __forceinline__ int swz(int t, int f, int row_bytes)
+__device__ __forceinline__ void load_wave_frag(const char *L, int ks, int wj, int wi, int lane, WaveFrag &f)
 {
-    return t * row_bytes + 16 * ((f >> 3) ^ (4 * (t & 3))) + 2 * (f & 7);
-}
-
-// One MFMA operand: eight consecutive rows of one feature per lane (rows
-// t_base + 8 * (lane / 32) .., feature f_base + lane % 32), from two
-// transposing reads of four rows each.
-__device__ __forceinline__ bf16x8_t read_operand(const char *L, int row_bytes, int t_base, int f_base, int lane)
-{
-    const int g = lane >> 4, s = lane & 15;
-    const int t = t_base + 8 * (g >> 1) + (s >> 2);
-    const int f = f_base + 16 * (g & 1) + 4 * (s & 3);
-    const i16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t *)(L + swz(t, f, row_bytes)));
-    const i16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t *)(L + swz(t + 4, f, row_bytes)));
-    const i16x8_t v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-    return __builtin_bit_cast(bf16x8_t, v);
-}
-
-struct Frag {
-    bf16x8_t a[4], b[2];
-};
-
-// The operands of one k-step (rows 16*ks .. 16*ks+15 of a staged stage) for
-// the wave's 128 (j) x 64 (i) part of the tile.
-__device__ __forceinline__ void load_frag(const char *L, int ks, int wj, int wi, int lane, Frag &f)
-{
-#pragma unroll
-    for (int x = 0; x < 4; ++x) f.a[x] = read_operand(L, A_ROW, 16 * ks, wj + 32 * x, lane);
-#pragma unroll
-    for (int y = 0; y < 2; ++y) f.b[y] = read_operand(L + A_BYTES, B_ROW, 16 * ks, wi + 32 * y, lane);
-}
-
-__device__ __forceinline__ void mma(const Frag &f, f32x16_t (&acc)[4][2])
-{
-#pragma unroll
-    for (int x = 0; x < 4; ++x)
-#pragma unroll
-        for (int y = 0; y < 2; ++y)
-            acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[x], f.b[y], acc[x][y], 0, 0, 0);
-}
-
-// Ask the scheduler to issue a k-step's 12 operand reads between its 8
-// MFMAs (one MFMA, two reads, ...), so the reads issue while the matrix unit
-// works instead of in a burst that leaves it idle.
-__device__ __forceinline__ void interleave_reads_with_mfma()
-{
-#pragma unroll
-    for (int i = 0; i < 6; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
-        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);   // two LDS reads
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-}
-
-__device__ __forceinline__ void wait_lgkmcnt0()
-{
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-}
-
-template <int N>
-__device__ __forceinline__ void wait_vmcnt()
-{
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
-
-// Wait until a stage's loads have landed, given how many stages exist after
-// it (`later`, of which at most kStages - 2 = 2 have been issued so far): the
-// loads of those later stages may stay in flight.
-__device__ __forceinline__ void wait_stages_after(int later)
-{
-    static_assert(kStages == 4, "two stages in flight behind the awaited one");
-    if (later >= 2) wait_vmcnt<2 * LOADS>();
-    else if (later == 1) wait_vmcnt<LOADS>();
-    else wait_vmcnt<0>();
-}
-
-__device__ __forceinline__ void stage_barrier()
-{
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-}
-
-// One global_load_lds_dwordx4: lane l's 16 bytes at `src` go to LDS byte
-// lds + 16 * l (lds is wave-uniform and goes through M0).  Written as inline
-// assembly so that the compiler, which cannot tell which LDS bytes such a
-// load writes, does not wait for every outstanding stage before each LDS
-// read; the stage pipeline below waits for exactly the loads it needs.
-__device__ __forceinline__ void dma16(const void *src, uint32_t lds)
-{
-    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src),
-                 "s"(__builtin_amdgcn_readfirstlane(lds))
-                 : "memory", "m0");
-}
-
-// Per-lane part of this wave's direct loads of a stage: element offsets
-// (row-in-stage * row length + feature) and LDS byte offsets.  A: 16
-// wave-instructions of two 512-byte rows, B: 8 of four 256-byte rows; wave w
-// takes instructions w, w + 4, ...  Features past the layer's end read a
-// clamped valid chunk (their outputs are never stored).
-struct StagePlan {
-    int offA[A_INSTR], offB[B_INSTR];
-    uint32_t ldsA[A_INSTR], ldsB[B_INSTR];
-};
-
-__device__ __forceinline__ StagePlan plan_stage(const Item &it, i64 m0, i64 n0, int wave, int lane)
-{
-    StagePlan sp;
-#pragma unroll
-    for (int r = 0; r < A_INSTR; ++r) {
-        const int a = wave + kWaves * r;
-        const int t = 2 * a + (lane >> 5);
-        const int q = (lane & 31) ^ (4 * (t & 3));
-        i64 f = m0 + 8 * q;
-        f = f < it.din ? f : it.din - 8;
-        sp.offA[r] = (int)(t * it.din + f);
-        sp.ldsA[r] = (uint32_t)(a * 1024);
-    }
-#pragma unroll
-    for (int r = 0; r < B_INSTR; ++r) {
-        const int a = wave + kWaves * r;
-        const int t = 4 * a + (lane >> 4);
-        const int q = (lane & 15) ^ (4 * (t & 3));
-        i64 f = n0 + 8 * q;
-        f = f < it.dout ? f : it.dout - 8;
-        sp.offB[r] = (int)(t * it.dout + f);
-        sp.ldsB[r] = (uint32_t)(A_BYTES + a * 1024);
-    }
-    return sp;
-}
-
-__device__ __forceinline__ void issue_stage(const Item &it, const StagePlan &sp, i64 k0, uint32_t L)
-{
-    const uint16_t *a = it.A + k0 * it.din;
-    const uint16_t *b = it.B + k0 * it.dout;
-#pragma unroll
-    for (int r = 0; r < A_INSTR; ++r) dma16(a + sp.offA[r], L + sp.ldsA[r]);
-#pragma unroll
-    for (int r = 0; r < B_INSTR; ++r) dma16(b + sp.offB[r], L + sp.ldsB[r]);
+    load_frag<4, 2, A_ROW, B_ROW, A_BYTES>(L, ks, wj, wi, lane, f);
 }
 
 // Pipeline.  Stage c (32 rows of A and B) lives in LDS buffer c % 4.  A wave
@@ -270,8 +119,8 @@ __global__ __launch_bounds__(kThreads, 1) void bf16_clipsum_many_kernel(Group g,
     const int sps = (int)(it.T / BK);              // stages per sample
     const int nst = g.N * sps;                     // stages
     // LDS byte address of the stage buffers (what M0 takes)
-    const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char *)smem;
-    const StagePlan sp = plan_stage(it, m0, n0, wave, lane);
+    const uint32_t lds0 = lds_addr(smem);
+    const Plan sp(it.din, it.dout, m0, n0, wave, lane);
 
     int zero = 0;
     for (int n = tid; n < g.N; n += kThreads) {
@@ -297,10 +146,11 @@ __global__ __launch_bounds__(kThreads, 1) void bf16_clipsum_many_kernel(Group g,
 
 #pragma unroll
     for (int c = 0; c < kStages - 1; ++c)
-        if (c < nst) issue_stage(it, sp, (i64)c * BK, lds0 + c * STAGE_BYTES);
-    wait_stages_after(nst - 1);      // stage 0 has landed
+        if (c < nst) sp.issue(it.A, it.B, it.din, it.dout, (i64)c * BK, lds0 + c * STAGE_BYTES);
+    wait_stages_after<Plan::LOADS>(nst - 1);   // stage 0 has landed
     stage_barrier();
-    if (kStages - 1 < nst) issue_stage(it, sp, (i64)(kStages - 1) * BK, lds0 + (kStages - 1) * STAGE_BYTES);
+    if (kStages - 1 < nst)
+        sp.issue(it.A, it.B, it.din, it.dout, (i64)(kStages - 1) * BK, lds0 + (kStages - 1) * STAGE_BYTES);
 
     float c_cur = 1.0f;      // the accumulators hold S / c_cur
     float c_bias = 0.0f;     // clip factor of the sample whose bias rows are in bcur
@@ -347,11 +197,12 @@ __global__ __launch_bounds__(kThreads, 1) void bf16_clipsum_many_kernel(Group g,
         }
     };
     auto next_stage = [&](int c) {
-        wait_stages_after(nst - 2 - c);   // stage c+1 has landed
+        wait_stages_after<Plan::LOADS>(nst - 2 - c);   // stage c+1 has landed
         wait_lgkmcnt0();                  // this wave's reads of stage c are done
         stage_barrier();
         if (c + kStages < nst)
-            issue_stage(it, sp, (i64)(c + kStages) * BK, lds0 + (uint32_t)(c % kStages) * STAGE_BYTES);
+            sp.issue(it.A, it.B, it.din, it.dout, (i64)(c + kStages) * BK,
+                     lds0 + (uint32_t)(c % kStages) * STAGE_BYTES);
     };
     auto end_stage = [&]() {
         if (++in_sample == sps) {
@@ -367,24 +218,24 @@ __global__ __launch_bounds__(kThreads, 1) void bf16_clipsum_many_kernel(Group g,
     // last stage is peeled so that every loop trip has the same blocks.
     auto run = [&](auto zero_tag) {
         constexpr bool kZero = decltype(zero_tag)::value;
-        Frag fa, fb;
-        if (nst > 0) load_frag(smem, 0, wj, wi, lane, fa);
+        WaveFrag fa, fb;
+        if (nst > 0) load_wave_frag(smem, 0, wj, wi, lane, fa);
         for (int c = 0; c + 1 < nst; ++c) {
             const char *L = smem + (c % kStages) * STAGE_BYTES;
             begin_stage(L, zero_tag);
-            load_frag(L, 1, wj, wi, lane, fb);
+            load_wave_frag(L, 1, wj, wi, lane, fb);
             if (!kZero || !skip) mma(fa, acc);
-            interleave_reads_with_mfma();
+            interleave_reads_with_mfma<4, 2>();
             next_stage(c);
-            load_frag(smem + ((c + 1) % kStages) * STAGE_BYTES, 0, wj, wi, lane, fa);
+            load_wave_frag(smem + ((c + 1) % kStages) * STAGE_BYTES, 0, wj, wi, lane, fa);
             if (!kZero || !skip) mma(fb, acc);
-            interleave_reads_with_mfma();
+            interleave_reads_with_mfma<4, 2>();
             end_stage();
         }
         if (nst > 0) {
             const char *L = smem + ((nst - 1) % kStages) * STAGE_BYTES;
             begin_stage(L, zero_tag);
-            load_frag(L, 1, wj, wi, lane, fb);
+            load_wave_frag(L, 1, wj, wi, lane, fb);
             if (!kZero || !skip) {
                 mma(fa, acc);
                 mma(fb, acc);

@@ -15,6 +15,7 @@
 #include "common.hpp"
 #include "mfma_tile.hpp"
 #include "linear_bf16.hpp"
+#include "grad_sample_bf16.hpp"
 
 namespace dpg {
 namespace {
@@ -370,11 +371,13 @@ using namespace dpg;
 extern "C" size_t dp_grad_sample_linear_workspace_bytes(int64_t N, int64_t T, int64_t d_in,
                                                         int64_t d_out, dp_dtype dt)
 {
-    (void)dt;
     if (N <= 0 || T <= 1 || d_in <= 0 || d_out <= 0) return 0;
-    // enough for either path (the 64x64 fp32-MFMA tiles outnumber the 128x128 bf16 ones)
-    const i64 tiles = ceil_div(d_in, kPM) * ceil_div(d_out, kPN);
-    return (size_t)(N * tiles) * sizeof(float);
+    // squared-norm partials of whichever path runs: one per 64x64 tile (fp32
+    // MFMA; more than the 128x128 tiles of the bf16 kernel), or one per wave
+    // and 128x128 tile (staged bf16 kernel)
+    i64 parts = ceil_div(d_in, kPM) * ceil_div(d_out, kPN);
+    if (dt == DP_BF16 && bf16_staged_parts(d_in, d_out) > parts) parts = bf16_staged_parts(d_in, d_out);
+    return (size_t)(N * parts) * sizeof(float);
 }
 
 extern "C" dp_status dp_grad_sample_linear(const void *A, const void *B, dp_dtype dt, int64_t N,
@@ -424,6 +427,12 @@ extern "C" dp_status dp_grad_sample_linear(const void *A, const void *B, dp_dtyp
     }
 
     float *partial = sqnorm ? (float *)ws : nullptr;
+    if (dt == DP_BF16 && bf16_staged_ok(A, B, gW, N, T, d_in, d_out)) {
+        bf16_grad_sample_staged(A, B, N, T, d_in, d_out, scale, gW, gb, partial, stream);
+        if (sqnorm)
+            sum_partials(partial, N, bf16_staged_parts(d_in, d_out), sqnorm, stream);
+        return launch_status();
+    }
     if (dt == DP_BF16 && bf16_path_ok(A, B, gW, T, d_in, d_out)) {
         bf16_grad_sample(A, B, N, T, d_in, d_out, scale, gW, gb, partial, stream);
         if (sqnorm)

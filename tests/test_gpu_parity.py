@@ -117,7 +117,10 @@ LINEAR_SHAPES = [(1, 1, 1, 1), (3, 1, 37, 13), (2, 2, 5, 3), (4, 5, 37, 13), (3,
                  # feature sizes that are multiples of 8: the bf16 MFMA path for bf16 inputs
                  (1, 2, 8, 8), (3, 33, 136, 72), (2, 130, 264, 392), (2, 64, 128, 128), (9, 16, 256, 24),
                  # multiples of 4 but not 8: 16-byte fp32 / 8-byte bf16 loads on the fp32-MFMA path
-                 (3, 40, 100, 20), (2, 256, 100, 400)]
+                 (3, 40, 100, 20), (2, 256, 100, 400),
+                 # T a multiple of 32: the staged bf16 kernel (ragged tiles; runs of several samples
+                 # per workgroup with a one-sample tail at N = 181)
+                 (1, 32, 8, 8), (3, 32, 136, 72), (2, 64, 264, 392), (5, 96, 128, 256), (181, 32, 512, 384)]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
