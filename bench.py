@@ -106,10 +106,12 @@ def call_costs(st):
             out["grad:" + L.name] = (2 * N * L.T * L.D * e + 2 * N * L.D * 4, 3 * N * L.T * L.D,
                                      "ln_partial_kernel", None)
             col_bytes += 2 * N * L.D * 4
-    out["norms"] = (len(st.layers) * N * 4 + N * 4, len(st.layers) * N, "norms_kernel", None)
+    if not st.fold_norms:
+        out["norms"] = (len(st.layers) * N * 4 + N * 4, len(st.layers) * N, "norms_kernel", None)
     P = st.wl.n_params
-    # grouped clip + noise: read the column-reduced grads once, write S and out, read fused S
-    out["clip+noise"] = (col_bytes + 12 * P, 0, "colsum_many_kernel+finish_many_kernel", None)
+    # one launch: (norms,) read the column-reduced grads once, write S and out, read fused S
+    norms_bytes = (len(st.layers) * N * 4 + N * 4) if st.fold_norms else 0
+    out["clip+noise"] = (col_bytes + 12 * P + norms_bytes, 0, "norms_clip_noise_kernel", None)
     return out
 
 
@@ -140,6 +142,7 @@ KERNEL_SOURCES = {
     "colsum_many_kernel+finish_many_kernel": ["paper_2109_12298_amd/csrc/group.hip",
                                               "paper_2109_12298_amd/csrc/philox.hpp"],
     "norms_kernel": ["paper_2109_12298_amd/csrc/clip.hip"],
+    "norms_clip_noise_kernel": ["paper_2109_12298_amd/csrc/group.hip", "paper_2109_12298_amd/csrc/philox.hpp"],
 }
 
 
@@ -386,7 +389,9 @@ def main():
 
     line = {"metric": METRIC, "value": round(wl.N * args.steps / elapsed, 1), "unit": "samples/s",
             "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
-            "launch": "eager" if args.eager else "hip_graph", "eager_ms_per_step": round(eager_ms, 4),
+            "launch": "eager" if args.eager else
+            ("hip_graph_branches" if st.graph_parallel else "hip_graph_chain"),
+            "eager_ms_per_step": round(eager_ms, 4),
             "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": dtype,
             "data": "synthetic",
             "config": {"workload": wl.name, "batch": wl.N, "params": wl.n_params,

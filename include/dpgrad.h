@@ -281,6 +281,23 @@ dp_status dp_clip_noise_many(const dp_param *params, int32_t count, int64_t N, c
                              float sigma, float denom, int32_t *status, void *ws, size_t ws_bytes,
                              hipStream_t stream);
 
+/* dp_per_sample_norms followed by dp_clip_noise_many, in one launch per
+ * group of up to 40 tensors: with sqnorm given, norm[n] = sqrt(sum_l
+ * sqnorm[l][n]) is computed and written as dp_per_sample_norms does
+ * (DP_FLAG_NONFINITE included); with sqnorm NULL, norm is an input.  Then,
+ * for every tensor, the clipped sum, noise and division of
+ * dp_clip_noise_many.  A workgroup reduces 64 consecutive elements of a
+ * tensor over the whole batch: sixteen contiguous sample ranges, each added
+ * in ascending n, then the sixteen range sums in range order, so the results
+ * are deterministic (they match dp_clip_noise_many to rounding, which groups
+ * the samples differently).  No workspace is needed (the size query returns
+ * 0; ws may be NULL). */
+size_t dp_norms_clip_noise_workspace_bytes(const dp_param *params, int32_t count, int64_t N);
+dp_status dp_norms_clip_noise(const float *sqnorm, int32_t n_layers, const dp_param *params,
+                              int32_t count, int64_t N, float *norm, float C, uint64_t seed,
+                              uint64_t step, const uint64_t *step_dev, float sigma, float denom,
+                              int32_t *status, void *ws, size_t ws_bytes, hipStream_t stream);
+
 /* *step_dev += by, on the device (one tiny kernel): advances the step counter
  * a captured graph reads through dp_clip_noise_many. */
 dp_status dp_step_advance(uint64_t *step_dev, uint64_t by, hipStream_t stream);

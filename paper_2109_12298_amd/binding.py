@@ -56,6 +56,8 @@ SIGNATURES = {
     "dp_clip_accumulate_embedding": (_ST, [_P, _P, _P, _I64, _P, _F, _I64, _I64, _I64, _P, _P, _P, _SZ, _P]),
     "dp_clip_noise_many_workspace_bytes": (_SZ, [_P, _I32, _I64]),
     "dp_clip_noise_many": (_ST, [_P, _I32, _I64, _P, _F, _U64, _U64, _P, _F, _F, _P, _P, _SZ, _P]),
+    "dp_norms_clip_noise_workspace_bytes": (_SZ, [_P, _I32, _I64]),
+    "dp_norms_clip_noise": (_ST, [_P, _I32, _P, _I32, _I64, _P, _F, _U64, _U64, _P, _F, _F, _P, _P, _SZ, _P]),
     "dp_step_advance": (_ST, [_P, _U64, _P]),
     "dp_add_noise": (_ST, [_P, _P, _I64, _U64, _U64, _U32, _F, _F, _F, _P, _P]),
     "dp_philox_normals": (_ST, [_P, _P, _I64, _U64, _U64, _U32, _P]),
@@ -308,6 +310,18 @@ def dp_clip_noise_many(params, count, N, norm, C, seed, step, step_dev, sigma, d
                                     _ptr(step_dev), sigma, denom, _ptr(status), _ptr(ws), _nbytes(ws),
                                     _stream(stream)),
            "dp_clip_noise_many")
+
+
+def dp_norms_clip_noise_workspace_bytes(params, count, N) -> int:
+    return lib().dp_norms_clip_noise_workspace_bytes(ctypes.cast(params, ctypes.c_void_p), count, N)
+
+
+def dp_norms_clip_noise(sqnorm, n_layers, params, count, N, norm, C, seed, step, step_dev, sigma, denom,
+                        status=None, ws=None, stream=None):
+    _check(lib().dp_norms_clip_noise(_ptr(sqnorm), n_layers, ctypes.cast(params, ctypes.c_void_p), count, N,
+                                     _ptr(norm), C, seed, step, _ptr(step_dev), sigma, denom, _ptr(status),
+                                     _ptr(ws), _nbytes(ws), _stream(stream)),
+           "dp_norms_clip_noise")
 
 
 def dp_step_advance(step_dev, by=1, stream=None):

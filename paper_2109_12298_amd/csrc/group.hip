@@ -154,6 +154,170 @@ __global__ __launch_bounds__(kThreads) void finish_many_kernel(GroupDesc d, cons
     }
 }
 
+// ---------------------------------------------------------------------------
+// One-launch variant: norms (optional), column reduce, and finish.
+//
+// A column workgroup owns 64 consecutive elements of a column-reduced tensor
+// (16 float4 columns; 16 scalar columns when the tensor is not 16-byte
+// vectorizable) for the whole batch: its 256 threads are 16 sample groups x
+// 16 columns, each group adding c_n * G[n] over a contiguous range of
+// ceil(N / 16) samples in ascending n.  The 16 range sums are then added in
+// range order through LDS, so the clipped sum is deterministic without a
+// second launch or any communication between workgroups, and the same
+// workgroup adds the noise and divides.  Blocks past the column work finish
+// the tensors whose sums were formed elsewhere.  With sqnorm given, every
+// workgroup computes the clip factors of the batch from the layers' squared
+// norms (added in layer order, as norms_kernel does) and workgroup 0 writes
+// the norms.
+// ---------------------------------------------------------------------------
+constexpr int kGroups = 16;                 // sample groups per column workgroup
+constexpr int kCols = kThreads / kGroups;   // columns per column workgroup
+constexpr int kCfChunk = 4096;              // clip factors held in LDS at a time
+
+struct FusedArgs {
+    const float *sqnorm;       // [L][N] or null (then norm is an input)
+    int L;
+    float *norm;               // [N]: written from sqnorm, else read
+    float C;
+    uint32_t k0, k1;
+    uint64_t step;
+    const uint64_t *step_dev;
+    float sc, denom;
+    int noise;
+    int32_t *status;
+    int cblocks;               // column workgroups
+    int cblk0[kMaxGroup + 1];  // first column workgroup of each tensor
+    int oblk0[kMaxGroup + 1];  // first finish-only workgroup of each tensor
+};
+
+__global__ __launch_bounds__(kThreads) void norms_clip_noise_kernel(GroupDesc d, FusedArgs f)
+{
+    __shared__ float cfs[kCfChunk];
+    __shared__ float4 part[kGroups][kCols];
+    const int tid = threadIdx.x;
+    if ((int)blockIdx.x >= f.cblocks) {
+        // finish-only: a tensor whose sum is already in S (or an empty batch)
+        const int b = (int)blockIdx.x - f.cblocks;
+        const int p = find_param(f.oblk0, d.count, b);
+        const i64 numel = d.numel[p];
+        const i64 q = (i64)(b - f.oblk0[p]) * kThreads + tid;
+        const i64 e0 = 4 * q;
+        if (e0 >= numel) return;
+        const int cnt = e0 + 4 <= numel ? 4 : (int)(numel - e0);
+        float s[4] = {0.f, 0.f, 0.f, 0.f};
+        if (d.R[p]) {
+            for (int i = 0; i < cnt; ++i) d.S[p][e0 + i] = 0.0f;   // N = 0: the clipped sum is zero
+        } else {
+            for (int i = 0; i < cnt; ++i) s[i] = d.S[p][e0 + i];
+        }
+        float *O = d.O[p];
+        if (O == nullptr) return;
+        float z[4] = {0.f, 0.f, 0.f, 0.f};
+        if (f.noise) {
+            const uint64_t st = f.step + (f.step_dev ? *f.step_dev : 0ull);
+            uint32_t w[4];
+            normals4(q, d.pidx[p], (uint32_t)st, (uint32_t)(st >> 32), f.k0, f.k1, z, w);
+        }
+        for (int i = 0; i < cnt; ++i) O[e0 + i] = (s[i] + f.sc * z[i]) / f.denom;
+        return;
+    }
+
+    const int b = (int)blockIdx.x;
+    const int p = find_param(f.cblk0, d.count, b);
+    const float *G = d.G[p];
+    const i64 numel = d.numel[p];
+    const bool vec = (d.flags[p] & 1u) != 0;
+    const int grp = tid / kCols, col = tid % kCols;
+    // this thread's column: float4 column q (elements 4q..4q+3) or element q
+    const i64 q = (i64)(b - f.cblk0[p]) * kCols + col;
+    const bool active = vec ? 4 * q < numel : q < numel;
+    const i64 N = d.N;
+    const i64 per = ceil_div(N, kGroups);
+    const i64 lo = grp * per < N ? grp * per : N, hi = lo + per < N ? lo + per : N;
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    const float4 *g4 = reinterpret_cast<const float4 *>(G);
+    const i64 st4 = numel / 4;
+
+    for (i64 c0 = 0; c0 < N; c0 += kCfChunk) {
+        const i64 c1 = c0 + kCfChunk < N ? c0 + kCfChunk : N;
+        __syncthreads();   // the previous chunk's factors have been used
+        for (i64 n = c0 + tid; n < c1; n += kThreads) {
+            float nr;
+            if (f.sqnorm) {
+                float sq = 0.0f;
+                for (int l = 0; l < f.L; ++l) sq += f.sqnorm[(i64)l * N + n];
+                nr = sqrtf(sq);
+                if (b == 0) {
+                    if (!isfinite(nr)) raise_flag(f.status, DP_FLAG_NONFINITE);
+                    f.norm[n] = nr;
+                }
+            } else {
+                nr = f.norm[n];
+            }
+            cfs[n - c0] = clip_factor(nr, f.C);
+        }
+        __syncthreads();
+        const i64 a0 = lo > c0 ? lo : c0, a1 = hi < c1 ? hi : c1;
+        if (!active || a0 >= a1) continue;
+        if (vec) {
+            i64 n = a0;
+            // eight samples' loads in flight before the (in-order) accumulation
+            for (; n + 8 <= a1; n += 8) {
+                float4 a[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) a[j] = g4[(n + j) * st4 + q];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const float cn = cfs[n + j - c0];
+                    acc[0] += cn * a[j].x; acc[1] += cn * a[j].y; acc[2] += cn * a[j].z; acc[3] += cn * a[j].w;
+                }
+            }
+            for (; n < a1; ++n) {
+                const float4 a = g4[n * st4 + q];
+                const float cn = cfs[n - c0];
+                acc[0] += cn * a.x; acc[1] += cn * a.y; acc[2] += cn * a.z; acc[3] += cn * a.w;
+            }
+        } else {
+            i64 n = a0;
+            for (; n + 8 <= a1; n += 8) {
+                float a[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) a[j] = G[(n + j) * numel + q];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) acc[0] += cfs[n + j - c0] * a[j];
+            }
+            for (; n < a1; ++n) acc[0] += cfs[n - c0] * G[n * numel + q];
+        }
+    }
+    // the sample groups' sums, added in group order
+    part[grp][col] = make_float4(acc[0], acc[1], acc[2], acc[3]);
+    __syncthreads();
+    if (grp != 0 || !active) return;
+    float s[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int k = 0; k < kGroups; ++k) {
+        const float4 v = part[k][col];
+        s[0] += v.x; s[1] += v.y; s[2] += v.z; s[3] += v.w;
+    }
+    // store the clipped sum and the noised average
+    const i64 e0 = vec ? 4 * q : q;
+    const int cnt = vec ? 4 : 1;
+    for (int i = 0; i < cnt; ++i) d.S[p][e0 + i] = s[i];
+    float *O = d.O[p];
+    if (O == nullptr) return;
+    float z[4] = {0.f, 0.f, 0.f, 0.f};
+    if (f.noise) {
+        const uint64_t st = f.step + (f.step_dev ? *f.step_dev : 0ull);
+        uint32_t w[4];
+        normals4(e0 >> 2, d.pidx[p], (uint32_t)st, (uint32_t)(st >> 32), f.k0, f.k1, z, w);
+    }
+    if (vec) {
+        for (int i = 0; i < 4; ++i) O[e0 + i] = (s[i] + f.sc * z[i]) / f.denom;
+    } else {
+        O[e0] = (s[0] + f.sc * z[e0 & 3]) / f.denom;
+    }
+}
+
 __global__ void step_advance_kernel(uint64_t *p, uint64_t by)
 {
     if (threadIdx.x == 0 && blockIdx.x == 0) *p += by;
@@ -267,6 +431,83 @@ extern "C" dp_status dp_clip_noise_many(const dp_param *params, int32_t count, i
             finish_many_kernel<<<(unsigned)d.fblocks, kThreads, 0, stream>>>(
                 d, (const float *)ws, (uint32_t)seed, (uint32_t)(seed >> 32), step, step_dev, sc, denom,
                 noise ? 1 : 0);
+    }
+    return launch_status();
+}
+
+extern "C" size_t dp_norms_clip_noise_workspace_bytes(const dp_param *params, int32_t count, int64_t N)
+{
+    (void)params;
+    (void)count;
+    (void)N;
+    return 0;
+}
+
+extern "C" dp_status dp_norms_clip_noise(const float *sqnorm, int32_t n_layers, const dp_param *params,
+                                         int32_t count, int64_t N, float *norm, float C, uint64_t seed,
+                                         uint64_t step, const uint64_t *step_dev, float sigma, float denom,
+                                         int32_t *status, void *ws, size_t ws_bytes, hipStream_t stream)
+{
+    (void)ws;
+    (void)ws_bytes;
+    DPG_REQUIRE(count >= 0 && N >= 0, DP_EINVAL);
+    DPG_REQUIRE(count == 0 || params != nullptr, DP_EINVAL);
+    DPG_REQUIRE(C > 0.0f && sigma >= 0.0f && denom > 0.0f, DP_EINVAL);
+    DPG_REQUIRE(!(sigma > 0.0f && __builtin_isinf(C)), DP_EINVAL);
+    DPG_REQUIRE(sqnorm == nullptr || n_layers >= 1, DP_EINVAL);
+    DPG_REQUIRE(N == 0 || norm != nullptr, DP_EINVAL);
+    for (int i = 0; i < count; ++i) {
+        const dp_param &q = params[i];
+        DPG_REQUIRE(q.numel >= 0 && (q.flags & ~(uint32_t)DP_PARAM_REDUCE) == 0, DP_EINVAL);
+        DPG_REQUIRE(q.numel / 4 < (i64(1) << 32), DP_EINVAL);
+        DPG_REQUIRE(q.numel == 0 || q.sum != nullptr, DP_EINVAL);
+        if (q.flags & DP_PARAM_REDUCE) DPG_REQUIRE(N == 0 || q.numel == 0 || q.grad_sample != nullptr, DP_EINVAL);
+    }
+    const bool noise = sigma > 0.0f;
+    FusedArgs f;
+    f.L = n_layers;
+    f.norm = norm;
+    f.C = C;
+    f.k0 = (uint32_t)seed;
+    f.k1 = (uint32_t)(seed >> 32);
+    f.step = step;
+    f.step_dev = step_dev;
+    f.sc = noise ? sigma * C : 0.0f;
+    f.denom = denom;
+    f.noise = noise ? 1 : 0;
+    f.status = status;
+    bool norms_done = sqnorm == nullptr || N == 0;
+    for (int first = 0; first < count; first += kMaxGroup) {
+        const int c = count - first < kMaxGroup ? count - first : kMaxGroup;
+        GroupDesc d;
+        describe(params, first, c, N, d);
+        int cb = 0, ob = 0;
+        for (int i = 0; i < c; ++i) {
+            f.cblk0[i] = cb;
+            f.oblk0[i] = ob;
+            const bool col = d.R[i] && N > 0 && d.numel[i] > 0;
+            if (col) {
+                // 16-byte columns need a 16-byte aligned tensor (the partial flag bit 0
+                // of describe() also asks for an aligned sum, which this path does not)
+                const bool v = (d.numel[i] & 3) == 0 && aligned(d.G[i], 16);
+                d.flags[i] = (d.flags[i] & ~1u) | (v ? 1u : 0u);
+                cb += (int)ceil_div(v ? d.numel[i] / 4 : d.numel[i], kCols);
+            } else {
+                ob += (int)ceil_div(ceil_div(d.numel[i], 4), kThreads);
+            }
+        }
+        f.cblk0[c] = cb;
+        f.oblk0[c] = ob;
+        f.cblocks = cb;
+        if (!norms_done && cb == 0) {
+            // no column work to compute the norms in: compute them first
+            const dp_status st = dp_per_sample_norms(sqnorm, n_layers, N, norm, status, stream);
+            if (st != DP_OK) return st;
+            norms_done = true;
+        }
+        f.sqnorm = norms_done ? nullptr : sqnorm;
+        if (cb + ob > 0) norms_clip_noise_kernel<<<(unsigned)(cb + ob), kThreads, 0, stream>>>(d, f);
+        norms_done = true;
     }
     return launch_status();
 }

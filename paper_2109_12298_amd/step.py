@@ -9,11 +9,12 @@ and enqueues the calls, in order, on one stream:
 
   1. one per-sample-gradient call per layer (each also writes that layer's
      row of per-sample squared norms);
-  2. dp_per_sample_norms;
-  3. fused clipped sums where they are cheaper (Linear: B^T diag(c) A;
-     Embedding: CSR -> dense);
-  4. one dp_clip_noise_many for every parameter tensor: column-reduces the
-     remaining per-sample gradients and writes every tensor's noised average.
+  2. dp_per_sample_norms, when a fused clipped sum needs the norms first;
+  3. fused clipped sums where they are cheaper (Linear: B^T diag(c) A, all
+     layers in one grouped call; Embedding: CSR -> dense);
+  4. one dp_norms_clip_noise launch for every parameter tensor: the norms
+     (unless step 2 ran), the column reductions of the remaining per-sample
+     gradients, and every tensor's noised average.
 
 A step can be captured once as a HIP graph and replayed; the noise step then
 comes from a device counter that the graph advances itself.
@@ -164,10 +165,15 @@ class DPStep:
             entries.append((self._grad_for(name), self.S[name], self.out[name], int(np.prod(shape)), pidx))
         self.group = dp.make_params(entries)
         self.group_count = len(entries)
-        need = dp.dp_clip_noise_many_workspace_bytes(self.group, self.group_count, N)
+        # the norms are computed inside the clip/noise launch unless a fused
+        # clipped sum (which needs them) runs before it
+        self.fold_norms = not self.fused_linear and not any(isinstance(lb.layer, W.Embedding)
+                                                              for lb in self.layers)
+        need = dp.dp_norms_clip_noise_workspace_bytes(self.group, self.group_count, N)
         self.ws = torch.empty(max(need, 256), dtype=torch.uint8, device=self.device)
         self.step_dev = torch.zeros(1, dtype=torch.int64, device=self.device)
         self.graph = None
+        self.graph_parallel = None
         self._side = None
 
     def _grad_for(self, pname: str):
@@ -223,13 +229,15 @@ class DPStep:
                                             lb.ws_clip, stream)
 
     def clip_noise(self, step: int, step_dev=None, stream=None):
-        dp.dp_clip_noise_many(self.group, self.group_count, self.N, self.norm, self.C, self.seed, step, step_dev,
-                              self.sigma, self.denom, self.status, self.ws, stream)
+        """Clipped sums, noise and division of every tensor (and the norms, when folded) in one launch."""
+        dp.dp_norms_clip_noise(self.sqnorm if self.fold_norms else None, len(self.layers), self.group,
+                               self.group_count, self.N, self.norm, self.C, self.seed, step, step_dev,
+                               self.sigma, self.denom, self.status, self.ws, stream)
 
     def call(self, name: str, step: int = 0, stream=None):
         """Enqueue one named call of the step ("grad:<layer>", "norms", "clip:<layer>", "clip+noise")."""
         if name == "norms":
-            return self.norms(stream)
+            return None if self.fold_norms else self.norms(stream)
         if name == "clip+noise":
             return self.clip_noise(step, None, stream)
         if name == "clip:linears":
@@ -250,15 +258,18 @@ class DPStep:
 
     # ------------------------------------------------------------------ whole step
     def run(self, step: int = 0, stream=None, mark: Optional[Callable[[str, str], None]] = None, step_dev=None,
-            parallel: bool = False, advance: bool = False):
+            parallel: bool = False, advance: bool = False, clear_status: bool = True):
         """Enqueue one whole step; nothing is synchronized here.
 
         parallel: the layers' per-sample-gradient calls (independent of each
         other) and the fused clipped sums run on side streams forked from and
         joined back into the current stream.  advance: also enqueue
-        dp_step_advance on step_dev, in a branch ahead of the noise."""
+        dp_step_advance on step_dev, in a branch ahead of the noise.
+        clear_status: zero the status word first (a captured step leaves it
+        alone, so flags accumulate over replays until the caller clears it)."""
         torch = _torch()
-        self.status.zero_()
+        if clear_status:
+            self.status.zero_()
         if not parallel:
             if advance:
                 dp.dp_step_advance(step_dev, 1, stream)
@@ -266,9 +277,10 @@ class DPStep:
                 if mark: mark("grad:" + lb.layer.name, "start")
                 self.grad_sample(i, stream)
                 if mark: mark("grad:" + lb.layer.name, "end")
-            if mark: mark("norms", "start")
-            self.norms(stream)
-            if mark: mark("norms", "end")
+            if not self.fold_norms:
+                if mark: mark("norms", "start")
+                self.norms(stream)
+                if mark: mark("norms", "end")
             if self.fused_linear:
                 if mark: mark("clip:linears", "start")
                 self.linear_clip_sums(stream)
@@ -294,7 +306,8 @@ class DPStep:
                 dp.dp_step_advance(step_dev, 1)
         for s_ in side:
             main.wait_stream(s_)
-        self.norms()
+        if not self.fold_norms:
+            self.norms()
         fused = [i for i, lb in enumerate(self.layers) if isinstance(lb.layer, W.Embedding)]
         for k, i in enumerate(fused):
             side[k].wait_stream(main)
@@ -309,12 +322,34 @@ class DPStep:
             main.wait_stream(side[k])
         self.clip_noise(step, step_dev)
 
-    def capture(self, first_step: int = 0, parallel: bool = True):
+    def capture(self, first_step: int = 0, parallel: Optional[bool] = None):
         """Capture one step as a HIP graph; replay r runs step first_step + r.
 
         The graph advances its own device step counter (in a branch that runs
-        before the noise), so nothing is re-recorded between replays."""
+        before the noise), so nothing is re-recorded between replays.
+        parallel: the layers' calls as parallel branches of the graph (True),
+        or one chain (False); None captures both, times a few replays of
+        each and keeps the faster (branches pay off when the layers' kernels
+        are long enough to overlap; for short kernels the single chain has
+        less scheduling overhead)."""
         torch = _torch()
+        if parallel is None:
+            import time
+            best = None
+            for par in (True, False):
+                self.capture(first_step, par)
+                for _ in range(5):
+                    self.replay()
+                torch.cuda.synchronize(self.device)
+                t0 = time.perf_counter()
+                for _ in range(20):
+                    self.replay()
+                torch.cuda.synchronize(self.device)
+                dt = time.perf_counter() - t0
+                if best is None or dt < best[0]:
+                    best = (dt, par)
+            self.graph_parallel = best[1]
+            return self.capture(first_step, best[1])
         side = torch.cuda.Stream(self.device)
         side.wait_stream(torch.cuda.current_stream(self.device))
         with torch.cuda.stream(side):
@@ -323,10 +358,11 @@ class DPStep:
         torch.cuda.synchronize(self.device)
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
-            self.run(step=0, step_dev=self.step_dev, parallel=parallel, advance=True)
+            self.run(step=0, step_dev=self.step_dev, parallel=parallel, advance=True, clear_status=False)
         torch.cuda.synchronize(self.device)
         self.step_dev.fill_(first_step - 1)    # advanced to first_step by the first replay
         self.graph = g
+        self.graph_parallel = parallel
         return g
 
     def replay(self):

@@ -473,3 +473,68 @@ def test_graph_replay_matches_eager_steps():
             np.testing.assert_array_equal(got["S"][name], ref["S"][name])
         np.testing.assert_array_equal(got["norm"], ref["norm"])
     assert int(st.step_dev.item()) == 7     # the counter holds the last replayed step
+
+
+@pytest.mark.parametrize("N", [0, 5, 40, 300, 4100])
+def test_norms_clip_noise_one_launch_matches_two_launch_path(N):
+    """dp_norms_clip_noise (norms, column reduce and finish in one launch)
+    matches dp_per_sample_norms + dp_clip_noise_many: norms bit for bit, sums
+    and outputs to rounding (the two group the samples differently), and it is
+    bitwise repeatable, also with more than 40 tensors and more samples than
+    its LDS chunk of clip factors."""
+    r = np.random.default_rng(31 + N)
+    say("norms_clip_noise N=", N)
+    shapes = [1, 7, 1024, 4099, 16, 33 * 3, 5000, 8] * 6      # 48 tensors: two groups
+    if N > 1000:
+        shapes = [1, 7, 64, 4099, 16, 33, 500, 8] * 6
+    L = 3
+    sq = torch.from_numpy(r.uniform(0.01, 1.5, (L, max(N, 1))).astype(np.float32)).to(DEV)[:, :N].contiguous()
+    entries_a, entries_b = [], []
+    for i, numel in enumerate(shapes):
+        G = torch.from_numpy(r.standard_normal((max(N, 1), numel)).astype(np.float32)).to(DEV)[:N]
+        Sa, Sb = torch.full((numel,), 7.0, device=DEV), torch.full((numel,), 7.0, device=DEV)
+        Oa, Ob = torch.empty(numel, device=DEV), torch.empty(numel, device=DEV)
+        if i % 5 == 2:      # sum given (fused route): only noise
+            Sa.copy_(torch.from_numpy(r.standard_normal(numel).astype(np.float32)))
+            Sb.copy_(Sa)
+            entries_a.append((None, Sa, Oa, numel, i))
+            entries_b.append((None, Sb, Ob, numel, i))
+        elif i % 5 == 4:    # no output
+            entries_a.append((G, Sa, None, numel, i))
+            entries_b.append((G, Sb, None, numel, i))
+        else:
+            entries_a.append((G, Sa, Oa, numel, i))
+            entries_b.append((G, Sb, Ob, numel, i))
+    pa, pb = dp.make_params(entries_a), dp.make_params(entries_b)
+    n = len(shapes)
+    assert dp.dp_norms_clip_noise_workspace_bytes(pa, n, N) == 0
+    ws_b = torch.empty(max(dp.dp_clip_noise_many_workspace_bytes(pb, n, N), 1), dtype=torch.uint8, device=DEV)
+    norm_a = torch.full((max(N, 1),), -1.0, device=DEV)
+    norm_b = torch.full((max(N, 1),), -1.0, device=DEV)
+    first = None
+    for step in (3, 3, 5):
+        dp.dp_norms_clip_noise(sq, L, pa, n, N, norm_a, 1.1, 17, step, None, 0.9, 13.0, None, None)
+        if N:
+            dp.dp_per_sample_norms(sq, L, N, norm_b)
+        dp.dp_clip_noise_many(pb, n, N, norm_b, 1.1, 17, step, None, 0.9, 13.0, None, ws_b)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(norm_a.cpu().numpy()[:N], norm_b.cpu().numpy()[:N])
+        got = [(sa.cpu().numpy(), None if oa is None else oa.cpu().numpy()) for (_, sa, oa, _, _) in entries_a]
+        for (ga, sa, oa, numel, _), (gb, sb, ob, _, _) in zip(entries_a, entries_b):
+            assert_g12(sa.cpu().numpy(), sb.cpu().numpy(), 1e-5, "S numel %d" % numel)
+            if oa is not None:
+                assert_g12(oa.cpu().numpy(), ob.cpu().numpy(), 1e-5, "out numel %d" % numel)
+        if first is None:
+            first = got
+        elif step == 3:
+            for (s1, o1), (s2, o2) in zip(first, got):      # same step again: the same bits
+                np.testing.assert_array_equal(s1, s2)
+                if o1 is not None:
+                    np.testing.assert_array_equal(o1, o2)
+    # a given norm (sqnorm NULL) is read, not written
+    if N:
+        dp.dp_norms_clip_noise(None, 0, pa, n, N, norm_b, 1.1, 17, 6, None, 0.9, 13.0, None, None)
+        dp.dp_clip_noise_many(pb, n, N, norm_b, 1.1, 17, 6, None, 0.9, 13.0, None, ws_b)
+        torch.cuda.synchronize()
+        for (ga, sa, oa, numel, _), (gb, sb, ob, _, _) in zip(entries_a, entries_b):
+            assert_g12(sa.cpu().numpy(), sb.cpu().numpy(), 1e-5, "S numel %d" % numel)
