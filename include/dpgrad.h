@@ -122,6 +122,17 @@ dp_status dp_grad_sample_conv2d(const void *X, const void *GY, dp_dtype dt, int6
                                 float *sqnorm, int32_t *status, void *ws, size_t ws_bytes,
                                 hipStream_t stream);
 
+/* Kernel choice of dp_grad_sample_conv2d, process-wide.  DP_CONV_AUTO (the
+ * default): a sample whose padded input planes and backprop fit one
+ * workgroup's LDS (48 KB), with Cout <= 256 and a weight gradient of at most
+ * 32 blocks of 16 (Cin*kh*kw) x 16 (Cout), runs one workgroup per sample;
+ * other shapes run the tiled kernel.  DP_CONV_TILED: always the tiled kernel.  Both give the same
+ * results to rounding.  Returns the previous choice, or -1 (choice unchanged)
+ * for an unknown value.  Not synchronized with calls in flight on other host
+ * threads: set it before enqueueing. */
+enum { DP_CONV_AUTO = 0, DP_CONV_TILED = 1 };
+int dp_conv2d_set_path(int path);
+
 /* Embedding y_t = E[ids[n][t]] over a [V][D] table.  Sample n's gradient is
  * zero except on the rows of the ids it holds; row v is s * sum of B[n][t][:]
  * over the positions t with ids[n][t] = v.  Returned sparse, as CSR over the

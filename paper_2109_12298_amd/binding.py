@@ -37,6 +37,7 @@ SIGNATURES = {
     "dp_grad_sample_linear": (_ST, [_P, _P, _ST, _I64, _I64, _I64, _I64, _F, _P, _P, _P, _P, _P, _SZ, _P]),
     "dp_grad_sample_conv2d_workspace_bytes": (_SZ, [_I64] * 11),
     "dp_grad_sample_conv2d": (_ST, [_P, _P, _ST] + [_I64] * 16 + [_F, _P, _P, _P, _P, _P, _SZ, _P]),
+    "dp_conv2d_set_path": (ctypes.c_int, [ctypes.c_int]),
     "dp_grad_sample_embedding_workspace_bytes": (_SZ, [_I64, _I64]),
     "dp_grad_sample_embedding": (_ST, [_P, _P, _ST, _I64, _I64, _I64, _I64, _F, _P, _P, _P, _I64, _P,
                                        _P, _P, _SZ, _P]),
@@ -208,6 +209,17 @@ def dp_grad_sample_conv2d(X, GY, dt, N, Cin, H, W, Cout, Ho, Wo, kh, kw, sh, sw,
                                        pw, dh, dw, groups, scale, _ptr(gW), _ptr(gb), _ptr(sqnorm),
                                        _ptr(status), _ptr(ws), _nbytes(ws), _stream(stream)),
            "dp_grad_sample_conv2d")
+
+
+DP_CONV_AUTO, DP_CONV_TILED = 0, 1
+
+
+def dp_conv2d_set_path(path: int) -> int:
+    """Process-wide kernel choice of dp_grad_sample_conv2d; returns the previous one."""
+    prev = lib().dp_conv2d_set_path(path)
+    if prev < 0:
+        raise ValueError("unknown conv2d path %r" % (path,))
+    return prev
 
 
 def dp_grad_sample_embedding_workspace_bytes(N, T) -> int:

@@ -21,6 +21,7 @@
 // unfold gathered through the cache into a K-major LDS tile per chunk.
 #include "common.hpp"
 #include "mfma_tile.hpp"
+#include "conv2d_small.hpp"
 
 #include <type_traits>
 
@@ -640,6 +641,16 @@ extern "C" size_t dp_grad_sample_conv2d_workspace_bytes(int64_t N, int64_t Cin, 
     return tiles > 1 ? (size_t)(N * tiles) * sizeof(float) : 0;
 }
 
+static int g_conv_path = DP_CONV_AUTO;
+
+extern "C" int dp_conv2d_set_path(int path)
+{
+    if (path != DP_CONV_AUTO && path != DP_CONV_TILED) return -1;
+    const int prev = g_conv_path;
+    g_conv_path = path;
+    return prev;
+}
+
 extern "C" dp_status dp_grad_sample_conv2d(const void *X, const void *GY, dp_dtype dt, int64_t N,
                                            int64_t Cin, int64_t H, int64_t W, int64_t Cout,
                                            int64_t Ho, int64_t Wo, int64_t kh, int64_t kw,
@@ -662,8 +673,14 @@ extern "C" dp_status dp_grad_sample_conv2d(const void *X, const void *GY, dp_dty
     DPG_REQUIRE(ws_bytes >= need && (need == 0 || ws != nullptr), DP_EINVAL);
     if (N == 0) return DP_OK;
 
-    const ConvShape s = make_shape(Cin, H, W, Cout, kh, kw, sh, sw, ph, pw);
     const bool bf = dt == DP_BF16;
+    const ConvSmallArgs small{X, GY, N, Cin, H, W, Cout, Ho, Wo, kh, kw, sh, sw, ph, pw};
+    if (g_conv_path == DP_CONV_AUTO && conv_small_ok(small)) {
+        // the whole sample fits one workgroup's LDS
+        conv_small_launch(small, bf, scale, gW, gb, sqnorm, stream);
+        return launch_status();
+    }
+    const ConvShape s = make_shape(Cin, H, W, Cout, kh, kw, sh, sw, ph, pw);
     Plan p = plan_conv(s, (long)N);
     p.g.vec = (s.KK % 4 == 0) && aligned(gW, 16);
     if (p.cfg >= 0) {

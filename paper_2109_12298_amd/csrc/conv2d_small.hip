@@ -1,0 +1,281 @@
+// Per-sample Conv2d gradients for samples small enough to sit whole in LDS
+// (the MNIST network's convolutions, for example): one workgroup per sample.
+//
+// gW_n[co][ci][u][v] = s * sum_{oh,ow} GY_n[co][oh][ow] * X_n[ci][oh*sh+u-ph][ow*sw+v-pw]
+// gb_n[co]           = s * sum_{oh,ow} GY_n[co][oh][ow]
+// (the weight gradient of the cross-correlation restricted to sample n; the
+// unfold's column order (ci, u, v) is the weight's own layout).
+//
+// The workgroup stages the sample's padded input planes (zero halo) and its
+// backprop [co][position] in LDS with every global load in flight at once,
+// plus a table of each output position's offset in the padded plane.  The
+// contraction over positions then runs on v_mfma_f32_16x16x4_f32 in 16 (kk)
+// x 16 (co) blocks, each wave holding up to eight blocks' accumulators: a
+// lane's operand is one LDS read of the unfold (its kk's plane offset + the
+// position's offset) and one of the backprop; the unfold is never formed.  A lane's four
+// accumulators are four consecutive kk of one co, stored as one float4.  The
+// bias sums and the sample's squared norm are added in a fixed order, so the
+// norm goes straight to sqnorm[n] (no partials).  Against the general kernel
+// this keeps a sample's fixed costs (one load round trip, no K split, no
+// second pass) small, which is what bounds these tiny convolutions.
+#include "common.hpp"
+#include "conv2d_small.hpp"
+
+namespace dpg {
+namespace {
+
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / 64;
+constexpr int kSmallLds = 48 * 1024;      // bytes of dynamic LDS
+constexpr int kBatch = 8;                 // global loads in flight per thread per round
+
+struct SmallShape {
+    int Cin, H, W, Cout, Ho, Wo, kh, kw, sh, sw, ph, pw;
+    int Hp, Wp, plane, L, Lp, KK, khw;
+    int nbm, nbn;                 // 16-blocks over kk and co
+    int bpw;                      // blocks per wave: 1, 2, 4 or 8
+    int gs_off, po_off;           // LDS float offsets of the backprop and the position table
+    int vec;                      // float4 stores of gW
+    float inv_hw, inv_w, inv_l, inv_wo;
+};
+
+constexpr int kMaxBpw = 8;        // accumulator blocks a wave holds at once
+
+// q = x / d, r = x % d for 0 <= x < 2^22 through a float reciprocal, corrected
+// to the exact quotient (the estimate is off by at most one)
+__device__ __forceinline__ void fdivmod(int x, int d, float inv_d, int &q, int &r)
+{
+    q = (int)((float)x * inv_d);
+    r = x - q * d;
+    q += (r >= d ? 1 : 0) - (r < 0 ? 1 : 0);
+    r = x - q * d;
+}
+
+// element e of the sample's input goes to its padded-plane slot
+__device__ __forceinline__ int x_slot(int e, const SmallShape &s)
+{
+    int c, r, h, w;
+    fdivmod(e, s.H * s.W, s.inv_hw, c, r);
+    fdivmod(r, s.W, s.inv_w, h, w);
+    return c * s.plane + (h + s.ph) * s.Wp + w + s.pw;
+}
+
+template <typename T, int BPW>
+__global__ __launch_bounds__(kThreads) void conv_small_kernel(const T *__restrict__ X, const T *__restrict__ GY,
+                                                              SmallShape s, float scale, float *__restrict__ gW,
+                                                              float *__restrict__ gb, float *__restrict__ sqnorm)
+{
+    extern __shared__ float lds[];
+    __shared__ float red[kWaves];
+    const i64 n = blockIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    float *Xs = lds;                             // [Cin][Hp][Wp], zero halo
+    float *Gs = lds + s.gs_off;                  // [Cout][Lp], zero past L
+    int *Po = reinterpret_cast<int *>(lds + s.po_off);   // [Lp]
+    const T *Xn = X + n * s.Cin * s.H * s.W;
+    const T *Gn = GY + n * s.Cout * s.L;
+    const int xcount = s.Cin * s.H * s.W, gcount = s.Cout * s.L;
+
+    // ---- staging: clear the planes and the backprop tail while the first
+    // round of loads is in flight, then write the loaded values
+    for (int e0 = 0; e0 < xcount || e0 < gcount; e0 += kBatch * kThreads) {
+        float xv[kBatch], gv[kBatch];
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+            const int e = e0 + j * kThreads + tid;
+            xv[j] = e < xcount ? load_elem<T>(Xn, e) : 0.0f;
+            gv[j] = e < gcount ? load_elem<T>(Gn, e) : 0.0f;
+        }
+        if (e0 == 0) {
+            for (int i = tid; i < s.Cin * s.plane; i += kThreads) Xs[i] = 0.0f;
+            for (int i = tid; i < s.Cout * (s.Lp - s.L); i += kThreads) {
+                const int co = i / (s.Lp - s.L);
+                Gs[co * s.Lp + s.L + (i - co * (s.Lp - s.L))] = 0.0f;
+            }
+            for (int p = tid; p < s.Lp; p += kThreads) {
+                int oh, ow;
+                fdivmod(p, s.Wo, s.inv_wo, oh, ow);
+                Po[p] = p < s.L ? oh * s.sh * s.Wp + ow * s.sw : 0;
+            }
+            __syncthreads();   // the cleared halo is in place before the interior lands
+        }
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+            const int e = e0 + j * kThreads + tid;
+            if (e < xcount) Xs[x_slot(e, s)] = xv[j];
+            if (e < gcount) {
+                int co, p;
+                fdivmod(e, s.L, s.inv_l, co, p);
+                Gs[co * s.Lp + p] = gv[j];
+            }
+        }
+    }
+    __syncthreads();
+
+    // ---- bias: thread (seg, co) adds positions seg, seg + segs, ...; the
+    // segments are then added in order
+    float sq = 0.0f;
+    if (gb != nullptr) {
+        float *bpart = reinterpret_cast<float *>(Po + s.Lp);    // [segs][Cout] after the table
+        const int segs = kThreads / s.Cout;
+        const int co = tid % s.Cout, seg = tid / s.Cout;
+        if (seg < segs) {
+            float b = 0.0f;
+            for (int p = seg; p < s.L; p += segs) b += Gs[co * s.Lp + p];
+            bpart[seg * s.Cout + co] = b;
+        }
+        __syncthreads();
+        if (tid < s.Cout) {
+            float b = 0.0f;
+            for (int k = 0; k < segs; ++k) b += bpart[k * s.Cout + tid];
+            b *= scale;
+            gb[n * s.Cout + tid] = b;
+            sq += b * b;
+        }
+    }
+
+    // ---- the contraction.  Wave w owns blocks w*bpw .. w*bpw + bpw - 1 in
+    // co-major order (so its blocks mostly share one co range, whose backprop
+    // reads then serve them all), all their accumulators at once; one pass
+    // over the positions reads each position's table entry once per wave.
+    const int nblocks = s.nbm * s.nbn;
+    const int r16 = lane & 15, kq = lane >> 4;
+    float *G = gW + n * s.Cout * s.KK;
+    const int b0 = wave * BPW;
+    int koff[BPW], bco[BPW];
+    bool kok[BPW], cok[BPW];
+    f32x4_t acc[BPW];
+#pragma unroll
+    for (int j = 0; j < BPW; ++j) {
+        const int blk = b0 + j;
+        const bool live = blk < nblocks;
+        const int bm = live ? blk % s.nbm : 0, bn = live ? blk / s.nbm : 0;
+        const int kk = bm * 16 + r16;
+        kok[j] = live && kk < s.KK;
+        koff[j] = 0;
+        if (kok[j]) {
+            const int ci = kk / s.khw, rem = kk - ci * s.khw;
+            const int u = rem / s.kw, v = rem - u * s.kw;
+            koff[j] = ci * s.plane + u * s.Wp + v;
+        }
+        const int co = bn * 16 + r16;
+        cok[j] = live && co < s.Cout;
+        bco[j] = cok[j] ? co : 0;
+        acc[j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+    }
+    for (int p0 = 0; p0 < s.Lp; p0 += 4) {
+        const int p = p0 + kq;
+        const int po = Po[p];
+        float b[BPW], a[BPW];
+#pragma unroll
+        for (int j = 0; j < BPW; ++j) {
+            const float y = Gs[bco[j] * s.Lp + p];
+            const float x = Xs[koff[j] + po];
+            b[j] = cok[j] ? y : 0.0f;
+            a[j] = kok[j] ? x : 0.0f;
+        }
+#pragma unroll
+        for (int j = 0; j < BPW; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[j], b[j], acc[j], 0, 0, 0);
+    }
+#pragma unroll
+    for (int j = 0; j < BPW; ++j) {
+        const int blk = b0 + j;
+        if (blk >= nblocks) continue;
+        const int bm = blk % s.nbm, bn = blk / s.nbm;
+        const int co = bn * 16 + r16;
+        // lane holds kk = bm*16 + 4*kq + r (r = 0..3) of column co
+        const int kk0 = bm * 16 + 4 * kq;
+        if (co < s.Cout) {
+            const float g0 = scale * acc[j][0], g1 = scale * acc[j][1];
+            const float g2 = scale * acc[j][2], g3 = scale * acc[j][3];
+            float *dst = G + (i64)co * s.KK + kk0;
+            if (s.vec && kk0 + 3 < s.KK) {
+                *reinterpret_cast<float4 *>(dst) = make_float4(g0, g1, g2, g3);
+                sq += g0 * g0 + g1 * g1 + g2 * g2 + g3 * g3;
+            } else {
+                if (kk0 + 0 < s.KK) { dst[0] = g0; sq += g0 * g0; }
+                if (kk0 + 1 < s.KK) { dst[1] = g1; sq += g1 * g1; }
+                if (kk0 + 2 < s.KK) { dst[2] = g2; sq += g2 * g2; }
+                if (kk0 + 3 < s.KK) { dst[3] = g3; sq += g3 * g3; }
+            }
+        }
+    }
+
+    // ---- the sample's squared norm: waves' sums in wave order
+    sq = wave_sum(sq);
+    if (lane == 0) red[wave] = sq;
+    __syncthreads();
+    if (tid == 0 && sqnorm) {
+        float t = 0.0f;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) t += red[w];
+        sqnorm[n] = t;
+    }
+}
+
+bool make_small(const ConvSmallArgs &a, SmallShape &s)
+{
+    s.Cin = (int)a.Cin; s.H = (int)a.H; s.W = (int)a.W; s.Cout = (int)a.Cout;
+    s.kh = (int)a.kh; s.kw = (int)a.kw; s.sh = (int)a.sh; s.sw = (int)a.sw; s.ph = (int)a.ph; s.pw = (int)a.pw;
+    s.Ho = (int)a.Ho; s.Wo = (int)a.Wo;
+    s.Hp = s.H + 2 * s.ph;
+    s.Wp = s.W + 2 * s.pw;
+    s.plane = s.Hp * s.Wp;
+    s.L = s.Ho * s.Wo;
+    s.Lp = (s.L + 3) & ~3;
+    s.khw = s.kh * s.kw;
+    s.KK = s.Cin * s.khw;
+    s.nbm = (s.KK + 15) / 16;
+    s.nbn = (s.Cout + 15) / 16;
+    s.bpw = 1;
+    while (s.bpw * kWaves < s.nbm * s.nbn) s.bpw *= 2;
+    s.gs_off = s.Cin * s.plane;
+    s.po_off = s.gs_off + s.Cout * s.Lp;
+    s.inv_hw = 1.0f / (float)(s.H * s.W);
+    s.inv_w = 1.0f / (float)s.W;
+    s.inv_l = 1.0f / (float)s.L;
+    s.inv_wo = 1.0f / (float)s.Wo;
+    // the bias partials [segs][Cout] follow the position table
+    const long floats = (long)s.po_off + s.Lp + kThreads;
+    return a.Cout <= kThreads && floats * 4 <= kSmallLds && s.bpw <= kMaxBpw &&
+           (long)s.Cin * s.H * s.W < (1L << 22) && (long)s.Cout * s.L < (1L << 22);
+}
+
+template <int BPW>
+void launch_small(const ConvSmallArgs &a, const SmallShape &s, bool bf16, float scale, float *gW, float *gb,
+                  float *sqnorm, size_t lds, hipStream_t stream)
+{
+    if (bf16)
+        conv_small_kernel<uint16_t, BPW><<<(unsigned)a.N, kThreads, lds, stream>>>(
+            (const uint16_t *)a.X, (const uint16_t *)a.GY, s, scale, gW, gb, sqnorm);
+    else
+        conv_small_kernel<float, BPW><<<(unsigned)a.N, kThreads, lds, stream>>>(
+            (const float *)a.X, (const float *)a.GY, s, scale, gW, gb, sqnorm);
+}
+
+}  // namespace
+
+bool conv_small_ok(const ConvSmallArgs &a)
+{
+    SmallShape s;
+    return make_small(a, s);
+}
+
+void conv_small_launch(const ConvSmallArgs &a, bool bf16, float scale, float *gW, float *gb, float *sqnorm,
+                       hipStream_t stream)
+{
+    SmallShape s;
+    make_small(a, s);
+    s.vec = s.KK % 4 == 0 && aligned(gW, 16);
+    const size_t lds = (size_t)(s.po_off + s.Lp + kThreads) * sizeof(float);
+    switch (s.bpw) {
+    case 1: launch_small<1>(a, s, bf16, scale, gW, gb, sqnorm, lds, stream); break;
+    case 2: launch_small<2>(a, s, bf16, scale, gW, gb, sqnorm, lds, stream); break;
+    case 4: launch_small<4>(a, s, bf16, scale, gW, gb, sqnorm, lds, stream); break;
+    default: launch_small<8>(a, s, bf16, scale, gW, gb, sqnorm, lds, stream); break;
+    }
+}
+
+}  // namespace dpg

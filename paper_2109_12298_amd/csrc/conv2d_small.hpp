@@ -1,0 +1,19 @@
+// One-workgroup-per-sample Conv2d per-sample gradients (conv2d_small.hip).
+#pragma once
+
+#include "common.hpp"
+
+namespace dpg {
+
+struct ConvSmallArgs {
+    const void *X, *GY;
+    i64 N, Cin, H, W, Cout, Ho, Wo, kh, kw, sh, sw, ph, pw;
+};
+
+// the sample's padded planes, backprop and position table fit the LDS budget
+bool conv_small_ok(const ConvSmallArgs &a);
+// writes gW, gb (if not null) and sqnorm[n] (if not null) directly
+void conv_small_launch(const ConvSmallArgs &a, bool bf16, float scale, float *gW, float *gb, float *sqnorm,
+                       hipStream_t stream);
+
+}  // namespace dpg

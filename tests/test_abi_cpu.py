@@ -136,3 +136,15 @@ def test_product_path_never_touches_the_oracle():
                 text = open(os.path.join(dirpath, fn)).read()
                 assert "import oracle" not in text and "from oracle" not in text, fn
                 assert "dp_oracle" not in text and "liboracle" not in text, fn
+
+
+def test_conv2d_path_choice_round_trips():
+    """The conv kernel choice is process-wide state: set returns the previous
+    value and an unknown value is refused without changing it."""
+    prev = dp.dp_conv2d_set_path(dp.DP_CONV_TILED)
+    try:
+        assert dp.dp_conv2d_set_path(dp.DP_CONV_AUTO) == dp.DP_CONV_TILED
+        assert dp.lib().dp_conv2d_set_path(7) == -1
+        assert dp.dp_conv2d_set_path(dp.DP_CONV_AUTO) == dp.DP_CONV_AUTO
+    finally:
+        dp.dp_conv2d_set_path(prev)

@@ -200,10 +200,20 @@ CONV_CONFIG_SHAPES = [
     (1, 24, 20, 21, 5, 3, 3, 2, 2, 1, 1), (1, 20, 5, 6, 5, 3, 3, 2, 2, 1, 1)]              # 256 x 32, 8 waves
 
 
+@pytest.fixture(params=["auto", "tiled"])
+def conv_path(request):
+    """Run a conv test with the automatic kernel choice (one workgroup per
+    sample for samples that fit LDS) and again with the tiled kernel forced."""
+    path = dp.DP_CONV_TILED if request.param == "tiled" else dp.DP_CONV_AUTO
+    prev = dp.dp_conv2d_set_path(path)
+    yield request.param
+    dp.dp_conv2d_set_path(prev)
+
+
 @pytest.mark.parametrize("shape", CONV_SHAPES + CONV_CONFIG_SHAPES)
-def test_conv_shapes(shape):
+def test_conv_shapes(shape, conv_path):
     N, Cin, H, Wd, Cout, kh, kw, sh, sw, ph, pw = shape
-    say("conv", shape)
+    say("conv", conv_path, shape)
     Ho = (H + 2 * ph - kh) // sh + 1
     Wo = (Wd + 2 * pw - kw) // sw + 1
     r = np.random.default_rng(sum(shape))
@@ -226,10 +236,10 @@ def test_conv_shapes(shape):
 
 
 @pytest.mark.parametrize("shape", [CONV_SHAPES[1], CONV_SHAPES[2], CONV_SHAPES[3], CONV_SHAPES[5]])
-def test_conv_shapes_bf16(shape):
+def test_conv_shapes_bf16(shape, conv_path):
     """bf16 inputs (scalar staging loads) against the oracle on the rounded values."""
     N, Cin, H, Wd, Cout, kh, kw, sh, sw, ph, pw = shape
-    say("conv bf16", shape)
+    say("conv bf16", conv_path, shape)
     Ho = (H + 2 * ph - kh) // sh + 1
     Wo = (Wd + 2 * pw - kw) // sw + 1
     r = np.random.default_rng(sum(shape) + 1)
