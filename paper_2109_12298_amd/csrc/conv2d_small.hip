@@ -29,11 +29,13 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
 constexpr int kSmallLds = 48 * 1024;      // bytes of dynamic LDS
-constexpr int kBatch = 8;                 // global loads in flight per thread per round
+constexpr int kBatch = 16;                // global loads in flight per thread per round
 
 struct SmallShape {
     int Cin, H, W, Cout, Ho, Wo, kh, kw, sh, sw, ph, pw;
     int Hp, Wp, plane, L, Lp, KK, khw;
+    int gst;                      // row stride of the staged backprop: 4 x odd, so the 16 rows
+                                  // x 4 positions a wave reads at once fall in 64 different banks
     int nbm, nbn;                 // 16-blocks over kk and co
     int bpw;                      // blocks per wave: 1, 2, 4 or 8
     int gs_off, po_off;           // LDS float offsets of the backprop and the position table
@@ -62,6 +64,40 @@ __device__ __forceinline__ int x_slot(int e, const SmallShape &s)
     return c * s.plane + (h + s.ph) * s.Wp + w + s.pw;
 }
 
+// U position steps (4 positions each: lane group kq takes position p0 + 4u + kq)
+// of a wave's BPW blocks: every LDS read first, then the MFMAs
+template <int BPW, int U, bool MASK>
+__device__ __forceinline__ void contract_step(const float *Xs, const float *Gs, const int *Po, const int (&koff)[BPW],
+                                              const int (&goff)[BPW], int p0, int kq, int L, f32x4_t (&acc)[BPW])
+{
+    int po[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) po[u] = Po[p0 + 4 * u + kq];
+    float a[U][BPW], b[U][BPW];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int j = 0; j < BPW; ++j) {
+            a[u][j] = Xs[koff[j] + po[u]];
+            b[u][j] = Gs[goff[j] + p0 + 4 * u];
+        }
+    if (MASK) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const bool in = p0 + 4 * u + kq < L;
+#pragma unroll
+            for (int j = 0; j < BPW; ++j) {
+                a[u][j] = in ? a[u][j] : 0.0f;
+                b[u][j] = in ? b[u][j] : 0.0f;
+            }
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int j = 0; j < BPW; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[u][j], b[u][j], acc[j], 0, 0, 0);
+}
+
 template <typename T, int BPW>
 __global__ __launch_bounds__(kThreads) void conv_small_kernel(const T *__restrict__ X, const T *__restrict__ GY,
                                                               SmallShape s, float scale, float *__restrict__ gW,
@@ -72,7 +108,7 @@ __global__ __launch_bounds__(kThreads) void conv_small_kernel(const T *__restric
     const i64 n = blockIdx.x;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     float *Xs = lds;                             // [Cin][Hp][Wp], zero halo
-    float *Gs = lds + s.gs_off;                  // [Cout][Lp], zero past L
+    float *Gs = lds + s.gs_off;                  // [Cout][gst], positions 0 .. L-1 used
     int *Po = reinterpret_cast<int *>(lds + s.po_off);   // [Lp]
     const T *Xn = X + n * s.Cin * s.H * s.W;
     const T *Gn = GY + n * s.Cout * s.L;
@@ -90,10 +126,6 @@ __global__ __launch_bounds__(kThreads) void conv_small_kernel(const T *__restric
         }
         if (e0 == 0) {
             for (int i = tid; i < s.Cin * s.plane; i += kThreads) Xs[i] = 0.0f;
-            for (int i = tid; i < s.Cout * (s.Lp - s.L); i += kThreads) {
-                const int co = i / (s.Lp - s.L);
-                Gs[co * s.Lp + s.L + (i - co * (s.Lp - s.L))] = 0.0f;
-            }
             for (int p = tid; p < s.Lp; p += kThreads) {
                 int oh, ow;
                 fdivmod(p, s.Wo, s.inv_wo, oh, ow);
@@ -108,7 +140,7 @@ __global__ __launch_bounds__(kThreads) void conv_small_kernel(const T *__restric
             if (e < gcount) {
                 int co, p;
                 fdivmod(e, s.L, s.inv_l, co, p);
-                Gs[co * s.Lp + p] = gv[j];
+                Gs[co * s.gst + p] = gv[j];
             }
         }
     }
@@ -123,7 +155,7 @@ __global__ __launch_bounds__(kThreads) void conv_small_kernel(const T *__restric
         const int co = tid % s.Cout, seg = tid / s.Cout;
         if (seg < segs) {
             float b = 0.0f;
-            for (int p = seg; p < s.L; p += segs) b += Gs[co * s.Lp + p];
+            for (int p = seg; p < s.L; p += segs) b += Gs[co * s.gst + p];
             bpart[seg * s.Cout + co] = b;
         }
         __syncthreads();
@@ -136,16 +168,16 @@ __global__ __launch_bounds__(kThreads) void conv_small_kernel(const T *__restric
         }
     }
 
-    // ---- the contraction.  Wave w owns blocks w*bpw .. w*bpw + bpw - 1 in
+    // ---- the contraction.  Wave w owns blocks w*BPW .. w*BPW + BPW - 1 in
     // co-major order (so its blocks mostly share one co range, whose backprop
-    // reads then serve them all), all their accumulators at once; one pass
-    // over the positions reads each position's table entry once per wave.
+    // reads then serve them all) and holds all their accumulators at once.
+    // Lanes of a kk or co past the end read a valid address (kk 0, co 0):
+    // they feed only output rows and columns that are never stored.
     const int nblocks = s.nbm * s.nbn;
     const int r16 = lane & 15, kq = lane >> 4;
     float *G = gW + n * s.Cout * s.KK;
     const int b0 = wave * BPW;
-    int koff[BPW], bco[BPW];
-    bool kok[BPW], cok[BPW];
+    int koff[BPW], goff[BPW];
     f32x4_t acc[BPW];
 #pragma unroll
     for (int j = 0; j < BPW; ++j) {
@@ -153,32 +185,23 @@ __global__ __launch_bounds__(kThreads) void conv_small_kernel(const T *__restric
         const bool live = blk < nblocks;
         const int bm = live ? blk % s.nbm : 0, bn = live ? blk / s.nbm : 0;
         const int kk = bm * 16 + r16;
-        kok[j] = live && kk < s.KK;
         koff[j] = 0;
-        if (kok[j]) {
+        if (live && kk < s.KK) {
             const int ci = kk / s.khw, rem = kk - ci * s.khw;
             const int u = rem / s.kw, v = rem - u * s.kw;
             koff[j] = ci * s.plane + u * s.Wp + v;
         }
         const int co = bn * 16 + r16;
-        cok[j] = live && co < s.Cout;
-        bco[j] = cok[j] ? co : 0;
+        goff[j] = (live && co < s.Cout ? co : 0) * s.gst + kq;
         acc[j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
     }
-    for (int p0 = 0; p0 < s.Lp; p0 += 4) {
-        const int p = p0 + kq;
-        const int po = Po[p];
-        float b[BPW], a[BPW];
-#pragma unroll
-        for (int j = 0; j < BPW; ++j) {
-            const float y = Gs[bco[j] * s.Lp + p];
-            const float x = Xs[koff[j] + po];
-            b[j] = cok[j] ? y : 0.0f;
-            a[j] = kok[j] ? x : 0.0f;
-        }
-#pragma unroll
-        for (int j = 0; j < BPW; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[j], b[j], acc[j], 0, 0, 0);
-    }
+    // U position steps per iteration, so that the table reads and the
+    // operand reads that depend on them are in flight together; the chunk
+    // that holds the end of the positions masks what lies past it
+    constexpr int U = BPW >= 8 ? 1 : 8 / BPW;
+    const int Lfull = s.L - s.L % (4 * U);
+    for (int p0 = 0; p0 < Lfull; p0 += 4 * U) contract_step<BPW, U, false>(Xs, Gs, Po, koff, goff, p0, kq, s.L, acc);
+    if (Lfull < s.L) contract_step<BPW, U, true>(Xs, Gs, Po, koff, goff, Lfull, kq, s.L, acc);
 #pragma unroll
     for (int j = 0; j < BPW; ++j) {
         const int blk = b0 + j;
@@ -224,7 +247,7 @@ bool make_small(const ConvSmallArgs &a, SmallShape &s)
     s.Wp = s.W + 2 * s.pw;
     s.plane = s.Hp * s.Wp;
     s.L = s.Ho * s.Wo;
-    s.Lp = (s.L + 3) & ~3;
+    s.Lp = (s.L + 31) & ~31;
     s.khw = s.kh * s.kw;
     s.KK = s.Cin * s.khw;
     s.nbm = (s.KK + 15) / 16;
@@ -232,7 +255,8 @@ bool make_small(const ConvSmallArgs &a, SmallShape &s)
     s.bpw = 1;
     while (s.bpw * kWaves < s.nbm * s.nbn) s.bpw *= 2;
     s.gs_off = s.Cin * s.plane;
-    s.po_off = s.gs_off + s.Cout * s.Lp;
+    s.gst = s.Lp + 4;
+    s.po_off = s.gs_off + s.Cout * s.gst;
     s.inv_hw = 1.0f / (float)(s.H * s.W);
     s.inv_w = 1.0f / (float)s.W;
     s.inv_l = 1.0f / (float)s.L;
