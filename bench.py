@@ -56,6 +56,7 @@ def log(*a):
 def call_costs(st):
     """name -> (algorithmic bytes, flops, kernel name, MFMA peak key or None) per call of one step."""
     from paper_2109_12298_amd import workloads as W
+    from paper_2109_12298_amd import binding as dp
     N = st.N
     bf = st.wl.dtype == W.BF16
     e = 2 if bf else 4
@@ -93,8 +94,11 @@ def call_costs(st):
             ho, wo = L.out_hw
             kk = L.c_in * L.k[0] * L.k[1]
             grads = N * L.n_params * 4
+            item = dp.make_layer_grads([st._grad_item(st.layers.index(lb))])
+            small = dp.dp_grad_sample_many_grouped(item, 0, st.dt, N)
             out["grad:" + L.name] = (N * (L.c_in * L.h * L.w + L.c_out * ho * wo) * e + grads + N * 4,
-                                     2 * N * L.c_out * kk * ho * wo, "conv_per_sample_kernel", "f32")
+                                     2 * N * L.c_out * kk * ho * wo,
+                                     "conv_small_kernel" if small else "conv_per_sample_kernel", "f32")
             col_bytes += grads
         elif isinstance(L, W.Embedding):
             nnz_bound = N * L.T
@@ -106,6 +110,14 @@ def call_costs(st):
             out["grad:" + L.name] = (2 * N * L.T * L.D * e + 2 * N * L.D * 4, 3 * N * L.T * L.D,
                                      "ln_partial_kernel", None)
             col_bytes += 2 * N * L.D * 4
+    if st.grad_group:
+        # the grouped layers' per-sample gradients are one launch
+        gb_, gf_ = 0, 0
+        for i in st.grad_group:
+            b0, f0, _, _ = out.pop("grad:" + st.layers[i].layer.name)
+            gb_ += b0
+            gf_ += f0
+        out["grad:group"] = (gb_, gf_, "grad_many_kernel", None)
     if not st.fold_norms:
         out["norms"] = (len(st.layers) * N * 4 + N * 4, len(st.layers) * N, "norms_kernel", None)
     P = st.wl.n_params
@@ -124,7 +136,11 @@ def src_hash(paths):
 
 
 KERNEL_SOURCES = {
-    "outer_kernel": ["paper_2109_12298_amd/csrc/linear.hip"],
+    "outer_kernel": ["paper_2109_12298_amd/csrc/linear.hip", "paper_2109_12298_amd/csrc/linear_outer.hpp"],
+    "conv_small_kernel": ["paper_2109_12298_amd/csrc/conv2d_small.hip",
+                          "paper_2109_12298_amd/csrc/conv2d_small_dev.hpp"],
+    "grad_many_kernel": ["paper_2109_12298_amd/csrc/grad_many.hip", "paper_2109_12298_amd/csrc/conv2d_small_dev.hpp",
+                         "paper_2109_12298_amd/csrc/linear_outer.hpp"],
     "bf16_per_sample_kernel": ["paper_2109_12298_amd/csrc/linear_bf16.hip"],
     "bf16_clipsum_kernel": ["paper_2109_12298_amd/csrc/linear_bf16.hip"],
     "bf16_clipsum_many_kernel": ["paper_2109_12298_amd/csrc/clipsum_many.hip",

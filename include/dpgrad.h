@@ -133,6 +133,43 @@ dp_status dp_grad_sample_conv2d(const void *X, const void *GY, dp_dtype dt, int6
 enum { DP_CONV_AUTO = 0, DP_CONV_TILED = 1 };
 int dp_conv2d_set_path(int path);
 
+/* One layer of dp_grad_sample_many: the arguments of dp_grad_sample_linear
+ * (kind DP_LAYER_LINEAR: A, B, T, d_in, d_out) or dp_grad_sample_conv2d
+ * (kind DP_LAYER_CONV2D: A = X, B = GY, Cin .. pw; groups = dilation = 1),
+ * with the same meaning, layouts and outputs (gW, gb or NULL, sqnorm or NULL;
+ * all fp32, overwritten).  The caller owns every buffer. */
+enum { DP_LAYER_LINEAR = 0, DP_LAYER_CONV2D = 1 };
+typedef struct dp_layer_grad {
+    int32_t kind;
+    const void *A;
+    const void *B;
+    int64_t T, d_in, d_out;
+    int64_t Cin, H, W, Cout, Ho, Wo, kh, kw, sh, sw, ph, pw;
+    float scale;
+    float *gW;
+    float *gb;
+    float *sqnorm;
+} dp_layer_grad;
+
+/* The per-sample gradients of `count` layers that share N and the dtype, as
+ * by one dp_grad_sample_linear / dp_grad_sample_conv2d call per layer (same
+ * formulas; results equal to rounding order), in one launch for the layers
+ * that qualify (dp_grad_sample_many_grouped): one workgroup per sample and
+ * layer, so that small layers' fixed costs (launch, load round trip) overlap
+ * instead of adding up.  The other layers run through the single-layer entry
+ * points inside this call, one after the other on `stream`, sharing `ws`.
+ * Arguments are checked as the single-layer calls check them; the first
+ * invalid layer's status is returned before anything is enqueued.  count in
+ * [0, 64].
+ * dp_grad_sample_many_grouped: 1 if the layer goes into the grouped launch
+ * (a Linear layer with T = 1; a Conv2d layer whose sample fits one
+ * workgroup, as for DP_CONV_AUTO, while that choice is in force), else 0. */
+int32_t dp_grad_sample_many_grouped(const dp_layer_grad *item, dp_dtype dt, int64_t N);
+size_t dp_grad_sample_many_workspace_bytes(const dp_layer_grad *items, int32_t count, dp_dtype dt,
+                                           int64_t N);
+dp_status dp_grad_sample_many(const dp_layer_grad *items, int32_t count, dp_dtype dt, int64_t N,
+                              int32_t *status, void *ws, size_t ws_bytes, hipStream_t stream);
+
 /* Embedding y_t = E[ids[n][t]] over a [V][D] table.  Sample n's gradient is
  * zero except on the rows of the ids it holds; row v is s * sum of B[n][t][:]
  * over the positions t with ids[n][t] = v.  Returned sparse, as CSR over the

@@ -38,6 +38,9 @@ SIGNATURES = {
     "dp_grad_sample_conv2d_workspace_bytes": (_SZ, [_I64] * 11),
     "dp_grad_sample_conv2d": (_ST, [_P, _P, _ST] + [_I64] * 16 + [_F, _P, _P, _P, _P, _P, _SZ, _P]),
     "dp_conv2d_set_path": (ctypes.c_int, [ctypes.c_int]),
+    "dp_grad_sample_many_grouped": (_I32, [_P, _ST, _I64]),
+    "dp_grad_sample_many_workspace_bytes": (_SZ, [_P, _I32, _ST, _I64]),
+    "dp_grad_sample_many": (_ST, [_P, _I32, _ST, _I64, _P, _P, _SZ, _P]),
     "dp_grad_sample_embedding_workspace_bytes": (_SZ, [_I64, _I64]),
     "dp_grad_sample_embedding": (_ST, [_P, _P, _ST, _I64, _I64, _I64, _I64, _F, _P, _P, _P, _I64, _P,
                                        _P, _P, _SZ, _P]),
@@ -107,6 +110,44 @@ def make_linear_clips(entries):
         arr[i].scale = float(scale)
         arr[i].sumW = _ptr(sumW)
         arr[i].sumb = _ptr(sumb)
+    return arr
+
+
+DP_LAYER_LINEAR, DP_LAYER_CONV2D = 0, 1
+
+
+class DPLayerGrad(ctypes.Structure):
+    """struct dp_layer_grad of dpgrad.h."""
+    _fields_ = [("kind", ctypes.c_int32), ("A", ctypes.c_void_p), ("B", ctypes.c_void_p)] + \
+               [(f, ctypes.c_int64) for f in ("T", "d_in", "d_out", "Cin", "H", "W", "Cout", "Ho", "Wo", "kh", "kw",
+                                              "sh", "sw", "ph", "pw")] + \
+               [("scale", ctypes.c_float), ("gW", ctypes.c_void_p), ("gb", ctypes.c_void_p),
+                ("sqnorm", ctypes.c_void_p)]
+
+
+def linear_grad_item(A, B, T, d_in, d_out, scale, gW, gb=None, sqnorm=None):
+    """The dp_layer_grad fields of a Linear layer (a dict for make_layer_grads)."""
+    return dict(kind=DP_LAYER_LINEAR, A=A, B=B, T=T, d_in=d_in, d_out=d_out, scale=scale, gW=gW, gb=gb,
+                sqnorm=sqnorm)
+
+
+def conv2d_grad_item(X, GY, Cin, H, W, Cout, Ho, Wo, kh, kw, sh, sw, ph, pw, scale, gW, gb=None, sqnorm=None):
+    """The dp_layer_grad fields of a Conv2d layer (a dict for make_layer_grads)."""
+    return dict(kind=DP_LAYER_CONV2D, A=X, B=GY, Cin=Cin, H=H, W=W, Cout=Cout, Ho=Ho, Wo=Wo, kh=kh, kw=kw, sh=sh,
+                sw=sw, ph=ph, pw=pw, scale=scale, gW=gW, gb=gb, sqnorm=sqnorm)
+
+
+def make_layer_grads(entries):
+    """A dp_layer_grad array from linear_grad_item / conv2d_grad_item dicts."""
+    arr = (DPLayerGrad * max(len(entries), 1))()
+    for i, e in enumerate(entries):
+        for k, v in e.items():
+            if k in ("A", "B", "gW", "gb", "sqnorm"):
+                setattr(arr[i], k, _ptr(v))
+            elif k == "scale":
+                arr[i].scale = float(v)
+            else:
+                setattr(arr[i], k, int(v))
     return arr
 
 
@@ -294,6 +335,21 @@ def dp_clip_accumulate_linear_many(items, count, dt, N, norm, C, status=None, ws
     _check(lib().dp_clip_accumulate_linear_many(ctypes.cast(items, ctypes.c_void_p), count, dt, N, _ptr(norm), C,
                                                 _ptr(status), _ptr(ws), _nbytes(ws), _stream(stream)),
            "dp_clip_accumulate_linear_many")
+
+
+def dp_grad_sample_many_grouped(items, k, dt, N) -> bool:
+    """Whether layer k of a dp_layer_grad array goes into the grouped launch."""
+    return bool(lib().dp_grad_sample_many_grouped(ctypes.cast(ctypes.byref(items[k]), ctypes.c_void_p), dt, N))
+
+
+def dp_grad_sample_many_workspace_bytes(items, count, dt, N) -> int:
+    return lib().dp_grad_sample_many_workspace_bytes(ctypes.cast(items, ctypes.c_void_p), count, dt, N)
+
+
+def dp_grad_sample_many(items, count, dt, N, status=None, ws=None, stream=None):
+    _check(lib().dp_grad_sample_many(ctypes.cast(items, ctypes.c_void_p), count, dt, N, _ptr(status), _ptr(ws),
+                                     _nbytes(ws), _stream(stream)),
+           "dp_grad_sample_many")
 
 
 def dp_clip_accumulate_embedding_workspace_bytes(N, V) -> int:

@@ -33,7 +33,8 @@ HIPFLAGS = ["-O3", "-std=c++17", "--offload-arch=" + ARCH, "-fPIC", "-Wall",
 # VGPRs (it rescales them with VALU multiplies once per sample) and clobbers
 # M0 in inline assembly on purpose.
 EXTRA = {"clipsum_many.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1", "-Wno-inline-asm"],
-         "conv2d_small.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
+         "conv2d_small.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+         "grad_many.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
 
 
 def _hipcc() -> str:

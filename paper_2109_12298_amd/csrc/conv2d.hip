@@ -643,6 +643,13 @@ extern "C" size_t dp_grad_sample_conv2d_workspace_bytes(int64_t N, int64_t Cin, 
 
 static int g_conv_path = DP_CONV_AUTO;
 
+namespace dpg {
+int conv_path()
+{
+    return g_conv_path;
+}
+}  // namespace dpg
+
 extern "C" int dp_conv2d_set_path(int path)
 {
     if (path != DP_CONV_AUTO && path != DP_CONV_TILED) return -1;

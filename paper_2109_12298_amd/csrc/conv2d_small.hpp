@@ -10,6 +10,9 @@ struct ConvSmallArgs {
     i64 N, Cin, H, W, Cout, Ho, Wo, kh, kw, sh, sw, ph, pw;
 };
 
+// the kernel choice of dp_conv2d_set_path in force
+int conv_path();
+
 // the sample's padded planes, backprop and position table fit the LDS budget
 bool conv_small_ok(const ConvSmallArgs &a);
 // writes gW, gb (if not null) and sqnorm[n] (if not null) directly

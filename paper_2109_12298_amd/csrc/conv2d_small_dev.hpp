@@ -1,0 +1,263 @@
+// Device side of the one-workgroup-per-sample Conv2d per-sample gradients:
+// the shape record, the per-sample body (shared by the single-layer kernel
+// and the grouped per-sample-gradient kernel) and its host-side planning.
+#pragma once
+
+#include "common.hpp"
+#include "conv2d_small.hpp"
+
+namespace dpg {
+namespace csmall {
+
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / 64;
+constexpr int kSmallLds = 48 * 1024;      // bytes of dynamic LDS
+constexpr int kBatch = 16;                // global loads in flight per thread per round
+
+struct SmallShape {
+    int Cin, H, W, Cout, Ho, Wo, kh, kw, sh, sw, ph, pw;
+    int Hp, Wp, plane, L, Lp, KK, khw;
+    int gst;                      // row stride of the staged backprop: 4 x odd, so the 16 rows
+                                  // x 4 positions a wave reads at once fall in 64 different banks
+    int nbm, nbn;                 // 16-blocks over kk and co
+    int bpw;                      // blocks per wave: 1, 2, 4 or 8
+    int gs_off, po_off;           // LDS float offsets of the backprop and the position table
+    int vec;                      // float4 stores of gW
+    float inv_hw, inv_w, inv_l, inv_wo;
+};
+
+constexpr int kMaxBpw = 8;        // accumulator blocks a wave holds at once
+
+// q = x / d, r = x % d for 0 <= x < 2^22 through a float reciprocal, corrected
+// to the exact quotient (the estimate is off by at most one)
+__device__ __forceinline__ void fdivmod(int x, int d, float inv_d, int &q, int &r)
+{
+    q = (int)((float)x * inv_d);
+    r = x - q * d;
+    q += (r >= d ? 1 : 0) - (r < 0 ? 1 : 0);
+    r = x - q * d;
+}
+
+// element e of the sample's input goes to its padded-plane slot
+__device__ __forceinline__ int x_slot(int e, const SmallShape &s)
+{
+    int c, r, h, w;
+    fdivmod(e, s.H * s.W, s.inv_hw, c, r);
+    fdivmod(r, s.W, s.inv_w, h, w);
+    return c * s.plane + (h + s.ph) * s.Wp + w + s.pw;
+}
+
+// U position steps (4 positions each: lane group kq takes position p0 + 4u + kq)
+// of a wave's BPW blocks: every LDS read first, then the MFMAs
+template <int BPW, int U, bool MASK>
+__device__ __forceinline__ void contract_step(const float *Xs, const float *Gs, const int *Po, const int (&koff)[BPW],
+                                              const int (&goff)[BPW], int p0, int kq, int L, f32x4_t (&acc)[BPW])
+{
+    int po[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) po[u] = Po[p0 + 4 * u + kq];
+    float a[U][BPW], b[U][BPW];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int j = 0; j < BPW; ++j) {
+            a[u][j] = Xs[koff[j] + po[u]];
+            b[u][j] = Gs[goff[j] + p0 + 4 * u];
+        }
+    if (MASK) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const bool in = p0 + 4 * u + kq < L;
+#pragma unroll
+            for (int j = 0; j < BPW; ++j) {
+                a[u][j] = in ? a[u][j] : 0.0f;
+                b[u][j] = in ? b[u][j] : 0.0f;
+            }
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int j = 0; j < BPW; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[u][j], b[u][j], acc[j], 0, 0, 0);
+}
+
+// Sample n's gradients by one workgroup of kThreads threads; `lds` holds
+// lds_floats(s) floats of dynamic LDS.
+template <typename T, int BPW>
+__device__ __forceinline__ void conv_small_sample(const T *__restrict__ X, const T *__restrict__ GY, const SmallShape &s,
+                                                  float scale, float *__restrict__ gW, float *__restrict__ gb,
+                                                  float *__restrict__ sqnorm, i64 n, float *lds)
+{
+    __shared__ float red[kWaves];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    float *Xs = lds;                             // [Cin][Hp][Wp], zero halo
+    float *Gs = lds + s.gs_off;                  // [Cout][gst], positions 0 .. L-1 used
+    int *Po = reinterpret_cast<int *>(lds + s.po_off);   // [Lp]
+    const T *Xn = X + n * s.Cin * s.H * s.W;
+    const T *Gn = GY + n * s.Cout * s.L;
+    const int xcount = s.Cin * s.H * s.W, gcount = s.Cout * s.L;
+
+    // ---- staging: clear the planes and the backprop tail while the first
+    // round of loads is in flight, then write the loaded values
+    for (int e0 = 0; e0 < xcount || e0 < gcount; e0 += kBatch * kThreads) {
+        float xv[kBatch], gv[kBatch];
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+            const int e = e0 + j * kThreads + tid;
+            xv[j] = e < xcount ? load_elem<T>(Xn, e) : 0.0f;
+            gv[j] = e < gcount ? load_elem<T>(Gn, e) : 0.0f;
+        }
+        if (e0 == 0) {
+            for (int i = tid; i < s.Cin * s.plane; i += kThreads) Xs[i] = 0.0f;
+            for (int p = tid; p < s.Lp; p += kThreads) {
+                int oh, ow;
+                fdivmod(p, s.Wo, s.inv_wo, oh, ow);
+                Po[p] = p < s.L ? oh * s.sh * s.Wp + ow * s.sw : 0;
+            }
+            __syncthreads();   // the cleared halo is in place before the interior lands
+        }
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+            const int e = e0 + j * kThreads + tid;
+            if (e < xcount) Xs[x_slot(e, s)] = xv[j];
+            if (e < gcount) {
+                int co, p;
+                fdivmod(e, s.L, s.inv_l, co, p);
+                Gs[co * s.gst + p] = gv[j];
+            }
+        }
+    }
+    __syncthreads();
+
+    // ---- bias: thread (seg, co) adds positions seg, seg + segs, ...; the
+    // segments are then added in order
+    float sq = 0.0f;
+    if (gb != nullptr) {
+        float *bpart = reinterpret_cast<float *>(Po + s.Lp);    // [segs][Cout] after the table
+        const int segs = kThreads / s.Cout;
+        const int co = tid % s.Cout, seg = tid / s.Cout;
+        if (seg < segs) {
+            float b = 0.0f;
+            for (int p = seg; p < s.L; p += segs) b += Gs[co * s.gst + p];
+            bpart[seg * s.Cout + co] = b;
+        }
+        __syncthreads();
+        if (tid < s.Cout) {
+            float b = 0.0f;
+            for (int k = 0; k < segs; ++k) b += bpart[k * s.Cout + tid];
+            b *= scale;
+            gb[n * s.Cout + tid] = b;
+            sq += b * b;
+        }
+    }
+
+    // ---- the contraction.  Wave w owns blocks w*BPW .. w*BPW + BPW - 1 in
+    // co-major order (so its blocks mostly share one co range, whose backprop
+    // reads then serve them all) and holds all their accumulators at once.
+    // Lanes of a kk or co past the end read a valid address (kk 0, co 0):
+    // they feed only output rows and columns that are never stored.
+    const int nblocks = s.nbm * s.nbn;
+    const int r16 = lane & 15, kq = lane >> 4;
+    float *G = gW + n * s.Cout * s.KK;
+    const int b0 = wave * BPW;
+    int koff[BPW], goff[BPW];
+    f32x4_t acc[BPW];
+#pragma unroll
+    for (int j = 0; j < BPW; ++j) {
+        const int blk = b0 + j;
+        const bool live = blk < nblocks;
+        const int bm = live ? blk % s.nbm : 0, bn = live ? blk / s.nbm : 0;
+        const int kk = bm * 16 + r16;
+        koff[j] = 0;
+        if (live && kk < s.KK) {
+            const int ci = kk / s.khw, rem = kk - ci * s.khw;
+            const int u = rem / s.kw, v = rem - u * s.kw;
+            koff[j] = ci * s.plane + u * s.Wp + v;
+        }
+        const int co = bn * 16 + r16;
+        goff[j] = (live && co < s.Cout ? co : 0) * s.gst + kq;
+        acc[j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+    }
+    // U position steps per iteration, so that the table reads and the
+    // operand reads that depend on them are in flight together; the chunk
+    // that holds the end of the positions masks what lies past it
+    constexpr int U = BPW >= 8 ? 1 : 8 / BPW;
+    const int Lfull = s.L - s.L % (4 * U);
+    for (int p0 = 0; p0 < Lfull; p0 += 4 * U) contract_step<BPW, U, false>(Xs, Gs, Po, koff, goff, p0, kq, s.L, acc);
+    if (Lfull < s.L) contract_step<BPW, U, true>(Xs, Gs, Po, koff, goff, Lfull, kq, s.L, acc);
+#pragma unroll
+    for (int j = 0; j < BPW; ++j) {
+        const int blk = b0 + j;
+        if (blk >= nblocks) continue;
+        const int bm = blk % s.nbm, bn = blk / s.nbm;
+        const int co = bn * 16 + r16;
+        // lane holds kk = bm*16 + 4*kq + r (r = 0..3) of column co
+        const int kk0 = bm * 16 + 4 * kq;
+        if (co < s.Cout) {
+            const float g0 = scale * acc[j][0], g1 = scale * acc[j][1];
+            const float g2 = scale * acc[j][2], g3 = scale * acc[j][3];
+            float *dst = G + (i64)co * s.KK + kk0;
+            if (s.vec && kk0 + 3 < s.KK) {
+                *reinterpret_cast<float4 *>(dst) = make_float4(g0, g1, g2, g3);
+                sq += g0 * g0 + g1 * g1 + g2 * g2 + g3 * g3;
+            } else {
+                if (kk0 + 0 < s.KK) { dst[0] = g0; sq += g0 * g0; }
+                if (kk0 + 1 < s.KK) { dst[1] = g1; sq += g1 * g1; }
+                if (kk0 + 2 < s.KK) { dst[2] = g2; sq += g2 * g2; }
+                if (kk0 + 3 < s.KK) { dst[3] = g3; sq += g3 * g3; }
+            }
+        }
+    }
+
+    // ---- the sample's squared norm: waves' sums in wave order
+    sq = wave_sum(sq);
+    if (lane == 0) red[wave] = sq;
+    __syncthreads();
+    if (tid == 0 && sqnorm) {
+        float t = 0.0f;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) t += red[w];
+        sqnorm[n] = t;
+    }
+}
+
+// floats of dynamic LDS a workgroup needs
+inline long lds_floats(const SmallShape &s)
+{
+    // the bias partials [segs][Cout] follow the position table
+    return (long)s.po_off + s.Lp + kThreads;
+}
+
+// the shape's derived sizes; false if the sample does not fit
+inline bool make_small(const ConvSmallArgs &a, SmallShape &s)
+{
+    s.Cin = (int)a.Cin; s.H = (int)a.H; s.W = (int)a.W; s.Cout = (int)a.Cout;
+    s.kh = (int)a.kh; s.kw = (int)a.kw; s.sh = (int)a.sh; s.sw = (int)a.sw; s.ph = (int)a.ph; s.pw = (int)a.pw;
+    s.Ho = (int)a.Ho; s.Wo = (int)a.Wo;
+    s.Hp = s.H + 2 * s.ph;
+    s.Wp = s.W + 2 * s.pw;
+    s.plane = s.Hp * s.Wp;
+    s.L = s.Ho * s.Wo;
+    s.Lp = (s.L + 31) & ~31;
+    s.khw = s.kh * s.kw;
+    s.KK = s.Cin * s.khw;
+    s.nbm = (s.KK + 15) / 16;
+    s.nbn = (s.Cout + 15) / 16;
+    s.bpw = 1;
+    while (s.bpw * kWaves < s.nbm * s.nbn) s.bpw *= 2;
+    s.gs_off = s.Cin * s.plane;
+    s.gst = s.Lp + 4;
+    s.po_off = s.gs_off + s.Cout * s.gst;
+    s.inv_hw = 1.0f / (float)(s.H * s.W);
+    s.inv_w = 1.0f / (float)s.W;
+    s.inv_l = 1.0f / (float)s.L;
+    s.inv_wo = 1.0f / (float)s.Wo;
+    s.vec = 0;
+    return a.Cout <= kThreads && lds_floats(s) * 4 <= kSmallLds && s.bpw <= kMaxBpw &&
+           (long)s.Cin * s.H * s.W < (1L << 22) && (long)s.Cout * s.L < (1L << 22);
+}
+
+}  // namespace csmall
+}  // namespace dpg

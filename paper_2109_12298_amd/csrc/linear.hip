@@ -3,9 +3,7 @@
 // Per-sample gradient of y_t = W x_t + b for sample n (appendix "Vectorized
 // Computation"; extra dimensions summed):
 //   gW_n = s * B_n^T A_n   (d_out x d_in, K = T positions),  gb_n = s * sum_t B_n,t
-// T = 1 is a rank-one outer product: pure HBM write traffic (about one flop
-// per 4 bytes written), so it gets a store-streaming kernel whose norm is the
-// closed form s^2 |B_n|^2 (|A_n|^2 + 1).  T > 1 is a real per-sample GEMM on
+// T = 1 is a rank-one outer product (linear_outer.hpp).  T > 1 is a real per-sample GEMM on
 // MFMA with the squared-norm partials taken from the accumulators in the
 // epilogue.
 //
@@ -16,13 +14,13 @@
 #include "mfma_tile.hpp"
 #include "linear_bf16.hpp"
 #include "grad_sample_bf16.hpp"
+#include "linear_outer.hpp"
 
 namespace dpg {
 namespace {
 
 constexpr int kThreads = 256;
 constexpr int kBM = 64, kBN = 64, kBK = 32;
-constexpr int kOuterMaxRows = 1024;   // gW rows per outer-product workgroup
 
 template <typename T>
 __device__ __forceinline__ float4 load4(const T *p, i64 i);
@@ -41,89 +39,15 @@ __device__ __forceinline__ float4 load4<uint16_t>(const uint16_t *p, i64 i)
                        __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u));
 }
 
-// ---------------------------------------------------------------------------
-// T = 1: gW[n][i][:] = s * B[n][i] * A[n][:]
-// ---------------------------------------------------------------------------
+// T = 1: the rank-one outer product (linear_outer.hpp), block = (sample, rows)
 template <typename T, bool VEC>
-__global__ __launch_bounds__(kThreads) void outer_kernel(const T *__restrict__ A,
-                                                         const T *__restrict__ B, i64 din,
+__global__ __launch_bounds__(kThreads) void outer_kernel(const T *__restrict__ A, const T *__restrict__ B, i64 din,
                                                          i64 dout, int rows, int bps, float scale,
-                                                         float *__restrict__ gW,
-                                                         float *__restrict__ gb,
+                                                         float *__restrict__ gW, float *__restrict__ gb,
                                                          float *__restrict__ sqnorm)
 {
-    __shared__ float red[16];
-    const i64 n = blockIdx.x / bps;
-    const int rb = blockIdx.x % bps;
-    const i64 i0 = (i64)rb * rows;
-    const i64 i1 = i0 + rows < dout ? i0 + rows : dout;
-    __shared__ float bsh[kOuterMaxRows];
-    const T *An = A + n * din;
-    const T *Bn = B + n * dout;
-    float *G = gW + n * dout * din;
-    const bool do_norm = sqnorm != nullptr && rb == 0;
-
-    // Every load of the block is issued before the one barrier: the sample's
-    // activation (kept in registers when it fits), the block's backprop rows
-    // (into LDS), and, for the norm, the whole backprop row.
-    constexpr int KA = 4;
-    const i64 nv = VEC ? din / 4 : 0;
-    const bool inreg = VEC && nv <= (i64)kThreads * KA;
-    float4 a[KA];
-    float na = 0.0f, nb = 0.0f;
-    if (inreg) {
-#pragma unroll
-        for (int k = 0; k < KA; ++k) {
-            const i64 j4 = threadIdx.x + (i64)k * kThreads;
-            a[k] = j4 < nv ? load4<T>(An, 4 * j4) : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
-    }
-    if (do_norm) {
-        for (i64 i = threadIdx.x; i < dout; i += kThreads) {
-            const float b = load_elem<T>(Bn, i);
-            nb += b * b;
-        }
-    }
-    for (i64 i = i0 + threadIdx.x; i < i1; i += kThreads) bsh[i - i0] = scale * load_elem<T>(Bn, i);
-    __syncthreads();
-
-    if (inreg) {
-#pragma unroll
-        for (int k = 0; k < KA; ++k) {
-            const i64 j4 = threadIdx.x + (i64)k * kThreads;
-            if (j4 >= nv) break;
-            na += a[k].x * a[k].x + a[k].y * a[k].y + a[k].z * a[k].z + a[k].w * a[k].w;
-            for (i64 i = i0; i < i1; ++i) {
-                const float b = bsh[i - i0];
-                *reinterpret_cast<float4 *>(G + i * din + 4 * j4) =
-                    make_float4(b * a[k].x, b * a[k].y, b * a[k].z, b * a[k].w);
-            }
-        }
-    } else if (VEC) {
-        for (i64 j4 = threadIdx.x; j4 < nv; j4 += kThreads) {
-            const float4 av = load4<T>(An, 4 * j4);
-            na += av.x * av.x + av.y * av.y + av.z * av.z + av.w * av.w;
-            for (i64 i = i0; i < i1; ++i) {
-                const float b = bsh[i - i0];
-                *reinterpret_cast<float4 *>(G + i * din + 4 * j4) = make_float4(b * av.x, b * av.y, b * av.z, b * av.w);
-            }
-        }
-    } else {
-        for (i64 j = threadIdx.x; j < din; j += kThreads) {
-            const float av = load_elem<T>(An, j);
-            na += av * av;
-            for (i64 i = i0; i < i1; ++i) G[i * din + j] = bsh[i - i0] * av;
-        }
-    }
-    if (gb) {
-        for (i64 i = i0 + threadIdx.x; i < i1; i += kThreads) gb[n * dout + i] = bsh[i - i0];
-    }
-    if (do_norm) {
-        // closed form of the rank-one gradient: s^2 |B_n|^2 (|A_n|^2 + 1)
-        na = block_sum(na, red);
-        nb = block_sum(nb, red);
-        if (threadIdx.x == 0) sqnorm[n] = scale * scale * nb * (na + (gb ? 1.0f : 0.0f));
-    }
+    louter::outer_block<T, VEC>(A, B, din, dout, rows, blockIdx.x / bps, (int)(blockIdx.x % bps), scale, gW, gb,
+                                sqnorm);
 }
 
 // ---------------------------------------------------------------------------
@@ -401,11 +325,8 @@ extern "C" dp_status dp_grad_sample_linear(const void *A, const void *B, dp_dtyp
         return launch_status();
     }
     if (T == 1) {
-        int rows = (int)(8192 / d_in);
-        if (rows < 1) rows = 1;
-        if (rows > kOuterMaxRows) rows = kOuterMaxRows;
-        if (rows > d_out) rows = (int)d_out;
-        const int bps = (int)ceil_div(d_out, rows);
+        const louter::OuterPlan op = louter::outer_plan(d_in, d_out);
+        const int rows = op.rows, bps = op.bps;
         const dim3 grid((unsigned)(N * bps));
         const bool vec = (d_in % 4) == 0 && aligned(A, dt == DP_F32 ? 16 : 8) && aligned(gW, 16);
         if (dt == DP_F32) {

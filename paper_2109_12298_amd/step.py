@@ -171,6 +171,18 @@ class DPStep:
                                                               for lb in self.layers)
         need = dp.dp_norms_clip_noise_workspace_bytes(self.group, self.group_count, N)
         self.ws = torch.empty(max(need, 256), dtype=torch.uint8, device=self.device)
+        # Linear (T = 1) and small Conv2d layers: per-sample grads in one grouped launch
+        self.grad_group: List[int] = []
+        items = [self._grad_item(i) for i in range(len(self.layers))]
+        cand = [i for i, it in enumerate(items) if it is not None]
+        if cand:
+            arr = dp.make_layer_grads([items[i] for i in cand])
+            grouped = [i for k, i in enumerate(cand) if dp.dp_grad_sample_many_grouped(arr, k, self.dt, N)]
+            if len(grouped) >= 2:
+                self.grad_group = grouped
+                self.group_items = dp.make_layer_grads([items[i] for i in grouped])
+                need = dp.dp_grad_sample_many_workspace_bytes(self.group_items, len(grouped), self.dt, N)
+                self.ws_group = torch.empty(max(need, 256), dtype=torch.uint8, device=self.device)
         self.step_dev = torch.zeros(1, dtype=torch.int64, device=self.device)
         self.graph = None
         self.graph_parallel = None
@@ -189,7 +201,30 @@ class DPStep:
             return lb.gW if key == "weight" else lb.gb
         raise KeyError(pname)
 
+    def _grad_item(self, i: int):
+        """Layer i as a dp_layer_grad entry (Linear and Conv2d only), else None."""
+        lb = self.layers[i]
+        L = lb.layer
+        sq = self.sqnorm[i]
+        if isinstance(L, W.Linear):
+            return dp.linear_grad_item(lb.A, lb.B, L.T, L.d_in, L.d_out, self.scale, lb.gW, lb.gb, sq)
+        if isinstance(L, W.Conv2d):
+            ho, wo = L.out_hw
+            return dp.conv2d_grad_item(lb.A, lb.B, L.c_in, L.h, L.w, L.c_out, ho, wo, L.k[0], L.k[1], L.stride[0],
+                                       L.stride[1], L.pad[0], L.pad[1], self.scale, lb.gW, lb.gb, sq)
+        return None
+
+    def grad_calls(self) -> List[str]:
+        """The per-sample-gradient calls of a step, in order."""
+        calls = ["grad:group"] if self.grad_group else []
+        return calls + ["grad:" + lb.layer.name for i, lb in enumerate(self.layers) if i not in self.grad_group]
+
     # ------------------------------------------------------------------ pieces
+    def grad_group_call(self, stream=None):
+        """The grouped layers' per-sample gradients in one launch."""
+        dp.dp_grad_sample_many(self.group_items, len(self.grad_group), self.dt, self.N, self.status, self.ws_group,
+                               stream)
+
     def grad_sample(self, i: int, stream=None):
         lb = self.layers[i]
         layer = lb.layer
@@ -242,6 +277,8 @@ class DPStep:
             return self.clip_noise(step, None, stream)
         if name == "clip:linears":
             return self.linear_clip_sums(stream)
+        if name == "grad:group":
+            return self.grad_group_call(stream)
         kind, lname = name.split(":", 1)
         i = next(k for k, lb in enumerate(self.layers) if lb.layer.name == lname)
         if kind == "grad":
@@ -273,10 +310,10 @@ class DPStep:
         if not parallel:
             if advance:
                 dp.dp_step_advance(step_dev, 1, stream)
-            for i, lb in enumerate(self.layers):
-                if mark: mark("grad:" + lb.layer.name, "start")
-                self.grad_sample(i, stream)
-                if mark: mark("grad:" + lb.layer.name, "end")
+            for name in self.grad_calls():
+                if mark: mark(name, "start")
+                self.call(name, step, stream)
+                if mark: mark(name, "end")
             if not self.fold_norms:
                 if mark: mark("norms", "start")
                 self.norms(stream)
@@ -296,10 +333,10 @@ class DPStep:
             return
         main = torch.cuda.current_stream(self.device)
         side = self._fork(len(self.layers) + 1)
-        for i in range(len(self.layers)):
-            side[i].wait_stream(main)
-            with torch.cuda.stream(side[i]):
-                self.grad_sample(i)
+        for k, name in enumerate(self.grad_calls()):
+            side[k].wait_stream(main)
+            with torch.cuda.stream(side[k]):
+                self.call(name, step)
         if advance:
             side[-1].wait_stream(main)
             with torch.cuda.stream(side[-1]):

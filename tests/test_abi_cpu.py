@@ -148,3 +148,39 @@ def test_conv2d_path_choice_round_trips():
         assert dp.dp_conv2d_set_path(dp.DP_CONV_AUTO) == dp.DP_CONV_AUTO
     finally:
         dp.dp_conv2d_set_path(prev)
+
+
+def test_grad_sample_many_grouping_and_validation():
+    """Which layers the grouped per-sample-gradient launch takes, and that an
+    invalid layer anywhere in the list is refused before anything runs."""
+    fc = dp.linear_grad_item(FAKE, FAKE, 1, 512, 32, 1.0, FAKE)
+    seq = dp.linear_grad_item(FAKE, FAKE, 8, 64, 16, 1.0, FAKE)
+    c1 = dp.conv2d_grad_item(FAKE, FAKE, 1, 28, 28, 16, 14, 14, 8, 8, 2, 2, 3, 3, 1.0, FAKE)
+    big = dp.conv2d_grad_item(FAKE, FAKE, 64, 32, 32, 64, 32, 32, 3, 3, 1, 1, 1, 1, 1.0, FAKE)
+    items = dp.make_layer_grads([fc, seq, c1, big])
+    got = [dp.dp_grad_sample_many_grouped(items, k, dp.DP_F32, 256) for k in range(4)]
+    assert got == [True, False, True, False]
+    # the forced tiled conv kernel keeps convolutions out of the group
+    prev = dp.dp_conv2d_set_path(dp.DP_CONV_TILED)
+    try:
+        assert not dp.dp_grad_sample_many_grouped(items, 2, dp.DP_F32, 256)
+    finally:
+        dp.dp_conv2d_set_path(prev)
+    # workspace: the largest need of the layers outside the group
+    need = dp.dp_grad_sample_many_workspace_bytes(items, 4, dp.DP_F32, 256)
+    assert need == max(dp.dp_grad_sample_linear_workspace_bytes(256, 8, 64, 16, dp.DP_F32),
+                       dp.dp_grad_sample_conv2d_workspace_bytes(256, 64, 32, 32, 64, 3, 3, 1, 1, 1, 1))
+    f = dp.dp_grad_sample_many
+    assert code_of(f, items, 2, 7, 256, stream=0) == dp.DP_EDTYPE
+    assert code_of(f, items, 65, dp.DP_F32, 256, stream=0) == dp.DP_EINVAL
+    bad_ho = dict(c1, Ho=13)
+    assert code_of(f, dp.make_layer_grads([fc, bad_ho]), 2, dp.DP_F32, 256, stream=0) == dp.DP_EINVAL
+    no_out = dict(fc, gW=None)
+    assert code_of(f, dp.make_layer_grads([c1, no_out]), 2, dp.DP_F32, 256, stream=0) == dp.DP_EINVAL
+    bad_kind = dict(fc, kind=5)
+    assert code_of(f, dp.make_layer_grads([bad_kind]), 1, dp.DP_F32, 4, stream=0) == dp.DP_EINVAL
+    # a missing workspace for the layers that run alone
+    assert code_of(f, items, 4, dp.DP_F32, 256, stream=0) == dp.DP_EINVAL
+    # empty batches and empty lists enqueue nothing
+    assert code_of(f, items, 4, dp.DP_F32, 0, stream=0) == dp.DP_OK
+    assert code_of(f, items, 0, dp.DP_F32, 256, stream=0) == dp.DP_OK
