@@ -17,7 +17,9 @@
 // bias sums and the sample's squared norm are added in a fixed order, so the
 // norm goes straight to sqnorm[n] (no partials).  Against the general kernel
 // this keeps a sample's fixed costs (one load round trip, no K split, no
-// second pass) small, which is what bounds these tiny convolutions.
+// second pass) small, which is what bounds these tiny convolutions.  The
+// body lives in conv2d_small_dev.hpp, shared with the grouped
+// per-sample-gradient kernel.
 #include "common.hpp"
 #include "conv2d_small.hpp"
 #include "conv2d_small_dev.hpp"

@@ -26,6 +26,9 @@ struct SmallShape {
     int gs_off, po_off;           // LDS float offsets of the backprop and the position table
     int vec;                      // float4 stores of gW
     float inv_hw, inv_w, inv_l, inv_wo;
+    // stepping a thread's element index by kThreads: the input's (row, column)
+    // advance and LDS slot advance, and the backprop's position and slot advance
+    int xd_w, xd_h, xd_slot, gd_p, gd_slot;
 };
 
 constexpr int kMaxBpw = 8;        // accumulator blocks a wave holds at once
@@ -38,15 +41,6 @@ __device__ __forceinline__ void fdivmod(int x, int d, float inv_d, int &q, int &
     r = x - q * d;
     q += (r >= d ? 1 : 0) - (r < 0 ? 1 : 0);
     r = x - q * d;
-}
-
-// element e of the sample's input goes to its padded-plane slot
-__device__ __forceinline__ int x_slot(int e, const SmallShape &s)
-{
-    int c, r, h, w;
-    fdivmod(e, s.H * s.W, s.inv_hw, c, r);
-    fdivmod(r, s.W, s.inv_w, h, w);
-    return c * s.plane + (h + s.ph) * s.Wp + w + s.pw;
 }
 
 // U position steps (4 positions each: lane group kq takes position p0 + 4u + kq)
@@ -99,15 +93,28 @@ __device__ __forceinline__ void conv_small_sample(const T *__restrict__ X, const
     const T *Gn = GY + n * s.Cout * s.L;
     const int xcount = s.Cin * s.H * s.W, gcount = s.Cout * s.L;
 
-    // ---- staging: clear the planes and the backprop tail while the first
-    // round of loads is in flight, then write the loaded values
+    // ---- staging: clear the planes and build the position table while the
+    // first round of loads is in flight, then write the loaded values.  A
+    // thread's elements are tid, tid + kThreads, ...; their LDS slots are
+    // stepped incrementally (one division per thread, not per element).
+    int xw, xh, xslot, gp, gslot;
+    {
+        int c, r, co;
+        fdivmod(tid, s.H * s.W, s.inv_hw, c, r);
+        fdivmod(r, s.W, s.inv_w, xh, xw);
+        xslot = c * s.plane + (xh + s.ph) * s.Wp + xw + s.pw;
+        fdivmod(tid, s.L, s.inv_l, co, gp);
+        gslot = co * s.gst + gp;
+    }
+    const T *xp = Xn + tid;
+    const T *gp_ = Gn + tid;
     for (int e0 = 0; e0 < xcount || e0 < gcount; e0 += kBatch * kThreads) {
         float xv[kBatch], gv[kBatch];
 #pragma unroll
         for (int j = 0; j < kBatch; ++j) {
             const int e = e0 + j * kThreads + tid;
-            xv[j] = e < xcount ? load_elem<T>(Xn, e) : 0.0f;
-            gv[j] = e < gcount ? load_elem<T>(Gn, e) : 0.0f;
+            xv[j] = e < xcount ? load_elem<T>(xp, e0 + j * kThreads) : 0.0f;
+            gv[j] = e < gcount ? load_elem<T>(gp_, e0 + j * kThreads) : 0.0f;
         }
         if (e0 == 0) {
             for (int i = tid; i < s.Cin * s.plane; i += kThreads) Xs[i] = 0.0f;
@@ -121,11 +128,26 @@ __device__ __forceinline__ void conv_small_sample(const T *__restrict__ X, const
 #pragma unroll
         for (int j = 0; j < kBatch; ++j) {
             const int e = e0 + j * kThreads + tid;
-            if (e < xcount) Xs[x_slot(e, s)] = xv[j];
-            if (e < gcount) {
-                int co, p;
-                fdivmod(e, s.L, s.inv_l, co, p);
-                Gs[co * s.gst + p] = gv[j];
+            if (e < xcount) Xs[xslot] = xv[j];
+            if (e < gcount) Gs[gslot] = gv[j];
+            // element e + kThreads: column carry into the row, row carry into the plane
+            xw += s.xd_w;
+            xslot += s.xd_slot;
+            if (xw >= s.W) {
+                xw -= s.W;
+                xslot += s.Wp - s.W;
+                ++xh;
+            }
+            xh += s.xd_h;
+            if (xh >= s.H) {
+                xh -= s.H;
+                xslot += s.plane - s.H * s.Wp;
+            }
+            gp += s.gd_p;
+            gslot += s.gd_slot;
+            if (gp >= s.L) {
+                gp -= s.L;
+                gslot += s.gst - s.L;
             }
         }
     }
@@ -254,6 +276,14 @@ inline bool make_small(const ConvSmallArgs &a, SmallShape &s)
     s.inv_w = 1.0f / (float)s.W;
     s.inv_l = 1.0f / (float)s.L;
     s.inv_wo = 1.0f / (float)s.Wo;
+    {
+        const int rows = kThreads / s.W;
+        s.xd_w = kThreads % s.W;
+        s.xd_h = rows % s.H;
+        s.xd_slot = (rows / s.H) * s.plane + s.xd_h * s.Wp + s.xd_w;
+        s.gd_p = kThreads % s.L;
+        s.gd_slot = (kThreads / s.L) * s.gst + s.gd_p;
+    }
     s.vec = 0;
     return a.Cout <= kThreads && lds_floats(s) * 4 <= kSmallLds && s.bpw <= kMaxBpw &&
            (long)s.Cin * s.H * s.W < (1L << 22) && (long)s.Cout * s.L < (1L << 22);

@@ -186,6 +186,7 @@ class DPStep:
         self.step_dev = torch.zeros(1, dtype=torch.int64, device=self.device)
         self.graph = None
         self.graph_parallel = None
+        self.steps_per_replay = 1
         self._side = None
 
     def _grad_for(self, pname: str):
@@ -359,7 +360,7 @@ class DPStep:
             main.wait_stream(side[k])
         self.clip_noise(step, step_dev)
 
-    def capture(self, first_step: int = 0, parallel: Optional[bool] = None):
+    def capture(self, first_step: int = 0, parallel: Optional[bool] = None, steps_per_replay: int = 1):
         """Capture one step as a HIP graph; replay r runs step first_step + r.
 
         The graph advances its own device step counter (in a branch that runs
@@ -368,7 +369,10 @@ class DPStep:
         or one chain (False); None captures both, times a few replays of
         each and keeps the faster (branches pay off when the layers' kernels
         are long enough to overlap; for short kernels the single chain has
-        less scheduling overhead)."""
+        less scheduling overhead).
+        steps_per_replay: whole steps recorded back to back in the graph, so
+        that one replay launch covers several steps (each still a full pass
+        over the batch, with its own step number)."""
         torch = _torch()
         if parallel is None:
             import time
@@ -386,7 +390,7 @@ class DPStep:
                 if best is None or dt < best[0]:
                     best = (dt, par)
             self.graph_parallel = best[1]
-            return self.capture(first_step, best[1])
+            return self.capture(first_step, best[1], steps_per_replay)
         side = torch.cuda.Stream(self.device)
         side.wait_stream(torch.cuda.current_stream(self.device))
         with torch.cuda.stream(side):
@@ -395,11 +399,13 @@ class DPStep:
         torch.cuda.synchronize(self.device)
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
-            self.run(step=0, step_dev=self.step_dev, parallel=parallel, advance=True, clear_status=False)
+            for _ in range(steps_per_replay):
+                self.run(step=0, step_dev=self.step_dev, parallel=parallel, advance=True, clear_status=False)
         torch.cuda.synchronize(self.device)
         self.step_dev.fill_(first_step - 1)    # advanced to first_step by the first replay
         self.graph = g
         self.graph_parallel = parallel
+        self.steps_per_replay = steps_per_replay
         return g
 
     def replay(self):

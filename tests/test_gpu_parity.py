@@ -485,6 +485,27 @@ def test_graph_replay_matches_eager_steps():
     assert int(st.step_dev.item()) == 7     # the counter holds the last replayed step
 
 
+@pytest.mark.parametrize("parallel", [False, True])
+def test_graph_with_several_steps_per_replay(parallel):
+    """A graph holding three steps: each replay runs steps s, s+1, s+2 (each
+    with its own noise), leaving the last step's outputs."""
+    wl = W.get("mnist_cnn")
+    inputs = W.make_inputs(wl, n=20)
+    st = DPStep(wl, inputs, DEV)
+    say("graph capture mnist_cnn, 3 steps per replay, parallel", parallel)
+    st.capture(first_step=2, parallel=parallel, steps_per_replay=3)
+    eager = DPStep(wl, inputs, DEV)
+    for k in range(2):
+        st.replay()
+        got = st.results()
+        eager.run(step=2 + 3 * k + 2)
+        ref = eager.results()
+        for name in ref["out"]:
+            np.testing.assert_array_equal(got["out"][name], ref["out"][name], err_msg="replay %d %s" % (k, name))
+        np.testing.assert_array_equal(got["norm"], ref["norm"])
+    assert int(st.step_dev.item()) == 7
+
+
 @pytest.mark.parametrize("N", [0, 5, 40, 300, 4100])
 def test_norms_clip_noise_one_launch_matches_two_launch_path(N):
     """dp_norms_clip_noise (norms, column reduce and finish in one launch)
