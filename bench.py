@@ -279,6 +279,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--breakdown", action="store_true", help="print per-call event times to stderr")
     ap.add_argument("--eager", action="store_true", help="time eager launches instead of graph replays")
+    ap.add_argument("--steps-per-replay", type=int, default=0,
+                    help="steps recorded in the replayed graph (default: the largest of 10, 8, 5, 4, 2, 1 "
+                         "dividing --steps)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run a plain device copy of this size (for counter calibration)")
     ap.add_argument("--meta-out", default="", help="write the dominant call's name and launch count here")
@@ -315,7 +318,9 @@ def main():
     # holds r steps back to back (r the largest of 10, 8, 5, 4, 2, 1 that
     # divides K, so that a replay's launch overhead is shared by r steps);
     # eager launches with --eager
-    r = next(d for d in (10, 8, 5, 4, 2, 1) if args.steps % d == 0)
+    r = args.steps_per_replay or next(d for d in (10, 8, 5, 4, 2, 1) if args.steps % d == 0)
+    if args.steps % r:
+        raise SystemExit("--steps must be a multiple of --steps-per-replay")
     if not args.eager:
         st.capture(first_step=0, steps_per_replay=r)
     for i in range(max(args.warmup // r, 1) if not args.eager else args.warmup):
