@@ -68,7 +68,12 @@ def call_costs(st):
             bias = L.d_out if L.bias else 0
             grads = N * (L.d_out * L.d_in + bias) * 4
             bf_mfma = bf and L.T > 1 and L.d_in % 8 == 0 and L.d_out % 8 == 0
-            if L.T == 1:
+            if lb.ghost:
+                # the two T x T Grams per sample; reads A and B, writes one norm
+                out["grad:" + L.name] = (N * L.T * (L.d_in + L.d_out) * e + N * 4,
+                                         2 * N * L.T * L.T * (L.d_in + L.d_out), "ghost_norm_kernel",
+                                         "bf16" if bf else "f32")
+            elif L.T == 1:
                 out["grad:" + L.name] = (N * (L.d_in + L.d_out) * e + grads + N * 4, N * L.d_out * L.d_in,
                                          "outer_kernel", None)
             else:
@@ -83,11 +88,12 @@ def call_costs(st):
                 # bias sums are column reductions of the stored bias gradients
                 grouped = bf and L.T % 32 == 0 and L.d_in % 8 == 0 and L.d_out % 8 == 0
                 b0, f0, _, _ = out.get("clip:linears", (0, 0, None, None))
-                out["clip:linears"] = (b0 + N * L.T * (L.d_in + L.d_out) * e + L.d_out * L.d_in * 4,
+                out["clip:linears"] = (b0 + N * L.T * (L.d_in + L.d_out) * e + L.d_out * L.d_in * 4
+                                       + (bias * 4 if lb.ghost else 0),
                                        f0 + 2 * N * L.T * L.d_in * L.d_out,
                                        "bf16_clipsum_many_kernel" if grouped else "clipsum_gemm_kernel",
                                        "bf16" if grouped else "f32")
-                col_bytes += N * bias * 4
+                col_bytes += 0 if lb.ghost else N * bias * 4
             else:
                 col_bytes += grads
         elif isinstance(L, W.Conv2d):
@@ -137,6 +143,7 @@ def src_hash(paths):
 
 KERNEL_SOURCES = {
     "outer_kernel": ["paper_2109_12298_amd/csrc/linear.hip", "paper_2109_12298_amd/csrc/linear_outer.hpp"],
+    "ghost_norm_kernel": ["paper_2109_12298_amd/csrc/ghost.hip"],
     "conv_small_kernel": ["paper_2109_12298_amd/csrc/conv2d_small.hip",
                           "paper_2109_12298_amd/csrc/conv2d_small_dev.hpp"],
     "grad_many_kernel": ["paper_2109_12298_amd/csrc/grad_many.hip", "paper_2109_12298_amd/csrc/conv2d_small_dev.hpp",
@@ -279,6 +286,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--breakdown", action="store_true", help="print per-call event times to stderr")
     ap.add_argument("--eager", action="store_true", help="time eager launches instead of graph replays")
+    ap.add_argument("--norm-mode", default="materialize", choices=["materialize", "ghost"],
+                    help="ghost: Linear layers with a fused clipped sum and 2T^2 < d_in*d_out take their "
+                         "per-sample norms from the Gram matrices and never form per-sample gradients")
     ap.add_argument("--steps-per-replay", type=int, default=0,
                     help="steps recorded in the replayed graph (default: the largest of 10, 8, 5, 4, 2, 1 "
                          "dividing --steps)")
@@ -306,7 +316,7 @@ def main():
     inputs = W.make_inputs(wl)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    st = DPStep(wl, inputs, dev, clip_mode=args.clip_mode)
+    st = DPStep(wl, inputs, dev, clip_mode=args.clip_mode, norm_mode=args.norm_mode)
     stream = torch.cuda.current_stream(dev)
     costs = call_costs(st)
 
@@ -421,7 +431,8 @@ def main():
             "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": dtype,
             "data": "synthetic",
             "config": {"workload": wl.name, "batch": wl.N, "params": wl.n_params,
-                       "layers": [l.name for l in wl.layers], "C": wl.C, "sigma": wl.sigma},
+                       "layers": [l.name for l in wl.layers], "C": wl.C, "sigma": wl.sigma,
+                       "norms": args.norm_mode},
             "roofline": roof}
     if args.meta_out:
         with open(args.meta_out, "w") as f:

@@ -213,6 +213,25 @@ dp_status dp_grad_sample_layernorm(const void *xhat, const void *B, dp_dtype dt,
 dp_status dp_per_sample_norms(const float *sqnorm, int32_t n_layers, int64_t N, float *norm,
                               int32_t *status, hipStream_t stream);
 
+/* Ghost norm of a Linear layer: its per-sample squared gradient norm without
+ * forming the per-sample gradient.  The related-work section ("Gradient
+ * Clipping") describes computing only each sample's gradient norm (exact for
+ * fully connected layers, extended to sequential inputs by ghost clipping).
+ * With the Gram matrices G_A = A_n A_n^T and G_B = B_n B_n^T (T x T):
+ *   sqnorm[n] = s^2 * sum_{t,t'} G_B[t][t'] * (G_A[t][t'] + (bias ? 1 : 0))
+ * which equals |gW_n|^2 + |gb_n|^2 of dp_grad_sample_linear on the same
+ * inputs (up to rounding).  Worth it when 2 T^2 < d_in * d_out.
+ * A: [N][T][d_in] of `dt`; B: [N][T][d_out] of `dt`; sqnorm fp32 [N]
+ * (overwritten, required when N > 0).  N >= 0, T >= 0 (T = 0 gives zeros),
+ * d_in, d_out >= 1.  Workspace: dp_ghost_norm_linear_workspace_bytes(N, T,
+ * d_in, d_out) bytes (the Gram tiles of the feature chunks, 16 KB per
+ * sample, 64 x 64 tile pair and chunk; zero when N or T is 0). */
+size_t dp_ghost_norm_linear_workspace_bytes(int64_t N, int64_t T, int64_t d_in, int64_t d_out);
+dp_status dp_ghost_norm_linear(const void *A, const void *B, dp_dtype dt, int64_t N, int64_t T,
+                               int64_t d_in, int64_t d_out, float scale, int32_t bias,
+                               float *sqnorm, int32_t *status, void *ws, size_t ws_bytes,
+                               hipStream_t stream);
+
 /* sqnorm[n] = sum_e G[n][e]^2 for an already materialized per-sample gradient
  * G fp32 [N][numel] (overwritten). */
 dp_status dp_sqnorm_from_grads(const float *G, int64_t N, int64_t numel, float *sqnorm,

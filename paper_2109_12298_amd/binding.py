@@ -47,6 +47,8 @@ SIGNATURES = {
     "dp_grad_sample_layernorm_workspace_bytes": (_SZ, [_I64, _I64, _I64]),
     "dp_grad_sample_layernorm": (_ST, [_P, _P, _ST, _I64, _I64, _I64, _F, _P, _P, _P, _P, _P, _SZ, _P]),
     "dp_per_sample_norms": (_ST, [_P, _I32, _I64, _P, _P, _P]),
+    "dp_ghost_norm_linear_workspace_bytes": (_SZ, [_I64, _I64, _I64, _I64]),
+    "dp_ghost_norm_linear": (_ST, [_P, _P, _ST, _I64, _I64, _I64, _I64, _F, _I32, _P, _P, _P, _SZ, _P]),
     "dp_sqnorm_from_grads": (_ST, [_P, _I64, _I64, _P, _P, _P]),
     "dp_clip_factors": (_ST, [_P, _I64, _F, _P, _P, _P]),
     "dp_clip_accumulate_workspace_bytes": (_SZ, [_I64, _I64]),
@@ -335,6 +337,16 @@ def dp_clip_accumulate_linear_many(items, count, dt, N, norm, C, status=None, ws
     _check(lib().dp_clip_accumulate_linear_many(ctypes.cast(items, ctypes.c_void_p), count, dt, N, _ptr(norm), C,
                                                 _ptr(status), _ptr(ws), _nbytes(ws), _stream(stream)),
            "dp_clip_accumulate_linear_many")
+
+
+def dp_ghost_norm_linear_workspace_bytes(N, T, d_in, d_out) -> int:
+    return lib().dp_ghost_norm_linear_workspace_bytes(N, T, d_in, d_out)
+
+
+def dp_ghost_norm_linear(A, B, dt, N, T, d_in, d_out, scale, bias, sqnorm, status=None, ws=None, stream=None):
+    _check(lib().dp_ghost_norm_linear(_ptr(A), _ptr(B), dt, N, T, d_in, d_out, scale, 1 if bias else 0,
+                                      _ptr(sqnorm), _ptr(status), _ptr(ws), _nbytes(ws), _stream(stream)),
+           "dp_ghost_norm_linear")
 
 
 def dp_grad_sample_many_grouped(items, k, dt, N) -> bool:

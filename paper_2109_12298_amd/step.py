@@ -54,6 +54,7 @@ class LayerBufs:
     uniq: object = None
     rows: object = None
     clip_mode: str = "colreduce"
+    ghost: bool = False         # norm from the Gram matrices, no per-sample gradient
     ws: object = None          # scratch of the per-sample-gradient call
     ws_clip: object = None     # scratch of the fused clipped sum
 
@@ -89,7 +90,13 @@ class DPStep:
     """Device buffers and the ordered calls of one DP-SGD step."""
 
     def __init__(self, wl: W.Workload, inputs: List[W.LayerInputs], device="cuda", C=None, sigma=None,
-                 denom=None, scale=None, clip_mode: str = "auto", seed: Optional[int] = None):
+                 denom=None, scale=None, clip_mode: str = "auto", seed: Optional[int] = None,
+                 norm_mode: str = "materialize"):
+        """norm_mode: 'materialize' computes every layer's per-sample gradients
+        (the paper's method); 'ghost' gives a Linear layer whose clipped sum is
+        fused, and for which 2 T^2 < d_in * d_out, its per-sample norm from
+        the T x T Gram matrices instead, and never forms its per-sample
+        gradient (weight and bias sums then both come from the fused GEMM)."""
         torch = _torch()
         self.wl = wl
         self.device = torch.device(device)
@@ -111,10 +118,15 @@ class DPStep:
             lb.B = to_device(li.B, wl.dtype, self.device)
             need_g = need_c = 0
             if isinstance(layer, W.Linear):
-                lb.gW = torch.empty((N, layer.d_out, layer.d_in), **f32)
-                lb.gb = torch.empty((N, layer.d_out), **f32) if layer.bias else None
                 lb.clip_mode = linear_clip_mode(layer, N, wl.dtype) if clip_mode == "auto" else clip_mode
-                need_g = dp.dp_grad_sample_linear_workspace_bytes(N, layer.T, layer.d_in, layer.d_out, self.dt)
+                lb.ghost = (norm_mode == "ghost" and lb.clip_mode == "fused"
+                            and 2 * layer.T * layer.T < layer.d_in * layer.d_out)
+                if lb.ghost:
+                    need_g = dp.dp_ghost_norm_linear_workspace_bytes(N, layer.T, layer.d_in, layer.d_out)
+                else:
+                    lb.gW = torch.empty((N, layer.d_out, layer.d_in), **f32)
+                    lb.gb = torch.empty((N, layer.d_out), **f32) if layer.bias else None
+                    need_g = dp.dp_grad_sample_linear_workspace_bytes(N, layer.T, layer.d_in, layer.d_out, self.dt)
             elif isinstance(layer, W.Conv2d):
                 lb.gW = torch.empty((N, layer.c_out, layer.c_in) + tuple(layer.k), **f32)
                 lb.gb = torch.empty((N, layer.c_out), **f32) if layer.bias else None
@@ -154,8 +166,10 @@ class DPStep:
             lb = self.layers[i]
             L = lb.layer
             # the bias sums are column reductions of the stored per-sample bias
-            # gradients (N x d_out values) in the grouped clip/noise call
-            ents.append((lb.A, lb.B, L.T, L.d_in, L.d_out, self.scale, self.S[L.name + ".weight"], None))
+            # gradients (N x d_out values) in the grouped clip/noise call,
+            # unless the layer's gradients are not formed (ghost norms)
+            sumb = self.S[L.name + ".bias"] if (lb.ghost and L.bias) else None
+            ents.append((lb.A, lb.B, L.T, L.d_in, L.d_out, self.scale, self.S[L.name + ".weight"], sumb))
         self.linear_items = dp.make_linear_clips(ents)
         need = dp.dp_clip_accumulate_linear_many_workspace_bytes(self.linear_items, len(ents), self.dt, N)
         self.ws_linear = torch.empty(max(need, 256), dtype=torch.uint8, device=self.device)
@@ -197,7 +211,7 @@ class DPStep:
                 continue
             if isinstance(lb.layer, W.Embedding):
                 return None
-            if isinstance(lb.layer, W.Linear) and lb.clip_mode == "fused" and key == "weight":
+            if isinstance(lb.layer, W.Linear) and lb.clip_mode == "fused" and (key == "weight" or lb.ghost):
                 return None
             return lb.gW if key == "weight" else lb.gb
         raise KeyError(pname)
@@ -208,6 +222,8 @@ class DPStep:
         L = lb.layer
         sq = self.sqnorm[i]
         if isinstance(L, W.Linear):
+            if lb.ghost:
+                return None
             return dp.linear_grad_item(lb.A, lb.B, L.T, L.d_in, L.d_out, self.scale, lb.gW, lb.gb, sq)
         if isinstance(L, W.Conv2d):
             ho, wo = L.out_hw
@@ -230,7 +246,10 @@ class DPStep:
         lb = self.layers[i]
         layer = lb.layer
         N, s, sq = self.N, self.scale, self.sqnorm[i]
-        if isinstance(layer, W.Linear):
+        if isinstance(layer, W.Linear) and lb.ghost:
+            dp.dp_ghost_norm_linear(lb.A, lb.B, self.dt, N, layer.T, layer.d_in, layer.d_out, s, layer.bias, sq,
+                                    self.status, lb.ws, stream)
+        elif isinstance(layer, W.Linear):
             dp.dp_grad_sample_linear(lb.A, lb.B, self.dt, N, layer.T, layer.d_in, layer.d_out, s, lb.gW, lb.gb,
                                      sq, self.status, lb.ws, stream)
         elif isinstance(layer, W.Conv2d):
@@ -424,6 +443,8 @@ class DPStep:
                 rp = lb.row_ptr.cpu().numpy()
                 nnz = int(rp[-1])
                 res["grads"].append({"csr": (rp, lb.uniq[:nnz].cpu().numpy(), lb.rows[:nnz].cpu().numpy())})
+            elif lb.gW is None:
+                res["grads"].append({})            # ghost norm: no per-sample gradient formed
             else:
                 g = {"weight": lb.gW.cpu().numpy()}
                 if lb.gb is not None:

@@ -184,3 +184,21 @@ def test_grad_sample_many_grouping_and_validation():
     # empty batches and empty lists enqueue nothing
     assert code_of(f, items, 4, dp.DP_F32, 0, stream=0) == dp.DP_OK
     assert code_of(f, items, 0, dp.DP_F32, 256, stream=0) == dp.DP_OK
+
+
+def test_ghost_norm_validation():
+    f = dp.dp_ghost_norm_linear
+    assert code_of(f, FAKE, FAKE, 7, 2, 8, 3, 4, 1.0, True, FAKE, stream=0) == dp.DP_EDTYPE
+    assert code_of(f, FAKE, FAKE, dp.DP_F32, 2, 8, 0, 4, 1.0, True, FAKE, stream=0) == dp.DP_EINVAL
+    assert code_of(f, None, FAKE, dp.DP_F32, 2, 8, 3, 4, 1.0, True, FAKE, stream=0) == dp.DP_EINVAL
+    assert code_of(f, FAKE, FAKE, dp.DP_F32, 2, 8, 3, 4, 1.0, True, None, stream=0) == dp.DP_EINVAL
+    # Gram tiles: 16 KB per (sample, tile pair, feature chunk), plus one
+    # partial per (sample, pair) when there are several pairs
+    assert dp.dp_ghost_norm_linear_workspace_bytes(0, 64, 3, 4) == 0
+    assert dp.dp_ghost_norm_linear_workspace_bytes(5, 0, 3, 4) == 0
+    assert dp.dp_ghost_norm_linear_workspace_bytes(5, 64, 3, 4) == 5 * 2 * 16384
+    assert dp.dp_ghost_norm_linear_workspace_bytes(5, 65, 3, 4) == 5 * 3 * 2 * 16384 + 5 * 3 * 4
+    big = dp.dp_ghost_norm_linear_workspace_bytes(32, 128, 768, 3072)
+    assert big % 16384 == 3 * 32 * 4 and big > 32 * 3 * 2 * 16384
+    assert code_of(f, FAKE, FAKE, dp.DP_F32, 2, 65, 3, 4, 1.0, True, FAKE, stream=0) == dp.DP_EINVAL
+    assert code_of(f, None, None, dp.DP_F32, 0, 8, 3, 4, 1.0, True, None, stream=0) == dp.DP_OK

@@ -25,6 +25,8 @@ def say(*a):
 def compare_step(wl, inputs, got, ref, rtol, what):
     for li, g, r in zip(inputs, got["grads"], ref["grads"]):
         name = li.layer.name
+        if not g:
+            continue                # ghost norm: the layer's per-sample gradient is never formed
         if "csr" in r:
             rp, uq, rows = g["csr"]
             rrp, ruq, rrows = r["csr"]
@@ -60,6 +62,27 @@ def test_workload_step_matches_oracle(name, n, mode):
     got = st.results()
     ref = oracle.dp_step(wl, inputs, step=3)
     compare_step(wl, inputs, got, ref, RTOL[wl.dtype], name)
+
+
+@pytest.mark.parametrize("name,n,mode", [("transformer_block", 2, "fused"), ("text_lstm", 5, "fused"),
+                                         ("linear_tiny", None, "fused"), ("cifar_cnn", 3, "fused")])
+def test_workload_step_with_ghost_norms_matches_oracle(name, n, mode):
+    """Ghost norms for the fused Linear layers where 2 T^2 < d_in d_out: the
+    norms, clipped sums and outputs still match the oracle's step, which
+    forms every per-sample gradient."""
+    wl = W.get(name)
+    say(name, "n=", n, "ghost norms, clip mode", mode)
+    inputs = W.make_inputs(wl, n=n)
+    st = DPStep(wl, inputs, DEV, clip_mode=mode, norm_mode="ghost")
+    ghosts = [lb.layer.name for lb in st.layers if lb.ghost]
+    if name == "transformer_block":
+        assert ghosts == ["wq", "wk", "wv", "wo", "ffn1", "ffn2"]
+    if name == "text_lstm":
+        assert ghosts == ["fc"]           # T = 256 is too long for the LSTM weights (2 T^2 > d_in d_out)
+    st.run(step=3)
+    got = st.results()
+    ref = oracle.dp_step(wl, inputs, step=3)
+    compare_step(wl, inputs, got, ref, RTOL[wl.dtype], name + " ghost")
 
 
 def test_runs_are_bitwise_deterministic():
