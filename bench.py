@@ -129,7 +129,9 @@ def call_costs(st):
     P = st.wl.n_params
     # one launch: (norms,) read the column-reduced grads once, write S and out, read fused S
     norms_bytes = (len(st.layers) * N * 4 + N * 4) if st.fold_norms else 0
-    out["clip+noise"] = (col_bytes + 12 * P + norms_bytes, 0, "norms_clip_noise_kernel", None)
+    # virtual steps: the running sums are read and written as well
+    acc_bytes = 8 * P if st.virtual_batches > 1 else 0
+    out["clip+noise"] = (col_bytes + 12 * P + norms_bytes + acc_bytes, 0, "norms_clip_noise_kernel", None)
     return out
 
 
@@ -286,6 +288,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--breakdown", action="store_true", help="print per-call event times to stderr")
     ap.add_argument("--eager", action="store_true", help="time eager launches instead of graph replays")
+    ap.add_argument("--virtual-batches", type=int, default=1,
+                    help="K > 1: virtual steps, K physical batches (the resident inputs each time) per logical "
+                         "step, noised once; a step of the timed region is a logical step of K*N samples")
     ap.add_argument("--norm-mode", default="materialize", choices=["materialize", "ghost"],
                     help="ghost: Linear layers with a fused clipped sum and 2T^2 < d_in*d_out take their "
                          "per-sample norms from the Gram matrices and never form per-sample gradients")
@@ -316,12 +321,18 @@ def main():
     inputs = W.make_inputs(wl)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    st = DPStep(wl, inputs, dev, clip_mode=args.clip_mode, norm_mode=args.norm_mode)
+    st = DPStep(wl, inputs, dev, clip_mode=args.clip_mode, norm_mode=args.norm_mode,
+                virtual_batches=args.virtual_batches)
+    K = args.virtual_batches
+
+    def eager_step(i):
+        for k in range(K):
+            st.run(step=i, clear_status=(k == 0), reset=(k == 0), emit=(k == K - 1))
     stream = torch.cuda.current_stream(dev)
     costs = call_costs(st)
 
     for i in range(3):
-        st.run(step=i)
+        eager_step(i)
     torch.cuda.synchronize()
 
     # the timed region: K whole steps, replayed from a captured HIP graph that
@@ -334,12 +345,12 @@ def main():
     if not args.eager:
         st.capture(first_step=0, steps_per_replay=r)
     for i in range(max(args.warmup // r, 1) if not args.eager else args.warmup):
-        st.replay() if not args.eager else st.run(step=i)
+        st.replay() if not args.eager else eager_step(i)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     if args.eager:
         for i in range(args.steps):
-            st.run(step=args.warmup + i)
+            eager_step(args.warmup + i)
     else:
         for i in range(args.steps // r):
             st.replay()
@@ -353,7 +364,7 @@ def main():
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     for i in range(args.steps):
-        st.run(step=i)
+        eager_step(i)
     torch.cuda.synchronize()
     eager_ms = (time.perf_counter() - t1) * 1e3 / args.steps
 
@@ -422,7 +433,7 @@ def main():
     roof.update({"kernel": kname, "call": dominant, "avg_us": round(dom_ms * 1e3, 2),
                  "algorithmic_bytes": nbytes, "algorithmic_flops": flops})
 
-    line = {"metric": METRIC, "value": round(wl.N * args.steps / elapsed, 1), "unit": "samples/s",
+    line = {"metric": METRIC, "value": round(K * wl.N * args.steps / elapsed, 1), "unit": "samples/s",
             "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
             "launch": "eager" if args.eager else
             ("hip_graph_branches" if st.graph_parallel else "hip_graph_chain"),
@@ -432,7 +443,7 @@ def main():
             "data": "synthetic",
             "config": {"workload": wl.name, "batch": wl.N, "params": wl.n_params,
                        "layers": [l.name for l in wl.layers], "C": wl.C, "sigma": wl.sigma,
-                       "norms": args.norm_mode},
+                       "norms": args.norm_mode, "virtual_batches": K},
             "roofline": roof}
     if args.meta_out:
         with open(args.meta_out, "w") as f:

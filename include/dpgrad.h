@@ -327,6 +327,8 @@ typedef struct dp_param {
     int64_t numel;
     uint32_t param_index;     /* index of the tensor's noise stream (see dp_add_noise) */
     uint32_t flags;           /* DP_PARAM_REDUCE or 0; other bits must be 0 */
+    float *accum;             /* fp32 [numel] running clipped sum over the physical batches of
+                                 a logical batch (virtual steps), or NULL */
 } dp_param;
 
 enum { DP_PARAM_REDUCE = 1 };
@@ -334,7 +336,12 @@ enum { DP_PARAM_REDUCE = 1 };
 /* For every tensor of `params` (a host array of `count` entries, read during
  * the call only): with DP_PARAM_REDUCE, sum = sum_n c_n * grad_sample[n]
  * with c_n = min(1, C / (norm[n] + 1e-6)) as dp_clip_accumulate (n ascending;
- * N = 0 gives zeros); then, if out is given, out = (sum + sigma*C*z) / denom
+ * N = 0 gives zeros); then, if accum is given, accum += sum (virtual steps:
+ * the paper's section on Opacus' features decouples the physical batch,
+ * bounded by memory, from the logical batch that one noised step covers;
+ * the caller zeroes accum before the first physical batch) and the output
+ * below is formed from accum instead of sum; then, if out is given (the last
+ * physical batch), out = (sum + sigma*C*z) / denom
  * with z the tensor's stream as in dp_add_noise at step
  * step + (*step_dev if step_dev is not NULL, read on the device).  The device
  * step lets one captured graph replay the call at an advancing step (see

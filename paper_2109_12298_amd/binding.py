@@ -73,19 +73,23 @@ SIGNATURES = {
 class DPParam(ctypes.Structure):
     """struct dp_param of dpgrad.h."""
     _fields_ = [("grad_sample", ctypes.c_void_p), ("sum", ctypes.c_void_p), ("out", ctypes.c_void_p),
-                ("numel", ctypes.c_int64), ("param_index", ctypes.c_uint32), ("flags", ctypes.c_uint32)]
+                ("numel", ctypes.c_int64), ("param_index", ctypes.c_uint32), ("flags", ctypes.c_uint32),
+                ("accum", ctypes.c_void_p)]
 
 
 DP_PARAM_REDUCE = 1
 
 
 def make_params(entries):
-    """A dp_param array from (grad_sample, sum, out, numel, param_index) tuples.
+    """A dp_param array from (grad_sample, sum, out, numel, param_index[, accum]) tuples.
 
     grad_sample None means the sum is already formed (no DP_PARAM_REDUCE);
-    an empty tensor (N = 0) still asks for the reduction."""
+    an empty tensor (N = 0) still asks for the reduction.  accum (optional,
+    default None) is the running sum of a virtual step."""
     arr = (DPParam * max(len(entries), 1))()
-    for i, (g, s, o, numel, pidx) in enumerate(entries):
+    for i, ent in enumerate(entries):
+        g, s, o, numel, pidx = ent[:5]
+        arr[i].accum = _ptr(ent[5]) if len(ent) > 5 else None
         arr[i].grad_sample = _ptr(g)
         arr[i].sum = _ptr(s)
         arr[i].out = _ptr(o)

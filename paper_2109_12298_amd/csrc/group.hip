@@ -28,6 +28,7 @@ struct GroupDesc {
     const float *G[kMaxGroup];
     float *S[kMaxGroup];
     float *O[kMaxGroup];
+    float *Acc[kMaxGroup];         // running sum over the physical batches of a logical one, or null
     i64 numel[kMaxGroup];
     i64 ws_off[kMaxGroup];         // first partial of the tensor, in floats
     i64 stride[kMaxGroup];         // floats between two ranges' partials of the tensor
@@ -37,6 +38,17 @@ struct GroupDesc {
     uint32_t flags[kMaxGroup];     // bit 0: column-reduce vectorized, bit 1: finish vectorized
     uint8_t R[kMaxGroup];          // 1: the tensor's sum is formed here from per-sample grads
 };
+
+// with a running sum: acc += s, and s becomes the running sum (what the
+// output is formed from)
+__device__ __forceinline__ void accumulate(float *acc, i64 e0, int cnt, float (&s)[4])
+{
+    if (acc == nullptr) return;
+    for (int i = 0; i < cnt; ++i) {
+        s[i] += acc[e0 + i];
+        acc[e0 + i] = s[i];
+    }
+}
 
 __device__ __forceinline__ int find_param(const int *blk0, int count, int b)
 {
@@ -134,6 +146,7 @@ __global__ __launch_bounds__(kThreads) void finish_many_kernel(GroupDesc d, cons
     if (col && (from_parts || d.N == 0)) {
         for (int i = 0; i < cnt; ++i) d.S[p][e0 + i] = s[i];
     }
+    accumulate(d.Acc[p], e0, cnt, s);
     float *O = d.O[p];
     if (O == nullptr) return;
     float z[4] = {0.f, 0.f, 0.f, 0.f};
@@ -190,6 +203,8 @@ struct FusedArgs {
     int oblk0[kMaxGroup + 1];  // first finish-only workgroup of each tensor
 };
 
+static_assert(sizeof(GroupDesc) + sizeof(FusedArgs) <= 4096, "kernel arguments");
+
 __global__ __launch_bounds__(kThreads) void norms_clip_noise_kernel(GroupDesc d, FusedArgs f)
 {
     __shared__ float cfs[kCfChunk];
@@ -210,6 +225,7 @@ __global__ __launch_bounds__(kThreads) void norms_clip_noise_kernel(GroupDesc d,
         } else {
             for (int i = 0; i < cnt; ++i) s[i] = d.S[p][e0 + i];
         }
+        accumulate(d.Acc[p], e0, cnt, s);
         float *O = d.O[p];
         if (O == nullptr) return;
         float z[4] = {0.f, 0.f, 0.f, 0.f};
@@ -303,6 +319,7 @@ __global__ __launch_bounds__(kThreads) void norms_clip_noise_kernel(GroupDesc d,
     const i64 e0 = vec ? 4 * q : q;
     const int cnt = vec ? 4 : 1;
     for (int i = 0; i < cnt; ++i) d.S[p][e0 + i] = s[i];
+    accumulate(d.Acc[p], e0, cnt, s);
     float *O = d.O[p];
     if (O == nullptr) return;
     float z[4] = {0.f, 0.f, 0.f, 0.f};
@@ -351,6 +368,7 @@ size_t describe(const dp_param *params, int first, int count, i64 N, GroupDesc &
         d.G[i] = q.grad_sample;
         d.S[i] = q.sum;
         d.O[i] = q.out;
+        d.Acc[i] = q.accum;
         d.numel[i] = q.numel;
         d.pidx[i] = q.param_index;
         d.stride[i] = (q.numel + 3) & ~i64(3);

@@ -91,19 +91,28 @@ class DPStep:
 
     def __init__(self, wl: W.Workload, inputs: List[W.LayerInputs], device="cuda", C=None, sigma=None,
                  denom=None, scale=None, clip_mode: str = "auto", seed: Optional[int] = None,
-                 norm_mode: str = "materialize"):
+                 norm_mode: str = "materialize", virtual_batches: int = 1):
         """norm_mode: 'materialize' computes every layer's per-sample gradients
         (the paper's method); 'ghost' gives a Linear layer whose clipped sum is
         fused, and for which 2 T^2 < d_in * d_out, its per-sample norm from
         the T x T Gram matrices instead, and never forms its per-sample
-        gradient (weight and bias sums then both come from the fused GEMM)."""
+        gradient (weight and bias sums then both come from the fused GEMM).
+
+        virtual_batches: K physical batches (of this step's N samples) per
+        logical batch; each physical batch's clipped sums are added into a
+        running sum, and only the last adds noise and divides (by K*N unless
+        denom is given).  Drive it with run(reset=..., emit=...) or
+        run_virtual."""
         torch = _torch()
         self.wl = wl
         self.device = torch.device(device)
         self.N = int(inputs[0].B.shape[0])
         self.C = float(wl.C if C is None else C)
         self.sigma = float(wl.sigma if sigma is None else sigma)
-        self.denom = float(self.N if denom is None else denom)
+        self.virtual_batches = int(virtual_batches)
+        if self.virtual_batches < 1:
+            raise ValueError("virtual_batches must be >= 1")
+        self.denom = float(self.N * self.virtual_batches if denom is None else denom)
         self.scale = float(wl.scale if scale is None else scale)
         self.seed = int(wl.seed if seed is None else seed)
         self.dt = dp.DP_BF16 if wl.dtype == W.BF16 else dp.DP_F32
@@ -179,6 +188,18 @@ class DPStep:
             entries.append((self._grad_for(name), self.S[name], self.out[name], int(np.prod(shape)), pidx))
         self.group = dp.make_params(entries)
         self.group_count = len(entries)
+        # virtual steps: running sums, a group that only accumulates and one
+        # that accumulates and forms the output
+        self.acc: Dict[str, object] = {}
+        if self.virtual_batches > 1:
+            for name, shape in self.params:
+                self.acc[name] = torch.zeros(shape, **f32)
+            ents_acc, ents_emit = [], []
+            for (g, s_, o, numel, pidx), (name, _) in zip(entries, self.params):
+                ents_acc.append((g, s_, None, numel, pidx, self.acc[name]))
+                ents_emit.append((g, s_, o, numel, pidx, self.acc[name]))
+            self.group_acc = dp.make_params(ents_acc)
+            self.group_emit = dp.make_params(ents_emit)
         # the norms are computed inside the clip/noise launch unless a fused
         # clipped sum (which needs them) runs before it
         self.fold_norms = not self.fused_linear and not any(isinstance(lb.layer, W.Embedding)
@@ -283,11 +304,19 @@ class DPStep:
                                             self.N, layer.V, layer.D, self.S[name + ".weight"], self.status,
                                             lb.ws_clip, stream)
 
-    def clip_noise(self, step: int, step_dev=None, stream=None):
-        """Clipped sums, noise and division of every tensor (and the norms, when folded) in one launch."""
-        dp.dp_norms_clip_noise(self.sqnorm if self.fold_norms else None, len(self.layers), self.group,
+    def clip_noise(self, step: int, step_dev=None, stream=None, emit: bool = True):
+        """Clipped sums, noise and division of every tensor (and the norms, when folded) in one launch.
+        With virtual steps the sums go into the running sums, and the output
+        is formed only when emit is set (the logical batch's last physical batch)."""
+        group = self.group if self.virtual_batches == 1 else (self.group_emit if emit else self.group_acc)
+        dp.dp_norms_clip_noise(self.sqnorm if self.fold_norms else None, len(self.layers), group,
                                self.group_count, self.N, self.norm, self.C, self.seed, step, step_dev,
                                self.sigma, self.denom, self.status, self.ws, stream)
+
+    def reset_running_sums(self):
+        """Zero the virtual step's running sums (a fill kernel, capturable)."""
+        for t in self.acc.values():
+            t.zero_()
 
     def call(self, name: str, step: int = 0, stream=None):
         """Enqueue one named call of the step ("grad:<layer>", "norms", "clip:<layer>", "clip+noise")."""
@@ -315,7 +344,8 @@ class DPStep:
 
     # ------------------------------------------------------------------ whole step
     def run(self, step: int = 0, stream=None, mark: Optional[Callable[[str, str], None]] = None, step_dev=None,
-            parallel: bool = False, advance: bool = False, clear_status: bool = True):
+            parallel: bool = False, advance: bool = False, clear_status: bool = True, reset: bool = True,
+            emit: bool = True):
         """Enqueue one whole step; nothing is synchronized here.
 
         parallel: the layers' per-sample-gradient calls (independent of each
@@ -323,10 +353,14 @@ class DPStep:
         joined back into the current stream.  advance: also enqueue
         dp_step_advance on step_dev, in a branch ahead of the noise.
         clear_status: zero the status word first (a captured step leaves it
-        alone, so flags accumulate over replays until the caller clears it)."""
+        alone, so flags accumulate over replays until the caller clears it).
+        reset, emit (virtual steps only): zero the running sums first (the
+        logical batch's first physical batch); form the output (its last)."""
         torch = _torch()
         if clear_status:
             self.status.zero_()
+        if self.virtual_batches > 1 and reset:
+            self.reset_running_sums()
         if not parallel:
             if advance:
                 dp.dp_step_advance(step_dev, 1, stream)
@@ -348,7 +382,7 @@ class DPStep:
                     self.fused_clip_sum(i, stream)
                     if mark: mark("clip:" + lb.layer.name, "end")
             if mark: mark("clip+noise", "start")
-            self.clip_noise(step, step_dev, stream)
+            self.clip_noise(step, step_dev, stream, emit)
             if mark: mark("clip+noise", "end")
             return
         main = torch.cuda.current_stream(self.device)
@@ -377,7 +411,7 @@ class DPStep:
                 self.linear_clip_sums()
         for k in range(len(fused) + (1 if self.fused_linear else 0)):
             main.wait_stream(side[k])
-        self.clip_noise(step, step_dev)
+        self.clip_noise(step, step_dev, emit=emit)
 
     def capture(self, first_step: int = 0, parallel: Optional[bool] = None, steps_per_replay: int = 1):
         """Capture one step as a HIP graph; replay r runs step first_step + r.
@@ -417,15 +451,38 @@ class DPStep:
         torch.cuda.current_stream(self.device).wait_stream(side)
         torch.cuda.synchronize(self.device)
         g = torch.cuda.CUDAGraph()
+        K = self.virtual_batches
         with torch.cuda.graph(g):
             for _ in range(steps_per_replay):
-                self.run(step=0, step_dev=self.step_dev, parallel=parallel, advance=True, clear_status=False)
+                for k in range(K):
+                    # virtual steps: K physical batches (here the resident inputs each time), the
+                    # step counter advanced once per logical step
+                    self.run(step=0, step_dev=self.step_dev, parallel=parallel, advance=(k == 0),
+                             clear_status=False, reset=(k == 0), emit=(k == K - 1))
         torch.cuda.synchronize(self.device)
         self.step_dev.fill_(first_step - 1)    # advanced to first_step by the first replay
         self.graph = g
         self.graph_parallel = parallel
         self.steps_per_replay = steps_per_replay
         return g
+
+    def load_inputs(self, inputs: List[W.LayerInputs]):
+        """Copy another physical batch's inputs (same shapes) into the step's device buffers."""
+        torch = _torch()
+        for lb, li in zip(self.layers, inputs):
+            if li.A is not None:
+                lb.A.copy_(to_device(li.A, self.wl.dtype, self.device))
+            lb.B.copy_(to_device(li.B, self.wl.dtype, self.device))
+            if li.ids is not None:
+                lb.ids.copy_(to_device(li.ids, "", self.device))
+
+    def run_virtual(self, batches: List[List[W.LayerInputs]], step: int = 0):
+        """One logical step over the physical batches `batches` (each with this step's N samples), eagerly."""
+        if len(batches) != self.virtual_batches:
+            raise ValueError("expected %d physical batches" % self.virtual_batches)
+        for k, inputs in enumerate(batches):
+            self.load_inputs(inputs)
+            self.run(step=step, clear_status=(k == 0), reset=(k == 0), emit=(k == len(batches) - 1))
 
     def replay(self):
         self.graph.replay()
@@ -437,7 +494,8 @@ class DPStep:
         res = {"grads": [], "sq_layers": self.sqnorm.cpu().numpy(), "norm": self.norm.cpu().numpy(),
                "S": {k: v.cpu().numpy() for k, v in self.S.items()},
                "out": {k: v.cpu().numpy() for k, v in self.out.items()},
-               "status": int(self.status.cpu().item())}
+               "status": int(self.status.cpu().item()),
+               "acc": {k: v.cpu().numpy() for k, v in self.acc.items()}}
         for lb in self.layers:
             if isinstance(lb.layer, W.Embedding):
                 rp = lb.row_ptr.cpu().numpy()

@@ -85,6 +85,65 @@ def test_workload_step_with_ghost_norms_matches_oracle(name, n, mode):
     compare_step(wl, inputs, got, ref, RTOL[wl.dtype], name + " ghost")
 
 
+def split_batches(inputs, K):
+    """K physical batches of a logical batch's inputs (along the sample axis)."""
+    N = inputs[0].B.shape[0]
+    n = N // K
+    out = []
+    for k in range(K):
+        sl = slice(k * n, (k + 1) * n)
+        out.append([W.LayerInputs(li.layer, A=None if li.A is None else li.A[sl], B=li.B[sl],
+                                  ids=None if li.ids is None else li.ids[sl]) for li in inputs])
+    return out
+
+
+@pytest.mark.parametrize("name,n,mode", [("mnist_cnn", 4, "auto"), ("linear_tiny", 5, "fused"),
+                                         ("text_lstm", 2, "auto"), ("transformer_block", 2, "fused"),
+                                         ("transformer_block", 2, "colreduce")])
+def test_virtual_steps_match_one_logical_step(name, n, mode):
+    """Virtual steps: three physical batches of n samples, their clipped sums
+    added up and noised once, equal the oracle's step over the 3n samples
+    (clipping is per sample, so the grouping into physical batches does not
+    change the result beyond summation order)."""
+    K = 3
+    wl = W.get(name)
+    say(name, "virtual steps", K, "x", n, "mode", mode)
+    inputs = W.make_inputs(wl, n=K * n)
+    batches = split_batches(inputs, K)
+    st = DPStep(wl, batches[0], DEV, clip_mode=mode, virtual_batches=K)
+    st.run_virtual(batches, step=3)
+    got = st.results()
+    ref = oracle.dp_step(wl, inputs, step=3)
+    rtol = RTOL[wl.dtype]
+    for k in ref["S"]:
+        assert_g12(got["acc"][k], ref["S"][k], rtol, "running sum " + k)
+        assert_g12(got["out"][k], ref["out"][k], rtol, "out " + k)
+    assert got["status"] == 0
+    # a second logical step starts again from zero
+    st.run_virtual(batches, step=3)
+    again = st.results()
+    for k in ref["out"]:
+        np.testing.assert_array_equal(again["out"][k], got["out"][k])
+
+
+def test_virtual_steps_in_a_graph_match_eager():
+    """A captured graph of virtual steps (two physical batches per logical
+    step, here the resident inputs twice) replays what eager calls compute."""
+    wl = W.get("mnist_cnn")
+    inputs = W.make_inputs(wl, n=6)
+    say("virtual steps graph")
+    st = DPStep(wl, inputs, DEV, virtual_batches=2)
+    st.capture(first_step=5, parallel=False, steps_per_replay=2)
+    st.replay()
+    got = st.results()
+    eager = DPStep(wl, inputs, DEV, virtual_batches=2)
+    eager.run_virtual([inputs, inputs], step=6)
+    ref = eager.results()
+    for k in ref["out"]:
+        np.testing.assert_array_equal(got["out"][k], ref["out"][k], err_msg=k)
+        np.testing.assert_array_equal(got["acc"][k], ref["acc"][k], err_msg=k)
+
+
 def test_runs_are_bitwise_deterministic():
     wl = W.get("text_lstm")
     inputs = W.make_inputs(wl, n=7)
