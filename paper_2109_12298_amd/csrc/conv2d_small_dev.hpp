@@ -24,8 +24,9 @@ struct SmallShape {
     int nbm, nbn;                 // 16-blocks over kk and co
     int bpw;                      // blocks per wave: 1, 2, 4 or 8
     int gs_off, po_off;           // LDS float offsets of the backprop and the position table
+    int ko_off, bp_off;           // ... of the weight-column offset table and the bias partials
     int vec;                      // float4 stores of gW
-    float inv_hw, inv_w, inv_l, inv_wo;
+    float inv_hw, inv_w, inv_l, inv_wo, inv_khw, inv_kw;
     // stepping a thread's element index by kThreads: the input's (row, column)
     // advance and LDS slot advance, and the backprop's position and slot advance
     int xd_w, xd_h, xd_slot, gd_p, gd_slot;
@@ -89,6 +90,7 @@ __device__ __forceinline__ void conv_small_sample(const T *__restrict__ X, const
     float *Xs = lds;                             // [Cin][Hp][Wp], zero halo
     float *Gs = lds + s.gs_off;                  // [Cout][gst], positions 0 .. L-1 used
     int *Po = reinterpret_cast<int *>(lds + s.po_off);   // [Lp]
+    int *Ko = reinterpret_cast<int *>(lds + s.ko_off);   // [KK]: plane offset of weight column kk
     const T *Xn = X + n * s.Cin * s.H * s.W;
     const T *Gn = GY + n * s.Cout * s.L;
     const int xcount = s.Cin * s.H * s.W, gcount = s.Cout * s.L;
@@ -108,10 +110,14 @@ __device__ __forceinline__ void conv_small_sample(const T *__restrict__ X, const
     }
     const T *xp = Xn + tid;
     const T *gp_ = Gn + tid;
-    for (int e0 = 0; e0 < xcount || e0 < gcount; e0 += kBatch * kThreads) {
+    // rounds of kThreads elements stop at the larger of the two counts (a
+    // wave-uniform test, so unused rounds cost no vector instructions)
+    const int lim = xcount > gcount ? xcount : gcount;
+    for (int e0 = 0; e0 < lim; e0 += kBatch * kThreads) {
         float xv[kBatch], gv[kBatch];
 #pragma unroll
         for (int j = 0; j < kBatch; ++j) {
+            if (e0 + j * kThreads >= lim) break;
             const int e = e0 + j * kThreads + tid;
             xv[j] = e < xcount ? load_elem<T>(xp, e0 + j * kThreads) : 0.0f;
             gv[j] = e < gcount ? load_elem<T>(gp_, e0 + j * kThreads) : 0.0f;
@@ -123,10 +129,17 @@ __device__ __forceinline__ void conv_small_sample(const T *__restrict__ X, const
                 fdivmod(p, s.Wo, s.inv_wo, oh, ow);
                 Po[p] = p < s.L ? oh * s.sh * s.Wp + ow * s.sw : 0;
             }
+            for (int k = tid; k < s.KK; k += kThreads) {
+                int ci, rem, u, v;
+                fdivmod(k, s.khw, s.inv_khw, ci, rem);
+                fdivmod(rem, s.kw, s.inv_kw, u, v);
+                Ko[k] = ci * s.plane + u * s.Wp + v;
+            }
             __syncthreads();   // the cleared halo is in place before the interior lands
         }
 #pragma unroll
         for (int j = 0; j < kBatch; ++j) {
+            if (e0 + j * kThreads >= lim) break;
             const int e = e0 + j * kThreads + tid;
             if (e < xcount) Xs[xslot] = xv[j];
             if (e < gcount) Gs[gslot] = gv[j];
@@ -157,7 +170,7 @@ __device__ __forceinline__ void conv_small_sample(const T *__restrict__ X, const
     // segments are then added in order
     float sq = 0.0f;
     if (gb != nullptr) {
-        float *bpart = reinterpret_cast<float *>(Po + s.Lp);    // [segs][Cout] after the table
+        float *bpart = lds + s.bp_off;    // [segs][Cout]
         const int segs = kThreads / s.Cout;
         const int co = tid % s.Cout, seg = tid / s.Cout;
         if (seg < segs) {
@@ -183,22 +196,29 @@ __device__ __forceinline__ void conv_small_sample(const T *__restrict__ X, const
     const int nblocks = s.nbm * s.nbn;
     const int r16 = lane & 15, kq = lane >> 4;
     float *G = gW + n * s.Cout * s.KK;
-    const int b0 = wave * BPW;
+    const int b0 = __builtin_amdgcn_readfirstlane(wave) * BPW;
+    // the wave's blocks (bm, bn) in order, stepped from the first one
+    int bms[BPW], bns[BPW];
+    {
+        int bm = b0 % s.nbm, bn = b0 / s.nbm;
+#pragma unroll
+        for (int j = 0; j < BPW; ++j) {
+            bms[j] = bm;
+            bns[j] = bn;
+            if (++bm == s.nbm) {
+                bm = 0;
+                ++bn;
+            }
+        }
+    }
     int koff[BPW], goff[BPW];
     f32x4_t acc[BPW];
 #pragma unroll
     for (int j = 0; j < BPW; ++j) {
-        const int blk = b0 + j;
-        const bool live = blk < nblocks;
-        const int bm = live ? blk % s.nbm : 0, bn = live ? blk / s.nbm : 0;
-        const int kk = bm * 16 + r16;
-        koff[j] = 0;
-        if (live && kk < s.KK) {
-            const int ci = kk / s.khw, rem = kk - ci * s.khw;
-            const int u = rem / s.kw, v = rem - u * s.kw;
-            koff[j] = ci * s.plane + u * s.Wp + v;
-        }
-        const int co = bn * 16 + r16;
+        const bool live = b0 + j < nblocks;
+        const int kk = bms[j] * 16 + r16;
+        koff[j] = Ko[live && kk < s.KK ? kk : 0];
+        const int co = bns[j] * 16 + r16;
         goff[j] = (live && co < s.Cout ? co : 0) * s.gst + kq;
         acc[j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
     }
@@ -211,9 +231,8 @@ __device__ __forceinline__ void conv_small_sample(const T *__restrict__ X, const
     if (Lfull < s.L) contract_step<BPW, U, true>(Xs, Gs, Po, koff, goff, Lfull, kq, s.L, acc);
 #pragma unroll
     for (int j = 0; j < BPW; ++j) {
-        const int blk = b0 + j;
-        if (blk >= nblocks) continue;
-        const int bm = blk % s.nbm, bn = blk / s.nbm;
+        if (b0 + j >= nblocks) continue;
+        const int bm = bms[j], bn = bns[j];
         const int co = bn * 16 + r16;
         // lane holds kk = bm*16 + 4*kq + r (r = 0..3) of column co
         const int kk0 = bm * 16 + 4 * kq;
@@ -248,8 +267,8 @@ __device__ __forceinline__ void conv_small_sample(const T *__restrict__ X, const
 // floats of dynamic LDS a workgroup needs
 inline long lds_floats(const SmallShape &s)
 {
-    // the bias partials [segs][Cout] follow the position table
-    return (long)s.po_off + s.Lp + kThreads;
+    // the bias partials [segs][Cout] follow the weight-column table
+    return (long)s.bp_off + kThreads;
 }
 
 // the shape's derived sizes; false if the sample does not fit
@@ -272,10 +291,14 @@ inline bool make_small(const ConvSmallArgs &a, SmallShape &s)
     s.gs_off = s.Cin * s.plane;
     s.gst = s.Lp + 4;
     s.po_off = s.gs_off + s.Cout * s.gst;
+    s.ko_off = s.po_off + s.Lp;
+    s.bp_off = s.ko_off + s.KK;
     s.inv_hw = 1.0f / (float)(s.H * s.W);
     s.inv_w = 1.0f / (float)s.W;
     s.inv_l = 1.0f / (float)s.L;
     s.inv_wo = 1.0f / (float)s.Wo;
+    s.inv_khw = 1.0f / (float)s.khw;
+    s.inv_kw = 1.0f / (float)s.kw;
     {
         const int rows = kThreads / s.W;
         s.xd_w = kThreads % s.W;
