@@ -26,7 +26,6 @@ enum { kConvSmall = 0, kOuter = 1 };
 
 struct ManyItem {
     int kind;
-    int blk0;                        // first block of the layer in the launch
     int bpw;                         // conv: accumulator blocks per wave
     int vec;                         // outer: float4 path
     int rows, bps;                   // outer: gW rows per block, blocks per sample
@@ -39,6 +38,7 @@ struct ManyItem {
 
 struct ManyDesc {
     int count;
+    int blk0[kManyMax + 1];          // first block of each layer in the launch (one scalar load)
     ManyItem it[kManyMax];
 };
 
@@ -48,9 +48,9 @@ __global__ __launch_bounds__(kThreads) void grad_many_kernel(const ManyDesc d)
     extern __shared__ float lds[];
     const int b = (int)blockIdx.x;
     int p = 0;
-    while (p + 1 < d.count && d.it[p + 1].blk0 <= b) ++p;
+    while (p + 1 < d.count && d.blk0[p + 1] <= b) ++p;
     const ManyItem &it = d.it[p];
-    const int local = b - it.blk0;
+    const int local = b - d.blk0[p];
     const T *A = (const T *)it.A;
     const T *B = (const T *)it.B;
     if (it.kind == kConvSmall) {
@@ -155,13 +155,14 @@ void launch_group(const dp_layer_grad *const *layers, int count, dp_dtype dt, i6
     for (int k = 0; k < count; ++k) {
         ManyItem &it = d.it[k];
         fill_item(*layers[k], dt, N, it);
-        it.blk0 = (int)blocks;
+        d.blk0[k] = (int)blocks;
         blocks += it.kind == kConvSmall ? N : N * it.bps;
         if (it.kind == kConvSmall) {
             const size_t need = (size_t)csmall::lds_floats(it.cs) * sizeof(float);
             lds = need > lds ? need : lds;
         }
     }
+    for (int k = count; k <= kManyMax; ++k) d.blk0[k] = (int)blocks;
     for (int k = count; k < kManyMax; ++k) d.it[k] = d.it[0];
     if (dt == DP_BF16)
         grad_many_kernel<uint16_t><<<(unsigned)blocks, kThreads, lds, stream>>>(d);

@@ -344,14 +344,15 @@ class DPStep:
 
     # ------------------------------------------------------------------ whole step
     def run(self, step: int = 0, stream=None, mark: Optional[Callable[[str, str], None]] = None, step_dev=None,
-            parallel: bool = False, advance: bool = False, clear_status: bool = True, reset: bool = True,
+            parallel: bool = False, advance: int = 0, clear_status: bool = True, reset: bool = True,
             emit: bool = True):
         """Enqueue one whole step; nothing is synchronized here.
 
         parallel: the layers' per-sample-gradient calls (independent of each
         other) and the fused clipped sums run on side streams forked from and
-        joined back into the current stream.  advance: also enqueue
-        dp_step_advance on step_dev, in a branch ahead of the noise.
+        joined back into the current stream.  advance: if nonzero, also
+        enqueue dp_step_advance(step_dev, advance), in a branch ahead of the
+        noise.
         clear_status: zero the status word first (a captured step leaves it
         alone, so flags accumulate over replays until the caller clears it).
         reset, emit (virtual steps only): zero the running sums first (the
@@ -363,7 +364,7 @@ class DPStep:
             self.reset_running_sums()
         if not parallel:
             if advance:
-                dp.dp_step_advance(step_dev, 1, stream)
+                dp.dp_step_advance(step_dev, advance, stream)
             for name in self.grad_calls():
                 if mark: mark(name, "start")
                 self.call(name, step, stream)
@@ -394,7 +395,7 @@ class DPStep:
         if advance:
             side[-1].wait_stream(main)
             with torch.cuda.stream(side[-1]):
-                dp.dp_step_advance(step_dev, 1)
+                dp.dp_step_advance(step_dev, advance)
         for s_ in side:
             main.wait_stream(s_)
         if not self.fold_norms:
@@ -414,10 +415,13 @@ class DPStep:
         self.clip_noise(step, step_dev, emit=emit)
 
     def capture(self, first_step: int = 0, parallel: Optional[bool] = None, steps_per_replay: int = 1):
-        """Capture one step as a HIP graph; replay r runs step first_step + r.
+        """Capture steps as a HIP graph; replay j runs steps first_step + j*r
+        .. first_step + j*r + r - 1 (r = steps_per_replay).
 
-        The graph advances its own device step counter (in a branch that runs
-        before the noise), so nothing is re-recorded between replays.
+        The graph advances its own device step counter by r at the start of
+        each replay (in a branch that runs before the noise); step k of the
+        replay uses step_dev + k.  Nothing is re-recorded between replays,
+        and step_dev holds the first step of the last replay.
         parallel: the layers' calls as parallel branches of the graph (True),
         or one chain (False); None captures both, times a few replays of
         each and keeps the faster (branches pay off when the layers' kernels
@@ -453,14 +457,15 @@ class DPStep:
         g = torch.cuda.CUDAGraph()
         K = self.virtual_batches
         with torch.cuda.graph(g):
-            for _ in range(steps_per_replay):
+            for i in range(steps_per_replay):
                 for k in range(K):
-                    # virtual steps: K physical batches (here the resident inputs each time), the
-                    # step counter advanced once per logical step
-                    self.run(step=0, step_dev=self.step_dev, parallel=parallel, advance=(k == 0),
+                    # virtual steps: K physical batches (here the resident inputs each time) of
+                    # logical step i; the counter moves once per replay
+                    self.run(step=i, step_dev=self.step_dev, parallel=parallel,
+                             advance=steps_per_replay if (i == 0 and k == 0) else 0,
                              clear_status=False, reset=(k == 0), emit=(k == K - 1))
         torch.cuda.synchronize(self.device)
-        self.step_dev.fill_(first_step - 1)    # advanced to first_step by the first replay
+        self.step_dev.fill_(first_step - steps_per_replay)    # advanced to first_step by the first replay
         self.graph = g
         self.graph_parallel = parallel
         self.steps_per_replay = steps_per_replay
