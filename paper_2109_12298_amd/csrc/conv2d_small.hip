@@ -64,6 +64,7 @@ void conv_small_launch(const ConvSmallArgs &a, bool bf16, float scale, float *gW
     SmallShape s;
     make_small(a, s);
     s.vec = s.KK % 4 == 0 && aligned(gW, 16);
+    s.dma = s.dma_layout && !bf16 && aligned(a.X, 16) && aligned(a.GY, 16);
     const size_t lds = (size_t)lds_floats(s) * sizeof(float);
     switch (s.bpw) {
     case 1: launch_small<1>(a, s, bf16, scale, gW, gb, sqnorm, lds, stream); break;

@@ -3,6 +3,9 @@
 // and the grouped per-sample-gradient kernel) and its host-side planning.
 #pragma once
 
+#include <type_traits>
+
+#include "bf16_stage.hpp"
 #include "common.hpp"
 #include "conv2d_small.hpp"
 
@@ -19,13 +22,14 @@ constexpr int kBatch = 16;                // global loads in flight per thread p
 struct SmallShape {
     int Cin, H, W, Cout, Ho, Wo, kh, kw, sh, sw, ph, pw;
     int Hp, Wp, plane, L, Lp, KK, khw;
-    int gst;                      // row stride of the staged backprop: 4 x odd, so the 16 rows
-                                  // x 4 positions a wave reads at once fall in 64 different banks
+    int gst;                      // row stride of the staged backprop (see make_small)
     int nbm, nbn;                 // 16-blocks over kk and co
     int bpw;                      // blocks per wave: 1, 2, 4 or 8
     int gs_off, po_off;           // LDS float offsets of the backprop and the position table
     int ko_off, bp_off;           // ... of the weight-column offset table and the bias partials
     int vec;                      // float4 stores of gW
+    int dma_layout;               // no padding: planes and backprop rows kept as they lie in memory
+    int dma;                      // stage them by direct-to-LDS copies (fp32, 16-byte aligned)
     float inv_hw, inv_w, inv_l, inv_wo, inv_khw, inv_kw;
     // stepping a thread's element index by kThreads: the input's (row, column)
     // advance and LDS slot advance, and the backprop's position and slot advance
@@ -110,9 +114,44 @@ __device__ __forceinline__ void conv_small_sample(const T *__restrict__ X, const
     }
     const T *xp = Xn + tid;
     const T *gp_ = Gn + tid;
+    bool staged = false;
+    if constexpr (std::is_same<T, float>::value) {
+        if (s.dma) {
+            // Unpadded fp32 sample: both tensors are copied into LDS as they
+            // lie in memory by global_load_lds_dwordx4 (1 KB per wave
+            // instruction, no VGPR round trip, no per-element index work).
+            // Lanes past a tensor's end re-read its first chunk into the
+            // slack that follows it in LDS.
+            const int nx = xcount / 4, ng = gcount / 4;
+            const int ix = (nx + 63) / 64, ig = (ng + 63) / 64;
+            const uint32_t lx = bf16s::lds_addr(Xs), lg = bf16s::lds_addr(Gs);
+            for (int i = wave; i < ix + ig; i += kWaves) {
+                if (i < ix) {
+                    const int c = i * 64 + lane;
+                    bf16s::dma16(Xn + 4 * (c < nx ? c : 0), lx + (uint32_t)i * 1024u);
+                } else {
+                    const int c = (i - ix) * 64 + lane;
+                    bf16s::dma16(Gn + 4 * (c < ng ? c : 0), lg + (uint32_t)(i - ix) * 1024u);
+                }
+            }
+            for (int p = tid; p < s.Lp; p += kThreads) {
+                int oh, ow;
+                fdivmod(p, s.Wo, s.inv_wo, oh, ow);
+                Po[p] = p < s.L ? oh * s.sh * s.Wp + ow * s.sw : 0;
+            }
+            for (int k = tid; k < s.KK; k += kThreads) {
+                int ci, rem, u, v;
+                fdivmod(k, s.khw, s.inv_khw, ci, rem);
+                fdivmod(rem, s.kw, s.inv_kw, u, v);
+                Ko[k] = ci * s.plane + u * s.Wp + v;
+            }
+            bf16s::wait_vmcnt<0>();
+            staged = true;
+        }
+    }
     // rounds of kThreads elements stop at the larger of the two counts (a
     // wave-uniform test, so unused rounds cost no vector instructions)
-    const int lim = xcount > gcount ? xcount : gcount;
+    const int lim = staged ? 0 : (xcount > gcount ? xcount : gcount);
     for (int e0 = 0; e0 < lim; e0 += kBatch * kThreads) {
         float xv[kBatch], gv[kBatch];
 #pragma unroll
@@ -288,9 +327,23 @@ inline bool make_small(const ConvSmallArgs &a, SmallShape &s)
     s.nbn = (s.Cout + 15) / 16;
     s.bpw = 1;
     while (s.bpw * kWaves < s.nbm * s.nbn) s.bpw *= 2;
-    s.gs_off = s.Cin * s.plane;
-    s.gst = s.Lp + 4;
-    s.po_off = s.gs_off + s.Cout * s.gst;
+    // Unpadded shapes keep the tensors' own layouts (backprop rows of L
+    // positions), each region followed by slack for the direct copies' last
+    // wave instruction (whole 1 KB blocks) and the masked final step's reads
+    // past the last row.  Otherwise a backprop row is padded to 4 x odd
+    // floats, so the 16 rows x 4 positions a wave reads at once fall in 64
+    // different banks.
+    s.dma_layout = s.ph == 0 && s.pw == 0 && (s.Cin * s.H * s.W) % 4 == 0 && (s.Cout * s.L) % 4 == 0;
+    s.dma = 0;
+    if (s.dma_layout) {
+        s.gs_off = (s.Cin * s.plane + 255) & ~255;
+        s.gst = s.L;
+        s.po_off = s.gs_off + ((s.Cout * s.L + 32 + 255) & ~255);
+    } else {
+        s.gs_off = s.Cin * s.plane;
+        s.gst = s.Lp + 4;
+        s.po_off = s.gs_off + s.Cout * s.gst;
+    }
     s.ko_off = s.po_off + s.Lp;
     s.bp_off = s.ko_off + s.KK;
     s.inv_hw = 1.0f / (float)(s.H * s.W);

@@ -134,6 +134,7 @@ void fill_item(const dp_layer_grad &L, dp_dtype dt, i64 N, ManyItem &it)
         it.kind = kConvSmall;
         csmall::make_small(conv_args(L, N), it.cs);
         it.cs.vec = it.cs.KK % 4 == 0 && aligned(L.gW, 16);
+        it.cs.dma = it.cs.dma_layout && dt == DP_F32 && aligned(L.A, 16) && aligned(L.B, 16);
         it.bpw = it.cs.bpw;
     } else {
         it.kind = kOuter;

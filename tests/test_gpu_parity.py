@@ -260,7 +260,9 @@ CONV_SHAPES = [  # N, Cin, H, W, Cout, kh, kw, sh, sw, ph, pw
     (1, 2, 130, 130, 4, 3, 3, 1, 1, 1, 1),     # input planes too large for LDS: gathered fallback
     (2, 32, 32, 32, 64, 3, 3, 1, 1, 1, 1), (2, 64, 16, 16, 64, 3, 3, 1, 1, 1, 1),
     (2, 64, 16, 16, 128, 3, 3, 1, 1, 1, 1), (2, 128, 8, 8, 128, 3, 3, 1, 1, 1, 1),
-    (2, 128, 8, 8, 256, 3, 3, 1, 1, 1, 1)]
+    (2, 128, 8, 8, 256, 3, 3, 1, 1, 1, 1),
+    (3, 4, 8, 8, 20, 3, 3, 1, 1, 0, 0),        # unpadded, sizes multiples of 4: direct-to-LDS staging
+    (2, 12, 9, 10, 24, 3, 2, 2, 2, 0, 0)]      # the same with stride 2
 
 
 # One shape per tile configuration of the fast path and staging mode (whole
