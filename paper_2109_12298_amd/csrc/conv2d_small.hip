@@ -34,7 +34,7 @@ __global__ __launch_bounds__(kThreads) void conv_small_kernel(const T *__restric
                                                               SmallShape s, float scale, float *__restrict__ gW,
                                                               float *__restrict__ gb, float *__restrict__ sqnorm)
 {
-    extern __shared__ float lds[];
+    extern __shared__ __attribute__((aligned(16))) float lds[];
     conv_small_sample<T, BPW>(X, GY, s, scale, gW, gb, sqnorm, blockIdx.x, lds);
 }
 
@@ -64,7 +64,8 @@ void conv_small_launch(const ConvSmallArgs &a, bool bf16, float scale, float *gW
     SmallShape s;
     make_small(a, s);
     s.vec = s.KK % 4 == 0 && aligned(gW, 16);
-    s.dma = s.dma_layout && !bf16 && aligned(a.X, 16) && aligned(a.GY, 16);
+    s.xdma = s.xplain && !bf16 && aligned(a.X, 16);
+    s.gdma = s.gplain && !bf16 && aligned(a.GY, 16);
     const size_t lds = (size_t)lds_floats(s) * sizeof(float);
     switch (s.bpw) {
     case 1: launch_small<1>(a, s, bf16, scale, gW, gb, sqnorm, lds, stream); break;

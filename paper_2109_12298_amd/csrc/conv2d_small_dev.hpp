@@ -28,8 +28,8 @@ struct SmallShape {
     int gs_off, po_off;           // LDS float offsets of the backprop and the position table
     int ko_off, bp_off;           // ... of the weight-column offset table and the bias partials
     int vec;                      // float4 stores of gW
-    int dma_layout;               // no padding: planes and backprop rows kept as they lie in memory
-    int dma;                      // stage them by direct-to-LDS copies (fp32, 16-byte aligned)
+    int xplain, gplain;           // input planes (unpadded) / backprop rows kept as they lie in memory
+    int xdma, gdma;               // ... and staged by direct-to-LDS copies (fp32, 16-byte aligned)
     float inv_hw, inv_w, inv_l, inv_wo, inv_khw, inv_kw;
     // stepping a thread's element index by kThreads: the input's (row, column)
     // advance and LDS slot advance, and the backprop's position and slot advance
@@ -83,7 +83,7 @@ __device__ __forceinline__ void contract_step(const float *Xs, const float *Gs, 
 }
 
 // Sample n's gradients by one workgroup of kThreads threads; `lds` holds
-// lds_floats(s) floats of dynamic LDS.
+// lds_floats(s) floats of dynamic LDS, 16-byte aligned.
 template <typename T, int BPW>
 __device__ __forceinline__ void conv_small_sample(const T *__restrict__ X, const T *__restrict__ GY, const SmallShape &s,
                                                   float scale, float *__restrict__ gW, float *__restrict__ gb,
@@ -114,55 +114,48 @@ __device__ __forceinline__ void conv_small_sample(const T *__restrict__ X, const
     }
     const T *xp = Xn + tid;
     const T *gp_ = Gn + tid;
-    bool staged = false;
+    // A tensor kept in its own layout (fp32, 16-byte aligned, a multiple of
+    // four elements; the input also unpadded) is copied into LDS by
+    // global_load_lds_dwordx4: 1 KB per wave instruction, no VGPR round trip,
+    // no per-element index work.  Lanes past its end re-read its first chunk
+    // into the slack that follows it in LDS.  The other tensor goes through
+    // registers below.
+    bool xdma = false, gdma = false;
     if constexpr (std::is_same<T, float>::value) {
-        if (s.dma) {
-            // Unpadded fp32 sample: both tensors are copied into LDS as they
-            // lie in memory by global_load_lds_dwordx4 (1 KB per wave
-            // instruction, no VGPR round trip, no per-element index work).
-            // Lanes past a tensor's end re-read its first chunk into the
-            // slack that follows it in LDS.
-            const int nx = xcount / 4, ng = gcount / 4;
-            const int ix = (nx + 63) / 64, ig = (ng + 63) / 64;
-            const uint32_t lx = bf16s::lds_addr(Xs), lg = bf16s::lds_addr(Gs);
-            for (int i = wave; i < ix + ig; i += kWaves) {
-                if (i < ix) {
-                    const int c = i * 64 + lane;
-                    bf16s::dma16(Xn + 4 * (c < nx ? c : 0), lx + (uint32_t)i * 1024u);
-                } else {
-                    const int c = (i - ix) * 64 + lane;
-                    bf16s::dma16(Gn + 4 * (c < ng ? c : 0), lg + (uint32_t)(i - ix) * 1024u);
-                }
+        xdma = s.xdma != 0;
+        gdma = s.gdma != 0;
+        const int nx = xdma ? xcount / 4 : 0, ng = gdma ? gcount / 4 : 0;
+        const int ix = (nx + 63) / 64, ig = (ng + 63) / 64;
+        const uint32_t lx = bf16s::lds_addr(Xs), lg = bf16s::lds_addr(Gs);
+        for (int i = wave; i < ix + ig; i += kWaves) {
+            if (i < ix) {
+                const int c = i * 64 + lane;
+                bf16s::dma16(Xn + 4 * (c < nx ? c : 0), lx + (uint32_t)i * 1024u);
+            } else {
+                const int c = (i - ix) * 64 + lane;
+                bf16s::dma16(Gn + 4 * (c < ng ? c : 0), lg + (uint32_t)(i - ix) * 1024u);
             }
-            for (int p = tid; p < s.Lp; p += kThreads) {
-                int oh, ow;
-                fdivmod(p, s.Wo, s.inv_wo, oh, ow);
-                Po[p] = p < s.L ? oh * s.sh * s.Wp + ow * s.sw : 0;
-            }
-            for (int k = tid; k < s.KK; k += kThreads) {
-                int ci, rem, u, v;
-                fdivmod(k, s.khw, s.inv_khw, ci, rem);
-                fdivmod(rem, s.kw, s.inv_kw, u, v);
-                Ko[k] = ci * s.plane + u * s.Wp + v;
-            }
-            bf16s::wait_vmcnt<0>();
-            staged = true;
         }
     }
-    // rounds of kThreads elements stop at the larger of the two counts (a
-    // wave-uniform test, so unused rounds cost no vector instructions)
-    const int lim = staged ? 0 : (xcount > gcount ? xcount : gcount);
-    for (int e0 = 0; e0 < lim; e0 += kBatch * kThreads) {
+    // The register path: rounds of kThreads elements, up to the larger of
+    // the two counts it handles (a wave-uniform test, so unused rounds cost
+    // no vector instructions).  The halo is cleared and the position and
+    // weight-column tables are built while the first round's loads (and the
+    // copies above) are in flight.
+    const int xreg = xdma ? 0 : xcount, greg = gdma ? 0 : gcount;
+    const int lim = xreg > greg ? xreg : greg;
+    for (int e0 = 0; e0 == 0 || e0 < lim; e0 += kBatch * kThreads) {
         float xv[kBatch], gv[kBatch];
 #pragma unroll
         for (int j = 0; j < kBatch; ++j) {
             if (e0 + j * kThreads >= lim) break;
             const int e = e0 + j * kThreads + tid;
-            xv[j] = e < xcount ? load_elem<T>(xp, e0 + j * kThreads) : 0.0f;
-            gv[j] = e < gcount ? load_elem<T>(gp_, e0 + j * kThreads) : 0.0f;
+            xv[j] = e < xreg ? load_elem<T>(xp, e0 + j * kThreads) : 0.0f;
+            gv[j] = e < greg ? load_elem<T>(gp_, e0 + j * kThreads) : 0.0f;
         }
         if (e0 == 0) {
-            for (int i = tid; i < s.Cin * s.plane; i += kThreads) Xs[i] = 0.0f;
+            if (!xdma)
+                for (int i = tid; i < s.Cin * s.plane; i += kThreads) Xs[i] = 0.0f;
             for (int p = tid; p < s.Lp; p += kThreads) {
                 int oh, ow;
                 fdivmod(p, s.Wo, s.inv_wo, oh, ow);
@@ -180,8 +173,8 @@ __device__ __forceinline__ void conv_small_sample(const T *__restrict__ X, const
         for (int j = 0; j < kBatch; ++j) {
             if (e0 + j * kThreads >= lim) break;
             const int e = e0 + j * kThreads + tid;
-            if (e < xcount) Xs[xslot] = xv[j];
-            if (e < gcount) Gs[gslot] = gv[j];
+            if (e < xreg) Xs[xslot] = xv[j];
+            if (e < greg) Gs[gslot] = gv[j];
             // element e + kThreads: column carry into the row, row carry into the plane
             xw += s.xd_w;
             xslot += s.xd_slot;
@@ -203,6 +196,7 @@ __device__ __forceinline__ void conv_small_sample(const T *__restrict__ X, const
             }
         }
     }
+    if (xdma || gdma) bf16s::wait_vmcnt<0>();
     __syncthreads();
 
     // ---- bias: thread (seg, co) adds positions seg, seg + segs, ...; the
@@ -327,20 +321,25 @@ inline bool make_small(const ConvSmallArgs &a, SmallShape &s)
     s.nbn = (s.Cout + 15) / 16;
     s.bpw = 1;
     while (s.bpw * kWaves < s.nbm * s.nbn) s.bpw *= 2;
-    // Unpadded shapes keep the tensors' own layouts (backprop rows of L
-    // positions), each region followed by slack for the direct copies' last
-    // wave instruction (whole 1 KB blocks) and the masked final step's reads
-    // past the last row.  Otherwise a backprop row is padded to 4 x odd
-    // floats, so the 16 rows x 4 positions a wave reads at once fall in 64
-    // different banks.
-    s.dma_layout = s.ph == 0 && s.pw == 0 && (s.Cin * s.H * s.W) % 4 == 0 && (s.Cout * s.L) % 4 == 0;
-    s.dma = 0;
-    if (s.dma_layout) {
-        s.gs_off = (s.Cin * s.plane + 255) & ~255;
+    // A tensor whose element count is a multiple of four (and, for the
+    // input, without padding) keeps its own layout in LDS (backprop rows of
+    // L positions), followed by slack for the direct copies' last wave
+    // instruction (whole 1 KB blocks) and, for the backprop, for the masked
+    // final step's reads past the last row.  Otherwise a backprop row is
+    // padded to 4 x odd floats, so that the 16 rows x 4 positions a wave reads
+    // at once fall in 64 different banks (L = 4 x odd, like the MNIST conv1's
+    // 196, has that property unpadded).
+    s.xplain = s.ph == 0 && s.pw == 0 && (s.Cin * s.H * s.W) % 4 == 0;
+    s.gplain = (s.Cout * s.L) % 4 == 0;
+    s.xdma = s.gdma = 0;
+    // (direct copies write 16-byte-aligned LDS, so a region they fill starts
+    // on a 256-byte boundary)
+    s.gs_off = (s.xplain || s.gplain) ? (s.Cin * s.plane + 63) & ~63 : s.Cin * s.plane;
+    if (s.xplain) s.gs_off = (s.Cin * s.plane + 255) & ~255;
+    if (s.gplain) {
         s.gst = s.L;
         s.po_off = s.gs_off + ((s.Cout * s.L + 32 + 255) & ~255);
     } else {
-        s.gs_off = s.Cin * s.plane;
         s.gst = s.Lp + 4;
         s.po_off = s.gs_off + s.Cout * s.gst;
     }

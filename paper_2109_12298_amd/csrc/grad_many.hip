@@ -45,7 +45,7 @@ struct ManyDesc {
 template <typename T>
 __global__ __launch_bounds__(kThreads) void grad_many_kernel(const ManyDesc d)
 {
-    extern __shared__ float lds[];
+    extern __shared__ __attribute__((aligned(16))) float lds[];
     const int b = (int)blockIdx.x;
     int p = 0;
     while (p + 1 < d.count && d.blk0[p + 1] <= b) ++p;
@@ -134,7 +134,8 @@ void fill_item(const dp_layer_grad &L, dp_dtype dt, i64 N, ManyItem &it)
         it.kind = kConvSmall;
         csmall::make_small(conv_args(L, N), it.cs);
         it.cs.vec = it.cs.KK % 4 == 0 && aligned(L.gW, 16);
-        it.cs.dma = it.cs.dma_layout && dt == DP_F32 && aligned(L.A, 16) && aligned(L.B, 16);
+        it.cs.xdma = it.cs.xplain && dt == DP_F32 && aligned(L.A, 16);
+        it.cs.gdma = it.cs.gplain && dt == DP_F32 && aligned(L.B, 16);
         it.bpw = it.cs.bpw;
     } else {
         it.kind = kOuter;
