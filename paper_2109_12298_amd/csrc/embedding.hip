@@ -12,7 +12,8 @@
 //   into row_ptr.
 // Pass 3 (one wave per sample and segment slot, so the grid fills the chip
 //   even for a small batch): the wave sums the segment's backprop rows in
-//   ascending t, eight positions' loads in flight at a time, lanes over the
+//   ascending t, eight positions' loads in flight at a time (32 for segments
+//   longer than eight, such as a hot id's), lanes over the
 //   columns (four per lane when the rows allow 16- or 8-byte loads), and
 //   writes the CSR row and its squared norm; the sample's norm is then added
 //   over its slots in slot order.  No atomics on data.
@@ -170,7 +171,29 @@ __device__ __forceinline__ void load_vec(const T *p, float (&v)[VEC])
     }
 }
 
-constexpr int kBatch = 8;   // positions whose loads are in flight together
+constexpr int kBatch = 8;       // positions whose loads are in flight together
+constexpr int kDeepBatch = 32;  // ... for segments longer than kBatch (hot ids)
+
+// acc += the rows perm[r0 .. r1-1] of Bn at column cc, in ascending r,
+// BATCH rows' loads in flight at a time
+template <typename T, int VEC, int BATCH>
+__device__ __forceinline__ void sum_rows(const T *Bn, const int32_t *perm, int r0, int r1, i64 D, i64 cc,
+                                         float (&acc)[VEC])
+{
+    for (int r = r0; r < r1; r += BATCH) {
+        float v[BATCH][VEC];
+#pragma unroll
+        for (int j = 0; j < BATCH; ++j) {
+            const int rj = r + j < r1 ? r + j : r1 - 1;
+            load_vec<T, VEC>(Bn + (i64)perm[rj] * D + cc, v[j]);
+        }
+#pragma unroll
+        for (int j = 0; j < BATCH; ++j)
+            if (r + j < r1)
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) acc[i] += v[j][i];
+    }
+}
 
 template <typename T, int VEC>
 __global__ __launch_bounds__(64) void emb_rows_kernel(
@@ -192,6 +215,7 @@ __global__ __launch_bounds__(64) void emb_rows_kernel(
     const int32_t *seg = w.segstart + n * (Tn + 1);
     const int r0 = seg[s], r1 = seg[s + 1];
     if (keep && lane == 0) uniq[k] = w.segid[n * Tn + s];
+
     const T *Bn = B + n * Tn * D;
     float sq = 0.0f;
     for (i64 c0 = 0; c0 < D; c0 += 64 * VEC) {
@@ -201,19 +225,8 @@ __global__ __launch_bounds__(64) void emb_rows_kernel(
         float acc[VEC];
 #pragma unroll
         for (int i = 0; i < VEC; ++i) acc[i] = 0.0f;
-        for (int r = r0; r < r1; r += kBatch) {
-            float v[kBatch][VEC];
-#pragma unroll
-            for (int j = 0; j < kBatch; ++j) {
-                const int rj = r + j < r1 ? r + j : r1 - 1;
-                load_vec<T, VEC>(Bn + (i64)perm[rj] * D + cc, v[j]);
-            }
-#pragma unroll
-            for (int j = 0; j < kBatch; ++j)
-                if (r + j < r1)
-#pragma unroll
-                    for (int i = 0; i < VEC; ++i) acc[i] += v[j][i];
-        }
+        if (r1 - r0 > kBatch) sum_rows<T, VEC, kDeepBatch>(Bn, perm, r0, r1, D, cc, acc);
+        else sum_rows<T, VEC, kBatch>(Bn, perm, r0, r1, D, cc, acc);
         if (on) {
             float g[VEC];
 #pragma unroll
