@@ -100,11 +100,12 @@ def call_costs(st):
             ho, wo = L.out_hw
             kk = L.c_in * L.k[0] * L.k[1]
             grads = N * L.n_params * 4
-            item = dp.make_layer_grads([st._grad_item(st.layers.index(lb))])
-            small = dp.dp_grad_sample_many_grouped(item, 0, st.dt, N)
+            choice = dp.dp_conv2d_kernel_choice(N, L.c_in, L.h, L.w, L.c_out, L.k[0], L.k[1], L.stride[0],
+                                                L.stride[1], L.pad[0], L.pad[1])
+            kname = {dp.DP_CONV_KERNEL_SMALL: "conv_small_kernel",
+                     dp.DP_CONV_KERNEL_ROWS: "conv_rows_kernel"}.get(choice, "conv_per_sample_kernel")
             out["grad:" + L.name] = (N * (L.c_in * L.h * L.w + L.c_out * ho * wo) * e + grads + N * 4,
-                                     2 * N * L.c_out * kk * ho * wo,
-                                     "conv_small_kernel" if small else "conv_per_sample_kernel", "f32")
+                                     2 * N * L.c_out * kk * ho * wo, kname, "f32")
             col_bytes += grads
         elif isinstance(L, W.Embedding):
             nnz_bound = N * L.T
@@ -146,6 +147,7 @@ def src_hash(paths):
 KERNEL_SOURCES = {
     "outer_kernel": ["paper_2109_12298_amd/csrc/linear.hip", "paper_2109_12298_amd/csrc/linear_outer.hpp"],
     "ghost_norm_kernel": ["paper_2109_12298_amd/csrc/ghost.hip"],
+    "conv_rows_kernel": ["paper_2109_12298_amd/csrc/conv2d_rows.hip"],
     "conv_small_kernel": ["paper_2109_12298_amd/csrc/conv2d_small.hip",
                           "paper_2109_12298_amd/csrc/conv2d_small_dev.hpp"],
     "grad_many_kernel": ["paper_2109_12298_amd/csrc/grad_many.hip", "paper_2109_12298_amd/csrc/conv2d_small_dev.hpp",

@@ -126,12 +126,24 @@ dp_status dp_grad_sample_conv2d(const void *X, const void *GY, dp_dtype dt, int6
  * default): a sample whose padded input planes and backprop fit one
  * workgroup's LDS (48 KB), with Cout <= 256 and a weight gradient of at most
  * 32 blocks of 16 (Cin*kh*kw) x 16 (Cout), runs one workgroup per sample;
- * other shapes run the tiled kernel.  DP_CONV_TILED: always the tiled kernel.  Both give the same
- * results to rounding.  Returns the previous choice, or -1 (choice unchanged)
+ * other shapes with at least 97 weight columns (Cin*kh*kw) run by output
+ * row chunks (a workgroup per sample and tile of up to 288 weight columns x
+ * 64 channels) when one output row's inputs fit its LDS, else the tiled
+ * kernel.  DP_CONV_ROWS: the row-chunked kernel
+ * wherever it applies, else the tiled one.  DP_CONV_TILED: always the tiled
+ * kernel.  All give the same results to rounding.  Returns the previous choice, or -1 (choice unchanged)
  * for an unknown value.  Not synchronized with calls in flight on other host
  * threads: set it before enqueueing. */
-enum { DP_CONV_AUTO = 0, DP_CONV_TILED = 1 };
+enum { DP_CONV_AUTO = 0, DP_CONV_TILED = 1, DP_CONV_ROWS = 2 };
 int dp_conv2d_set_path(int path);
+
+/* Which kernel dp_grad_sample_conv2d would run for this shape under the
+ * choice in force (dp_conv2d_set_path), for reports and tests:
+ * DP_CONV_KERNEL_SMALL (one workgroup per sample), _ROWS (row chunks),
+ * _TILED; -1 for a shape the call would refuse. */
+enum { DP_CONV_KERNEL_SMALL = 0, DP_CONV_KERNEL_ROWS = 1, DP_CONV_KERNEL_TILED = 2 };
+int32_t dp_conv2d_kernel_choice(int64_t N, int64_t Cin, int64_t H, int64_t W, int64_t Cout, int64_t kh,
+                                int64_t kw, int64_t sh, int64_t sw, int64_t ph, int64_t pw);
 
 /* One layer of dp_grad_sample_many: the arguments of dp_grad_sample_linear
  * (kind DP_LAYER_LINEAR: A, B, T, d_in, d_out) or dp_grad_sample_conv2d

@@ -38,6 +38,7 @@ SIGNATURES = {
     "dp_grad_sample_conv2d_workspace_bytes": (_SZ, [_I64] * 11),
     "dp_grad_sample_conv2d": (_ST, [_P, _P, _ST] + [_I64] * 16 + [_F, _P, _P, _P, _P, _P, _SZ, _P]),
     "dp_conv2d_set_path": (ctypes.c_int, [ctypes.c_int]),
+    "dp_conv2d_kernel_choice": (_I32, [_I64] * 11),
     "dp_grad_sample_many_grouped": (_I32, [_P, _ST, _I64]),
     "dp_grad_sample_many_workspace_bytes": (_SZ, [_P, _I32, _ST, _I64]),
     "dp_grad_sample_many": (_ST, [_P, _I32, _ST, _I64, _P, _P, _SZ, _P]),
@@ -258,7 +259,7 @@ def dp_grad_sample_conv2d(X, GY, dt, N, Cin, H, W, Cout, Ho, Wo, kh, kw, sh, sw,
            "dp_grad_sample_conv2d")
 
 
-DP_CONV_AUTO, DP_CONV_TILED = 0, 1
+DP_CONV_AUTO, DP_CONV_TILED, DP_CONV_ROWS = 0, 1, 2
 
 
 def dp_conv2d_set_path(path: int) -> int:
@@ -267,6 +268,14 @@ def dp_conv2d_set_path(path: int) -> int:
     if prev < 0:
         raise ValueError("unknown conv2d path %r" % (path,))
     return prev
+
+
+DP_CONV_KERNEL_SMALL, DP_CONV_KERNEL_ROWS, DP_CONV_KERNEL_TILED = 0, 1, 2
+
+
+def dp_conv2d_kernel_choice(N, Cin, H, W, Cout, kh, kw, sh, sw, ph, pw) -> int:
+    """The conv kernel dp_grad_sample_conv2d would run for this shape now."""
+    return lib().dp_conv2d_kernel_choice(N, Cin, H, W, Cout, kh, kw, sh, sw, ph, pw)
 
 
 def dp_grad_sample_embedding_workspace_bytes(N, T) -> int:

@@ -22,6 +22,7 @@
 #include "common.hpp"
 #include "mfma_tile.hpp"
 #include "conv2d_small.hpp"
+#include "conv2d_rows.hpp"
 
 #include <type_traits>
 
@@ -638,7 +639,12 @@ extern "C" size_t dp_grad_sample_conv2d_workspace_bytes(int64_t N, int64_t Cin, 
     if (!fits_int32(Cin, H + 2 * ph, W + 2 * pw, Cout, kh, kw)) return 0;
     const ConvShape s = make_shape(Cin, H, W, Cout, kh, kw, sh, sw, ph, pw);
     const int tiles = conv_tiles(s, (long)N);
-    return tiles > 1 ? (size_t)(N * tiles) * sizeof(float) : 0;
+    // the row-chunked kernel's norm partials, when it has several tiles
+    const ConvRowsArgs ra{nullptr, nullptr, N, Cin, H, W, Cout, (H + 2 * ph - kh) / sh + 1, (W + 2 * pw - kw) / sw + 1,
+                          kh, kw, sh, sw, ph, pw};
+    const int rtiles = conv_rows_tiles(ra);
+    const int most = rtiles > tiles ? rtiles : tiles;
+    return most > 1 ? (size_t)(N * most) * sizeof(float) : 0;
 }
 
 static int g_conv_path = DP_CONV_AUTO;
@@ -652,10 +658,24 @@ int conv_path()
 
 extern "C" int dp_conv2d_set_path(int path)
 {
-    if (path != DP_CONV_AUTO && path != DP_CONV_TILED) return -1;
+    if (path != DP_CONV_AUTO && path != DP_CONV_TILED && path != DP_CONV_ROWS) return -1;
     const int prev = g_conv_path;
     g_conv_path = path;
     return prev;
+}
+
+extern "C" int32_t dp_conv2d_kernel_choice(int64_t N, int64_t Cin, int64_t H, int64_t W, int64_t Cout, int64_t kh,
+                                           int64_t kw, int64_t sh, int64_t sw, int64_t ph, int64_t pw)
+{
+    if (N < 0 || !shape_ok(Cin, H, W, Cout, kh, kw, sh, sw, ph, pw)) return -1;
+    if (!fits_int32(Cin, H + 2 * ph, W + 2 * pw, Cout, kh, kw)) return -1;
+    const int64_t Ho = (H + 2 * ph - kh) / sh + 1, Wo = (W + 2 * pw - kw) / sw + 1;
+    const ConvSmallArgs small{nullptr, nullptr, N, Cin, H, W, Cout, Ho, Wo, kh, kw, sh, sw, ph, pw};
+    if (g_conv_path == DP_CONV_AUTO && conv_small_ok(small)) return DP_CONV_KERNEL_SMALL;
+    const ConvRowsArgs rows{nullptr, nullptr, N, Cin, H, W, Cout, Ho, Wo, kh, kw, sh, sw, ph, pw};
+    if (g_conv_path == DP_CONV_ROWS ? conv_rows_ok(rows) : g_conv_path == DP_CONV_AUTO && conv_rows_preferred(rows))
+        return DP_CONV_KERNEL_ROWS;
+    return DP_CONV_KERNEL_TILED;
 }
 
 extern "C" dp_status dp_grad_sample_conv2d(const void *X, const void *GY, dp_dtype dt, int64_t N,
@@ -685,6 +705,12 @@ extern "C" dp_status dp_grad_sample_conv2d(const void *X, const void *GY, dp_dty
     if (g_conv_path == DP_CONV_AUTO && conv_small_ok(small)) {
         // the whole sample fits one workgroup's LDS
         conv_small_launch(small, bf, scale, gW, gb, sqnorm, stream);
+        return launch_status();
+    }
+    const ConvRowsArgs rows{X, GY, N, Cin, H, W, Cout, Ho, Wo, kh, kw, sh, sw, ph, pw};
+    if (g_conv_path == DP_CONV_ROWS ? conv_rows_ok(rows) : g_conv_path == DP_CONV_AUTO && conv_rows_preferred(rows)) {
+        // output row chunks, the whole weight-column tile in registers
+        conv_rows_launch(rows, bf, scale, gW, gb, sqnorm, (float *)ws, stream);
         return launch_status();
     }
     const ConvShape s = make_shape(Cin, H, W, Cout, kh, kw, sh, sw, ph, pw);

@@ -144,8 +144,31 @@ def test_conv2d_path_choice_round_trips():
     prev = dp.dp_conv2d_set_path(dp.DP_CONV_TILED)
     try:
         assert dp.dp_conv2d_set_path(dp.DP_CONV_AUTO) == dp.DP_CONV_TILED
+        assert dp.dp_conv2d_set_path(dp.DP_CONV_ROWS) == dp.DP_CONV_AUTO
+        assert dp.dp_conv2d_set_path(dp.DP_CONV_AUTO) == dp.DP_CONV_ROWS
         assert dp.lib().dp_conv2d_set_path(7) == -1
         assert dp.dp_conv2d_set_path(dp.DP_CONV_AUTO) == dp.DP_CONV_AUTO
+    finally:
+        dp.dp_conv2d_set_path(prev)
+
+
+def test_conv2d_kernel_choice_follows_the_path():
+    """Which conv kernel runs: the one-workgroup-per-sample kernel for a plane
+    that fits LDS (MNIST's first layer), the row-chunked kernel for a wide
+    32x32 plane with 288 weight columns, the tiled kernel when forced, and -1
+    for a shape the call refuses."""
+    prev = dp.dp_conv2d_set_path(dp.DP_CONV_AUTO)
+    try:
+        mnist_c1 = (256, 1, 28, 28, 16, 8, 8, 2, 2, 3, 3)
+        cifar_c2 = (256, 32, 32, 32, 32, 3, 3, 1, 1, 1, 1)
+        assert dp.dp_conv2d_kernel_choice(*mnist_c1) == dp.DP_CONV_KERNEL_SMALL
+        assert dp.dp_conv2d_kernel_choice(*cifar_c2) == dp.DP_CONV_KERNEL_ROWS
+        assert dp.dp_conv2d_kernel_choice(256, 1, 2, 2, 4, 3, 3, 1, 1, 0, 0) == -1
+        dp.dp_conv2d_set_path(dp.DP_CONV_TILED)
+        assert dp.dp_conv2d_kernel_choice(*mnist_c1) == dp.DP_CONV_KERNEL_TILED
+        assert dp.dp_conv2d_kernel_choice(*cifar_c2) == dp.DP_CONV_KERNEL_TILED
+        dp.dp_conv2d_set_path(dp.DP_CONV_ROWS)
+        assert dp.dp_conv2d_kernel_choice(*cifar_c2) == dp.DP_CONV_KERNEL_ROWS
     finally:
         dp.dp_conv2d_set_path(prev)
 

@@ -284,11 +284,12 @@ CONV_CONFIG_SHAPES = [
     (1, 24, 20, 21, 5, 3, 3, 2, 2, 1, 1), (1, 20, 5, 6, 5, 3, 3, 2, 2, 1, 1)]              # 256 x 32, 8 waves
 
 
-@pytest.fixture(params=["auto", "tiled"])
+@pytest.fixture(params=["auto", "tiled", "rows"])
 def conv_path(request):
     """Run a conv test with the automatic kernel choice (one workgroup per
-    sample for samples that fit LDS) and again with the tiled kernel forced."""
-    path = dp.DP_CONV_TILED if request.param == "tiled" else dp.DP_CONV_AUTO
+    sample for samples that fit LDS, else output row chunks), and again with
+    the tiled and the row-chunked kernels forced."""
+    path = {"tiled": dp.DP_CONV_TILED, "rows": dp.DP_CONV_ROWS}.get(request.param, dp.DP_CONV_AUTO)
     prev = dp.dp_conv2d_set_path(path)
     yield request.param
     dp.dp_conv2d_set_path(prev)
