@@ -37,11 +37,11 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 constexpr int kThreads = 256;
 constexpr int kWaves = 4;
 constexpr int kMaxBlk = 9;                 // 32-column blocks per tile
-constexpr int kRowsLds = 60 * 1024;        // dynamic LDS budget (two workgroups per CU)
 
 struct RowsShape {
     int Cin, H, W, Cout, Ho, Wo, kh, kw, sh, sw, ph, pw;
     int Wp, L, KK, khw;
+    int xR, xC;           // staged input: LDS floats per row and per channel
     int nblk;             // 32-column blocks per tile (<= 9)
     int ktiles, ctiles;   // column tiles, channel tiles
     int np;               // input channels a column tile touches (upper bound)
@@ -50,10 +50,15 @@ struct RowsShape {
     int x_floats;         // np * XR * Wp
     int vec;              // float4 stores of gW
     float inv_khw, inv_kw, inv_wo;
-    // stepping an element index by kThreads in the input stage [np][XR][Wp]
-    // (channel, row, column) and in the backprop stage (channel, pair)
-    int xs_c, xs_r, xs_w, gs_c, gs_p;
-    float inv_xrw, inv_wp, inv_pairs;
+    // staging runs of VW elements: xwv = W / VW runs per input row, gqv =
+    // PC / VW runs per channel of the chunk's backprop.  Stepping a run index
+    // by kThreads: (channel, row, run) of the input by (xs_c, xs_r, xs_k),
+    // (channel, run) of the backprop by (gs_c, gs_q); the global element
+    // offsets and the LDS offsets follow by the step and wrap constants.
+    int vw, xwv, gqv;
+    int xs_c, xs_r, xs_k, gs_c, gs_q;
+    int xg_step, xg_wrap_r, xl_step, xl_wrap_k, xl_wrap_r, gg_step, gg_wrap_q;
+    float inv_xrw, inv_xwv, inv_gqv;
 };
 
 __device__ __forceinline__ void fdivmod(int x, int d, float inv_d, int &q, int &r)
@@ -64,13 +69,67 @@ __device__ __forceinline__ void fdivmod(int x, int d, float inv_d, int &q, int &
     r = x - q * d;
 }
 
+// Raw-buffer loads over one sample's tensor: 32-bit byte offsets, and an
+// offset past the buffer's size reads zero (the zero halo and everything past
+// the chunk or the tile come from that, with no branch and no mask).
+constexpr uint32_t kOutside = 0x80000000u;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t sample_buffer(const void *base, uint32_t bytes)
+{
+    // 0x00020000: the gfx9 descriptor word for 32-bit untyped accesses
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, (int)bytes, 0x00020000);
+}
+
+// XW dwords of raw data: VW elements of T (one bf16 element sits in the low
+// half of its dword)
+template <int XW>
+struct Raw {
+    uint32_t w[XW];
+};
+
+template <typename T, int VW, int XW>
+__device__ __forceinline__ Raw<XW> raw_load_v(__amdgpu_buffer_rsrc_t r, uint32_t byte_off)
+{
+    Raw<XW> x;
+    if constexpr (XW == 4) {
+        const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 0);
+        x.w[0] = v[0]; x.w[1] = v[1]; x.w[2] = v[2]; x.w[3] = v[3];
+    } else if constexpr (XW == 2) {
+        const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, byte_off, 0, 0);
+        x.w[0] = v[0]; x.w[1] = v[1];
+    } else if constexpr (sizeof(T) == 4) {
+        x.w[0] = __builtin_amdgcn_raw_buffer_load_b32(r, byte_off, 0, 0);
+    } else {
+        x.w[0] = __builtin_amdgcn_raw_buffer_load_b16(r, byte_off, 0, 0);
+    }
+    return x;
+}
+
+template <typename T, int VW, int XW>
+__device__ __forceinline__ void unpack(const Raw<XW> &x, float (&v)[VW])
+{
+    if constexpr (sizeof(T) == 4) {
+#pragma unroll
+        for (int t = 0; t < VW; ++t) v[t] = __builtin_bit_cast(float, x.w[t]);
+    } else if constexpr (VW == 1) {
+        v[0] = __builtin_bit_cast(float, x.w[0] << 16);
+    } else {
+#pragma unroll
+        for (int t = 0; t < VW; ++t)
+            v[t] = __builtin_bit_cast(float, (t & 1) ? (x.w[t >> 1] & 0xFFFF0000u) : (x.w[t >> 1] << 16));
+    }
+}
+
 // WCO: 32-channel blocks per tile (1 or 2).  The waves form (4 / WCO) column
 // rows x WCO channel columns; wave row q takes blocks q, q + 4/WCO, ...
-template <typename T, int WCO>
-__global__ __launch_bounds__(kThreads, 2) void conv_rows_kernel(const T *__restrict__ X, const T *__restrict__ GY,
-                                                                RowsShape s, float scale, float *__restrict__ gW,
-                                                                float *__restrict__ gb, float *__restrict__ sqout,
-                                                                int direct)
+// VW: elements per staging load (4: a 16-byte run of an input row or of a
+// channel's backprop; 1: single elements).  XS, GS: X and backprop loads per
+// thread per chunk, at most.  OCC: workgroups per CU the registers allow.
+template <typename T, int WCO, int VW, int XS, int GS, int OCC>
+__global__ __launch_bounds__(kThreads, OCC) void conv_rows_kernel(const T *__restrict__ X, const T *__restrict__ GY,
+                                                                  RowsShape s, float scale, float *__restrict__ gW,
+                                                                  float *__restrict__ gb, float *__restrict__ sqout,
+                                                                  int direct)
 {
     constexpr int WKK = kWaves / WCO;
     constexpr int FM = (kMaxBlk + WKK - 1) / WKK;
@@ -90,8 +149,8 @@ __global__ __launch_bounds__(kThreads, 2) void conv_rows_kernel(const T *__restr
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wq = wave / WCO, wc = wave % WCO;
     float *Xs = lds;                                   // [np][XR][Wp]
-    constexpr int GSP = 2 * BN + 2;                    // floats per position pair
-    float *Gs = lds + s.x_floats;                      // [PC/2][BN][2], pair stride GSP
+    constexpr int GSP = 2 * BN + 1;                    // floats per position pair (odd: staging writes spread over banks)
+    float *Gs = lds + s.x_floats;                      // [PC/2][2][BN], pair stride GSP
     int *Pt = reinterpret_cast<int *>(Gs + s.PC / 2 * GSP);   // [PC] offset of position p in the staged rows
     const T *Xn = X + n * (i64)s.Cin * s.H * s.W;
     const T *Gn = GY + n * (i64)s.Cout * s.L;
@@ -111,7 +170,7 @@ __global__ __launch_bounds__(kThreads, 2) void conv_rows_kernel(const T *__restr
             int ci, rem, u, v;
             fdivmod(kk, s.khw, s.inv_khw, ci, rem);
             fdivmod(rem, s.kw, s.inv_kw, u, v);
-            koff[x] = (ci - ci0) * s.XR * s.Wp + u * s.Wp + v;
+            koff[x] = (ci - ci0) * s.xC + u * s.xR + v;
         }
     }
     f32x16_t acc[FM];
@@ -123,72 +182,150 @@ __global__ __launch_bounds__(kThreads, 2) void conv_rows_kernel(const T *__restr
     float bacc = 0.0f;    // bias: thread (bseg, bco) adds positions bseg, bseg + kSegs, ... of each chunk
     const int bco = tid % BN, bseg = tid / BN;
     constexpr int kSegs = kThreads / BN;
-    // the thread's first element in each stage
-    int xc0, xr0, xw0, gc0, gp0;
+    // ---- staging.  The input stage holds, per tile channel c < np and staged
+    // row r < XR, the row's W data columns at LDS c * xC + r * xR + pw + w; the
+    // halo columns are cleared once and never written again, rows outside the
+    // input read zeros.  A load covers a run of VW consecutive elements: runs
+    // (c, r, k) of W / VW, and of the backprop (channel co, run q of the
+    // chunk's positions).  Thread t takes runs t, t + kThreads, ...; their
+    // indices and offsets are stepped by constants, not divided out.  An
+    // element outside the input, the chunk or the tile reads past the
+    // sample's buffer, which gives zero; the loaded values are not touched
+    // until the chunk is written to LDS, so every load stays in flight.
+    const __amdgpu_buffer_rsrc_t xbuf = sample_buffer(Xn, (uint32_t)(s.Cin * s.H * s.W) * (uint32_t)sizeof(T));
+    const __amdgpu_buffer_rsrc_t gbuf = sample_buffer(Gn, (uint32_t)(s.Cout * s.L) * (uint32_t)sizeof(T));
+    constexpr int XW = VW * sizeof(T) / 4 > 0 ? VW * sizeof(T) / 4 : 1;   // dwords per X load (bf16 singles: 1)
+    Raw<XW> xv[XS], gv[GS];
+    const int xruns = s.np * s.XR * s.xwv;                 // X runs per chunk
+    const int gruns = BN * s.gqv;                          // backprop runs per chunk
+    const int cmax = s.Cin - ci0 < s.np ? s.Cin - ci0 : s.np;
+    int xc0, xr0, xk0, gc0, gq0;
     {
         int rem;
-        fdivmod(tid, s.XR * s.Wp, s.inv_xrw, xc0, rem);
-        fdivmod(rem, s.Wp, s.inv_wp, xr0, xw0);
-        fdivmod(tid, s.PC / 2, s.inv_pairs, gc0, gp0);
+        fdivmod(tid, s.XR * s.xwv, s.inv_xrw, xc0, rem);
+        fdivmod(rem, s.xwv, s.inv_xwv, xr0, xk0);
+        fdivmod(tid, s.gqv, s.inv_gqv, gc0, gq0);
+    }
+    // halo columns: cleared once (they are never loaded)
+    if (s.pw > 0) {
+        for (int i = tid; i < s.x_floats; i += kThreads) Xs[i] = 0.0f;
     }
 
-    for (int oh0 = 0; oh0 < s.Ho; oh0 += s.RC) {
+    auto load_chunk = [&](int oh0) {
         const int rows = s.Ho - oh0 < s.RC ? s.Ho - oh0 : s.RC;
-        const int len = rows * s.Wo;                   // positions of this chunk
-        const int pbase = oh0 * s.Wo;
+        const int len = rows * s.Wo;
         const int ih0 = oh0 * s.sh - s.ph;
-        __syncthreads();                               // the previous chunk is consumed
-        // ---- input rows ih0 .. ih0 + XR - 1 of the tile's channels, zero
-        // outside.  Thread elements tid, tid + kThreads, ... of [np][XR][Wp];
-        // their (channel, row, column) are stepped, not divided out.
-        {
-            int c = xc0, r = xr0, w = xw0;
-            for (int idx = tid; idx < s.np * s.XR * s.Wp; idx += kThreads) {
-                const int ci = ci0 + c, ih = ih0 + r, iw = w - s.pw;
-                const bool in = ci < s.Cin && ih >= 0 && ih < s.H && iw >= 0 && iw < s.W;
-                Xs[idx] = in ? load_elem<T>(Xn, ((i64)ci * s.H + ih) * s.W + iw) : 0.0f;
-                w += s.xs_w;
-                if (w >= s.Wp) {
-                    w -= s.Wp;
+        int c = xc0, r = xr0, k = xk0;
+        int off = ((ci0 + c) * s.H + ih0 + r) * s.W + VW * k;      // element offset in the sample's input
+#pragma unroll
+        for (int j = 0; j < XS; ++j) {
+            if (j * kThreads < xruns) {
+                const bool in = (c < cmax) & ((unsigned)(ih0 + r) < (unsigned)s.H);
+                xv[j] = raw_load_v<T, VW, XW>(xbuf, in ? (uint32_t)off * (uint32_t)sizeof(T) : kOutside);
+                k += s.xs_k;
+                if (k >= s.xwv) {
+                    k -= s.xwv;
                     ++r;
                 }
                 r += s.xs_r;
                 if (r >= s.XR) {
                     r -= s.XR;
                     ++c;
+                    off += s.xg_wrap_r;
                 }
                 c += s.xs_c;
+                off += s.xg_step;
             }
         }
-        // ---- the chunk's backprop as [pair][channel][parity], zero past len;
-        // consecutive threads take consecutive pairs of one channel (coalesced
-        // loads), (channel, pair) stepped like the input's indices
-        {
-            int co = gc0, pr = gp0;
-            for (int e = tid; e < BN * (s.PC / 2); e += kThreads) {
-                const int p = 2 * pr;
-                const bool cin = co < cvalid;
-                const T *src = Gn + (i64)(n0 + co) * s.L + pbase;
-                const float g0 = cin && p < len ? load_elem<T>(src, p) : 0.0f;
-                const float g1 = cin && p + 1 < len ? load_elem<T>(src, p + 1) : 0.0f;
-                *reinterpret_cast<float2 *>(Gs + pr * GSP + 2 * co) = make_float2(g0, g1);
-                pr += s.gs_p;
-                if (pr >= s.PC / 2) {
-                    pr -= s.PC / 2;
+        int co = gc0, q = gq0;
+        int goff = (n0 + co) * s.L + oh0 * s.Wo + VW * q;
+#pragma unroll
+        for (int j = 0; j < GS; ++j) {
+            if (j * kThreads < gruns) {
+                const bool in = (co < cvalid) & (VW * q < len);
+                gv[j] = raw_load_v<T, VW, XW>(gbuf, in ? (uint32_t)goff * (uint32_t)sizeof(T) : kOutside);
+                q += s.gs_q;
+                if (q >= s.gqv) {
+                    q -= s.gqv;
+                    ++co;
+                    goff += s.gg_wrap_q;
+                }
+                co += s.gs_c;
+                goff += s.gg_step;
+            }
+        }
+    };
+    // ---- the loaded chunk into LDS: the input rows at c * xC + r * xR + pw +
+    // w, the backprop as [pair][parity][channel]
+    auto store_chunk = [&]() {
+        // every load has landed: said once here (vmcnt 0, the other counters
+        // untouched) so that no later write of these registers waits again
+        __builtin_amdgcn_s_waitcnt(0x0F70);
+        int c = xc0, r = xr0, k = xk0;
+        int lo = c * s.xC + r * s.xR + s.pw + VW * k;
+#pragma unroll
+        for (int j = 0; j < XS; ++j) {
+            if (j * kThreads < xruns) {
+                if (c < s.np) {
+                    float v[VW];
+                    unpack<T, VW, XW>(xv[j], v);
+#pragma unroll
+                    for (int t = 0; t < VW; ++t) Xs[lo + t] = v[t];
+                }
+                k += s.xs_k;
+                if (k >= s.xwv) {
+                    k -= s.xwv;
+                    ++r;
+                    lo += s.xl_wrap_k;
+                }
+                r += s.xs_r;
+                if (r >= s.XR) {
+                    r -= s.XR;
+                    ++c;
+                    lo += s.xl_wrap_r;
+                }
+                c += s.xs_c;
+                lo += s.xl_step;
+            }
+        }
+        int co = gc0, q = gq0;
+#pragma unroll
+        for (int j = 0; j < GS; ++j) {
+            if (j * kThreads < gruns) {
+                if (co < BN) {
+                    float v[VW];
+                    unpack<T, VW, XW>(gv[j], v);
+#pragma unroll
+                    for (int t = 0; t < VW; ++t) {
+                        const int p = VW * q + t;
+                        Gs[(p >> 1) * GSP + (p & 1) * BN + co] = v[t];
+                    }
+                }
+                q += s.gs_q;
+                if (q >= s.gqv) {
+                    q -= s.gqv;
                     ++co;
                 }
                 co += s.gs_c;
             }
         }
+    };
+
+    for (int oh0 = 0; oh0 < s.Ho; oh0 += s.RC) {
+        const int rows = s.Ho - oh0 < s.RC ? s.Ho - oh0 : s.RC;
+        const int len = rows * s.Wo;                   // positions of this chunk
+        load_chunk(oh0);                               // in flight while the other waves finish
+        __syncthreads();                               // the previous chunk is consumed
+        store_chunk();
         for (int p = tid; p < s.PC; p += kThreads) {
             int oh, ow;
             fdivmod(p, s.Wo, s.inv_wo, oh, ow);
-            Pt[p] = p < len ? oh * s.sh * s.Wp + ow * s.sw : 0;
+            Pt[p] = p < len ? oh * s.sh * s.xR + ow * s.sw : 0;
         }
         __syncthreads();
         if (do_bias) {
             // thread (bseg, bco): positions bseg, bseg + kSegs, ... of the chunk, in order
-            for (int p = bseg; p < len; p += kSegs) bacc += Gs[(p >> 1) * GSP + 2 * bco + (p & 1)];
+            for (int p = bseg; p < len; p += kSegs) bacc += Gs[(p >> 1) * GSP + (p & 1) * BN + bco];
         }
         // ---- contraction over the chunk's position pairs; the next pair's
         // reads are issued before the current pair's MFMAs
@@ -202,7 +339,7 @@ __global__ __launch_bounds__(kThreads, 2) void conv_rows_kernel(const T *__restr
             for (int h = 0; h < 2; ++h) {
                 const int pr = q + h;
                 const int po = Pt[2 * pr + half];
-                b[h] = Gs[pr * GSP + 2 * gl + half];
+                b[h] = Gs[pr * GSP + half * BN + gl];
 #pragma unroll
                 for (int x = 0; x < FM; ++x) a[h][x] = Xs[koff[x] + po];
             }
@@ -222,7 +359,7 @@ __global__ __launch_bounds__(kThreads, 2) void conv_rows_kernel(const T *__restr
                 // a position past the chunk (the second of a last, odd pair,
                 // or a pair past the end) contributes exactly zero
                 const bool pin = q + h < npairs && p < len;
-                const float bv = Gs[pr * GSP + 2 * gl + half];
+                const float bv = Gs[pr * GSP + half * BN + gl];
                 b[h] = pin ? bv : 0.0f;
 #pragma unroll
                 for (int x = 0; x < FM; ++x) {
@@ -288,7 +425,32 @@ __global__ __launch_bounds__(kThreads, 2) void conv_rows_kernel(const T *__restr
     }
 }
 
-bool plan_rows(const ConvRowsArgs &a, RowsShape &s)
+// LDS strides of the staged input.  A 32-column block's unfold read has lane
+// j at column kk0 + j, i.e. at ci * xC + u * xR + v for kk = (ci, u, v); with
+// xR = kw and xC = kh * kw (mod 32) that is kk (mod 32) plus a constant, so the
+// 32 lanes of a half-wave hit 32 different banks for any kernel size.
+int row_stride(int Wp, int kw)
+{
+    return Wp + (((kw - Wp) % 32) + 32) % 32;
+}
+
+int chan_stride(int XR, int xR, int khw)
+{
+    const int d = XR * xR;
+    return d + (((khw - d) % 32) + 32) % 32;
+}
+
+// Kernel variants: elements per staging load, loads per thread, workgroups
+// per CU and the LDS budget that keeps them resident.
+struct Variant {
+    int vw, xs, gs, occ, lds;
+};
+constexpr Variant kLarge4{4, 8, 8, 2, 72 * 1024};     // 16-byte runs, two workgroups per CU
+constexpr Variant kSmall4{4, 2, 2, 3, 50 * 1024};     // 16-byte runs, three workgroups per CU
+constexpr Variant kSingle{1, 24, 24, 2, 72 * 1024};   // single elements (any shape)
+
+// The row chunk and staging constants of a variant; false if no chunk fits.
+bool plan_rows(const ConvRowsArgs &a, const Variant &v, RowsShape &s)
 {
     s.Cin = (int)a.Cin; s.H = (int)a.H; s.W = (int)a.W; s.Cout = (int)a.Cout;
     s.Ho = (int)a.Ho; s.Wo = (int)a.Wo;
@@ -304,14 +466,20 @@ bool plan_rows(const ConvRowsArgs &a, RowsShape &s)
     s.ctiles = (s.Cout + 32 * wco - 1) / (32 * wco);
     s.np = (s.nblk * 32 + s.khw - 1) / s.khw + 1;
     if (s.np > s.Cin) s.np = s.Cin;
-    // the largest row chunk whose stage fits: np * XR * Wp + PC * BN + PC
+    s.vw = v.vw;
+    if (v.vw > 1 && (s.W % v.vw != 0 || s.Wo % v.vw != 0)) return false;
+    // the largest row chunk whose stage fits the LDS budget (np * xC + PC / 2
+    // * (2 BN + 1) + PC floats) and the per-thread load registers
     const int BN = 32 * wco;
     s.RC = 0;
     for (int rc = s.Ho; rc >= 1; --rc) {
         const int xr = (rc - 1) * s.sh + s.kh;
         const int pc = (rc * s.Wo + 1) & ~1;
-        const long fl = (long)s.np * xr * s.Wp + 3 + (long)pc / 2 * (2 * BN + 2) + pc;
-        if (fl * 4 <= kRowsLds) {
+        const long xf = ((long)s.np * chan_stride(xr, row_stride(s.Wp, s.kw), s.khw) + 3) & ~3L;
+        const long fl = xf + (long)pc / 2 * (2 * BN + 1) + pc;
+        const bool regs = (long)s.np * xr * (s.W / v.vw) <= (long)v.xs * kThreads &&
+                          (long)BN * (pc / v.vw) <= (long)v.gs * kThreads;
+        if (fl * 4 <= v.lds && regs) {
             s.RC = rc;
             break;
         }
@@ -319,32 +487,71 @@ bool plan_rows(const ConvRowsArgs &a, RowsShape &s)
     if (s.RC == 0) return false;
     s.XR = (s.RC - 1) * s.sh + s.kh;
     s.PC = (s.RC * s.Wo + 1) & ~1;
-    s.x_floats = s.np * s.XR * s.Wp;
-    s.x_floats = (s.x_floats + 3) & ~3;       // keeps the backprop's float2 stores 8-byte aligned
+    s.xR = row_stride(s.Wp, s.kw);
+    s.xC = chan_stride(s.XR, s.xR, s.khw);
+    s.x_floats = (s.np * s.xC + 3) & ~3;      // the backprop stage starts 16-byte aligned
     s.vec = 0;
     s.inv_khw = 1.0f / (float)s.khw;
     s.inv_kw = 1.0f / (float)s.kw;
     s.inv_wo = 1.0f / (float)s.Wo;
-    s.inv_xrw = 1.0f / (float)(s.XR * s.Wp);
-    s.inv_wp = 1.0f / (float)s.Wp;
-    s.inv_pairs = 1.0f / (float)(s.PC / 2);
+    s.xwv = s.W / v.vw;
+    s.gqv = s.PC / v.vw;
+    s.inv_xrw = 1.0f / (float)(s.XR * s.xwv);
+    s.inv_xwv = 1.0f / (float)s.xwv;
+    s.inv_gqv = 1.0f / (float)s.gqv;
     {
-        const int rows = kThreads / s.Wp;
-        s.xs_w = kThreads % s.Wp;
+        const int rows = kThreads / s.xwv;
+        s.xs_k = kThreads % s.xwv;
         s.xs_r = rows % s.XR;
         s.xs_c = rows / s.XR;
-        s.gs_p = kThreads % (s.PC / 2);
-        s.gs_c = kThreads / (s.PC / 2);
+        s.gs_q = kThreads % s.gqv;
+        s.gs_c = kThreads / s.gqv;
+        const int hw = s.H * s.W;
+        // input element offset ((ci0 + c) * H + ih0 + r) * W + VW * k: a run
+        // wrap (k past the row, r + 1) leaves it unchanged
+        s.xg_step = v.vw * s.xs_k + s.xs_r * s.W + s.xs_c * hw;
+        s.xg_wrap_r = hw - s.XR * s.W;
+        // LDS offset c * xC + r * xR + pw + VW * k
+        s.xl_step = v.vw * s.xs_k + s.xs_r * s.xR + s.xs_c * s.xC;
+        s.xl_wrap_k = s.xR - s.W;
+        s.xl_wrap_r = s.xC - s.XR * s.xR;
+        // backprop element offset (n0 + co) * L + oh0 * Wo + VW * q
+        s.gg_step = v.vw * s.gs_q + s.gs_c * s.L;
+        s.gg_wrap_q = s.L - v.vw * s.gqv;
     }
     // index arithmetic through float reciprocals needs values below 2^22
     return (long)s.x_floats < (1L << 22) && (long)s.PC * BN < (1L << 22) && (long)s.L < (1L << 22) &&
-           (long)s.KK < (1L << 22);
+           (long)s.KK < (1L << 22) && (long)s.np * s.XR * s.W < (1L << 22);
 }
 
 size_t lds_bytes(const RowsShape &s)
 {
     const int BN = s.Cout > 32 ? 64 : 32;
-    return ((size_t)s.x_floats + (size_t)(s.PC / 2) * (2 * BN + 2) + (size_t)s.PC) * sizeof(float);
+    return ((size_t)s.x_floats + (size_t)(s.PC / 2) * (2 * BN + 1) + (size_t)s.PC) * sizeof(float);
+}
+
+template <typename T, int WCO, int VW, int XS, int GS, int OCC>
+void launch_variant(const ConvRowsArgs &a, const RowsShape &s, float scale, float *gW, float *gb, float *sqout,
+                    int direct, hipStream_t stream)
+{
+    const dim3 grid((unsigned)(a.N * s.ktiles * s.ctiles));
+    conv_rows_kernel<T, WCO, VW, XS, GS, OCC><<<grid, kThreads, lds_bytes(s), stream>>>(
+        (const T *)a.X, (const T *)a.GY, s, scale, gW, gb, sqout, direct);
+}
+
+template <typename T, int WCO>
+void launch_typed(const ConvRowsArgs &a, int which, const RowsShape &s, float scale, float *gW, float *gb,
+                  float *sqout, int direct, hipStream_t stream)
+{
+    if (which == 0)
+        launch_variant<T, WCO, kLarge4.vw, kLarge4.xs, kLarge4.gs, kLarge4.occ>(a, s, scale, gW, gb, sqout, direct,
+                                                                              stream);
+    else if (which == 1)
+        launch_variant<T, WCO, kSmall4.vw, kSmall4.xs, kSmall4.gs, kSmall4.occ>(a, s, scale, gW, gb, sqout, direct,
+                                                                              stream);
+    else
+        launch_variant<T, WCO, kSingle.vw, kSingle.xs, kSingle.gs, kSingle.occ>(a, s, scale, gW, gb, sqout, direct,
+                                                                              stream);
 }
 
 }  // namespace
@@ -352,47 +559,45 @@ size_t lds_bytes(const RowsShape &s)
 bool conv_rows_ok(const ConvRowsArgs &a)
 {
     RowsShape s;
-    return plan_rows(a, s);
+    return plan_rows(a, kSingle, s);
 }
 
 bool conv_rows_preferred(const ConvRowsArgs &a)
 {
     RowsShape s;
-    return plan_rows(a, s) && s.nblk >= 4;
+    return plan_rows(a, kSingle, s) && s.nblk >= 4;
 }
 
 int conv_rows_tiles(const ConvRowsArgs &a)
 {
     RowsShape s;
-    if (!plan_rows(a, s)) return 0;
+    if (!plan_rows(a, kSingle, s)) return 0;
     return s.ktiles * s.ctiles;
 }
 
 void conv_rows_launch(const ConvRowsArgs &a, bool bf16, float scale, float *gW, float *gb, float *sqnorm,
                       float *partial, hipStream_t stream)
 {
+    // 16-byte runs (8-byte for bf16) where rows and pointers allow; three
+    // workgroups per CU where their smaller stage still takes chunks of four
+    // or more output rows (or the whole plane)
     RowsShape s;
-    plan_rows(a, s);
+    const int run_bytes = 4 * (bf16 ? 2 : 4);
+    const bool runs = aligned(a.X, run_bytes) && aligned(a.GY, run_bytes);
+    int which = 2;
+    if (runs && plan_rows(a, kSmall4, s) && (s.RC >= 4 || s.RC == s.Ho)) which = 1;
+    else if (runs && plan_rows(a, kLarge4, s)) which = 0;
+    else plan_rows(a, kSingle, s);
     s.vec = s.KK % 4 == 0 && aligned(gW, 16);
     const int tiles = s.ktiles * s.ctiles;
     const int direct = tiles == 1;
     float *sqout = sqnorm ? (direct ? sqnorm : partial) : nullptr;
-    const dim3 grid((unsigned)(a.N * tiles));
-    const size_t lds = lds_bytes(s);
     if (s.Cout > 32) {
-        if (bf16)
-            conv_rows_kernel<uint16_t, 2><<<grid, kThreads, lds, stream>>>(
-                (const uint16_t *)a.X, (const uint16_t *)a.GY, s, scale, gW, gb, sqout, direct);
-        else
-            conv_rows_kernel<float, 2><<<grid, kThreads, lds, stream>>>((const float *)a.X, (const float *)a.GY, s,
-                                                                        scale, gW, gb, sqout, direct);
+        if (bf16) launch_typed<uint16_t, 2>(a, which, s, scale, gW, gb, sqout, direct, stream);
+        else launch_typed<float, 2>(a, which, s, scale, gW, gb, sqout, direct, stream);
     } else {
-        if (bf16)
-            conv_rows_kernel<uint16_t, 1><<<grid, kThreads, lds, stream>>>(
-                (const uint16_t *)a.X, (const uint16_t *)a.GY, s, scale, gW, gb, sqout, direct);
-        else
-            conv_rows_kernel<float, 1><<<grid, kThreads, lds, stream>>>((const float *)a.X, (const float *)a.GY, s,
-                                                                        scale, gW, gb, sqout, direct);
+        if (bf16) launch_typed<uint16_t, 1>(a, which, s, scale, gW, gb, sqout, direct, stream);
+        else launch_typed<float, 1>(a, which, s, scale, gW, gb, sqout, direct, stream);
     }
     if (sqnorm && !direct) sum_partials(partial, a.N, tiles, sqnorm, stream);
 }
