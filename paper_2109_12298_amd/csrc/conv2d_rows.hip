@@ -157,12 +157,19 @@ __global__ __launch_bounds__(kThreads, OCC) void conv_rows_kernel(const T *__res
     const int cvalid = s.Cout - n0 < BN ? s.Cout - n0 : BN;
 
     // the lane's unfold column offsets in the staged rows (a column past the
-    // tile or the weight reads offset 0; its output rows are never stored)
-    int koff[FM];
-    bool bon[FM];
+    // tile or the weight reads offset 0; its output rows are never stored).
+    // Wave row wq takes blocks wq, wq + WKK, ...; with two wave rows and an
+    // odd block count the last block is shared: each wave row runs its MFMAs
+    // for one of the two pairs of every step (h == wq), and the two partial
+    // tiles are added before the store, so both rows carry nblk / 2 blocks.
+    int koff[FM], blkx[FM];
+    bool bon[FM], bsh[FM];
 #pragma unroll
     for (int x = 0; x < FM; ++x) {
-        const int blk = wq + WKK * x;
+        int blk = wq + WKK * x;
+        bsh[x] = WKK == 2 && (s.nblk & 1) && x == s.nblk / 2;
+        if (bsh[x]) blk = s.nblk - 1;
+        blkx[x] = blk;
         bon[x] = blk < s.nblk;
         const int kk = m0 + blk * 32 + (lane & 31);
         koff[x] = 0;
@@ -341,13 +348,15 @@ __global__ __launch_bounds__(kThreads, OCC) void conv_rows_kernel(const T *__res
                 const int po = Pt[2 * pr + half];
                 b[h] = Gs[pr * GSP + half * BN + gl];
 #pragma unroll
-                for (int x = 0; x < FM; ++x) a[h][x] = Xs[koff[x] + po];
+                for (int x = 0; x < FM; ++x)
+                    if (!bsh[x] || h == wq) a[h][x] = Xs[koff[x] + po];
             }
 #pragma unroll
             for (int h = 0; h < 2; ++h)
 #pragma unroll
                 for (int x = 0; x < FM; ++x)
-                    if (bon[x]) acc[x] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[h][x], b[h], acc[x], 0, 0, 0);
+                    if (bon[x] && (!bsh[x] || h == wq))
+                        acc[x] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[h][x], b[h], acc[x], 0, 0, 0);
         }
         for (int q = qfull; q < npairs; q += 2) {
             float a[2][FM], b[2];
@@ -363,16 +372,36 @@ __global__ __launch_bounds__(kThreads, OCC) void conv_rows_kernel(const T *__res
                 b[h] = pin ? bv : 0.0f;
 #pragma unroll
                 for (int x = 0; x < FM; ++x) {
-                    const float av = Xs[koff[x] + po];
-                    a[h][x] = pin ? av : 0.0f;
+                    if (!bsh[x] || h == wq) {
+                        const float av = Xs[koff[x] + po];
+                        a[h][x] = pin ? av : 0.0f;
+                    }
                 }
             }
 #pragma unroll
             for (int h = 0; h < 2; ++h)
 #pragma unroll
                 for (int x = 0; x < FM; ++x)
-                    if (bon[x]) acc[x] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[h][x], b[h], acc[x], 0, 0, 0);
+                    if (bon[x] && (!bsh[x] || h == wq))
+                        acc[x] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[h][x], b[h], acc[x], 0, 0, 0);
         }
+    }
+    if (WKK == 2 && (s.nblk & 1)) {
+        // the shared block: wave row 1 hands its partial tile to wave row 0
+        // through LDS ([channel column][register][lane], 8 KB)
+        __syncthreads();                               // the stage is consumed
+        float *part = lds + wc * 16 * 64;
+#pragma unroll
+        for (int x = 0; x < FM; ++x)
+            if (bsh[x] && wq == 1)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) part[r * 64 + lane] = acc[x][r];
+        __syncthreads();
+#pragma unroll
+        for (int x = 0; x < FM; ++x)
+            if (bsh[x] && wq == 0)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[x][r] += part[r * 64 + lane];
     }
 
     // ---- store the tile and its squared norm
@@ -381,8 +410,8 @@ __global__ __launch_bounds__(kThreads, OCC) void conv_rows_kernel(const T *__res
     float *G = gW + n * (i64)s.Cout * s.KK;
 #pragma unroll
     for (int x = 0; x < FM; ++x) {
-        if (!bon[x] || co >= s.Cout) continue;
-        const int kb = m0 + (wq + WKK * x) * 32;
+        if (!bon[x] || co >= s.Cout || (bsh[x] && wq != 0)) continue;
+        const int kb = m0 + blkx[x] * 32;
 #pragma unroll
         for (int rb = 0; rb < 4; ++rb) {
             const int kk = kb + 8 * rb + 4 * half;
@@ -447,7 +476,7 @@ struct Variant {
 };
 constexpr Variant kLarge4{4, 8, 8, 2, 72 * 1024};     // 16-byte runs, two workgroups per CU
 constexpr Variant kSmall4{4, 2, 2, 3, 50 * 1024};     // 16-byte runs, three workgroups per CU
-constexpr Variant kSingle{1, 24, 24, 2, 72 * 1024};   // single elements (any shape)
+constexpr Variant kSingle{1, 16, 16, 2, 72 * 1024};   // single elements (any shape)
 
 // The row chunk and staging constants of a variant; false if no chunk fits.
 bool plan_rows(const ConvRowsArgs &a, const Variant &v, RowsShape &s)
@@ -527,7 +556,10 @@ bool plan_rows(const ConvRowsArgs &a, const Variant &v, RowsShape &s)
 size_t lds_bytes(const RowsShape &s)
 {
     const int BN = s.Cout > 32 ? 64 : 32;
-    return ((size_t)s.x_floats + (size_t)(s.PC / 2) * (2 * BN + 1) + (size_t)s.PC) * sizeof(float);
+    const size_t b = ((size_t)s.x_floats + (size_t)(s.PC / 2) * (2 * BN + 1) + (size_t)s.PC) * sizeof(float);
+    // two wave rows hand a shared block's partial tile over in 8 KB
+    const size_t hand = BN == 64 ? 2 * 16 * 64 * sizeof(float) : 0;
+    return b > hand ? b : hand;
 }
 
 template <typename T, int WCO, int VW, int XS, int GS, int OCC>
