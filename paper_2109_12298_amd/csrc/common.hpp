@@ -58,6 +58,15 @@ __device__ __forceinline__ float load_elem<uint16_t>(const uint16_t *p, i64 i)
     return bf16_to_f32(p[i]);
 }
 
+// A 16-byte store marked non-temporal (streamed past the caches), for large
+// outputs that the next kernel reads from memory anyway.
+__device__ __forceinline__ void store_stream4(float *p, float a, float b, float c, float d)
+{
+    typedef float f32x4_t __attribute__((ext_vector_type(4)));
+    const f32x4_t v = {a, b, c, d};
+    __builtin_nontemporal_store(v, reinterpret_cast<f32x4_t *>(p));
+}
+
 // ---------------------------------------------------------------------------
 // XCD-aware block order.  Workgroups are dispatched round-robin over the 8
 // XCDs (each with its own L2): block b runs on XCD b % 8.  Renumbering so that

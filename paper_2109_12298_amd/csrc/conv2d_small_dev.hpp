@@ -274,7 +274,7 @@ __device__ __forceinline__ void conv_small_sample(const T *__restrict__ X, const
             const float g2 = scale * acc[j][2], g3 = scale * acc[j][3];
             float *dst = G + (i64)co * s.KK + kk0;
             if (s.vec && kk0 + 3 < s.KK) {
-                *reinterpret_cast<float4 *>(dst) = make_float4(g0, g1, g2, g3);
+                store_stream4(dst, g0, g1, g2, g3);
                 sq += g0 * g0 + g1 * g1 + g2 * g2 + g3 * g3;
             } else {
                 if (kk0 + 0 < s.KK) { dst[0] = g0; sq += g0 * g0; }

@@ -81,8 +81,7 @@ __device__ __forceinline__ void outer_block(const T *__restrict__ A, const T *__
             na += a[k].x * a[k].x + a[k].y * a[k].y + a[k].z * a[k].z + a[k].w * a[k].w;
             for (i64 i = i0; i < i1; ++i) {
                 const float b = bsh[i - i0];
-                *reinterpret_cast<float4 *>(G + i * din + 4 * j4) =
-                    make_float4(b * a[k].x, b * a[k].y, b * a[k].z, b * a[k].w);
+                store_stream4(G + i * din + 4 * j4, b * a[k].x, b * a[k].y, b * a[k].z, b * a[k].w);
             }
         }
     } else if (VEC) {
@@ -91,7 +90,7 @@ __device__ __forceinline__ void outer_block(const T *__restrict__ A, const T *__
             na += av.x * av.x + av.y * av.y + av.z * av.z + av.w * av.w;
             for (i64 i = i0; i < i1; ++i) {
                 const float b = bsh[i - i0];
-                *reinterpret_cast<float4 *>(G + i * din + 4 * j4) = make_float4(b * av.x, b * av.y, b * av.z, b * av.w);
+                store_stream4(G + i * din + 4 * j4, b * av.x, b * av.y, b * av.z, b * av.w);
             }
         }
     } else {
