@@ -67,6 +67,14 @@ __device__ __forceinline__ void store_stream4(float *p, float a, float b, float 
     __builtin_nontemporal_store(v, reinterpret_cast<f32x4_t *>(p));
 }
 
+// A 16-byte load marked non-temporal, for data read once.
+__device__ __forceinline__ float4 load_stream4(const float *p)
+{
+    typedef float f32x4_t __attribute__((ext_vector_type(4)));
+    const f32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const f32x4_t *>(p));
+    return make_float4(v[0], v[1], v[2], v[3]);
+}
+
 // ---------------------------------------------------------------------------
 // XCD-aware block order.  Workgroups are dispatched round-robin over the 8
 // XCDs (each with its own L2): block b runs on XCD b % 8.  Renumbering so that

@@ -205,6 +205,10 @@ struct FusedArgs {
 
 static_assert(sizeof(GroupDesc) + sizeof(FusedArgs) <= 4096, "kernel arguments");
 
+// STREAM: the per-sample gradients are read with non-temporal loads (they
+// are read once, and a large set of them would only push out of the caches
+// what the next kernels read).
+template <bool STREAM>
 __global__ __launch_bounds__(kThreads) void norms_clip_noise_kernel(GroupDesc d, FusedArgs f)
 {
     __shared__ float cfs[kCfChunk];
@@ -281,7 +285,9 @@ __global__ __launch_bounds__(kThreads) void norms_clip_noise_kernel(GroupDesc d,
             for (; n + 8 <= a1; n += 8) {
                 float4 a[8];
 #pragma unroll
-                for (int j = 0; j < 8; ++j) a[j] = g4[(n + j) * st4 + q];
+                for (int j = 0; j < 8; ++j)
+                    a[j] = STREAM ? load_stream4(reinterpret_cast<const float *>(g4 + (n + j) * st4 + q))
+                                  : g4[(n + j) * st4 + q];
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
                     const float cn = cfs[n + j - c0];
@@ -500,11 +506,13 @@ extern "C" dp_status dp_norms_clip_noise(const float *sqnorm, int32_t n_layers, 
         GroupDesc d;
         describe(params, first, c, N, d);
         int cb = 0, ob = 0;
+        i64 col_bytes = 0;     // per-sample gradient bytes the column reduce reads
         for (int i = 0; i < c; ++i) {
             f.cblk0[i] = cb;
             f.oblk0[i] = ob;
             const bool col = d.R[i] && N > 0 && d.numel[i] > 0;
             if (col) {
+                col_bytes += 4 * N * d.numel[i];
                 // 16-byte columns need a 16-byte aligned tensor (the partial flag bit 0
                 // of describe() also asks for an aligned sum, which this path does not)
                 const bool v = (d.numel[i] & 3) == 0 && aligned(d.G[i], 16);
@@ -524,7 +532,13 @@ extern "C" dp_status dp_norms_clip_noise(const float *sqnorm, int32_t n_layers, 
             norms_done = true;
         }
         f.sqnorm = norms_done ? nullptr : sqnorm;
-        if (cb + ob > 0) norms_clip_noise_kernel<<<(unsigned)(cb + ob), kThreads, 0, stream>>>(d, f);
+        if (cb + ob > 0) {
+            // stream the gradients when there are many of them (16 MB or more)
+            if (col_bytes >= (i64(16) << 20))
+                norms_clip_noise_kernel<true><<<(unsigned)(cb + ob), kThreads, 0, stream>>>(d, f);
+            else
+                norms_clip_noise_kernel<false><<<(unsigned)(cb + ob), kThreads, 0, stream>>>(d, f);
+        }
         norms_done = true;
     }
     return launch_status();
