@@ -9,21 +9,21 @@
 // A workgroup owns one sample's gradient tile of up to 288 weight columns
 // (nine MFMA blocks of 32) by 64 (or 32) output channels, with every
 // accumulator of the tile in registers, and walks the sample's output rows in
-// chunks.  Per chunk it stages the input rows the chunk reads (for the tile's
-// input channels, with a zero halo) and the chunk's backprop, then contracts
-// over the chunk's positions on v_mfma_f32_32x32x2_f32: per position pair a
-// lane reads one unfold element per block (its column's offset plus the
-// position's, from a table) and one backprop element, and the same position
-// work feeds up to five MFMAs.  Against tiling the unfold by columns and
-// staging whole planes, this stages each backprop element once per column
-// tile instead of once per 32 columns, and keeps the index arithmetic per
-// MFMA small (the tiled kernel was bound by it, not by the matrix unit).
+// chunks.  Per chunk it loads the input rows the chunk reads (the tile's input
+// channels) and the chunk's backprop into registers, all loads in flight at
+// once, writes them to LDS, and contracts over the chunk's positions on
+// v_mfma_f32_32x32x2_f32: per position pair a lane reads one unfold element
+// per block (its column's offset plus the position's, from a table) and one
+// backprop element, and the same position work feeds four or five MFMAs.
+// Against tiling the unfold by columns and staging whole planes, this stages
+// each backprop element once per column tile instead of once per 32 columns,
+// and keeps the index arithmetic per MFMA small.
 //
-// The backprop chunk sits in LDS as [position pair][channel][parity] with a
-// pair stride of 2 * channels + 2 floats: the two positions of a pair (the
-// two halves of the wave) read different banks, and the staging writes, whose
-// consecutive lanes take consecutive pairs of one channel (coalesced loads),
-// spread over the banks.
+// LDS banks.  The staged input has a row stride = kw and a channel stride =
+// kh * kw (mod 32), so the 32 consecutive unfold columns a half-wave reads
+// land in 32 different banks whatever the kernel size; the backprop sits as
+// [position pair][parity][channel], so each half-wave reads 32 consecutive
+// channels, with an odd pair stride that spreads the staging writes.
 // A sample's norm partials (one per tile) are added in tile order by a
 // second kernel; a single tile writes the norm directly.
 #include "common.hpp"
