@@ -384,6 +384,26 @@ dp_status dp_norms_clip_noise(const float *sqnorm, int32_t n_layers, const dp_pa
                               uint64_t step, const uint64_t *step_dev, float sigma, float denom,
                               int32_t *status, void *ws, size_t ws_bytes, hipStream_t stream);
 
+/* dp_norms_clip_noise with a noise schedule (section "Design Principles and
+ * Features", "Noise scheduler and variable batch size": the noise multiplier
+ * evolves during training by a predefined schedule, such as exponential,
+ * step or a custom function; the table holds any such schedule, evaluated
+ * by the caller): the noise multiplier of step t (t = step + *step_dev, the
+ * same step the noise stream is keyed by) is
+ * sigma_table[min(t, table_len - 1)], read on the device, so a captured graph
+ * follows the schedule from replay to replay.  sigma_table: table_len >= 1
+ * floats in device memory, owned by the caller and read while the launch
+ * runs; each entry must be finite and >= 0 (an entry that is not raises
+ * DP_FLAG_NONFINITE in *status and turns that step's noised outputs to NaN).
+ * A NULL table, table_len < 1 or an infinite C returns DP_EINVAL.  Everything else is as dp_norms_clip_noise; with a table
+ * of one entry s it gives the same results as dp_norms_clip_noise with sigma
+ * = s. */
+dp_status dp_norms_clip_noise_sched(const float *sqnorm, int32_t n_layers, const dp_param *params,
+                                    int32_t count, int64_t N, float *norm, float C, uint64_t seed,
+                                    uint64_t step, const uint64_t *step_dev, const float *sigma_table,
+                                    int64_t table_len, float denom, int32_t *status, void *ws,
+                                    size_t ws_bytes, hipStream_t stream);
+
 /* *step_dev += by, on the device (one tiny kernel): advances the step counter
  * a captured graph reads through dp_clip_noise_many. */
 dp_status dp_step_advance(uint64_t *step_dev, uint64_t by, hipStream_t stream);

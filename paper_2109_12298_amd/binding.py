@@ -65,6 +65,8 @@ SIGNATURES = {
     "dp_clip_noise_many": (_ST, [_P, _I32, _I64, _P, _F, _U64, _U64, _P, _F, _F, _P, _P, _SZ, _P]),
     "dp_norms_clip_noise_workspace_bytes": (_SZ, [_P, _I32, _I64]),
     "dp_norms_clip_noise": (_ST, [_P, _I32, _P, _I32, _I64, _P, _F, _U64, _U64, _P, _F, _F, _P, _P, _SZ, _P]),
+    "dp_norms_clip_noise_sched": (_ST, [_P, _I32, _P, _I32, _I64, _P, _F, _U64, _U64, _P, _P, _I64, _F, _P, _P, _SZ,
+                                        _P]),
     "dp_step_advance": (_ST, [_P, _U64, _P]),
     "dp_add_noise": (_ST, [_P, _P, _I64, _U64, _U64, _U32, _F, _F, _F, _P, _P]),
     "dp_philox_normals": (_ST, [_P, _P, _I64, _U64, _U64, _U32, _P]),
@@ -207,6 +209,10 @@ def _nbytes(x) -> int:
     if x is None:
         return 0
     return x.numel() * x.element_size()
+
+
+def _numel(x) -> int:
+    return 0 if x is None else x.numel()
 
 
 def _stream(stream):
@@ -415,6 +421,17 @@ def dp_norms_clip_noise(sqnorm, n_layers, params, count, N, norm, C, seed, step,
                                      _ptr(norm), C, seed, step, _ptr(step_dev), sigma, denom, _ptr(status),
                                      _ptr(ws), _nbytes(ws), _stream(stream)),
            "dp_norms_clip_noise")
+
+
+def dp_norms_clip_noise_sched(sqnorm, n_layers, params, count, N, norm, C, seed, step, step_dev, sigma_table,
+                              denom, status=None, ws=None, stream=None):
+    """dp_norms_clip_noise with the noise multiplier of step t read from
+    sigma_table[min(t, len - 1)] (a device float tensor) on the device."""
+    _check(lib().dp_norms_clip_noise_sched(_ptr(sqnorm), n_layers, ctypes.cast(params, ctypes.c_void_p), count, N,
+                                           _ptr(norm), C, seed, step, _ptr(step_dev), _ptr(sigma_table),
+                                           _numel(sigma_table), denom, _ptr(status), _ptr(ws), _nbytes(ws),
+                                           _stream(stream)),
+           "dp_norms_clip_noise_sched")
 
 
 def dp_step_advance(step_dev, by=1, stream=None):

@@ -197,6 +197,10 @@ struct FusedArgs {
     const uint64_t *step_dev;
     float sc, denom;
     int noise;
+    // noise schedule: sigma of step t is sigma_tab[min(t, tab_len - 1)]
+    // (then sc = sigma * C and noise = sigma > 0 are taken at run time)
+    const float *sigma_tab;
+    i64 tab_len;
     int32_t *status;
     int cblocks;               // column workgroups
     int cblk0[kMaxGroup + 1];  // first column workgroup of each tensor
@@ -204,6 +208,29 @@ struct FusedArgs {
 };
 
 static_assert(sizeof(GroupDesc) + sizeof(FusedArgs) <= 4096, "kernel arguments");
+
+// The noise scale sigma * C of this launch's step, and whether to draw noise:
+// fixed, or the step's entry of the schedule (a negative or non-finite entry
+// raises DP_FLAG_NONFINITE and gives a NaN scale).
+__device__ __forceinline__ void noise_scale(const FusedArgs &f, float &sc, bool &noise)
+{
+    if (f.sigma_tab == nullptr) {
+        sc = f.sc;
+        noise = f.noise != 0;
+        return;
+    }
+    const uint64_t t = f.step + (f.step_dev ? *f.step_dev : 0ull);
+    const uint64_t last = (uint64_t)(f.tab_len - 1);
+    const float sg = f.sigma_tab[t < last ? t : last];
+    if (!(sg >= 0.0f) || !isfinite(sg)) {
+        if (threadIdx.x == 0) raise_flag(f.status, DP_FLAG_NONFINITE);
+        sc = __builtin_nanf("");
+        noise = true;
+        return;
+    }
+    sc = sg * f.C;
+    noise = sg > 0.0f;
+}
 
 // STREAM: the per-sample gradients are read with non-temporal loads (they
 // are read once, and a large set of them would only push out of the caches
@@ -233,12 +260,15 @@ __global__ __launch_bounds__(kThreads) void norms_clip_noise_kernel(GroupDesc d,
         float *O = d.O[p];
         if (O == nullptr) return;
         float z[4] = {0.f, 0.f, 0.f, 0.f};
-        if (f.noise) {
+        float sc;
+        bool noise;
+        noise_scale(f, sc, noise);
+        if (noise) {
             const uint64_t st = f.step + (f.step_dev ? *f.step_dev : 0ull);
             uint32_t w[4];
             normals4(q, d.pidx[p], (uint32_t)st, (uint32_t)(st >> 32), f.k0, f.k1, z, w);
         }
-        for (int i = 0; i < cnt; ++i) O[e0 + i] = (s[i] + f.sc * z[i]) / f.denom;
+        for (int i = 0; i < cnt; ++i) O[e0 + i] = (s[i] + sc * z[i]) / f.denom;
         return;
     }
 
@@ -329,15 +359,18 @@ __global__ __launch_bounds__(kThreads) void norms_clip_noise_kernel(GroupDesc d,
     float *O = d.O[p];
     if (O == nullptr) return;
     float z[4] = {0.f, 0.f, 0.f, 0.f};
-    if (f.noise) {
+    float sc;
+    bool noise;
+    noise_scale(f, sc, noise);
+    if (noise) {
         const uint64_t st = f.step + (f.step_dev ? *f.step_dev : 0ull);
         uint32_t w[4];
         normals4(e0 >> 2, d.pidx[p], (uint32_t)st, (uint32_t)(st >> 32), f.k0, f.k1, z, w);
     }
     if (vec) {
-        for (int i = 0; i < 4; ++i) O[e0 + i] = (s[i] + f.sc * z[i]) / f.denom;
+        for (int i = 0; i < 4; ++i) O[e0 + i] = (s[i] + sc * z[i]) / f.denom;
     } else {
-        O[e0] = (s[0] + f.sc * z[e0 & 3]) / f.denom;
+        O[e0] = (s[0] + sc * z[e0 & 3]) / f.denom;
     }
 }
 
@@ -467,17 +500,17 @@ extern "C" size_t dp_norms_clip_noise_workspace_bytes(const dp_param *params, in
     return 0;
 }
 
-extern "C" dp_status dp_norms_clip_noise(const float *sqnorm, int32_t n_layers, const dp_param *params,
-                                         int32_t count, int64_t N, float *norm, float C, uint64_t seed,
-                                         uint64_t step, const uint64_t *step_dev, float sigma, float denom,
-                                         int32_t *status, void *ws, size_t ws_bytes, hipStream_t stream)
+static dp_status norms_clip_noise(const float *sqnorm, int32_t n_layers, const dp_param *params, int32_t count,
+                                  int64_t N, float *norm, float C, uint64_t seed, uint64_t step,
+                                  const uint64_t *step_dev, float sigma, const float *sigma_table,
+                                  int64_t table_len, float denom, int32_t *status, hipStream_t stream)
 {
-    (void)ws;
-    (void)ws_bytes;
     DPG_REQUIRE(count >= 0 && N >= 0, DP_EINVAL);
     DPG_REQUIRE(count == 0 || params != nullptr, DP_EINVAL);
     DPG_REQUIRE(C > 0.0f && sigma >= 0.0f && denom > 0.0f, DP_EINVAL);
     DPG_REQUIRE(!(sigma > 0.0f && __builtin_isinf(C)), DP_EINVAL);
+    // a schedule may hold positive entries: it needs a finite clipping bound
+    DPG_REQUIRE(sigma_table == nullptr || (table_len >= 1 && !__builtin_isinf(C)), DP_EINVAL);
     DPG_REQUIRE(sqnorm == nullptr || n_layers >= 1, DP_EINVAL);
     DPG_REQUIRE(N == 0 || norm != nullptr, DP_EINVAL);
     for (int i = 0; i < count; ++i) {
@@ -499,6 +532,8 @@ extern "C" dp_status dp_norms_clip_noise(const float *sqnorm, int32_t n_layers, 
     f.sc = noise ? sigma * C : 0.0f;
     f.denom = denom;
     f.noise = noise ? 1 : 0;
+    f.sigma_tab = sigma_table;
+    f.tab_len = table_len;
     f.status = status;
     bool norms_done = sqnorm == nullptr || N == 0;
     for (int first = 0; first < count; first += kMaxGroup) {
@@ -542,6 +577,30 @@ extern "C" dp_status dp_norms_clip_noise(const float *sqnorm, int32_t n_layers, 
         norms_done = true;
     }
     return launch_status();
+}
+
+extern "C" dp_status dp_norms_clip_noise(const float *sqnorm, int32_t n_layers, const dp_param *params,
+                                         int32_t count, int64_t N, float *norm, float C, uint64_t seed,
+                                         uint64_t step, const uint64_t *step_dev, float sigma, float denom,
+                                         int32_t *status, void *ws, size_t ws_bytes, hipStream_t stream)
+{
+    (void)ws;
+    (void)ws_bytes;
+    return norms_clip_noise(sqnorm, n_layers, params, count, N, norm, C, seed, step, step_dev, sigma, nullptr, 0,
+                            denom, status, stream);
+}
+
+extern "C" dp_status dp_norms_clip_noise_sched(const float *sqnorm, int32_t n_layers, const dp_param *params,
+                                               int32_t count, int64_t N, float *norm, float C, uint64_t seed,
+                                               uint64_t step, const uint64_t *step_dev, const float *sigma_table,
+                                               int64_t table_len, float denom, int32_t *status, void *ws,
+                                               size_t ws_bytes, hipStream_t stream)
+{
+    (void)ws;
+    (void)ws_bytes;
+    DPG_REQUIRE(sigma_table != nullptr, DP_EINVAL);
+    return norms_clip_noise(sqnorm, n_layers, params, count, N, norm, C, seed, step, step_dev, 0.0f, sigma_table,
+                            table_len, denom, status, stream);
 }
 
 extern "C" dp_status dp_step_advance(uint64_t *step_dev, uint64_t by, hipStream_t stream)

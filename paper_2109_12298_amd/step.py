@@ -22,7 +22,7 @@ comes from a device counter that the graph advances itself.
 from __future__ import annotations
 
 from dataclasses import dataclass
-from typing import Callable, Dict, List, Optional
+from typing import Callable, Dict, List, Optional, Sequence
 
 import numpy as np
 
@@ -91,7 +91,8 @@ class DPStep:
 
     def __init__(self, wl: W.Workload, inputs: List[W.LayerInputs], device="cuda", C=None, sigma=None,
                  denom=None, scale=None, clip_mode: str = "auto", seed: Optional[int] = None,
-                 norm_mode: str = "materialize", virtual_batches: int = 1):
+                 norm_mode: str = "materialize", virtual_batches: int = 1,
+                 sigma_schedule: Optional[Sequence[float]] = None):
         """norm_mode: 'materialize' computes every layer's per-sample gradients
         (the paper's method); 'ghost' gives a Linear layer whose clipped sum is
         fused, and for which 2 T^2 < d_in * d_out, its per-sample norm from
@@ -102,13 +103,27 @@ class DPStep:
         logical batch; each physical batch's clipped sums are added into a
         running sum, and only the last adds noise and divides (by K*N unless
         denom is given).  Drive it with run(reset=..., emit=...) or
-        run_virtual."""
+        run_virtual.
+
+        sigma_schedule: the noise multiplier per step (a noise scheduler:
+        exponential, step or any custom schedule, evaluated beforehand);
+        step t uses sigma_schedule[min(t, len - 1)], read on the device, so
+        captured graphs follow it from replay to replay.  It replaces sigma.
+        denom: the divisor of the noisy sum, e.g. the expected batch size
+        q * dataset size under Poisson sampling (the default is the physical
+        batch times virtual_batches)."""
         torch = _torch()
         self.wl = wl
         self.device = torch.device(device)
         self.N = int(inputs[0].B.shape[0])
         self.C = float(wl.C if C is None else C)
         self.sigma = float(wl.sigma if sigma is None else sigma)
+        self.sigma_tab = None
+        if sigma_schedule is not None:
+            sched = [float(x) for x in sigma_schedule]
+            if not sched:
+                raise ValueError("sigma_schedule needs at least one entry")
+            self.sigma_tab = torch.tensor(sched, dtype=torch.float32, device=torch.device(device))
         self.virtual_batches = int(virtual_batches)
         if self.virtual_batches < 1:
             raise ValueError("virtual_batches must be >= 1")
@@ -309,9 +324,14 @@ class DPStep:
         With virtual steps the sums go into the running sums, and the output
         is formed only when emit is set (the logical batch's last physical batch)."""
         group = self.group if self.virtual_batches == 1 else (self.group_emit if emit else self.group_acc)
-        dp.dp_norms_clip_noise(self.sqnorm if self.fold_norms else None, len(self.layers), group,
-                               self.group_count, self.N, self.norm, self.C, self.seed, step, step_dev,
-                               self.sigma, self.denom, self.status, self.ws, stream)
+        if self.sigma_tab is not None:
+            dp.dp_norms_clip_noise_sched(self.sqnorm if self.fold_norms else None, len(self.layers), group,
+                                         self.group_count, self.N, self.norm, self.C, self.seed, step, step_dev,
+                                         self.sigma_tab, self.denom, self.status, self.ws, stream)
+        else:
+            dp.dp_norms_clip_noise(self.sqnorm if self.fold_norms else None, len(self.layers), group,
+                                   self.group_count, self.N, self.norm, self.C, self.seed, step, step_dev,
+                                   self.sigma, self.denom, self.status, self.ws, stream)
 
     def reset_running_sums(self):
         """Zero the virtual step's running sums (a fill kernel, capturable)."""

@@ -119,6 +119,18 @@ def test_clip_and_noise_validation():
     assert code_of(dp.dp_grad_sample_linear, None, None, dp.DP_F32, 0, 3, 4, 5, 1.0, None, stream=0) == dp.DP_OK
 
 
+def test_noise_schedule_validation():
+    """dp_norms_clip_noise_sched refuses a missing table, an empty one and an
+    infinite C (a schedule may hold positive entries), and a zero
+    denominator, before enqueueing anything."""
+    f = dp.lib().dp_norms_clip_noise_sched
+    # (sqnorm, L, params, count, N, norm, C, seed, step, step_dev, table, len, denom, status, ws, ws_bytes, stream)
+    assert f(None, 0, None, 0, 0, None, 1.0, 0, 0, None, None, 1, 1.0, None, None, 0, None) == dp.DP_EINVAL
+    assert f(None, 0, None, 0, 0, None, 1.0, 0, 0, None, FAKE, 0, 1.0, None, None, 0, None) == dp.DP_EINVAL
+    assert f(None, 0, None, 0, 0, None, math.inf, 0, 0, None, FAKE, 3, 1.0, None, None, 0, None) == dp.DP_EINVAL
+    assert f(None, 0, None, 0, 0, None, 1.0, 0, 0, None, FAKE, 3, 0.0, None, None, 0, None) == dp.DP_EINVAL
+
+
 def test_clip_sum_route_choice():
     # small T = 1 Linear: rereading 16.8 MB of grads in the shared grouped launch beats two extra launches
     assert stepmod.linear_clip_mode(W.Linear("fc1", 512, 32), 256, W.F32) == "colreduce"

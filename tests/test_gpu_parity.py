@@ -591,6 +591,67 @@ def test_graph_with_several_steps_per_replay(parallel):
     assert int(st.step_dev.item()) == 5     # the first step of the last replay (steps 5, 6, 7)
 
 
+def test_noise_schedule_and_expected_batch_match_oracle():
+    """A noise schedule (three entries, step t takes entry min(t, 2), one of
+    them 0) and an expected-batch denominator (q times a pool of 40): each
+    eager step matches the oracle's step with that step's sigma and the same
+    denominator; a one-entry schedule equals the fixed sigma bit for bit."""
+    wl = W.get("mnist_cnn")
+    inputs = W.make_inputs(wl, n=12)
+    sched = [1.3, 0.0, 0.6]
+    denom = 0.25 * 40
+    st = DPStep(wl, inputs, DEV, sigma_schedule=sched, denom=denom)
+    for t in (0, 1, 2, 5):
+        say("noise schedule, step", t)
+        st.run(step=t)
+        got = st.results()
+        ref = oracle.dp_step(wl, inputs, step=t, sigma=sched[min(t, 2)], denom=denom)
+        compare_step(wl, inputs, got, ref, RTOL[wl.dtype], "schedule step %d" % t)
+    one = DPStep(wl, inputs, DEV, sigma_schedule=[0.7])
+    fixed = DPStep(wl, inputs, DEV, sigma=0.7)
+    one.run(step=4)
+    fixed.run(step=4)
+    a, b = one.results(), fixed.results()
+    for k in b["out"]:
+        np.testing.assert_array_equal(a["out"][k], b["out"][k], err_msg=k)
+
+
+@pytest.mark.parametrize("parallel", [False, True])
+def test_noise_schedule_in_a_graph_matches_eager(parallel):
+    """A captured graph with three steps per replay follows the schedule
+    from replay to replay (the step counter on the device picks the entry)."""
+    wl = W.get("mnist_cnn")
+    inputs = W.make_inputs(wl, n=20)
+    sched = [0.5, 1.5, 0.0, 2.0, 0.25]
+    st = DPStep(wl, inputs, DEV, sigma_schedule=sched)
+    say("graph with a noise schedule, parallel", parallel)
+    st.capture(first_step=1, parallel=parallel, steps_per_replay=3)
+    eager = DPStep(wl, inputs, DEV, sigma_schedule=sched)
+    for k in range(3):
+        st.replay()
+        got = st.results()
+        eager.run(step=1 + 3 * k + 2)
+        ref = eager.results()
+        for name in ref["out"]:
+            np.testing.assert_array_equal(got["out"][name], ref["out"][name], err_msg="replay %d %s" % (k, name))
+    assert got["status"] == 0
+
+
+def test_noise_schedule_bad_entry_raises_the_flag():
+    """A negative schedule entry raises DP_FLAG_NONFINITE for that step and
+    leaves NaN outputs; the steps before it are unaffected."""
+    wl = W.get("linear_tiny")
+    inputs = W.make_inputs(wl)
+    st = DPStep(wl, inputs, DEV, sigma_schedule=[0.5, -1.0])
+    st.run(step=0)
+    ok = st.results()
+    assert ok["status"] == 0
+    st.run(step=1)
+    bad = st.results()
+    assert bad["status"] & dp.DP_FLAG_NONFINITE
+    assert all(np.isnan(v).all() for v in bad["out"].values())
+
+
 @pytest.mark.parametrize("N", [0, 5, 40, 300, 4100])
 def test_norms_clip_noise_one_launch_matches_two_launch_path(N):
     """dp_norms_clip_noise (norms, column reduce and finish in one launch)
