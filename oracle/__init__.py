@@ -54,6 +54,7 @@ def lib():
         L.dpo_embedding.argtypes = [_i64, _d, _L, _L, _L, _L, ctypes.c_double, _i64, _i64, _d, _L]
         L.dpo_embedding.restype = _L
         L.dpo_layernorm.argtypes = [_d, _d, _L, _L, _L, ctypes.c_double, _d, _d]
+        L.dpo_groupnorm.argtypes = [_d, _d, _L, _L, _L, ctypes.c_double, _d, _d]
         L.dpo_sqnorm_accumulate.argtypes = [_d, _L, _L, _d]
         L.dpo_norms.argtypes = [_d, _L, _d]
         L.dpo_clip_factors.argtypes = [_d, _L, ctypes.c_double, _d]
@@ -136,6 +137,18 @@ def layernorm_grad(xhat, B, scale: float = 1.0):
     N, T, D = B.shape
     gg = np.empty((N, D)); gbt = np.empty((N, D))
     lib().dpo_layernorm(_p(xhat), _p(B), N, T, D, float(scale), _p(gg), _p(gbt))
+    return gg, gbt
+
+
+def groupnorm_grad(xhat, B, scale: float = 1.0):
+    """Per-sample GroupNorm / InstanceNorm affine grads from the normalized
+    input: (ggamma [N, C], gbeta [N, C]); xhat and B are [N, C, *spatial]."""
+    xhat = _f64(xhat); B = _f64(B)
+    N, C = B.shape[0], B.shape[1]
+    P = int(np.prod(B.shape[2:])) if B.ndim > 2 else 1
+    xhat = np.ascontiguousarray(xhat.reshape(N, C, P)); B = np.ascontiguousarray(B.reshape(N, C, P))
+    gg = np.empty((N, C)); gbt = np.empty((N, C))
+    lib().dpo_groupnorm(_p(xhat), _p(B), N, C, P, float(scale), _p(gg), _p(gbt))
     return gg, gbt
 
 

@@ -183,6 +183,27 @@ void dpo_layernorm(const double *xhat, const double *B, long N, long T, long D,
     }
 }
 
+/* GroupNorm's / InstanceNorm's per-channel affine y = gamma[c] * xhat + beta[c]
+ * over the channel's P spatial positions: dl_n/dgamma[c] = sum_p B[n][c][p] *
+ * xhat[n][c][p], dl_n/dbeta[c] = sum_p B[n][c][p].                          */
+void dpo_groupnorm(const double *xhat, const double *B, long N, long C, long P,
+                   double s, double *ggamma, double *gbeta)
+{
+#pragma omp parallel for schedule(static)
+    for (long n = 0; n < N; n++) {
+        for (long c = 0; c < C; c++) {
+            double ag = 0.0, ab = 0.0;
+            for (long p = 0; p < P; p++) {
+                double b = B[(n * C + c) * P + p];
+                ag += b * xhat[(n * C + c) * P + p];
+                ab += b;
+            }
+            ggamma[n * C + c] = s * ag;
+            gbeta[n * C + c] = s * ab;
+        }
+    }
+}
+
 /* ---------------------------------------------------------------------------
  * Norms, clipping, clipped sum (the DP-SGD step of section 1, figure 1)
  * ------------------------------------------------------------------------- */

@@ -262,6 +262,45 @@ def test_layernorm_bruteforce_and_autograd():
         np.testing.assert_allclose(b.grad.numpy(), gbt[n], rtol=1e-12)
 
 
+# ---------------------------------------------------------------- groupnorm / instancenorm
+
+def test_groupnorm_and_instancenorm_against_autograd():
+    """The oracle's per-sample affine grads from the normalized input equal
+    autograd of torch's group_norm / instance_norm (fp64) for each sample,
+    with the affine applied after normalizing within the sample."""
+    import torch.nn.functional as F
+    r = rng(61)
+    N, C, H, Wd, G, s = 3, 6, 4, 5, 2, 0.7
+    x = r.standard_normal((N, C, H, Wd)); B = r.standard_normal((N, C, H, Wd))
+    gamma = r.standard_normal(C); beta = r.standard_normal(C)
+    xt = torch.from_numpy(x)
+    for kind in ("group", "instance"):
+        xhat = (F.group_norm(xt, G, eps=1e-5) if kind == "group" else F.instance_norm(xt, eps=1e-5)).numpy()
+        gg, gbt = oracle.groupnorm_grad(xhat, B, s)
+        for n in range(N):
+            g = torch.tensor(gamma, requires_grad=True); b = torch.tensor(beta, requires_grad=True)
+            xn = xt[n:n + 1]
+            y = F.group_norm(xn, G, g, b, eps=1e-5) if kind == "group" else F.instance_norm(xn, weight=g, bias=b,
+                                                                                             eps=1e-5)
+            (s * torch.from_numpy(B[n:n + 1]) * y).sum().backward()
+            np.testing.assert_allclose(g.grad.numpy(), gg[n], rtol=1e-10, atol=1e-12, err_msg=kind)
+            np.testing.assert_allclose(b.grad.numpy(), gbt[n], rtol=1e-10, atol=1e-12, err_msg=kind)
+
+
+def test_groupnorm_closed_forms():
+    """B = 1 gives gbeta = s * P and ggamma = s * (sum of xhat over the
+    channel); xhat = B gives ggamma = s * |B_c|^2."""
+    r = rng(62)
+    N, C, P, s = 2, 3, 7, 1.5
+    xh = r.standard_normal((N, C, P))
+    gg, gbt = oracle.groupnorm_grad(xh, np.ones((N, C, P)), s)
+    np.testing.assert_allclose(gbt, np.full((N, C), s * P), rtol=1e-15)
+    np.testing.assert_allclose(gg, s * xh.sum(axis=2), rtol=1e-13)
+    B = r.standard_normal((N, C, P))
+    gg2, _ = oracle.groupnorm_grad(B, B, s)
+    np.testing.assert_allclose(gg2, s * (B * B).sum(axis=2), rtol=1e-13)
+
+
 # ---------------------------------------------------------------- clipping
 
 def test_clip_invariants():
