@@ -214,6 +214,23 @@ dp_status dp_grad_sample_layernorm(const void *xhat, const void *B, dp_dtype dt,
                                    float *gbeta, float *sqnorm, int32_t *status, void *ws,
                                    size_t ws_bytes, hipStream_t stream);
 
+/* GroupNorm's and InstanceNorm's per-channel affine y = gamma[c] * xhat +
+ * beta[c] over a channel's P spatial positions (normalization layers are
+ * among the predefined layer types of section "Design Principles and
+ * Features"; these two normalize within each sample, so, unlike BatchNorm,
+ * their per-sample gradients exist):
+ *   ggamma[n][c] = s * sum_p B[n][c][p] * xhat[n][c][p]
+ *   gbeta[n][c]  = s * sum_p B[n][c][p]
+ * xhat (the normalized input), B: [N][C][P] of `dt` (P = the product of the
+ * spatial sizes, contiguous); ggamma fp32 [N][C]; gbeta fp32 [N][C] or NULL
+ * (no bias); sqnorm fp32 [N] or NULL (overwritten with |ggamma_n|^2 +
+ * |gbeta_n|^2).  ws: dp_grad_sample_groupnorm_workspace_bytes(N, C, P)
+ * bytes (non-zero when C > 16), else DP_EINVAL.  Sums are deterministic. */
+size_t dp_grad_sample_groupnorm_workspace_bytes(int64_t N, int64_t C, int64_t P);
+dp_status dp_grad_sample_groupnorm(const void *xhat, const void *B, dp_dtype dt, int64_t N, int64_t C,
+                                   int64_t P, float scale, float *ggamma, float *gbeta, float *sqnorm,
+                                   int32_t *status, void *ws, size_t ws_bytes, hipStream_t stream);
+
 /* ---------------------------------------------------------------------------
  * Norms and clipping
  * ------------------------------------------------------------------------- */

@@ -47,6 +47,8 @@ SIGNATURES = {
                                        _P, _P, _SZ, _P]),
     "dp_grad_sample_layernorm_workspace_bytes": (_SZ, [_I64, _I64, _I64]),
     "dp_grad_sample_layernorm": (_ST, [_P, _P, _ST, _I64, _I64, _I64, _F, _P, _P, _P, _P, _P, _SZ, _P]),
+    "dp_grad_sample_groupnorm_workspace_bytes": (_SZ, [_I64, _I64, _I64]),
+    "dp_grad_sample_groupnorm": (_ST, [_P, _P, _ST, _I64, _I64, _I64, _F, _P, _P, _P, _P, _P, _SZ, _P]),
     "dp_per_sample_norms": (_ST, [_P, _I32, _I64, _P, _P, _P]),
     "dp_ghost_norm_linear_workspace_bytes": (_SZ, [_I64, _I64, _I64, _I64]),
     "dp_ghost_norm_linear": (_ST, [_P, _P, _ST, _I64, _I64, _I64, _I64, _F, _I32, _P, _P, _P, _SZ, _P]),
@@ -306,6 +308,18 @@ def dp_grad_sample_layernorm(xhat, B, dt, N, T, D, scale, ggamma, gbeta, sqnorm=
                                           _ptr(sqnorm), _ptr(status), _ptr(ws), _nbytes(ws),
                                           _stream(stream)),
            "dp_grad_sample_layernorm")
+
+
+def dp_grad_sample_groupnorm_workspace_bytes(N, C, P) -> int:
+    return lib().dp_grad_sample_groupnorm_workspace_bytes(N, C, P)
+
+
+def dp_grad_sample_groupnorm(xhat, B, dt, N, C, P, scale, ggamma, gbeta=None, sqnorm=None, status=None, ws=None,
+                             stream=None):
+    _check(lib().dp_grad_sample_groupnorm(_ptr(xhat), _ptr(B), dt, N, C, P, scale, _ptr(ggamma), _ptr(gbeta),
+                                          _ptr(sqnorm), _ptr(status), _ptr(ws), _nbytes(ws),
+                                          _stream(stream)),
+           "dp_grad_sample_groupnorm")
 
 
 # ---------------------------------------------------------------------------

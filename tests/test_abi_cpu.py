@@ -119,6 +119,21 @@ def test_clip_and_noise_validation():
     assert code_of(dp.dp_grad_sample_linear, None, None, dp.DP_F32, 0, 3, 4, 5, 1.0, None, stream=0) == dp.DP_OK
 
 
+def test_groupnorm_validation_and_workspace():
+    """dp_grad_sample_groupnorm: workspace only for several channel blocks;
+    bad sizes, a missing output or workspace are refused before any launch."""
+    assert dp.dp_grad_sample_groupnorm_workspace_bytes(4, 16, 64) == 0
+    assert dp.dp_grad_sample_groupnorm_workspace_bytes(4, 17, 64) == 4 * 2 * 4
+    assert dp.dp_grad_sample_groupnorm_workspace_bytes(0, 17, 64) == 0
+    f = dp.dp_grad_sample_groupnorm
+    assert code_of(f, FAKE, FAKE, dp.DP_F32, 2, 0, 8, 1.0, FAKE, stream=0) == dp.DP_EINVAL       # C = 0
+    assert code_of(f, FAKE, FAKE, dp.DP_F32, 2, 3, -1, 1.0, FAKE, stream=0) == dp.DP_EINVAL      # P < 0
+    assert code_of(f, FAKE, FAKE, dp.DP_F32, 2, 3, 8, 1.0, None, stream=0) == dp.DP_EINVAL       # no ggamma
+    assert code_of(f, None, FAKE, dp.DP_F32, 2, 3, 8, 1.0, FAKE, stream=0) == dp.DP_EINVAL       # no xhat
+    assert code_of(f, FAKE, FAKE, 7, 2, 3, 8, 1.0, FAKE, stream=0) == dp.DP_EDTYPE
+    assert code_of(f, FAKE, FAKE, dp.DP_F32, 2, 40, 8, 1.0, FAKE, FAKE, FAKE, stream=0) == dp.DP_EINVAL  # ws
+
+
 def test_noise_schedule_validation():
     """dp_norms_clip_noise_sched refuses a missing table, an empty one and an
     infinite C (a schedule may hold positive entries), and a zero
