@@ -117,6 +117,10 @@ def call_costs(st):
             out["grad:" + L.name] = (2 * N * L.T * L.D * e + 2 * N * L.D * 4, 3 * N * L.T * L.D,
                                      "ln_partial_kernel", None)
             col_bytes += 2 * N * L.D * 4
+        elif isinstance(L, W.GroupNorm):
+            out["grad:" + L.name] = (2 * N * L.C * L.P * e + 2 * N * L.C * 4 + N * 4, 3 * N * L.C * L.P,
+                                     "gn_affine_kernel", None)
+            col_bytes += 2 * N * L.C * 4
     if st.grad_group:
         # the grouped layers' per-sample gradients are one launch
         gb_, gf_ = 0, 0
@@ -147,6 +151,7 @@ def src_hash(paths):
 KERNEL_SOURCES = {
     "outer_kernel": ["paper_2109_12298_amd/csrc/linear.hip", "paper_2109_12298_amd/csrc/linear_outer.hpp"],
     "ghost_norm_kernel": ["paper_2109_12298_amd/csrc/ghost.hip"],
+    "gn_affine_kernel": ["paper_2109_12298_amd/csrc/groupnorm.hip"],
     "conv_rows_kernel": ["paper_2109_12298_amd/csrc/conv2d_rows.hip"],
     "conv_small_kernel": ["paper_2109_12298_amd/csrc/conv2d_small.hip",
                           "paper_2109_12298_amd/csrc/conv2d_small_dev.hpp"],

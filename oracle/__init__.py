@@ -242,6 +242,9 @@ def layer_grads(layer, li, scale: float) -> Dict[str, object]:
     if isinstance(layer, W.LayerNorm):
         gg, gbt = layernorm_grad(li.A, li.B, scale)
         return {"weight": gg, "bias": gbt}
+    if isinstance(layer, W.GroupNorm):
+        gg, gbt = groupnorm_grad(li.A, li.B, scale)
+        return {"weight": gg, "bias": gbt}
     raise TypeError(layer)
 
 

@@ -7,8 +7,9 @@
 //   gbeta_n[c]  = s * sum_p B[n][c][p]
 // over the channel's P spatial positions, which are contiguous in memory.
 // A wave reduces one channel at a time (lanes over the positions, 16-byte
-// loads when the rows allow, then a fixed tree), so the sums are
-// deterministic; a workgroup takes 16 channels of one sample, and the
+// loads when the rows allow, then a fixed tree), or, for planes of at most 64
+// positions, four channels at a time on 16 lanes each; the sums are
+// deterministic.  A workgroup takes 16 channels of one sample, and the
 // sample's squared norm is added over its channel blocks in block order.
 #include "common.hpp"
 
@@ -36,8 +37,20 @@ __device__ __forceinline__ float4 ld4<uint16_t>(const uint16_t *p)
                        __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u));
 }
 
-// VEC: P % 4 == 0 and 16-byte (fp32) / 8-byte (bf16) aligned rows
-template <typename T, bool VEC>
+// sum over the LPC lanes of a segment (a fixed butterfly; every lane of the
+// segment ends with the sum)
+template <int LPC>
+__device__ __forceinline__ float seg_sum(float v)
+{
+    if constexpr (LPC == 64) return wave_sum(v);
+#pragma unroll
+    for (int o = LPC / 2; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    return v;
+}
+
+// VEC: P % 4 == 0 and 16-byte (fp32) / 8-byte (bf16) aligned rows.
+// LPC: lanes per channel (64, or 16 for planes of at most 64 positions)
+template <typename T, bool VEC, int LPC>
 __global__ __launch_bounds__(kThreads) void gn_affine_kernel(const T *__restrict__ xh, const T *__restrict__ B,
                                                              i64 C, i64 P, int cblocks, float scale,
                                                              float *__restrict__ gg, float *__restrict__ gbt,
@@ -48,35 +61,40 @@ __global__ __launch_bounds__(kThreads) void gn_affine_kernel(const T *__restrict
     const int cb = (int)(blockIdx.x % cblocks);
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
+    constexpr int SEGS = 64 / LPC;                 // channels a wave takes at once
+    const int seg = lane / LPC, sl = lane % LPC;
     float sq = 0.0f;
-    for (int k = wave; k < kChanPerBlock; k += kWaves) {
-        const i64 c = (i64)cb * kChanPerBlock + k;
-        if (c >= C) break;
-        const T *x = xh + (n * C + c) * P;
-        const T *b = B + (n * C + c) * P;
+    for (int k = wave * SEGS; k < kChanPerBlock; k += kWaves * SEGS) {
+        const i64 c = (i64)cb * kChanPerBlock + k + seg;
+        const bool live = c < C;
+        const T *x = xh + (n * C + (live ? c : 0)) * P;
+        const T *b = B + (n * C + (live ? c : 0)) * P;
         float ag = 0.0f, ab = 0.0f;
-        if (VEC) {
-            for (i64 p = 4 * lane; p < P; p += 256) {
-                const float4 bv = ld4<T>(b + p), xv = ld4<T>(x + p);
-                ag += bv.x * xv.x + bv.y * xv.y + bv.z * xv.z + bv.w * xv.w;
-                ab += bv.x + bv.y + bv.z + bv.w;
-            }
-        } else {
-            for (i64 p = lane; p < P; p += 64) {
-                const float bv = load_elem<T>(b, p);
-                ag += bv * load_elem<T>(x, p);
-                ab += bv;
+        if (live) {
+            if (VEC) {
+                for (i64 p = 4 * sl; p < P; p += 4 * LPC) {
+                    const float4 bv = ld4<T>(b + p), xv = ld4<T>(x + p);
+                    ag += bv.x * xv.x + bv.y * xv.y + bv.z * xv.z + bv.w * xv.w;
+                    ab += bv.x + bv.y + bv.z + bv.w;
+                }
+            } else {
+                for (i64 p = sl; p < P; p += LPC) {
+                    const float bv = load_elem<T>(b, p);
+                    ag += bv * load_elem<T>(x, p);
+                    ab += bv;
+                }
             }
         }
-        ag = wave_sum(ag);
-        ab = wave_sum(ab);
-        if (lane == 0) {
+        ag = seg_sum<LPC>(ag);
+        ab = seg_sum<LPC>(ab);
+        if (live && sl == 0) {
             const float g = scale * ag, e = scale * ab;
             gg[n * C + c] = g;
             if (gbt) gbt[n * C + c] = e;
             sq += g * g + (gbt ? e * e : 0.0f);
         }
     }
+    sq = wave_sum(sq);                             // the segments' shares (one lane each), in a fixed order
     if (lane == 0) red[wave] = sq;
     __syncthreads();
     if (threadIdx.x == 0 && sqout) {
@@ -86,6 +104,23 @@ __global__ __launch_bounds__(kThreads) void gn_affine_kernel(const T *__restrict
         if (direct) sqout[n] = t;
         else sqout[n * cblocks + cb] = t;
     }
+}
+
+template <typename T>
+void launch_gn(bool vec, bool narrow, dim3 grid, const void *xh, const void *B, i64 C, i64 P, int cblocks,
+               float scale, float *gg, float *gbt, float *sqout, int direct, hipStream_t stream)
+{
+    const T *x = (const T *)xh, *b = (const T *)B;
+    if (vec && narrow)
+        gn_affine_kernel<T, true, 16><<<grid, kThreads, 0, stream>>>(x, b, C, P, cblocks, scale, gg, gbt, sqout, direct);
+    else if (vec)
+        gn_affine_kernel<T, true, 64><<<grid, kThreads, 0, stream>>>(x, b, C, P, cblocks, scale, gg, gbt, sqout, direct);
+    else if (narrow)
+        gn_affine_kernel<T, false, 16><<<grid, kThreads, 0, stream>>>(x, b, C, P, cblocks, scale, gg, gbt, sqout,
+                                                                      direct);
+    else
+        gn_affine_kernel<T, false, 64><<<grid, kThreads, 0, stream>>>(x, b, C, P, cblocks, scale, gg, gbt, sqout,
+                                                                      direct);
 }
 
 }  // namespace
@@ -119,21 +154,10 @@ extern "C" dp_status dp_grad_sample_groupnorm(const void *xhat, const void *B, d
     const dim3 grid((unsigned)(N * cblocks));
     const bool bf = dt == DP_BF16;
     const bool vec = P % 4 == 0 && aligned(xhat, bf ? 8 : 16) && aligned(B, bf ? 8 : 16);
-    if (bf) {
-        if (vec)
-            gn_affine_kernel<uint16_t, true><<<grid, kThreads, 0, stream>>>(
-                (const uint16_t *)xhat, (const uint16_t *)B, C, P, cblocks, scale, ggamma, gbeta, sqout, direct);
-        else
-            gn_affine_kernel<uint16_t, false><<<grid, kThreads, 0, stream>>>(
-                (const uint16_t *)xhat, (const uint16_t *)B, C, P, cblocks, scale, ggamma, gbeta, sqout, direct);
-    } else {
-        if (vec)
-            gn_affine_kernel<float, true><<<grid, kThreads, 0, stream>>>(
-                (const float *)xhat, (const float *)B, C, P, cblocks, scale, ggamma, gbeta, sqout, direct);
-        else
-            gn_affine_kernel<float, false><<<grid, kThreads, 0, stream>>>(
-                (const float *)xhat, (const float *)B, C, P, cblocks, scale, ggamma, gbeta, sqout, direct);
-    }
+    const bool narrow = P <= 64;                   // four channels per wave, 16 lanes each
+    if (bf) launch_gn<uint16_t>(vec, narrow, grid, xhat, B, C, P, cblocks, scale, ggamma, gbeta, sqout, direct,
+                                stream);
+    else launch_gn<float>(vec, narrow, grid, xhat, B, C, P, cblocks, scale, ggamma, gbeta, sqout, direct, stream);
     if (sqnorm && !direct) sum_partials((const float *)ws, N, cblocks, sqnorm, stream);
     return launch_status();
 }

@@ -169,6 +169,10 @@ class DPStep:
                 lb.gW = torch.empty((N, layer.D), **f32)
                 lb.gb = torch.empty((N, layer.D), **f32)
                 need_g = dp.dp_grad_sample_layernorm_workspace_bytes(N, layer.T, layer.D)
+            elif isinstance(layer, W.GroupNorm):
+                lb.gW = torch.empty((N, layer.C), **f32)
+                lb.gb = torch.empty((N, layer.C), **f32)
+                need_g = dp.dp_grad_sample_groupnorm_workspace_bytes(N, layer.C, layer.P)
             # each layer has its own scratch, so its calls may run concurrently with other layers'
             lb.ws = torch.empty(max(need_g, 256), dtype=torch.uint8, device=self.device)
             lb.ws_clip = torch.empty(max(need_c, 256), dtype=torch.uint8, device=self.device)
@@ -298,6 +302,9 @@ class DPStep:
                                         lb.uniq, lb.rows, N * layer.T, sq, self.status, lb.ws, stream)
         elif isinstance(layer, W.LayerNorm):
             dp.dp_grad_sample_layernorm(lb.A, lb.B, self.dt, N, layer.T, layer.D, s, lb.gW, lb.gb, sq,
+                                        self.status, lb.ws, stream)
+        elif isinstance(layer, W.GroupNorm):
+            dp.dp_grad_sample_groupnorm(lb.A, lb.B, self.dt, N, layer.C, layer.P, s, lb.gW, lb.gb, sq,
                                         self.status, lb.ws, stream)
 
     def norms(self, stream=None):

@@ -104,6 +104,18 @@ class LayerNorm:
 
 
 @dataclass(frozen=True)
+class GroupNorm:
+    """GroupNorm's (or InstanceNorm's) per-channel affine y = g[c] * xhat + b[c]
+    over C channels of P spatial positions each."""
+    name: str
+    C: int
+    P: int
+    @property
+    def n_params(self) -> int:
+        return 2 * self.C
+
+
+@dataclass(frozen=True)
 class Workload:
     wid: int
     name: str
@@ -137,6 +149,9 @@ class Workload:
             elif isinstance(l, LayerNorm):
                 out.append((l.name + ".weight", (l.D,)))
                 out.append((l.name + ".bias", (l.D,)))
+            elif isinstance(l, GroupNorm):
+                out.append((l.name + ".weight", (l.C,)))
+                out.append((l.name + ".bias", (l.C,)))
         return out
 
 
@@ -179,11 +194,22 @@ def _build_workloads() -> Dict[str, Workload]:
                 LayerNorm("ln1", 768, 128),
                 Linear("ffn1", 768, 3072, T=128), Linear("ffn2", 3072, 768, T=128),
                 LayerNorm("ln2", 768, 128)))
+    # The CIFAR-shaped CNN with a GroupNorm after each convolution (the
+    # normalization layers Opacus supports per sample), batch 512.
+    w["cifar_gn"] = Workload(
+        5, "cifar_gn", N=512, dtype=F32, C=1.5, sigma=1.5,
+        layers=(Conv2d("c1", 3, 32, 32, 32, (3, 3), (1, 1), (1, 1)), GroupNorm("g1", 32, 1024),
+                Conv2d("c2", 32, 64, 32, 32, (3, 3), (1, 1), (1, 1)), GroupNorm("g2", 64, 1024),
+                Conv2d("c3", 64, 64, 16, 16, (3, 3), (1, 1), (1, 1)), GroupNorm("g3", 64, 256),
+                Conv2d("c4", 64, 128, 16, 16, (3, 3), (1, 1), (1, 1)), GroupNorm("g4", 128, 256),
+                Conv2d("c5", 128, 128, 8, 8, (3, 3), (1, 1), (1, 1)), GroupNorm("g5", 128, 64),
+                Conv2d("c6", 128, 256, 8, 8, (3, 3), (1, 1), (1, 1)), GroupNorm("g6", 256, 64),
+                Linear("fc", 4096, 10, act="relu")))
     return w
 
 
 WORKLOADS: Dict[str, Workload] = _build_workloads()
-WORKLOAD_ORDER = ["linear_tiny", "mnist_cnn", "cifar_cnn", "text_lstm", "transformer_block"]
+WORKLOAD_ORDER = ["linear_tiny", "mnist_cnn", "cifar_cnn", "text_lstm", "transformer_block", "cifar_gn"]
 
 
 def get(name: str) -> Workload:
@@ -283,6 +309,12 @@ def make_inputs(wl: Workload, n: Optional[int] = None) -> List[LayerInputs]:
             rB = _rng(wl.wid, tid); tid += 1
             li.A = _normal(rA, (N, layer.T, layer.D))
             li.B = _normal(rB, (N, layer.T, layer.D)) / np.float32(wl.N)
+        elif isinstance(layer, GroupNorm):
+            # A: the normalized input xhat [N, C, P]
+            rA = _rng(wl.wid, tid); tid += 1
+            rB = _rng(wl.wid, tid); tid += 1
+            li.A = _normal(rA, (N, layer.C, layer.P))
+            li.B = _normal(rB, (N, layer.C, layer.P)) / np.float32(wl.N)
         else:
             raise TypeError(layer)
         out.append(li)

@@ -46,7 +46,7 @@ def compare_step(wl, inputs, got, ref, rtol, what):
 
 
 SMALL = [("linear_tiny", None), ("mnist_cnn", None), ("cifar_cnn", 3), ("text_lstm", 5),
-         ("transformer_block", 2)]
+         ("transformer_block", 2), ("cifar_gn", 3)]
 
 
 @pytest.mark.parametrize("name,n", SMALL)
