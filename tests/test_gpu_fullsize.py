@@ -70,6 +70,10 @@ def element_grads(wl, li, key, index, scale):
         (k,) = index
         gg, gbt = oracle.layernorm_grad(A[:, :, k:k + 1], B[:, :, k:k + 1], scale)
         return (gg if key == "weight" else gbt)[:, 0]
+    if isinstance(layer, W.GroupNorm):
+        (c,) = index
+        gg, gbt = oracle.groupnorm_grad(A[:, c:c + 1], B[:, c:c + 1], scale)
+        return (gg if key == "weight" else gbt)[:, 0]
     if isinstance(layer, W.Embedding):
         v, d = index
         N = li.ids.shape[0]
@@ -81,7 +85,8 @@ def element_grads(wl, li, key, index, scale):
     raise TypeError(layer)
 
 
-@pytest.mark.parametrize("name", ["linear_tiny", "mnist_cnn", "cifar_cnn", "text_lstm", "transformer_block"])
+@pytest.mark.parametrize("name", ["linear_tiny", "mnist_cnn", "cifar_cnn", "text_lstm", "transformer_block",
+                                  "cifar_gn"])
 def test_full_size_sampled_parity(name):
     wl = W.get(name)
     rtol = RTOL[wl.dtype]
