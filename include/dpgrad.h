@@ -242,6 +242,19 @@ dp_status dp_grad_sample_groupnorm(const void *xhat, const void *B, dp_dtype dt,
 dp_status dp_per_sample_norms(const float *sqnorm, int32_t n_layers, int64_t N, float *norm,
                               int32_t *status, hipStream_t stream);
 
+/* dp_per_sample_norms over a batch of variable size held in N rows (section
+ * "Design Principles and Features": with Poisson sampling the batch size
+ * changes from step to step).  n_active: one int64 in device memory, read
+ * while the launch runs, so a captured graph follows it from replay to
+ * replay; rows n >= *n_active are padding and get norm[n] = -1 with no flag.
+ * Every clip factor of this library is 0 for a negative norm, so padding rows
+ * add nothing to any clipped sum that takes these norms (their per-sample
+ * gradients must still be finite: 0 times a non-finite value is NaN).
+ * n_active NULL: every row is active, as dp_per_sample_norms. */
+dp_status dp_per_sample_norms_active(const float *sqnorm, int32_t n_layers, int64_t N,
+                                     const int64_t *n_active, float *norm, int32_t *status,
+                                     hipStream_t stream);
+
 /* Ghost norm of a Linear layer: its per-sample squared gradient norm without
  * forming the per-sample gradient.  The related-work section ("Gradient
  * Clipping") describes computing only each sample's gradient norm (exact for
@@ -268,7 +281,9 @@ dp_status dp_sqnorm_from_grads(const float *G, int64_t N, int64_t numel, float *
 
 /* Clip factors c[n] = min(1, C / (norm[n] + 1e-6)), computed in fp32.
  * C = +inf gives 1; a NaN or infinite norm gives NaN (and DP_FLAG_NONFINITE)
- * so a broken sample poisons the sum rather than passing unclipped.
+ * so a broken sample poisons the sum rather than passing unclipped.  A
+ * negative norm (a padding row, see dp_per_sample_norms_active) gives 0; the
+ * same rule holds wherever a clipped sum takes norms.
  * C must be > 0 (else DP_EINVAL). */
 dp_status dp_clip_factors(const float *norm, int64_t N, float C, float *c, int32_t *status,
                           hipStream_t stream);
@@ -412,14 +427,19 @@ dp_status dp_norms_clip_noise(const float *sqnorm, int32_t n_layers, const dp_pa
  * floats in device memory, owned by the caller and read while the launch
  * runs; each entry must be finite and >= 0 (an entry that is not raises
  * DP_FLAG_NONFINITE in *status and turns that step's noised outputs to NaN).
- * A NULL table, table_len < 1 or an infinite C returns DP_EINVAL.  Everything else is as dp_norms_clip_noise; with a table
- * of one entry s it gives the same results as dp_norms_clip_noise with sigma
- * = s. */
+ * A NULL table, table_len < 1 or an infinite C returns DP_EINVAL.
+ * n_active (device int64, may be NULL): the batch of variable size of
+ * dp_per_sample_norms_active; rows n >= *n_active (clamped to [0, N]) are
+ * left out of every column sum (they are not read), and, with sqnorm given,
+ * get norm[n] = -1; the sample ranges are still those of N rows, so a sum
+ * matches a call with N = *n_active to rounding.  Everything else is as
+ * dp_norms_clip_noise; with a table of one entry s and n_active NULL it
+ * gives the same results as dp_norms_clip_noise with sigma = s. */
 dp_status dp_norms_clip_noise_sched(const float *sqnorm, int32_t n_layers, const dp_param *params,
                                     int32_t count, int64_t N, float *norm, float C, uint64_t seed,
                                     uint64_t step, const uint64_t *step_dev, const float *sigma_table,
-                                    int64_t table_len, float denom, int32_t *status, void *ws,
-                                    size_t ws_bytes, hipStream_t stream);
+                                    int64_t table_len, const int64_t *n_active, float denom,
+                                    int32_t *status, void *ws, size_t ws_bytes, hipStream_t stream);
 
 /* *step_dev += by, on the device (one tiny kernel): advances the step counter
  * a captured graph reads through dp_clip_noise_many. */

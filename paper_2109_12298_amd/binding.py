@@ -50,6 +50,7 @@ SIGNATURES = {
     "dp_grad_sample_groupnorm_workspace_bytes": (_SZ, [_I64, _I64, _I64]),
     "dp_grad_sample_groupnorm": (_ST, [_P, _P, _ST, _I64, _I64, _I64, _F, _P, _P, _P, _P, _P, _SZ, _P]),
     "dp_per_sample_norms": (_ST, [_P, _I32, _I64, _P, _P, _P]),
+    "dp_per_sample_norms_active": (_ST, [_P, _I32, _I64, _P, _P, _P, _P]),
     "dp_ghost_norm_linear_workspace_bytes": (_SZ, [_I64, _I64, _I64, _I64]),
     "dp_ghost_norm_linear": (_ST, [_P, _P, _ST, _I64, _I64, _I64, _I64, _F, _I32, _P, _P, _P, _SZ, _P]),
     "dp_sqnorm_from_grads": (_ST, [_P, _I64, _I64, _P, _P, _P]),
@@ -67,8 +68,8 @@ SIGNATURES = {
     "dp_clip_noise_many": (_ST, [_P, _I32, _I64, _P, _F, _U64, _U64, _P, _F, _F, _P, _P, _SZ, _P]),
     "dp_norms_clip_noise_workspace_bytes": (_SZ, [_P, _I32, _I64]),
     "dp_norms_clip_noise": (_ST, [_P, _I32, _P, _I32, _I64, _P, _F, _U64, _U64, _P, _F, _F, _P, _P, _SZ, _P]),
-    "dp_norms_clip_noise_sched": (_ST, [_P, _I32, _P, _I32, _I64, _P, _F, _U64, _U64, _P, _P, _I64, _F, _P, _P, _SZ,
-                                        _P]),
+    "dp_norms_clip_noise_sched": (_ST, [_P, _I32, _P, _I32, _I64, _P, _F, _U64, _U64, _P, _P, _I64, _P, _F, _P, _P,
+                                        _SZ, _P]),
     "dp_step_advance": (_ST, [_P, _U64, _P]),
     "dp_add_noise": (_ST, [_P, _P, _I64, _U64, _U64, _U32, _F, _F, _F, _P, _P]),
     "dp_philox_normals": (_ST, [_P, _P, _I64, _U64, _U64, _U32, _P]),
@@ -331,6 +332,11 @@ def dp_per_sample_norms(sqnorm, n_layers, N, norm, status=None, stream=None):
            "dp_per_sample_norms")
 
 
+def dp_per_sample_norms_active(sqnorm, n_layers, N, n_active, norm, status=None, stream=None):
+    _check(lib().dp_per_sample_norms_active(_ptr(sqnorm), n_layers, N, _ptr(n_active), _ptr(norm), _ptr(status),
+                                            _stream(stream)), "dp_per_sample_norms_active")
+
+
 def dp_sqnorm_from_grads(G, N, numel, sqnorm, status=None, stream=None):
     _check(lib().dp_sqnorm_from_grads(_ptr(G), N, numel, _ptr(sqnorm), _ptr(status), _stream(stream)),
            "dp_sqnorm_from_grads")
@@ -438,13 +444,14 @@ def dp_norms_clip_noise(sqnorm, n_layers, params, count, N, norm, C, seed, step,
 
 
 def dp_norms_clip_noise_sched(sqnorm, n_layers, params, count, N, norm, C, seed, step, step_dev, sigma_table,
-                              denom, status=None, ws=None, stream=None):
+                              denom, status=None, ws=None, stream=None, n_active=None):
     """dp_norms_clip_noise with the noise multiplier of step t read from
-    sigma_table[min(t, len - 1)] (a device float tensor) on the device."""
+    sigma_table[min(t, len - 1)] (a device float tensor) on the device, and
+    optionally the active batch size from n_active (a device int64)."""
     _check(lib().dp_norms_clip_noise_sched(_ptr(sqnorm), n_layers, ctypes.cast(params, ctypes.c_void_p), count, N,
                                            _ptr(norm), C, seed, step, _ptr(step_dev), _ptr(sigma_table),
-                                           _numel(sigma_table), denom, _ptr(status), _ptr(ws), _nbytes(ws),
-                                           _stream(stream)),
+                                           _numel(sigma_table), _ptr(n_active), denom, _ptr(status), _ptr(ws),
+                                           _nbytes(ws), _stream(stream)),
            "dp_norms_clip_noise_sched")
 
 

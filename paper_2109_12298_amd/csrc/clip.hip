@@ -13,11 +13,17 @@ namespace {
 
 constexpr int kThreads = 256;
 
-__global__ void norms_kernel(const float *__restrict__ sq, int L, i64 N, float *__restrict__ norm,
-                             int32_t *status)
+// n_active (device, may be null): samples n >= *n_active are outside the
+// batch and get the norm -1 (clip factor 0), without a flag.
+__global__ void norms_kernel(const float *__restrict__ sq, int L, i64 N, const int64_t *n_active,
+                             float *__restrict__ norm, int32_t *status)
 {
     const i64 n = (i64)blockIdx.x * blockDim.x + threadIdx.x;
     if (n >= N) return;
+    if (n_active && n >= *n_active) {
+        norm[n] = -1.0f;
+        return;
+    }
     float s = 0.0f;
     s = ordered_sum(sq + n, N, L);
     const float r = sqrtf(s);
@@ -243,7 +249,18 @@ extern "C" dp_status dp_per_sample_norms(const float *sqnorm, int32_t n_layers, 
     DPG_REQUIRE(n_layers >= 0 && N >= 0, DP_EINVAL);
     DPG_REQUIRE(N == 0 || (norm != nullptr && (n_layers == 0 || sqnorm != nullptr)), DP_EINVAL);
     if (N == 0) return DP_OK;
-    norms_kernel<<<(unsigned)ceil_div(N, 256), 256, 0, stream>>>(sqnorm, n_layers, N, norm, status);
+    norms_kernel<<<(unsigned)ceil_div(N, 256), 256, 0, stream>>>(sqnorm, n_layers, N, nullptr, norm, status);
+    return launch_status();
+}
+
+extern "C" dp_status dp_per_sample_norms_active(const float *sqnorm, int32_t n_layers, int64_t N,
+                                                const int64_t *n_active, float *norm, int32_t *status,
+                                                hipStream_t stream)
+{
+    DPG_REQUIRE(n_layers >= 0 && N >= 0, DP_EINVAL);
+    DPG_REQUIRE(N == 0 || (norm != nullptr && (n_layers == 0 || sqnorm != nullptr)), DP_EINVAL);
+    if (N == 0) return DP_OK;
+    norms_kernel<<<(unsigned)ceil_div(N, 256), 256, 0, stream>>>(sqnorm, n_layers, N, n_active, norm, status);
     return launch_status();
 }
 

@@ -100,8 +100,11 @@ __device__ __forceinline__ void raise_flag(int32_t *status, int32_t flag)
 
 // Clip factor min(1, C / (norm + 1e-6)) in fp32; C = +inf gives 1 and a
 // non-finite norm gives NaN (never silently 1).
+// A negative norm marks a sample outside the active batch (a padded row of
+// a batch of variable size): its factor is 0, so it adds nothing.
 __device__ __forceinline__ float clip_factor(float norm, float C)
 {
+    if (norm < 0.0f) return 0.0f;
     if (!isfinite(norm)) return __builtin_nanf("");
     if (isinf(C)) return 1.0f;
     float q = C / (norm + 1e-6f);

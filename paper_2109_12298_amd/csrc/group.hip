@@ -201,6 +201,9 @@ struct FusedArgs {
     // (then sc = sigma * C and noise = sigma > 0 are taken at run time)
     const float *sigma_tab;
     i64 tab_len;
+    // active batch (device, may be null): samples n >= *n_active are padding,
+    // left out of the sums, their norms set to -1 when computed here
+    const int64_t *n_active;
     int32_t *status;
     int cblocks;               // column workgroups
     int cblk0[kMaxGroup + 1];  // first column workgroup of each tensor
@@ -282,6 +285,11 @@ __global__ __launch_bounds__(kThreads) void norms_clip_noise_kernel(GroupDesc d,
     const i64 q = (i64)(b - f.cblk0[p]) * kCols + col;
     const bool active = vec ? 4 * q < numel : q < numel;
     const i64 N = d.N;
+    i64 na = N;
+    if (f.n_active) {
+        const int64_t v = *f.n_active;
+        na = v < 0 ? 0 : (v < N ? v : N);
+    }
     const i64 per = ceil_div(N, kGroups);
     const i64 lo = grp * per < N ? grp * per : N, hi = lo + per < N ? lo + per : N;
     float acc[4] = {0.f, 0.f, 0.f, 0.f};
@@ -296,7 +304,7 @@ __global__ __launch_bounds__(kThreads) void norms_clip_noise_kernel(GroupDesc d,
             if (f.sqnorm) {
                 float sq = 0.0f;
                 for (int l = 0; l < f.L; ++l) sq += f.sqnorm[(i64)l * N + n];
-                nr = sqrtf(sq);
+                nr = n < na ? sqrtf(sq) : -1.0f;
                 if (b == 0) {
                     if (!isfinite(nr)) raise_flag(f.status, DP_FLAG_NONFINITE);
                     f.norm[n] = nr;
@@ -307,7 +315,8 @@ __global__ __launch_bounds__(kThreads) void norms_clip_noise_kernel(GroupDesc d,
             cfs[n - c0] = clip_factor(nr, f.C);
         }
         __syncthreads();
-        const i64 a0 = lo > c0 ? lo : c0, a1 = hi < c1 ? hi : c1;
+        const i64 e1 = hi < na ? hi : na;
+        const i64 a0 = lo > c0 ? lo : c0, a1 = e1 < c1 ? e1 : c1;
         if (!active || a0 >= a1) continue;
         if (vec) {
             i64 n = a0;
@@ -503,7 +512,8 @@ extern "C" size_t dp_norms_clip_noise_workspace_bytes(const dp_param *params, in
 static dp_status norms_clip_noise(const float *sqnorm, int32_t n_layers, const dp_param *params, int32_t count,
                                   int64_t N, float *norm, float C, uint64_t seed, uint64_t step,
                                   const uint64_t *step_dev, float sigma, const float *sigma_table,
-                                  int64_t table_len, float denom, int32_t *status, hipStream_t stream)
+                                  int64_t table_len, const int64_t *n_active, float denom, int32_t *status,
+                                  hipStream_t stream)
 {
     DPG_REQUIRE(count >= 0 && N >= 0, DP_EINVAL);
     DPG_REQUIRE(count == 0 || params != nullptr, DP_EINVAL);
@@ -534,6 +544,7 @@ static dp_status norms_clip_noise(const float *sqnorm, int32_t n_layers, const d
     f.noise = noise ? 1 : 0;
     f.sigma_tab = sigma_table;
     f.tab_len = table_len;
+    f.n_active = n_active;
     f.status = status;
     bool norms_done = sqnorm == nullptr || N == 0;
     for (int first = 0; first < count; first += kMaxGroup) {
@@ -587,20 +598,20 @@ extern "C" dp_status dp_norms_clip_noise(const float *sqnorm, int32_t n_layers, 
     (void)ws;
     (void)ws_bytes;
     return norms_clip_noise(sqnorm, n_layers, params, count, N, norm, C, seed, step, step_dev, sigma, nullptr, 0,
-                            denom, status, stream);
+                            nullptr, denom, status, stream);
 }
 
 extern "C" dp_status dp_norms_clip_noise_sched(const float *sqnorm, int32_t n_layers, const dp_param *params,
                                                int32_t count, int64_t N, float *norm, float C, uint64_t seed,
                                                uint64_t step, const uint64_t *step_dev, const float *sigma_table,
-                                               int64_t table_len, float denom, int32_t *status, void *ws,
-                                               size_t ws_bytes, hipStream_t stream)
+                                               int64_t table_len, const int64_t *n_active, float denom,
+                                               int32_t *status, void *ws, size_t ws_bytes, hipStream_t stream)
 {
     (void)ws;
     (void)ws_bytes;
     DPG_REQUIRE(sigma_table != nullptr, DP_EINVAL);
     return norms_clip_noise(sqnorm, n_layers, params, count, N, norm, C, seed, step, step_dev, 0.0f, sigma_table,
-                            table_len, denom, status, stream);
+                            table_len, n_active, denom, status, stream);
 }
 
 extern "C" dp_status dp_step_advance(uint64_t *step_dev, uint64_t by, hipStream_t stream)

@@ -92,7 +92,7 @@ class DPStep:
     def __init__(self, wl: W.Workload, inputs: List[W.LayerInputs], device="cuda", C=None, sigma=None,
                  denom=None, scale=None, clip_mode: str = "auto", seed: Optional[int] = None,
                  norm_mode: str = "materialize", virtual_batches: int = 1,
-                 sigma_schedule: Optional[Sequence[float]] = None):
+                 sigma_schedule: Optional[Sequence[float]] = None, variable_batch: bool = False):
         """norm_mode: 'materialize' computes every layer's per-sample gradients
         (the paper's method); 'ghost' gives a Linear layer whose clipped sum is
         fused, and for which 2 T^2 < d_in * d_out, its per-sample norm from
@@ -111,7 +111,15 @@ class DPStep:
         captured graphs follow it from replay to replay.  It replaces sigma.
         denom: the divisor of the noisy sum, e.g. the expected batch size
         q * dataset size under Poisson sampling (the default is the physical
-        batch times virtual_batches)."""
+        batch times virtual_batches).
+
+        variable_batch: the step's N rows hold a batch of variable size (the
+        Poisson-sampled batch, padded to N rows); set_active(n) sets its size
+        in device memory, so a captured graph follows it from replay to
+        replay.  Rows past it still have their per-sample gradients formed
+        (fixed shapes) but get the norm -1 and clip factor 0, and add nothing
+        to the sums; they must hold finite values.  Pass denom (the expected
+        batch size) with it."""
         torch = _torch()
         self.wl = wl
         self.device = torch.device(device)
@@ -124,6 +132,12 @@ class DPStep:
             if not sched:
                 raise ValueError("sigma_schedule needs at least one entry")
             self.sigma_tab = torch.tensor(sched, dtype=torch.float32, device=torch.device(device))
+        self.n_active = None
+        if variable_batch:
+            if self.sigma_tab is None:   # the schedule entry point carries the batch size
+                self.sigma_tab = torch.tensor([self.sigma], dtype=torch.float32, device=torch.device(device))
+            self.n_active = torch.tensor([int(inputs[0].B.shape[0])], dtype=torch.int64,
+                                         device=torch.device(device))
         self.virtual_batches = int(virtual_batches)
         if self.virtual_batches < 1:
             raise ValueError("virtual_batches must be >= 1")
@@ -308,7 +322,20 @@ class DPStep:
                                         self.status, lb.ws, stream)
 
     def norms(self, stream=None):
-        dp.dp_per_sample_norms(self.sqnorm, len(self.layers), self.N, self.norm, self.status, stream)
+        if self.n_active is not None:
+            dp.dp_per_sample_norms_active(self.sqnorm, len(self.layers), self.N, self.n_active, self.norm,
+                                          self.status, stream)
+        else:
+            dp.dp_per_sample_norms(self.sqnorm, len(self.layers), self.N, self.norm, self.status, stream)
+
+    def set_active(self, n: int):
+        """The size of the variable batch (rows 0..n-1 of the step's N), written
+        to device memory on the current stream (not inside a captured graph)."""
+        if self.n_active is None:
+            raise RuntimeError("set_active needs a DPStep built with variable_batch=True")
+        if not 0 <= int(n) <= self.N:
+            raise ValueError("active batch size %d outside [0, %d]" % (n, self.N))
+        self.n_active.fill_(int(n))
 
     def linear_clip_sums(self, stream=None):
         """The fused Linear layers' clipped sums, in one grouped call."""
@@ -334,7 +361,8 @@ class DPStep:
         if self.sigma_tab is not None:
             dp.dp_norms_clip_noise_sched(self.sqnorm if self.fold_norms else None, len(self.layers), group,
                                          self.group_count, self.N, self.norm, self.C, self.seed, step, step_dev,
-                                         self.sigma_tab, self.denom, self.status, self.ws, stream)
+                                         self.sigma_tab, self.denom, self.status, self.ws, stream,
+                                         n_active=self.n_active)
         else:
             dp.dp_norms_clip_noise(self.sqnorm if self.fold_norms else None, len(self.layers), group,
                                    self.group_count, self.N, self.norm, self.C, self.seed, step, step_dev,

@@ -139,11 +139,25 @@ def test_noise_schedule_validation():
     infinite C (a schedule may hold positive entries), and a zero
     denominator, before enqueueing anything."""
     f = dp.lib().dp_norms_clip_noise_sched
-    # (sqnorm, L, params, count, N, norm, C, seed, step, step_dev, table, len, denom, status, ws, ws_bytes, stream)
-    assert f(None, 0, None, 0, 0, None, 1.0, 0, 0, None, None, 1, 1.0, None, None, 0, None) == dp.DP_EINVAL
-    assert f(None, 0, None, 0, 0, None, 1.0, 0, 0, None, FAKE, 0, 1.0, None, None, 0, None) == dp.DP_EINVAL
-    assert f(None, 0, None, 0, 0, None, math.inf, 0, 0, None, FAKE, 3, 1.0, None, None, 0, None) == dp.DP_EINVAL
-    assert f(None, 0, None, 0, 0, None, 1.0, 0, 0, None, FAKE, 3, 0.0, None, None, 0, None) == dp.DP_EINVAL
+    # (sqnorm, L, params, count, N, norm, C, seed, step, step_dev, table, len, n_active, denom, status, ws,
+    #  ws_bytes, stream)
+    assert f(None, 0, None, 0, 0, None, 1.0, 0, 0, None, None, 1, None, 1.0, None, None, 0, None) == dp.DP_EINVAL
+    assert f(None, 0, None, 0, 0, None, 1.0, 0, 0, None, FAKE, 0, None, 1.0, None, None, 0, None) == dp.DP_EINVAL
+    assert f(None, 0, None, 0, 0, None, math.inf, 0, 0, None, FAKE, 3, FAKE, 1.0, None, None, 0,
+             None) == dp.DP_EINVAL
+    assert f(None, 0, None, 0, 0, None, 1.0, 0, 0, None, FAKE, 3, FAKE, 0.0, None, None, 0, None) == dp.DP_EINVAL
+
+
+def test_active_norms_validation():
+    """dp_per_sample_norms_active refuses a negative batch or layer count and
+    missing buffers before enqueueing anything; N = 0 is a no-op."""
+    f = dp.lib().dp_per_sample_norms_active
+    # (sqnorm, L, N, n_active, norm, status, stream)
+    assert f(FAKE, 2, -1, FAKE, FAKE, None, None) == dp.DP_EINVAL
+    assert f(FAKE, -1, 4, FAKE, FAKE, None, None) == dp.DP_EINVAL
+    assert f(FAKE, 2, 4, FAKE, None, None, None) == dp.DP_EINVAL
+    assert f(None, 2, 4, FAKE, FAKE, None, None) == dp.DP_EINVAL
+    assert f(None, 0, 0, None, None, None, None) == dp.DP_OK
 
 
 def test_clip_sum_route_choice():

@@ -671,6 +671,70 @@ def test_noise_schedule_in_a_graph_matches_eager(parallel):
     assert got["status"] == 0
 
 
+def _prefix(inputs, n):
+    return [W.LayerInputs(li.layer, None if li.A is None else li.A[:n], li.B[:n],
+                          None if li.ids is None else li.ids[:n]) for li in inputs]
+
+
+@pytest.mark.parametrize("name,nmax", [("mnist_cnn", 20), ("text_lstm", 9), ("transformer_block", 5)])
+def test_variable_batch_in_a_graph_matches_eager(name, nmax):
+    """A graph captured once on nmax rows follows the batch size set on the
+    device before each replay (Poisson sampling's variable batch): its noised
+    outputs match an eager step on just the active rows, the padding rows
+    (random, nonzero) add nothing, their norms are -1, and an empty batch
+    leaves every clipped sum zero.  Covers the norms folded into the clip
+    launch (MNIST), the embedding's and the bf16 fused clipped sums (the LSTM
+    and the transformer block take their norms first)."""
+    wl = W.get(name)
+    inputs = W.make_inputs(wl, n=nmax)
+    denom = 0.8 * nmax                        # an expected batch size q * pool
+    st = DPStep(wl, inputs, DEV, denom=denom, variable_batch=True)
+    say("variable batch in a graph", name, nmax)
+    st.capture(first_step=0, steps_per_replay=1)
+    for k, na in enumerate([nmax, nmax // 2 + 1, 0, 1, nmax - 1]):
+        st.set_active(na)
+        st.replay()
+        got = st.results()
+        assert got["status"] == 0, (k, na)
+        assert np.all(got["norm"][na:] == -1.0), (k, na)
+        if na == 0:
+            for pn, v in got["S"].items():
+                assert np.all(v == 0.0), (k, pn)
+            continue
+        eager = DPStep(wl, _prefix(inputs, na), DEV, denom=denom)
+        eager.run(step=k)
+        ref = eager.results()
+        np.testing.assert_allclose(got["norm"][:na], ref["norm"], rtol=1e-5, err_msg="norms %d" % k)
+        for pn in ref["out"]:
+            r = ref["out"][pn]
+            np.testing.assert_allclose(got["out"][pn], r, rtol=2e-4, atol=2e-5 * float(np.abs(r).max() + 1e-30),
+                                       err_msg="replay %d (batch %d) %s" % (k, na, pn))
+
+
+def test_negative_norm_gives_a_zero_clip_factor():
+    """The padding marker: dp_per_sample_norms_active writes -1 past the
+    active size (clamped to N) without a flag, and dp_clip_factors maps a
+    negative norm to 0 while a NaN norm still gives NaN and the flag."""
+    r = np.random.default_rng(5)
+    sq = torch.tensor(r.random((3, 10), dtype=np.float32), device=DEV)
+    norm = torch.empty(10, dtype=torch.float32, device=DEV)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    for na, want in [(4, 4), (0, 0), (25, 10), (-3, 0)]:
+        nd = torch.tensor([na], dtype=torch.int64, device=DEV)
+        dp.dp_per_sample_norms_active(sq, 3, 10, nd, norm, status)
+        got = norm.cpu().numpy()
+        ref = np.sqrt(sq.cpu().numpy().astype(np.float64).sum(axis=0))
+        np.testing.assert_allclose(got[:want], ref[:want], rtol=1e-6)
+        assert np.all(got[want:] == -1.0)
+    assert int(status.item()) == 0
+    nrm = torch.tensor([-1.0, 0.5, 4.0, float("nan")], device=DEV)
+    c = torch.empty(4, dtype=torch.float32, device=DEV)
+    dp.dp_clip_factors(nrm, 4, 1.0, c, status)
+    cv = c.cpu().numpy()
+    assert cv[0] == 0.0 and cv[1] == 1.0 and abs(cv[2] - 1.0 / (4.0 + 1e-6)) < 1e-7 and np.isnan(cv[3])
+    assert int(status.item()) & dp.DP_FLAG_NONFINITE
+
+
 def test_noise_schedule_bad_entry_raises_the_flag():
     """A negative schedule entry raises DP_FLAG_NONFINITE for that step and
     leaves NaN outputs; the steps before it are unaffected."""
