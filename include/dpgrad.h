@@ -404,11 +404,13 @@ dp_status dp_clip_noise_many(const dp_param *params, int32_t count, int64_t N, c
  * sqnorm[l][n]) is computed and written as dp_per_sample_norms does
  * (DP_FLAG_NONFINITE included); with sqnorm NULL, norm is an input.  Then,
  * for every tensor, the clipped sum, noise and division of
- * dp_clip_noise_many.  A workgroup reduces 64 consecutive elements of a
- * tensor over the whole batch: sixteen contiguous sample ranges, each added
- * in ascending n, then the sixteen range sums in range order, so the results
- * are deterministic (they match dp_clip_noise_many to rounding, which groups
- * the samples differently).  No workspace is needed (the size query returns
+ * dp_clip_noise_many.  A workgroup reduces a run of consecutive elements of
+ * a tensor over the whole batch: KG contiguous sample ranges, each added in
+ * ascending n, then the KG range sums in range order, so the results are
+ * deterministic (they match dp_clip_noise_many to rounding, which groups
+ * the samples differently).  KG is 4, 8 or 16, the fewest that still give
+ * 256 such workgroups for the call's tensors; it depends only on the
+ * tensors' sizes and alignment.  No workspace is needed (the size query returns
  * 0; ws may be NULL). */
 size_t dp_norms_clip_noise_workspace_bytes(const dp_param *params, int32_t count, int64_t N);
 dp_status dp_norms_clip_noise(const float *sqnorm, int32_t n_layers, const dp_param *params,

@@ -170,12 +170,12 @@ __global__ __launch_bounds__(kThreads) void finish_many_kernel(GroupDesc d, cons
 // ---------------------------------------------------------------------------
 // One-launch variant: norms (optional), column reduce, and finish.
 //
-// A column workgroup owns 64 consecutive elements of a column-reduced tensor
-// (16 float4 columns; 16 scalar columns when the tensor is not 16-byte
-// vectorizable) for the whole batch: its 256 threads are 16 sample groups x
-// 16 columns, each group adding c_n * G[n] over a contiguous range of
-// ceil(N / 16) samples in ascending n.  The 16 range sums are then added in
-// range order through LDS, so the clipped sum is deterministic without a
+// A column workgroup owns 256 / KG float4 columns of a column-reduced tensor
+// (scalar columns when the tensor is not 16-byte vectorizable) for the whole
+// batch: its 256 threads are KG sample groups x 256 / KG columns, each group
+// adding c_n * G[n] over a contiguous range of ceil(N / KG) samples in
+// ascending n.  The KG range sums are then added in range order through LDS,
+// so the clipped sum is deterministic without a
 // second launch or any communication between workgroups, and the same
 // workgroup adds the noise and divides.  Blocks past the column work finish
 // the tensors whose sums were formed elsewhere.  With sqnorm given, every
@@ -183,8 +183,11 @@ __global__ __launch_bounds__(kThreads) void finish_many_kernel(GroupDesc d, cons
 // norms (added in layer order, as norms_kernel does) and workgroup 0 writes
 // the norms.
 // ---------------------------------------------------------------------------
-constexpr int kGroups = 16;                 // sample groups per column workgroup
-constexpr int kCols = kThreads / kGroups;   // columns per column workgroup
+// A column workgroup splits the batch into KG sample groups (4, 8 or 16) and
+// covers kThreads / KG columns: fewer groups give longer contiguous rows per
+// load, more groups give more workgroups; the launch takes the fewest groups
+// that still give every CU a column workgroup.
+constexpr int kMinColBlocks = 256;
 constexpr int kCfChunk = 4096;              // clip factors held in LDS at a time
 
 struct FusedArgs {
@@ -238,11 +241,12 @@ __device__ __forceinline__ void noise_scale(const FusedArgs &f, float &sc, bool 
 // STREAM: the per-sample gradients are read with non-temporal loads (they
 // are read once, and a large set of them would only push out of the caches
 // what the next kernels read).
-template <bool STREAM>
+template <bool STREAM, int KG>
 __global__ __launch_bounds__(kThreads) void norms_clip_noise_kernel(GroupDesc d, FusedArgs f)
 {
+    constexpr int kCols = kThreads / KG;
     __shared__ float cfs[kCfChunk];
-    __shared__ float4 part[kGroups][kCols];
+    __shared__ float4 part[KG][kCols];
     const int tid = threadIdx.x;
     if ((int)blockIdx.x >= f.cblocks) {
         // finish-only: a tensor whose sum is already in S (or an empty batch)
@@ -290,7 +294,7 @@ __global__ __launch_bounds__(kThreads) void norms_clip_noise_kernel(GroupDesc d,
         const int64_t v = *f.n_active;
         na = v < 0 ? 0 : (v < N ? v : N);
     }
-    const i64 per = ceil_div(N, kGroups);
+    const i64 per = ceil_div(N, KG);
     const i64 lo = grp * per < N ? grp * per : N, hi = lo + per < N ? lo + per : N;
     float acc[4] = {0.f, 0.f, 0.f, 0.f};
     const float4 *g4 = reinterpret_cast<const float4 *>(G);
@@ -356,7 +360,7 @@ __global__ __launch_bounds__(kThreads) void norms_clip_noise_kernel(GroupDesc d,
     if (grp != 0 || !active) return;
     float s[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int k = 0; k < kGroups; ++k) {
+    for (int k = 0; k < KG; ++k) {
         const float4 v = part[k][col];
         s[0] += v.x; s[1] += v.y; s[2] += v.z; s[3] += v.w;
     }
@@ -551,11 +555,12 @@ static dp_status norms_clip_noise(const float *sqnorm, int32_t n_layers, const d
         const int c = count - first < kMaxGroup ? count - first : kMaxGroup;
         GroupDesc d;
         describe(params, first, c, N, d);
-        int cb = 0, ob = 0;
+        int ob = 0;
         i64 col_bytes = 0;     // per-sample gradient bytes the column reduce reads
+        i64 cols[kMaxGroup];   // columns (float4 or single) of each column-reduced tensor, else 0
         for (int i = 0; i < c; ++i) {
-            f.cblk0[i] = cb;
             f.oblk0[i] = ob;
+            cols[i] = 0;
             const bool col = d.R[i] && N > 0 && d.numel[i] > 0;
             if (col) {
                 col_bytes += 4 * N * d.numel[i];
@@ -563,27 +568,46 @@ static dp_status norms_clip_noise(const float *sqnorm, int32_t n_layers, const d
                 // of describe() also asks for an aligned sum, which this path does not)
                 const bool v = (d.numel[i] & 3) == 0 && aligned(d.G[i], 16);
                 d.flags[i] = (d.flags[i] & ~1u) | (v ? 1u : 0u);
-                cb += (int)ceil_div(v ? d.numel[i] / 4 : d.numel[i], kCols);
+                cols[i] = v ? d.numel[i] / 4 : d.numel[i];
             } else {
                 ob += (int)ceil_div(ceil_div(d.numel[i], 4), kThreads);
             }
+        }
+        auto col_blocks = [&](int kg) {
+            i64 n = 0;
+            for (int i = 0; i < c; ++i) n += ceil_div(cols[i], kThreads / kg);
+            return n;
+        };
+        const int kg = col_blocks(4) >= kMinColBlocks ? 4 : (col_blocks(8) >= kMinColBlocks ? 8 : 16);
+        int cb = 0;
+        for (int i = 0; i < c; ++i) {
+            f.cblk0[i] = cb;
+            cb += (int)ceil_div(cols[i], kThreads / kg);
         }
         f.cblk0[c] = cb;
         f.oblk0[c] = ob;
         f.cblocks = cb;
         if (!norms_done && cb == 0) {
             // no column work to compute the norms in: compute them first
-            const dp_status st = dp_per_sample_norms(sqnorm, n_layers, N, norm, status, stream);
+            const dp_status st = dp_per_sample_norms_active(sqnorm, n_layers, N, n_active, norm, status, stream);
             if (st != DP_OK) return st;
             norms_done = true;
         }
         f.sqnorm = norms_done ? nullptr : sqnorm;
         if (cb + ob > 0) {
             // stream the gradients when there are many of them (16 MB or more)
-            if (col_bytes >= (i64(16) << 20))
-                norms_clip_noise_kernel<true><<<(unsigned)(cb + ob), kThreads, 0, stream>>>(d, f);
-            else
-                norms_clip_noise_kernel<false><<<(unsigned)(cb + ob), kThreads, 0, stream>>>(d, f);
+            const unsigned grid = (unsigned)(cb + ob);
+            const bool stream_loads = col_bytes >= (i64(16) << 20);
+            if (kg == 4) {
+                if (stream_loads) norms_clip_noise_kernel<true, 4><<<grid, kThreads, 0, stream>>>(d, f);
+                else norms_clip_noise_kernel<false, 4><<<grid, kThreads, 0, stream>>>(d, f);
+            } else if (kg == 8) {
+                if (stream_loads) norms_clip_noise_kernel<true, 8><<<grid, kThreads, 0, stream>>>(d, f);
+                else norms_clip_noise_kernel<false, 8><<<grid, kThreads, 0, stream>>>(d, f);
+            } else {
+                if (stream_loads) norms_clip_noise_kernel<true, 16><<<grid, kThreads, 0, stream>>>(d, f);
+                else norms_clip_noise_kernel<false, 16><<<grid, kThreads, 0, stream>>>(d, f);
+            }
         }
         norms_done = true;
     }
