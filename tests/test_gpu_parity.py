@@ -750,6 +750,35 @@ def test_noise_schedule_bad_entry_raises_the_flag():
     assert all(np.isnan(v).all() for v in bad["out"].values())
 
 
+@pytest.mark.parametrize("numel,N", [(4 * 64 * 300, 37), (4 * 32 * 300, 70), (4 * 16 * 100, 33), (4099, 129)])
+def test_norms_clip_noise_each_sample_group_count_matches_oracle(numel, N):
+    """The one-launch clip takes 4, 8 or 16 sample groups per workgroup from
+    the tensors' sizes (the first three shapes give 4, 8 and 16; the last is
+    a scalar-column tensor): norms, clipped sum and noised output each
+    against the oracle."""
+    r = np.random.default_rng(numel + N)
+    say("norms_clip_noise groups, numel", numel, "N", N)
+    L, C, sigma, denom, seed, step = 2, 0.9, 0.7, 41.0, 23, 6
+    sq_h = r.uniform(0.05, 2.0, (L, N)).astype(np.float32)
+    G_h = r.standard_normal((N, numel)).astype(np.float32)
+    sq = torch.from_numpy(sq_h).to(DEV)
+    G = torch.from_numpy(G_h).to(DEV)
+    S = torch.empty(numel, device=DEV)
+    O = torch.empty(numel, device=DEV)
+    norm = torch.empty(N, device=DEV)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    pa = dp.make_params([(G, S, O, numel, 3)])
+    dp.dp_norms_clip_noise(sq, L, pa, 1, N, norm, C, seed, step, None, sigma, denom, status, None)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    nr = oracle.norms(sq_h.astype(np.float64).sum(axis=0))   # layers added, then the root
+    assert_rel(norm.cpu().numpy(), nr, RTOL["f32"], "norms")
+    ref_s = oracle.clip_sum(G_h, oracle.clip_factors(nr, C))
+    assert_g12(S.cpu().numpy(), ref_s, RTOL["f32"], "clipped sum")
+    ref_o = oracle.add_noise(ref_s, seed, step, 3, sigma, C, denom)
+    assert_g12(O.cpu().numpy(), ref_o, RTOL["f32"], "noised output")
+
+
 @pytest.mark.parametrize("N", [0, 5, 40, 300, 4100])
 def test_norms_clip_noise_one_launch_matches_two_launch_path(N):
     """dp_norms_clip_noise (norms, column reduce and finish in one launch)
