@@ -53,8 +53,12 @@ def log(*a):
 # algorithmic cost of each call of the step
 # ---------------------------------------------------------------------------
 
-def call_costs(st):
-    """name -> (algorithmic bytes, flops, kernel name, MFMA peak key or None) per call of one step."""
+def call_costs(st, nnz=None):
+    """name -> (algorithmic bytes, flops, kernel name, MFMA peak key or None) per call of one step.
+
+    nnz: layer name -> the number of (sample, distinct id) rows an Embedding
+    layer's per-sample gradient holds (row_ptr[N], read back after a warm-up
+    step); without it the CSR is priced at its capacity N*T."""
     from paper_2109_12298_amd import workloads as W
     from paper_2109_12298_amd import binding as dp
     N = st.N
@@ -108,10 +112,12 @@ def call_costs(st):
                                      2 * N * L.c_out * kk * ho * wo, kname, "f32")
             col_bytes += grads
         elif isinstance(L, W.Embedding):
-            nnz_bound = N * L.T
-            out["grad:" + L.name] = (N * L.T * (8 + L.D * e) + N * L.T * (L.D * 4 + 8), N * L.T * L.D,
-                                     "emb_rows_kernel", None)
-            out["clip:" + L.name] = (nnz_bound * L.D * 4 + L.V * L.D * 4, 2 * nnz_bound * L.D,
+            u = (nnz or {}).get(L.name, N * L.T)
+            # reads ids and backprops; writes row_ptr, the distinct ids, their rows and the squared norms
+            out["grad:" + L.name] = (N * L.T * (8 + L.D * e) + (N + 1) * 8 + u * (L.D * 4 + 8) + N * 4,
+                                     N * L.T * L.D, "emb_rows_kernel", None)
+            # reads row_ptr, the ids, the rows and the norms; writes the dense [V][D] sum
+            out["clip:" + L.name] = ((N + 1) * 8 + u * (L.D * 4 + 8) + N * 4 + L.V * L.D * 4, 2 * u * L.D,
                                      "emb_clipsum_kernel", None)
         elif isinstance(L, W.LayerNorm):
             out["grad:" + L.name] = (2 * N * L.T * L.D * e + 2 * N * L.D * 4, 3 * N * L.T * L.D,
@@ -253,32 +259,65 @@ def record_traffic(meta_path, fetch_csv, write_csv):
         print(k, table[k]["bytes_per_launch"], "algorithmic", table[k]["algorithmic_bytes"])
 
 
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(wl, inputs, budget_s: float):
+    """The oracle's whole step on a bounded sample of the batch: the median of
+    three runs on all of the host's cores, and of three single-threaded runs
+    on a smaller sample."""
     import numpy as np
     import oracle
     from paper_2109_12298_amd import workloads as W
     N = wl.N
-    # a sample of n samples, grown until one oracle step takes a good part of the budget
+
+    def sub(n):
+        return [W.LayerInputs(li.layer, A=None if li.A is None else li.A[:n], B=li.B[:n],
+                              ids=None if li.ids is None else li.ids[:n]) for li in inputs]
+
+    def timed(n, step):
+        s_ = sub(n)
+        t0 = time.perf_counter()
+        oracle.dp_step(wl, s_, step=step, denom=float(N))
+        return time.perf_counter() - t0
+
+    cores = oracle.num_threads()
+    # a sample of n samples, grown until one multi-threaded step takes about a
+    # sixth of the budget (three of them here, three single-threaded below)
     n = max(1, min(N, 8))
     while True:
-        sub = [W.LayerInputs(li.layer, A=None if li.A is None else li.A[:n], B=li.B[:n],
-                             ids=None if li.ids is None else li.ids[:n]) for li in inputs]
-        t0 = time.perf_counter()
-        oracle.dp_step(wl, sub, step=0, denom=float(N))
-        dt = time.perf_counter() - t0
-        if dt > budget_s / 4 or n >= N:
+        dt = timed(n, 0)
+        if dt > budget_s / 6 or n >= N:
             break
-        n = min(N, n * 4 if dt < budget_s / 40 else n * 2)
-    reps, total = 1, dt
-    while total < budget_s and reps < 100000:
-        t0 = time.perf_counter()
-        oracle.dp_step(wl, sub, step=reps, denom=float(N))
-        total += time.perf_counter() - t0
-        reps += 1
-    return {"value": reps * n / total, "unit": "samples/s", "cores": oracle.num_threads(),
-            "kind": "oracle",
-            "sample": "%d of the %d samples of one batch, whole step (grads, norms, clip, sum, noise), "
-                      "%d repetitions, %.1f s" % (n, N, reps, total)}
+        n = min(N, n * 4 if dt < budget_s / 60 else n * 2)
+    mt = sorted(timed(n, k + 1) for k in range(3))[1]
+    n1 = max(1, n // cores)
+    oracle.set_num_threads(1)
+    try:
+        st1 = sorted(timed(n1, k + 4) for k in range(3))[1]
+    finally:
+        oracle.set_num_threads(cores)
+    return {"value": round(n / mt, 3), "unit": "samples/s", "cores": cores, "kind": "oracle",
+            "cpu_model": cpu_model(), "nproc": len(os.sched_getaffinity(0)),
+            "median_of": 3, "step_s": round(mt, 3),
+            "sample": "%d of the %d samples of one batch, whole step (grads, norms, clip, sum, noise over all "
+                      "parameters), median of 3 runs on %d threads" % (n, N, cores),
+            "single_thread": {"value": round(n1 / st1, 3), "unit": "samples/s", "cores": 1, "step_s": round(st1, 3),
+                              "sample": "%d of the %d samples, median of 3 runs" % (n1, N)}}
+
+
+def percentiles(ms):
+    import numpy as np
+    a = np.asarray(ms, dtype=np.float64)
+    return {"median": round(float(np.median(a)), 4), "p10": round(float(np.percentile(a, 10)), 4),
+            "p90": round(float(np.percentile(a, 90)), 4)}
 
 
 # ---------------------------------------------------------------------------
@@ -288,8 +327,13 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="mnist_cnn")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--workload", default="transformer_block",
+                    help="default: the transformer encoder block (N=32, T=128, d_model 768, bf16), the largest "
+                         "workload; the others are parity cases")
+    ap.add_argument("--cpu-seconds", type=float, default=20.0)
+    ap.add_argument("--cold-reps", type=int, default=20,
+                    help="cold-cache steps: one step per replay after a write of --flush-mib of scratch")
+    ap.add_argument("--flush-mib", type=int, default=512)
     ap.add_argument("--clip-mode", default="auto", choices=["auto", "fused", "colreduce"],
                     help="clipped-sum route of Linear layers (default: per layer by modelled cost)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -336,11 +380,13 @@ def main():
         for k in range(K):
             st.run(step=i, clear_status=(k == 0), reset=(k == 0), emit=(k == K - 1))
     stream = torch.cuda.current_stream(dev)
-    costs = call_costs(st)
 
     for i in range(3):
         eager_step(i)
     torch.cuda.synchronize()
+    # an Embedding layer's CSR holds row_ptr[N] rows: priced at that count
+    nnz = {lb.layer.name: int(lb.row_ptr[-1].item()) for lb in st.layers if isinstance(lb.layer, W.Embedding)}
+    costs = call_costs(st, nnz)
 
     # the timed region: K whole steps, replayed from a captured HIP graph that
     # holds r steps back to back (r the largest of 10, 8, 5, 4, 2, 1 that
@@ -354,18 +400,50 @@ def main():
     for i in range(max(args.warmup // r, 1) if not args.eager else args.warmup):
         st.replay() if not args.eager else eager_step(i)
     torch.cuda.synchronize()
+    # HIP events on the replay stream around every replay (or eager step)
+    # give the spread of step times; the wall clock around the whole region
+    # gives the value
+    n_rep = args.steps if args.eager else args.steps // r
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(n_rep + 1)]
     t0 = time.perf_counter()
+    ev[0].record(stream)
     if args.eager:
         for i in range(args.steps):
             eager_step(args.warmup + i)
+            ev[i + 1].record(stream)
     else:
-        for i in range(args.steps // r):
+        for i in range(n_rep):
             st.replay()
+            ev[i + 1].record(stream)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    per_step = [ev[i].elapsed_time(ev[i + 1]) / (1 if args.eager else r) for i in range(n_rep)]
+    warm = percentiles(per_step)
     status = int(st.status.item())
     if status != 0:
         log("[bench] device status flags %d" % status)
+
+    # cold cache: one step per replay, each after a write of flush-mib of
+    # scratch that evicts the inputs from the 256 MB Infinity Cache and the L2s
+    cold = None
+    if args.cold_reps > 0 and not args.eager:
+        flush = torch.empty((args.flush_mib << 20) // 4, dtype=torch.float32, device=dev)
+        st.capture(first_step=args.steps, parallel=st.graph_parallel, steps_per_replay=1)
+        st.replay()
+        ce = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(args.cold_reps)]
+        for j in range(args.cold_reps):
+            flush.fill_(float(j))
+            ce[j][0].record(stream)
+            st.replay()
+            ce[j][1].record(stream)
+        torch.cuda.synchronize()
+        cold_ms = [a.elapsed_time(b) for a, b in ce]
+        cold = percentiles(cold_ms)
+        cold.update({"samples_per_s": round(K * wl.N / (cold["median"] * 1e-3), 1), "reps": args.cold_reps,
+                     "flush_mib": args.flush_mib, "steps_per_replay": 1})
+        del flush
+        status |= int(st.status.item())
 
     # eager launches of the same steps, for comparison
     torch.cuda.synchronize()
@@ -445,6 +523,8 @@ def main():
             "launch": "eager" if args.eager else
             ("hip_graph_branches" if st.graph_parallel else "hip_graph_chain"),
             "steps_per_replay": 1 if args.eager else r,
+            "ms_per_step_warm": warm,
+            "cold_cache": cold,
             "eager_ms_per_step": round(eager_ms, 4),
             "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": dtype,
             "data": "synthetic",

@@ -195,7 +195,7 @@ dp_status dp_grad_sample_many(const dp_layer_grad *items, int32_t count, dp_dtyp
  * suffices; a smaller cap that the data overflows sets DP_FLAG_CAP, row_ptr
  * still holds the true counts and rows past cap are not written.  An id
  * outside [0, V) sets DP_FLAG_BAD_INDEX and its position is left out.
- * Needs T <= 4096 (else DP_EUNSUPPORTED) and V < 2^31. */
+ * Needs T <= 4096 and N*T < 2^26 (else DP_EUNSUPPORTED) and V < 2^31. */
 size_t dp_grad_sample_embedding_workspace_bytes(int64_t N, int64_t T);
 dp_status dp_grad_sample_embedding(const int64_t *ids, const void *B, dp_dtype dt, int64_t N,
                                    int64_t T, int64_t V, int64_t D, float scale,

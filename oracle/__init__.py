@@ -63,6 +63,7 @@ def lib():
         L.dpo_philox4x32_10.argtypes = [_u32, _u32, _u32]
         L.dpo_philox_normals.argtypes = [_L, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint32, _u32, _d]
         L.dpo_num_threads.restype = ctypes.c_int
+        L.dpo_set_num_threads.argtypes = [ctypes.c_int]
         L.dpo_add_noise.argtypes = [_d, _L, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint32,
                                     ctypes.c_double, ctypes.c_double, ctypes.c_double, _d]
         _lib = L
@@ -71,6 +72,11 @@ def lib():
 
 def num_threads() -> int:
     return int(lib().dpo_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """OpenMP threads for the parallel loops (timing only; results do not depend on it)."""
+    lib().dpo_set_num_threads(int(n))
 
 
 def _f64(a) -> np.ndarray:
@@ -159,7 +165,7 @@ def groupnorm_grad(xhat, B, scale: float = 1.0):
 def sqnorm_accumulate(G, sq: np.ndarray) -> np.ndarray:
     G = _f64(G)
     N = G.shape[0]
-    G2 = G.reshape(N, -1)
+    G2 = G.reshape(N, int(np.prod(G.shape[1:])))
     lib().dpo_sqnorm_accumulate(_p(G2), N, G2.shape[1], _p(sq))
     return sq
 
@@ -181,7 +187,7 @@ def clip_factors(norm, C: float) -> np.ndarray:
 def clip_sum(G, c) -> np.ndarray:
     G = _f64(G); c = _f64(c)
     N = G.shape[0]
-    G2 = G.reshape(N, -1)
+    G2 = G.reshape(N, int(np.prod(G.shape[1:])))
     S = np.empty(G2.shape[1])
     lib().dpo_clip_sum(_p(G2), _p(c), N, G2.shape[1], _p(S))
     return S.reshape(G.shape[1:])
@@ -192,7 +198,7 @@ def clip_sum_embedding(row_ptr, uniq, rows, c, V: int) -> np.ndarray:
     uniq = np.ascontiguousarray(uniq, dtype=np.int64)
     rows = _f64(rows); c = _f64(c)
     N = row_ptr.shape[0] - 1
-    D = rows.shape[1] if rows.ndim == 2 and rows.shape[0] else 1
+    D = rows.shape[1] if rows.ndim == 2 else 1
     S = np.empty((V, D))
     lib().dpo_clip_sum_embedding(_p(row_ptr, _i64), _p(uniq, _i64), _p(rows), _p(c), N, V, D, _p(S))
     return S

@@ -29,6 +29,9 @@
 /* Number of OpenMP threads the parallel loops below use. */
 int dpo_num_threads(void) { return omp_get_max_threads(); }
 
+/* Set that number (the single-threaded timing of the oracle uses 1). */
+void dpo_set_num_threads(int n) { omp_set_num_threads(n > 0 ? n : 1); }
+
 /* ---------------------------------------------------------------------------
  * Per-sample gradients
  * ------------------------------------------------------------------------- */
@@ -230,13 +233,18 @@ void dpo_norms(const double *sq, long N, double *norm)
 
 /* Clip factor c_n = min(1, C / (norm_n + 1e-6)).
  * C = +inf gives c = 1 (no clipping); a non-finite norm gives c = NaN so the
- * sample poisons the sum instead of passing unclipped.                     */
+ * sample poisons the sum instead of passing unclipped.  A negative norm is
+ * not a norm: it marks a row of a variable-size batch that holds no sample
+ * (the batch size changes from step to step under Poisson sampling), and its
+ * factor is 0, so the row adds nothing to the clipped sum.                 */
 void dpo_clip_factors(const double *norm, long N, double C, double *c)
 {
     for (long n = 0; n < N; n++) {
         double x = norm[n];
         if (isnan(x) || isinf(x)) {
             c[n] = NAN;
+        } else if (x < 0.0) {
+            c[n] = 0.0;
         } else if (isinf(C)) {
             c[n] = 1.0;
         } else {

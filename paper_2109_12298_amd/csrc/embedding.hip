@@ -285,6 +285,8 @@ extern "C" dp_status dp_grad_sample_embedding(const int64_t *ids, const void *B,
     DPG_REQUIRE(N >= 0 && T >= 0 && V >= 1 && D >= 1 && cap >= 0, DP_EINVAL);
     DPG_REQUIRE(V < (i64(1) << 31), DP_EINVAL);
     DPG_REQUIRE(T <= kMaxT, DP_EUNSUPPORTED);
+    // one 64-lane workgroup per position: the grid's 2^32 work-items cap N*T
+    DPG_REQUIRE(N * T < (i64(1) << 26), DP_EUNSUPPORTED);
     DPG_REQUIRE(row_ptr != nullptr, DP_EINVAL);
     DPG_REQUIRE(N * T == 0 || (ids != nullptr && B != nullptr), DP_EINVAL);
     DPG_REQUIRE(cap == 0 || (uniq_ids != nullptr && rows != nullptr), DP_EINVAL);

@@ -7,7 +7,11 @@ positive and use plain relative error.  Integer results compare exactly.
 """
 import numpy as np
 
-RTOL = {"f32": 1e-4, "bf16": 2e-2}
+# bf16-input workloads: the oracle reads the very bf16 values the kernels
+# read and every product of two bf16 values is exact in fp32, so the only
+# differences are fp32 rounding of the sums, as for fp32 inputs; the tests
+# hold them to the fp32 bound (the contract's bf16 bound is 2e-2).
+RTOL = {"f32": 1e-4, "bf16": 1e-4}
 
 
 def g12_error(x, y) -> float:

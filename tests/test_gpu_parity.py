@@ -200,8 +200,8 @@ LINEAR_SHAPES = [(1, 1, 1, 1), (3, 1, 37, 13), (2, 2, 5, 3), (4, 5, 37, 13), (3,
                  (1, 2, 8, 8), (3, 33, 136, 72), (2, 130, 264, 392), (2, 64, 128, 128), (9, 16, 256, 24),
                  # multiples of 4 but not 8: 16-byte fp32 / 8-byte bf16 loads on the fp32-MFMA path
                  (3, 40, 100, 20), (2, 256, 100, 400),
-                 # T a multiple of 32: the staged bf16 kernel (ragged tiles; runs of several samples
-                 # per workgroup with a one-sample tail at N = 181)
+                 # T a multiple of 32: the staged bf16 kernel (ragged tiles; one sample per workgroup;
+                 # runs of several samples are covered by test_bf16_staged_sample_runs_with_a_tail)
                  (1, 32, 8, 8), (3, 32, 136, 72), (2, 64, 264, 392), (5, 96, 128, 256), (181, 32, 512, 384)]
 
 
@@ -250,6 +250,77 @@ def test_linear_ragged_shapes(dtype, N, T, din, dout):
     dp.dp_clip_accumulate(gW, normt, C, N, dout * din, s2, cout, None, ws3)
     assert_g12(s2.cpu().numpy(), oracle.clip_sum(rW, cf), 1e-4, "colreduce sumW")
     assert_rel(cout.cpu().numpy(), cf, 1e-6, "c")
+
+
+def staged_run_length(N, din, dout):
+    """Samples per workgroup of the staged bf16 kernel: its 256 (d_in) x 128
+    (d_out) tiles times N spread over about 1024 workgroups, between 1 and 8."""
+    tiles = -(-din // 256) * -(-dout // 128)
+    return min(max(tiles * N // 1024, 1), 8)
+
+
+@pytest.mark.parametrize("N,T,din,dout,check", [
+    (29, 32, 768, 3072, None),                     # runs of 2 samples, the 15th run a one-sample tail
+    (181, 32, 512, 1536, [0, 3, 4, 7, 176, 179, 180])])   # runs of 4, the 46th a one-sample tail
+def test_bf16_staged_sample_runs_with_a_tail(N, T, din, dout, check):
+    """The staged bf16 kernel walks a run of consecutive samples per
+    workgroup, storing each at its boundary while the next one's operands are
+    already staged; a last run shorter than the others stops early.  Every
+    sample (or the run-boundary samples and the tail) against the oracle, at
+    the fp32 tolerance (the oracle reads the same bf16 bits)."""
+    per = staged_run_length(N, din, dout)
+    assert per >= 2 and N % per == 1, (per, N)
+    say("bf16 staged runs", N, T, din, dout, "per", per)
+    r = np.random.default_rng(N + din)
+    A = torch.from_numpy(r.standard_normal((N, T, din)).astype(np.float32)).to(torch.bfloat16)
+    B = torch.from_numpy((r.standard_normal((N, T, dout)) / 8).astype(np.float32)).to(torch.bfloat16)
+    At, Bt = A.to(DEV), B.to(DEV)
+    gW = torch.empty((N, dout, din), device=DEV)
+    gb = torch.empty((N, dout), device=DEV)
+    sq = torch.empty(N, device=DEV)
+    ws = torch.empty(max(dp.dp_grad_sample_linear_workspace_bytes(N, T, din, dout, dp.DP_BF16), 1),
+                     dtype=torch.uint8, device=DEV)
+    dp.dp_grad_sample_linear(At, Bt, dp.DP_BF16, N, T, din, dout, 0.9, gW, gb, sq, None, ws)
+    torch.cuda.synchronize()
+    idx = list(range(N)) if check is None else check
+    Ad = A.float().numpy().astype(np.float64)[idx]
+    Bd = B.float().numpy().astype(np.float64)[idx]
+    rW, rb = oracle.linear_grad(Ad, Bd, 0.9)
+    rsq = np.zeros(len(idx))
+    oracle.sqnorm_accumulate(rW, rsq); oracle.sqnorm_accumulate(rb, rsq)
+    sel = torch.tensor(idx, device=DEV)
+    assert_g12(gW[sel].cpu().numpy(), rW, 1e-4, "gW")
+    assert_g12(gb[sel].cpu().numpy(), rb, 1e-4, "gb")
+    assert_rel(sq[sel].cpu().numpy(), rsq, 1e-4, "sqnorm")
+
+
+def test_sqnorm_from_grads_and_clip_factors_match_oracle():
+    """dp_sqnorm_from_grads (squared norm of materialized per-sample
+    gradients) and dp_clip_factors on a random batch whose norms straddle C,
+    including a zero norm and norms at C and just below it."""
+    r = np.random.default_rng(77)
+    for N, numel in [(1, 1), (37, 1000), (300, 4099), (5, 262144)]:
+        say("sqnorm_from_grads", N, numel)
+        G = (r.standard_normal((N, numel)) * r.uniform(0.01, 3.0, (N, 1))).astype(np.float32)
+        G[0] = 0.0
+        sq = torch.empty(N, device=DEV)
+        dp.dp_sqnorm_from_grads(torch.from_numpy(G).to(DEV), N, numel, sq)
+        rsq = np.zeros(N)
+        oracle.sqnorm_accumulate(G.astype(np.float64), rsq)
+        got = sq.cpu().numpy()
+        assert got[0] == 0.0
+        assert_rel(got[1:], rsq[1:], 1e-5, "sqnorm_from_grads")
+    N, C = 4096, 1.3
+    norm = np.exp(r.normal(np.log(C), 1.0, N)).astype(np.float32)
+    norm[:4] = [0.0, C, np.float32(C - 1e-6), np.float32(C + 1e-6)]
+    c = torch.empty(N, device=DEV)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    dp.dp_clip_factors(torch.from_numpy(norm).to(DEV), N, C, c, status)
+    ref = oracle.clip_factors(norm.astype(np.float64), C)
+    got = c.cpu().numpy()
+    assert_rel(got, ref, 1e-6, "clip factors")
+    assert np.all((got == 1.0) == (ref == 1.0)), "which samples are left unclipped"
+    assert int(status.item()) == 0
 
 
 CONV_SHAPES = [  # N, Cin, H, W, Cout, kh, kw, sh, sw, ph, pw
@@ -470,7 +541,7 @@ def test_groupnorm_affine_matches_oracle(N, C, P, dtype):
     xd, Bd = xh.to(DEV), B.to(DEV)
     dp.dp_grad_sample_groupnorm(xd, Bd, dt, N, C, P, 1.25, g, b, sq, None, ws)
     rg, rb = oracle.groupnorm_grad(xh.float().numpy(), B.float().numpy(), 1.25)
-    rtol = 1e-4 if dtype == torch.float32 else 2e-2
+    rtol = 1e-4        # the oracle reads the same bf16 values; only fp32 sums differ
     assert_g12(g.cpu().numpy(), rg, rtol, "ggamma")
     assert_g12(b.cpu().numpy(), rb, rtol, "gbeta")
     assert_rel(sq.cpu().numpy(), (rg ** 2).sum(1) + (rb ** 2).sum(1), rtol, "groupnorm sqnorm")
@@ -697,10 +768,16 @@ def test_variable_batch_in_a_graph_matches_eager(name, nmax):
         got = st.results()
         assert got["status"] == 0, (k, na)
         assert np.all(got["norm"][na:] == -1.0), (k, na)
+        # the oracle's step over just the active rows, same step and divisor
+        ref_o = oracle.dp_step(wl, _prefix(inputs, na), step=k, denom=denom)
+        for pn in ref_o["out"]:
+            assert_g12(got["out"][pn], ref_o["out"][pn], RTOL[wl.dtype], "oracle replay %d (batch %d) %s" % (k, na, pn))
+            assert_g12(got["S"][pn], ref_o["S"][pn], RTOL[wl.dtype], "oracle S %d (batch %d) %s" % (k, na, pn))
         if na == 0:
             for pn, v in got["S"].items():
                 assert np.all(v == 0.0), (k, pn)
             continue
+        assert_rel(got["norm"][:na], ref_o["norm"], RTOL[wl.dtype], "oracle norms %d" % k)
         eager = DPStep(wl, _prefix(inputs, na), DEV, denom=denom)
         eager.run(step=k)
         ref = eager.results()

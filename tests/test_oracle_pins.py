@@ -326,6 +326,15 @@ def test_clip_invariants():
     np.testing.assert_array_equal(c, [1.0, 1.0])
     S = oracle.clip_sum(G, oracle.clip_factors(norm, C))
     np.testing.assert_allclose(S, (G * oracle.clip_factors(norm, C)[:, None]).sum(0), rtol=1e-12)
+    # a negative norm marks a padding row of a variable-size batch: factor 0,
+    # so a batch padded with random rows sums to the batch of its active rows
+    na = 23
+    padded = norm.copy()
+    padded[na:] = -1.0
+    cp = oracle.clip_factors(padded, C)
+    assert np.all(cp[na:] == 0.0)
+    np.testing.assert_array_equal(cp[:na], c_act := oracle.clip_factors(norm[:na], C))
+    np.testing.assert_allclose(oracle.clip_sum(G, cp), (G[:na] * c_act[:, None]).sum(0), rtol=1e-12)
 
 
 def test_clipped_sum_is_the_gradient_of_the_reweighted_loss():
