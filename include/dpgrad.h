@@ -98,6 +98,23 @@ dp_status dp_grad_sample_linear(const void *A, const void *B, dp_dtype dt, int64
                                 float *gW, float *gb, float *sqnorm, int32_t *status,
                                 void *ws, size_t ws_bytes, hipStream_t stream);
 
+/* dp_grad_sample_linear for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): the same arguments and results without `ws`, the scratch
+ * being a fixed array inside the library (8 MiB on each GPU it runs on, held
+ * until the process ends; dp_grad_sample_linear_noalloc_max_bytes() returns
+ * the size).  A call whose dp_grad_sample_linear_workspace_bytes() exceeds it
+ * returns DP_ECAP and enqueues nothing.  Allocates and frees nothing.  Every
+ * call on one GPU uses that GPU's one array (each call overwrites what it
+ * reads; nothing there needs to start at zero), so calls that may overlap on
+ * one GPU (different streams, or graphs replayed concurrently) race and must
+ * be serialized by the caller; the stream's device picks the array. */
+size_t dp_grad_sample_linear_noalloc_max_bytes(void);
+dp_status dp_grad_sample_linear_noalloc(const void *A, const void *B, dp_dtype dt, int64_t N,
+                                        int64_t T, int64_t d_in, int64_t d_out, float scale,
+                                        float *gW, float *gb, float *sqnorm, int32_t *status,
+                                        hipStream_t stream);
+
 /* Conv2d (cross-correlation, zero padding) with groups = 1 and dilation = 1.
  * The paper defers this layer's formula to its tutorials; it is the weight
  * gradient of the convolution restricted to one sample:

@@ -35,6 +35,8 @@ SIGNATURES = {
     "dp_abi_version": (ctypes.c_int, []),
     "dp_grad_sample_linear_workspace_bytes": (_SZ, [_I64, _I64, _I64, _I64, _ST]),
     "dp_grad_sample_linear": (_ST, [_P, _P, _ST, _I64, _I64, _I64, _I64, _F, _P, _P, _P, _P, _P, _SZ, _P]),
+    "dp_grad_sample_linear_noalloc_max_bytes": (_SZ, []),
+    "dp_grad_sample_linear_noalloc": (_ST, [_P, _P, _ST, _I64, _I64, _I64, _I64, _F, _P, _P, _P, _P, _P]),
     "dp_grad_sample_conv2d_workspace_bytes": (_SZ, [_I64] * 11),
     "dp_grad_sample_conv2d": (_ST, [_P, _P, _ST] + [_I64] * 16 + [_F, _P, _P, _P, _P, _P, _SZ, _P]),
     "dp_conv2d_set_path": (ctypes.c_int, [ctypes.c_int]),
@@ -254,6 +256,17 @@ def dp_grad_sample_linear(A, B, dt, N, T, d_in, d_out, scale, gW, gb=None, sqnor
     _check(lib().dp_grad_sample_linear(_ptr(A), _ptr(B), dt, N, T, d_in, d_out, scale, _ptr(gW), _ptr(gb),
                                        _ptr(sqnorm), _ptr(status), _ptr(ws), _nbytes(ws), _stream(stream)),
            "dp_grad_sample_linear")
+
+
+def dp_grad_sample_linear_noalloc_max_bytes() -> int:
+    return lib().dp_grad_sample_linear_noalloc_max_bytes()
+
+
+def dp_grad_sample_linear_noalloc(A, B, dt, N, T, d_in, d_out, scale, gW, gb=None, sqnorm=None, status=None,
+                                  stream=None):
+    _check(lib().dp_grad_sample_linear_noalloc(_ptr(A), _ptr(B), dt, N, T, d_in, d_out, scale, _ptr(gW),
+                                               _ptr(gb), _ptr(sqnorm), _ptr(status), _stream(stream)),
+           "dp_grad_sample_linear_noalloc")
 
 
 def dp_grad_sample_conv2d_workspace_bytes(N, Cin, H, W, Cout, kh, kw, sh, sw, ph, pw) -> int:

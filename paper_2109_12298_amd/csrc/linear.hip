@@ -278,6 +278,8 @@ ClipSplit clip_split(i64 N, i64 T, i64 din, i64 dout)
     return s;
 }
 
+}  // namespace
+
 dp_status check_linear(const void *A, const void *B, dp_dtype dt, i64 N, i64 T, i64 din, i64 dout)
 {
     DPG_REQUIRE(dtype_ok(dt), DP_EDTYPE);
@@ -287,7 +289,6 @@ dp_status check_linear(const void *A, const void *B, dp_dtype dt, i64 N, i64 T, 
     return DP_OK;
 }
 
-}  // namespace
 }  // namespace dpg
 
 using namespace dpg;

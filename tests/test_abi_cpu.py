@@ -80,6 +80,17 @@ def test_conv_validation():
     assert code_of(f, FAKE, FAKE, 9, *good, 1.0, FAKE, stream=0) == dp.DP_EDTYPE
 
 
+def test_noalloc_linear_validation():
+    f = dp.dp_grad_sample_linear_noalloc
+    assert dp.dp_grad_sample_linear_noalloc_max_bytes() == 8 << 20
+    # a workspace beyond the fixed scratch array: refused before anything is enqueued
+    assert dp.dp_grad_sample_linear_workspace_bytes(2**20, 2, 1024, 1024, dp.DP_F32) > 8 << 20
+    assert code_of(f, FAKE, FAKE, dp.DP_F32, 2**20, 2, 1024, 1024, 1.0, FAKE, FAKE, FAKE, stream=0) == dp.DP_ECAP
+    assert code_of(f, FAKE, FAKE, 7, 2, 2, 8, 8, 1.0, FAKE, stream=0) == dp.DP_EDTYPE
+    assert code_of(f, None, FAKE, dp.DP_F32, 2, 2, 8, 8, 1.0, FAKE, stream=0) == dp.DP_EINVAL
+    assert code_of(f, FAKE, FAKE, dp.DP_F32, 2, 2, 8, 8, 1.0, None, stream=0) == dp.DP_EINVAL
+
+
 def test_embedding_layernorm_validation():
     f = dp.dp_grad_sample_embedding
     assert code_of(f, FAKE, FAKE, dp.DP_F32, 2, 5000, 10, 4, 1.0, FAKE, FAKE, FAKE, 10, stream=0) == \
