@@ -128,13 +128,16 @@ def call_costs(st, nnz=None):
                                      "gn_affine_kernel", None)
             col_bytes += 2 * N * L.C * 4
     if st.grad_group:
-        # the grouped layers' per-sample gradients are one launch
-        gb_, gf_ = 0, 0
+        # the grouped layers' per-sample gradients: the small layers' launch
+        # and the bf16 sequence layers' launch
+        gb_, gf_, kinds = 0, 0, set()
         for i in st.grad_group:
-            b0, f0, _, _ = out.pop("grad:" + st.layers[i].layer.name)
+            b0, f0, kn, _ = out.pop("grad:" + st.layers[i].layer.name)
             gb_ += b0
             gf_ += f0
-        out["grad:group"] = (gb_, gf_, "grad_many_kernel", None)
+            kinds.add("bf16_grad_group_kernel" if kn == "bf16_grad_sample_kernel" else "grad_many_kernel")
+        kname = "+".join(sorted(kinds))
+        out["grad:group"] = (gb_, gf_, kname, "bf16" if kname == "bf16_grad_group_kernel" else None)
     if not st.fold_norms:
         out["norms"] = (len(st.layers) * N * 4 + N * 4, len(st.layers) * N, "norms_kernel", None)
     P = st.wl.n_params
@@ -169,6 +172,8 @@ KERNEL_SOURCES = {
                                  "paper_2109_12298_amd/csrc/bf16_stage.hpp"],
     "bf16_grad_sample_kernel": ["paper_2109_12298_amd/csrc/grad_sample_bf16.hip",
                                 "paper_2109_12298_amd/csrc/bf16_stage.hpp"],
+    "bf16_grad_group_kernel": ["paper_2109_12298_amd/csrc/grad_sample_bf16.hip",
+                               "paper_2109_12298_amd/csrc/bf16_stage.hpp", "paper_2109_12298_amd/csrc/grad_many.hip"],
     "ps_gemm_kernel": ["paper_2109_12298_amd/csrc/linear.hip"],
     "clipsum_gemm_kernel": ["paper_2109_12298_amd/csrc/linear.hip", "paper_2109_12298_amd/csrc/mfma_tile.hpp"],
     "conv_per_sample_kernel": ["paper_2109_12298_amd/csrc/conv2d.hip", "paper_2109_12298_amd/csrc/mfma_tile.hpp"],

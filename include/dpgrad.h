@@ -182,17 +182,25 @@ typedef struct dp_layer_grad {
 
 /* The per-sample gradients of `count` layers that share N and the dtype, as
  * by one dp_grad_sample_linear / dp_grad_sample_conv2d call per layer (same
- * formulas; results equal to rounding order), in one launch for the layers
- * that qualify (dp_grad_sample_many_grouped): one workgroup per sample and
- * layer, so that small layers' fixed costs (launch, load round trip) overlap
- * instead of adding up.  The other layers run through the single-layer entry
- * points inside this call, one after the other on `stream`, sharing `ws`.
- * Arguments are checked as the single-layer calls check them; the first
- * invalid layer's status is returned before anything is enqueued.  count in
- * [0, 64].
- * dp_grad_sample_many_grouped: 1 if the layer goes into the grouped launch
- * (a Linear layer with T = 1; a Conv2d layer whose sample fits one
- * workgroup, as for DP_CONV_AUTO, while that choice is in force), else 0. */
+ * formulas; results equal to rounding order, and bit for bit for the bf16
+ * sequence layers), in grouped launches for the layers that qualify
+ * (dp_grad_sample_many_grouped), so that the layers' fixed costs (launch,
+ * load round trip) and their last, partly idle rounds of workgroups overlap
+ * instead of adding up:
+ *  - small layers (a Linear layer with T = 1; a Conv2d layer whose sample
+ *    fits one workgroup, as for DP_CONV_AUTO, while that choice is in force):
+ *    one workgroup per sample and layer, up to 8 layers per launch;
+ *  - bf16 Linear layers over a sequence that dp_grad_sample_linear runs on
+ *    its staged kernel (T a multiple of 32, d_in and d_out multiples of 8,
+ *    16-byte aligned A, B, gW): runs of consecutive samples per 256 x 128
+ *    tile, the run length balanced over all of them, up to 16 layers per
+ *    launch, plus one launch adding each layer's squared-norm partials.
+ * The other layers run through the single-layer entry points inside this
+ * call, one after the other on `stream`, sharing `ws`.  Arguments are
+ * checked as the single-layer calls check them; the first invalid layer's
+ * status is returned before anything is enqueued.  count in [0, 64].
+ * dp_grad_sample_many_grouped: 1 if the layer goes into a grouped launch,
+ * else 0. */
 int32_t dp_grad_sample_many_grouped(const dp_layer_grad *item, dp_dtype dt, int64_t N);
 size_t dp_grad_sample_many_workspace_bytes(const dp_layer_grad *items, int32_t count, dp_dtype dt,
                                            int64_t N);

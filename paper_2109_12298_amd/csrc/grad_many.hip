@@ -13,6 +13,7 @@
 #include "common.hpp"
 #include "conv2d_small.hpp"
 #include "conv2d_small_dev.hpp"
+#include "grad_sample_bf16.hpp"
 #include "linear_outer.hpp"
 
 namespace dpg {
@@ -104,11 +105,28 @@ dp_status validate(const dp_layer_grad &L, dp_dtype dt, i64 N)
     return DP_OK;
 }
 
-bool grouped(const dp_layer_grad &L, dp_dtype dt, i64 N)
+// a bf16 Linear layer over a sequence that the staged kernel takes: these
+// layers share a launch of their own (bf16_grad_sample_group)
+bool staged(const dp_layer_grad &L, dp_dtype dt, i64 N)
+{
+    return validate(L, dt, N) == DP_OK && N > 0 && L.kind == DP_LAYER_LINEAR && dt == DP_BF16 && L.T > 1 &&
+           bf16_staged_ok(L.A, L.B, L.gW, N, L.T, L.d_in, L.d_out);
+}
+
+// a layer of the small-layer launch (grad_many_kernel)
+bool small(const dp_layer_grad &L, dp_dtype dt, i64 N)
 {
     if (validate(L, dt, N) != DP_OK || N >= (i64(1) << 24)) return false;
     if (L.kind == DP_LAYER_LINEAR) return L.T == 1 && L.d_in * L.d_out < (i64(1) << 31);
     return conv_path() == DP_CONV_AUTO && conv_small_ok(conv_args(L, N));
+}
+
+bool grouped(const dp_layer_grad &L, dp_dtype dt, i64 N) { return small(L, dt, N) || staged(L, dt, N); }
+
+// scratch of the staged launch: each layer's squared-norm partials
+size_t staged_partials_bytes(const dp_layer_grad &L, i64 N)
+{
+    return L.sqnorm ? align_up((size_t)N * bf16_staged_parts(L.d_in, L.d_out) * sizeof(float), 256) : 0;
 }
 
 size_t single_workspace(const dp_layer_grad &L, dp_dtype dt, i64 N)
@@ -187,6 +205,20 @@ extern "C" size_t dp_grad_sample_many_workspace_bytes(const dp_layer_grad *items
 {
     size_t need = 0;
     if (items == nullptr || count < 0) return 0;
+    // the staged layers' partials, per launch of up to kBf16GroupMax layers;
+    // the single-layer calls reuse the same scratch afterwards
+    size_t launch = 0;
+    int in_launch = 0;
+    for (int k = 0; k < count; ++k) {
+        if (!staged(items[k], dt, N)) continue;
+        if (in_launch == kBf16GroupMax) {
+            launch = 0;
+            in_launch = 0;
+        }
+        launch += staged_partials_bytes(items[k], N);
+        ++in_launch;
+        need = launch > need ? launch : need;
+    }
     for (int k = 0; k < count; ++k) {
         if (grouped(items[k], dt, N) || validate(items[k], dt, N) != DP_OK) continue;
         const size_t w = single_workspace(items[k], dt, N);
@@ -208,16 +240,40 @@ extern "C" dp_status dp_grad_sample_many(const dp_layer_grad *items, int32_t cou
     DPG_REQUIRE(ws_bytes >= need && (need == 0 || ws != nullptr), DP_EINVAL);
     if (N == 0 || count == 0) return DP_OK;
 
-    // grouped layers, convolutions first, in launches of up to kManyMax
+    // small layers, convolutions first, in launches of up to kManyMax
     const dp_layer_grad *order[64];
     int ng = 0;
     for (int pass = 0; pass < 2; ++pass)
         for (int k = 0; k < count; ++k)
-            if (grouped(items[k], dt, N) && (items[k].kind == DP_LAYER_CONV2D) == (pass == 0)) order[ng++] = &items[k];
+            if (small(items[k], dt, N) && (items[k].kind == DP_LAYER_CONV2D) == (pass == 0)) order[ng++] = &items[k];
     for (int k0 = 0; k0 < ng; k0 += kManyMax)
         launch_group(order + k0, ng - k0 < kManyMax ? ng - k0 : kManyMax, dt, N, stream);
     dp_status st = launch_status();
     if (st != DP_OK) return st;
+
+    // bf16 sequence layers, in launches of up to kBf16GroupMax, their norm
+    // partials laid out one layer after another in the scratch
+    {
+        Bf16GroupLayer grp[kBf16GroupMax];
+        int n = 0;
+        size_t off = 0;
+        auto flush = [&]() {
+            bf16_grad_sample_group(grp, n, N, stream);
+            n = 0;
+            off = 0;
+        };
+        for (int k = 0; k < count; ++k) {
+            const dp_layer_grad &L = items[k];
+            if (!staged(L, dt, N)) continue;
+            if (n == kBf16GroupMax) flush();
+            grp[n++] = Bf16GroupLayer{L.A, L.B, L.T, L.d_in, L.d_out, L.scale, L.gW, L.gb, L.sqnorm,
+                                      L.sqnorm ? (float *)((char *)ws + off) : nullptr};
+            off += staged_partials_bytes(L, N);
+        }
+        if (n) flush();
+        st = launch_status();
+        if (st != DP_OK) return st;
+    }
 
     // the others through their single-layer entry points
     for (int k = 0; k < count && st == DP_OK; ++k) {

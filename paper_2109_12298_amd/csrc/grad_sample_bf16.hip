@@ -6,16 +6,24 @@
 // norm written as partials (one per wave) from the values it stores.
 //
 // The layer's per-sample gradients are N * d_out * d_in fp32 values, written
-// once: the kernel is bound by that write, not by the MFMAs (a 128 x 128
-// tile is 2M multiply-adds per 64 KB stored).  So a workgroup owns one
-// 128 (j) x 128 (i) tile for a run of consecutive samples, and its operand
+// once: the kernel is bound by that write, not by the MFMAs (a 256 x 128
+// tile is 4M multiply-adds per 128 KB stored).  So a workgroup owns one
+// 256 (j) x 128 (i) tile for a run of consecutive samples, and its operand
 // loads never stop: the rows of consecutive samples are consecutive rows of
 // A [N*T][d_in] and B [N*T][d_out], so the 32-row stages (bf16_stage.hpp:
-// direct-to-LDS loads, four stages deep, transposing operand reads) run
+// direct-to-LDS loads, three stages deep, transposing operand reads) run
 // straight through the sample boundaries.  At the end of each sample the
 // accumulators are scaled and stored and the next sample's MFMAs start on
 // operands already in LDS, so the stores of one sample drain while the next
 // is multiplied.  Needs T % 32 == 0 and d_in, d_out multiples of 8.
+//
+// Balance.  Every (sample, tile) unit costs the same, and two workgroups fit
+// a CU, so 512 run at once.  The run length p is chosen so that the units
+// divide into whole rounds of 512 workgroups: a launch of 1152 two-sample
+// runs would leave three quarters of the machine idle for its third round.
+// The grouped launch (bf16_grad_group_kernel) takes every such layer of a
+// step at once, its workgroups the concatenation of the layers' runs, so the
+// layers' last rounds fill each other's idle slots.
 #include "bf16_stage.hpp"
 #include "grad_sample_bf16.hpp"
 
@@ -38,13 +46,14 @@ struct GsCfg {
 // the configuration the entry point uses
 typedef GsCfg<4, 2, 3> Gs;
 
-// Block b = (run of samples, tile); consecutive blocks share the run and walk
-// the tiles (neighbouring tiles share operand rows in one XCD's L2).
+// The run of one workgroup: tile `tile` of a layer (tiles_m tiles along j)
+// for samples s0 .. s0+ns-1; partial[n][tile][wave] receives each sample's
+// squared-norm partials (if partial is not NULL).
 template <typename Cfg>
-__global__ __launch_bounds__(Cfg::THREADS, 2) void bf16_grad_sample_kernel(
-    const uint16_t *__restrict__ A, const uint16_t *__restrict__ B, i64 N, i64 T, i64 din, i64 dout, int tiles_m,
-    int tiles, int per_block, float scale, float *__restrict__ gW, float *__restrict__ gb,
-    float *__restrict__ partial)
+__device__ __forceinline__ void grad_sample_run(const uint16_t *__restrict__ A, const uint16_t *__restrict__ B,
+                                                i64 T, i64 din, i64 dout, int tiles_m, int tiles, int tile, i64 s0,
+                                                int ns, float scale, float *__restrict__ gW,
+                                                float *__restrict__ gb, float *__restrict__ partial)
 {
     typedef typename Cfg::Plan Plan;
     constexpr int FM = Cfg::FM, FN = Cfg::FN, BMJ = Cfg::BMJ, BNI = Cfg::BNI, kStages = Cfg::STAGES;
@@ -57,10 +66,6 @@ __global__ __launch_bounds__(Cfg::THREADS, 2) void bf16_grad_sample_kernel(
     };
     __shared__ __attribute__((aligned(1024))) char smem[kStages * STAGE_BYTES];
     __shared__ float bred[kThreads / 32][BNI];
-    const i64 blk = xcd_swizzle(blockIdx.x, gridDim.x);
-    const int tile = (int)(blk % tiles);
-    const i64 s0 = (blk / tiles) * per_block;
-    const int ns = (int)(s0 + per_block < N ? per_block : N - s0);   // samples of this block
     const int tn = tile / tiles_m, tm = tile % tiles_m;
     const i64 m0 = (i64)tm * BMJ, n0 = (i64)tn * BNI;
     const int tid = threadIdx.x, lane = tid & 63;
@@ -208,12 +213,98 @@ __global__ __launch_bounds__(Cfg::THREADS, 2) void bf16_grad_sample_kernel(
     }
 }
 
+// Single layer: block b = (run of samples, tile); consecutive blocks share
+// the run and walk the tiles (neighbouring tiles share operand rows in one
+// XCD's L2).
+template <typename Cfg>
+__global__ __launch_bounds__(Cfg::THREADS, 2) void bf16_grad_sample_kernel(
+    const uint16_t *__restrict__ A, const uint16_t *__restrict__ B, i64 N, i64 T, i64 din, i64 dout, int tiles_m,
+    int tiles, int per_block, float scale, float *__restrict__ gW, float *__restrict__ gb,
+    float *__restrict__ partial)
+{
+    const i64 blk = xcd_swizzle(blockIdx.x, gridDim.x);
+    const int tile = (int)(blk % tiles);
+    const i64 s0 = (blk / tiles) * per_block;
+    const int ns = (int)(s0 + per_block < N ? per_block : N - s0);   // samples of this block
+    grad_sample_run<Cfg>(A, B, T, din, dout, tiles_m, tiles, tile, s0, ns, scale, gW, gb, partial);
+}
+
+struct GsItem {
+    const uint16_t *A, *B;
+    float *gW, *gb, *partial, *sqnorm;
+    i64 din, dout, T;
+    float scale;
+    int tiles_m, tiles;
+};
+
+struct GsGroup {
+    int count;
+    int per;                          // samples per run
+    i64 N;
+    int blk0[kBf16GroupMax + 1];      // first block of each layer
+    GsItem it[kBf16GroupMax];
+};
+
+// Several layers: the blocks are the concatenation of every layer's (run,
+// tile) blocks; a block finds its layer in the prefix table.
+template <typename Cfg>
+__global__ __launch_bounds__(Cfg::THREADS, 2) void bf16_grad_group_kernel(const GsGroup g)
+{
+    const int blk = (int)xcd_swizzle(blockIdx.x, gridDim.x);
+    int k = 0;
+    while (k + 1 < g.count && g.blk0[k + 1] <= blk) ++k;
+    const GsItem &it = g.it[k];
+    const int local = blk - g.blk0[k];
+    const int tile = local % it.tiles;
+    const i64 s0 = (i64)(local / it.tiles) * g.per;
+    const int ns = (int)(s0 + g.per < g.N ? g.per : g.N - s0);
+    grad_sample_run<Cfg>(it.A, it.B, it.T, it.din, it.dout, it.tiles_m, it.tiles, tile, s0, ns, it.scale, it.gW,
+                         it.gb, it.partial);
+}
+
+// One wave per (layer, sample): sqnorm[n] = the sample's partials added in
+// tile and wave order (lane l takes partials l, l+64, ..., then a fixed
+// butterfly), as sum_partials does for one layer.
+__global__ __launch_bounds__(256) void bf16_group_sqnorm_kernel(const GsGroup g)
+{
+    const GsItem &it = g.it[blockIdx.y];
+    const i64 n = (i64)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    if (it.sqnorm == nullptr || n >= g.N) return;
+    const int parts = it.tiles * Gs::WAVES;
+    const float *p = it.partial + n * parts;
+    float s = 0.0f;
+    for (int t = lane; t < parts; t += kWave) s += p[t];
+    s = wave_sum(s);
+    if (lane == 0) it.sqnorm[n] = s;
+}
+
+constexpr int kSlots = 2 * 256;      // resident workgroups: two per CU, 256 CUs
+
+// Samples per run for `tiles` tiles (all layers) of N samples: the fewest
+// rounds of kSlots workgroups times the run length, ties to the longer run
+// (fewer pipeline starts).
+int run_length(i64 N, i64 tiles)
+{
+    int best = 1;
+    i64 best_cost = -1;
+    for (int p = 1; p <= 8; ++p) {
+        const i64 cost = ceil_div(tiles * ceil_div(N, p), kSlots) * p;
+        if (best_cost < 0 || cost <= best_cost) {
+            best_cost = cost;
+            best = p;
+        }
+    }
+    return best;
+}
+
 }  // namespace
 
 bool bf16_staged_ok(const void *A, const void *B, const void *gW, i64 N, i64 T, i64 din, i64 dout)
 {
     return T >= BK && T % BK == 0 && din % 8 == 0 && dout % 8 == 0 && aligned(A, 16) && aligned(B, 16) &&
-           aligned(gW, 16) && T * (din > dout ? din : dout) < (i64(1) << 31) && N < (i64(1) << 40);
+           aligned(gW, 16) && T * (din > dout ? din : dout) < (i64(1) << 31) && N < (i64(1) << 40) &&
+           N * ceil_div(din, Gs::BMJ) * ceil_div(dout, Gs::BNI) < (i64(1) << 30);
 }
 
 int bf16_staged_parts(i64 din, i64 dout)
@@ -226,14 +317,49 @@ void bf16_grad_sample_staged(const void *A, const void *B, i64 N, i64 T, i64 din
 {
     const int tiles_m = (int)ceil_div(din, Gs::BMJ);
     const int tiles = tiles_m * (int)ceil_div(dout, Gs::BNI);
-    // about 1024 workgroups (two per CU, four rounds), each with a run of samples
-    i64 per = (i64)tiles * N / 1024;
-    if (per < 1) per = 1;
-    if (per > 8) per = 8;
+    const int per = run_length(N, tiles);
     const i64 runs = ceil_div(N, per);
     bf16_grad_sample_kernel<Gs><<<(unsigned)(runs * tiles), Gs::THREADS, 0, stream>>>(
-        (const uint16_t *)A, (const uint16_t *)B, N, T, din, dout, tiles_m, tiles, (int)per, scale, gW, gb,
-        partial);
+        (const uint16_t *)A, (const uint16_t *)B, N, T, din, dout, tiles_m, tiles, per, scale, gW, gb, partial);
+}
+
+void bf16_grad_sample_group(const Bf16GroupLayer *layers, int count, i64 N, hipStream_t stream)
+{
+    if (count <= 0 || N <= 0) return;
+    GsGroup g;
+    g.count = count;
+    g.N = N;
+    i64 tiles = 0;
+    bool norms = false;
+    for (int k = 0; k < count; ++k) {
+        const Bf16GroupLayer &L = layers[k];
+        GsItem &it = g.it[k];
+        it.A = (const uint16_t *)L.A;
+        it.B = (const uint16_t *)L.B;
+        it.gW = L.gW;
+        it.gb = L.gb;
+        it.sqnorm = L.sqnorm;
+        it.partial = L.sqnorm ? L.partial : nullptr;
+        it.din = L.din;
+        it.dout = L.dout;
+        it.T = L.T;
+        it.scale = L.scale;
+        it.tiles_m = (int)ceil_div(L.din, Gs::BMJ);
+        it.tiles = it.tiles_m * (int)ceil_div(L.dout, Gs::BNI);
+        tiles += it.tiles;
+        norms = norms || L.sqnorm != nullptr;
+    }
+    g.per = run_length(N, tiles);
+    const i64 runs = ceil_div(N, g.per);
+    int blocks = 0;
+    for (int k = 0; k < count; ++k) {
+        g.blk0[k] = blocks;
+        blocks += (int)(runs * g.it[k].tiles);
+    }
+    for (int k = count; k <= kBf16GroupMax; ++k) g.blk0[k] = blocks;
+    for (int k = count; k < kBf16GroupMax; ++k) g.it[k] = g.it[0];
+    bf16_grad_group_kernel<Gs><<<(unsigned)blocks, Gs::THREADS, 0, stream>>>(g);
+    if (norms) bf16_group_sqnorm_kernel<<<dim3((unsigned)ceil_div(N, 4), (unsigned)count), 256, 0, stream>>>(g);
 }
 
 }  // namespace dpg

@@ -146,3 +146,40 @@ def test_grouped_more_layers_than_one_launch():
     specs = MNIST + RAGGED[:5] + MNIST[:2]
     bufs, _ = run_many(specs, 2, dp.DP_F32, 1.0, seed=21)
     check_oracle(specs, bufs, 1.0, "eleven")
+
+
+# bf16 Linear layers over a sequence: the staged grouped launch (runs of
+# samples per tile, balanced over every layer), and one that is not staged
+SEQ = [("lin", 768, 768, 128, True), ("lin", 768, 3072, 128, True), ("lin", 3072, 768, 128, True),
+       ("lin", 264, 392, 64, False),                         # ragged tiles, no bias
+       ("lin", 64, 16, 8, True)]                             # T % 32 != 0: the single-layer path
+
+
+@pytest.mark.parametrize("N", [1, 5, 37])
+def test_grouped_bf16_sequence_layers_match_oracle_and_single_calls(N):
+    say("grad_many bf16 sequence layers N=", N)
+    specs = SEQ if N < 37 else SEQ[3:]
+    bufs, items = run_many(specs, N, dp.DP_BF16, 0.9, seed=40 + N)
+    got = [dp.dp_grad_sample_many_grouped(items, k, dp.DP_BF16, N) for k in range(len(specs))]
+    assert got == [s[3] % 32 == 0 for s in specs]
+    check_oracle(specs, bufs, 0.9, "bf16 seq")
+    for spec, (At, Bt, gW, gb, sq) in zip(specs, bufs):
+        _, din, dout, T, _ = spec
+        gW2, gb2, sq2 = torch.empty_like(gW), (torch.empty_like(gb) if gb is not None else None), torch.empty_like(sq)
+        ws = torch.empty(max(dp.dp_grad_sample_linear_workspace_bytes(N, T, din, dout, dp.DP_BF16), 1),
+                         dtype=torch.uint8, device=DEV)
+        dp.dp_grad_sample_linear(At, Bt, dp.DP_BF16, N, T, din, dout, 0.9, gW2, gb2, sq2, None, ws)
+        torch.cuda.synchronize()
+        assert torch.equal(gW, gW2), spec
+        if gb is not None:
+            assert torch.equal(gb, gb2), spec
+        assert torch.equal(sq, sq2), spec
+
+
+def test_grouped_bf16_more_layers_than_one_launch():
+    """Eighteen staged layers: two grouped launches, each with its own partials."""
+    say("grad_many 18 bf16 sequence layers")
+    specs = [("lin", 64 + 8 * (k % 3), 128 + 8 * (k % 5), 32 * (1 + k % 2), k % 4 != 1) for k in range(18)]
+    bufs, items = run_many(specs, 3, dp.DP_BF16, 1.2, seed=77)
+    assert all(dp.dp_grad_sample_many_grouped(items, k, dp.DP_BF16, 3) for k in range(len(specs)))
+    check_oracle(specs, bufs, 1.2, "eighteen bf16")
