@@ -55,6 +55,8 @@ def lib():
         L.dpo_embedding.restype = _L
         L.dpo_layernorm.argtypes = [_d, _d, _L, _L, _L, ctypes.c_double, _d, _d]
         L.dpo_groupnorm.argtypes = [_d, _d, _L, _L, _L, ctypes.c_double, _d, _d]
+        L.dpo_lstm_forward.argtypes = [_d, _d, _d, _d, _d, _L, _L, _L, _L, _d, _d, _d]
+        L.dpo_lstm_backward.argtypes = [_d, _d, _d, _d, _d, _L, _L, _L, _d]
         L.dpo_sqnorm_accumulate.argtypes = [_d, _L, _L, _d]
         L.dpo_norms.argtypes = [_d, _L, _d]
         L.dpo_clip_factors.argtypes = [_d, _L, ctypes.c_double, _d]
@@ -144,6 +146,39 @@ def layernorm_grad(xhat, B, scale: float = 1.0):
     gg = np.empty((N, D)); gbt = np.empty((N, D))
     lib().dpo_layernorm(_p(xhat), _p(B), N, T, D, float(scale), _p(gg), _p(gbt))
     return gg, gbt
+
+
+def _opt(a):
+    return None if a is None else _f64(a)
+
+
+def _popt(a):
+    return None if a is None else _p(a)
+
+
+def lstm_forward(x, W_ih, W_hh, b_ih=None, b_hh=None):
+    """LSTM forward (gate order i, f, g, o; zero initial state): returns
+    (gates [N, T, 4H] after their nonlinearities, c [N, T, H], h [N, T, H])."""
+    x = _f64(x); W_ih = _f64(W_ih); W_hh = _f64(W_hh)
+    b_ih = _opt(b_ih); b_hh = _opt(b_hh)
+    N, T, D = x.shape
+    H = W_hh.shape[1]
+    gates = np.empty((N, T, 4 * H)); c = np.empty((N, T, H)); h = np.empty((N, T, H))
+    lib().dpo_lstm_forward(_p(x), _p(W_ih), _p(W_hh), _popt(b_ih), _popt(b_hh), N, T, D, H, _p(gates), _p(c), _p(h))
+    return gates, c, h
+
+
+def lstm_backward(gates, c, W_hh, dh_out=None, dh_last=None):
+    """Backward through time of the LSTM: the gradient of each sample's loss
+    with respect to the gate pre-activations, delta [N, T, 4H], from the
+    stored gates and cell states and the loss gradient at the hidden states
+    (dh_out [N, T, H] at every step and/or dh_last [N, H] at the last)."""
+    gates = _f64(gates); c = _f64(c); W_hh = _f64(W_hh)
+    dh_out = _opt(dh_out); dh_last = _opt(dh_last)
+    N, T, H = c.shape
+    delta = np.empty((N, T, 4 * H))
+    lib().dpo_lstm_backward(_p(gates), _p(c), _p(W_hh), _popt(dh_out), _popt(dh_last), N, T, H, _p(delta))
+    return delta
 
 
 def groupnorm_grad(xhat, B, scale: float = 1.0):

@@ -208,6 +208,98 @@ void dpo_groupnorm(const double *xhat, const double *B, long N, long C, long P,
 }
 
 /* ---------------------------------------------------------------------------
+ * The LSTM's recurrence (the paper's DPLSTM module: a recurrent layer whose
+ * per-sample gradients need its backward through time; its weights act as a
+ * Linear layer on the input x_t and one on the previous hidden state h_{t-1},
+ * both fed the same gate backprop).  Gate order i, f, g, o, as in PyTorch's
+ * LSTM; zero initial state.
+ * ------------------------------------------------------------------------- */
+
+static double sigmoid(double z) { return 1.0 / (1.0 + exp(-z)); }
+
+/* Forward over T steps (used by the tests to produce consistent activations):
+ *   z_t = W_ih x_t + b_ih + W_hh h_{t-1} + b_hh                 [4H]
+ *   i = sig(z_i), f = sig(z_f), g = tanh(z_g), o = sig(z_o)
+ *   c_t = f * c_{t-1} + i * g,   h_t = o * tanh(c_t),   h_{-1} = c_{-1} = 0
+ * x [N][T][D], W_ih [4H][D], W_hh [4H][H], b_* [4H] (may be NULL);
+ * gates [N][T][4H] (i, f, g, o after their nonlinearities), c, h [N][T][H]. */
+void dpo_lstm_forward(const double *x, const double *W_ih, const double *W_hh, const double *b_ih,
+                      const double *b_hh, long N, long T, long D, long H, double *gates, double *c,
+                      double *h)
+{
+#pragma omp parallel for schedule(static)
+    for (long n = 0; n < N; n++) {
+        for (long t = 0; t < T; t++) {
+            double *gt = gates + (n * T + t) * 4 * H;
+            for (long r = 0; r < 4 * H; r++) {
+                double z = (b_ih ? b_ih[r] : 0.0) + (b_hh ? b_hh[r] : 0.0);
+                for (long d = 0; d < D; d++)
+                    z += W_ih[r * D + d] * x[(n * T + t) * D + d];
+                if (t > 0)
+                    for (long k = 0; k < H; k++)
+                        z += W_hh[r * H + k] * h[(n * T + t - 1) * H + k];
+                gt[r] = (r >= 2 * H && r < 3 * H) ? tanh(z) : sigmoid(z);
+            }
+            for (long k = 0; k < H; k++) {
+                double cp = t > 0 ? c[(n * T + t - 1) * H + k] : 0.0;
+                double ct = gt[H + k] * cp + gt[k] * gt[2 * H + k];
+                c[(n * T + t) * H + k] = ct;
+                h[(n * T + t) * H + k] = gt[3 * H + k] * tanh(ct);
+            }
+        }
+    }
+}
+
+/* Backward through time: the gradient of sample n's loss with respect to the
+ * gate pre-activations z_t (the backprop B that both weight matrices' per-
+ * sample gradients take), from the stored gate activations and cell states
+ * and the loss gradient arriving at the hidden states (dh_out[n][t][k], or
+ * NULL for none, plus dh_last[n][k] at the last step, or NULL).  For t from
+ * T-1 down to 0, with dh_rec = W_hh^T delta_{t+1} (0 at t = T-1), dc_{T} = 0,
+ * f_{T} = 0 and c_{-1} = 0, by the chain rule through the equations above:
+ *   dh      = dh_out_t (+ dh_last at T-1) + dh_rec
+ *   dc_t    = dh * o * (1 - tanh(c_t)^2) + dc_{t+1} * f_{t+1}
+ *   delta_i = dc_t * g * i (1 - i)          delta_f = dc_t * c_{t-1} * f (1 - f)
+ *   delta_g = dc_t * i * (1 - g^2)          delta_o = dh * tanh(c_t) * o (1 - o)
+ * gates [N][T][4H], c [N][T][H], W_hh [4H][H]; delta [N][T][4H].            */
+void dpo_lstm_backward(const double *gates, const double *c, const double *W_hh, const double *dh_out,
+                       const double *dh_last, long N, long T, long H, double *delta)
+{
+#pragma omp parallel for schedule(static)
+    for (long n = 0; n < N; n++) {
+        double *dc_next = calloc((size_t)H, sizeof(double));
+        double *f_next = calloc((size_t)H, sizeof(double));
+        for (long t = T - 1; t >= 0; t--) {
+            const double *gt = gates + (n * T + t) * 4 * H;
+            double *dt = delta + (n * T + t) * 4 * H;
+            for (long k = 0; k < H; k++) {
+                double dh = dh_out ? dh_out[(n * T + t) * H + k] : 0.0;
+                if (t == T - 1 && dh_last)
+                    dh += dh_last[n * H + k];
+                if (t < T - 1) {
+                    const double *dn = delta + (n * T + t + 1) * 4 * H;
+                    for (long r = 0; r < 4 * H; r++)
+                        dh += W_hh[r * H + k] * dn[r];
+                }
+                double i = gt[k], f = gt[H + k], g = gt[2 * H + k], o = gt[3 * H + k];
+                double ct = c[(n * T + t) * H + k];
+                double cp = t > 0 ? c[(n * T + t - 1) * H + k] : 0.0;
+                double tc = tanh(ct);
+                double dc = dh * o * (1.0 - tc * tc) + dc_next[k] * f_next[k];
+                dt[k] = dc * g * i * (1.0 - i);
+                dt[H + k] = dc * cp * f * (1.0 - f);
+                dt[2 * H + k] = dc * i * (1.0 - g * g);
+                dt[3 * H + k] = dh * tc * o * (1.0 - o);
+                dc_next[k] = dc;
+                f_next[k] = f;
+            }
+        }
+        free(dc_next);
+        free(f_next);
+    }
+}
+
+/* ---------------------------------------------------------------------------
  * Norms, clipping, clipped sum (the DP-SGD step of section 1, figure 1)
  * ------------------------------------------------------------------------- */
 

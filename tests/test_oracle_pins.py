@@ -468,3 +468,67 @@ def test_workload_parameter_counts_match_the_paper():
     assert W.get("linear_tiny").n_params == 1040
     for wl in W.WORKLOADS.values():
         assert sum(int(np.prod(s)) for _, s in wl.param_tensors()) == wl.n_params
+
+
+def _torch_lstm(D, H, W_ih, W_hh, b_ih, b_hh):
+    import torch
+    m = torch.nn.LSTM(D, H, batch_first=True).double()
+    with torch.no_grad():
+        m.weight_ih_l0.copy_(torch.from_numpy(W_ih))
+        m.weight_hh_l0.copy_(torch.from_numpy(W_hh))
+        m.bias_ih_l0.copy_(torch.from_numpy(b_ih))
+        m.bias_hh_l0.copy_(torch.from_numpy(b_hh))
+    return m
+
+
+def test_lstm_forward_matches_torch():
+    import torch
+    r = rng(90)
+    N, T, D, H = 3, 7, 5, 4
+    x = r.standard_normal((N, T, D))
+    W_ih, W_hh = r.standard_normal((4 * H, D)) * 0.6, r.standard_normal((4 * H, H)) * 0.6
+    b_ih, b_hh = r.standard_normal(4 * H) * 0.3, r.standard_normal(4 * H) * 0.3
+    gates, c, h = oracle.lstm_forward(x, W_ih, W_hh, b_ih, b_hh)
+    m = _torch_lstm(D, H, W_ih, W_hh, b_ih, b_hh)
+    with torch.no_grad():
+        hy, (hT, cT) = m(torch.from_numpy(x))
+    np.testing.assert_allclose(h, hy.numpy(), rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(c[:, -1], cT[0].numpy(), rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(h, gates[..., 3 * H:] * np.tanh(c), rtol=1e-13)
+
+
+@pytest.mark.parametrize("per_step", [False, True])
+def test_lstm_backward_gives_the_autograd_gradients_of_each_sample(per_step):
+    """The gate backprop delta of the backward through time, fed to the
+    Linear per-sample gradient (A = x_t for W_ih, A = h_{t-1} for W_hh), gives
+    torch autograd's gradients of each sample's own loss (a batch of one, the
+    micro-batch definition) for all four LSTM parameters, and delta W_ih is
+    the gradient at the input."""
+    import torch
+    r = rng(91 + per_step)
+    N, T, D, H = 3, 6, 5, 4
+    x = r.standard_normal((N, T, D))
+    W_ih, W_hh = r.standard_normal((4 * H, D)) * 0.6, r.standard_normal((4 * H, H)) * 0.6
+    b_ih, b_hh = r.standard_normal(4 * H) * 0.3, r.standard_normal(4 * H) * 0.3
+    dh_last = r.standard_normal((N, H))
+    dh_out = r.standard_normal((N, T, H)) if per_step else None
+    gates, c, h = oracle.lstm_forward(x, W_ih, W_hh, b_ih, b_hh)
+    delta = oracle.lstm_backward(gates, c, W_hh, dh_out=dh_out, dh_last=dh_last)
+    h_prev = np.zeros_like(h)
+    h_prev[:, 1:] = h[:, :-1]
+    gWi, gbi = oracle.linear_grad(x, delta)
+    gWh, gbh = oracle.linear_grad(h_prev, delta)
+    m = _torch_lstm(D, H, W_ih, W_hh, b_ih, b_hh)
+    for n in range(N):
+        m.zero_grad()
+        xt = torch.from_numpy(x[n:n + 1].copy()).requires_grad_(True)
+        hy, _ = m(xt)
+        loss = (hy[0, -1] * torch.from_numpy(dh_last[n])).sum()
+        if per_step:
+            loss = loss + (hy[0] * torch.from_numpy(dh_out[n])).sum()
+        loss.backward()
+        np.testing.assert_allclose(gWi[n], m.weight_ih_l0.grad.numpy(), rtol=1e-10, atol=1e-13)
+        np.testing.assert_allclose(gbi[n], m.bias_ih_l0.grad.numpy(), rtol=1e-10, atol=1e-13)
+        np.testing.assert_allclose(gWh[n], m.weight_hh_l0.grad.numpy(), rtol=1e-10, atol=1e-13)
+        np.testing.assert_allclose(gbh[n], m.bias_hh_l0.grad.numpy(), rtol=1e-10, atol=1e-13)
+        np.testing.assert_allclose(delta[n] @ W_ih, xt.grad[0].numpy(), rtol=1e-10, atol=1e-13)
