@@ -119,6 +119,11 @@ def call_costs(st, nnz=None):
             # reads row_ptr, the ids, the rows and the norms; writes the dense [V][D] sum
             out["clip:" + L.name] = ((N + 1) * 8 + u * (L.D * 4 + 8) + N * 4 + L.V * L.D * 4, 2 * u * L.D,
                                      "emb_clipsum_kernel", None)
+        elif isinstance(L, W.LSTMRecurrence):
+            # reads the stored gates and cell states, W_hh and dh_last; writes the gate backprop
+            G = 4 * L.H
+            out["grad:" + L.name] = (N * L.T * (2 * G + L.H) * 4 + G * L.H * 4 + N * L.H * 4,
+                                     2 * N * L.T * G * L.H, "lstm_bptt_kernel", None)
         elif isinstance(L, W.LayerNorm):
             out["grad:" + L.name] = (2 * N * L.T * L.D * e + 2 * N * L.D * 4, 3 * N * L.T * L.D,
                                      "ln_partial_kernel", None)
@@ -181,6 +186,7 @@ KERNEL_SOURCES = {
     "emb_rows_kernel": ["paper_2109_12298_amd/csrc/embedding.hip"],
     "emb_clipsum_kernel": ["paper_2109_12298_amd/csrc/clip.hip"],
     "ln_partial_kernel": ["paper_2109_12298_amd/csrc/layernorm.hip"],
+    "lstm_bptt_kernel": ["paper_2109_12298_amd/csrc/lstm.hip"],
     "add_noise_kernel": ["paper_2109_12298_amd/csrc/noise.hip"],
     "colsum_many_kernel+finish_many_kernel": ["paper_2109_12298_amd/csrc/group.hip",
                                               "paper_2109_12298_amd/csrc/philox.hpp"],

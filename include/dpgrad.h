@@ -256,6 +256,26 @@ dp_status dp_grad_sample_groupnorm(const void *xhat, const void *B, dp_dtype dt,
                                    int64_t P, float scale, float *ggamma, float *gbeta, float *sqnorm,
                                    int32_t *status, void *ws, size_t ws_bytes, hipStream_t stream);
 
+/* Backward through time of an LSTM layer (the paper's DPLSTM: its recurrent
+ * modules are the layers whose per-sample gradients cost it most): the
+ * gradient of each sample's loss with respect to the gate pre-activations,
+ * delta, which the per-sample gradients of W_ih (A = x_t) and W_hh
+ * (A = h_{t-1}) and of both biases take as B (dp_grad_sample_linear with
+ * T positions).  PyTorch's gate order i, f, g, o; zero initial state.  For t
+ * = T-1 down to 0, with dc_T = 0, f_T = 0, c_{-1} = 0:
+ *   dh      = dh_out[t] (+ dh_last at T-1) + W_hh^T delta_{t+1}   (no term at T-1)
+ *   dc_t    = dh * o * (1 - tanh(c_t)^2) + dc_{t+1} * f_{t+1}
+ *   delta_i = dc_t * g * i * (1 - i)        delta_f = dc_t * c_{t-1} * f * (1 - f)
+ *   delta_g = dc_t * i * (1 - g^2)          delta_o = dh * tanh(c_t) * o * (1 - o)
+ * gates fp32 [N][T][4H]: i, f, g, o after their nonlinearities (as stored by
+ * the forward); c fp32 [N][T][H]: cell states; W_hh fp32 [4H][H]; dh_out fp32
+ * [N][T][H] or NULL (loss gradient at every hidden state); dh_last fp32 [N][H]
+ * or NULL (at the last one); delta fp32 [N][T][4H] (written).  Needs
+ * 1 <= H <= 128 (else DP_EINVAL / DP_EUNSUPPORTED); N < 2^31. */
+dp_status dp_lstm_backward(const float *gates, const float *c, const float *W_hh, const float *dh_out,
+                           const float *dh_last, int64_t N, int64_t T, int64_t H, float *delta,
+                           int32_t *status, hipStream_t stream);
+
 /* ---------------------------------------------------------------------------
  * Norms and clipping
  * ------------------------------------------------------------------------- */

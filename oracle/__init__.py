@@ -305,10 +305,20 @@ def dp_step(wl, inputs, step: int = 0, C: Optional[float] = None, sigma: Optiona
     denom = float(N) if denom is None else denom
     grads: List[Dict[str, object]] = []
     sq_layers = []
+    derived: Dict[str, np.ndarray] = {}
     for li in inputs:
         layer = li.layer
+        if isinstance(layer, W.LSTMRecurrence):
+            # the gate backprop of the LSTM's weights, by the backward through
+            # time; the recurrence has no parameters of its own
+            a = li.aux
+            derived[layer.name] = lstm_backward(a["gates"], a["c"], a["W_hh"], dh_last=a["dh_last"])
+            grads.append({})
+            sq_layers.append(np.zeros(N))
+            continue
+        B = derived[layer.bsource] if getattr(layer, "bsource", None) else li.B
         dev = W.LayerInputs(layer, A=W.rounded_like_device(wl, li.A),
-                            B=W.rounded_like_device(wl, li.B), ids=li.ids)
+                            B=W.rounded_like_device(wl, B), ids=li.ids)
         g = layer_grads(layer, dev, scale)
         sq = np.zeros(N)
         if "csr" in g:
@@ -340,4 +350,4 @@ def dp_step(wl, inputs, step: int = 0, C: Optional[float] = None, sigma: Optiona
         for pidx, (pname, shape) in enumerate(wl.param_tensors()):
             out[pname] = add_noise(S[pname], wl.seed, step, pidx, sigma, C, denom)
     return {"grads": grads, "sq_layers": np.stack(sq_layers), "norm": norm, "c": c, "S": S,
-            "out": out}
+            "out": out, "derived": derived}

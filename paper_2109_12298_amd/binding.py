@@ -51,6 +51,7 @@ SIGNATURES = {
     "dp_grad_sample_layernorm": (_ST, [_P, _P, _ST, _I64, _I64, _I64, _F, _P, _P, _P, _P, _P, _SZ, _P]),
     "dp_grad_sample_groupnorm_workspace_bytes": (_SZ, [_I64, _I64, _I64]),
     "dp_grad_sample_groupnorm": (_ST, [_P, _P, _ST, _I64, _I64, _I64, _F, _P, _P, _P, _P, _P, _SZ, _P]),
+    "dp_lstm_backward": (_ST, [_P, _P, _P, _P, _P, _I64, _I64, _I64, _P, _P, _P]),
     "dp_per_sample_norms": (_ST, [_P, _I32, _I64, _P, _P, _P]),
     "dp_per_sample_norms_active": (_ST, [_P, _I32, _I64, _P, _P, _P, _P]),
     "dp_ghost_norm_linear_workspace_bytes": (_SZ, [_I64, _I64, _I64, _I64]),
@@ -310,6 +311,11 @@ def dp_grad_sample_embedding(ids, B, dt, N, T, V, D, scale, row_ptr, uniq_ids, r
                                           _ptr(uniq_ids), _ptr(rows), cap, _ptr(sqnorm), _ptr(status),
                                           _ptr(ws), _nbytes(ws), _stream(stream)),
            "dp_grad_sample_embedding")
+
+
+def dp_lstm_backward(gates, c, W_hh, dh_out, dh_last, N, T, H, delta, status=None, stream=None):
+    _check(lib().dp_lstm_backward(_ptr(gates), _ptr(c), _ptr(W_hh), _ptr(dh_out), _ptr(dh_last), N, T, H,
+                                  _ptr(delta), _ptr(status), _stream(stream)), "dp_lstm_backward")
 
 
 def dp_grad_sample_layernorm_workspace_bytes(N, T, D) -> int:

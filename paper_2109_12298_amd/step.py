@@ -57,6 +57,7 @@ class LayerBufs:
     ghost: bool = False         # norm from the Gram matrices, no per-sample gradient
     ws: object = None          # scratch of the per-sample-gradient call
     ws_clip: object = None     # scratch of the fused clipped sum
+    aux: object = None         # LSTMRecurrence: stored gates, cell states, W_hh, dh_last
 
 
 def _torch():
@@ -123,7 +124,7 @@ class DPStep:
         torch = _torch()
         self.wl = wl
         self.device = torch.device(device)
-        self.N = int(inputs[0].B.shape[0])
+        self.N = int(next(li.B.shape[0] for li in inputs if li.B is not None))
         self.C = float(wl.C if C is None else C)
         self.sigma = float(wl.sigma if sigma is None else sigma)
         self.sigma_tab = None
@@ -136,8 +137,7 @@ class DPStep:
         if variable_batch:
             if self.sigma_tab is None:   # the schedule entry point carries the batch size
                 self.sigma_tab = torch.tensor([self.sigma], dtype=torch.float32, device=torch.device(device))
-            self.n_active = torch.tensor([int(inputs[0].B.shape[0])], dtype=torch.int64,
-                                         device=torch.device(device))
+            self.n_active = torch.tensor([self.N], dtype=torch.int64, device=torch.device(device))
         self.virtual_batches = int(virtual_batches)
         if self.virtual_batches < 1:
             raise ValueError("virtual_batches must be >= 1")
@@ -148,12 +148,22 @@ class DPStep:
         N = self.N
         f32 = dict(dtype=torch.float32, device=self.device)
         self.layers: List[LayerBufs] = []
+        self.recurrences: Dict[str, object] = {}      # LSTMRecurrence name -> its gate backprop buffer
         for li in inputs:
             layer = li.layer
             lb = LayerBufs(layer)
             if li.A is not None:
                 lb.A = to_device(li.A, wl.dtype, self.device)
-            lb.B = to_device(li.B, wl.dtype, self.device)
+            if isinstance(layer, W.LSTMRecurrence):
+                # stored forward activations in, the gate backprop (B of the
+                # LSTM's weight layers) out
+                lb.aux = {k: to_device(v, W.F32, self.device) for k, v in li.aux.items()}
+                lb.B = torch.empty((N, layer.T, 4 * layer.H), **f32)
+                self.recurrences[layer.name] = lb.B
+            elif getattr(layer, "bsource", None):
+                lb.B = self.recurrences[layer.bsource]
+            else:
+                lb.B = to_device(li.B, wl.dtype, self.device)
             need_g = need_c = 0
             if isinstance(layer, W.Linear):
                 lb.clip_mode = linear_clip_mode(layer, N, wl.dtype) if clip_mode == "auto" else clip_mode
@@ -192,6 +202,9 @@ class DPStep:
             lb.ws_clip = torch.empty(max(need_c, 256), dtype=torch.uint8, device=self.device)
             self.layers.append(lb)
         self.sqnorm = torch.empty((len(self.layers), N), **f32)
+        for i, lb in enumerate(self.layers):
+            if isinstance(lb.layer, W.LSTMRecurrence):
+                self.sqnorm[i].zero_()            # no parameters: its row stays zero
         self.norm = torch.empty(N, **f32)
         self.status = torch.zeros(1, dtype=torch.int32, device=self.device)
         self.params = wl.param_tensors()
@@ -285,10 +298,15 @@ class DPStep:
                                        L.stride[1], L.pad[0], L.pad[1], self.scale, lb.gW, lb.gb, sq)
         return None
 
+    def recurrence_calls(self) -> List[str]:
+        """Backward-through-time calls, which the gradient calls of the layers they feed wait for."""
+        return ["grad:" + lb.layer.name for lb in self.layers if isinstance(lb.layer, W.LSTMRecurrence)]
+
     def grad_calls(self) -> List[str]:
-        """The per-sample-gradient calls of a step, in order."""
+        """The per-sample-gradient calls of a step, in order (after the recurrences)."""
         calls = ["grad:group"] if self.grad_group else []
-        return calls + ["grad:" + lb.layer.name for i, lb in enumerate(self.layers) if i not in self.grad_group]
+        return calls + ["grad:" + lb.layer.name for i, lb in enumerate(self.layers)
+                        if i not in self.grad_group and not isinstance(lb.layer, W.LSTMRecurrence)]
 
     # ------------------------------------------------------------------ pieces
     def grad_group_call(self, stream=None):
@@ -300,7 +318,11 @@ class DPStep:
         lb = self.layers[i]
         layer = lb.layer
         N, s, sq = self.N, self.scale, self.sqnorm[i]
-        if isinstance(layer, W.Linear) and lb.ghost:
+        if isinstance(layer, W.LSTMRecurrence):
+            a = lb.aux
+            dp.dp_lstm_backward(a["gates"], a["c"], a["W_hh"], None, a["dh_last"], N, layer.T, layer.H, lb.B,
+                                self.status, stream)
+        elif isinstance(layer, W.Linear) and lb.ghost:
             dp.dp_ghost_norm_linear(lb.A, lb.B, self.dt, N, layer.T, layer.d_in, layer.d_out, s, layer.bias, sq,
                                     self.status, lb.ws, stream)
         elif isinstance(layer, W.Linear):
@@ -420,7 +442,7 @@ class DPStep:
         if not parallel:
             if advance:
                 dp.dp_step_advance(step_dev, advance, stream)
-            for name in self.grad_calls():
+            for name in self.recurrence_calls() + self.grad_calls():
                 if mark: mark(name, "start")
                 self.call(name, step, stream)
                 if mark: mark(name, "end")
@@ -443,6 +465,8 @@ class DPStep:
             return
         main = torch.cuda.current_stream(self.device)
         side = self._fork(len(self.layers) + 1)
+        for name in self.recurrence_calls():      # before the branches that read their output
+            self.call(name, step)
         for k, name in enumerate(self.grad_calls()):
             side[k].wait_stream(main)
             with torch.cuda.stream(side[k]):
@@ -532,7 +556,11 @@ class DPStep:
         for lb, li in zip(self.layers, inputs):
             if li.A is not None:
                 lb.A.copy_(to_device(li.A, self.wl.dtype, self.device))
-            lb.B.copy_(to_device(li.B, self.wl.dtype, self.device))
+            if li.aux is not None:
+                for k, v in li.aux.items():
+                    lb.aux[k].copy_(to_device(v, W.F32, self.device))
+            if li.B is not None:
+                lb.B.copy_(to_device(li.B, self.wl.dtype, self.device))
             if li.ids is not None:
                 lb.ids.copy_(to_device(li.ids, "", self.device))
 
@@ -556,8 +584,12 @@ class DPStep:
                "out": {k: v.cpu().numpy() for k, v in self.out.items()},
                "status": int(self.status.cpu().item()),
                "acc": {k: v.cpu().numpy() for k, v in self.acc.items()}}
+        res["derived"] = {lb.layer.name: lb.B.cpu().numpy() for lb in self.layers
+                          if isinstance(lb.layer, W.LSTMRecurrence)}
         for lb in self.layers:
-            if isinstance(lb.layer, W.Embedding):
+            if isinstance(lb.layer, W.LSTMRecurrence):
+                res["grads"].append({})            # no parameters of its own
+            elif isinstance(lb.layer, W.Embedding):
                 rp = lb.row_ptr.cpu().numpy()
                 nnz = int(rp[-1])
                 res["grads"].append({"csr": (rp, lb.uniq[:nnz].cpu().numpy(), lb.rows[:nnz].cpu().numpy())})

@@ -20,6 +20,12 @@ Stand-ins: the paper trains on MNIST, CIFAR-10 and IMDb (section 3.1.2).  No
 dataset item is used; the activations and backprops below have the shapes of
 those networks' layers and simple distributions (N(0,1), post-ReLU
 max(0, N(0,1)), backprops N(0,1)/batch, token ids Zipf(1.1)).
+
+One workload (``text_lstm_bptt``) stores what an LSTM's forward pass keeps:
+its gate activations, cell states and hidden states over the sequence, from
+a forward over the embedded tokens with randomly initialised weights (the
+model's own forward, run here in numpy; the DP step starts after it).  Its
+gate backprop is not drawn: the step derives it by the backward through time.
 """
 from __future__ import annotations
 
@@ -44,8 +50,9 @@ class Linear:
     d_out: int
     T: int = 1
     bias: bool = True
-    act: str = "normal"          # distribution of A: normal | relu | tanh_prev | tanh_last | embed
+    act: str = "normal"          # A: normal | relu | tanh_prev | tanh_last | embed | lstm_x | lstm_hprev | lstm_hlast
     bshare: Optional[str] = None  # name of a layer whose B this layer reuses (LSTM W_ih / W_hh)
+    bsource: Optional[str] = None  # name of an LSTMRecurrence whose derived gate backprop is this layer's B
 
     @property
     def n_params(self) -> int:
@@ -113,6 +120,25 @@ class GroupNorm:
     @property
     def n_params(self) -> int:
         return 2 * self.C
+
+
+@dataclass(frozen=True)
+class LSTMRecurrence:
+    """The backward through time of an LSTM layer (input D, hidden H, T steps).
+
+    It has no parameters of its own: the LSTM's weights are the Linear layers
+    that name it as ``bsource`` (W_ih over x_t, W_hh over h_{t-1}, each with
+    its bias), and their per-sample gradients take the gate backprop this
+    layer derives, from the stored gate activations and cell states and the
+    loss gradient arriving at the last hidden state, as B."""
+    name: str
+    D: int
+    H: int
+    T: int
+
+    @property
+    def n_params(self) -> int:
+        return 0
 
 
 @dataclass(frozen=True)
@@ -186,6 +212,15 @@ def _build_workloads() -> Dict[str, Workload]:
                 Linear("lstm_ih", 100, 400, T=256, act="embed"),
                 Linear("lstm_hh", 100, 400, T=256, act="tanh_prev", bshare="lstm_ih"),
                 Linear("fc", 100, 2, act="tanh_last")))
+    # The text LSTM with its gate backprop derived by the backward through time
+    # from a forward pass's stored activations (same shapes and parameters).
+    w["text_lstm_bptt"] = Workload(
+        6, "text_lstm_bptt", N=64, dtype=F32, C=1.0, sigma=1.0,
+        layers=(Embedding("emb", 10000, 100, 256),
+                LSTMRecurrence("lstm", 100, 100, 256),
+                Linear("lstm_ih", 100, 400, T=256, act="lstm_x", bsource="lstm"),
+                Linear("lstm_hh", 100, 400, T=256, act="lstm_hprev", bsource="lstm"),
+                Linear("fc", 100, 2, act="lstm_hlast")))
     # Transformer encoder block, bf16 activations/backprops.
     w["transformer_block"] = Workload(
         4, "transformer_block", N=32, dtype=BF16, C=1.0, sigma=0.8,
@@ -209,7 +244,8 @@ def _build_workloads() -> Dict[str, Workload]:
 
 
 WORKLOADS: Dict[str, Workload] = _build_workloads()
-WORKLOAD_ORDER = ["linear_tiny", "mnist_cnn", "cifar_cnn", "text_lstm", "transformer_block", "cifar_gn"]
+WORKLOAD_ORDER = ["linear_tiny", "mnist_cnn", "cifar_cnn", "text_lstm", "transformer_block", "cifar_gn",
+                  "text_lstm_bptt"]
 
 
 def get(name: str) -> Workload:
@@ -239,8 +275,32 @@ def _zipf_ids(rng, shape, V: int, s: float, truncate: bool) -> np.ndarray:
 class LayerInputs:
     layer: object
     A: Optional[np.ndarray] = None     # activation (fp32 array; bf16 workloads round later)
-    B: Optional[np.ndarray] = None     # backprop at the layer output
+    B: Optional[np.ndarray] = None     # backprop at the layer output (None: derived by the step)
     ids: Optional[np.ndarray] = None   # int64 token ids (embedding)
+    aux: Optional[Dict[str, np.ndarray]] = None   # LSTMRecurrence: gates, c, W_hh, dh_last
+
+
+def _sigmoid(z):
+    return 1.0 / (1.0 + np.exp(-z))
+
+
+def lstm_forward_activations(x: np.ndarray, W_ih, W_hh, b_ih, b_hh):
+    """The stored activations of an LSTM forward over x [N, T, D] (gate order
+    i, f, g, o, zero initial state), in float64: gates after their
+    nonlinearities [N, T, 4H], cell states and hidden states [N, T, H]."""
+    N, T, _ = x.shape
+    H = W_hh.shape[1]
+    gates = np.empty((N, T, 4 * H)); c = np.empty((N, T, H)); h = np.empty((N, T, H))
+    hp = np.zeros((N, H)); cp = np.zeros((N, H))
+    for t in range(T):
+        z = x[:, t] @ W_ih.T + b_ih + hp @ W_hh.T + b_hh
+        i, f, g, o = _sigmoid(z[:, :H]), _sigmoid(z[:, H:2 * H]), np.tanh(z[:, 2 * H:3 * H]), _sigmoid(z[:, 3 * H:])
+        cp = f * cp + i * g
+        hp = o * np.tanh(cp)
+        gates[:, t] = np.concatenate([i, f, g, o], axis=1)
+        c[:, t] = cp
+        h[:, t] = hp
+    return gates, c, h
 
 
 def make_inputs(wl: Workload, n: Optional[int] = None) -> List[LayerInputs]:
@@ -257,6 +317,7 @@ def make_inputs(wl: Workload, n: Optional[int] = None) -> List[LayerInputs]:
     emb_table = None
     emb_ids = None
     lstm_hidden = None
+    lstm_fwd = None           # (x, h) of an LSTMRecurrence's forward pass
     for layer in wl.layers:
         li = LayerInputs(layer)
         if isinstance(layer, Conv2d):
@@ -282,6 +343,15 @@ def make_inputs(wl: Workload, n: Optional[int] = None) -> List[LayerInputs]:
                 if emb_table is None:
                     emb_table = _normal(rA, (by_name_emb(wl).V, by_name_emb(wl).D))
                 a = emb_table[emb_ids]
+            elif layer.act in ("lstm_x", "lstm_hprev", "lstm_hlast"):
+                x, h = lstm_fwd
+                if layer.act == "lstm_x":
+                    a = x
+                elif layer.act == "lstm_hprev":
+                    a = np.zeros_like(h)
+                    a[:, 1:, :] = h[:, :-1, :]
+                else:
+                    a = np.ascontiguousarray(h[:, -1, :])
             elif layer.act in ("tanh_prev", "tanh_last"):
                 if lstm_hidden is None:
                     T = layer.T if layer.T > 1 else max(l.T for l in wl.layers if isinstance(l, Linear))
@@ -294,7 +364,9 @@ def make_inputs(wl: Workload, n: Optional[int] = None) -> List[LayerInputs]:
             else:
                 raise ValueError(layer.act)
             li.A = np.ascontiguousarray(a, dtype=np.float32)
-            if layer.bshare is not None:
+            if layer.bsource is not None:
+                li.B = None                      # derived by the step (backward through time)
+            elif layer.bshare is not None:
                 li.B = by_name[layer.bshare].B
             else:
                 li.B = _normal(rB, shapeB) / np.float32(wl.N)
@@ -304,6 +376,28 @@ def make_inputs(wl: Workload, n: Optional[int] = None) -> List[LayerInputs]:
             li.ids = _zipf_ids(rA, (N, layer.T), layer.V, layer.zipf_s, layer.truncate)
             emb_ids = li.ids
             li.B = _normal(rB, (N, layer.T, layer.D)) / np.float32(wl.N)
+        elif isinstance(layer, LSTMRecurrence):
+            # the embedding table, the LSTM's weights (PyTorch's default
+            # U(-1/sqrt(H), 1/sqrt(H)) init) and the loss gradient at the last
+            # hidden state; the forward pass gives what it stores
+            rE = _rng(wl.wid, tid); tid += 1
+            rW = _rng(wl.wid, tid); tid += 1
+            rD = _rng(wl.wid, tid); tid += 1
+            emb = by_name_emb(wl)
+            E = _normal(rE, (emb.V, emb.D))
+            k = 1.0 / np.sqrt(layer.H)
+            G = 4 * layer.H
+            W_ih = rW.uniform(-k, k, (G, layer.D)).astype(np.float32)
+            W_hh = rW.uniform(-k, k, (G, layer.H)).astype(np.float32)
+            b_ih = rW.uniform(-k, k, G).astype(np.float32)
+            b_hh = rW.uniform(-k, k, G).astype(np.float32)
+            x = E[emb_ids].astype(np.float32)
+            gates, c, h = lstm_forward_activations(x.astype(np.float64), W_ih.astype(np.float64),
+                                                   W_hh.astype(np.float64), b_ih.astype(np.float64),
+                                                   b_hh.astype(np.float64))
+            lstm_fwd = (x, h.astype(np.float32))
+            li.aux = {"gates": gates.astype(np.float32), "c": c.astype(np.float32), "W_hh": W_hh,
+                      "dh_last": _normal(rD, (N, layer.H)) / np.float32(wl.N)}
         elif isinstance(layer, LayerNorm):
             rA = _rng(wl.wid, tid); tid += 1
             rB = _rng(wl.wid, tid); tid += 1
@@ -319,6 +413,23 @@ def make_inputs(wl: Workload, n: Optional[int] = None) -> List[LayerInputs]:
             raise TypeError(layer)
         out.append(li)
         by_name[layer.name] = li
+    return out
+
+
+# entries of LayerInputs.aux that are per sample (the first axis is the batch)
+_AUX_PER_SAMPLE = ("gates", "c", "dh_last")
+
+
+def take_samples(inputs: List[LayerInputs], idx) -> List[LayerInputs]:
+    """The same layers' inputs for the samples ``idx`` (an index array or a slice)."""
+    out = []
+    for li in inputs:
+        aux = None
+        if li.aux is not None:
+            aux = {k: (v[idx] if k in _AUX_PER_SAMPLE else v) for k, v in li.aux.items()}
+        out.append(LayerInputs(li.layer, A=None if li.A is None else li.A[idx],
+                               B=None if li.B is None else li.B[idx],
+                               ids=None if li.ids is None else li.ids[idx], aux=aux))
     return out
 
 

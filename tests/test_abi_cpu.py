@@ -91,6 +91,16 @@ def test_noalloc_linear_validation():
     assert code_of(f, FAKE, FAKE, dp.DP_F32, 2, 2, 8, 8, 1.0, None, stream=0) == dp.DP_EINVAL
 
 
+def test_lstm_backward_validation():
+    f = dp.dp_lstm_backward
+    assert code_of(f, FAKE, FAKE, FAKE, None, FAKE, 2, 5, 129, FAKE, stream=0) == dp.DP_EUNSUPPORTED
+    assert code_of(f, FAKE, FAKE, FAKE, None, FAKE, 2, 5, 0, FAKE, stream=0) == dp.DP_EINVAL
+    assert code_of(f, None, FAKE, FAKE, None, FAKE, 2, 5, 100, FAKE, stream=0) == dp.DP_EINVAL
+    assert code_of(f, FAKE, FAKE, FAKE, None, FAKE, 2, 5, 100, None, stream=0) == dp.DP_EINVAL
+    assert code_of(f, FAKE, FAKE, FAKE, None, FAKE, -1, 5, 100, FAKE, stream=0) == dp.DP_EINVAL
+    assert code_of(f, None, None, None, None, None, 0, 5, 100, None, stream=0) == dp.DP_OK   # nothing to do
+
+
 def test_embedding_layernorm_validation():
     f = dp.dp_grad_sample_embedding
     assert code_of(f, FAKE, FAKE, dp.DP_F32, 2, 5000, 10, 4, 1.0, FAKE, FAKE, FAKE, 10, stream=0) == \

@@ -34,23 +34,21 @@ def device_values(wl, a):
 
 
 def sub_inputs(wl, inputs, idx):
-    out = []
-    for li in inputs:
-        out.append(W.LayerInputs(li.layer, A=None if li.A is None else li.A[idx],
-                                 B=li.B[idx], ids=None if li.ids is None else li.ids[idx]))
-    return out
+    return W.take_samples(inputs, idx)
 
 
 _DEVICE_VALUES = {}
 
 
-def element_grads(wl, li, key, index, scale):
-    """Per-sample gradient of one parameter element for every sample (oracle, sliced inputs)."""
+def element_grads(wl, li, key, index, scale, derived=None):
+    """Per-sample gradient of one parameter element for every sample (oracle,
+    sliced inputs; a layer whose backprop is derived takes it from `derived`)."""
     layer = li.layer
     ck = (wl.name, layer.name)
     if ck not in _DEVICE_VALUES:
         _DEVICE_VALUES.clear()
-        _DEVICE_VALUES[ck] = (device_values(wl, li.A), device_values(wl, li.B))
+        B = derived[layer.bsource] if getattr(layer, "bsource", None) else li.B
+        _DEVICE_VALUES[ck] = (device_values(wl, li.A), device_values(wl, B))
     A, B = _DEVICE_VALUES[ck]
     if isinstance(layer, W.Linear):
         if A.ndim == 2:
@@ -92,7 +90,7 @@ def element_grads(wl, li, key, index, scale):
 
 
 @pytest.mark.parametrize("name", ["linear_tiny", "mnist_cnn", "cifar_cnn", "text_lstm", "transformer_block",
-                                  "cifar_gn"])
+                                  "cifar_gn", "text_lstm_bptt"])
 def test_full_size_sampled_parity(name):
     wl = W.get(name)
     rtol = RTOL[wl.dtype]
@@ -113,8 +111,18 @@ def test_full_size_sampled_parity(name):
 
     # per-sample gradients, squared norms, norms of the sampled samples
     ref = oracle.dp_step(wl, sub_inputs(wl, inputs, samples), step=step, denom=float(N), noise=False)
+    for name, d in ref["derived"].items():
+        dev = st.recurrences[name].cpu().numpy()
+        for k, n in enumerate(samples):
+            assert_g12(dev[n], d[k], rtol, "derived %s n=%d" % (name, n))
+    # the derived backprops of every sample, for the clipped sums below
+    derived = {li.layer.name: oracle.lstm_backward(li.aux["gates"], li.aux["c"], li.aux["W_hh"],
+                                                   dh_last=li.aux["dh_last"])
+               for li in inputs if isinstance(li.layer, W.LSTMRecurrence)}
     for k, n in enumerate(samples):
         for li_idx, (lb, g_ref) in enumerate(zip(st.layers, ref["grads"])):
+            if not g_ref:
+                continue                      # a recurrence: no parameters of its own
             if "csr" in g_ref:
                 rp, uq, rows = g_ref["csr"]
                 rp_dev = lb.row_ptr.cpu().numpy()
@@ -144,7 +152,7 @@ def test_full_size_sampled_parity(name):
         sel = torch.tensor(flat_idx, device=DEV)
         S_dev = st.S[pname].reshape(-1)[sel].cpu().numpy()
         out_dev = st.out[pname].reshape(-1)[sel].cpu().numpy()
-        S_ref = np.array([np.dot(c, element_grads(wl, li, key, np.unravel_index(e, shape), wl.scale))
+        S_ref = np.array([np.dot(c, element_grads(wl, li, key, np.unravel_index(e, shape), wl.scale, derived))
                           for e in flat_idx])
         _, z = oracle.philox_normals(numel, wl.seed, step, pidx)
         out_ref = (S_ref + wl.sigma * wl.C * z[flat_idx]) / float(N)

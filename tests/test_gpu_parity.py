@@ -36,6 +36,10 @@ def compare_step(wl, inputs, got, ref, rtol, what):
         else:
             for k in r:
                 assert_g12(g[k], r[k], rtol, "%s grad %s.%s" % (what, name, k))
+    for name, d in ref.get("derived", {}).items():
+        # a derived backprop decays back through time: each sample against its own scale
+        for n in range(d.shape[0]):
+            assert_g12(got["derived"][name][n], d[n], rtol, "%s derived %s n=%d" % (what, name, n))
     assert_rel(got["sq_layers"], ref["sq_layers"], rtol, what + " sqnorm")
     assert_rel(got["norm"], ref["norm"], rtol, what + " norm")
     for k in ref["S"]:
@@ -46,7 +50,7 @@ def compare_step(wl, inputs, got, ref, rtol, what):
 
 
 SMALL = [("linear_tiny", None), ("mnist_cnn", None), ("cifar_cnn", 3), ("text_lstm", 5),
-         ("transformer_block", 2), ("cifar_gn", 3)]
+         ("transformer_block", 2), ("cifar_gn", 3), ("text_lstm_bptt", 5)]
 
 
 @pytest.mark.parametrize("name,n", SMALL)
@@ -87,19 +91,14 @@ def test_workload_step_with_ghost_norms_matches_oracle(name, n, mode):
 
 def split_batches(inputs, K):
     """K physical batches of a logical batch's inputs (along the sample axis)."""
-    N = inputs[0].B.shape[0]
+    N = next(li.B.shape[0] for li in inputs if li.B is not None)
     n = N // K
-    out = []
-    for k in range(K):
-        sl = slice(k * n, (k + 1) * n)
-        out.append([W.LayerInputs(li.layer, A=None if li.A is None else li.A[sl], B=li.B[sl],
-                                  ids=None if li.ids is None else li.ids[sl]) for li in inputs])
-    return out
+    return [W.take_samples(inputs, slice(k * n, (k + 1) * n)) for k in range(K)]
 
 
 @pytest.mark.parametrize("name,n,mode", [("mnist_cnn", 4, "auto"), ("linear_tiny", 5, "fused"),
                                          ("text_lstm", 2, "auto"), ("transformer_block", 2, "fused"),
-                                         ("transformer_block", 2, "colreduce")])
+                                         ("transformer_block", 2, "colreduce"), ("text_lstm_bptt", 2, "auto")])
 def test_virtual_steps_match_one_logical_step(name, n, mode):
     """Virtual steps: three physical batches of n samples, their clipped sums
     added up and noised once, equal the oracle's step over the 3n samples
@@ -743,11 +742,11 @@ def test_noise_schedule_in_a_graph_matches_eager(parallel):
 
 
 def _prefix(inputs, n):
-    return [W.LayerInputs(li.layer, None if li.A is None else li.A[:n], li.B[:n],
-                          None if li.ids is None else li.ids[:n]) for li in inputs]
+    return W.take_samples(inputs, slice(0, n))
 
 
-@pytest.mark.parametrize("name,nmax", [("mnist_cnn", 20), ("text_lstm", 9), ("transformer_block", 5)])
+@pytest.mark.parametrize("name,nmax", [("mnist_cnn", 20), ("text_lstm", 9), ("transformer_block", 5),
+                                       ("text_lstm_bptt", 6)])
 def test_variable_batch_in_a_graph_matches_eager(name, nmax):
     """A graph captured once on nmax rows follows the batch size set on the
     device before each replay (Poisson sampling's variable batch): its noised
