@@ -210,6 +210,18 @@ def traffic_for(kernel, workload, call):
     return rec.get("bytes_per_launch")
 
 
+def counters_for(kernel, workload, call):
+    """The counter record of a call from a committed counter run, if the kernel source is unchanged."""
+    path = os.path.join(ROOT, "profiles", "counters.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f).get("%s/%s" % (workload, call))
+    if not rec or rec.get("kernel") != kernel or rec.get("source_sha") != src_hash(KERNEL_SOURCES.get(kernel, [])):
+        return None
+    return rec
+
+
 # ---------------------------------------------------------------------------
 # CPU baseline: the oracle on a bounded sample
 # ---------------------------------------------------------------------------
@@ -268,6 +280,61 @@ def record_traffic(meta_path, fetch_csv, write_csv):
     for n in calls:
         k = "%s/%s" % (meta["workload"], n)
         print(k, table[k]["bytes_per_launch"], "algorithmic", table[k]["algorithmic_bytes"])
+
+
+def record_counters(meta_path, csv_path):
+    """Reduce one rocprofv3 --pmc pass of this benchmark (any counters, e.g.
+    MfmaUtil SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_INSTS_VALU_MFMA_MOPS_F32) to per-launch
+    figures of each event-timed call block; update profiles/counters.json.
+
+    MfmaUtil (rocprofv3's derived counter: MFMA-busy cycles over the active
+    cycles of all 1024 SIMDs, in percent) is averaged over the block's
+    dispatches weighted by their duration; every other counter is summed over
+    the block and divided by the number of launches.  The MOPS counters count
+    MFMA multiply-adds in units of 256 (512 flops), so they give the MFMA
+    flops a launch actually issued, next to its algorithmic flops."""
+    import csv
+
+    with open(meta_path) as f:
+        meta = json.load(f)
+    calls = meta["calls"]
+    rows = {}
+    for r in csv.DictReader(open(csv_path)):
+        d = int(r["Dispatch_Id"])
+        e = rows.setdefault(d, {"kernel": r["Kernel_Name"], "ns": 0.0, "c": {}})
+        if "End_Timestamp" in r and "Start_Timestamp" in r:
+            e["ns"] = float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
+        e["c"][r["Counter_Name"]] = e["c"].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    seq = [rows[d] for d in sorted(rows)]
+    cut = [i for i, e in enumerate(seq) if SENTINEL in e["kernel"]]
+    regs = [seq[a + 1:b] for a, b in zip(cut[0::2], cut[1::2])]
+    if len(regs) < len(calls):
+        raise SystemExit("record-counters: %d sentinel regions in %s, expected %d" % (len(regs), csv_path,
+                                                                                     len(calls)))
+    path = os.path.join(ROOT, "profiles", "counters.json")
+    table = json.load(open(path)) if os.path.exists(path) else {}
+    for n, reg in zip(calls, regs):
+        kern = meta["kernels"][n]
+        names = sorted({k for e in reg for k in e["c"]})
+        rec = {"kernel": kern, "source_sha": src_hash(KERNEL_SOURCES.get(kern, [])), "launches": meta["launches"],
+               "algorithmic_flops": meta.get("algorithmic_flops", {}).get(n)}
+        for k in names:
+            if k == "MfmaUtil":
+                w = [max(e["ns"], 1.0) for e in reg if k in e["c"]]
+                v = [e["c"][k] for e in reg if k in e["c"]]
+                rec[k] = round(sum(a * b for a, b in zip(v, w)) / sum(w), 3)
+            else:
+                rec[k] = sum(e["c"].get(k, 0.0) for e in reg) / meta["launches"]
+        for k in names:
+            if k.startswith("SQ_INSTS_VALU_MFMA_MOPS_"):
+                rec[k.replace("SQ_INSTS_VALU_MFMA_MOPS_", "mfma_flops_")] = rec[k] * 512
+        table["%s/%s" % (meta["workload"], n)] = rec
+    with open(path, "w") as fh:
+        json.dump(table, fh, indent=1, sort_keys=True)
+        fh.write("\n")
+    for n in calls:
+        print("%s/%s" % (meta["workload"], n), {k: v for k, v in table["%s/%s" % (meta["workload"], n)].items()
+                                                 if k not in ("source_sha",)})
 
 
 def cpu_model() -> str:
@@ -364,9 +431,14 @@ def main():
     ap.add_argument("--meta-out", default="", help="write the dominant call's name and launch count here")
     ap.add_argument("--record-traffic", nargs=3, metavar=("META", "FETCH_CSV", "WRITE_CSV"),
                     help="reduce two rocprofv3 counter runs of this benchmark into profiles/traffic.json")
+    ap.add_argument("--record-counters", nargs=2, metavar=("META", "CSV"),
+                    help="reduce one rocprofv3 --pmc run of this benchmark into profiles/counters.json")
     args = ap.parse_args()
     if args.record_traffic:
         record_traffic(*args.record_traffic)
+        return
+    if args.record_counters:
+        record_counters(*args.record_counters)
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -526,6 +598,9 @@ def main():
         roof = {"bound": "hbm", "achieved": round(nbytes / dt_s / 1e9, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s"}
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
     roof["traffic"] = traffic_for(kname, wl.name, dominant)
+    crec = counters_for(kname, wl.name, dominant)
+    # MFMA-busy fraction from a committed counter run of the same kernel source (null otherwise)
+    roof["mfma_busy_counter"] = None if crec is None or "MfmaUtil" not in crec else round(crec["MfmaUtil"] / 100, 4)
     roof.update({"kernel": kname, "call": dominant, "avg_us": round(dom_ms * 1e3, 2),
                  "algorithmic_bytes": nbytes, "algorithmic_flops": flops})
 
@@ -548,6 +623,7 @@ def main():
             json.dump({"workload": wl.name, "calls": names, "launches": args.steps,
                        "kernels": {n: costs[n][2] for n in names},
                        "algorithmic_bytes": {n: costs[n][0] for n in names},
+                       "algorithmic_flops": {n: costs[n][1] for n in names},
                        "avg_us": {n: round(avg[n] * 1e3, 2) for n in names},
                        "copy_bytes": args.copy_calibration_mib << 20}, f)
     if not args.no_cpu_baseline:
