@@ -40,7 +40,11 @@
  *  - Results are deterministic: no floating-point atomics, every reduction
  *    has a fixed order, so the same inputs give the same bits run to run.
  *  - Entry points are stateless and re-entrant; calls on different streams
- *    with disjoint outputs and workspaces may overlap.
+ *    with disjoint outputs and workspaces may overlap.  One exception:
+ *    dp_conv2d_set_path is a process-wide switch of the convolution kernel
+ *    (a test and tuning aid, to be set while no call is in flight; every
+ *    choice gives the same results to rounding), and
+ *    dp_grad_sample_linear_noalloc shares one scratch array per GPU.
  */
 #ifndef DPGRAD_H
 #define DPGRAD_H
