@@ -217,14 +217,16 @@ dp_status dp_grad_sample_many(const dp_layer_grad *items, int32_t count, dp_dtyp
  * batch (a dense [N][V][D] gradient is never formed):
  *   row_ptr[n] .. row_ptr[n+1]   the stored rows of sample n
  *   uniq_ids[k]                  the id of stored row k; ascending within a sample
- *   rows[k][:]                   its gradient row (positions added in ascending t)
+ *   rows[k][:]                   its gradient row (positions added in ascending t; a long
+ *                                segment is added in consecutive pieces, each in ascending
+ *                                t, the pieces then added in t order: a fixed order)
  *   sqnorm[n]                    sum of the squares of sample n's rows (overwritten)
  * ids: int64 [N][T]; B: [N][T][D] of `dt`; row_ptr int64 [N+1]; uniq_ids int64
  * [cap]; rows fp32 [cap][D]; sqnorm fp32 [N] or NULL.  cap >= N*T always
  * suffices; a smaller cap that the data overflows sets DP_FLAG_CAP, row_ptr
  * still holds the true counts and rows past cap are not written.  An id
  * outside [0, V) sets DP_FLAG_BAD_INDEX and its position is left out.
- * Needs T <= 4096 and N*T < 2^26 (else DP_EUNSUPPORTED) and V < 2^31. */
+ * Needs T <= 4096 and N*T < 2^31 (else DP_EUNSUPPORTED) and V < 2^31. */
 size_t dp_grad_sample_embedding_workspace_bytes(int64_t N, int64_t T);
 dp_status dp_grad_sample_embedding(const int64_t *ids, const void *B, dp_dtype dt, int64_t N,
                                    int64_t T, int64_t V, int64_t D, float scale,

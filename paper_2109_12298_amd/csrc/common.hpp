@@ -111,6 +111,31 @@ __device__ __forceinline__ float clip_factor(float norm, float C)
     return q < 1.0f ? q : 1.0f;
 }
 
+// A workgroup barrier that orders LDS only.  __syncthreads() also waits for
+// every outstanding global access of the wave, loads in flight and stores
+// not yet acknowledged alike; this one leaves them outstanding.
+__device__ __forceinline__ void lds_barrier()
+{
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+// Raw-buffer descriptor over an array of `bytes` bytes (gfx9 word for 32-bit
+// untyped accesses): a load at a byte offset at or past `bytes` reads zero,
+// so bounded loads need no branch (and no wait at the branch's join).
+// kOutside is an offset that is always past the end.
+constexpr uint32_t kOutside = 0x80000000u;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t sample_rsrc(const void *base, uint32_t bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, (int)bytes, 0x00020000);
+}
+
+__device__ __forceinline__ int32_t buffer_load_i32(__amdgpu_buffer_rsrc_t r, uint32_t byte_offset)
+{
+    return __builtin_amdgcn_raw_buffer_load_b32(r, byte_offset, 0, 0);
+}
+
 // ---------------------------------------------------------------------------
 // fixed-order reductions
 // ---------------------------------------------------------------------------

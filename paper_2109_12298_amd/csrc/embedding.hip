@@ -5,18 +5,28 @@
 // of the dense [N][V][D] tensor (which makes embeddings the paper's worst
 // case for memory and runtime) the result is CSR over the batch.
 //
-// Pass 1 (one workgroup per sample): bitonic sort of the keys (id, t) in LDS;
-//   since t is unique the order is total, so equal ids stay in ascending t.
-//   Segment starts come from a block scan of the "new id" flags.
-// Pass 2 (one workgroup): exclusive scan of the per-sample distinct counts
-//   into row_ptr.
-// Pass 3 (one wave per sample and segment slot, so the grid fills the chip
-//   even for a small batch): the wave sums the segment's backprop rows in
-//   ascending t, eight positions' loads in flight at a time (32 for segments
-//   longer than eight, such as a hot id's), lanes over the
-//   columns (four per lane when the rows allow 16- or 8-byte loads), and
-//   writes the CSR row and its squared norm; the sample's norm is then added
-//   over its slots in slot order.  No atomics on data.
+// Two launches (three when N > 2048):
+// Pass 1 (one workgroup per sample): sort the keys (id, t) in LDS.  The keys
+//   are unique (t is), so for T <= 512 each key's rank is the number of
+//   smaller keys and the sort is one scatter (no barrier per pass); longer
+//   samples use a bitonic network.  Equal ids end up in ascending t.  Then
+//   the segment index of each sorted position (a prefix count of the "new
+//   id" heads), the distinct count and the valid count.
+// Pass 2 (G workgroups per sample, G = T / 64 clamped to [1, 8]): the
+//   sample's sorted positions are cut into G ranges at segment boundaries
+//   (range g starts at the first segment that starts at or after g * P / G),
+//   so no segment crosses workgroups.  Each workgroup adds the distinct
+//   counts of the samples before n (its first CSR row; a scan launch in
+//   between does it for N > 2048), then splits its range over 4 waves.  A
+//   wave issues the row loads of 16 positions at once (lanes over columns)
+//   and adds them in ascending t, writing every segment that starts and ends
+//   in its range; a segment that crosses waves is finished by the wave where
+//   it starts, which adds the pieces of the following waves in wave order.
+//   So a segment's order is fixed: ascending t within a piece, pieces in t
+//   order.  The squared norm is each wave's sum over the rows it wrote, the
+//   waves' sums in wave order, then the G workgroups' sums in g order, added
+//   by whichever workgroup of the sample finishes last (a per-sample
+//   completion counter; no atomics on data, no workgroup waits for another).
 #include "common.hpp"
 
 #include <type_traits>
@@ -24,110 +34,193 @@
 namespace dpg {
 namespace {
 
-constexpr int kThreads = 256;
+constexpr int kSortThreads = 1024;
 constexpr i64 kMaxT = 4096;
-constexpr uint64_t kNoKey = ~0ull;
-
-// Exclusive scan of one int per thread over the block; returns the total.
-__device__ int block_exclusive_scan(int v, int *buf, int &total)
-{
-    const int tid = threadIdx.x;
-    buf[tid] = v;
-    __syncthreads();
-    for (int off = 1; off < kThreads; off <<= 1) {
-        const int x = tid >= off ? buf[tid - off] : 0;
-        __syncthreads();
-        buf[tid] += x;
-        __syncthreads();
-    }
-    total = buf[kThreads - 1];
-    const int incl = buf[tid];
-    __syncthreads();
-    return incl - v;
-}
+constexpr i64 kRankMaxT = 512;      // rank sort up to here, bitonic beyond
+constexpr i64 kPrefixMaxN = 2048;   // pass 2 adds the distinct counts itself up to here
+constexpr int kCsrWaves = 4;        // pass 2 workgroup: 256 threads
+constexpr int kCsrThreads = 64 * kCsrWaves;
+constexpr int kMaxSplit = 8;        // pass 2 workgroups per sample, at most
+constexpr int kStage = (int)(kMaxT / kCsrThreads);          // staged positions per thread, at most
+constexpr int kPrefixLoads = (int)(kPrefixMaxN / kCsrThreads);
+constexpr uint32_t kInvalidHi = 0xffffffffu;   // key high word of an id outside [0, V)
 
 struct EmbWs {
-    int32_t *perm;      // [N][T]   positions in sorted order
-    int32_t *segstart;  // [N][T+1] first sorted index of each segment, then the end
-    int32_t *segid;     // [N][T]   id of each segment
-    int32_t *counts;    // [N]      distinct valid ids
-    float *sqpart;      // [N][T]   squared norm of each segment slot (0 past the last)
+    int32_t *perm;      // [N][T] position t of each sorted position
+    int32_t *sidx;      // [N][T] segment index of each sorted position
+    int32_t *segid;     // [N][T] id of each segment
+    int32_t *counts;    // [N]    distinct valid ids
+    int32_t *valid;     // [N]    valid positions
+    int32_t *done;      // [N]    pass 2 workgroups of the sample that have finished
+    float *sqpart;      // [N][kMaxSplit] squared norm of each pass 2 workgroup's rows
 };
 
-__global__ __launch_bounds__(kThreads) void emb_sort_kernel(const int64_t *__restrict__ ids, i64 T,
-                                                            i64 V, int P2, EmbWs w,
-                                                            int32_t *status)
+// pass 2 workgroups per sample
+int split_for(i64 T)
 {
-    extern __shared__ uint64_t keys[];
-    __shared__ int scan_buf[kThreads];
+    const i64 g = T / 64;
+    return (int)(g < 1 ? 1 : (g > kMaxSplit ? kMaxSplit : g));
+}
+
+// Exclusive scan of one int per thread over the block (wave scans, then the
+// wave totals); returns the total in `total`.  wsum: __shared__ int[16], not
+// reused after the call.
+__device__ int block_exclusive_scan(int v, int *wsum, int &total)
+{
+    const int lane = threadIdx.x & (kWave - 1), w = threadIdx.x / kWave;
+    const int nw = (int)(blockDim.x / kWave);
+    int x = v;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        const int y = __shfl_up(x, o, kWave);
+        if (lane >= o) x += y;
+    }
+    if (lane == kWave - 1) wsum[w] = x;
+    lds_barrier();
+    int pre = 0, tot = 0;
+    for (int i = 0; i < nw; ++i) {
+        const int t = wsum[i];
+        pre += i < w ? t : 0;
+        tot += t;
+    }
+    total = tot;
+    return pre + x - v;
+}
+
+__device__ __forceinline__ int pick4(const int (&a)[4], int q)
+{
+    return q == 0 ? a[0] : q == 1 ? a[1] : q == 2 ? a[2] : a[3];
+}
+
+// Rank of each of the T (<= 512) unique keys kk[] among all of them, and
+// keys[i] stored at sorted[rank].  Groups of S adjacent lanes own four keys;
+// each lane reads every S-th key and compares it with all four (one LDS read
+// per four comparisons), then the counts are added over the group.  The
+// comparisons bound it (T^2 per sample), hence 32-bit keys where they fit.
+template <typename K>
+__device__ __forceinline__ void rank_scatter(const K *kk, const uint64_t *keys, uint64_t *sorted, int T, int tid)
+{
+    const int S = T <= kSortThreads / 4 ? 16 : 8;
+    const int grp = tid / S, sub = tid % S;
+    K ki[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int i = 4 * grp + q;
+        ki[q] = kk[i < T ? i : 0];
+    }
+    int r[4] = {0, 0, 0, 0};
+    int j = sub;
+    for (; j + 3 * S < T; j += 4 * S) {
+        K kj[4];
+#pragma unroll
+        for (int a = 0; a < 4; ++a) kj[a] = kk[j + a * S];
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) r[q] += kj[a] < ki[q] ? 1 : 0;
+    }
+    for (; j < T; j += S) {
+        const K kj = kk[j];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) r[q] += kj < ki[q] ? 1 : 0;
+    }
+    for (int off = S >> 1; off >= 1; off >>= 1)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) r[q] += __shfl_xor(r[q], off, kWave);
+    const int i = 4 * grp + sub;
+    if (sub < 4 && i < T) sorted[pick4(r, sub)] = keys[i];
+}
+
+__global__ __launch_bounds__(kSortThreads) void emb_sort_kernel(const int64_t *__restrict__ ids, i64 T, i64 V,
+                                                                int P2, EmbWs w, int32_t *status)
+{
+    extern __shared__ uint64_t keys[];           // [2][T] + uint32 [T] (rank sort) or [P2] (bitonic)
+    __shared__ int wsum[kSortThreads / kWave];
     const i64 n = blockIdx.x;
     const int tid = threadIdx.x;
     const int64_t *idn = ids + n * T;
+    const bool rank = T <= kRankMaxT;
+    const int L = rank ? (int)T : P2;            // keys in the sorted array
+    uint64_t *sorted = rank ? keys + T : keys;
+    // 32-bit keys id * T + t (V * T + t for an invalid id) when they fit
+    uint32_t *k32 = reinterpret_cast<uint32_t *>(keys + 2 * T);
+    const bool small = rank && (uint64_t)(V + 1) * (uint64_t)T <= 0xffffffffull;
     bool bad = false;
-    for (int i = tid; i < P2; i += kThreads) {
-        uint64_t k = kNoKey;
+    for (int i = tid; i < L; i += kSortThreads) {
+        uint64_t k = ~0ull;                      // bitonic padding
         if (i < T) {
             const int64_t id = idn[i];
-            if (id >= 0 && id < V) k = ((uint64_t)id << 32) | (uint32_t)i;
-            else bad = true;
+            const bool ok = id >= 0 && id < V;
+            bad |= !ok;
+            // an invalid id keeps a unique key that sorts after every valid one
+            k = ((uint64_t)(ok ? (uint32_t)id : kInvalidHi) << 32) | (uint32_t)i;
+            if (small) k32[i] = (uint32_t)((ok ? id : V) * T + i);
         }
         keys[i] = k;
     }
     if (bad) raise_flag(status, DP_FLAG_BAD_INDEX);
-    __syncthreads();
-    for (int k = 2; k <= P2; k <<= 1) {
-        for (int j = k >> 1; j > 0; j >>= 1) {
-            for (int i = tid; i < P2; i += kThreads) {
-                const int ixj = i ^ j;
-                if (ixj > i) {
-                    const uint64_t a = keys[i], b = keys[ixj];
-                    const bool up = (i & k) == 0;
-                    if ((a > b) == up) {
-                        keys[i] = b;
-                        keys[ixj] = a;
+    if (tid == 0) w.done[n] = 0;
+    lds_barrier();
+    if (rank) {
+        if (small) rank_scatter<uint32_t>(k32, keys, sorted, (int)T, tid);
+        else rank_scatter<uint64_t>(keys, keys, sorted, (int)T, tid);
+        lds_barrier();
+    } else {
+        for (int k = 2; k <= P2; k <<= 1) {
+            for (int j = k >> 1; j > 0; j >>= 1) {
+                for (int i = tid; i < P2; i += kSortThreads) {
+                    const int ixj = i ^ j;
+                    if (ixj > i) {
+                        const uint64_t a = keys[i], b = keys[ixj];
+                        const bool up = (i & k) == 0;
+                        if ((a > b) == up) {
+                            keys[i] = b;
+                            keys[ixj] = a;
+                        }
                     }
                 }
+                lds_barrier();
             }
-            __syncthreads();
         }
     }
-    // each thread owns a contiguous range of sorted positions
-    const int per = (int)((T + kThreads - 1) / kThreads);
+    // each thread owns a contiguous range of sorted positions: heads of new
+    // ids (low half) and valid positions (high half; both at most 4096),
+    // counted, then scanned over the block
+    const int per = (int)((T + kSortThreads - 1) / kSortThreads);
     const int r0 = tid * per;
     const int r1 = (int)(r0 + per < T ? r0 + per : T);
-    int heads = 0, valid = 0;
+    int cnt = 0;
     for (int r = r0; r < r1; ++r) {
-        const uint64_t k = keys[r];
-        if (k == kNoKey) continue;
-        ++valid;
-        if (r == 0 || (keys[r - 1] >> 32) != (k >> 32)) ++heads;
+        const uint32_t hi = (uint32_t)(sorted[r] >> 32);
+        if (hi == kInvalidHi) continue;
+        cnt += 1 << 16;
+        if (r == 0 || (uint32_t)(sorted[r - 1] >> 32) != hi) ++cnt;
     }
-    int nseg, nvalid;
-    int s = block_exclusive_scan(heads, scan_buf, nseg);
-    int vtot;
-    (void)block_exclusive_scan(valid, scan_buf, vtot);
-    nvalid = vtot;
+    int tot;
+    int s = (block_exclusive_scan(cnt, wsum, tot) & 0xffff) - 1;   // segment of the position before r0
     int32_t *perm = w.perm + n * T;
-    int32_t *seg = w.segstart + n * (T + 1);
+    int32_t *sidx = w.sidx + n * T;
+    int32_t *segid = w.segid + n * T;
     for (int r = r0; r < r1; ++r) {
-        const uint64_t k = keys[r];
-        if (k == kNoKey) continue;
+        const uint64_t k = sorted[r];
+        const uint32_t hi = (uint32_t)(k >> 32);
+        if (hi == kInvalidHi) continue;
+        if (r == 0 || (uint32_t)(sorted[r - 1] >> 32) != hi) segid[++s] = (int32_t)hi;
         perm[r] = (int32_t)(k & 0xffffffffu);
-        if (r == 0 || (keys[r - 1] >> 32) != (k >> 32)) {
-            w.segid[n * T + s] = (int32_t)(k >> 32);
-            seg[s++] = r;
-        }
+        sidx[r] = s;
     }
     if (tid == 0) {
-        seg[nseg] = nvalid;
-        w.counts[n] = nseg;
+        w.counts[n] = tot & 0xffff;
+        w.valid[n] = tot >> 16;
     }
 }
 
-__global__ __launch_bounds__(kThreads) void emb_scan_kernel(const int32_t *__restrict__ counts,
-                                                            i64 N, int64_t *__restrict__ row_ptr)
+// row_ptr[n + 1] = the distinct counts of samples 0..n (one workgroup; the
+// path for more samples than pass 2 adds up itself)
+__global__ __launch_bounds__(256) void emb_scan_kernel(const int32_t *__restrict__ counts, i64 N,
+                                                       int64_t *__restrict__ row_ptr)
 {
-    __shared__ int64_t buf[kThreads];
+    __shared__ int64_t buf[256];
     __shared__ int64_t carry;
     const int tid = threadIdx.x;
     if (tid == 0) {
@@ -135,12 +228,12 @@ __global__ __launch_bounds__(kThreads) void emb_scan_kernel(const int32_t *__res
         row_ptr[0] = 0;
     }
     __syncthreads();
-    for (i64 c = 0; c < N; c += kThreads) {
+    for (i64 c = 0; c < N; c += 256) {
         const i64 n = c + tid;
         const int64_t v = n < N ? counts[n] : 0;
         buf[tid] = v;
         __syncthreads();
-        for (int off = 1; off < kThreads; off <<= 1) {
+        for (int off = 1; off < 256; off <<= 1) {
             const int64_t x = tid >= off ? buf[tid - off] : 0;
             __syncthreads();
             buf[tid] += x;
@@ -148,7 +241,7 @@ __global__ __launch_bounds__(kThreads) void emb_scan_kernel(const int32_t *__res
         }
         if (n < N) row_ptr[n + 1] = carry + buf[tid];
         __syncthreads();
-        if (tid == 0) carry += buf[kThreads - 1];
+        if (tid == 0) carry += buf[255];
         __syncthreads();
     }
 }
@@ -171,79 +264,245 @@ __device__ __forceinline__ void load_vec(const T *p, float (&v)[VEC])
     }
 }
 
-constexpr int kBatch = 8;       // positions whose loads are in flight together
-constexpr int kDeepBatch = 32;  // ... for segments longer than kBatch (hot ids)
+constexpr int kBatch = 16;    // positions whose row loads a wave has in flight together
 
-// acc += the rows perm[r0 .. r1-1] of Bn at column cc, in ascending r,
-// BATCH rows' loads in flight at a time
-template <typename T, int VEC, int BATCH>
-__device__ __forceinline__ void sum_rows(const T *Bn, const int32_t *perm, int r0, int r1, i64 D, i64 cc,
-                                         float (&acc)[VEC])
-{
-    for (int r = r0; r < r1; r += BATCH) {
-        float v[BATCH][VEC];
-#pragma unroll
-        for (int j = 0; j < BATCH; ++j) {
-            const int rj = r + j < r1 ? r + j : r1 - 1;
-            load_vec<T, VEC>(Bn + (i64)perm[rj] * D + cc, v[j]);
-        }
-#pragma unroll
-        for (int j = 0; j < BATCH; ++j)
-            if (r + j < r1)
-#pragma unroll
-                for (int i = 0; i < VEC; ++i) acc[i] += v[j][i];
-    }
-}
+// pieces of segments that cross waves, per wave: the end of a segment that
+// started in an earlier wave (head), the start of one that continues (tail),
+// or the middle of one that covers the whole range (mid)
+enum { kHead = 0, kTail = 1, kMid = 2 };
 
 template <typename T, int VEC>
-__global__ __launch_bounds__(64) void emb_rows_kernel(
-    const T *__restrict__ B, i64 Tn, i64 D, float scale, EmbWs w, const int64_t *__restrict__ row_ptr,
-    int64_t *__restrict__ uniq, float *__restrict__ rows, i64 cap, int32_t *status)
+__global__ __launch_bounds__(kCsrThreads) void emb_csr_kernel(
+    const T *__restrict__ B, i64 Tn, i64 D, float scale, EmbWs w, int G, int prefix_here,
+    int64_t *__restrict__ row_ptr, int64_t *__restrict__ uniq, float *__restrict__ rows, i64 cap,
+    float *__restrict__ sqnorm, int32_t *status)
 {
-    const i64 n = blockIdx.x / Tn;
-    const int s = (int)(blockIdx.x % Tn);
-    const int lane = threadIdx.x;
-    const int u = w.counts[n];
-    if (s >= u) {
-        if (lane == 0) w.sqpart[n * Tn + s] = 0.0f;
-        return;
+    constexpr int CB = 64 * VEC;                         // columns per column block
+    extern __shared__ int32_t order[];                   // the sample's perm, sidx, segid (3 * Tn)
+    __shared__ float piece[kCsrWaves][3][CB];
+    __shared__ int pseg[kCsrWaves][3];                   // segment of each piece, -1 for none
+    __shared__ float wsq[kCsrWaves];
+    __shared__ int64_t wpart[kCsrWaves];
+    __shared__ int wbound[kCsrWaves][2];
+    const i64 n = blockIdx.x / G;
+    const int g = (int)(blockIdx.x % G);
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int u = w.counts[n], P = w.valid[n];
+
+    // Every load that does not depend on another is issued before the first
+    // wait: the distinct counts of the samples before n (N <= 2048) and the
+    // sample's sorted positions, segments and ids (T <= 4096).  Bounded
+    // raw-buffer loads read zero past the end.
+    const __amdgpu_buffer_rsrc_t rcnt = sample_rsrc(w.counts, prefix_here ? (uint32_t)n * 4u : 0u);
+    const __amdgpu_buffer_rsrc_t rperm = sample_rsrc(w.perm + n * Tn, (uint32_t)P * 4u);
+    const __amdgpu_buffer_rsrc_t rsidx = sample_rsrc(w.sidx + n * Tn, (uint32_t)P * 4u);
+    const __amdgpu_buffer_rsrc_t rseg = sample_rsrc(w.segid + n * Tn, (uint32_t)u * 4u);
+    int64_t part = 0, base_in = 0;
+    int32_t cl[kPrefixLoads];
+#pragma unroll
+    for (int k = 0; k < kPrefixLoads; ++k) cl[k] = buffer_load_i32(rcnt, 4u * (uint32_t)(tid + kCsrThreads * k));
+    if (!prefix_here) base_in = row_ptr[n];
+    int32_t pv[kStage], sv[kStage], gv[kStage];
+#pragma unroll
+    for (int k = 0; k < kStage; ++k) {
+        pv[k] = sv[k] = gv[k] = 0;
+        if (kCsrThreads * k < P) {
+            const uint32_t o = 4u * (uint32_t)(tid + kCsrThreads * k);
+            pv[k] = buffer_load_i32(rperm, o);
+            sv[k] = buffer_load_i32(rsidx, o);
+            gv[k] = buffer_load_i32(rseg, o);
+        }
     }
-    const i64 k = row_ptr[n] + s;                 // CSR row of this segment
-    if (s == u - 1 && k >= cap && lane == 0) raise_flag(status, DP_FLAG_CAP);
-    const bool keep = k < cap;
-    const int32_t *perm = w.perm + n * Tn;
-    const int32_t *seg = w.segstart + n * (Tn + 1);
-    const int r0 = seg[s], r1 = seg[s + 1];
-    if (keep && lane == 0) uniq[k] = w.segid[n * Tn + s];
+    int32_t *perm = order;
+    int32_t *sidx = order + Tn;
+    int32_t *segid = order + 2 * Tn;
+#pragma unroll
+    for (int k = 0; k < kStage; ++k) {
+        const int r = tid + kCsrThreads * k;
+        if (r < P) {
+            perm[r] = pv[k];
+            sidx[r] = sv[k];
+            segid[r] = gv[k];    // u <= P, so every segment is staged
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < kPrefixLoads; ++k) part += cl[k];
+    for (int off = 32; off >= 1; off >>= 1) part += __shfl_xor(part, off, kWave);
+    if (lane == 0) wpart[wv] = part;
+    lds_barrier();
+
+    // the workgroup's range [lo, hi): from the first segment start at or after
+    // g * P / G to the first at or after (g + 1) * P / G
+    // (the lowest lane of a ballot is the wave's first such position, then
+    // the minimum over the waves)
+    const int c0 = (int)((uint32_t)(g * P) / (uint32_t)G), c1 = (int)((uint32_t)((g + 1) * P) / (uint32_t)G);
+    int f0 = P, f1 = P;
+    for (int rb = wv * 64; rb < P; rb += kCsrThreads) {
+        const int r = rb + lane;
+        const bool start = r < P && (r == 0 || sidx[r] != sidx[r - 1]);
+        const uint64_t b0 = __ballot(start && r >= c0), b1 = __ballot(start && r >= c1);
+        if (b0 && f0 == P) f0 = rb + __ffsll((unsigned long long)b0) - 1;
+        if (b1 && f1 == P) f1 = rb + __ffsll((unsigned long long)b1) - 1;
+    }
+    if (lane == 0) {
+        wbound[wv][0] = f0;
+        wbound[wv][1] = f1;
+    }
+    i64 base = base_in;
+    if (prefix_here) {
+        base = 0;
+        for (int i = 0; i < kCsrWaves; ++i) base += wpart[i];
+    }
+    lds_barrier();
+    int lo = P, hi = P;
+    for (int i = 0; i < kCsrWaves; ++i) {
+        lo = wbound[i][0] < lo ? wbound[i][0] : lo;
+        hi = wbound[i][1] < hi ? wbound[i][1] : hi;
+    }
 
     const T *Bn = B + n * Tn * D;
+    const int R = (hi - lo + kCsrWaves - 1) / kCsrWaves;       // sorted positions per wave
+    const int r_lo = lo + wv * R < hi ? lo + wv * R : hi;
+    const int r_hi = r_lo + R < hi ? r_lo + R : hi;
+    // does the wave's first segment start before its range, its last continue after it?
+    const bool first_cont = r_lo < r_hi && r_lo > lo && sidx[r_lo - 1] == sidx[r_lo];
+    const bool last_cont = r_lo < r_hi && r_hi < hi && sidx[r_hi] == sidx[r_hi - 1];
     float sq = 0.0f;
-    for (i64 c0 = 0; c0 < D; c0 += 64 * VEC) {
-        const i64 c = c0 + (i64)VEC * lane;
+
+    auto finish = [&](i64 s, const float (&acc)[VEC], i64 c, bool on) {
+        const i64 k = base + s;
+        if (on) {
+            float gr[VEC];
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) {
+                gr[i] = scale * acc[i];
+                sq += gr[i] * gr[i];
+            }
+            if (k < cap) {
+                if constexpr (VEC == 4)
+                    *reinterpret_cast<float4 *>(rows + k * D + c) = make_float4(gr[0], gr[1], gr[2], gr[3]);
+                else
+                    rows[k * D + c] = gr[0];
+            }
+        }
+    };
+
+    for (i64 c0c = 0; c0c < D; c0c += CB) {
+        const i64 c = c0c + (i64)VEC * lane;
         const bool on = c < D;
         const i64 cc = on ? c : 0;
         float acc[VEC];
 #pragma unroll
         for (int i = 0; i < VEC; ++i) acc[i] = 0.0f;
-        if (r1 - r0 > kBatch) sum_rows<T, VEC, kDeepBatch>(Bn, perm, r0, r1, D, cc, acc);
-        else sum_rows<T, VEC, kBatch>(Bn, perm, r0, r1, D, cc, acc);
-        if (on) {
-            float g[VEC];
+        bool started_here = !first_cont;
+        if (lane < 3) pseg[wv][lane] = -1;
+        for (int r0 = r_lo; r0 < r_hi; r0 += kBatch) {
+            // lane l (and l + 16, l + 32, l + 48) holds position r0 + l of the
+            // batch: its t, its segment, whether the segment ends there
+            const int rl = r0 + (lane & (kBatch - 1));
+            const bool in = rl < r_hi;
+            const int tl = perm[in ? rl : r0];
+            const int sl = sidx[in ? rl : r0];
+            const bool ends = in && (rl + 1 == P || sidx[rl + 1] != sl);
+            const uint32_t endm = (uint32_t)__ballot(ends);
+            float v[kBatch][VEC];
 #pragma unroll
-            for (int i = 0; i < VEC; ++i) {
-                g[i] = scale * acc[i];
-                sq += g[i] * g[i];
+            for (int j = 0; j < kBatch; ++j) {
+                const int t = __builtin_amdgcn_readlane(tl, j);
+                load_vec<T, VEC>(Bn + (i64)t * D + cc, v[j]);
             }
-            if (keep) {
-                if constexpr (VEC == 4)
-                    *reinterpret_cast<float4 *>(rows + k * D + c) = make_float4(g[0], g[1], g[2], g[3]);
-                else
-                    rows[k * D + c] = g[0];
+            // (fully unrolled with a uniform guard instead of a break, so
+            // that v stays in registers)
+#pragma unroll
+            for (int j = 0; j < kBatch; ++j) {
+                if (r0 + j >= r_hi) continue;
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) acc[i] += v[j][i];
+                if ((endm >> j) & 1u) {
+                    const int s = __builtin_amdgcn_readlane(sl, j);
+                    if (started_here) {
+                        finish(s, acc, c, on);
+                    } else {
+                        // the end of a segment from an earlier wave
+#pragma unroll
+                        for (int i = 0; i < VEC; ++i) piece[wv][kHead][VEC * lane + i] = acc[i];
+                        if (lane == 0) pseg[wv][kHead] = s;
+                    }
+#pragma unroll
+                    for (int i = 0; i < VEC; ++i) acc[i] = 0.0f;
+                    started_here = true;
+                }
             }
         }
+        if (last_cont) {
+            const int kind = started_here ? kTail : kMid;
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) piece[wv][kind][VEC * lane + i] = acc[i];
+            if (lane == 0) pseg[wv][kind] = sidx[r_hi - 1];
+        }
+        lds_barrier();
+        // a segment that starts in this wave and continues: add the following
+        // waves' pieces in wave order, then write it
+        if (pseg[wv][kTail] >= 0) {
+            const int s = pseg[wv][kTail];
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) acc[i] = piece[wv][kTail][VEC * lane + i];
+            for (int x = wv + 1; x < kCsrWaves; ++x) {
+                if (pseg[x][kMid] == s) {
+#pragma unroll
+                    for (int i = 0; i < VEC; ++i) acc[i] += piece[x][kMid][VEC * lane + i];
+                } else {
+#pragma unroll
+                    for (int i = 0; i < VEC; ++i) acc[i] += piece[x][kHead][VEC * lane + i];
+                    break;
+                }
+            }
+            finish(s, acc, c, on);
+        }
+        lds_barrier();                                   // the pieces are rewritten by the next block
     }
+
+    // the ids of the segments the workgroup owns and the sample's CSR bound,
+    // stored last (a store issued before the walk would make the walk's first
+    // loads wait for it)
+    if (lo < hi) {
+        const int s_first = sidx[lo], s_last = sidx[hi - 1];
+        for (int s = s_first + tid; s <= s_last; s += kCsrThreads)
+            if (base + s < cap) uniq[base + s] = segid[s];
+    }
+    if (g == 0 && tid == 0) {
+        if (prefix_here) {
+            row_ptr[n + 1] = base + u;
+            if (n == 0) row_ptr[0] = 0;
+        }
+        if (base + u > cap) raise_flag(status, DP_FLAG_CAP);
+    }
+    if (!sqnorm) return;
     sq = wave_sum(sq);
-    if (lane == 0) w.sqpart[n * Tn + s] = sq;
+    if (lane == 0) wsq[wv] = sq;
+    lds_barrier();
+    if (tid != 0) return;
+    float t = 0.0f;
+    for (int i = 0; i < kCsrWaves; ++i) t += wsq[i];
+    if (G == 1) {
+        sqnorm[n] = t;
+        return;
+    }
+    // The sample's last workgroup to finish adds the G sums in g order.  The
+    // sum is stored with device-scope coherence (written through to where
+    // every XCD sees it) and acknowledged before the counter is bumped; the
+    // last workgroup reads the sums the same way after its bump returns.
+    // (An acquire-release counter would also write back every dirty line of
+    // the XCD's L2, the rows included, for each workgroup.)
+    __hip_atomic_store(w.sqpart + n * kMaxSplit + g, t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    const int before = __hip_atomic_fetch_add(w.done + n, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (before != G - 1) return;
+    float tot = 0.0f;
+    for (int x = 0; x < G; ++x)
+        tot += __hip_atomic_load(w.sqpart + n * kMaxSplit + x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    sqnorm[n] = tot;
 }
 
 EmbWs carve(void *ws, i64 N, i64 T)
@@ -252,11 +511,15 @@ EmbWs carve(void *ws, i64 N, i64 T)
     char *p = (char *)ws;
     w.perm = (int32_t *)p;
     p += align_up(sizeof(int32_t) * N * T, 256);
-    w.segstart = (int32_t *)p;
-    p += align_up(sizeof(int32_t) * N * (T + 1), 256);
+    w.sidx = (int32_t *)p;
+    p += align_up(sizeof(int32_t) * N * T, 256);
     w.segid = (int32_t *)p;
     p += align_up(sizeof(int32_t) * N * T, 256);
     w.counts = (int32_t *)p;
+    p += align_up(sizeof(int32_t) * N, 256);
+    w.valid = (int32_t *)p;
+    p += align_up(sizeof(int32_t) * N, 256);
+    w.done = (int32_t *)p;
     p += align_up(sizeof(int32_t) * N, 256);
     w.sqpart = (float *)p;
     return w;
@@ -270,8 +533,8 @@ using namespace dpg;
 extern "C" size_t dp_grad_sample_embedding_workspace_bytes(int64_t N, int64_t T)
 {
     if (N <= 0 || T < 0) return 0;
-    return 2 * align_up(sizeof(int32_t) * N * T, 256) + align_up(sizeof(int32_t) * N * (T + 1), 256) +
-           align_up(sizeof(int32_t) * N, 256) + align_up(sizeof(float) * N * T, 256);
+    return 3 * align_up(sizeof(int32_t) * N * T, 256) + 3 * align_up(sizeof(int32_t) * N, 256) +
+           align_up(sizeof(float) * N * kMaxSplit, 256);
 }
 
 extern "C" dp_status dp_grad_sample_embedding(const int64_t *ids, const void *B, dp_dtype dt,
@@ -285,8 +548,8 @@ extern "C" dp_status dp_grad_sample_embedding(const int64_t *ids, const void *B,
     DPG_REQUIRE(N >= 0 && T >= 0 && V >= 1 && D >= 1 && cap >= 0, DP_EINVAL);
     DPG_REQUIRE(V < (i64(1) << 31), DP_EINVAL);
     DPG_REQUIRE(T <= kMaxT, DP_EUNSUPPORTED);
-    // one 64-lane workgroup per position: the grid's 2^32 work-items cap N*T
-    DPG_REQUIRE(N * T < (i64(1) << 26), DP_EUNSUPPORTED);
+    // 32-bit sorted-position indices, and one pass 2 workgroup per sample and range
+    DPG_REQUIRE(N * T < (i64(1) << 31) && N * kMaxSplit < (i64(1) << 31), DP_EUNSUPPORTED);
     DPG_REQUIRE(row_ptr != nullptr, DP_EINVAL);
     DPG_REQUIRE(N * T == 0 || (ids != nullptr && B != nullptr), DP_EINVAL);
     DPG_REQUIRE(cap == 0 || (uniq_ids != nullptr && rows != nullptr), DP_EINVAL);
@@ -294,38 +557,41 @@ extern "C" dp_status dp_grad_sample_embedding(const int64_t *ids, const void *B,
     DPG_REQUIRE(ws_bytes >= need && (need == 0 || ws != nullptr), DP_EINVAL);
     if (N == 0) {
         // row_ptr[0] = 0 for an empty batch
-        emb_scan_kernel<<<1, kThreads, 0, stream>>>(nullptr, 0, row_ptr);
+        emb_scan_kernel<<<1, 256, 0, stream>>>(nullptr, 0, row_ptr);
         return launch_status();
     }
     EmbWs w = carve(ws, N, T);
     int P2 = 1;
     while (P2 < T) P2 <<= 1;
-    emb_sort_kernel<<<(unsigned)N, kThreads, sizeof(uint64_t) * P2, stream>>>(ids, T, V, P2, w, status);
-    emb_scan_kernel<<<1, kThreads, 0, stream>>>(w.counts, N, row_ptr);
-    if (T > 0) {
-        const unsigned grid = (unsigned)(N * T);
-        // four columns per lane when every row starts on a 16-byte (fp32) or
-        // 8-byte (bf16) boundary, and rows likewise
-        const bool vec = D % 4 == 0 && aligned(rows, 16) && aligned(B, dt == DP_F32 ? 16 : 8);
-        if (dt == DP_F32) {
-            if (vec)
-                emb_rows_kernel<float, 4><<<grid, 64, 0, stream>>>((const float *)B, T, D, scale, w, row_ptr,
-                                                                   uniq_ids, rows, cap, status);
-            else
-                emb_rows_kernel<float, 1><<<grid, 64, 0, stream>>>((const float *)B, T, D, scale, w, row_ptr,
-                                                                   uniq_ids, rows, cap, status);
-        } else {
-            if (vec)
-                emb_rows_kernel<uint16_t, 4><<<grid, 64, 0, stream>>>((const uint16_t *)B, T, D, scale, w,
-                                                                      row_ptr, uniq_ids, rows, cap, status);
-            else
-                emb_rows_kernel<uint16_t, 1><<<grid, 64, 0, stream>>>((const uint16_t *)B, T, D, scale, w,
-                                                                      row_ptr, uniq_ids, rows, cap, status);
-        }
-    }
-    if (sqnorm) {
-        if (T > 0) sum_partials(w.sqpart, N, (int)T, sqnorm, stream);
-        else zero_fill(sqnorm, N, stream);
+    const size_t lds = T <= kRankMaxT ? (2 * sizeof(uint64_t) + sizeof(uint32_t)) * (size_t)(T > 0 ? T : 1)
+                                      : sizeof(uint64_t) * P2;
+    emb_sort_kernel<<<(unsigned)N, kSortThreads, lds, stream>>>(ids, T, V, P2, w, status);
+    const int prefix_here = N <= kPrefixMaxN ? 1 : 0;
+    if (!prefix_here) emb_scan_kernel<<<1, 256, 0, stream>>>(w.counts, N, row_ptr);
+    // four columns per lane when every row starts on a 16-byte (fp32) or
+    // 8-byte (bf16) boundary, and rows likewise
+    const bool vec = D % 4 == 0 && aligned(rows, 16) && aligned(B, dt == DP_F32 ? 16 : 8);
+    const int G = split_for(T);
+    const unsigned grid = (unsigned)(N * G);
+    const size_t olds = 3 * sizeof(int32_t) * (size_t)(T > 0 ? T : 1);
+    if (dt == DP_F32) {
+        if (vec)
+            emb_csr_kernel<float, 4><<<grid, kCsrThreads, olds, stream>>>((const float *)B, T, D, scale, w, G,
+                                                                          prefix_here, row_ptr, uniq_ids, rows,
+                                                                          cap, sqnorm, status);
+        else
+            emb_csr_kernel<float, 1><<<grid, kCsrThreads, olds, stream>>>((const float *)B, T, D, scale, w, G,
+                                                                          prefix_here, row_ptr, uniq_ids, rows,
+                                                                          cap, sqnorm, status);
+    } else {
+        if (vec)
+            emb_csr_kernel<uint16_t, 4><<<grid, kCsrThreads, olds, stream>>>((const uint16_t *)B, T, D, scale, w,
+                                                                             G, prefix_here, row_ptr, uniq_ids,
+                                                                             rows, cap, sqnorm, status);
+        else
+            emb_csr_kernel<uint16_t, 1><<<grid, kCsrThreads, olds, stream>>>((const uint16_t *)B, T, D, scale, w,
+                                                                             G, prefix_here, row_ptr, uniq_ids,
+                                                                             rows, cap, sqnorm, status);
     }
     return launch_status();
 }

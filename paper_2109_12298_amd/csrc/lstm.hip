@@ -31,23 +31,6 @@
 namespace dpg {
 namespace {
 
-// A workgroup barrier that orders LDS only: __syncthreads() would also wait
-// for every outstanding global load (the prefetched steps) at every step.
-__device__ __forceinline__ void lds_barrier()
-{
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-}
-
-// raw-buffer descriptor over one sample's array (gfx9 word for 32-bit
-// untyped accesses); offsets at or past `bytes` read zero
-constexpr uint32_t kOutside = 0x80000000u;
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t sample_rsrc(const void *base, uint32_t bytes)
-{
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, (int)bytes, 0x00020000);
-}
-
 constexpr int kQ = 4;          // lanes per hidden unit
 constexpr int kMaxH = 128;     // 4 * 128 = 512 threads, two waves per SIMD
 // MB: blocks of 16 gate rows (4H <= 16 * MB); DHO: a loss gradient at every

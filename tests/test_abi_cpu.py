@@ -109,8 +109,8 @@ def test_embedding_layernorm_validation():
     assert code_of(f, FAKE, FAKE, dp.DP_F32, 2, 5, 10, 4, 1.0, None, FAKE, FAKE, 10, stream=0) == dp.DP_EINVAL
     assert code_of(f, FAKE, FAKE, dp.DP_F32, 2, 5, 10, 4, 1.0, FAKE, FAKE, FAKE, 10, None, None, None,
                    stream=0) == dp.DP_EINVAL   # workspace required
-    # N*T beyond the launch grid's reach is refused before anything is enqueued
-    assert code_of(f, FAKE, FAKE, dp.DP_F32, 2**16, 1024, 10, 4, 1.0, FAKE, FAKE, FAKE, 10, stream=0) == \
+    # N*T beyond 32-bit position indices is refused before anything is enqueued
+    assert code_of(f, FAKE, FAKE, dp.DP_F32, 2**20, 4096, 10, 4, 1.0, FAKE, FAKE, FAKE, 10, stream=0) == \
         dp.DP_EUNSUPPORTED
     g = dp.dp_grad_sample_layernorm
     assert code_of(g, FAKE, FAKE, dp.DP_F32, 2, 5, 0, 1.0, FAKE, FAKE, stream=0) == dp.DP_EINVAL

@@ -436,9 +436,9 @@ def run_embedding(ids, B, V, cap=None, scale=1.0, dt=None):
     return rp.cpu().numpy(), uq.cpu().numpy(), rows.cpu().numpy(), sq.cpu().numpy(), int(st.item())
 
 
-@pytest.mark.parametrize("D", [37, 100])
+@pytest.mark.parametrize("D", [37, 100, 300])
 @pytest.mark.parametrize("case", ["zipf", "truncated", "all_equal", "all_distinct", "T1", "long", "batch130",
-                                  "bf16"])
+                                  "bf16", "T600", "N2100", "equal256", "half_equal"])
 def test_embedding_cases(case, D):
     say("embedding", case, D)
     r = np.random.default_rng(11)
@@ -460,6 +460,14 @@ def test_embedding_cases(case, D):
     elif case == "bf16":
         ids = np.minimum(r.zipf(1.1, (9, 100)), V) - 1
         dt = dp.DP_BF16
+    elif case == "T600":            # past the rank sort: the bitonic network with padding
+        ids = np.minimum(r.zipf(1.1, (3, 600)), V) - 1
+    elif case == "N2100":           # more samples than the rows pass adds up itself: a scan launch
+        ids = np.minimum(r.zipf(1.3, (2100, 6)), V) - 1
+    elif case == "equal256":        # several rows-pass workgroups per sample; the first owns every position
+        ids = np.full((3, 256), 17)
+    elif case == "half_equal":      # one segment across the workgroups' nominal split points, then distinct ids
+        ids = np.stack([np.concatenate([np.full(160, 3), 10 + r.permutation(900)[:96]]) for _ in range(5)])
     else:
         ids = r.integers(0, 40, (2, 4096))
     ids = ids.astype(np.int64)
