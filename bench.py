@@ -82,10 +82,13 @@ def call_costs(st, nnz=None):
                                          "outer_kernel", None)
             else:
                 staged = bf_mfma and L.T % 32 == 0
+                # fp32 operands whose rows are 16-byte multiples over T % 16 == 0 are staged straight into LDS
+                staged32 = not bf and L.T % 16 == 0 and L.d_in % 4 == 0 and L.d_out % 4 == 0
                 out["grad:" + L.name] = (N * L.T * (L.d_in + L.d_out) * e + grads + N * 4,
                                          2 * N * L.T * L.d_in * L.d_out,
                                          "bf16_grad_sample_kernel" if staged else
-                                         "bf16_per_sample_kernel" if bf_mfma else "ps_gemm_kernel",
+                                         "bf16_per_sample_kernel" if bf_mfma else
+                                         "ps_gemm_dma_kernel" if staged32 else "ps_gemm_kernel",
                                          "bf16" if bf_mfma else "f32")
             if lb.clip_mode == "fused":
                 # all fused Linear layers' weight sums share one grouped call; their
@@ -180,6 +183,7 @@ KERNEL_SOURCES = {
     "bf16_grad_group_kernel": ["paper_2109_12298_amd/csrc/grad_sample_bf16.hip",
                                "paper_2109_12298_amd/csrc/bf16_stage.hpp", "paper_2109_12298_amd/csrc/grad_many.hip"],
     "ps_gemm_kernel": ["paper_2109_12298_amd/csrc/linear.hip"],
+    "ps_gemm_dma_kernel": ["paper_2109_12298_amd/csrc/linear.hip", "paper_2109_12298_amd/csrc/bf16_stage.hpp"],
     "clipsum_gemm_kernel": ["paper_2109_12298_amd/csrc/linear.hip", "paper_2109_12298_amd/csrc/mfma_tile.hpp"],
     "conv_per_sample_kernel": ["paper_2109_12298_amd/csrc/conv2d.hip", "paper_2109_12298_amd/csrc/mfma_tile.hpp"],
     "colsum_kernel": ["paper_2109_12298_amd/csrc/clip.hip"],

@@ -15,6 +15,7 @@
 #include "linear_bf16.hpp"
 #include "grad_sample_bf16.hpp"
 #include "linear_outer.hpp"
+#include "bf16_stage.hpp"
 
 namespace dpg {
 namespace {
@@ -182,6 +183,186 @@ __global__ __launch_bounds__(kThreads) void ps_gemm_kernel(
     }
     sq = block_sum(sq, red);
     if (partial && tid == 0) partial[n * tiles + tile] = sq;
+}
+
+// ---------------------------------------------------------------------------
+// T > 1, fp32, staged straight into LDS (T % 16 == 0, d_in and d_out
+// multiples of 4, 16-byte aligned operands).  Block = (sample n, 64 x 64
+// tile of gW_n) as above.  Stages of 16 positions of both tiles (4 KB each)
+// are copied by global_load_lds_dwordx4 into a ring of four, and the waves
+// wait for exactly the stage they need: no operand passes through registers
+// on its way to LDS, so no wait for a later stage's loads couples in.  A
+// stage's operands are read into registers one stage ahead, while the
+// previous stage's MFMAs run.  Inside a row the 16-byte chunks of
+// odd rows are shifted by half a row, so the two rows a wave's operand read
+// touches fall in different banks.  Each wave keeps two accumulators (odd
+// and even k-steps: two independent MFMA chains), added at the end; the bias
+// gradient is the column sum of the B operands the waves already hold.  Features past the layer's edge read a clamped valid chunk, whose
+// outputs are never stored.
+// ---------------------------------------------------------------------------
+constexpr int kDK = 16;                          // positions per stage
+constexpr int kDStages = 4;
+constexpr int kDRow = kPM * 4;                   // bytes per staged row (64 floats)
+constexpr int kDTile = kDK * kDRow;              // 4 KB per operand tile and stage
+constexpr int kDStageBytes = 2 * kDTile;
+
+__device__ __forceinline__ int dma_chunk_pos(int row, int chunk) { return chunk ^ (8 * (row & 1)); }
+
+__global__ __launch_bounds__(kThreads) void ps_gemm_dma_kernel(const float *__restrict__ A, const float *__restrict__ B,
+                                                               i64 Tn, i64 din, i64 dout, int tiles_j, int tiles,
+                                                               float scale, float *__restrict__ gW,
+                                                               float *__restrict__ gb, float *__restrict__ partial)
+{
+    __shared__ __attribute__((aligned(1024))) char smem[kDStages * kDStageBytes];
+    __shared__ float red[16];
+    __shared__ float bred[2][kPN];
+    const i64 bsw = xcd_swizzle(blockIdx.x, gridDim.x);
+    const i64 n = bsw / tiles;
+    const int tile = (int)(bsw % tiles);
+    const int ti = tile / tiles_j, tj = tile % tiles_j;
+    const i64 j0 = (i64)tj * kPM, i0 = (i64)ti * kPN;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = (wave & 1) * 32, wn = (wave >> 1) * 32;
+    const bool do_bias = gb != nullptr && tj == 0;
+    const int nst = (int)(Tn / kDK);
+    const uint32_t lds0 = bf16s::lds_addr(smem);
+
+    // wave w copies rows 4w .. 4w+3 of both tiles of a stage (one 1 KB
+    // instruction each): lane l -> row 4w + l / 16, LDS chunk l % 16, which
+    // holds feature chunk dma_chunk_pos(row, l % 16) of that row
+    const int srow = 4 * wave + lane / 16;
+    const int schunk = dma_chunk_pos(srow, lane % 16);
+    i64 fa = j0 + 4 * schunk, fb = i0 + 4 * schunk;
+    fa = fa < din ? fa : din - 4;
+    fb = fb < dout ? fb : dout - 4;
+    const float *An = A + n * Tn * din + (i64)srow * din + fa;
+    const float *Bn = B + n * Tn * dout + (i64)srow * dout + fb;
+    const uint32_t lds_a = (uint32_t)(4 * wave * kDRow), lds_b = (uint32_t)(kDTile + 4 * wave * kDRow);
+    auto issue = [&](int c) {
+        const uint32_t L = lds0 + (uint32_t)(c % kDStages) * kDStageBytes;
+        bf16s::dma16(An + (i64)c * kDK * din, L + lds_a);
+        bf16s::dma16(Bn + (i64)c * kDK * dout, L + lds_b);
+    };
+    constexpr int LOADS = 2;                     // per wave per stage
+
+    f32x16 acc0, acc1;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc0[r] = acc1[r] = 0.0f;
+    // column sums of the wave's B operands: lane l holds rows of parity l / 32
+    // of column wn + l % 32 (the bias gradient, from the registers the MFMAs read)
+    float bias_acc = 0.0f;
+    const int li = lane & 31, lk = lane >> 5;
+    // operand addresses inside a stage: A feature wm + li, B feature wn + li, row kk + lk
+    auto opnd = [&](int row, int f) { return row * kDRow + 16 * dma_chunk_pos(row, f >> 2) + 4 * (f & 3); };
+
+    // a stage's operands in registers: k-steps 0, 2, .., 14 of the wave's A and B columns
+    struct Ops {
+        float a[kDK / 2], b[kDK / 2];
+    };
+    auto read_ops = [&](int c, Ops &o) {
+        const char *L = smem + (c % kDStages) * kDStageBytes;
+#pragma unroll
+        for (int k = 0; k < kDK / 2; ++k) {
+            o.a[k] = *reinterpret_cast<const float *>(L + opnd(2 * k + lk, wm + li));
+            o.b[k] = *reinterpret_cast<const float *>(L + kDTile + opnd(2 * k + lk, wn + li));
+        }
+    };
+    auto mma = [&](const Ops &o) {
+#pragma unroll
+        for (int k = 0; k < kDK / 2; k += 2) {
+            acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(o.a[k], o.b[k], acc0, 0, 0, 0);
+            acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(o.a[k + 1], o.b[k + 1], acc1, 0, 0, 0);
+        }
+        float s = 0.0f;
+#pragma unroll
+        for (int k = 0; k < kDK / 2; ++k) s += o.b[k];
+        bias_acc += s;
+    };
+    // stage c has landed once only the loads of the `later` stages after it remain
+    auto wait_landed = [&](int later) {
+        if (later >= 3) bf16s::wait_vmcnt<3 * LOADS>();
+        else if (later == 2) bf16s::wait_vmcnt<2 * LOADS>();
+        else if (later == 1) bf16s::wait_vmcnt<LOADS>();
+        else bf16s::wait_vmcnt<0>();
+    };
+
+    // Per stage c (its operands already in registers): wait for stage c+1,
+    // meet at the barrier (every wave has its stage c operands, so stage c's
+    // buffer may take stage c+4), issue stage c+4, then the MFMAs of stage c
+    // with the reads of stage c+1 between them.
+#pragma unroll
+    for (int c = 0; c < kDStages; ++c)
+        if (c < nst) issue(c);
+    // one stage c < nst - 1: its MFMAs (operands in cur) and the reads of stage c+1 into nxt
+    auto step = [&](int c, const Ops &cur, Ops &nxt) {
+        wait_landed(nst - 2 - c < kDStages - 2 ? nst - 2 - c : kDStages - 2);
+        bf16s::wait_lgkmcnt0();
+        bf16s::stage_barrier();
+        if (c + kDStages < nst) issue(c + kDStages);
+        read_ops(c + 1, nxt);
+        mma(cur);
+#pragma unroll
+        for (int k = 0; k < kDK / 2; ++k) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read (two rows)
+        }
+    };
+    Ops x, y;   // two register sets, stages alternate between them
+    if (nst > 0) {
+        wait_landed(nst - 1 < kDStages - 1 ? nst - 1 : kDStages - 1);
+        bf16s::stage_barrier();
+        read_ops(0, x);
+        int c = 0;
+        for (; c + 2 < nst; c += 2) {
+            step(c, x, y);
+            step(c + 1, y, x);
+        }
+        if (c + 1 < nst) {   // two stages left
+            step(c, x, y);
+            x = y;
+        }
+        mma(x);
+    }
+
+    // acc[r] holds gW[i][j], j = j0 + wm + 8 (r / 4) + 4 (lane / 32) + r % 4, i = i0 + wn + lane % 32
+    float sq = 0.0f;
+    const i64 i = i0 + wn + (lane & 31);
+    if (i < dout) {
+        float *G = gW + n * dout * din + i * din;
+#pragma unroll
+        for (int rb4 = 0; rb4 < 4; ++rb4) {
+            const i64 j = j0 + wm + 8 * rb4 + 4 * (lane >> 5);
+            const float g0 = scale * (acc0[4 * rb4 + 0] + acc1[4 * rb4 + 0]);
+            const float g1 = scale * (acc0[4 * rb4 + 1] + acc1[4 * rb4 + 1]);
+            const float g2 = scale * (acc0[4 * rb4 + 2] + acc1[4 * rb4 + 2]);
+            const float g3 = scale * (acc0[4 * rb4 + 3] + acc1[4 * rb4 + 3]);
+            if (j < din) {   // d_in % 4 == 0: the four j are all in or all out
+                *reinterpret_cast<float4 *>(G + j) = make_float4(g0, g1, g2, g3);
+                sq += g0 * g0 + g1 * g1 + g2 * g2 + g3 * g3;
+            }
+        }
+    }
+    if (do_bias) {
+        // waves 0 and 2 (wm == 0) hold columns 0..31 and 32..63; a column's
+        // even rows (lane l) and odd rows (lane l + 32) are added in that order
+        if (wm == 0 && lane < 32) bred[0][wn + lane] = bias_acc;
+        if (wm == 0 && lane >= 32) bred[1][wn + lane - 32] = bias_acc;
+        __syncthreads();
+        if (tid < kPN && i0 + tid < dout) {
+            const float g = scale * (bred[0][tid] + bred[1][tid]);
+            gb[n * dout + i0 + tid] = g;
+            sq += g * g;
+        }
+    }
+    sq = block_sum(sq, red);
+    if (partial && tid == 0) partial[n * tiles + tile] = sq;
+}
+
+bool ps_dma_ok(const void *A, const void *B, const float *gW, i64 T, i64 din, i64 dout)
+{
+    return T >= kDK && T % kDK == 0 && din % 4 == 0 && dout % 4 == 0 && aligned(A, 16) && aligned(B, 16) &&
+           aligned(gW, 16) && T * (din > dout ? din : dout) < (i64(1) << 31);
 }
 
 // ---------------------------------------------------------------------------
@@ -364,6 +545,13 @@ extern "C" dp_status dp_grad_sample_linear(const void *A, const void *B, dp_dtyp
     const int tiles_j = (int)ceil_div(d_in, kPM);
     const int tiles = (int)ceil_div(d_out, kPN) * tiles_j;
     const dim3 grid((unsigned)(N * tiles));
+    if (dt == DP_F32 && ps_dma_ok(A, B, gW, T, d_in, d_out)) {
+        ps_gemm_dma_kernel<<<grid, kThreads, 0, stream>>>((const float *)A, (const float *)B, T, d_in, d_out,
+                                                          tiles_j, tiles, scale, gW, gb, partial);
+        if (sqnorm)
+            sum_partials(partial, N, tiles, sqnorm, stream);
+        return launch_status();
+    }
     // 16-byte (fp32) / 8-byte (bf16) operand loads and float4 stores when
     // every row starts on such a boundary
     const size_t ea = dt == DP_F32 ? 16 : 8;

@@ -201,7 +201,10 @@ LINEAR_SHAPES = [(1, 1, 1, 1), (3, 1, 37, 13), (2, 2, 5, 3), (4, 5, 37, 13), (3,
                  (3, 40, 100, 20), (2, 256, 100, 400),
                  # T a multiple of 32: the staged bf16 kernel (ragged tiles; one sample per workgroup;
                  # runs of several samples are covered by test_bf16_staged_sample_runs_with_a_tail)
-                 (1, 32, 8, 8), (3, 32, 136, 72), (2, 64, 264, 392), (5, 96, 128, 256), (181, 32, 512, 384)]
+                 (1, 32, 8, 8), (3, 32, 136, 72), (2, 64, 264, 392), (5, 96, 128, 256), (181, 32, 512, 384),
+                 # fp32 with T a multiple of 16 and features multiples of 4 (several of the above too): the
+                 # fp32 kernel staged straight into LDS, at its narrowest and with mostly clamped chunks
+                 (4, 16, 4, 4), (3, 48, 12, 68)]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
