@@ -42,6 +42,8 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0
 PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}     # dense MFMA peaks
+# fp32 vector ALU: 256 CUs x 4 SIMDs x 16 lanes x 2 flops (FMA) x 2 (packed FP32) x 2.4 GHz
+ALU_PEAK_TFLOPS = 157.3
 METRIC = "DP-SGD grad step samples/sec at 1 MI355X; achieved HBM GB/s / MFMA util"
 
 
@@ -125,8 +127,9 @@ def call_costs(st, nnz=None):
         elif isinstance(L, W.LSTMRecurrence):
             # reads the stored gates and cell states, W_hh and dh_last; writes the gate backprop
             G = 4 * L.H
+            # (its dot products are vector-ALU FMAs on a chain of T dependent steps: priced as "alu")
             out["grad:" + L.name] = (N * L.T * (2 * G + L.H) * 4 + G * L.H * 4 + N * L.H * 4,
-                                     2 * N * L.T * G * L.H, "lstm_bptt_kernel", None)
+                                     2 * N * L.T * G * L.H, "lstm_bptt_kernel", "alu")
         elif isinstance(L, W.LayerNorm):
             out["grad:" + L.name] = (2 * N * L.T * L.D * e + 2 * N * L.D * 4, 3 * N * L.T * L.D,
                                      "ln_partial_kernel", None)
@@ -594,8 +597,11 @@ def main():
     dtype = "bf16" if wl.dtype == W.BF16 else "f32"
     # MFMA kernels are priced at their own input type's matrix peak; noise and
     # the column reductions are VALU/HBM work and are compared against HBM
-    mfma_s = flops / (PEAK_TFLOPS[mfma_dtype] * 1e12) if mfma_dtype else 0.0
-    if mfma_s > hbm_s:
+    mfma_s = flops / (PEAK_TFLOPS[mfma_dtype] * 1e12) if mfma_dtype in PEAK_TFLOPS else 0.0
+    if mfma_dtype == "alu":
+        roof = {"bound": "alu", "achieved": round(flops / dt_s / 1e12, 3), "peak": ALU_PEAK_TFLOPS,
+                "unit": "TFLOP/s"}
+    elif mfma_s > hbm_s:
         roof = {"bound": "mfma", "achieved": round(flops / dt_s / 1e12, 3), "peak": PEAK_TFLOPS[mfma_dtype],
                 "unit": "TFLOP/s"}
     else:

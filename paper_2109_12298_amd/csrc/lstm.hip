@@ -19,10 +19,12 @@
 // their gate rows g = 4q + 16m + r (r < 4): W_hh is read once per workgroup.
 // A step reads delta_{t+1} from LDS in 16-byte pieces (the four lanes of a
 // unit read four different pieces, the units of a wave the same ones:
-// broadcasts; two waves per SIMD leave room for all of a lane's reads in
-// flight at once), multiplies it into the lane's rows, adds the four lanes'
-// partial sums with two quad permutes, and every lane of the unit then runs the
-// elementwise update and writes gate q's delta to LDS and to memory.  delta
+// broadcasts), multiplies it into the lane's rows in two fma chains, adds the
+// four lanes' partial sums with two quad permutes, and every lane of the unit
+// then runs the elementwise update (branch-free: lane q selects its gate's
+// factors) and writes gate q's delta to LDS and to memory.  The step is bound
+// by VALU issue (about 140 instructions per wave, two waves on three of the
+// four SIMDs) and the per-step barrier and LDS latencies.  delta
 // is double-buffered in LDS, so one barrier per step.  The gate activations
 // and cell states of a step are loaded kRing steps ahead into a register
 // ring, so their latency is hidden behind the chain.
@@ -30,6 +32,15 @@
 
 namespace dpg {
 namespace {
+
+// tanh(x) = 1 - 2 / (1 + e^{2x}), from the hardware base-2 exponential and
+// reciprocal (about 1e-7 absolute error; e^{2x} overflowing to infinity gives
+// 1, underflowing to 0 gives -1)
+__device__ __forceinline__ float tanh_exp(float x)
+{
+    const float e = __builtin_amdgcn_exp2f(x * 2.8853900817779268f);   // 2 log2(e)
+    return 1.0f - 2.0f * __builtin_amdgcn_rcpf(1.0f + e);
+}
 
 constexpr int kQ = 4;          // lanes per hidden unit
 constexpr int kMaxH = 128;     // 4 * 128 = 512 threads, two waves per SIMD
@@ -92,9 +103,11 @@ __global__ __launch_bounds__(512) void lstm_bptt_kernel(const float *__restrict_
     // update, delta_t to LDS and memory
     auto step = [&](i64 t, const float (&v)[NV], float cp) {
         const float *d = dbuf[cur ^ 1];
-        // the reads in two groups, each group's reads issued together
-        constexpr int HALF = (MB + 1) / 2;
-        float part = 0.0f;
+        // the reads in three groups, each group's reads issued together
+        // (measured at 4H = 400: two groups or one are slower, as are more than five)
+        constexpr int HALF = (MB + 2) / 3;
+        // two fma chains (even and odd rows of each 16-byte piece), added at the end
+        float p0 = 0.0f, p1 = 0.0f;
 #pragma unroll
         for (int m0 = 0; m0 < MB; m0 += HALF) {
             float4 x[HALF];
@@ -103,22 +116,27 @@ __global__ __launch_bounds__(512) void lstm_bptt_kernel(const float *__restrict_
                 if (m0 + m < MB) x[m] = *reinterpret_cast<const float4 *>(d + 4 * q + 16 * (m0 + m));
 #pragma unroll
             for (int m = 0; m < HALF; ++m)
-                if (m0 + m < MB)
-                    part += w[m0 + m][0] * x[m].x + w[m0 + m][1] * x[m].y + w[m0 + m][2] * x[m].z +
-                            w[m0 + m][3] * x[m].w;
+                if (m0 + m < MB) {
+                    p0 = __builtin_fmaf(w[m0 + m][0], x[m].x, p0);
+                    p1 = __builtin_fmaf(w[m0 + m][1], x[m].y, p1);
+                    p0 = __builtin_fmaf(w[m0 + m][2], x[m].z, p0);
+                    p1 = __builtin_fmaf(w[m0 + m][3], x[m].w, p1);
+                }
         }
+        float part = p0 + p1;
         // the unit's four lanes are a quad: two quad permutes add them
         part += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(part), 0xB1, 0xF, 0xF, false));
         part += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(part), 0x4E, 0xF, 0xF, false));
         const float gi = v[0], gf = v[1], gg = v[2], go = v[3], ct = v[4];
         const float dh = part + (DHO ? v[NV - 1] : 0.0f) + (t == T - 1 ? dlast : 0.0f);
-        const float tc = tanhf(ct);
+        const float tc = tanh_exp(ct);
         const float dc = dh * go * (1.0f - tc * tc) + dc_next * f_next;
-        float val;
-        if (q == 0) val = dc * gg * gi * (1.0f - gi);
-        else if (q == 1) val = dc * cp * gf * (1.0f - gf);
-        else if (q == 2) val = dc * gi * (1.0f - gg * gg);
-        else val = dh * tc * go * (1.0f - go);
+        // lane q's gate: delta_q = s1 * s2 * s3 (selects, no branches)
+        const float s1 = q == 3 ? dh : dc;
+        const float s2 = q == 0 ? gg : q == 1 ? cp : q == 2 ? gi : tc;
+        const float gq = q == 0 ? gi : q == 1 ? gf : go;
+        const float s3 = q == 2 ? 1.0f - gg * gg : gq * (1.0f - gq);
+        const float val = s1 * s2 * s3;
         if (live) {
             dbuf[cur][q * H + u] = val;
             dn[t * G + q * H + u] = val;
