@@ -139,16 +139,18 @@ def call_costs(st, nnz=None):
                                      "gn_affine_kernel", None)
             col_bytes += 2 * N * L.C * 4
     if st.grad_group:
-        # the grouped layers' per-sample gradients: the small layers' launch
-        # and the bf16 sequence layers' launch
+        # the grouped layers' per-sample gradients: the small layers' launch,
+        # the bf16 sequence layers' launch and the fp32 sequence layers' launch
         gb_, gf_, kinds = 0, 0, set()
         for i in st.grad_group:
             b0, f0, kn, _ = out.pop("grad:" + st.layers[i].layer.name)
             gb_ += b0
             gf_ += f0
-            kinds.add("bf16_grad_group_kernel" if kn == "bf16_grad_sample_kernel" else "grad_many_kernel")
+            kinds.add({"bf16_grad_sample_kernel": "bf16_grad_group_kernel",
+                       "ps_gemm_dma_kernel": "ps_dma_group_kernel"}.get(kn, "grad_many_kernel"))
         kname = "+".join(sorted(kinds))
-        out["grad:group"] = (gb_, gf_, kname, "bf16" if kname == "bf16_grad_group_kernel" else None)
+        mt = "bf16" if "bf16_grad_group_kernel" in kinds else "f32" if "ps_dma_group_kernel" in kinds else None
+        out["grad:group"] = (gb_, gf_, kname, mt)
     if not st.fold_norms:
         out["norms"] = (len(st.layers) * N * 4 + N * 4, len(st.layers) * N, "norms_kernel", None)
     P = st.wl.n_params
@@ -187,6 +189,8 @@ KERNEL_SOURCES = {
                                "paper_2109_12298_amd/csrc/bf16_stage.hpp", "paper_2109_12298_amd/csrc/grad_many.hip"],
     "ps_gemm_kernel": ["paper_2109_12298_amd/csrc/linear.hip"],
     "ps_gemm_dma_kernel": ["paper_2109_12298_amd/csrc/linear.hip", "paper_2109_12298_amd/csrc/bf16_stage.hpp"],
+    "ps_dma_group_kernel": ["paper_2109_12298_amd/csrc/linear.hip", "paper_2109_12298_amd/csrc/bf16_stage.hpp",
+                            "paper_2109_12298_amd/csrc/linear_staged.hpp", "paper_2109_12298_amd/csrc/grad_many.hip"],
     "clipsum_gemm_kernel": ["paper_2109_12298_amd/csrc/linear.hip", "paper_2109_12298_amd/csrc/mfma_tile.hpp"],
     "conv_per_sample_kernel": ["paper_2109_12298_amd/csrc/conv2d.hip", "paper_2109_12298_amd/csrc/mfma_tile.hpp"],
     "colsum_kernel": ["paper_2109_12298_amd/csrc/clip.hip"],
@@ -202,6 +206,14 @@ KERNEL_SOURCES = {
 }
 
 
+def kernel_sources(kernel):
+    """The sources of a kernel, or of every kernel of a "+"-joined group of them."""
+    out = []
+    for k in kernel.split("+"):
+        out += [f for f in KERNEL_SOURCES.get(k, []) if f not in out]
+    return out
+
+
 def traffic_for(kernel, workload, call):
     """HBM bytes per launch from committed counter runs, if the kernel source is unchanged."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
@@ -212,7 +224,7 @@ def traffic_for(kernel, workload, call):
     rec = table.get("%s/%s" % (workload, call))
     if not rec or rec.get("kernel") != kernel:
         return None
-    if rec.get("source_sha") != src_hash(KERNEL_SOURCES.get(kernel, [])):
+    if rec.get("source_sha") != src_hash(kernel_sources(kernel)):
         return None
     return rec.get("bytes_per_launch")
 
@@ -224,7 +236,7 @@ def counters_for(kernel, workload, call):
         return None
     with open(path) as f:
         rec = json.load(f).get("%s/%s" % (workload, call))
-    if not rec or rec.get("kernel") != kernel or rec.get("source_sha") != src_hash(KERNEL_SOURCES.get(kernel, [])):
+    if not rec or rec.get("kernel") != kernel or rec.get("source_sha") != src_hash(kernel_sources(kernel)):
         return None
     return rec
 
@@ -277,7 +289,7 @@ def record_traffic(meta_path, fetch_csv, write_csv):
         kern = meta["kernels"][n]
         f, w = per[n]["FETCH_SIZE"], per[n]["WRITE_SIZE"]
         table["%s/%s" % (meta["workload"], n)] = {
-            "kernel": kern, "source_sha": src_hash(KERNEL_SOURCES.get(kern, [])),
+            "kernel": kern, "source_sha": src_hash(kernel_sources(kern)),
             "bytes_per_launch": round(f[0] + w[0]), "fetch_bytes_per_launch": round(f[0]),
             "write_bytes_per_launch": round(w[0]), "fetch_scale": round(f[1], 4), "write_scale": round(w[1], 4),
             "algorithmic_bytes": meta["algorithmic_bytes"][n], "dispatched": f[2]}
@@ -323,7 +335,7 @@ def record_counters(meta_path, csv_path):
     for n, reg in zip(calls, regs):
         kern = meta["kernels"][n]
         names = sorted({k for e in reg for k in e["c"]})
-        rec = {"kernel": kern, "source_sha": src_hash(KERNEL_SOURCES.get(kern, [])), "launches": meta["launches"],
+        rec = {"kernel": kern, "source_sha": src_hash(kernel_sources(kern)), "launches": meta["launches"],
                "algorithmic_flops": meta.get("algorithmic_flops", {}).get(n)}
         for k in names:
             if k == "MfmaUtil":

@@ -187,7 +187,7 @@ typedef struct dp_layer_grad {
 /* The per-sample gradients of `count` layers that share N and the dtype, as
  * by one dp_grad_sample_linear / dp_grad_sample_conv2d call per layer (same
  * formulas; results equal to rounding order, and bit for bit for the bf16
- * sequence layers), in grouped launches for the layers that qualify
+ * and fp32 sequence layers), in grouped launches for the layers that qualify
  * (dp_grad_sample_many_grouped), so that the layers' fixed costs (launch,
  * load round trip) and their last, partly idle rounds of workgroups overlap
  * instead of adding up:
@@ -198,7 +198,14 @@ typedef struct dp_layer_grad {
  *    its staged kernel (T a multiple of 32, d_in and d_out multiples of 8,
  *    16-byte aligned A, B, gW): runs of consecutive samples per 256 x 128
  *    tile, the run length balanced over all of them, up to 16 layers per
- *    launch, plus one launch adding each layer's squared-norm partials.
+ *    launch, plus one launch adding each layer's squared-norm partials;
+ *  - fp32 Linear layers over a sequence that dp_grad_sample_linear runs on
+ *    its staged kernel (T a multiple of 16, d_in and d_out multiples of 4,
+ *    16-byte aligned A, B, gW): up to 16 layers per launch, each workgroup
+ *    taking one 64 x 64 tile of one sample, a sample's tiles of all the
+ *    layers together (layers that read the same B, as an LSTM's two weight
+ *    matrices do, read it while it is cached), plus one launch adding each
+ *    layer's squared-norm partials.
  * The other layers run through the single-layer entry points inside this
  * call, one after the other on `stream`, sharing `ws`.  Arguments are
  * checked as the single-layer calls check them; the first invalid layer's

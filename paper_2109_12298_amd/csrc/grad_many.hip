@@ -15,6 +15,7 @@
 #include "conv2d_small_dev.hpp"
 #include "grad_sample_bf16.hpp"
 #include "linear_outer.hpp"
+#include "linear_staged.hpp"
 
 namespace dpg {
 namespace {
@@ -113,6 +114,14 @@ bool staged(const dp_layer_grad &L, dp_dtype dt, i64 N)
            bf16_staged_ok(L.A, L.B, L.gW, N, L.T, L.d_in, L.d_out);
 }
 
+// an fp32 Linear layer over a sequence that the staged fp32 kernel takes:
+// these layers share a launch of their own (fp32_grad_sample_group)
+bool staged32(const dp_layer_grad &L, dp_dtype dt, i64 N)
+{
+    return validate(L, dt, N) == DP_OK && N > 0 && L.kind == DP_LAYER_LINEAR && dt == DP_F32 && L.T > 1 &&
+           fp32_staged_ok(L.A, L.B, L.gW, N, L.T, L.d_in, L.d_out);
+}
+
 // a layer of the small-layer launch (grad_many_kernel)
 bool small(const dp_layer_grad &L, dp_dtype dt, i64 N)
 {
@@ -121,12 +130,20 @@ bool small(const dp_layer_grad &L, dp_dtype dt, i64 N)
     return conv_path() == DP_CONV_AUTO && conv_small_ok(conv_args(L, N));
 }
 
-bool grouped(const dp_layer_grad &L, dp_dtype dt, i64 N) { return small(L, dt, N) || staged(L, dt, N); }
+bool grouped(const dp_layer_grad &L, dp_dtype dt, i64 N)
+{
+    return small(L, dt, N) || staged(L, dt, N) || staged32(L, dt, N);
+}
 
 // scratch of the staged launch: each layer's squared-norm partials
 size_t staged_partials_bytes(const dp_layer_grad &L, i64 N)
 {
     return L.sqnorm ? align_up((size_t)N * bf16_staged_parts(L.d_in, L.d_out) * sizeof(float), 256) : 0;
+}
+
+size_t staged32_partials_bytes(const dp_layer_grad &L, i64 N)
+{
+    return L.sqnorm ? align_up((size_t)N * fp32_staged_parts(L.d_in, L.d_out) * sizeof(float), 256) : 0;
 }
 
 size_t single_workspace(const dp_layer_grad &L, dp_dtype dt, i64 N)
@@ -219,6 +236,18 @@ extern "C" size_t dp_grad_sample_many_workspace_bytes(const dp_layer_grad *items
         ++in_launch;
         need = launch > need ? launch : need;
     }
+    launch = 0;
+    in_launch = 0;
+    for (int k = 0; k < count; ++k) {
+        if (!staged32(items[k], dt, N)) continue;
+        if (in_launch == kPsGroupMax) {
+            launch = 0;
+            in_launch = 0;
+        }
+        launch += staged32_partials_bytes(items[k], N);
+        ++in_launch;
+        need = launch > need ? launch : need;
+    }
     for (int k = 0; k < count; ++k) {
         if (grouped(items[k], dt, N) || validate(items[k], dt, N) != DP_OK) continue;
         const size_t w = single_workspace(items[k], dt, N);
@@ -269,6 +298,30 @@ extern "C" dp_status dp_grad_sample_many(const dp_layer_grad *items, int32_t cou
             grp[n++] = Bf16GroupLayer{L.A, L.B, L.T, L.d_in, L.d_out, L.scale, L.gW, L.gb, L.sqnorm,
                                       L.sqnorm ? (float *)((char *)ws + off) : nullptr};
             off += staged_partials_bytes(L, N);
+        }
+        if (n) flush();
+        st = launch_status();
+        if (st != DP_OK) return st;
+    }
+
+    // fp32 sequence layers on the staged kernel, in launches of up to
+    // kPsGroupMax, their norm partials one layer after another in the scratch
+    {
+        Fp32GroupLayer grp[kPsGroupMax];
+        int n = 0;
+        size_t off = 0;
+        auto flush = [&]() {
+            fp32_grad_sample_group(grp, n, N, stream);
+            n = 0;
+            off = 0;
+        };
+        for (int k = 0; k < count; ++k) {
+            const dp_layer_grad &L = items[k];
+            if (!staged32(L, dt, N)) continue;
+            if (n == kPsGroupMax) flush();
+            grp[n++] = Fp32GroupLayer{L.A, L.B, L.T, L.d_in, L.d_out, L.scale, L.gW, L.gb, L.sqnorm,
+                                      L.sqnorm ? (float *)((char *)ws + off) : nullptr};
+            off += staged32_partials_bytes(L, N);
         }
         if (n) flush();
         st = launch_status();

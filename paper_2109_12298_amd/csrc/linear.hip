@@ -16,6 +16,7 @@
 #include "grad_sample_bf16.hpp"
 #include "linear_outer.hpp"
 #include "bf16_stage.hpp"
+#include "linear_staged.hpp"
 
 namespace dpg {
 namespace {
@@ -208,17 +209,22 @@ constexpr int kDStageBytes = 2 * kDTile;
 
 __device__ __forceinline__ int dma_chunk_pos(int row, int chunk) { return chunk ^ (8 * (row & 1)); }
 
-__global__ __launch_bounds__(kThreads) void ps_gemm_dma_kernel(const float *__restrict__ A, const float *__restrict__ B,
-                                                               i64 Tn, i64 din, i64 dout, int tiles_j, int tiles,
-                                                               float scale, float *__restrict__ gW,
-                                                               float *__restrict__ gb, float *__restrict__ partial)
+// LDS of one workgroup of the staged kernels
+struct DmaShared {
+    __attribute__((aligned(1024))) char ring[kDStages * kDStageBytes];
+    float red[16];
+    float bred[2][kPN];
+};
+
+// Tile `tile` of sample n (the body of the single-layer and grouped launches)
+__device__ __forceinline__ void ps_dma_tile(const float *__restrict__ A, const float *__restrict__ B, i64 Tn,
+                                            i64 din, i64 dout, int tiles_j, int tiles, i64 n, int tile,
+                                            float scale, float *__restrict__ gW, float *__restrict__ gb,
+                                            float *__restrict__ partial, DmaShared &sh)
 {
-    __shared__ __attribute__((aligned(1024))) char smem[kDStages * kDStageBytes];
-    __shared__ float red[16];
-    __shared__ float bred[2][kPN];
-    const i64 bsw = xcd_swizzle(blockIdx.x, gridDim.x);
-    const i64 n = bsw / tiles;
-    const int tile = (int)(bsw % tiles);
+    char *smem = sh.ring;
+    float *red = sh.red;
+    float (*bred)[kPN] = sh.bred;
     const int ti = tile / tiles_j, tj = tile % tiles_j;
     const i64 j0 = (i64)tj * kPM, i0 = (i64)ti * kPN;
     const int tid = threadIdx.x, lane = tid & 63;
@@ -359,6 +365,63 @@ __global__ __launch_bounds__(kThreads) void ps_gemm_dma_kernel(const float *__re
     if (partial && tid == 0) partial[n * tiles + tile] = sq;
 }
 
+__global__ __launch_bounds__(kThreads) void ps_gemm_dma_kernel(const float *__restrict__ A, const float *__restrict__ B,
+                                                               i64 Tn, i64 din, i64 dout, int tiles_j, int tiles,
+                                                               float scale, float *__restrict__ gW,
+                                                               float *__restrict__ gb, float *__restrict__ partial)
+{
+    __shared__ DmaShared sh;
+    const i64 bsw = xcd_swizzle(blockIdx.x, gridDim.x);
+    ps_dma_tile(A, B, Tn, din, dout, tiles_j, tiles, bsw / tiles, (int)(bsw % tiles), scale, gW, gb, partial, sh);
+}
+
+// Several staged layers sharing N in one launch: workgroup b takes sample
+// b / tiles_all and, of that sample's tiles of all layers (layer after layer),
+// tile b % tiles_all, so layers that read the same B (an LSTM's two weight
+// matrices) read it while it is in L2.
+struct PsDmaItem {
+    const float *A, *B;
+    i64 T, din, dout;
+    int tiles_j, tiles, tile0;
+    float scale;
+    float *gW, *gb, *sqnorm, *partial;
+};
+struct PsDmaGroup {
+    int count, tiles_all;
+    i64 N;
+    PsDmaItem it[kPsGroupMax];
+};
+
+__global__ __launch_bounds__(kThreads) void ps_dma_group_kernel(const PsDmaGroup g)
+{
+    __shared__ DmaShared sh;
+    const i64 bsw = xcd_swizzle(blockIdx.x, gridDim.x);
+    const i64 n = bsw / g.tiles_all;
+    const int r = (int)(bsw % g.tiles_all);
+    int k = 0;
+    while (k + 1 < g.count && g.it[k + 1].tile0 <= r) ++k;
+    const PsDmaItem &L = g.it[k];
+    ps_dma_tile(L.A, L.B, L.T, L.din, L.dout, L.tiles_j, L.tiles, n, r - L.tile0, L.scale, L.gW, L.gb, L.partial,
+                sh);
+}
+
+// One wave per (layer, sample): sqnorm[n] = the sample's tile partials added
+// as sum_partials adds them (lane l takes partials l, l+64, ..., then the
+// same butterfly), so the grouped launch matches the single-layer call bit
+// for bit.
+__global__ __launch_bounds__(256) void ps_dma_group_sqnorm_kernel(const PsDmaGroup g)
+{
+    const PsDmaItem &L = g.it[blockIdx.y];
+    const i64 n = (i64)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    if (L.sqnorm == nullptr || n >= g.N) return;
+    const float *p = L.partial + n * L.tiles;
+    float s = 0.0f;
+    for (int t = lane; t < L.tiles; t += kWave) s += p[t];
+    s = wave_sum(s);
+    if (lane == 0) L.sqnorm[n] = s;
+}
+
 bool ps_dma_ok(const void *A, const void *B, const float *gW, i64 T, i64 din, i64 dout)
 {
     return T >= kDK && T % kDK == 0 && din % 4 == 0 && dout % 4 == 0 && aligned(A, 16) && aligned(B, 16) &&
@@ -460,6 +523,51 @@ ClipSplit clip_split(i64 N, i64 T, i64 din, i64 dout)
 }
 
 }  // namespace
+
+bool fp32_staged_ok(const void *A, const void *B, const void *gW, i64 N, i64 T, i64 din, i64 dout)
+{
+    return ps_dma_ok(A, B, (const float *)gW, T, din, dout) && N < (i64(1) << 40) &&
+           N * ceil_div(din, kPM) * ceil_div(dout, kPN) < (i64(1) << 26);
+}
+
+int fp32_staged_parts(i64 din, i64 dout) { return (int)(ceil_div(din, kPM) * ceil_div(dout, kPN)); }
+
+void fp32_grad_sample_group(const Fp32GroupLayer *layers, int count, i64 N, hipStream_t stream)
+{
+    if (count <= 0 || N <= 0) return;
+    PsDmaGroup g;
+    g.count = count;
+    g.N = N;
+    int tiles_all = 0;
+    bool norms = false;
+    for (int k = 0; k < count; ++k) {
+        const Fp32GroupLayer &L = layers[k];
+        PsDmaItem &it = g.it[k];
+        it.A = (const float *)L.A;
+        it.B = (const float *)L.B;
+        it.T = L.T;
+        it.din = L.din;
+        it.dout = L.dout;
+        it.tiles_j = (int)ceil_div(L.din, kPM);
+        it.tiles = fp32_staged_parts(L.din, L.dout);
+        it.tile0 = tiles_all;
+        it.scale = L.scale;
+        it.gW = L.gW;
+        it.gb = L.gb;
+        it.sqnorm = L.sqnorm;
+        it.partial = L.sqnorm ? L.partial : nullptr;
+        tiles_all += it.tiles;
+        norms = norms || L.sqnorm != nullptr;
+    }
+    for (int k = count; k < kPsGroupMax; ++k) {
+        g.it[k] = g.it[count - 1];
+        g.it[k].tile0 = tiles_all;
+    }
+    g.tiles_all = tiles_all;
+    ps_dma_group_kernel<<<(unsigned)(N * tiles_all), kThreads, 0, stream>>>(g);
+    if (norms)
+        ps_dma_group_sqnorm_kernel<<<dim3((unsigned)ceil_div(N, 4), (unsigned)count), 256, 0, stream>>>(g);
+}
 
 dp_status check_linear(const void *A, const void *B, dp_dtype dt, i64 N, i64 T, i64 din, i64 dout)
 {

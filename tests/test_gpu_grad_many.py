@@ -183,3 +183,49 @@ def test_grouped_bf16_more_layers_than_one_launch():
     bufs, items = run_many(specs, 3, dp.DP_BF16, 1.2, seed=77)
     assert all(dp.dp_grad_sample_many_grouped(items, k, dp.DP_BF16, 3) for k in range(len(specs)))
     check_oracle(specs, bufs, 1.2, "eighteen bf16")
+
+
+# fp32 Linear layers over a sequence: the staged grouped launch (a sample's
+# tiles of all layers together); the first two read the same B, as an LSTM's
+# W_ih and W_hh do
+SEQ32 = [("lin", 100, 400, 256, True), ("lin", 100, 400, 256, True),
+         ("lin", 36, 52, 48, False),                         # ragged tiles, no bias
+         ("lin", 64, 16, 8, True),                           # T % 16 != 0: the single-layer path
+         ("lin", 7, 9, 1, True)]                             # T = 1: the small-layer launch
+
+
+@pytest.mark.parametrize("N", [1, 5, 37])
+def test_grouped_fp32_sequence_layers_match_oracle_and_single_calls(N):
+    say("grad_many fp32 sequence layers N=", N)
+    specs = SEQ32 if N < 37 else [("lin", 100, 400, 64, True), ("lin", 100, 400, 64, True)] + SEQ32[2:]
+    rng = np.random.default_rng(60 + N)
+    bufs = [make(s, N, rng, torch.float32) for s in specs]
+    bufs[1] = (bufs[1][0], bufs[0][1]) + tuple(bufs[1][2:])
+    items = dp.make_layer_grads([item(s, *b, 0.7) for s, b in zip(specs, bufs)])
+    ws = torch.empty(max(dp.dp_grad_sample_many_workspace_bytes(items, len(specs), dp.DP_F32, N), 1),
+                     dtype=torch.uint8, device=DEV)
+    dp.dp_grad_sample_many(items, len(specs), dp.DP_F32, N, None, ws)
+    torch.cuda.synchronize()
+    got = [dp.dp_grad_sample_many_grouped(items, k, dp.DP_F32, N) for k in range(len(specs))]
+    assert got == [True, True, True, False, True]
+    check_oracle(specs, bufs, 0.7, "fp32 seq")
+    for spec, (At, Bt, gW, gb, sq) in zip(specs, bufs):
+        _, din, dout, T, _ = spec
+        gW2, gb2, sq2 = torch.empty_like(gW), (torch.empty_like(gb) if gb is not None else None), torch.empty_like(sq)
+        ws1 = torch.empty(max(dp.dp_grad_sample_linear_workspace_bytes(N, T, din, dout, dp.DP_F32), 1),
+                          dtype=torch.uint8, device=DEV)
+        dp.dp_grad_sample_linear(At, Bt, dp.DP_F32, N, T, din, dout, 0.7, gW2, gb2, sq2, None, ws1)
+        torch.cuda.synchronize()
+        assert torch.equal(gW, gW2), spec
+        if gb is not None:
+            assert torch.equal(gb, gb2), spec
+        assert torch.equal(sq, sq2), spec
+
+
+def test_grouped_fp32_more_layers_than_one_launch():
+    """Eighteen staged fp32 layers: two grouped launches, each with its own partials."""
+    say("grad_many 18 fp32 sequence layers")
+    specs = [("lin", 16 + 4 * (k % 3), 20 + 4 * (k % 5), 16 * (1 + k % 2), k % 4 != 1) for k in range(18)]
+    bufs, items = run_many(specs, 3, dp.DP_F32, 1.2, seed=78)
+    assert all(dp.dp_grad_sample_many_grouped(items, k, dp.DP_F32, 3) for k in range(len(specs)))
+    check_oracle(specs, bufs, 1.2, "eighteen fp32")
