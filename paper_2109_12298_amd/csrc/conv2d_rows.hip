@@ -49,6 +49,7 @@ struct RowsShape {
     int PC;               // positions per chunk, RC * Wo rounded up to even
     int x_floats;         // np * XR * Wp
     int vec;              // float4 stores of gW
+    int fast;             // full tiles (nblk == kMaxBlk), stride 1, 16-byte runs: the branch-free contraction
     float inv_khw, inv_kw, inv_wo;
     // staging runs of VW elements: xwv = W / VW runs per input row, gqv =
     // PC / VW runs per channel of the chunk's backprop.  Stepping a run index
@@ -120,12 +121,58 @@ __device__ __forceinline__ void unpack(const Raw<XW> &x, float (&v)[VW])
     }
 }
 
+// The contraction of a chunk for full tiles at stride 1 (Wo a multiple of 4,
+// so the chunk holds whole groups of four positions and the four positions
+// 4k .. 4k+3 sit in one output row): the wave's NACT blocks are compile-time,
+// so the loop has no branch; pair q's position offset is pbase + half and
+// pair q+1's two further, tracked in scalars instead of read from the
+// position table, and each block's two operands are one ds_read2.  SHX is
+// the block shared by the two wave rows (-1: none), whose MFMA wave row wq
+// runs for pair q + wq of each step only (operands chosen by selects).  The
+// accumulation order per block is the generic loop's (pair q, then q+1).
+template <int FM, int NACT, int SHX, int BN>
+__device__ __forceinline__ void contract_fast(f32x16_t (&acc)[FM], const int (&koff)[FM], const float *Xs,
+                                              const float *Gs, int qfull, int half, int gl, int Wo, int xR, int wq)
+{
+    constexpr int GSP = 2 * BN + 1;
+    const float *gp = Gs + half * BN + gl;
+    int pbase = 0, ow0 = 0;
+    for (int q = 0; q < qfull; q += 2) {
+        const int po = pbase + half;
+        float a0[NACT], a1[NACT];
+#pragma unroll
+        for (int x = 0; x < NACT; ++x) {
+            const float *xp = Xs + koff[x] + po;
+            a0[x] = xp[0];
+            a1[x] = xp[2];
+        }
+        const float b0 = gp[q * GSP], b1 = gp[(q + 1) * GSP];
+#pragma unroll
+        for (int x = 0; x < NACT; ++x)
+            if (x != SHX) acc[x] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0[x], b0, acc[x], 0, 0, 0);
+#pragma unroll
+        for (int x = 0; x < NACT; ++x)
+            if (x != SHX) acc[x] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1[x], b1, acc[x], 0, 0, 0);
+        if constexpr (SHX >= 0) {
+            // the shared block: wave row wq takes pair q + wq of the two
+            const float as = wq == 0 ? a0[SHX] : a1[SHX];
+            const float bs = wq == 0 ? b0 : b1;
+            acc[SHX] = __builtin_amdgcn_mfma_f32_32x32x2f32(as, bs, acc[SHX], 0, 0, 0);
+        }
+        ow0 += 4;
+        pbase += 4;
+        const bool wrap = ow0 == Wo;
+        ow0 = wrap ? 0 : ow0;
+        pbase += wrap ? xR - Wo : 0;
+    }
+}
+
 // WCO: 32-channel blocks per tile (1 or 2).  The waves form (4 / WCO) column
 // rows x WCO channel columns; wave row q takes blocks q, q + 4/WCO, ...
 // VW: elements per staging load (4: a 16-byte run of an input row or of a
 // channel's backprop; 1: single elements).  XS, GS: X and backprop loads per
 // thread per chunk, at most.  OCC: workgroups per CU the registers allow.
-template <typename T, int WCO, int VW, int XS, int GS, int OCC>
+template <typename T, int WCO, int VW, int XS, int GS, int OCC, bool FAST>
 __global__ __launch_bounds__(kThreads, OCC) void conv_rows_kernel(const T *__restrict__ X, const T *__restrict__ GY,
                                                                   RowsShape s, float scale, float *__restrict__ gW,
                                                                   float *__restrict__ gb, float *__restrict__ sqout,
@@ -324,10 +371,12 @@ __global__ __launch_bounds__(kThreads, OCC) void conv_rows_kernel(const T *__res
         load_chunk(oh0);                               // in flight while the other waves finish
         __syncthreads();                               // the previous chunk is consumed
         store_chunk();
-        for (int p = tid; p < s.PC; p += kThreads) {
-            int oh, ow;
-            fdivmod(p, s.Wo, s.inv_wo, oh, ow);
-            Pt[p] = p < len ? oh * s.sh * s.xR + ow * s.sw : 0;
+        if constexpr (!FAST) {
+            for (int p = tid; p < s.PC; p += kThreads) {
+                int oh, ow;
+                fdivmod(p, s.Wo, s.inv_wo, oh, ow);
+                Pt[p] = p < len ? oh * s.sh * s.xR + ow * s.sw : 0;
+            }
         }
         __syncthreads();
         if (do_bias) {
@@ -340,6 +389,18 @@ __global__ __launch_bounds__(kThreads, OCC) void conv_rows_kernel(const T *__res
         const int gl = wc * 32 + (lane & 31);
         // whole pairs two at a time without masks, then what is left masked
         const int qfull = (len >> 2) << 1;
+        if constexpr (FAST) {
+            // (the chunk holds whole groups of four positions: no remainder)
+            if constexpr (WKK == 2) {
+                // nine blocks over two wave rows: five each, the last shared
+                contract_fast<FM, 5, 4, BN>(acc, koff, Xs, Gs, qfull, half, gl, s.Wo, s.xR, wq);
+            } else {
+                // nine blocks over four wave rows: row 0 takes 0, 4, 8, the others two
+                if (wq == 0) contract_fast<FM, 3, -1, BN>(acc, koff, Xs, Gs, qfull, half, gl, s.Wo, s.xR, wq);
+                else contract_fast<FM, 2, -1, BN>(acc, koff, Xs, Gs, qfull, half, gl, s.Wo, s.xR, wq);
+            }
+            continue;
+        }
         for (int q = 0; q < qfull; q += 2) {
             float a[2][FM], b[2];
 #pragma unroll
@@ -520,6 +581,7 @@ bool plan_rows(const ConvRowsArgs &a, const Variant &v, RowsShape &s)
     s.xC = chan_stride(s.XR, s.xR, s.khw);
     s.x_floats = (s.np * s.xC + 3) & ~3;      // the backprop stage starts 16-byte aligned
     s.vec = 0;
+    s.fast = v.vw == 4 && s.nblk == kMaxBlk && s.sh == 1 && s.sw == 1 && s.Wo % 4 == 0;
     s.inv_khw = 1.0f / (float)s.khw;
     s.inv_kw = 1.0f / (float)s.kw;
     s.inv_wo = 1.0f / (float)s.Wo;
@@ -567,7 +629,14 @@ void launch_variant(const ConvRowsArgs &a, const RowsShape &s, float scale, floa
                     int direct, hipStream_t stream)
 {
     const dim3 grid((unsigned)(a.N * s.ktiles * s.ctiles));
-    conv_rows_kernel<T, WCO, VW, XS, GS, OCC><<<grid, kThreads, lds_bytes(s), stream>>>(
+    if constexpr (VW == 4) {
+        if (s.fast) {
+            conv_rows_kernel<T, WCO, VW, XS, GS, OCC, true><<<grid, kThreads, lds_bytes(s), stream>>>(
+                (const T *)a.X, (const T *)a.GY, s, scale, gW, gb, sqout, direct);
+            return;
+        }
+    }
+    conv_rows_kernel<T, WCO, VW, XS, GS, OCC, false><<<grid, kThreads, lds_bytes(s), stream>>>(
         (const T *)a.X, (const T *)a.GY, s, scale, gW, gb, sqout, direct);
 }
 

@@ -335,7 +335,11 @@ CONV_SHAPES = [  # N, Cin, H, W, Cout, kh, kw, sh, sw, ph, pw
     (2, 64, 16, 16, 128, 3, 3, 1, 1, 1, 1), (2, 128, 8, 8, 128, 3, 3, 1, 1, 1, 1),
     (2, 128, 8, 8, 256, 3, 3, 1, 1, 1, 1),
     (3, 4, 8, 8, 20, 3, 3, 1, 1, 0, 0),        # unpadded, sizes multiples of 4: direct-to-LDS staging
-    (2, 12, 9, 10, 24, 3, 2, 2, 2, 0, 0)]      # the same with stride 2
+    (2, 12, 9, 10, 24, 3, 2, 2, 2, 0, 0),      # the same with stride 2
+    # row chunks with full nine-block tiles at stride 1 (the branch-free contraction):
+    (2, 32, 16, 16, 20, 3, 3, 1, 1, 1, 1),     # one channel block, four wave rows
+    (2, 62, 8, 8, 64, 3, 3, 1, 1, 1, 1),       # two column tiles, the last block past the weight's columns
+    (3, 32, 12, 12, 96, 3, 3, 1, 1, 1, 1)]     # a second channel tile only half used
 
 
 # One shape per tile configuration of the fast path and staging mode (whole
@@ -393,7 +397,8 @@ def test_conv_shapes(shape, conv_path):
     assert_rel(sq.cpu().numpy(), rsq, 1e-4, "conv sqnorm")
 
 
-@pytest.mark.parametrize("shape", [CONV_SHAPES[1], CONV_SHAPES[2], CONV_SHAPES[3], CONV_SHAPES[5]])
+@pytest.mark.parametrize("shape", [CONV_SHAPES[1], CONV_SHAPES[2], CONV_SHAPES[3], CONV_SHAPES[5], CONV_SHAPES[-3],
+                                   CONV_SHAPES[-2]])
 def test_conv_shapes_bf16(shape, conv_path):
     """bf16 inputs (scalar staging loads) against the oracle on the rounded values."""
     N, Cin, H, Wd, Cout, kh, kw, sh, sw, ph, pw = shape
