@@ -491,9 +491,11 @@ __global__ __launch_bounds__(kThreads, OCC) void conv_rows_kernel(const T *__res
             }
         }
     }
+    // LDS-only barriers from here on: a __syncthreads would also wait for the
+    // gradient stores just issued, and hold the workgroup's slot until they land
     if (do_bias) {
         bsum[bseg * BN + bco] = bacc;
-        __syncthreads();
+        lds_barrier();
         if (tid < BN && n0 + tid < s.Cout) {
             float b = 0.0f;
 #pragma unroll
@@ -505,7 +507,7 @@ __global__ __launch_bounds__(kThreads, OCC) void conv_rows_kernel(const T *__res
     }
     sq = wave_sum(sq);
     if (lane == 0) red[wave] = sq;
-    __syncthreads();
+    lds_barrier();
     if (tid == 0 && sqout) {
         float t = 0.0f;
 #pragma unroll
