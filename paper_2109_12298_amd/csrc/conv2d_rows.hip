@@ -50,6 +50,7 @@ struct RowsShape {
     int x_floats;         // np * XR * Wp
     int vec;              // float4 stores of gW
     int fast;             // full tiles (nblk == kMaxBlk), stride 1, 16-byte runs: the branch-free contraction
+    int xcd;              // a sample's tiles on one XCD (where a tile reads at least the bytes it stores)
     float inv_khw, inv_kw, inv_wo;
     // staging runs of VW elements: xwv = W / VW runs per input row, gqv =
     // PC / VW runs per channel of the chunk's backprop.  Stepping a run index
@@ -186,8 +187,12 @@ __global__ __launch_bounds__(kThreads, OCC) void conv_rows_kernel(const T *__res
     __shared__ float bsum[kThreads];          // bias partials [segment][channel]
 
     const int tiles = s.ktiles * s.ctiles;
-    const i64 n = blockIdx.x / tiles;
-    const int tile = (int)(blockIdx.x % tiles);
+    // a sample's tiles on one XCD, so that the input channels and backprop
+    // rows that several of them read are served from that XCD's L2 (for
+    // tiles whose stores outweigh their reads, spreading them measured better)
+    const i64 bsw = s.xcd ? xcd_swizzle(blockIdx.x, gridDim.x) : (i64)blockIdx.x;
+    const i64 n = bsw / tiles;
+    const int tile = (int)(bsw % tiles);
     const int tk = tile / s.ctiles, tc = tile % s.ctiles;
     const int m0 = tk * s.nblk * 32;          // first weight column
     const int n0 = tc * BN;                   // first output channel
@@ -584,6 +589,12 @@ bool plan_rows(const ConvRowsArgs &a, const Variant &v, RowsShape &s)
     s.x_floats = (s.np * s.xC + 3) & ~3;      // the backprop stage starts 16-byte aligned
     s.vec = 0;
     s.fast = v.vw == 4 && s.nblk == kMaxBlk && s.sh == 1 && s.sw == 1 && s.Wo % 4 == 0;
+    {
+        // per tile: the input channels and backprop rows read, the gradient block stored
+        const long reads = (long)s.np * s.H * s.W + (long)BN * s.L;
+        const long writes = (long)s.nblk * 32 * BN;
+        s.xcd = s.ktiles * s.ctiles > 1 && reads >= writes;
+    }
     s.inv_khw = 1.0f / (float)s.khw;
     s.inv_kw = 1.0f / (float)s.kw;
     s.inv_wo = 1.0f / (float)s.Wo;
