@@ -397,6 +397,45 @@ def test_conv_shapes(shape, conv_path):
     assert_rel(sq.cpu().numpy(), rsq, 1e-4, "conv sqnorm")
 
 
+def run_conv_case(shape, dt, scale, seed):
+    N, Cin, H, Wd, Cout, kh, kw, sh, sw, ph, pw = shape
+    Ho = (H + 2 * ph - kh) // sh + 1
+    Wo = (Wd + 2 * pw - kw) // sw + 1
+    r = np.random.default_rng(seed)
+    X = torch.from_numpy(r.standard_normal((N, Cin, H, Wd)).astype(np.float32))
+    GY = torch.from_numpy((r.standard_normal((N, Cout, Ho, Wo)) / 4).astype(np.float32))
+    if dt == dp.DP_BF16:
+        X, GY = X.to(torch.bfloat16), GY.to(torch.bfloat16)
+    gW = torch.empty((N, Cout, Cin, kh, kw), device=DEV)
+    gb = torch.empty((N, Cout), device=DEV)
+    sq = torch.empty(N, device=DEV)
+    ws = torch.empty(max(dp.dp_grad_sample_conv2d_workspace_bytes(N, Cin, H, Wd, Cout, kh, kw, sh, sw, ph, pw), 1),
+                     dtype=torch.uint8, device=DEV)
+    dp.dp_grad_sample_conv2d(X.to(DEV), GY.to(DEV), dt, N, Cin, H, Wd, Cout, Ho, Wo, kh, kw, sh, sw, ph, pw, 1, 1, 1,
+                             scale, gW, gb, sq, None, ws)
+    Xr, Gr = X.float().numpy().astype(np.float64), GY.float().numpy().astype(np.float64)
+    rW, rb = oracle.conv2d_grad(Xr, Gr, (kh, kw), (sh, sw), (ph, pw), scale)
+    rsq = np.zeros(N)
+    oracle.sqnorm_accumulate(rW, rsq); oracle.sqnorm_accumulate(rb, rsq)
+    assert_g12(gW.cpu().numpy(), rW, 1e-4, "conv gW")
+    assert_g12(gb.cpu().numpy(), rb, 1e-4, "conv gb")
+    assert_rel(sq.cpu().numpy(), rsq, 1e-4, "conv sqnorm")
+
+
+@pytest.mark.parametrize("dt", [dp.DP_F32, dp.DP_BF16])
+def test_conv_rows_many_units(dt):
+    """The row-chunked kernel on more (sample, tile) workgroups than the CUs
+    hold at once (100 samples x 16 tiles of the CIFAR c6 shape), every
+    sample compared with the oracle."""
+    prev = dp.dp_conv2d_set_path(dp.DP_CONV_ROWS)
+    try:
+        shape = (100, 128, 8, 8, 256, 3, 3, 1, 1, 1, 1)
+        say("conv many units", dt, shape)
+        run_conv_case(shape, dt, 0.7, seed=91 + dt)
+    finally:
+        dp.dp_conv2d_set_path(prev)
+
+
 @pytest.mark.parametrize("shape", [CONV_SHAPES[1], CONV_SHAPES[2], CONV_SHAPES[3], CONV_SHAPES[5], CONV_SHAPES[-3],
                                    CONV_SHAPES[-2]])
 def test_conv_shapes_bf16(shape, conv_path):
