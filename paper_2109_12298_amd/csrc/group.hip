@@ -35,7 +35,8 @@ struct GroupDesc {
     int cblk0[kMaxGroup + 1];      // first column-reduce workgroup of each tensor
     int fblk0[kMaxGroup + 1];      // first finish workgroup of each tensor
     uint32_t pidx[kMaxGroup];
-    uint32_t flags[kMaxGroup];     // bit 0: column-reduce vectorized, bit 1: finish vectorized
+    uint32_t flags[kMaxGroup];     // bit 0: column-reduce vectorized, bit 1: finish vectorized,
+                                   // bit 2: the sum S is read in 16-byte pieces
     uint8_t R[kMaxGroup];          // 1: the tensor's sum is formed here from per-sample grads
 };
 
@@ -140,6 +141,9 @@ __global__ __launch_bounds__(kThreads) void finish_many_kernel(GroupDesc d, cons
             const float4 v = *reinterpret_cast<const float4 *>(part + (i64)k * st);
             s[0] += v.x; s[1] += v.y; s[2] += v.z; s[3] += v.w;
         }
+    } else if (cnt == 4 && (d.flags[p] & 4u)) {
+        const float4 v = reinterpret_cast<const float4 *>(d.S[p])[e0 / 4];
+        s[0] = v.x; s[1] = v.y; s[2] = v.z; s[3] = v.w;
     } else {
         for (int i = 0; i < cnt; ++i) s[i] = d.S[p][e0 + i];
     }
@@ -260,6 +264,9 @@ __global__ __launch_bounds__(kThreads) void norms_clip_noise_kernel(GroupDesc d,
         float s[4] = {0.f, 0.f, 0.f, 0.f};
         if (d.R[p]) {
             for (int i = 0; i < cnt; ++i) d.S[p][e0 + i] = 0.0f;   // N = 0: the clipped sum is zero
+        } else if (cnt == 4 && (d.flags[p] & 4u)) {
+            const float4 v = reinterpret_cast<const float4 *>(d.S[p])[q];
+            s[0] = v.x; s[1] = v.y; s[2] = v.z; s[3] = v.w;
         } else {
             for (int i = 0; i < cnt; ++i) s[i] = d.S[p][e0 + i];
         }
@@ -275,7 +282,16 @@ __global__ __launch_bounds__(kThreads) void norms_clip_noise_kernel(GroupDesc d,
             uint32_t w[4];
             normals4(q, d.pidx[p], (uint32_t)st, (uint32_t)(st >> 32), f.k0, f.k1, z, w);
         }
-        for (int i = 0; i < cnt; ++i) O[e0 + i] = (s[i] + sc * z[i]) / f.denom;
+        if (cnt == 4 && (d.flags[p] & 2u)) {
+            float4 o;
+            o.x = (s[0] + sc * z[0]) / f.denom;
+            o.y = (s[1] + sc * z[1]) / f.denom;
+            o.z = (s[2] + sc * z[2]) / f.denom;
+            o.w = (s[3] + sc * z[3]) / f.denom;
+            reinterpret_cast<float4 *>(O)[q] = o;
+        } else {
+            for (int i = 0; i < cnt; ++i) O[e0 + i] = (s[i] + sc * z[i]) / f.denom;
+        }
         return;
     }
 
@@ -437,6 +453,7 @@ size_t describe(const dp_param *params, int first, int count, i64 N, GroupDesc &
             if (to_ws) ws_floats += (size_t)d.splits * d.stride[i];
         }
         if ((q.numel & 3) == 0 && aligned(q.out, 16)) f |= 2u;
+        if ((q.numel & 3) == 0 && aligned(q.sum, 16)) f |= 4u;
         d.flags[i] = f;
         fb += (int)ceil_div(ceil_div(q.numel, 4), kThreads);
     }
