@@ -461,8 +461,9 @@ def main():
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py: this build runs the DP-SGD step on one GPU only; --gpus %d is not supported "
-              "(the step shards by samples, see the design notes)" % max(args.gpus, world), file=sys.stderr)
+        print("bench.py: the DP-SGD step runs on one GPU only; --gpus %d is not supported "
+              "(across GPUs the step would shard by samples, with one all-reduce of the clipped sums)"
+              % max(args.gpus, world), file=sys.stderr)
         sys.exit(2)
 
     import torch
