@@ -76,9 +76,11 @@ def call_costs(st, nnz=None):
             bf_mfma = bf and L.T > 1 and L.d_in % 8 == 0 and L.d_out % 8 == 0
             if lb.ghost:
                 # the two T x T Grams per sample; reads A and B, writes one norm
-                out["grad:" + L.name] = (N * L.T * (L.d_in + L.d_out) * e + N * 4,
-                                         2 * N * L.T * L.T * (L.d_in + L.d_out), "ghost_norm_kernel",
-                                         "bf16" if bf else "f32")
+                # (all ghost layers share one grouped call)
+                b0, f0, _, _ = out.get("grad:ghost", (0, 0, None, None))
+                out["grad:ghost"] = (b0 + N * L.T * (L.d_in + L.d_out) * e + N * 4,
+                                     f0 + 2 * N * L.T * L.T * (L.d_in + L.d_out), "ghost_gram_kernel",
+                                     "bf16" if bf else "f32")
             elif L.T == 1:
                 out["grad:" + L.name] = (N * (L.d_in + L.d_out) * e + grads + N * 4, N * L.d_out * L.d_in,
                                          "outer_kernel", None)
@@ -172,7 +174,7 @@ def src_hash(paths):
 
 KERNEL_SOURCES = {
     "outer_kernel": ["paper_2109_12298_amd/csrc/linear.hip", "paper_2109_12298_amd/csrc/linear_outer.hpp"],
-    "ghost_norm_kernel": ["paper_2109_12298_amd/csrc/ghost.hip"],
+    "ghost_gram_kernel": ["paper_2109_12298_amd/csrc/ghost.hip", "paper_2109_12298_amd/csrc/bf16_stage.hpp"],
     "gn_affine_kernel": ["paper_2109_12298_amd/csrc/groupnorm.hip"],
     "conv_rows_kernel": ["paper_2109_12298_amd/csrc/conv2d_rows.hip"],
     "conv_small_kernel": ["paper_2109_12298_amd/csrc/conv2d_small.hip",

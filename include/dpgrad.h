@@ -323,14 +323,48 @@ dp_status dp_per_sample_norms_active(const float *sqnorm, int32_t n_layers, int6
  * inputs (up to rounding).  Worth it when 2 T^2 < d_in * d_out.
  * A: [N][T][d_in] of `dt`; B: [N][T][d_out] of `dt`; sqnorm fp32 [N]
  * (overwritten, required when N > 0).  N >= 0, T >= 0 (T = 0 gives zeros),
- * d_in, d_out >= 1.  Workspace: dp_ghost_norm_linear_workspace_bytes(N, T,
- * d_in, d_out) bytes (the Gram tiles of the feature chunks, 16 KB per
- * sample, 64 x 64 tile pair and chunk; zero when N or T is 0). */
+ * d_in, d_out >= 1, T < 2^20, T * max(d_in, d_out) < 2^31
+ * (DP_EUNSUPPORTED beyond).  Workspace:
+ * dp_ghost_norm_linear_workspace_bytes(N, T, d_in, d_out) bytes (one float
+ * per sample and 64 x 64 tile pair of the Grams when T > 64, and, when the
+ * call has too few of those to fill the GPU, the partial Gram tiles of the
+ * feature chunks it then splits each pair into: 32 KB per sample, pair and
+ * chunk; zero when N or T is 0).  The same as dp_ghost_norm_linear_many
+ * with one layer. */
 size_t dp_ghost_norm_linear_workspace_bytes(int64_t N, int64_t T, int64_t d_in, int64_t d_out);
 dp_status dp_ghost_norm_linear(const void *A, const void *B, dp_dtype dt, int64_t N, int64_t T,
                                int64_t d_in, int64_t d_out, float scale, int32_t bias,
                                float *sqnorm, int32_t *status, void *ws, size_t ws_bytes,
                                hipStream_t stream);
+
+/* One layer of dp_ghost_norm_linear_many: the arguments of
+ * dp_ghost_norm_linear (A, B, T, d_in, d_out, scale, bias, sqnorm) with the
+ * same meaning and layouts.  The caller owns every buffer. */
+typedef struct dp_ghost_layer {
+    const void *A;
+    const void *B;
+    int64_t T, d_in, d_out;
+    float scale;
+    int32_t bias;
+    float *sqnorm;
+} dp_ghost_layer;
+
+/* The ghost norms of `count` Linear layers that share N and the dtype, as by
+ * one dp_ghost_norm_linear call per layer (same formula; equal up to
+ * rounding order, and bit for bit when both split the layer's features into
+ * the same number of chunks), in one launch over all the layers' (sample,
+ * tile pair) units, one more adding each layer's pairs when T > 64, and one
+ * adding the feature chunks when the units are too few to fill the GPU (up
+ * to 16 layers per launch; layers whose d_in or d_out is not a multiple of 16
+ * bytes' worth of elements, or whose A or B is not 16-byte aligned, take a
+ * launch of their own with element loads).  Arguments are checked as
+ * dp_ghost_norm_linear checks them; the first invalid layer's status is
+ * returned before anything is enqueued.  count in [0, 64].  Workspace:
+ * dp_ghost_norm_linear_many_workspace_bytes(items, count, N) bytes (the
+ * layers' pair values and chunk tiles, in item order). */
+size_t dp_ghost_norm_linear_many_workspace_bytes(const dp_ghost_layer *items, int32_t count, int64_t N);
+dp_status dp_ghost_norm_linear_many(const dp_ghost_layer *items, int32_t count, dp_dtype dt, int64_t N,
+                                    int32_t *status, void *ws, size_t ws_bytes, hipStream_t stream);
 
 /* sqnorm[n] = sum_e G[n][e]^2 for an already materialized per-sample gradient
  * G fp32 [N][numel] (overwritten). */

@@ -56,6 +56,8 @@ SIGNATURES = {
     "dp_per_sample_norms_active": (_ST, [_P, _I32, _I64, _P, _P, _P, _P]),
     "dp_ghost_norm_linear_workspace_bytes": (_SZ, [_I64, _I64, _I64, _I64]),
     "dp_ghost_norm_linear": (_ST, [_P, _P, _ST, _I64, _I64, _I64, _I64, _F, _I32, _P, _P, _P, _SZ, _P]),
+    "dp_ghost_norm_linear_many_workspace_bytes": (_SZ, [_P, _I32, _I64]),
+    "dp_ghost_norm_linear_many": (_ST, [_P, _I32, _ST, _I64, _P, _P, _SZ, _P]),
     "dp_sqnorm_from_grads": (_ST, [_P, _I64, _I64, _P, _P, _P]),
     "dp_clip_factors": (_ST, [_P, _I64, _F, _P, _P, _P]),
     "dp_clip_accumulate_workspace_bytes": (_SZ, [_I64, _I64]),
@@ -163,6 +165,26 @@ def make_layer_grads(entries):
                 arr[i].scale = float(v)
             else:
                 setattr(arr[i], k, int(v))
+    return arr
+
+
+class DPGhostLayer(ctypes.Structure):
+    """struct dp_ghost_layer of dpgrad.h."""
+    _fields_ = [("A", ctypes.c_void_p), ("B", ctypes.c_void_p), ("T", ctypes.c_int64), ("d_in", ctypes.c_int64),
+                ("d_out", ctypes.c_int64), ("scale", ctypes.c_float), ("bias", ctypes.c_int32),
+                ("sqnorm", ctypes.c_void_p)]
+
+
+def make_ghost_layers(entries):
+    """A dp_ghost_layer array from (A, B, T, d_in, d_out, scale, bias, sqnorm) tuples."""
+    arr = (DPGhostLayer * max(len(entries), 1))()
+    for i, (A, B, T, d_in, d_out, scale, bias, sqnorm) in enumerate(entries):
+        arr[i].A = _ptr(A)
+        arr[i].B = _ptr(B)
+        arr[i].T, arr[i].d_in, arr[i].d_out = int(T), int(d_in), int(d_out)
+        arr[i].scale = float(scale)
+        arr[i].bias = 1 if bias else 0
+        arr[i].sqnorm = _ptr(sqnorm)
     return arr
 
 
@@ -405,6 +427,16 @@ def dp_ghost_norm_linear(A, B, dt, N, T, d_in, d_out, scale, bias, sqnorm, statu
     _check(lib().dp_ghost_norm_linear(_ptr(A), _ptr(B), dt, N, T, d_in, d_out, scale, 1 if bias else 0,
                                       _ptr(sqnorm), _ptr(status), _ptr(ws), _nbytes(ws), _stream(stream)),
            "dp_ghost_norm_linear")
+
+
+def dp_ghost_norm_linear_many_workspace_bytes(items, count, N) -> int:
+    return lib().dp_ghost_norm_linear_many_workspace_bytes(ctypes.cast(items, ctypes.c_void_p), count, N)
+
+
+def dp_ghost_norm_linear_many(items, count, dt, N, status=None, ws=None, stream=None):
+    _check(lib().dp_ghost_norm_linear_many(ctypes.cast(items, ctypes.c_void_p), count, dt, N, _ptr(status),
+                                           _ptr(ws), _nbytes(ws), _stream(stream)),
+           "dp_ghost_norm_linear_many")
 
 
 def dp_grad_sample_many_grouped(items, k, dt, N) -> bool:

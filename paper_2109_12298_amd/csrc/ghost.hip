@@ -13,54 +13,80 @@
 // so sqnorm_n = s^2 * sum_{t,t'} G_B[t][t'] * (G_A[t][t'] + bias), with the
 // T x T Gram matrices G_A = A_n A_n^T and G_B = B_n B_n^T.  That costs
 // 2 T^2 (d_in + d_out) flops per sample against 2 T d_in d_out for the
-// gradient, and writes one float per sample instead of d_out * d_in.
+// gradient, and writes one float per sample instead of d_out * d_in.  The
+// flops per byte read are T / 2 (bf16), so at transformer shapes the call is
+// bound by reading A and B once.
 //
-// Kernels.  (1) `ghost_gram_kernel`: one workgroup per (sample, 64 x 64
-// tile pair (bi <= bj) of the Gram matrices, chunk of features of A or of
-// B); it writes that chunk's contribution to the tile of G_A or G_B.  Both
-// Grams contract over the feature index, which is the contiguous one in
-// memory, so each MFMA operand is eight (bf16) or one (fp32) consecutive
-// features of one position row: stages of 32 features of the tile's 2 x 64
-// rows are copied to LDS with 16-byte loads (double buffered, the next
-// stage's loads in flight during the current stage's MFMAs) and read back
-// with one ds_read per operand.  Wave w computes the 32 x 32 sub-tile
-// (w & 1, w >> 1); rows past T are staged as zeros.  The feature chunks
-// exist to give a small batch enough workgroups to fill the GPU.  (2)
-// `ghost_combine_kernel`: per (sample, tile pair), adds the chunks of G_A and
-// of G_B in chunk order (the tiles share one register layout, so this is
-// elementwise), forms sum G_B (G_A + bias), counts off-diagonal pairs twice
-// (the Grams are symmetric) and writes s^2 times that; the pairs of a sample
-// are then added in pair order.
-#include "common.hpp"
+// Work unit: (layer, sample, 64 x 64 tile pair (bi <= bj) of the Grams,
+// feature chunk).  A workgroup of four waves walks the features of A, then
+// those of B, in stages of 128 bytes per position row (64 bf16 or 32 fp32
+// features) of the tile's i-block rows and j-block rows (one block when bi =
+// bj): the stages are copied straight into LDS by 16-byte direct loads,
+// several stages in flight, each row's 16-byte chunks stored at chunk
+// position q ^ (row & 7) so that the operand reads (32 rows, one chunk each)
+// are free of bank conflicts.  Wave w computes the 32 x 32 sub-tile (w & 1,
+// w >> 1) of the pair.  Both Grams contract over the feature index, the
+// contiguous one in memory, so an MFMA operand is one 16-byte chunk of one
+// row: eight bf16 features for v_mfma_f32_32x32x16_bf16, or four fp32
+// features for four v_mfma_f32_32x32x2f32 (the order in which features are
+// contracted is immaterial as long as both operands share it).  Rows past T
+// and features past d read as zeros.
+//
+// With one chunk (a launch with enough units to fill the GPU: the usual case
+// once the layers of a step share the launch) the workgroup holds G_A's and
+// G_B's tiles in registers at the end, so it forms sum G_B (G_A + bias)
+// itself, counts an off-diagonal pair twice (the Grams are symmetric) and
+// writes s^2 times that: nothing is written but one float per (sample,
+// pair).  With several chunks (a small batch) each chunk writes its two
+// partial tiles and a second launch adds them in chunk order before forming
+// the product.  The pairs of a sample are then added in pair order.
+//
+// The units of a launch are all its layers' (a grouped call): a layer's
+// workgroups are numbered so that the pairs and chunks of one sample run on
+// one XCD at once (workgroups are dealt to the eight XCDs in turn), where
+// the pairs that share row blocks read them from that XCD's L2; layers with
+// more features per sample come first.
+#include "bf16_stage.hpp"
 
 namespace dpg {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kBT = 64;            // Gram tile edge (positions)
-constexpr int kKC = 32;            // features per stage
-constexpr int kRows = 2 * kBT;     // staged rows: the tile's i-block, then its j-block
+constexpr int kWaves = kThreads / kWave;
+constexpr int kBT = 64;                               // Gram tile edge (positions)
+constexpr int kRowBytes = 128;                        // bytes of one position row per stage
+constexpr int kStageBytes = 2 * kBT * kRowBytes;      // the i-block's rows, then the j-block's
+#ifndef DPG_GHOST_STAGES
+#define DPG_GHOST_STAGES 4
+#endif
+constexpr int kStages = DPG_GHOST_STAGES;             // stages in the LDS ring (64 KB at 4)
+constexpr int kGroupMax = 16;                         // layers per launch table
+constexpr int kFill = 512;                            // workgroups that give every CU two
+constexpr int kTile = kBT * kBT;                      // floats of one partial Gram tile
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
-template <typename T>
-struct Elem;
+// the source of every 16-byte chunk that lies past T or past d (never written)
+__device__ __attribute__((aligned(64))) uint32_t g_ghost_zero[16];
 
-template <>
-struct Elem<uint16_t> {
-    static constexpr int ROW = 80;            // 64 bytes of features + 16 of padding (spreads the banks)
+// One layer of a launch.  out[n * pairs + p] receives the value of (sample n,
+// pair p): part when pairs > 1 (then added into sqnorm by the pair sum),
+// else sqnorm itself.
+struct GhostLayer {
+    const void *A, *B;
+    float *out, *tiles, *part, *sqnorm;
+    i64 T, din, dout;
+    int nb, pairs, chunks, sa, sb;   // row blocks, tile pairs, feature chunks, stages over d_in and d_out
+    int blk0, cblk0;                 // first workgroup of the layer in the Gram and the combine launches
+    float bias, s2;
 };
 
-template <>
-struct Elem<float> {
-    static constexpr int ROW = 144;           // 128 + 16
+struct GhostGroup {
+    i64 N;
+    int count;
+    GhostLayer L[kGroupMax];
 };
-
-template <typename T>
-constexpr int kChunks = (kRows * kKC * (int)sizeof(T)) / 16 / kThreads;   // 16-byte chunks per thread per stage
-
-constexpr int kPerChunk(int elem_bytes) { return 16 / elem_bytes; }
 
 // (bi, bj), bi <= bj, of pair p in row-major order of the upper triangle
 __device__ __forceinline__ void pair_of(int p, int nb, int &bi, int &bj)
@@ -73,152 +99,237 @@ __device__ __forceinline__ void pair_of(int p, int nb, int &bi, int &bj)
     bj = bi + p;
 }
 
-// One stage's loads for this thread: chunk q = tid + kThreads * c covers
-// staged row q / CPR, features (q % CPR) * PC .. + PC - 1 of rows of length
-// ld; features at or past fend read as zeros.
-template <typename T, bool VEC>
-struct StageRegs {
-    uint4 v[kChunks<T>];
-};
-
-template <typename T, bool VEC>
-__device__ __forceinline__ void load_stage(const T *X, i64 Tn, i64 ld, i64 fend, int bi, int bj, i64 f0, int tid,
-                                           StageRegs<T, VEC> &r)
+// the layer of workgroup b: the last whose first workgroup is at or before b
+__device__ __forceinline__ int layer_of(const GhostGroup &g, int b, bool combine)
 {
-    constexpr int PC = kPerChunk(sizeof(T));
-    constexpr int CPR = kKC / PC;
+    int k = 0;
+    while (k + 1 < g.count && (combine ? g.L[k + 1].cblk0 : g.L[k + 1].blk0) <= b) ++k;
+    return k;
+}
+
+// s_waitcnt vmcnt(later * LOADS) for a run-time later in [0, MAXL]
+template <int LOADS, int MAXL>
+__device__ __forceinline__ void wait_later(int later)
+{
+    if constexpr (MAXL == 0) {
+        bf16s::wait_vmcnt<0>();
+    } else {
+        if (later >= MAXL) bf16s::wait_vmcnt<MAXL * LOADS>();
+        else wait_later<LOADS, MAXL - 1>(later);
+    }
+}
+
+__device__ __forceinline__ uint32_t elem_bits(uint16_t v) { return v; }
+__device__ __forceinline__ uint32_t elem_bits(float v) { return __float_as_uint(v); }
+
+__device__ __forceinline__ void mma_chunk(const uint4 &a, const uint4 &b, f32x16_t &acc, uint16_t)
+{
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b),
+                                                  acc, 0, 0, 0);
+}
+
+__device__ __forceinline__ void mma_chunk(const uint4 &a, const uint4 &b, f32x16_t &acc, float)
+{
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.x), __uint_as_float(b.x), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.y), __uint_as_float(b.y), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.z), __uint_as_float(b.z), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.w), __uint_as_float(b.w), acc, 0, 0, 0);
+}
+
+// One work unit: sample n, pair p = (bi, bj), chunk c of layer L.  VEC:
+// every row is 16-byte aligned and d_in, d_out are whole chunks, so the
+// stages are direct loads; otherwise each thread loads its chunks element by
+// element (bounds-checked) and stores them to LDS itself.
+template <typename T, bool VEC, bool DIAG>
+__device__ __forceinline__ void gram_unit(const GhostLayer &L, i64 n, int p, int bi, int bj, int c, char *smem,
+                                          float *red)
+{
+    constexpr int EPC = 16 / (int)sizeof(T);                 // elements per 16-byte chunk
+    constexpr int F = kRowBytes / (int)sizeof(T);            // features per stage
+    constexpr int ROWS = DIAG ? kBT : 2 * kBT;               // staged rows
+    constexpr int LOADS = ROWS * kRowBytes / 1024 / kWaves;  // 16-byte loads per lane per stage
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const i64 Tn = L.T, din = L.din, dout = L.dout;
+    const int C = L.chunks;
+    const int a0 = (int)((i64)c * L.sa / C), a1 = (int)((i64)(c + 1) * L.sa / C);
+    const int b0 = (int)((i64)c * L.sb / C), b1 = (int)((i64)(c + 1) * L.sb / C);
+    const int na = a1 - a0, nst = na + (b1 - b0);
+    const T *An = reinterpret_cast<const T *>(L.A) + n * Tn * din;
+    const T *Bn = reinterpret_cast<const T *>(L.B) + n * Tn * dout;
+
+    // this lane's share of a stage: load r covers LDS bytes 1024 a + 16 lane,
+    // a = wave + 4 r, i.e. staged row 8 a + lane / 8, chunk position lane % 8
+    int offA[LOADS], offB[LOADS], fq[LOADS];
+    bool rok[LOADS];
 #pragma unroll
-    for (int c = 0; c < kChunks<T>; ++c) {
-        const int q = tid + kThreads * c;
-        const int row = q / CPR, cc = q % CPR;
+    for (int r = 0; r < LOADS; ++r) {
+        const int a = wave + kWaves * r;
+        const int row = 8 * a + (lane >> 3);
+        const int q = (lane & 7) ^ (row & 7);
         const i64 t = row < kBT ? (i64)bi * kBT + row : (i64)bj * kBT + (row - kBT);
-        const i64 f = f0 + (i64)cc * PC;
-        if (VEC) {
-            uint4 z = make_uint4(0u, 0u, 0u, 0u);
-            if (t < Tn && f < fend) z = *reinterpret_cast<const uint4 *>(X + t * ld + f);
-            r.v[c] = z;
-        } else {
-            T e[PC];
+        rok[r] = t < Tn;
+        fq[r] = q * EPC;
+        offA[r] = (int)(t * din) + fq[r];
+        offB[r] = (int)(t * dout) + fq[r];
+    }
+    const uint32_t lds0 = bf16s::lds_addr(smem);
+    auto issue = [&](int k, int slot) {
+        const bool onA = k < na;
+        const int f0 = (onA ? a0 + k : b0 + (k - na)) * F;
+        const i64 d = onA ? din : dout;
+        const T *X = onA ? An : Bn;
 #pragma unroll
-            for (int k = 0; k < PC; ++k) e[k] = (t < Tn && f + k < fend) ? X[t * ld + f + k] : T(0);
-            r.v[c] = *reinterpret_cast<const uint4 *>(e);
+        for (int r = 0; r < LOADS; ++r) {
+            const int a = wave + kWaves * r;
+            const int f = f0 + fq[r];
+            const int off = (onA ? offA[r] : offB[r]) + f0;
+            if constexpr (VEC) {
+                const void *src = (rok[r] && f < d) ? (const void *)(X + off) : (const void *)g_ghost_zero;
+                bf16s::dma16(src, lds0 + (uint32_t)(slot * kStageBytes + a * 1024));
+            } else {
+                uint32_t wd[4];
+#pragma unroll
+                for (int x = 0; x < 4; ++x) wd[x] = 0u;
+#pragma unroll
+                for (int x = 0; x < EPC; ++x) {
+                    const uint32_t v = (rok[r] && f + x < d) ? elem_bits(X[off + x]) : 0u;
+                    wd[x * (int)sizeof(T) / 4] |= v << (8 * ((x * (int)sizeof(T)) & 3));
+                }
+                *reinterpret_cast<uint4 *>(smem + slot * kStageBytes + a * 1024 + 16 * lane) =
+                    make_uint4(wd[0], wd[1], wd[2], wd[3]);
+            }
+        }
+    };
+
+    // operand rows: ra on the i side, rb on the j side; chunk 2 g + lane / 32
+    // of each for the four MFMA steps of a stage
+    const int ra = 32 * (wave & 1) + (lane & 31);
+    const int rb = (DIAG ? 0 : kBT) + 32 * (wave >> 1) + (lane & 31);
+    const int h = lane >> 5;
+    int oa[4], ob[4];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+        oa[g] = ra * kRowBytes + 16 * ((2 * g + h) ^ (ra & 7));
+        ob[g] = rb * kRowBytes + 16 * ((2 * g + h) ^ (rb & 7));
+    }
+
+    f32x16_t acc, accA;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[r] = accA[r] = 0.0f;
+
+#pragma unroll
+    for (int k = 0; k < kStages - 1; ++k)
+        if (k < nst) issue(k, k);
+    int slot = 0;
+    for (int k = 0; k < nst; ++k) {
+        if constexpr (VEC) {
+            const int later = nst - 1 - k < kStages - 2 ? nst - 1 - k : kStages - 2;
+            wait_later<LOADS, kStages - 2>(later);       // stage k has landed (this wave's loads)
+        }
+        bf16s::wait_lgkmcnt0();                          // this wave's reads of stage k - 1 are done
+        bf16s::stage_barrier();
+        if (k + kStages - 1 < nst) issue(k + kStages - 1, slot == 0 ? kStages - 1 : slot - 1);
+        if (k == na) {                                   // the B side starts: keep G_A's tile
+            accA = acc;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
+        }
+        const char *Ls = smem + slot * kStageBytes;
+        uint4 av[4], bv[4];
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            av[g] = *reinterpret_cast<const uint4 *>(Ls + oa[g]);
+            bv[g] = *reinterpret_cast<const uint4 *>(Ls + ob[g]);
+        }
+#pragma unroll
+        for (int g = 0; g < 4; ++g) mma_chunk(av[g], bv[g], acc, T());
+        slot = slot + 1 == kStages ? 0 : slot + 1;
+    }
+    if (na == nst) {                                     // no B stages in this chunk
+        accA = acc;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
+    }
+
+    if (C == 1) {
+        float s = 0.0f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s += acc[r] * (accA[r] + L.bias);
+        s = wave_sum(s);
+        if (lane == 0) red[wave] = s;
+        __syncthreads();
+        if (tid == 0) {
+            float t = 0.0f;
+#pragma unroll
+            for (int w = 0; w < kWaves; ++w) t += red[w];
+            L.out[n * L.pairs + p] = L.s2 * (DIAG ? t : 2.0f * t);
+        }
+    } else {
+        // the two partial tiles in register order: wave, lane, register
+        float *tA = L.tiles + ((size_t)((n * L.pairs + p) * C + c) * 2) * kTile + wave * 1024 + lane * 16;
+        float4 *oA = reinterpret_cast<float4 *>(tA);
+        float4 *oB = reinterpret_cast<float4 *>(tA + kTile);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            oA[q] = make_float4(accA[4 * q], accA[4 * q + 1], accA[4 * q + 2], accA[4 * q + 3]);
+            oB[q] = make_float4(acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]);
         }
     }
 }
 
+// Workgroup b of layer k (local index l = b - blk0): XCD x = l % 8 takes,
+// in turn, the pairs * chunks workgroups of samples x, x + 8, ...
 template <typename T, bool VEC>
-__device__ __forceinline__ void store_stage(char *L, int tid, const StageRegs<T, VEC> &r)
+__global__ __launch_bounds__(kThreads, 2) void ghost_gram_kernel(const GhostGroup g)
 {
-    constexpr int CPR = kKC / kPerChunk(sizeof(T));
-#pragma unroll
-    for (int c = 0; c < kChunks<T>; ++c) {
-        const int q = tid + kThreads * c;
-        const int row = q / CPR, cc = q % CPR;
-        *reinterpret_cast<uint4 *>(L + row * Elem<T>::ROW + cc * 16) = r.v[c];
-    }
-}
-
-// The stage's MFMAs for the wave's sub-tile: rows ra (i side) and rb (j side)
-// of the staged tile are this lane's operand rows.
-__device__ __forceinline__ void mma_stage(const char *L, int ra, int rb, int lane, f32x16_t &acc, uint16_t)
-{
-    constexpr int ROW = Elem<uint16_t>::ROW;
-#pragma unroll
-    for (int ks = 0; ks < kKC / 16; ++ks) {
-        const int off = ks * 32 + 16 * (lane >> 5);
-        const bf16x8_t a = *reinterpret_cast<const bf16x8_t *>(L + ra * ROW + off);
-        const bf16x8_t b = *reinterpret_cast<const bf16x8_t *>(L + rb * ROW + off);
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc, 0, 0, 0);
-    }
-}
-
-__device__ __forceinline__ void mma_stage(const char *L, int ra, int rb, int lane, f32x16_t &acc, float)
-{
-    constexpr int ROW = Elem<float>::ROW;
-#pragma unroll
-    for (int ks = 0; ks < kKC / 2; ++ks) {
-        const int off = 4 * (2 * ks + (lane >> 5));
-        const float a = *reinterpret_cast<const float *>(L + ra * ROW + off);
-        const float b = *reinterpret_cast<const float *>(L + rb * ROW + off);
-        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, acc, 0, 0, 0);
-    }
-}
-
-template <typename T, bool VEC>
-__global__ __launch_bounds__(kThreads) void ghost_gram_kernel(const T *__restrict__ A, const T *__restrict__ B,
-                                                              i64 Tn, i64 din, i64 dout, int nb, int pairs, int kch,
-                                                              int ca, int chunks, float *__restrict__ tiles)
-{
-    __shared__ __attribute__((aligned(16))) char lds[2][kRows * Elem<T>::ROW];
-    const int c = (int)(blockIdx.x % chunks);
-    const i64 np = blockIdx.x / chunks;
-    const i64 n = np / pairs;
-    const int p = (int)(np % pairs);
+    __shared__ __attribute__((aligned(1024))) char smem[kStages * kStageBytes];
+    __shared__ float red[kWaves];
+    const int b = (int)blockIdx.x;
+    const GhostLayer &L = g.L[layer_of(g, b, false)];
+    const int l = b - L.blk0;
+    const int m = L.pairs * L.chunks;
+    const int kk = l >> 3;
+    const i64 n = 8 * (i64)(kk / m) + (l & 7);
+    if (n >= g.N) return;
+    const int j = kk % m;
+    const int p = j / L.chunks, c = j % L.chunks;
     int bi, bj;
-    pair_of(p, nb, bi, bj);
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int ra = 32 * (wave & 1) + (lane & 31);          // i-side row of the lane's operand
-    const int rb = kBT + 32 * (wave >> 1) + (lane & 31);   // j-side row
-    const bool onA = c < ca;
-    const i64 d = onA ? din : dout;
-    const T *X = onA ? A + n * Tn * din : B + n * Tn * dout;
-    const i64 f_begin = (i64)(onA ? c : c - ca) * kch;
-    const i64 f_end = f_begin + kch < d ? f_begin + kch : d;
-    const int stages = (int)ceil_div(f_end - f_begin, kKC);
-
-    f32x16_t acc;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
-
-    StageRegs<T, VEC> regs;
-    load_stage<T, VEC>(X, Tn, d, f_end, bi, bj, f_begin, tid, regs);
-    store_stage<T, VEC>(lds[0], tid, regs);
-    __syncthreads();
-    for (int st = 0; st < stages; ++st) {
-        const bool more = st + 1 < stages;
-        if (more) load_stage<T, VEC>(X, Tn, d, f_end, bi, bj, f_begin + (i64)(st + 1) * kKC, tid, regs);
-        mma_stage(lds[st & 1], ra, rb, lane, acc, T());
-        if (more) store_stage<T, VEC>(lds[(st + 1) & 1], tid, regs);
-        __syncthreads();
-    }
-    // the tile in register order: wave, lane, register
-    float4 *o = reinterpret_cast<float4 *>(tiles + (size_t)blockIdx.x * (kBT * kBT) + wave * 1024 + lane * 16);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) o[q] = make_float4(acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]);
+    pair_of(p, L.nb, bi, bj);
+    if (bi == bj) gram_unit<T, VEC, true>(L, n, p, bi, bj, c, smem, red);
+    else gram_unit<T, VEC, false>(L, n, p, bi, bj, c, smem, red);
 }
 
-// one workgroup per (sample, pair); thread i owns entries 16 i .. 16 i + 15
-__global__ __launch_bounds__(kThreads) void ghost_combine_kernel(const float *__restrict__ tiles, int nb, int pairs,
-                                                                 int ca, int chunks, float bias, float s2,
-                                                                 float *__restrict__ out)
+// Several chunks: one workgroup per (layer, sample, pair); thread i owns
+// entries 16 i .. 16 i + 15 of the two tiles, adds the chunks in chunk order
+// and forms the pair's value as the one-chunk path does.
+__global__ __launch_bounds__(kThreads) void ghost_combine_kernel(const GhostGroup g)
 {
-    __shared__ float red[kThreads / kWave];
-    const int p = (int)(blockIdx.x % pairs);
+    __shared__ float red[kWaves];
+    const int b = (int)blockIdx.x;
+    const GhostLayer &L = g.L[layer_of(g, b, true)];
+    const int u = b - L.cblk0;
+    const i64 n = u / L.pairs;
+    const int p = u % L.pairs;
     int bi, bj;
-    pair_of(p, nb, bi, bj);
-    const float *base = tiles + (size_t)blockIdx.x * chunks * (kBT * kBT) + threadIdx.x * 16;
+    pair_of(p, L.nb, bi, bj);
+    const float *base = L.tiles + (size_t)(n * L.pairs + p) * L.chunks * 2 * kTile + threadIdx.x * 16;
     float ga[16], gb[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) ga[r] = gb[r] = 0.0f;
-    for (int c = 0; c < chunks; ++c) {
-        const float4 *t = reinterpret_cast<const float4 *>(base + (size_t)c * (kBT * kBT));
-        float v[16];
+    for (int c = 0; c < L.chunks; ++c) {
+        const float4 *ta = reinterpret_cast<const float4 *>(base + (size_t)(2 * c) * kTile);
+        const float4 *tb = reinterpret_cast<const float4 *>(base + (size_t)(2 * c + 1) * kTile);
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-            const float4 x = t[q];
-            v[4 * q] = x.x; v[4 * q + 1] = x.y; v[4 * q + 2] = x.z; v[4 * q + 3] = x.w;
-        }
-        if (c < ca) {
-#pragma unroll
-            for (int r = 0; r < 16; ++r) ga[r] += v[r];
-        } else {
-#pragma unroll
-            for (int r = 0; r < 16; ++r) gb[r] += v[r];
+            const float4 x = ta[q], y = tb[q];
+            ga[4 * q] += x.x; ga[4 * q + 1] += x.y; ga[4 * q + 2] += x.z; ga[4 * q + 3] += x.w;
+            gb[4 * q] += y.x; gb[4 * q + 1] += y.y; gb[4 * q + 2] += y.z; gb[4 * q + 3] += y.w;
         }
     }
     float s = 0.0f;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) s += gb[r] * (ga[r] + bias);
+    for (int r = 0; r < 16; ++r) s += gb[r] * (ga[r] + L.bias);
     s = wave_sum(s);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     if (lane == 0) red[wave] = s;
@@ -226,50 +337,84 @@ __global__ __launch_bounds__(kThreads) void ghost_combine_kernel(const float *__
     if (threadIdx.x == 0) {
         float t = 0.0f;
 #pragma unroll
-        for (int w = 0; w < kThreads / kWave; ++w) t += red[w];
-        out[blockIdx.x] = s2 * (bi == bj ? t : 2.0f * t);
+        for (int w = 0; w < kWaves; ++w) t += red[w];
+        L.out[n * L.pairs + p] = L.s2 * (bi == bj ? t : 2.0f * t);
     }
 }
 
-int tile_pairs(i64 T)
+// sqnorm[n] of every layer with several pairs: one wave per (layer, sample)
+// adds its pairs' values (lane l takes pairs l, l + 64, ..., then a butterfly)
+__global__ __launch_bounds__(256) void ghost_pair_sum_kernel(const GhostGroup g)
 {
-    const i64 nb = ceil_div(T, kBT);
-    return (int)(nb * (nb + 1) / 2);
+    const GhostLayer &L = g.L[blockIdx.y];
+    const i64 n = (i64)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    if (L.pairs == 1 || n >= g.N) return;
+    const float *q = L.part + n * L.pairs;
+    float s = 0.0f;
+    for (int t = lane; t < L.pairs; t += kWave) s += q[t];
+    s = wave_sum(s);
+    if (lane == 0) L.sqnorm[n] = s;
 }
 
-// feature chunk per workgroup: enough (sample, pair, chunk) workgroups to
-// give every CU a few, in whole stages
-struct GhostPlan {
-    int nb, pairs, kch, ca, cb, chunks;
+// ---------------------------------------------------------------------------
+// host side
+// ---------------------------------------------------------------------------
+struct Plan {
+    int nb, pairs, chunks;
 };
 
-GhostPlan ghost_plan(i64 N, i64 Tn, i64 din, i64 dout)
+// chunks per unit for a launch of `units` (sample, pair) units: one when
+// they fill the GPU, else enough to give every CU two workgroups, with at
+// least 256 features per chunk on average
+Plan layer_plan(i64 T, i64 din, i64 dout, i64 units)
 {
-    GhostPlan g;
-    g.nb = (int)ceil_div(Tn, kBT);
-    g.pairs = tile_pairs(Tn);
-    const i64 want = ceil_div(1024, N * g.pairs > 0 ? N * g.pairs : 1);       // chunks per (sample, pair)
-    i64 kch = ceil_div(din + dout, want);
-    kch = ceil_div(kch, kKC) * kKC;
-    if (kch < 256) kch = 256;
-    g.kch = (int)kch;
-    g.ca = (int)ceil_div(din, kch);
-    g.cb = (int)ceil_div(dout, kch);
-    g.chunks = g.ca + g.cb;
-    return g;
+    Plan pl;
+    pl.nb = (int)ceil_div(T, kBT);
+    pl.pairs = pl.nb * (pl.nb + 1) / 2;
+    i64 c = units >= kFill ? 1 : ceil_div(kFill, units > 0 ? units : 1);
+    const i64 cap = ceil_div(din + dout, 256);
+    pl.chunks = (int)(c < cap ? c : cap);
+    return pl;
 }
 
-template <typename T>
-void launch_ghost(const void *A, const void *B, i64 N, i64 Tn, i64 din, i64 dout, bool vec, const GhostPlan &g,
-                  float *tiles, hipStream_t stream)
+i64 launch_units(const dp_ghost_layer *items, int count, i64 N)
 {
-    const dim3 grid((unsigned)(N * g.pairs * g.chunks));
-    if (vec)
-        ghost_gram_kernel<T, true><<<grid, kThreads, 0, stream>>>((const T *)A, (const T *)B, Tn, din, dout, g.nb,
-                                                                  g.pairs, g.kch, g.ca, g.chunks, tiles);
-    else
-        ghost_gram_kernel<T, false><<<grid, kThreads, 0, stream>>>((const T *)A, (const T *)B, Tn, din, dout, g.nb,
-                                                                   g.pairs, g.kch, g.ca, g.chunks, tiles);
+    i64 u = 0;
+    for (int i = 0; i < count; ++i)
+        if (items[i].T > 0) {
+            const i64 nb = ceil_div(items[i].T, kBT);
+            u += N * (nb * (nb + 1) / 2);
+        }
+    return u;
+}
+
+size_t round256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+// workspace of one layer: the pair values (several pairs), then the chunks'
+// partial tiles (several chunks)
+size_t layer_ws(const Plan &pl, i64 N)
+{
+    size_t b = 0;
+    if (pl.pairs > 1) b += round256((size_t)(N * pl.pairs) * sizeof(float));
+    if (pl.chunks > 1) b += (size_t)(N * pl.pairs) * pl.chunks * 2 * kTile * sizeof(float);
+    return b;
+}
+
+dp_status check_item(const dp_ghost_layer &it, i64 N)
+{
+    DPG_REQUIRE(it.T >= 0 && it.d_in >= 1 && it.d_out >= 1, DP_EINVAL);
+    DPG_REQUIRE(it.T < (i64(1) << 20) && it.d_in < (i64(1) << 31) && it.d_out < (i64(1) << 31), DP_EINVAL);
+    DPG_REQUIRE(N == 0 || it.sqnorm != nullptr, DP_EINVAL);
+    DPG_REQUIRE(N * it.T == 0 || (it.A != nullptr && it.B != nullptr), DP_EINVAL);
+    DPG_REQUIRE(it.T * (it.d_in > it.d_out ? it.d_in : it.d_out) < (i64(1) << 31), DP_EUNSUPPORTED);
+    return DP_OK;
+}
+
+template <typename T, bool VEC>
+void launch_gram(const GhostGroup &g, int blocks, hipStream_t stream)
+{
+    ghost_gram_kernel<T, VEC><<<(unsigned)blocks, kThreads, 0, stream>>>(g);
 }
 
 }  // namespace
@@ -277,48 +422,189 @@ void launch_ghost(const void *A, const void *B, i64 N, i64 Tn, i64 din, i64 dout
 
 using namespace dpg;
 
+extern "C" size_t dp_ghost_norm_linear_many_workspace_bytes(const dp_ghost_layer *items, int32_t count, int64_t N)
+{
+    if (items == nullptr || count <= 0 || N <= 0) return 0;
+    const i64 units = launch_units(items, count, N);
+    size_t b = 0;
+    for (int i = 0; i < count; ++i) {
+        const dp_ghost_layer &it = items[i];
+        if (it.T <= 0 || it.d_in <= 0 || it.d_out <= 0) continue;
+        b += layer_ws(layer_plan(it.T, it.d_in, it.d_out, units), N);
+    }
+    return b;
+}
+
+extern "C" dp_status dp_ghost_norm_linear_many(const dp_ghost_layer *items, int32_t count, dp_dtype dt, int64_t N,
+                                               int32_t *status, void *ws, size_t ws_bytes, hipStream_t stream)
+{
+    (void)status;
+    DPG_REQUIRE(dtype_ok(dt), DP_EDTYPE);
+    DPG_REQUIRE(count >= 0 && count <= 64 && (count == 0 || items != nullptr), DP_EINVAL);
+    DPG_REQUIRE(N >= 0 && N < (i64(1) << 31), DP_EINVAL);
+    for (int i = 0; i < count; ++i) {
+        const dp_status st = check_item(items[i], N);
+        if (st != DP_OK) return st;
+    }
+    const size_t need = dp_ghost_norm_linear_many_workspace_bytes(items, count, N);
+    DPG_REQUIRE(ws_bytes >= need && (need == 0 || ws != nullptr), DP_EINVAL);
+    if (N == 0 || count == 0) return DP_OK;
+
+    const i64 units = launch_units(items, count, N);
+    const i64 pc = 16 / (i64)dtype_bytes(dt);
+    const i64 F = kRowBytes / (i64)dtype_bytes(dt);
+    GhostLayer lay[64];
+    bool vec[64];
+    int order[64], live = 0;
+    char *w = (char *)ws;
+    for (int i = 0; i < count; ++i) {
+        const dp_ghost_layer &it = items[i];
+        if (it.T == 0) {                         // an empty sum over positions: zero norms
+            zero_fill(it.sqnorm, N, stream);
+            continue;
+        }
+        const Plan pl = layer_plan(it.T, it.d_in, it.d_out, units);
+        GhostLayer &L = lay[i];
+        L.A = it.A;
+        L.B = it.B;
+        L.T = it.T;
+        L.din = it.d_in;
+        L.dout = it.d_out;
+        L.nb = pl.nb;
+        L.pairs = pl.pairs;
+        L.chunks = pl.chunks;
+        L.sa = (int)ceil_div(it.d_in, F);
+        L.sb = (int)ceil_div(it.d_out, F);
+        L.bias = it.bias ? 1.0f : 0.0f;
+        L.s2 = it.scale * it.scale;
+        L.sqnorm = it.sqnorm;
+        L.part = nullptr;
+        L.tiles = nullptr;
+        if (pl.pairs > 1) {
+            L.part = (float *)w;
+            w += round256((size_t)(N * pl.pairs) * sizeof(float));
+        }
+        if (pl.chunks > 1) {
+            L.tiles = (float *)w;
+            w += (size_t)(N * pl.pairs) * pl.chunks * 2 * kTile * sizeof(float);
+        }
+        L.out = pl.pairs > 1 ? L.part : it.sqnorm;
+        vec[i] = it.d_in % pc == 0 && it.d_out % pc == 0 && aligned(it.A, 16) && aligned(it.B, 16);
+        order[live++] = i;
+    }
+    // more features per sample first (the longest units start first)
+    for (int a = 1; a < live; ++a)
+        for (int b = a; b > 0 && lay[order[b]].din + lay[order[b]].dout > lay[order[b - 1]].din +
+                                                                           lay[order[b - 1]].dout; --b) {
+            const int t = order[b];
+            order[b] = order[b - 1];
+            order[b - 1] = t;
+        }
+
+    // the Gram launches: the 16-byte class, then the element class, up to
+    // kGroupMax layers per launch
+    for (int cls = 0; cls < 2; ++cls) {
+        const bool want_vec = cls == 0;
+        GhostGroup g;
+        g.N = N;
+        g.count = 0;
+        i64 blocks = 0;
+        auto flush = [&]() -> dp_status {
+            if (g.count == 0) return DP_OK;
+            DPG_REQUIRE(blocks < (i64(1) << 31), DP_EUNSUPPORTED);
+            if (dt == DP_BF16) {
+                if (want_vec) launch_gram<uint16_t, true>(g, (int)blocks, stream);
+                else launch_gram<uint16_t, false>(g, (int)blocks, stream);
+            } else {
+                if (want_vec) launch_gram<float, true>(g, (int)blocks, stream);
+                else launch_gram<float, false>(g, (int)blocks, stream);
+            }
+            g.count = 0;
+            blocks = 0;
+            return DP_OK;
+        };
+        for (int a = 0; a < live; ++a) {
+            const int i = order[a];
+            if (vec[i] != want_vec) continue;
+            GhostLayer &L = lay[i];
+            L.blk0 = (int)blocks;
+            blocks += 8 * (i64)(L.pairs * L.chunks) * ceil_div(N, 8);
+            DPG_REQUIRE(blocks < (i64(1) << 31), DP_EUNSUPPORTED);
+            g.L[g.count++] = L;
+            if (g.count == kGroupMax) {
+                const dp_status st = flush();
+                if (st != DP_OK) return st;
+            }
+        }
+        const dp_status st = flush();
+        if (st != DP_OK) return st;
+    }
+    // several chunks: add them and form the pair values
+    {
+        GhostGroup g;
+        g.N = N;
+        g.count = 0;
+        i64 blocks = 0;
+        for (int a = 0; a <= live; ++a) {
+            if (a < live) {
+                GhostLayer &L = lay[order[a]];
+                if (L.chunks == 1) continue;
+                L.cblk0 = (int)blocks;
+                blocks += N * L.pairs;
+                g.L[g.count++] = L;
+            }
+            if (g.count > 0 && (g.count == kGroupMax || a == live)) {
+                ghost_combine_kernel<<<(unsigned)blocks, kThreads, 0, stream>>>(g);
+                g.count = 0;
+                blocks = 0;
+            }
+        }
+    }
+    // several pairs: add them into sqnorm
+    {
+        GhostGroup g;
+        g.N = N;
+        g.count = 0;
+        for (int a = 0; a <= live; ++a) {
+            if (a < live) {
+                const GhostLayer &L = lay[order[a]];
+                if (L.pairs == 1) continue;
+                g.L[g.count++] = L;
+            }
+            if (g.count > 0 && (g.count == kGroupMax || a == live)) {
+                const dim3 grid((unsigned)ceil_div(N, 4), (unsigned)g.count);
+                ghost_pair_sum_kernel<<<grid, 256, 0, stream>>>(g);
+                g.count = 0;
+            }
+        }
+    }
+    return launch_status();
+}
+
 extern "C" size_t dp_ghost_norm_linear_workspace_bytes(int64_t N, int64_t T, int64_t d_in, int64_t d_out)
 {
     if (N <= 0 || T <= 0 || d_in <= 0 || d_out <= 0) return 0;
-    const GhostPlan g = ghost_plan(N, T, d_in, d_out);
-    // the chunks' Gram tiles, then (several pairs) one partial per (sample, pair)
-    size_t b = (size_t)(N * g.pairs * g.chunks) * (kBT * kBT) * sizeof(float);
-    if (g.pairs > 1) b += (size_t)(N * g.pairs) * sizeof(float);
-    return b;
+    dp_ghost_layer it{};
+    it.T = T;
+    it.d_in = d_in;
+    it.d_out = d_out;
+    return dp_ghost_norm_linear_many_workspace_bytes(&it, 1, N);
 }
 
 extern "C" dp_status dp_ghost_norm_linear(const void *A, const void *B, dp_dtype dt, int64_t N, int64_t T,
                                           int64_t d_in, int64_t d_out, float scale, int32_t bias, float *sqnorm,
                                           int32_t *status, void *ws, size_t ws_bytes, hipStream_t stream)
 {
-    (void)status;
     DPG_REQUIRE(dtype_ok(dt), DP_EDTYPE);
-    DPG_REQUIRE(N >= 0 && T >= 0 && d_in >= 1 && d_out >= 1, DP_EINVAL);
-    DPG_REQUIRE(N < (i64(1) << 31) && T < (i64(1) << 20) && d_in < (i64(1) << 31) && d_out < (i64(1) << 31),
-                DP_EINVAL);
-    DPG_REQUIRE(N == 0 || sqnorm != nullptr, DP_EINVAL);
-    DPG_REQUIRE(N * T == 0 || (A != nullptr && B != nullptr), DP_EINVAL);
-    if (N > 0 && T > 0) {
-        const GhostPlan g = ghost_plan(N, T, d_in, d_out);
-        DPG_REQUIRE(N * g.pairs * g.chunks < (i64(1) << 31), DP_EUNSUPPORTED);
-    }
-    const size_t need = dp_ghost_norm_linear_workspace_bytes(N, T, d_in, d_out);
-    DPG_REQUIRE(ws_bytes >= need && (need == 0 || ws != nullptr), DP_EINVAL);
-    if (N == 0) return DP_OK;
-    if (T == 0) {
-        zero_fill(sqnorm, N, stream);
-        return launch_status();
-    }
-    const GhostPlan g = ghost_plan(N, T, d_in, d_out);
-    const i64 pc = 16 / (i64)dtype_bytes(dt);
-    const bool vec = d_in % pc == 0 && d_out % pc == 0 && aligned(A, 16) && aligned(B, 16);
-    float *tiles = (float *)ws;
-    float *part = tiles + (size_t)(N * g.pairs * g.chunks) * (kBT * kBT);
-    if (dt == DP_BF16) launch_ghost<uint16_t>(A, B, N, T, d_in, d_out, vec, g, tiles, stream);
-    else launch_ghost<float>(A, B, N, T, d_in, d_out, vec, g, tiles, stream);
-    float *out = g.pairs > 1 ? part : sqnorm;
-    ghost_combine_kernel<<<(unsigned)(N * g.pairs), kThreads, 0, stream>>>(tiles, g.nb, g.pairs, g.ca, g.chunks,
-                                                                          bias ? 1.0f : 0.0f, scale * scale, out);
-    if (g.pairs > 1) sum_partials(part, N, g.pairs, sqnorm, stream);
-    return launch_status();
+    DPG_REQUIRE(N >= 0 && N < (i64(1) << 31), DP_EINVAL);
+    dp_ghost_layer it;
+    it.A = A;
+    it.B = B;
+    it.T = T;
+    it.d_in = d_in;
+    it.d_out = d_out;
+    it.scale = scale;
+    it.bias = bias;
+    it.sqnorm = sqnorm;
+    return dp_ghost_norm_linear_many(&it, 1, dt, N, status, ws, ws_bytes, stream);
 }

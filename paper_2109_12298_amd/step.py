@@ -169,9 +169,7 @@ class DPStep:
                 lb.clip_mode = linear_clip_mode(layer, N, wl.dtype) if clip_mode == "auto" else clip_mode
                 lb.ghost = (norm_mode == "ghost" and lb.clip_mode == "fused"
                             and 2 * layer.T * layer.T < layer.d_in * layer.d_out)
-                if lb.ghost:
-                    need_g = dp.dp_ghost_norm_linear_workspace_bytes(N, layer.T, layer.d_in, layer.d_out)
-                else:
+                if not lb.ghost:            # ghost layers share one grouped call and its workspace
                     lb.gW = torch.empty((N, layer.d_out, layer.d_in), **f32)
                     lb.gb = torch.empty((N, layer.d_out), **f32) if layer.bias else None
                     need_g = dp.dp_grad_sample_linear_workspace_bytes(N, layer.T, layer.d_in, layer.d_out, self.dt)
@@ -264,6 +262,14 @@ class DPStep:
                 self.group_items = dp.make_layer_grads([items[i] for i in grouped])
                 need = dp.dp_grad_sample_many_workspace_bytes(self.group_items, len(grouped), self.dt, N)
                 self.ws_group = torch.empty(max(need, 256), dtype=torch.uint8, device=self.device)
+        # ghost-norm Linear layers: one grouped call over all of them
+        self.ghost = [i for i, lb in enumerate(self.layers) if lb.ghost]
+        if self.ghost:
+            self.ghost_items = dp.make_ghost_layers(
+                [(lb.A, lb.B, lb.layer.T, lb.layer.d_in, lb.layer.d_out, self.scale, lb.layer.bias, self.sqnorm[i])
+                 for i, lb in ((i, self.layers[i]) for i in self.ghost)])
+            need = dp.dp_ghost_norm_linear_many_workspace_bytes(self.ghost_items, len(self.ghost), N)
+            self.ws_ghost = torch.empty(max(need, 256), dtype=torch.uint8, device=self.device)
         self.step_dev = torch.zeros(1, dtype=torch.int64, device=self.device)
         self.graph = None
         self.graph_parallel = None
@@ -305,14 +311,21 @@ class DPStep:
     def grad_calls(self) -> List[str]:
         """The per-sample-gradient calls of a step, in order (after the recurrences)."""
         calls = ["grad:group"] if self.grad_group else []
+        calls += ["grad:ghost"] if self.ghost else []
         return calls + ["grad:" + lb.layer.name for i, lb in enumerate(self.layers)
-                        if i not in self.grad_group and not isinstance(lb.layer, W.LSTMRecurrence)]
+                        if i not in self.grad_group and not lb.ghost
+                        and not isinstance(lb.layer, W.LSTMRecurrence)]
 
     # ------------------------------------------------------------------ pieces
     def grad_group_call(self, stream=None):
         """The grouped layers' per-sample gradients in one launch."""
         dp.dp_grad_sample_many(self.group_items, len(self.grad_group), self.dt, self.N, self.status, self.ws_group,
                                stream)
+
+    def ghost_call(self, stream=None):
+        """The ghost-norm layers' per-sample squared norms in one grouped call."""
+        dp.dp_ghost_norm_linear_many(self.ghost_items, len(self.ghost), self.dt, self.N, self.status, self.ws_ghost,
+                                     stream)
 
     def grad_sample(self, i: int, stream=None):
         lb = self.layers[i]
@@ -323,8 +336,7 @@ class DPStep:
             dp.dp_lstm_backward(a["gates"], a["c"], a["W_hh"], None, a["dh_last"], N, layer.T, layer.H, lb.B,
                                 self.status, stream)
         elif isinstance(layer, W.Linear) and lb.ghost:
-            dp.dp_ghost_norm_linear(lb.A, lb.B, self.dt, N, layer.T, layer.d_in, layer.d_out, s, layer.bias, sq,
-                                    self.status, lb.ws, stream)
+            raise KeyError("ghost-norm layer %s runs in the grouped call grad:ghost" % layer.name)
         elif isinstance(layer, W.Linear):
             dp.dp_grad_sample_linear(lb.A, lb.B, self.dt, N, layer.T, layer.d_in, layer.d_out, s, lb.gW, lb.gb,
                                      sq, self.status, lb.ws, stream)
@@ -405,6 +417,8 @@ class DPStep:
             return self.linear_clip_sums(stream)
         if name == "grad:group":
             return self.grad_group_call(stream)
+        if name == "grad:ghost":
+            return self.ghost_call(stream)
         kind, lname = name.split(":", 1)
         i = next(k for k, lb in enumerate(self.layers) if lb.layer.name == lname)
         if kind == "grad":

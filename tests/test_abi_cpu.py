@@ -280,13 +280,42 @@ def test_ghost_norm_validation():
     assert code_of(f, FAKE, FAKE, dp.DP_F32, 2, 8, 0, 4, 1.0, True, FAKE, stream=0) == dp.DP_EINVAL
     assert code_of(f, None, FAKE, dp.DP_F32, 2, 8, 3, 4, 1.0, True, FAKE, stream=0) == dp.DP_EINVAL
     assert code_of(f, FAKE, FAKE, dp.DP_F32, 2, 8, 3, 4, 1.0, True, None, stream=0) == dp.DP_EINVAL
-    # Gram tiles: 16 KB per (sample, tile pair, feature chunk), plus one
-    # partial per (sample, pair) when there are several pairs
-    assert dp.dp_ghost_norm_linear_workspace_bytes(0, 64, 3, 4) == 0
-    assert dp.dp_ghost_norm_linear_workspace_bytes(5, 0, 3, 4) == 0
-    assert dp.dp_ghost_norm_linear_workspace_bytes(5, 64, 3, 4) == 5 * 2 * 16384
-    assert dp.dp_ghost_norm_linear_workspace_bytes(5, 65, 3, 4) == 5 * 3 * 2 * 16384 + 5 * 3 * 4
-    big = dp.dp_ghost_norm_linear_workspace_bytes(32, 128, 768, 3072)
-    assert big % 16384 == 3 * 32 * 4 and big > 32 * 3 * 2 * 16384
+    # one float per (sample, 64 x 64 tile pair) when there are several pairs
+    # (padded to 256 bytes); the partial Gram tiles (2 x 16 KB per sample,
+    # pair and feature chunk) only when the units are too few to fill the GPU
+    ws = dp.dp_ghost_norm_linear_workspace_bytes
+    assert ws(0, 64, 3, 4) == 0
+    assert ws(5, 0, 3, 4) == 0
+    assert ws(5, 64, 3, 4) == 0                     # one pair, one chunk: written into sqnorm
+    assert ws(5, 65, 3, 4) == 256                   # three pairs; 7 features make one chunk
+    assert ws(32, 128, 768, 3072) == 512 + 32 * 3 * 6 * 2 * 16384    # 96 units: six chunks each
+    assert ws(200, 128, 768, 3072) == 200 * 3 * 4 + 160          # 600 units: one chunk
     assert code_of(f, FAKE, FAKE, dp.DP_F32, 2, 65, 3, 4, 1.0, True, FAKE, stream=0) == dp.DP_EINVAL
     assert code_of(f, None, None, dp.DP_F32, 0, 8, 3, 4, 1.0, True, None, stream=0) == dp.DP_OK
+
+
+def test_ghost_norm_many_validation():
+    f = dp.dp_ghost_norm_linear_many
+    FF = 1 << 20
+    lay = lambda T, din, dout, sq=FF: (FF, FF, T, din, dout, 1.0, True, sq)
+    transformer = [lay(128, 768, 768)] * 4 + [lay(128, 768, 3072), lay(128, 3072, 768)]
+    items = dp.make_ghost_layers(transformer)
+    # 6 layers x 32 samples x 3 pairs fill the GPU: one chunk, the pair values only
+    assert dp.dp_ghost_norm_linear_many_workspace_bytes(items, 6, 32) == 6 * 512
+    # alone, each layer's 96 units are split into feature chunks
+    one = dp.make_ghost_layers(transformer[:1])
+    assert dp.dp_ghost_norm_linear_many_workspace_bytes(one, 1, 32) == \
+        dp.dp_ghost_norm_linear_workspace_bytes(32, 128, 768, 768)
+    assert dp.dp_ghost_norm_linear_many_workspace_bytes(items, 0, 32) == 0
+    assert code_of(f, items, 6, 7, 32, stream=0) == dp.DP_EDTYPE
+    assert code_of(f, items, 65, dp.DP_BF16, 32, stream=0) == dp.DP_EINVAL
+    assert code_of(f, items, 6, dp.DP_BF16, 32, stream=0) == dp.DP_EINVAL       # no workspace
+    bad = dp.make_ghost_layers(transformer[:2] + [lay(128, 0, 768)])
+    assert code_of(f, bad, 3, dp.DP_BF16, 32, stream=0) == dp.DP_EINVAL
+    nosq = dp.make_ghost_layers([lay(128, 768, 768, None)])
+    assert code_of(f, nosq, 1, dp.DP_BF16, 32, stream=0) == dp.DP_EINVAL
+    huge = dp.make_ghost_layers([lay(1 << 12, 1 << 20, 8)])
+    assert code_of(f, huge, 1, dp.DP_BF16, 1, stream=0) == dp.DP_EUNSUPPORTED
+    # empty batches and empty lists enqueue nothing
+    assert code_of(f, items, 6, dp.DP_BF16, 0, stream=0) == dp.DP_OK
+    assert code_of(f, items, 0, dp.DP_BF16, 32, stream=0) == dp.DP_OK

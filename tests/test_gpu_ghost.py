@@ -105,3 +105,84 @@ def test_ghost_norm_transformer_ffn_full_size_sampled():
     got = ghost(At, Bt, dp.DP_BF16, N, T, din, dout, 1.0, True)
     picks = [0, 7, 19, 31]
     assert_rel(got[picks], oracle_sq(At, Bt, 1.0, True, samples=picks), 1e-4, "ffn1 sampled")
+
+
+def ghost_many(layers, dt, N, scale=0.9):
+    """dp_ghost_norm_linear_many over (A, B, T, d_in, d_out, bias) layers: each layer's sqnorm."""
+    outs = [torch.full((max(N, 1),), 7.0, device=DEV)[:N] for _ in layers]
+    items = dp.make_ghost_layers([(A, B, T, din, dout, scale, bias, sq)
+                                  for (A, B, T, din, dout, bias), sq in zip(layers, outs)])
+    ws = torch.empty(max(dp.dp_ghost_norm_linear_many_workspace_bytes(items, len(layers), N), 1),
+                     dtype=torch.uint8, device=DEV)
+    dp.dp_ghost_norm_linear_many(items, len(layers), dt, N, None, ws)
+    torch.cuda.synchronize()
+    return [o.cpu().numpy() for o in outs]
+
+
+# (T, d_in, d_out, bias) per layer; one call per list
+MANY_BF16 = [(128, 264, 136, True),     # three pairs, ragged feature stages
+             (130, 16, 24, False),      # ragged T: six pairs
+             (64, 768, 768, True),      # one pair
+             (200, 33, 64, True),       # d_in not a multiple of 8: the element-load launch
+             (0, 8, 8, True),           # no positions: zero norms
+             (96, 40, 3000, True)]      # d_out much larger than d_in
+
+
+@pytest.mark.parametrize("N", [1, 3])
+def test_ghost_norm_many_matches_oracle(N):
+    """A few samples: the units do not fill the GPU, so each pair is split
+    into feature chunks and a second launch adds them."""
+    say("ghost many bf16 N", N)
+    rng = np.random.default_rng(40 + N)
+    layers = []
+    for T, din, dout, bias in MANY_BF16:
+        A, B = inputs(rng, N, T, din, dout, "bf16")
+        layers.append((A, B, T, din, dout, bias))
+    got = ghost_many(layers, dp.DP_BF16, N)
+    for (A, B, T, din, dout, bias), g in zip(layers, got):
+        assert_rel(g, oracle_sq(A, B, 0.9, bias), 1e-4, "many T=%d %dx%d" % (T, din, dout))
+        alone = ghost(A, B, dp.DP_BF16, N, T, din, dout, 0.9, bias)
+        assert_rel(g, alone, 1e-5, "many vs alone T=%d %dx%d" % (T, din, dout))
+
+
+def test_ghost_norm_many_one_chunk_matches_oracle_and_single_calls():
+    """64 samples of T = 256 (ten tile pairs each): enough units for one chunk
+    per pair, the Gram tiles' product formed in registers; each layer alone
+    has enough units too, so the grouped call equals the single calls bit for
+    bit.  fp32 and bf16, with an element-load layer."""
+    N = 64
+    for dtype, shapes in (("f32", [(256, 40, 24, True), (256, 16, 48, False)]),
+                          ("bf16", [(256, 40, 24, True), (256, 16, 48, False), (250, 20, 12, True)])):
+        say("ghost many one chunk", dtype)
+        rng = np.random.default_rng(9)
+        dt = dp.DP_BF16 if dtype == "bf16" else dp.DP_F32
+        layers = []
+        for T, din, dout, bias in shapes:
+            A, B = inputs(rng, N, T, din, dout, dtype)
+            layers.append((A, B, T, din, dout, bias))
+        got = ghost_many(layers, dt, N)
+        for (A, B, T, din, dout, bias), g in zip(layers, got):
+            assert_rel(g, oracle_sq(A, B, 0.9, bias), 1e-4, "one chunk %s T=%d %dx%d" % (dtype, T, din, dout))
+            alone = ghost(A, B, dt, N, T, din, dout, 0.9, bias)
+            np.testing.assert_array_equal(g, alone)
+
+
+def test_ghost_norm_many_transformer_full_size_sampled():
+    """The transformer block's six Linear layers (N = 32, T = 128, bf16) in one
+    grouped call, the benchmark's launch: every sample on the GPU, two per
+    layer through the oracle, and every sample against the layer's own call
+    (which splits its 96 units into feature chunks)."""
+    N, T = 32, 128
+    say("ghost many transformer full size")
+    rng = np.random.default_rng(78)
+    shapes = [(768, 768)] * 4 + [(768, 3072), (3072, 768)]
+    layers = []
+    for din, dout in shapes:
+        A, B = inputs(rng, N, T, din, dout, "bf16")
+        layers.append((A, B, T, din, dout, True))
+    got = ghost_many(layers, dp.DP_BF16, N, scale=1.0)
+    for k, ((A, B, _, din, dout, bias), g) in enumerate(zip(layers, got)):
+        picks = [k, 31 - 2 * k]
+        assert_rel(g[picks], oracle_sq(A, B, 1.0, bias, samples=picks), 1e-4, "layer %d sampled" % k)
+        alone = ghost(A, B, dp.DP_BF16, N, T, din, dout, 1.0, bias)
+        assert_rel(g, alone, 1e-5, "layer %d vs alone" % k)
