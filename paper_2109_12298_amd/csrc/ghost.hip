@@ -22,20 +22,21 @@
 // those of B, in stages of 128 bytes per position row (64 bf16 or 32 fp32
 // features) of the tile's i-block rows and j-block rows (one block when bi =
 // bj): the stages are copied straight into LDS by 16-byte direct loads,
-// several stages in flight, each row's 16-byte chunks stored at chunk
-// position q ^ (row & 7) so that the operand reads (32 rows, one chunk each)
-// are free of bank conflicts.  Wave w computes the 32 x 32 sub-tile (w & 1,
-// w >> 1) of the pair.  Both Grams contract over the feature index, the
-// contiguous one in memory, so an MFMA operand is one 16-byte chunk of one
-// row: eight bf16 features for v_mfma_f32_32x32x16_bf16, or four fp32
-// features for four v_mfma_f32_32x32x2f32 (the order in which features are
-// contracted is immaterial as long as both operands share it).  Rows past T
-// and features past d read as zeros.
+// several stages in flight, each row's 16-byte chunks swizzled so that the
+// operand reads (one chunk from each of 32 rows) are free of bank conflicts.
+// Both Grams contract over the feature index, the contiguous one in memory,
+// so an MFMA operand is one 16-byte chunk of one row: eight bf16 features
+// for v_mfma_f32_32x32x16_bf16, or four fp32 features for four
+// v_mfma_f32_32x32x2f32 (the order in which features are contracted is
+// immaterial as long as both operands share it).  The four waves split each
+// stage's k-steps and each computes the whole pair, so every operand
+// fragment read from LDS feeds two MFMAs; LDS bandwidth, not the MFMAs,
+// bounds the loop.  Rows past T and features past d read as zeros.
 //
 // With one chunk (a launch with enough units to fill the GPU: the usual case
-// once the layers of a step share the launch) the workgroup holds G_A's and
-// G_B's tiles in registers at the end, so it forms sum G_B (G_A + bias)
-// itself, counts an off-diagonal pair twice (the Grams are symmetric) and
+// once the layers of a step share the launch) the workgroup ends with G_A's
+// and G_B's tiles (its waves' shares added through LDS), so it forms
+// sum G_B (G_A + bias) itself, counts an off-diagonal pair twice (the Grams are symmetric) and
 // writes s^2 times that: nothing is written but one float per (sample,
 // pair).  With several chunks (a small batch) each chunk writes its two
 // partial tiles and a second launch adds them in chunk order before forming
@@ -119,6 +120,12 @@ __device__ __forceinline__ void wait_later(int later)
     }
 }
 
+// Chunk q of staged row r sits at chunk position q ^ swz(r).  Rows are 128
+// bytes, so two rows span the 256 bytes of the LDS banks; an operand read
+// takes one chunk from each of 32 consecutive rows, and with this swizzle any
+// 16 consecutive rows put that chunk in 16 different 16-byte bank groups.
+__device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
+
 __device__ __forceinline__ uint32_t elem_bits(uint16_t v) { return v; }
 __device__ __forceinline__ uint32_t elem_bits(float v) { return __float_as_uint(v); }
 
@@ -136,10 +143,27 @@ __device__ __forceinline__ void mma_chunk(const uint4 &a, const uint4 &b, f32x16
     acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.w), __uint_as_float(b.w), acc, 0, 0, 0);
 }
 
+// Weight of 32 x 32 block b = 2 x + y of a pair's tiles in the pair's value:
+// a diagonal pair (bi = bj) skips block (1, 0), the transpose of (0, 1)
+// (both Grams are symmetric), and counts (0, 1) twice.
+__host__ __device__ __forceinline__ float block_weight(int b, bool diag)
+{
+    return diag ? (b == 1 ? 2.0f : b == 2 ? 0.0f : 1.0f) : 1.0f;
+}
+
 // One work unit: sample n, pair p = (bi, bj), chunk c of layer L.  VEC:
 // every row is 16-byte aligned and d_in, d_out are whole chunks, so the
 // stages are direct loads; otherwise each thread loads its chunks element by
 // element (bounds-checked) and stores them to LDS itself.
+//
+// Wave w = 2 kh + x computes the blocks (x, 0) and (x, 1) of the pair (x
+// over the i-block's halves, y over the j-block's) over k-steps kh and kh + 2
+// of every stage (16-byte chunks 2 s and 2 s + 1 of each row for k-step s:
+// lanes 0-31 the first, 32-63 the second).  Per k-step it reads the i-half
+// and both j-halves (a diagonal pair: the two halves, the i-half being one
+// of them) for two MFMAs, and a stage's reads are issued while the MFMAs of
+// the stage before run.  At the end the two k-parities' tiles are added
+// through LDS (kh = 0 first).
 template <typename T, bool VEC, bool DIAG>
 __device__ __forceinline__ void gram_unit(const GhostLayer &L, i64 n, int p, int bi, int bj, int c, char *smem,
                                           float *red)
@@ -148,8 +172,10 @@ __device__ __forceinline__ void gram_unit(const GhostLayer &L, i64 n, int p, int
     constexpr int F = kRowBytes / (int)sizeof(T);            // features per stage
     constexpr int ROWS = DIAG ? kBT : 2 * kBT;               // staged rows
     constexpr int LOADS = ROWS * kRowBytes / 1024 / kWaves;  // 16-byte loads per lane per stage
+    static_assert(kStages * kStageBytes >= 2 * kTile * (int)sizeof(float), "the final sum reuses the ring");
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int x = wave & 1, kh = wave >> 1;
     const i64 Tn = L.T, din = L.din, dout = L.dout;
     const int C = L.chunks;
     const int a0 = (int)((i64)c * L.sa / C), a1 = (int)((i64)(c + 1) * L.sa / C);
@@ -160,41 +186,45 @@ __device__ __forceinline__ void gram_unit(const GhostLayer &L, i64 n, int p, int
 
     // this lane's share of a stage: load r covers LDS bytes 1024 a + 16 lane,
     // a = wave + 4 r, i.e. staged row 8 a + lane / 8, chunk position lane % 8
-    int offA[LOADS], offB[LOADS], fq[LOADS];
-    bool rok[LOADS];
+    // (which holds chunk (lane % 8) ^ swz(row))
+    int trow[LOADS];
+    uint32_t fq[LOADS];
 #pragma unroll
     for (int r = 0; r < LOADS; ++r) {
         const int a = wave + kWaves * r;
         const int row = 8 * a + (lane >> 3);
-        const int q = (lane & 7) ^ (row & 7);
+        const int q = (lane & 7) ^ swz(row);
         const i64 t = row < kBT ? (i64)bi * kBT + row : (i64)bj * kBT + (row - kBT);
-        rok[r] = t < Tn;
-        fq[r] = q * EPC;
-        offA[r] = (int)(t * din) + fq[r];
-        offB[r] = (int)(t * dout) + fq[r];
+        // a row past T never passes the feature test below
+        fq[r] = t < Tn ? (uint32_t)(q * EPC) : 0x80000000u;
+        trow[r] = t < Tn ? (int)t : 0;
     }
     const uint32_t lds0 = bf16s::lds_addr(smem);
+    // the zero source's address, held in registers (not reloaded per stage)
+    uint64_t zaddr = reinterpret_cast<uint64_t>(g_ghost_zero);
+    asm volatile("" : "+s"(zaddr));
+    const void *zero = reinterpret_cast<const void *>(zaddr);
     auto issue = [&](int k, int slot) {
         const bool onA = k < na;
         const int f0 = (onA ? a0 + k : b0 + (k - na)) * F;
-        const i64 d = onA ? din : dout;
+        const uint32_t d = (uint32_t)(onA ? din : dout);
         const T *X = onA ? An : Bn;
 #pragma unroll
         for (int r = 0; r < LOADS; ++r) {
             const int a = wave + kWaves * r;
-            const int f = f0 + fq[r];
-            const int off = (onA ? offA[r] : offB[r]) + f0;
+            const uint32_t f = (uint32_t)f0 + fq[r];        // f0 < 2^31: no wrap
+            const int off = trow[r] * (int)d + (int)f;
             if constexpr (VEC) {
-                const void *src = (rok[r] && f < d) ? (const void *)(X + off) : (const void *)g_ghost_zero;
+                const void *src = f < d ? (const void *)(X + off) : zero;
                 bf16s::dma16(src, lds0 + (uint32_t)(slot * kStageBytes + a * 1024));
             } else {
                 uint32_t wd[4];
 #pragma unroll
-                for (int x = 0; x < 4; ++x) wd[x] = 0u;
+                for (int e = 0; e < 4; ++e) wd[e] = 0u;
 #pragma unroll
-                for (int x = 0; x < EPC; ++x) {
-                    const uint32_t v = (rok[r] && f + x < d) ? elem_bits(X[off + x]) : 0u;
-                    wd[x * (int)sizeof(T) / 4] |= v << (8 * ((x * (int)sizeof(T)) & 3));
+                for (int e = 0; e < EPC; ++e) {
+                    const uint32_t v = f + (uint32_t)e < d ? elem_bits(X[off + e]) : 0u;
+                    wd[e * (int)sizeof(T) / 4] |= v << (8 * ((e * (int)sizeof(T)) & 3));
                 }
                 *reinterpret_cast<uint4 *>(smem + slot * kStageBytes + a * 1024 + 16 * lane) =
                     make_uint4(wd[0], wd[1], wd[2], wd[3]);
@@ -202,61 +232,124 @@ __device__ __forceinline__ void gram_unit(const GhostLayer &L, i64 n, int p, int
         }
     };
 
-    // operand rows: ra on the i side, rb on the j side; chunk 2 g + lane / 32
-    // of each for the four MFMA steps of a stage
-    const int ra = 32 * (wave & 1) + (lane & 31);
-    const int rb = (DIAG ? 0 : kBT) + 32 * (wave >> 1) + (lane & 31);
-    const int h = lane >> 5;
-    int oa[4], ob[4];
+    // LDS offsets of the wave's fragments in k-step s = kh + 2 u: the j-halves
+    // (rows 32 y + lane % 32 of the j-block) and, off the diagonal, the i-half
+    constexpr int NF = DIAG ? 2 : 3;
+    int of[2][NF];
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-        oa[g] = ra * kRowBytes + 16 * ((2 * g + h) ^ (ra & 7));
-        ob[g] = rb * kRowBytes + 16 * ((2 * g + h) ^ (rb & 7));
+    for (int u = 0; u < 2; ++u) {
+        const int ch = 2 * (kh + 2 * u) + (lane >> 5);
+#pragma unroll
+        for (int f = 0; f < NF; ++f) {
+            const int row = f < 2 ? (DIAG ? 0 : kBT) + 32 * f + (lane & 31) : 32 * x + (lane & 31);
+            of[u][f] = row * kRowBytes + 16 * (ch ^ swz(row));
+        }
     }
-
-    f32x16_t acc, accA;
+    struct Frags {
+        uint4 v[2][NF];
+    };
+    auto read = [&](int slot, Frags &fr) {
+        const char *Ls = smem + slot * kStageBytes;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) acc[r] = accA[r] = 0.0f;
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+            for (int f = 0; f < NF; ++f) fr.v[u][f] = *reinterpret_cast<const uint4 *>(Ls + of[u][f]);
+    };
+
+    f32x16_t acc[2], accA[2];     // blocks (x, 0), (x, 1) of G_B and of G_A
+#pragma unroll
+    for (int y = 0; y < 2; ++y)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[y][r] = accA[y][r] = 0.0f;
+    auto mma = [&](const Frags &fr, f32x16_t (&G)[2]) {
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            const uint4 &j0 = fr.v[u][0], &j1 = fr.v[u][1];
+            uint4 i;
+            if constexpr (DIAG) {
+                i = x ? j1 : j0;
+            } else {
+                i = fr.v[u][NF - 1];
+            }
+            mma_chunk(i, j0, G[0], T());
+            mma_chunk(i, j1, G[1], T());
+        }
+    };
 
 #pragma unroll
     for (int k = 0; k < kStages - 1; ++k)
         if (k < nst) issue(k, k);
-    int slot = 0;
-    for (int k = 0; k < nst; ++k) {
+    // stage k: wait for its loads, then (all waves) for everyone's; refill the
+    // slot of stage k - 1, whose reads every wave has finished
+    auto arrive = [&](int k) {
         if constexpr (VEC) {
             const int later = nst - 1 - k < kStages - 2 ? nst - 1 - k : kStages - 2;
-            wait_later<LOADS, kStages - 2>(later);       // stage k has landed (this wave's loads)
+            wait_later<LOADS, kStages - 2>(later);
         }
-        bf16s::wait_lgkmcnt0();                          // this wave's reads of stage k - 1 are done
+        bf16s::wait_lgkmcnt0();
         bf16s::stage_barrier();
-        if (k + kStages - 1 < nst) issue(k + kStages - 1, slot == 0 ? kStages - 1 : slot - 1);
-        if (k == na) {                                   // the B side starts: keep G_A's tile
-            accA = acc;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
+        if (k + kStages - 1 < nst) issue(k + kStages - 1, (k + kStages - 1) % kStages);
+    };
+    // stages k0 .. k1 - 1 into G: iteration k reads stage k into nxt while the
+    // MFMAs of stage k - 1 run on cur.  The A side and the B side are two such
+    // loops, each with its own accumulators (the loads run on across them).
+    auto run = [&](int k0, int k1, f32x16_t (&G)[2]) {
+        if (k0 >= k1) return;
+        Frags fx, fy;
+        arrive(k0);
+        read(k0 % kStages, fx);
+        int k = k0 + 1;
+        for (; k + 1 < k1; k += 2) {
+            arrive(k);
+            read(k % kStages, fy);
+            mma(fx, G);
+            arrive(k + 1);
+            read((k + 1) % kStages, fx);
+            mma(fy, G);
         }
-        const char *Ls = smem + slot * kStageBytes;
-        uint4 av[4], bv[4];
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-            av[g] = *reinterpret_cast<const uint4 *>(Ls + oa[g]);
-            bv[g] = *reinterpret_cast<const uint4 *>(Ls + ob[g]);
+        if (k < k1) {
+            arrive(k);
+            read(k % kStages, fy);
+            mma(fx, G);
+            fx = fy;
         }
+        mma(fx, G);
+    };
+    run(0, na, accA);
+    run(na, nst, acc);
+
+    // the two k-parities' blocks added (kh = 0 first), G_A then G_B, through
+    // two 16 KB regions of the ring: register group q (registers 4 q .. 4 q +
+    // 3) of lane l of block b sits at float 4 ((4 b + q) 64 + l), so a wave's
+    // 16-byte stores and loads are consecutive.  Thread t ends with entries
+    // 16 t .. 16 t + 15 (block t / 64, lane t % 64, registers 0-15).
+    float ga[16], gb[16];
+    float *R = reinterpret_cast<float *>(smem);
+    auto add_parities = [&](const f32x16_t (&v)[2], float (&out)[16]) {
+        __syncthreads();                  // the ring (or the last sum) is free
 #pragma unroll
-        for (int g = 0; g < 4; ++g) mma_chunk(av[g], bv[g], acc, T());
-        slot = slot + 1 == kStages ? 0 : slot + 1;
-    }
-    if (na == nst) {                                     // no B stages in this chunk
-        accA = acc;
+        for (int y = 0; y < 2; ++y)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
-    }
+            for (int q = 0; q < 4; ++q)
+                *reinterpret_cast<float4 *>(R + kh * kTile + 4 * ((4 * (2 * x + y) + q) * 64 + lane)) =
+                    make_float4(v[y][4 * q], v[y][4 * q + 1], v[y][4 * q + 2], v[y][4 * q + 3]);
+        __syncthreads();
+        const int b = tid >> 6;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const float4 e = *reinterpret_cast<const float4 *>(R + 4 * ((4 * b + q) * 64 + lane));
+            const float4 g = *reinterpret_cast<const float4 *>(R + kTile + 4 * ((4 * b + q) * 64 + lane));
+            out[4 * q] = e.x + g.x; out[4 * q + 1] = e.y + g.y; out[4 * q + 2] = e.z + g.z; out[4 * q + 3] = e.w + g.w;
+        }
+    };
+    add_parities(accA, ga);
+    add_parities(acc, gb);
 
     if (C == 1) {
         float s = 0.0f;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) s += acc[r] * (accA[r] + L.bias);
-        s = wave_sum(s);
+        for (int r = 0; r < 16; ++r) s += gb[r] * (ga[r] + L.bias);
+        s = wave_sum(s * block_weight(tid >> 6, DIAG));
         if (lane == 0) red[wave] = s;
         __syncthreads();
         if (tid == 0) {
@@ -266,14 +359,14 @@ __device__ __forceinline__ void gram_unit(const GhostLayer &L, i64 n, int p, int
             L.out[n * L.pairs + p] = L.s2 * (DIAG ? t : 2.0f * t);
         }
     } else {
-        // the two partial tiles in register order: wave, lane, register
-        float *tA = L.tiles + ((size_t)((n * L.pairs + p) * C + c) * 2) * kTile + wave * 1024 + lane * 16;
+        // the two partial tiles, thread t's 16 entries at 16 t
+        float *tA = L.tiles + ((size_t)((n * L.pairs + p) * C + c) * 2) * kTile + tid * 16;
         float4 *oA = reinterpret_cast<float4 *>(tA);
         float4 *oB = reinterpret_cast<float4 *>(tA + kTile);
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-            oA[q] = make_float4(accA[4 * q], accA[4 * q + 1], accA[4 * q + 2], accA[4 * q + 3]);
-            oB[q] = make_float4(acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]);
+            oA[q] = make_float4(ga[4 * q], ga[4 * q + 1], ga[4 * q + 2], ga[4 * q + 3]);
+            oB[q] = make_float4(gb[4 * q], gb[4 * q + 1], gb[4 * q + 2], gb[4 * q + 3]);
         }
     }
 }
@@ -330,7 +423,7 @@ __global__ __launch_bounds__(kThreads) void ghost_combine_kernel(const GhostGrou
     float s = 0.0f;
 #pragma unroll
     for (int r = 0; r < 16; ++r) s += gb[r] * (ga[r] + L.bias);
-    s = wave_sum(s);
+    s = wave_sum(s * block_weight(threadIdx.x >> 6, bi == bj));
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     if (lane == 0) red[wave] = s;
     __syncthreads();
