@@ -622,8 +622,10 @@ def main():
     else:
         roof = {"bound": "hbm", "achieved": round(nbytes / dt_s / 1e9, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s"}
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-    roof["traffic"] = traffic_for(kname, wl.name, dominant)
-    crec = counters_for(kname, wl.name, dominant)
+    # counter records are kept per workload and norm mode (the ghost step's calls differ)
+    pkey = wl.name + ("+ghost" if args.norm_mode == "ghost" else "")
+    roof["traffic"] = traffic_for(kname, pkey, dominant)
+    crec = counters_for(kname, pkey, dominant)
     # MFMA-busy fraction from a committed counter run of the same kernel source (null otherwise)
     roof["mfma_busy_counter"] = None if crec is None or "MfmaUtil" not in crec else round(crec["MfmaUtil"] / 100, 4)
     roof.update({"kernel": kname, "call": dominant, "avg_us": round(dom_ms * 1e3, 2),
@@ -645,7 +647,7 @@ def main():
             "roofline": roof}
     if args.meta_out:
         with open(args.meta_out, "w") as f:
-            json.dump({"workload": wl.name, "calls": names, "launches": args.steps,
+            json.dump({"workload": pkey, "calls": names, "launches": args.steps,
                        "kernels": {n: costs[n][2] for n in names},
                        "algorithmic_bytes": {n: costs[n][0] for n in names},
                        "algorithmic_flops": {n: costs[n][1] for n in names},
