@@ -133,8 +133,10 @@ def call_costs(st, nnz=None):
             out["grad:" + L.name] = (N * L.T * (2 * G + L.H) * 4 + G * L.H * 4 + N * L.H * 4,
                                      2 * N * L.T * G * L.H, "lstm_bptt_kernel", "alu")
         elif isinstance(L, W.LayerNorm):
-            out["grad:" + L.name] = (2 * N * L.T * L.D * e + 2 * N * L.D * 4, 3 * N * L.T * L.D,
-                                     "ln_partial_kernel", None)
+            # all LayerNorm layers share one grouped call
+            b0, f0, _, _ = out.get("grad:lns", (0, 0, None, None))
+            out["grad:lns"] = (b0 + 2 * N * L.T * L.D * e + 2 * N * L.D * 4 + N * 4, f0 + 3 * N * L.T * L.D,
+                               "ln_rows_kernel", None)
             col_bytes += 2 * N * L.D * 4
         elif isinstance(L, W.GroupNorm):
             out["grad:" + L.name] = (2 * N * L.C * L.P * e + 2 * N * L.C * 4 + N * 4, 3 * N * L.C * L.P,
@@ -199,6 +201,7 @@ KERNEL_SOURCES = {
     "emb_csr_kernel": ["paper_2109_12298_amd/csrc/embedding.hip"],
     "emb_clipsum_kernel": ["paper_2109_12298_amd/csrc/clip.hip"],
     "ln_partial_kernel": ["paper_2109_12298_amd/csrc/layernorm.hip"],
+    "ln_rows_kernel": ["paper_2109_12298_amd/csrc/layernorm.hip"],
     "lstm_bptt_kernel": ["paper_2109_12298_amd/csrc/lstm.hip"],
     "add_noise_kernel": ["paper_2109_12298_amd/csrc/noise.hip"],
     "colsum_many_kernel+finish_many_kernel": ["paper_2109_12298_amd/csrc/group.hip",

@@ -252,6 +252,38 @@ dp_status dp_grad_sample_layernorm(const void *xhat, const void *B, dp_dtype dt,
                                    float *gbeta, float *sqnorm, int32_t *status, void *ws,
                                    size_t ws_bytes, hipStream_t stream);
 
+/* One layer of dp_grad_sample_layernorm_many: the arguments of
+ * dp_grad_sample_layernorm (xhat, B, T, D, scale, ggamma, gbeta, sqnorm or
+ * NULL) with the same meaning and layouts.  The caller owns every buffer. */
+typedef struct dp_layernorm_layer {
+    const void *xhat;
+    const void *B;
+    int64_t T, D;
+    float scale;
+    float *ggamma;
+    float *gbeta;
+    float *sqnorm;
+} dp_layernorm_layer;
+
+/* The LayerNorm affine gradients of `count` layers that share N and the
+ * dtype, as by one dp_grad_sample_layernorm call per layer (same formulas;
+ * equal up to rounding order), in one launch over every layer's (sample,
+ * 128-byte feature chunk) pairs, each adding all T positions in a fixed
+ * order, and one more adding each sample's chunk partials of the squared
+ * norm in chunk order (layers whose D is not a multiple of 16 bytes' worth
+ * of elements, or whose xhat or B is not 16-byte aligned, take a launch of
+ * their own with element loads; up to 16 layers per launch).  Arguments are
+ * checked as dp_grad_sample_layernorm checks them; the first invalid layer's
+ * status is returned before anything is enqueued.  count in [0, 64].
+ * Workspace: dp_grad_sample_layernorm_many_workspace_bytes(items, count, N,
+ * dt) bytes (one float per sample and chunk of each layer with more than one
+ * chunk, in item order). */
+size_t dp_grad_sample_layernorm_many_workspace_bytes(const dp_layernorm_layer *items, int32_t count,
+                                                     int64_t N, dp_dtype dt);
+dp_status dp_grad_sample_layernorm_many(const dp_layernorm_layer *items, int32_t count, dp_dtype dt,
+                                        int64_t N, int32_t *status, void *ws, size_t ws_bytes,
+                                        hipStream_t stream);
+
 /* GroupNorm's and InstanceNorm's per-channel affine y = gamma[c] * xhat +
  * beta[c] over a channel's P spatial positions (normalization layers are
  * among the predefined layer types of section "Design Principles and

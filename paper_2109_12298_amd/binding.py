@@ -57,6 +57,8 @@ SIGNATURES = {
     "dp_ghost_norm_linear_workspace_bytes": (_SZ, [_I64, _I64, _I64, _I64]),
     "dp_ghost_norm_linear": (_ST, [_P, _P, _ST, _I64, _I64, _I64, _I64, _F, _I32, _P, _P, _P, _SZ, _P]),
     "dp_ghost_norm_linear_many_workspace_bytes": (_SZ, [_P, _I32, _I64]),
+    "dp_grad_sample_layernorm_many_workspace_bytes": (_SZ, [_P, _I32, _I64, _ST]),
+    "dp_grad_sample_layernorm_many": (_ST, [_P, _I32, _ST, _I64, _P, _P, _SZ, _P]),
     "dp_ghost_norm_linear_many": (_ST, [_P, _I32, _ST, _I64, _P, _P, _SZ, _P]),
     "dp_sqnorm_from_grads": (_ST, [_P, _I64, _I64, _P, _P, _P]),
     "dp_clip_factors": (_ST, [_P, _I64, _F, _P, _P, _P]),
@@ -185,6 +187,27 @@ def make_ghost_layers(entries):
         arr[i].scale = float(scale)
         arr[i].bias = 1 if bias else 0
         arr[i].sqnorm = _ptr(sqnorm)
+    return arr
+
+
+class DPLayerNormLayer(ctypes.Structure):
+    """struct dp_layernorm_layer of dpgrad.h."""
+    _fields_ = [("xhat", ctypes.c_void_p), ("B", ctypes.c_void_p), ("T", ctypes.c_int64), ("D", ctypes.c_int64),
+                ("scale", ctypes.c_float), ("ggamma", ctypes.c_void_p), ("gbeta", ctypes.c_void_p),
+                ("sqnorm", ctypes.c_void_p)]
+
+
+def make_layernorm_layers(entries):
+    """A dp_layernorm_layer array from (xhat, B, T, D, scale, ggamma, gbeta, sqnorm) tuples."""
+    arr = (DPLayerNormLayer * max(len(entries), 1))()
+    for i, (xh, B, T, D, scale, gg, gb, sq) in enumerate(entries):
+        arr[i].xhat = _ptr(xh)
+        arr[i].B = _ptr(B)
+        arr[i].T, arr[i].D = int(T), int(D)
+        arr[i].scale = float(scale)
+        arr[i].ggamma = _ptr(gg)
+        arr[i].gbeta = _ptr(gb)
+        arr[i].sqnorm = _ptr(sq)
     return arr
 
 
@@ -437,6 +460,16 @@ def dp_ghost_norm_linear_many(items, count, dt, N, status=None, ws=None, stream=
     _check(lib().dp_ghost_norm_linear_many(ctypes.cast(items, ctypes.c_void_p), count, dt, N, _ptr(status),
                                            _ptr(ws), _nbytes(ws), _stream(stream)),
            "dp_ghost_norm_linear_many")
+
+
+def dp_grad_sample_layernorm_many_workspace_bytes(items, count, N, dt) -> int:
+    return lib().dp_grad_sample_layernorm_many_workspace_bytes(ctypes.cast(items, ctypes.c_void_p), count, N, dt)
+
+
+def dp_grad_sample_layernorm_many(items, count, dt, N, status=None, ws=None, stream=None):
+    _check(lib().dp_grad_sample_layernorm_many(ctypes.cast(items, ctypes.c_void_p), count, dt, N, _ptr(status),
+                                               _ptr(ws), _nbytes(ws), _stream(stream)),
+           "dp_grad_sample_layernorm_many")
 
 
 def dp_grad_sample_many_grouped(items, k, dt, N) -> bool:

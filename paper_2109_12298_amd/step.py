@@ -262,6 +262,14 @@ class DPStep:
                 self.group_items = dp.make_layer_grads([items[i] for i in grouped])
                 need = dp.dp_grad_sample_many_workspace_bytes(self.group_items, len(grouped), self.dt, N)
                 self.ws_group = torch.empty(max(need, 256), dtype=torch.uint8, device=self.device)
+        # LayerNorm layers: one grouped call over all of them
+        self.lns = [i for i, lb in enumerate(self.layers) if isinstance(lb.layer, W.LayerNorm)]
+        if self.lns:
+            self.ln_items = dp.make_layernorm_layers(
+                [(lb.A, lb.B, lb.layer.T, lb.layer.D, self.scale, lb.gW, lb.gb, self.sqnorm[i])
+                 for i, lb in ((i, self.layers[i]) for i in self.lns)])
+            need = dp.dp_grad_sample_layernorm_many_workspace_bytes(self.ln_items, len(self.lns), N, self.dt)
+            self.ws_lns = torch.empty(max(need, 256), dtype=torch.uint8, device=self.device)
         # ghost-norm Linear layers: one grouped call over all of them
         self.ghost = [i for i, lb in enumerate(self.layers) if lb.ghost]
         if self.ghost:
@@ -312,8 +320,9 @@ class DPStep:
         """The per-sample-gradient calls of a step, in order (after the recurrences)."""
         calls = ["grad:group"] if self.grad_group else []
         calls += ["grad:ghost"] if self.ghost else []
+        calls += ["grad:lns"] if self.lns else []
         return calls + ["grad:" + lb.layer.name for i, lb in enumerate(self.layers)
-                        if i not in self.grad_group and not lb.ghost
+                        if i not in self.grad_group and not lb.ghost and i not in self.lns
                         and not isinstance(lb.layer, W.LSTMRecurrence)]
 
     # ------------------------------------------------------------------ pieces
@@ -326,6 +335,11 @@ class DPStep:
         """The ghost-norm layers' per-sample squared norms in one grouped call."""
         dp.dp_ghost_norm_linear_many(self.ghost_items, len(self.ghost), self.dt, self.N, self.status, self.ws_ghost,
                                      stream)
+
+    def layernorm_call(self, stream=None):
+        """The LayerNorm layers' affine gradients in one grouped call."""
+        dp.dp_grad_sample_layernorm_many(self.ln_items, len(self.lns), self.dt, self.N, self.status, self.ws_lns,
+                                         stream)
 
     def grad_sample(self, i: int, stream=None):
         lb = self.layers[i]
@@ -419,6 +433,8 @@ class DPStep:
             return self.grad_group_call(stream)
         if name == "grad:ghost":
             return self.ghost_call(stream)
+        if name == "grad:lns":
+            return self.layernorm_call(stream)
         kind, lname = name.split(":", 1)
         i = next(k for k, lb in enumerate(self.layers) if lb.layer.name == lname)
         if kind == "grad":

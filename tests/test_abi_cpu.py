@@ -294,6 +294,27 @@ def test_ghost_norm_validation():
     assert code_of(f, None, None, dp.DP_F32, 0, 8, 3, 4, 1.0, True, None, stream=0) == dp.DP_OK
 
 
+def test_layernorm_many_validation():
+    f = dp.dp_grad_sample_layernorm_many
+    FF = 1 << 20
+    lay = lambda T, D, gg=FF: (FF, FF, T, D, 1.0, gg, FF, FF)
+    items = dp.make_layernorm_layers([lay(128, 768), lay(128, 768), lay(7, 64)])
+    ws = dp.dp_grad_sample_layernorm_many_workspace_bytes
+    # one float per (sample, 128-byte feature chunk) of a layer with several chunks
+    assert ws(items, 3, 32, dp.DP_BF16) == 2 * 32 * 12 * 4            # 12 chunks of 64; 64 features: one
+    assert ws(items, 3, 32, dp.DP_F32) == 2 * 32 * 24 * 4 + 256       # 24 chunks of 32; 2 chunks (256-padded)
+    assert ws(items, 3, 0, dp.DP_BF16) == 0 and ws(items, 0, 32, dp.DP_BF16) == 0
+    assert code_of(f, items, 3, 7, 32, stream=0) == dp.DP_EDTYPE
+    assert code_of(f, items, 65, dp.DP_BF16, 32, stream=0) == dp.DP_EINVAL
+    assert code_of(f, items, 3, dp.DP_BF16, 32, stream=0) == dp.DP_EINVAL       # no workspace
+    bad = dp.make_layernorm_layers([lay(128, 768), lay(128, 0)])
+    assert code_of(f, bad, 2, dp.DP_BF16, 32, stream=0) == dp.DP_EINVAL
+    nog = dp.make_layernorm_layers([lay(8, 64, None)])
+    assert code_of(f, nog, 1, dp.DP_BF16, 32, stream=0) == dp.DP_EINVAL
+    assert code_of(f, items, 3, dp.DP_BF16, 0, stream=0) == dp.DP_OK
+    assert code_of(f, items, 0, dp.DP_BF16, 32, stream=0) == dp.DP_OK
+
+
 def test_ghost_norm_many_validation():
     f = dp.dp_ghost_norm_linear_many
     FF = 1 << 20

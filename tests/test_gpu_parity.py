@@ -647,6 +647,48 @@ def test_layernorm_and_empty_inputs():
     assert float(S.abs().sum()) == 0
 
 
+def test_layernorm_many_matches_oracle_and_single_calls():
+    """dp_grad_sample_layernorm_many: 16-byte and element-load layers, a
+    partial last chunk, one-chunk layers (squared norm written directly), no
+    positions, a layer without sqnorm; against the oracle and the
+    single-layer call."""
+    r = np.random.default_rng(17)
+    for dtype, shapes in ((torch.bfloat16, [(37, 771), (41, 1028), (128, 768), (0, 64), (5, 40), (33, 8)]),
+                          (torch.float32, [(37, 771), (41, 1028), (200, 100), (3, 32)])):
+        N = 5
+        dt = dp.DP_BF16 if dtype == torch.bfloat16 else dp.DP_F32
+        say("layernorm many", dtype)
+        ents, outs, ins = [], [], []
+        for k, (T, D) in enumerate(shapes):
+            xh = torch.from_numpy(r.standard_normal((N, T, D)).astype(np.float32)).to(dtype).to(DEV)
+            B = torch.from_numpy(r.standard_normal((N, T, D)).astype(np.float32)).to(dtype).to(DEV)
+            g = torch.full((N, D), 7.0, device=DEV)
+            b = torch.full((N, D), 7.0, device=DEV)
+            sq = None if k == 1 else torch.full((N,), 7.0, device=DEV)
+            ents.append((xh, B, T, D, 1.5, g, b, sq))
+            outs.append((g, b, sq))
+            ins.append((xh, B, T, D))
+        items = dp.make_layernorm_layers(ents)
+        ws = torch.empty(max(dp.dp_grad_sample_layernorm_many_workspace_bytes(items, len(ents), N, dt), 1),
+                         dtype=torch.uint8, device=DEV)
+        dp.dp_grad_sample_layernorm_many(items, len(ents), dt, N, None, ws)
+        torch.cuda.synchronize()
+        for (xh, B, T, D), (g, b, sq) in zip(ins, outs):
+            rg, rb = oracle.layernorm_grad(xh.float().cpu().numpy().astype(np.float64),
+                                           B.float().cpu().numpy().astype(np.float64), 1.5)
+            assert_g12(g.cpu().numpy(), rg, 1e-4, "ggamma many T=%d D=%d" % (T, D))
+            assert_g12(b.cpu().numpy(), rb, 1e-4, "gbeta many T=%d D=%d" % (T, D))
+            if sq is not None:
+                assert_rel(sq.cpu().numpy(), (rg ** 2).sum(1) + (rb ** 2).sum(1), 1e-4, "ln many sqnorm")
+            g1 = torch.empty((N, D), device=DEV); b1 = torch.empty((N, D), device=DEV)
+            ws1 = torch.empty(max(dp.dp_grad_sample_layernorm_workspace_bytes(N, T, D), 1), dtype=torch.uint8,
+                              device=DEV)
+            dp.dp_grad_sample_layernorm(xh, B, dt, N, T, D, 1.5, g1, b1, None, None, ws1)
+            torch.cuda.synchronize()
+            assert_g12(g.cpu().numpy(), g1.cpu().numpy(), 1e-5, "many vs single")
+            assert_g12(b.cpu().numpy(), b1.cpu().numpy(), 1e-5, "many vs single")
+
+
 def test_nonfinite_sample_poisons_instead_of_passing():
     wl = W.get("linear_tiny")
     inputs = W.make_inputs(wl, n=8)
