@@ -36,7 +36,9 @@
  *    int32, zeroed by the caller; may be NULL to ignore them):
  *    DP_FLAG_BAD_INDEX (a token id outside [0, V)), DP_FLAG_NONFINITE (a
  *    per-sample norm that is NaN or infinite), DP_FLAG_CAP (CSR capacity
- *    exceeded).  The caller reads the word after its own synchronization.
+ *    exceeded), DP_FLAG_WAIT (a bounded wait of one workgroup for another
+ *    ran out: an internal error, the outputs are not to be trusted).  The
+ *    caller reads the word after its own synchronization.
  *  - Results are deterministic: no floating-point atomics, every reduction
  *    has a fixed order, so the same inputs give the same bits run to run.
  *  - Entry points are stateless and re-entrant; calls on different streams
@@ -71,7 +73,8 @@ typedef enum dp_dtype { DP_F32 = 0, DP_BF16 = 1 } dp_dtype;
 enum {
     DP_FLAG_BAD_INDEX = 1,
     DP_FLAG_NONFINITE = 2,
-    DP_FLAG_CAP = 4
+    DP_FLAG_CAP = 4,
+    DP_FLAG_WAIT = 8
 };
 
 /* Human-readable text for a status code (static storage; never NULL). */

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(PKG, "libdpgrad.so")
 
 DP_OK, DP_EINVAL, DP_EDTYPE, DP_EUNSUPPORTED, DP_ECAP, DP_EHIP = range(6)
 DP_F32, DP_BF16 = 0, 1
-DP_FLAG_BAD_INDEX, DP_FLAG_NONFINITE, DP_FLAG_CAP = 1, 2, 4
+DP_FLAG_BAD_INDEX, DP_FLAG_NONFINITE, DP_FLAG_CAP, DP_FLAG_WAIT = 1, 2, 4, 8
 
 # (name, restype, argtypes) of every exported entry point
 _P = ctypes.c_void_p

@@ -271,6 +271,122 @@ constexpr int kBatch = 16;    // positions whose row loads a wave has in flight 
 // or the middle of one that covers the whole range (mid)
 enum { kHead = 0, kTail = 1, kMid = 2 };
 
+// The walk of the sorted positions [lo, hi) by WAVES waves: wave wv takes a
+// contiguous share, adds each segment's rows in ascending t (rows of Bn, the
+// sample's backprops) and writes s * sum as CSR row base + segment; a segment
+// that crosses waves is finished by the wave where it starts, which adds the
+// following waves' pieces in wave order.  sq accumulates the squares of the
+// rows this thread wrote.  Every thread of the workgroup calls it (it holds
+// workgroup barriers).
+template <typename T, int VEC, int WAVES>
+__device__ __forceinline__ void walk_rows(const T *__restrict__ Bn, i64 D, float scale,
+                                          const int32_t *perm, const int32_t *sidx, int P, int lo, int hi,
+                                          i64 base, float *__restrict__ rows, i64 cap,
+                                          float (*piece)[3][64 * VEC], int (*pseg)[3], int wv, int lane, float &sq)
+{
+    constexpr int CB = 64 * VEC;                         // columns per column block
+    const int R = (hi - lo + WAVES - 1) / WAVES;       // sorted positions per wave
+    const int r_lo = lo + wv * R < hi ? lo + wv * R : hi;
+    const int r_hi = r_lo + R < hi ? r_lo + R : hi;
+    // does the wave's first segment start before its range, its last continue after it?
+    const bool first_cont = r_lo < r_hi && r_lo > lo && sidx[r_lo - 1] == sidx[r_lo];
+    const bool last_cont = r_lo < r_hi && r_hi < hi && sidx[r_hi] == sidx[r_hi - 1];
+
+    auto finish = [&](i64 s, const float (&acc)[VEC], i64 c, bool on) {
+        const i64 k = base + s;
+        if (on) {
+            float gr[VEC];
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) {
+                gr[i] = scale * acc[i];
+                sq += gr[i] * gr[i];
+            }
+            if (k < cap) {
+                if constexpr (VEC == 4)
+                    *reinterpret_cast<float4 *>(rows + k * D + c) = make_float4(gr[0], gr[1], gr[2], gr[3]);
+                else
+                    rows[k * D + c] = gr[0];
+            }
+        }
+    };
+
+    for (i64 c0c = 0; c0c < D; c0c += CB) {
+        const i64 c = c0c + (i64)VEC * lane;
+        const bool on = c < D;
+        const i64 cc = on ? c : 0;
+        float acc[VEC];
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) acc[i] = 0.0f;
+        bool started_here = !first_cont;
+        if (lane < 3) pseg[wv][lane] = -1;
+        for (int r0 = r_lo; r0 < r_hi; r0 += kBatch) {
+            // lane l (and l + 16, l + 32, l + 48) holds position r0 + l of the
+            // batch: its t, its segment, whether the segment ends there
+            const int rl = r0 + (lane & (kBatch - 1));
+            const bool in = rl < r_hi;
+            const int tl = perm[in ? rl : r0];
+            const int sl = sidx[in ? rl : r0];
+            const bool ends = in && (rl + 1 == P || sidx[rl + 1] != sl);
+            const uint32_t endm = (uint32_t)__ballot(ends);
+            float v[kBatch][VEC];
+#pragma unroll
+            for (int j = 0; j < kBatch; ++j) {
+                const int t = __builtin_amdgcn_readlane(tl, j);
+                load_vec<T, VEC>(Bn + (i64)t * D + cc, v[j]);
+            }
+            // (fully unrolled with a uniform guard instead of a break, so
+            // that v stays in registers)
+#pragma unroll
+            for (int j = 0; j < kBatch; ++j) {
+                if (r0 + j >= r_hi) continue;
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) acc[i] += v[j][i];
+                if ((endm >> j) & 1u) {
+                    const int s = __builtin_amdgcn_readlane(sl, j);
+                    if (started_here) {
+                        finish(s, acc, c, on);
+                    } else {
+                        // the end of a segment from an earlier wave
+#pragma unroll
+                        for (int i = 0; i < VEC; ++i) piece[wv][kHead][VEC * lane + i] = acc[i];
+                        if (lane == 0) pseg[wv][kHead] = s;
+                    }
+#pragma unroll
+                    for (int i = 0; i < VEC; ++i) acc[i] = 0.0f;
+                    started_here = true;
+                }
+            }
+        }
+        if (last_cont) {
+            const int kind = started_here ? kTail : kMid;
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) piece[wv][kind][VEC * lane + i] = acc[i];
+            if (lane == 0) pseg[wv][kind] = sidx[r_hi - 1];
+        }
+        lds_barrier();
+        // a segment that starts in this wave and continues: add the following
+        // waves' pieces in wave order, then write it
+        if (pseg[wv][kTail] >= 0) {
+            const int s = pseg[wv][kTail];
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) acc[i] = piece[wv][kTail][VEC * lane + i];
+            for (int x = wv + 1; x < WAVES; ++x) {
+                if (pseg[x][kMid] == s) {
+#pragma unroll
+                    for (int i = 0; i < VEC; ++i) acc[i] += piece[x][kMid][VEC * lane + i];
+                } else {
+#pragma unroll
+                    for (int i = 0; i < VEC; ++i) acc[i] += piece[x][kHead][VEC * lane + i];
+                    break;
+                }
+            }
+            finish(s, acc, c, on);
+        }
+        lds_barrier();                                   // the pieces are rewritten by the next block
+    }
+
+}
+
 template <typename T, int VEC>
 __global__ __launch_bounds__(kCsrThreads) void emb_csr_kernel(
     const T *__restrict__ B, i64 Tn, i64 D, float scale, EmbWs w, int G, int prefix_here,
@@ -362,106 +478,8 @@ __global__ __launch_bounds__(kCsrThreads) void emb_csr_kernel(
     }
 
     const T *Bn = B + n * Tn * D;
-    const int R = (hi - lo + kCsrWaves - 1) / kCsrWaves;       // sorted positions per wave
-    const int r_lo = lo + wv * R < hi ? lo + wv * R : hi;
-    const int r_hi = r_lo + R < hi ? r_lo + R : hi;
-    // does the wave's first segment start before its range, its last continue after it?
-    const bool first_cont = r_lo < r_hi && r_lo > lo && sidx[r_lo - 1] == sidx[r_lo];
-    const bool last_cont = r_lo < r_hi && r_hi < hi && sidx[r_hi] == sidx[r_hi - 1];
     float sq = 0.0f;
-
-    auto finish = [&](i64 s, const float (&acc)[VEC], i64 c, bool on) {
-        const i64 k = base + s;
-        if (on) {
-            float gr[VEC];
-#pragma unroll
-            for (int i = 0; i < VEC; ++i) {
-                gr[i] = scale * acc[i];
-                sq += gr[i] * gr[i];
-            }
-            if (k < cap) {
-                if constexpr (VEC == 4)
-                    *reinterpret_cast<float4 *>(rows + k * D + c) = make_float4(gr[0], gr[1], gr[2], gr[3]);
-                else
-                    rows[k * D + c] = gr[0];
-            }
-        }
-    };
-
-    for (i64 c0c = 0; c0c < D; c0c += CB) {
-        const i64 c = c0c + (i64)VEC * lane;
-        const bool on = c < D;
-        const i64 cc = on ? c : 0;
-        float acc[VEC];
-#pragma unroll
-        for (int i = 0; i < VEC; ++i) acc[i] = 0.0f;
-        bool started_here = !first_cont;
-        if (lane < 3) pseg[wv][lane] = -1;
-        for (int r0 = r_lo; r0 < r_hi; r0 += kBatch) {
-            // lane l (and l + 16, l + 32, l + 48) holds position r0 + l of the
-            // batch: its t, its segment, whether the segment ends there
-            const int rl = r0 + (lane & (kBatch - 1));
-            const bool in = rl < r_hi;
-            const int tl = perm[in ? rl : r0];
-            const int sl = sidx[in ? rl : r0];
-            const bool ends = in && (rl + 1 == P || sidx[rl + 1] != sl);
-            const uint32_t endm = (uint32_t)__ballot(ends);
-            float v[kBatch][VEC];
-#pragma unroll
-            for (int j = 0; j < kBatch; ++j) {
-                const int t = __builtin_amdgcn_readlane(tl, j);
-                load_vec<T, VEC>(Bn + (i64)t * D + cc, v[j]);
-            }
-            // (fully unrolled with a uniform guard instead of a break, so
-            // that v stays in registers)
-#pragma unroll
-            for (int j = 0; j < kBatch; ++j) {
-                if (r0 + j >= r_hi) continue;
-#pragma unroll
-                for (int i = 0; i < VEC; ++i) acc[i] += v[j][i];
-                if ((endm >> j) & 1u) {
-                    const int s = __builtin_amdgcn_readlane(sl, j);
-                    if (started_here) {
-                        finish(s, acc, c, on);
-                    } else {
-                        // the end of a segment from an earlier wave
-#pragma unroll
-                        for (int i = 0; i < VEC; ++i) piece[wv][kHead][VEC * lane + i] = acc[i];
-                        if (lane == 0) pseg[wv][kHead] = s;
-                    }
-#pragma unroll
-                    for (int i = 0; i < VEC; ++i) acc[i] = 0.0f;
-                    started_here = true;
-                }
-            }
-        }
-        if (last_cont) {
-            const int kind = started_here ? kTail : kMid;
-#pragma unroll
-            for (int i = 0; i < VEC; ++i) piece[wv][kind][VEC * lane + i] = acc[i];
-            if (lane == 0) pseg[wv][kind] = sidx[r_hi - 1];
-        }
-        lds_barrier();
-        // a segment that starts in this wave and continues: add the following
-        // waves' pieces in wave order, then write it
-        if (pseg[wv][kTail] >= 0) {
-            const int s = pseg[wv][kTail];
-#pragma unroll
-            for (int i = 0; i < VEC; ++i) acc[i] = piece[wv][kTail][VEC * lane + i];
-            for (int x = wv + 1; x < kCsrWaves; ++x) {
-                if (pseg[x][kMid] == s) {
-#pragma unroll
-                    for (int i = 0; i < VEC; ++i) acc[i] += piece[x][kMid][VEC * lane + i];
-                } else {
-#pragma unroll
-                    for (int i = 0; i < VEC; ++i) acc[i] += piece[x][kHead][VEC * lane + i];
-                    break;
-                }
-            }
-            finish(s, acc, c, on);
-        }
-        lds_barrier();                                   // the pieces are rewritten by the next block
-    }
+    walk_rows<T, VEC, kCsrWaves>(Bn, D, scale, perm, sidx, P, lo, hi, base, rows, cap, piece, pseg, wv, lane, sq);
 
     // the ids of the segments the workgroup owns and the sample's CSR bound,
     // stored last (a store issued before the walk would make the walk's first
@@ -503,6 +521,154 @@ __global__ __launch_bounds__(kCsrThreads) void emb_csr_kernel(
     for (int x = 0; x < G; ++x)
         tot += __hip_atomic_load(w.sqpart + n * kMaxSplit + x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     sqnorm[n] = tot;
+}
+
+// ---------------------------------------------------------------------------
+// One launch for T <= 512 (after a fill that clears the ticket and the
+// per-sample states): one workgroup of 16 waves per sample sorts, walks and
+// writes the sample's CSR block.  The sample's first CSR row (the distinct
+// counts of the samples before it) comes from a decoupled look-back: each
+// workgroup publishes its distinct count as soon as its sort is done, then
+// adds its predecessors' published values, 64 at a time, back to the nearest
+// one that already holds its inclusive prefix, and publishes its own
+// inclusive prefix.  Samples are taken in ticket order (an atomic counter),
+// so a workgroup only waits for samples whose workgroups already run; the
+// wait is bounded (past the bound it sets DP_FLAG_WAIT and counts the
+// missing sample as empty).  The sums are those of the two-launch path's
+// walk over 16 waves: same segments, same ascending-t order within a piece.
+// ---------------------------------------------------------------------------
+constexpr int kFusedWaves = 16;
+constexpr int kFusedThreads = 64 * kFusedWaves;
+constexpr uint64_t kAgg = 1ull << 62;          // state: the sample's distinct count
+constexpr uint64_t kIncl = 2ull << 62;         // state: its inclusive prefix
+constexpr uint64_t kStateVal = (1ull << 62) - 1;
+constexpr int kSpinMax = 1 << 20;
+
+template <typename T, int VEC>
+__global__ __launch_bounds__(kFusedThreads) void emb_fused_kernel(
+    const int64_t *__restrict__ ids, const T *__restrict__ B, i64 Tn, i64 V, i64 D, float scale,
+    int32_t *__restrict__ ticket, uint64_t *__restrict__ state, int64_t *__restrict__ row_ptr,
+    int64_t *__restrict__ uniq, float *__restrict__ rows, i64 cap, float *__restrict__ sqnorm, int32_t *status)
+{
+    constexpr int CB = 64 * VEC;
+    extern __shared__ uint64_t keys[];           // keys [T], sorted [T], 32-bit keys [T], perm, sidx, segid [T] each
+    __shared__ float piece[kFusedWaves][3][CB];
+    __shared__ int pseg[kFusedWaves][3];
+    __shared__ float wsq[kFusedWaves];
+    __shared__ int wsum[kFusedWaves];
+    __shared__ int s_n;
+    __shared__ int64_t s_base;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+    if (tid == 0) s_n = __hip_atomic_fetch_add(ticket, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();
+    const i64 n = s_n;
+    const int Tp = (int)Tn;
+    const int64_t *idn = ids + n * Tn;
+    uint64_t *sorted = keys + Tp;
+    uint32_t *k32 = reinterpret_cast<uint32_t *>(keys + 2 * Tp);
+    int32_t *perm = reinterpret_cast<int32_t *>(k32 + Tp);
+    int32_t *sidx = perm + Tp;
+    int32_t *segid = sidx + Tp;
+
+    // the keys (id, t), unique; 32-bit when they fit; an invalid id sorts last
+    const bool small = (uint64_t)(V + 1) * (uint64_t)Tn <= 0xffffffffull;
+    bool bad = false;
+    for (int i = tid; i < Tp; i += kFusedThreads) {
+        const int64_t id = idn[i];
+        const bool ok = id >= 0 && id < V;
+        bad |= !ok;
+        keys[i] = ((uint64_t)(ok ? (uint32_t)id : kInvalidHi) << 32) | (uint32_t)i;
+        if (small) k32[i] = (uint32_t)((ok ? id : V) * Tn + i);
+    }
+    if (bad) raise_flag(status, DP_FLAG_BAD_INDEX);
+    lds_barrier();
+    if (small) rank_scatter<uint32_t>(k32, keys, sorted, Tp, tid);
+    else rank_scatter<uint64_t>(keys, keys, sorted, Tp, tid);
+    lds_barrier();
+    // heads of new ids and valid positions per thread (at most one position
+    // each here), scanned over the workgroup
+    int cnt = 0;
+    if (tid < Tp) {
+        const uint32_t hi = (uint32_t)(sorted[tid] >> 32);
+        if (hi != kInvalidHi) {
+            cnt = 1 << 16;
+            if (tid == 0 || (uint32_t)(sorted[tid - 1] >> 32) != hi) ++cnt;
+        }
+    }
+    int tot;
+    const int sx = (block_exclusive_scan(cnt, wsum, tot) & 0xffff) - 1;
+    if (tid < Tp) {
+        const uint64_t k = sorted[tid];
+        const uint32_t hi = (uint32_t)(k >> 32);
+        if (hi != kInvalidHi) {
+            const bool head = tid == 0 || (uint32_t)(sorted[tid - 1] >> 32) != hi;
+            const int s = head ? sx + 1 : sx;
+            if (head) segid[s] = (int32_t)hi;
+            perm[tid] = (int32_t)(k & 0xffffffffu);
+            sidx[tid] = s;
+        }
+    }
+    const int u = tot & 0xffff, P = tot >> 16;
+
+    // the first CSR row of the sample
+    if (wv == 0) {
+        if (lane == 0)
+            __hip_atomic_store(state + n, (n == 0 ? kIncl : kAgg) | (uint64_t)u, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        int64_t excl = 0;
+        bool timed_out = false;
+        for (i64 j = n - 1; j >= 0; j -= kWave) {
+            const i64 jj = j - lane;
+            uint64_t v = kIncl;                        // lanes past sample 0 add nothing
+            if (jj >= 0) {
+                int spins = 0;
+                v = __hip_atomic_load(state + jj, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                while ((v >> 62) == 0 && spins < kSpinMax) {
+                    __builtin_amdgcn_s_sleep(1);
+                    v = __hip_atomic_load(state + jj, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    ++spins;
+                }
+                timed_out |= (v >> 62) == 0;
+            }
+            // the nearest predecessor holding an inclusive prefix ends the look-back
+            const uint64_t incl = __ballot(jj >= 0 && (v >> 62) == 2);
+            const int stop = incl ? __ffsll((unsigned long long)incl) - 1 : kWave;
+            int64_t x = (jj >= 0 && lane <= stop) ? (int64_t)(v & kStateVal) : 0;
+            for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off, kWave);
+            excl += x;
+            if (incl) break;
+        }
+        if (__ballot(timed_out) && lane == 0) raise_flag(status, DP_FLAG_WAIT);
+        if (lane == 0) {
+            if (n > 0)
+                __hip_atomic_store(state + n, kIncl | (uint64_t)(excl + u), __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+            s_base = excl;
+        }
+    }
+    __syncthreads();
+    const i64 base = s_base;
+
+    float sq = 0.0f;
+    walk_rows<T, VEC, kFusedWaves>(B + n * Tn * D, D, scale, perm, sidx, P, 0, P, base, rows, cap, piece, pseg,
+                                   wv, lane, sq);
+    for (int s = tid; s < u; s += kFusedThreads)
+        if (base + s < cap) uniq[base + s] = segid[s];
+    if (tid == 0) {
+        row_ptr[n + 1] = base + u;
+        if (n == 0) row_ptr[0] = 0;
+        if (base + u > cap) raise_flag(status, DP_FLAG_CAP);
+    }
+    if (!sqnorm) return;
+    sq = wave_sum(sq);
+    if (lane == 0) wsq[wv] = sq;
+    lds_barrier();
+    if (tid == 0) {
+        float t = 0.0f;
+        for (int i = 0; i < kFusedWaves; ++i) t += wsq[i];
+        sqnorm[n] = t;
+    }
 }
 
 EmbWs carve(void *ws, i64 N, i64 T)
@@ -560,6 +726,34 @@ extern "C" dp_status dp_grad_sample_embedding(const int64_t *ids, const void *B,
         emb_scan_kernel<<<1, 256, 0, stream>>>(nullptr, 0, row_ptr);
         return launch_status();
     }
+    // four columns per lane when every row starts on a 16-byte (fp32) or
+    // 8-byte (bf16) boundary, and rows likewise
+    const bool vec = D % 4 == 0 && aligned(rows, 16) && aligned(B, dt == DP_F32 ? 16 : 8);
+    if (T > 0 && T <= kRankMaxT) {
+        // one launch after clearing the ticket and the N per-sample states
+        int32_t *ticket = (int32_t *)ws;
+        uint64_t *state = (uint64_t *)((char *)ws + 256);
+        zero_fill((float *)ws, (i64)((256 + 8 * (size_t)N) / 4), stream);
+        const size_t flds = 32 * (size_t)T;
+        if (dt == DP_F32) {
+            if (vec)
+                emb_fused_kernel<float, 4><<<(unsigned)N, kFusedThreads, flds, stream>>>(
+                    ids, (const float *)B, T, V, D, scale, ticket, state, row_ptr, uniq_ids, rows, cap, sqnorm, status);
+            else
+                emb_fused_kernel<float, 1><<<(unsigned)N, kFusedThreads, flds, stream>>>(
+                    ids, (const float *)B, T, V, D, scale, ticket, state, row_ptr, uniq_ids, rows, cap, sqnorm, status);
+        } else {
+            if (vec)
+                emb_fused_kernel<uint16_t, 4><<<(unsigned)N, kFusedThreads, flds, stream>>>(
+                    ids, (const uint16_t *)B, T, V, D, scale, ticket, state, row_ptr, uniq_ids, rows, cap, sqnorm,
+                    status);
+            else
+                emb_fused_kernel<uint16_t, 1><<<(unsigned)N, kFusedThreads, flds, stream>>>(
+                    ids, (const uint16_t *)B, T, V, D, scale, ticket, state, row_ptr, uniq_ids, rows, cap, sqnorm,
+                    status);
+        }
+        return launch_status();
+    }
     EmbWs w = carve(ws, N, T);
     int P2 = 1;
     while (P2 < T) P2 <<= 1;
@@ -568,9 +762,6 @@ extern "C" dp_status dp_grad_sample_embedding(const int64_t *ids, const void *B,
     emb_sort_kernel<<<(unsigned)N, kSortThreads, lds, stream>>>(ids, T, V, P2, w, status);
     const int prefix_here = N <= kPrefixMaxN ? 1 : 0;
     if (!prefix_here) emb_scan_kernel<<<1, 256, 0, stream>>>(w.counts, N, row_ptr);
-    // four columns per lane when every row starts on a 16-byte (fp32) or
-    // 8-byte (bf16) boundary, and rows likewise
-    const bool vec = D % 4 == 0 && aligned(rows, 16) && aligned(B, dt == DP_F32 ? 16 : 8);
     const int G = split_for(T);
     const unsigned grid = (unsigned)(N * G);
     const size_t olds = 3 * sizeof(int32_t) * (size_t)(T > 0 ? T : 1);

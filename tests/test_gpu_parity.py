@@ -544,10 +544,27 @@ def test_embedding_cases(case, D):
     assert_g12(S.cpu().numpy(), oracle.clip_sum_embedding(rrp, ruq, rrows, c, V), 1e-4, "dense S")
 
 
-def test_embedding_flags():
+def test_embedding_two_pass_scan():
+    """T > 512 takes the two-launch path; with N > 2048 it adds the distinct
+    counts in a scan launch of its own."""
+    r = np.random.default_rng(14)
+    V, D = 1000, 4
+    ids = (np.minimum(r.zipf(1.3, (2100, 520)), V) - 1).astype(np.int64)
+    B = r.standard_normal(ids.shape + (D,))
+    say("embedding two-pass scan")
+    rp, uq, rows, sq, st = run_embedding(ids, B, V, scale=0.5)
+    rrp, ruq, rrows = oracle.embedding_grad(ids, B.astype(np.float32).astype(np.float64), V, 0.5)
+    assert st == 0
+    np.testing.assert_array_equal(rp, rrp)
+    np.testing.assert_array_equal(uq[:rp[-1]], ruq)
+    assert_g12(rows[:rp[-1]], rrows, 1e-4, "rows")
+
+
+@pytest.mark.parametrize("T", [20, 600])
+def test_embedding_flags(T):
     r = np.random.default_rng(12)
-    ids = r.integers(0, 50, (3, 20)).astype(np.int64)
-    B = r.standard_normal((3, 20, 4))
+    ids = r.integers(0, 50, (3, T)).astype(np.int64)
+    B = r.standard_normal((3, T, 4))
     # capacity too small: flagged, true counts kept, nothing written past cap
     say("embedding cap")
     rp, uq, rows, sq, st = run_embedding(ids, B, 50, cap=10)
