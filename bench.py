@@ -122,7 +122,7 @@ def call_costs(st, nnz=None):
             u = (nnz or {}).get(L.name, N * L.T)
             # reads ids and backprops; writes row_ptr, the distinct ids, their rows and the squared norms
             out["grad:" + L.name] = (N * L.T * (8 + L.D * e) + (N + 1) * 8 + u * (L.D * 4 + 8) + N * 4,
-                                     N * L.T * L.D, "emb_csr_kernel", None)
+                                     N * L.T * L.D, "emb_fused_kernel" if L.T <= 512 else "emb_csr_kernel", None)
             # reads row_ptr, the ids, the rows and the norms; writes the dense [V][D] sum
             out["clip:" + L.name] = ((N + 1) * 8 + u * (L.D * 4 + 8) + N * 4 + L.V * L.D * 4, 2 * u * L.D,
                                      "emb_clipsum_kernel", None)
@@ -199,6 +199,7 @@ KERNEL_SOURCES = {
     "conv_per_sample_kernel": ["paper_2109_12298_amd/csrc/conv2d.hip", "paper_2109_12298_amd/csrc/mfma_tile.hpp"],
     "colsum_kernel": ["paper_2109_12298_amd/csrc/clip.hip"],
     "emb_csr_kernel": ["paper_2109_12298_amd/csrc/embedding.hip"],
+    "emb_fused_kernel": ["paper_2109_12298_amd/csrc/embedding.hip"],
     "emb_clipsum_kernel": ["paper_2109_12298_amd/csrc/clip.hip"],
     "ln_partial_kernel": ["paper_2109_12298_amd/csrc/layernorm.hip"],
     "ln_rows_kernel": ["paper_2109_12298_amd/csrc/layernorm.hip"],
