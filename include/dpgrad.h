@@ -236,7 +236,13 @@ dp_status dp_grad_sample_many(const dp_layer_grad *items, int32_t count, dp_dtyp
  * suffices; a smaller cap that the data overflows sets DP_FLAG_CAP, row_ptr
  * still holds the true counts and rows past cap are not written.  An id
  * outside [0, V) sets DP_FLAG_BAD_INDEX and its position is left out.
- * Needs T <= 4096 and N*T < 2^31 (else DP_EUNSUPPORTED) and V < 2^31. */
+ * Needs T <= 4096 and N*T < 2^31 (else DP_EUNSUPPORTED) and V < 2^31.
+ * For T <= 512 the call is one kernel (after a small clearing launch): a
+ * workgroup per sample, each taking its first CSR row from the distinct
+ * counts that the earlier samples' workgroups publish (a bounded wait; past
+ * the bound DP_FLAG_WAIT is raised and the result is not to be trusted).
+ * Workspace: dp_grad_sample_embedding_workspace_bytes(N, T) bytes, contents
+ * arbitrary on entry. */
 size_t dp_grad_sample_embedding_workspace_bytes(int64_t N, int64_t T);
 dp_status dp_grad_sample_embedding(const int64_t *ids, const void *B, dp_dtype dt, int64_t N,
                                    int64_t T, int64_t V, int64_t D, float scale,
