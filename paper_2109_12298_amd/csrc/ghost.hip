@@ -144,7 +144,7 @@ __device__ __forceinline__ void mma_chunk(const uint4 &a, const uint4 &b, f32x16
 }
 
 // Weight of 32 x 32 block b = 2 x + y of a pair's tiles in the pair's value:
-// a diagonal pair (bi = bj) skips block (1, 0), the transpose of (0, 1)
+// a diagonal pair (bi = bj) leaves out block (1, 0), the transpose of (0, 1)
 // (both Grams are symmetric), and counts (0, 1) twice.
 __host__ __device__ __forceinline__ float block_weight(int b, bool diag)
 {
