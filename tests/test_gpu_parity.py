@@ -788,6 +788,33 @@ def test_graph_replay_matches_eager_steps():
     assert int(st.step_dev.item()) == 7     # the counter holds the last replayed step
 
 
+@pytest.mark.parametrize("name,n,mode", [("text_lstm", 8, "materialize"), ("transformer_block", 4, "materialize"),
+                                         ("transformer_block", 4, "ghost")])
+def test_grouped_calls_replay_like_eager(name, n, mode):
+    """Graph replays of the steps whose calls keep state between launches of
+    one call (the embedding's ticket and per-sample states, cleared by a fill
+    kernel) or group layers (LayerNorm, ghost norms): every replay, with eager
+    work in between, equals the eager step bit for bit."""
+    wl = W.get(name)
+    inputs = W.make_inputs(wl, n=n)
+    clip = "fused" if mode == "ghost" else "auto"          # ghost norms need the fused clipped sum
+    st = DPStep(wl, inputs, DEV, clip_mode=clip, norm_mode=mode)
+    if mode == "ghost":
+        assert st.ghost
+    say("graph capture", name, mode)
+    st.capture(first_step=3)
+    eager = DPStep(wl, inputs, DEV, clip_mode=clip, norm_mode=mode)
+    for k in range(3):
+        st.replay()
+        got = st.results()
+        eager.run(step=3 + k)
+        ref = eager.results()
+        np.testing.assert_array_equal(got["norm"], ref["norm"], err_msg="replay %d norm" % k)
+        for key in ref["out"]:
+            np.testing.assert_array_equal(got["out"][key], ref["out"][key], err_msg="replay %d %s" % (k, key))
+    assert int(st.status.item()) == 0
+
+
 @pytest.mark.parametrize("parallel", [False, True])
 def test_graph_with_several_steps_per_replay(parallel):
     """A graph holding three steps: each replay runs steps s, s+1, s+2 (each
