@@ -186,3 +186,25 @@ def test_ghost_norm_many_transformer_full_size_sampled():
         assert_rel(g[picks], oracle_sq(A, B, 1.0, bias, samples=picks), 1e-4, "layer %d sampled" % k)
         alone = ghost(A, B, dp.DP_BF16, N, T, din, dout, 1.0, bias)
         assert_rel(g, alone, 1e-5, "layer %d vs alone" % k)
+
+
+def test_ghost_norm_many_more_layers_than_one_launch_table():
+    """18 layers: the Gram launch, the pair sums and (few units) the chunk
+    combine each run as two launches of up to 16 layers; every layer against
+    its own single call."""
+    N = 2
+    say("ghost many, 18 layers")
+    rng = np.random.default_rng(21)
+    layers = []
+    for k in range(18):
+        T, din, dout = 64 + 17 * (k % 3), 16 + 8 * (k % 5), 24 + 8 * (k % 4)
+        A, B = inputs(rng, N, T, din, dout, "bf16")
+        layers.append((A, B, T, din, dout, k % 2 == 0))
+    got = ghost_many(layers, dp.DP_BF16, N)
+    for (A, B, T, din, dout, bias), g in zip(layers, got):
+        alone = ghost(A, B, dp.DP_BF16, N, T, din, dout, 0.9, bias)
+        assert_rel(g, alone, 1e-5, "18 layers T=%d %dx%d" % (T, din, dout))
+    picks = [0, 17]
+    for k in picks:
+        A, B, T, din, dout, bias = layers[k]
+        assert_rel(got[k], oracle_sq(A, B, 0.9, bias), 1e-4, "18 layers oracle %d" % k)

@@ -706,6 +706,34 @@ def test_layernorm_many_matches_oracle_and_single_calls():
             assert_g12(b.cpu().numpy(), b1.cpu().numpy(), 1e-5, "many vs single")
 
 
+def test_layernorm_many_more_layers_than_one_launch_table():
+    """18 LayerNorm layers (two launches of up to 16), against single calls."""
+    r = np.random.default_rng(18)
+    N = 3
+    say("layernorm many, 18 layers")
+    ents, outs, ins = [], [], []
+    for k in range(18):
+        T, D = 5 + 7 * (k % 4), 64 * (1 + k % 3) + (4 if k % 5 == 0 else 0)
+        xh = torch.from_numpy(r.standard_normal((N, T, D)).astype(np.float32)).to(DEV)
+        B = torch.from_numpy(r.standard_normal((N, T, D)).astype(np.float32)).to(DEV)
+        g = torch.empty((N, D), device=DEV); b = torch.empty((N, D), device=DEV); sq = torch.empty(N, device=DEV)
+        ents.append((xh, B, T, D, 0.7, g, b, sq)); outs.append((g, b, sq)); ins.append((xh, B, T, D))
+    items = dp.make_layernorm_layers(ents)
+    ws = torch.empty(max(dp.dp_grad_sample_layernorm_many_workspace_bytes(items, 18, N, dp.DP_F32), 1),
+                     dtype=torch.uint8, device=DEV)
+    dp.dp_grad_sample_layernorm_many(items, 18, dp.DP_F32, N, None, ws)
+    torch.cuda.synchronize()
+    for (xh, B, T, D), (g, b, sq) in zip(ins, outs):
+        g1 = torch.empty((N, D), device=DEV); b1 = torch.empty((N, D), device=DEV); sq1 = torch.empty(N, device=DEV)
+        ws1 = torch.empty(max(dp.dp_grad_sample_layernorm_workspace_bytes(N, T, D), 1), dtype=torch.uint8,
+                          device=DEV)
+        dp.dp_grad_sample_layernorm(xh, B, dp.DP_F32, N, T, D, 0.7, g1, b1, sq1, None, ws1)
+        torch.cuda.synchronize()
+        assert_g12(g.cpu().numpy(), g1.cpu().numpy(), 1e-5, "18 layers ggamma")
+        assert_g12(b.cpu().numpy(), b1.cpu().numpy(), 1e-5, "18 layers gbeta")
+        assert_rel(sq.cpu().numpy(), sq1.cpu().numpy(), 1e-5, "18 layers sqnorm")
+
+
 def test_nonfinite_sample_poisons_instead_of_passing():
     wl = W.get("linear_tiny")
     inputs = W.make_inputs(wl, n=8)
