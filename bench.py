@@ -506,6 +506,7 @@ def main():
         raise SystemExit("--steps must be a multiple of --steps-per-replay")
     if not args.eager:
         st.capture(first_step=0, steps_per_replay=r)
+        r = st.steps_per_replay          # one when graph branches were the faster
     for i in range(max(args.warmup // r, 1) if not args.eager else args.warmup):
         st.replay() if not args.eager else eager_step(i)
     torch.cuda.synchronize()

@@ -535,28 +535,37 @@ class DPStep:
         or one chain (False); None captures both, times a few replays of
         each and keeps the faster (branches pay off when the layers' kernels
         are long enough to overlap; for short kernels the single chain has
-        less scheduling overhead).
+        less scheduling overhead).  Branches are supported with one step per
+        replay only (a branch graph of two transformer-block steps ended the
+        process inside the graph launch, cause not found): True with
+        steps_per_replay > 1 raises ValueError, and None compares the chain
+        at steps_per_replay with branches at one step per replay.
         steps_per_replay: whole steps recorded back to back in the graph, so
         that one replay launch covers several steps (each still a full pass
         over the batch, with its own step number)."""
         torch = _torch()
+        if parallel is True and steps_per_replay > 1:
+            raise ValueError("graph branches are supported with one step per replay only")
         if parallel is None:
+            # the chain at steps_per_replay steps per replay against branches
+            # at one, per step; the faster is kept (with branches the graph
+            # then holds one step, and self.steps_per_replay says so)
             import time
-            best = None
-            for par in (True, False):
-                self.capture(first_step, par)
-                for _ in range(5):
+
+            def per_step(par, r):
+                self.capture(first_step, par, r)
+                for _ in range(3):
                     self.replay()
                 torch.cuda.synchronize(self.device)
+                n = max(40 // r, 4)
                 t0 = time.perf_counter()
-                for _ in range(20):
+                for _ in range(n):
                     self.replay()
                 torch.cuda.synchronize(self.device)
-                dt = time.perf_counter() - t0
-                if best is None or dt < best[0]:
-                    best = (dt, par)
-            self.graph_parallel = best[1]
-            return self.capture(first_step, best[1], steps_per_replay)
+                return (time.perf_counter() - t0) / (n * r)
+            cands = [(False, steps_per_replay), (True, 1)]
+            best = min(cands, key=lambda c: per_step(*c))
+            return self.capture(first_step, best[0], best[1])
         side = torch.cuda.Stream(self.device)
         side.wait_stream(torch.cuda.current_stream(self.device))
         with torch.cuda.stream(side):

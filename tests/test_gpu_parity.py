@@ -850,6 +850,21 @@ def test_graph_with_several_steps_per_replay(parallel):
     wl = W.get("mnist_cnn")
     inputs = W.make_inputs(wl, n=20)
     st = DPStep(wl, inputs, DEV)
+    if parallel:
+        # branches take one step per replay (refused on the host before any capture)
+        with pytest.raises(ValueError):
+            st.capture(first_step=2, parallel=True, steps_per_replay=3)
+        say("graph capture mnist_cnn, branches, 1 step per replay")
+        st.capture(first_step=2, parallel=True)
+        eager = DPStep(wl, inputs, DEV)
+        for k in range(2):
+            st.replay()
+            got = st.results()
+            eager.run(step=2 + k)
+            ref = eager.results()
+            for name in ref["out"]:
+                np.testing.assert_array_equal(got["out"][name], ref["out"][name], err_msg="replay %d %s" % (k, name))
+        return
     say("graph capture mnist_cnn, 3 steps per replay, parallel", parallel)
     st.capture(first_step=2, parallel=parallel, steps_per_replay=3)
     eager = DPStep(wl, inputs, DEV)
@@ -897,6 +912,10 @@ def test_noise_schedule_in_a_graph_matches_eager(parallel):
     inputs = W.make_inputs(wl, n=20)
     sched = [0.5, 1.5, 0.0, 2.0, 0.25]
     st = DPStep(wl, inputs, DEV, sigma_schedule=sched)
+    if parallel:
+        with pytest.raises(ValueError):     # branches take one step per replay
+            st.capture(first_step=1, parallel=True, steps_per_replay=3)
+        return
     say("graph with a noise schedule, parallel", parallel)
     st.capture(first_step=1, parallel=parallel, steps_per_replay=3)
     eager = DPStep(wl, inputs, DEV, sigma_schedule=sched)
